@@ -1,0 +1,197 @@
+"""Time-to-first-token from an evicted state on one MI355X.
+
+One step = evict (idle phase, untimed) -> [restore_and_prefill -> first_token]
+(timed).  The timed part is the whole hot path: restore planning, swap-in on
+the side stream, recompute of dropped chunks layer by layer, output head and
+argmax.  Inputs (model, context KV, host swap space) are resident before the
+timed region starts.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 8b]
+
+Prints one JSON line: recompute tokens/s (positions pushed through the model
+per second of TTFT) as `value`, TTFT in ms, the dominant kernel's roofline
+(HIP-event timing of its launches inside the timed steps) and the CPU
+oracle's rate on a bounded sample of the same workload.
+"""
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "KV-recompute prefill tokens/s + TTFT ms from evicted state, 1 MI355X"
+PEAK_MFMA_TFLOPS = 2500.0      # MI355X dense bf16 / fp16 MFMA
+PEAK_HBM_GBPS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(w, blob, plan_nR, sample_rows=64):
+    """The oracle as it stands, on a bounded sample: one layer's weight decode
+    plus `sample_rows` evenly spaced positions through that layer (attention
+    over a synthetic KV cache of the full context), extrapolated to the whole
+    restore: L decodes and sum_l nR(l) row-layers."""
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    m = w.model
+    hp = O.Hyper(m)
+    wts = O.Weights(hp, blob)
+    S = w.n_ctx + w.n_prompt
+    t0 = time.perf_counter()
+    lw = wts.layer(0)
+    t_decode = time.perf_counter() - t0
+    pos = np.linspace(0, S - 1, sample_rows).astype(np.int64)
+    rng = np.random.default_rng(0)
+    K = rng.standard_normal((S, m.dkv)).astype(np.float16)
+    V = rng.standard_normal((S, m.dkv)).astype(np.float16)
+    h = wts.rows("emb", rng.integers(0, m.vocab, sample_rows))
+    t1 = time.perf_counter()
+    O.layer_forward(hp, lw, h, pos, lambda k, v: None,
+                    lambda last: (K[:last].astype(np.float64), V[:last].astype(np.float64)))
+    t_rows = time.perf_counter() - t1
+    total = m.n_layers * t_decode + t_rows * float(np.sum(plan_nR)) / sample_rows
+    return {"value": round(plan_nR[0] / total, 3), "unit": "tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": (f"layer-0 weight decode ({t_decode:.2f} s) + {sample_rows} evenly spaced positions "
+                       f"through layer 0 with attention over all {S} keys ({t_rows:.2f} s), extrapolated "
+                       f"to {m.n_layers} layers and sum nR = {int(np.sum(plan_nR))} row-layers "
+                       f"(est. {total:.1f} s per restore)")}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="8b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-overlap", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
+              file=sys.stderr)
+        sys.exit(2)
+
+    from paper_2609_01338_amd import mz
+    from paper_2609_01338_amd import workloads as W
+
+    w = W.WORKLOADS[args.workload]
+    m = w.model
+    S = w.n_ctx + w.n_prompt
+    t = time.perf_counter()
+    blob = W.make_blob(w)
+    log(f"[bench] {w.key}: blob {blob.nbytes / 1e9:.2f} GB in {time.perf_counter() - t:.1f} s")
+    ctx_tok, prompt = W.make_tokens(w)
+    plan = W.make_plan(w)
+
+    t = time.perf_counter()
+    eng = mz.Engine(m, blob, max_ctx=S)
+    e = eng.ctx
+    log(f"[bench] model loaded in {time.perf_counter() - t:.1f} s")
+    if args.no_overlap:
+        mz.mz_set_option(e, "overlap", 0)
+
+    # never-evicted reference: clean prefill of context + prompt
+    t = time.perf_counter()
+    mz.mz_prefill_context(e, np.concatenate([ctx_tok, prompt]))
+    clean_tok, clean_logits = mz.mz_first_token(e, m.vocab)
+    mz.mz_truncate_context(e, w.n_ctx)
+    log(f"[bench] clean prefill of {S} tokens in {time.perf_counter() - t:.2f} s, token {clean_tok}")
+
+    ttft, toks, logit_err = [], [], []
+    stats = None
+    for step in range(args.warmup + args.steps):
+        timed = step >= args.warmup
+        if step == args.warmup:
+            mz.mz_set_option(e, "kernel_timing", 1)
+        mz.mz_evict(e, plan.kv_state, plan.w_state)
+        t0 = time.perf_counter()
+        mz.mz_restore_and_prefill(e, prompt)
+        tok, logits = mz.mz_first_token(e, m.vocab)
+        dt = time.perf_counter() - t0
+        if timed:
+            ttft.append(dt)
+        toks.append(tok)
+        logit_err.append(float(np.abs(logits - clean_logits).max()))
+        stats = mz.mz_stats(e)
+        mz.mz_truncate_context(e, w.n_ctx)
+        log(f"[bench] step {step} {'timed' if timed else 'warmup'}: TTFT {dt * 1e3:.2f} ms, token {tok}, "
+            f"max |logit - clean| {logit_err[-1]:.2e}")
+
+    nR = stats["nR"]
+    n_tok = nR[0]
+    total_s = sum(ttft)
+    ttft_med = statistics.median(ttft)
+    value = n_tok * len(ttft) / total_s
+    # per-kernel aggregates over the timed steps, grouped by HIP kernel symbol
+    by_kernel = {}
+    for kind, k in stats["kernels"].items():
+        g = by_kernel.setdefault(k["kernel"], {"launches": 0, "ms": 0.0, "flops": 0.0, "bytes": 0.0,
+                                               "roles": []})
+        for f in ("launches", "ms", "flops", "bytes"):
+            g[f] += k[f]
+        g["roles"].append(kind)
+    dom_name, dom = max(by_kernel.items(), key=lambda kv: kv[1]["ms"])
+    if dom["flops"] > 0:
+        achieved = dom["flops"] / (dom["ms"] * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_MFMA_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_MFMA_TFLOPS, 4), "traffic": None,
+                "kernel": dom_name, "roles": dom["roles"],
+                "avg_launch_ms": round(dom["ms"] / dom["launches"], 5),
+                "flops_per_launch": dom["flops"] / dom["launches"]}
+    else:
+        achieved = dom["bytes"] / (dom["ms"] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": None, "kernel": dom_name,
+                "avg_launch_ms": round(dom["ms"] / dom["launches"], 5)}
+    steps = len(ttft)
+    kernels_ms_per_step = {k: round(v["ms"] / steps, 3) for k, v in stats["kernels"].items()}
+    kernel_tflops = {k: round(v["flops"] / (v["ms"] * 1e-3) / 1e12, 1)
+                     for k, v in stats["kernels"].items() if v["flops"] > 0}
+    algo = stats["algo_flops"]
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": steps,
+        "warmup": args.warmup, "ms_per_step": round(total_s / steps * 1e3, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{w.key}: {w.description}", "model": m.name, "n_ctx": w.n_ctx,
+                   "n_prompt": w.n_prompt, "chunk_tokens": m.chunk_tokens, "plan": plan.counts(),
+                   "weight_units_swapped": int((plan.w_state == W.SWAP).sum()),
+                   "nR0": n_tok, "sum_nR": int(sum(nR)), "sum_nD": int(sum(stats["nD"])),
+                   "overlap": not args.no_overlap},
+        "ttft_ms": round(ttft_med * 1e3, 3),
+        "ttft_ms_steps": [round(x * 1e3, 3) for x in ttft],
+        "algo_tflop": round(algo / 1e12, 3),
+        "ttft_mfma_frac": round(algo / ttft_med / 1e12 / PEAK_MFMA_TFLOPS, 4),
+        "swap_in": {"kv_bytes": stats["swap_kv_bytes"], "w_bytes": stats["swap_w_bytes"],
+                    "copies": stats["copies"], "ms": stats["swap_ms"],
+                    "GBps": (round((stats["swap_kv_bytes"] + stats["swap_w_bytes"]) / stats["swap_ms"] / 1e6, 2)
+                             if stats["swap_ms"] and stats["swap_ms"] > 0 else None)},
+        "kernel_ms_per_step": kernels_ms_per_step,
+        "kernel_tflops": kernel_tflops,
+        "invariant": {"clean_token": clean_tok, "tokens": toks,
+                      "max_logit_err_vs_clean": max(logit_err)},
+        "roofline": roof,
+    }
+    eng.close()
+    if not args.no_cpu_baseline:
+        t = time.perf_counter()
+        out["cpu_baseline"] = cpu_baseline(w, blob, nR)
+        log(f"[bench] cpu baseline in {time.perf_counter() - t:.1f} s")
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

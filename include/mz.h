@@ -1,0 +1,209 @@
+/*
+ * mz.h -- C ABI of the MI355X restore-and-prefill engine.
+ *
+ * The engine rebuilds an evicted LLM context on one GPU.  The model's weights
+ * are held per transformer layer and its KV cache per layer in fixed-size
+ * token chunks (paper Sec. 4.2); each unit is resident, swapped to pinned host
+ * memory, or dropped.  Restoring copies swapped units back and recomputes
+ * dropped KV chunks with a Q4_0-weight Llama-style prefill, layer by layer, so
+ * the first token waits only for what is actually missing.  The calls follow
+ * the paper's interface pair evict(size) / restore_generate(input_tokens)
+ * (Sec. 5), with the eviction amount given as an explicit per-unit plan.
+ *
+ * Conventions shared by every call:
+ *  - Every call returns mz_status.  On error the context is left as it was
+ *    and mz_last_error() describes the failure.
+ *  - The library owns all device memory and all pinned host memory it
+ *    allocates.  Input arrays are copied before the call returns; the caller
+ *    owns every output buffer.
+ *  - "host" pointers are ordinary CPU memory; "device" pointers are HBM
+ *    addresses on the context's GPU (the kernel-level calls at the end).
+ *  - One context is used by one thread at a time.
+ */
+#ifndef MZ_H
+#define MZ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct mz_ctx mz_ctx;
+
+typedef enum {
+  MZ_OK = 0,
+  MZ_EINVAL = -1,   /* bad shape, token id, state value or size */
+  MZ_ENOMEM = -2,   /* pool, arena or device allocation exhausted */
+  MZ_EHIP = -3,     /* a HIP runtime call failed */
+  MZ_ESTATE = -4    /* call not valid in the current state */
+} mz_status;
+
+/* State of one unit (a layer's weights, or one KV chunk of one layer). */
+typedef enum { MZ_RES = 0, MZ_SWAP = 1, MZ_DROP = 2 } mz_unit_state;
+
+/* Model shape.  d_model must be a multiple of 128; d_ffn need not be a
+ * multiple of 32 (Q4_0 rows of W_down are zero-padded); head_dim must be 64 or
+ * 128; n_q_heads a multiple of n_kv_heads with a group of at most 8;
+ * max_ctx bounds context + prompt tokens. */
+typedef struct {
+  int32_t n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ffn, vocab;
+  int32_t chunk_tokens, max_ctx;
+  float rope_theta, rms_eps;
+} mz_model_cfg;
+
+/* Eviction plan (paper Sec. 4.3-4.4).  kv_state is [n_layers][n_chunks]
+ * (n_chunks = chunks of the cached context), w_state is [n_layers] or NULL
+ * (all resident).  A target of MZ_RES leaves a unit as it is; MZ_SWAP moves a
+ * resident unit to the pinned host arena; MZ_DROP releases it (a dropped KV
+ * chunk is recomputed at restore; a dropped weight unit is reloaded from the
+ * model image kept in host memory, standing in for the paper's storage).
+ * Units are visited in `order` (unit ids: KV chunk (l, c) is l * n_chunks + c,
+ * weight unit l is n_layers * n_chunks + l); NULL means backward-out: last
+ * layer first, within a layer its chunks from the last, then its weights
+ * (Sec. 4.4).  Swapped units are pushed on the arena stack in that order. */
+typedef struct {
+  const uint8_t *kv_state;
+  int32_t n_layers;
+  int32_t n_chunks;
+  const uint8_t *w_state;
+  const int32_t *order;
+  int32_t n_order;
+} mz_evict_plan;
+
+/* ---- model-level calls ------------------------------------------------- */
+
+/* Create a context on GPU `device` from a Q4_0 model blob (host, nbytes).
+ * Blob: per layer Wq, Wk, Wv, Wo, W_gate, W_up, W_down, then E and W_lm; each
+ * [out][in] as rows of ceil(in/32) 18-byte Q4_0 blocks (fp16 scale, then 16
+ * bytes: element j in the low nibble of byte j, element j+16 in the high).
+ * The blob is repacked into device layouts and a host copy of the layer
+ * weights is retained for dropped-weight reloads.  EINVAL on a shape or size
+ * mismatch, ENOMEM / EHIP on allocation failure. */
+mz_status mz_load_model(const mz_model_cfg *cfg, const void *q4_blob, size_t nbytes,
+                        int32_t device, mz_ctx **out);
+
+/* Replace the cached context by tokens[0..n) (host) and build its KV cache
+ * with a full prefill on the GPU (every chunk resident afterwards). */
+mz_status mz_prefill_context(mz_ctx *ctx, const int32_t *tokens, int32_t n);
+
+/* Replace the cached context by tokens[0..n) (host) without computing KV:
+ * every chunk is allocated, zero-filled and resident; fill it with
+ * mz_import_kv.  Used to start from KV produced elsewhere. */
+mz_status mz_set_context(mz_ctx *ctx, const int32_t *tokens, int32_t n);
+
+/* Write chunk `chunk` of layer `layer` from host arrays k, v, each
+ * [chunk_tokens][n_kv_heads * head_dim] IEEE half, hidden index innermost.
+ * ESTATE if the chunk is not resident. */
+mz_status mz_import_kv(mz_ctx *ctx, int32_t layer, int32_t chunk, const void *k_f16,
+                       const void *v_f16);
+
+/* Read a resident chunk into host arrays laid out as in mz_import_kv.
+ * ESTATE if the chunk is not resident. */
+mz_status mz_read_kv(mz_ctx *ctx, int32_t layer, int32_t chunk, void *k_f16, void *v_f16);
+
+/* Keep only the first n tokens of the cached context (0 <= n <= current):
+ * chunks entirely past n are released and the rest stay as they are.  Every
+ * unit must be resident (ESTATE otherwise). */
+mz_status mz_truncate_context(mz_ctx *ctx, int32_t n);
+
+/* Apply an eviction plan (idle phase; synchronous).  Allowed moves:
+ * RES->SWAP, RES->DROP, SWAP->DROP.  ESTATE for SWAP of a dropped unit or when
+ * no context is cached; EINVAL for a plan whose shape does not match. */
+mz_status mz_evict(mz_ctx *ctx, const mz_evict_plan *plan);
+
+/* Restore every evicted unit and prefill prompt[0..n_prompt) (host) after the
+ * cached context.  Swapped units are copied back on a side stream earliest
+ * layer first (forward-in, Sec. 4.4) while the compute stream recomputes the
+ * dropped chunks; each layer's compute waits only on that layer's copies.
+ * Asynchronous: returns once the work is enqueued.  Afterwards every unit is
+ * resident and the context holds n_ctx + n_prompt tokens.  EINVAL if the
+ * total exceeds max_ctx or a token is out of range. */
+mz_status mz_restore_and_prefill(mz_ctx *ctx, const int32_t *prompt, int32_t n_prompt);
+
+/* Greedy first token after mz_restore_and_prefill / mz_prefill_context:
+ * RMSNorm of the last position's final hidden state, output head, argmax
+ * (lowest index on ties).  Synchronizes.  logits_out (host, [vocab] float) may
+ * be NULL.  ESTATE if nothing was prefilled since the last first token. */
+mz_status mz_first_token(mz_ctx *ctx, int32_t *token_out, float *logits_out);
+
+/* Engine options: "overlap" (1: swap-in overlapped with compute, default;
+ * 0: every copy finishes before compute starts), "kernel_timing" (1: time
+ * every kernel launch with HIP events on its stream; setting it clears the
+ * accumulated kernel statistics).  Test hooks: "debug_poison" (1: fill every
+ * slot and weight unit allocated by a restore with NaN before it is
+ * restored or recomputed), "debug_swap_delay_us" (delay the swap stream by a
+ * bounded busy wait before its copies).  EINVAL for an unknown key. */
+mz_status mz_set_option(mz_ctx *ctx, const char *key, int64_t value);
+
+/* JSON summary of the last restore (row counts, bytes moved, per-kernel
+ * launch counts / time / algorithmic work, pool occupancy), written to
+ * json_out (host, cap bytes, NUL-terminated).  EINVAL if cap is too small. */
+mz_status mz_stats(mz_ctx *ctx, char *json_out, size_t cap);
+
+/* Description of the last error on ctx (or of the last failed mz_load_model
+ * when ctx is NULL).  Valid until the next call on the same context. */
+const char *mz_last_error(const mz_ctx *ctx);
+
+/* Release the context and everything it owns (NULL is allowed). */
+void mz_free(mz_ctx *ctx);
+
+/* ---- host-only helpers (no GPU needed) --------------------------------- */
+
+/* Library version string. */
+const char *mz_version(void);
+
+/* Rows of the restore (R_l: positions that pass through layer l; D_l: rows
+ * whose layer-l K/V is written) for kv_state [n_layers][n_chunks] (host),
+ * n_ctx context and n_prompt prompt tokens.  Writes nR[l], nD[l] (host,
+ * [n_layers]) and, if rows is not NULL, the concatenation of every R_l
+ * (ascending positions) into rows (host, rows_cap entries).  EINVAL if
+ * rows_cap is too small. */
+mz_status mz_plan_rows(const mz_model_cfg *cfg, const uint8_t *kv_state, int32_t n_chunks,
+                       int32_t n_ctx, int32_t n_prompt, int32_t *nR, int32_t *nD,
+                       int32_t *rows, int64_t rows_cap);
+
+/* Bytes of the device GEMM layout of a Q4_0 matrix [n][k] (n padded to 128,
+ * k to 64). */
+int64_t mz_q4_gemm_packed_bytes(int32_t n, int32_t k);
+
+/* Repack a Q4_0 matrix [n][k] (host, blob row format) into the device GEMM
+ * layout (host out, mz_q4_gemm_packed_bytes(n, k) bytes).  If w_up is not
+ * NULL, w and w_up are the gate and up matrices [n][k] and are interleaved
+ * in groups of 16 rows (gate group i, then up group i) for the SwiGLU
+ * epilogue; out then needs mz_q4_gemm_packed_bytes(2 * n_pad64, k) bytes. */
+mz_status mz_q4_gemm_pack(const void *w, const void *w_up, int32_t n, int32_t k, void *out);
+
+/* ---- kernel-level calls (device pointers, enqueue on `stream`) --------- */
+/* These run one kernel of the path on caller-owned device buffers; stream is
+ * a hipStream_t (NULL = default stream).  They validate shapes and return
+ * EINVAL without launching on a mismatch. */
+
+/* Y = X . W^T with X f16 [m][k] row-major and W packed by mz_q4_gemm_pack
+ * (weights dequantized to f16, fp32 accumulation).
+ * epilogue 0: y float [m][n_pad] = acc;  1: y float [m][n_pad] += acc;
+ * 2: y f16 [m][n_pad/2] = silu(gate) * up (W packed with w_up). */
+mz_status mz_q4_gemm(const void *x_f16, int32_t m, int32_t n_pad, int32_t k,
+                     const void *w_packed, int32_t epilogue, void *y, void *stream);
+
+/* Causal GQA attention of q (f16 [m][n_q_heads][head_dim], rotated) at
+ * positions qpos (int32 [m], ascending) over the KV chunks of one layer:
+ * chunk c of the layer lives in slot table[c] of slab (each slot: K then V,
+ * each [chunk_tokens][n_kv_heads * head_dim] f16).  Keys 0..qpos[i] are read;
+ * table must cover chunk (qpos[m-1] / chunk_tokens).  out: f16
+ * [m][n_q_heads * head_dim]. */
+mz_status mz_attention(const void *q_f16, const int32_t *qpos, int32_t m, const void *slab,
+                       const int32_t *table, int32_t n_table, int32_t chunk_tokens,
+                       int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, void *out_f16,
+                       void *stream);
+
+/* x = h / sqrt(mean(h^2) + eps) per row: h float [m][d] -> x f16 [m][d]. */
+mz_status mz_rmsnorm(const void *h_f32, int32_t m, int32_t d, float eps, void *x_f16,
+                     void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MZ_H */

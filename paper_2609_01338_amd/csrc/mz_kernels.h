@@ -1,0 +1,67 @@
+// Launchers of the gfx950 kernels of the restore-and-prefill path.  Each takes
+// device pointers and a stream, checks nothing, and enqueues one kernel; the
+// callers (runtime and ABI) validate shapes first.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mzk {
+
+// Device GEMM layout of a Q4_0 matrix [n][k]: tiles of 128 rows x 64 columns,
+// ordered n-tile major, k-tile minor.  A tile holds 128*2 blocks of 16 nibble
+// bytes (row-major over (row, block)), then their 128*2 fp16 scales.
+constexpr int kGemmTileN = 128;
+constexpr int kGemmTileK = 64;
+constexpr int kGemmTileBytes = kGemmTileN * kGemmTileK / 2 + kGemmTileN * (kGemmTileK / 32) * 2;
+
+enum GemmEpilogue { kEpiStore = 0, kEpiAdd = 1, kEpiSwiGLU = 2 };
+
+// Y = X . W^T: X f16 [m][k], W packed [n][k] (n % 128 == 0, k % 64 == 0).
+// kEpiStore: Y float [m][n] = acc; kEpiAdd: Y float [m][n] += acc;
+// kEpiSwiGLU: Y f16 [m][n/2] = silu(gate) * up for the interleaved layout.
+void launch_gemm_q4(const void* x, int m, int n, int k, const void* w, int epilogue, void* y,
+                    hipStream_t s);
+
+// Causal GQA attention over chunked KV (see mz.h, mz_attention).
+void launch_attention(const void* q, const int32_t* qpos, int m, const void* slab,
+                      const int32_t* table, int chunk_tokens, int64_t slot_bytes, int n_q,
+                      int n_kv, int head_dim, void* out, hipStream_t s);
+
+// x f16 [m][d] = RMSNorm(h float [m][d]).
+void launch_rmsnorm(const float* h, int m, int d, float eps, void* x, hipStream_t s);
+
+// Rotary embedding + KV scatter.  qkv float [m][qkv_stride] holding q, k, v; rope_cs
+// float2 [max_pos][hd/2] (cos, sin); kv_off int64 [m]: byte offset of the
+// row's K in slab (its V is kv_bytes_half later) or -1 to skip.
+// q_out f16 [m][nq*hd].
+void launch_rope_kv(const float* qkv, int qkv_stride, int m, const int32_t* pos,
+                    const int64_t* kv_off, const float2* rope_cs, int nq, int nkv, int hd,
+                    int64_t v_delta, void* q_out, void* slab, hipStream_t s);
+
+// h float [m][d] = dequant(E[tok[i]]) with E split into nibbles [V][d/2] and
+// fp16 scales [V][d/32].
+void launch_embed(const uint8_t* e_nib, const uint16_t* e_scale, const int32_t* tok, int m, int d,
+                  float* h, hipStream_t s);
+
+// dst[i] = src[idx[i]] for rows of d floats.
+void launch_gather_rows(const float* src, const int32_t* idx, int m, int d, float* dst,
+                        hipStream_t s);
+
+// logits float [V] = RMSNorm(h_last) . W_lm^T (split layout as the embedding),
+// then token = argmax (lowest index on ties).  part_val/part_idx hold
+// ceil(V / 64) partials.
+void launch_lm_head(const float* h_last, int d, float eps, const uint8_t* w_nib,
+                    const uint16_t* w_scale, int vocab, float* logits, float* part_val,
+                    int32_t* part_idx, int32_t* token, hipStream_t s);
+
+// Fill n 32-bit words with zero (graph-capturable, unlike memset nodes).
+void launch_zero(void* p, int64_t n_words, hipStream_t s);
+
+// Fill n 32-bit words with `value` (test hook: NaN-poison fresh slots).
+void launch_fill(void* p, int64_t n_words, uint32_t value, hipStream_t s);
+
+// Busy-wait about `us` microseconds of wall clock on stream s (test hook that
+// delays a stream).  Bounded: always exits.
+void launch_spin(int64_t us, hipStream_t s);
+
+}  // namespace mzk

@@ -1,0 +1,1341 @@
+// Runtime and C ABI of the restore-and-prefill engine (see include/mz.h).
+//
+// Memory (paper Sec. 4.2, re-targeted to a discrete GPU):
+//  - KV: one HBM slab of fixed-size slots, one slot per (layer, chunk), each
+//    holding K then V of chunk_tokens tokens ([C][dkv] f16 each).  A per-layer
+//    chunk table maps chunk -> slot; free slots sit in an ordered set so that
+//    contiguous runs can be handed out for coalesced copies.  Allocation at
+//    restore time is O(log n) with no driver call.
+//  - Weights: one unit per layer (fused QKV, O, gate/up interleaved, down, all
+//    in the tiled GEMM layout) in a pool of equal-size unit slots; embedding
+//    and output head are never evicted.
+//  - Swap space: a stack of pinned host segments; eviction pushes units in
+//    plan order (backward-out by default) and restoration reads them back
+//    forward-in (Sec. 4.4).
+// Restore (Sec. 4.4, 5): a host planner derives the rows R_l that must pass
+// through each layer and the rows D_l whose K/V is written, allocates slots,
+// uploads the row metadata, issues the swap-in copies on a side stream with
+// one event per layer and kind, and enqueues the per-layer kernels on the
+// compute stream, which waits on a layer's events only right before the first
+// kernel that reads the restored data.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <memory>
+#include <set>
+#include <string>
+#include <vector>
+
+#include "../../include/mz.h"
+#include "mz_kernels.h"
+
+namespace {
+
+constexpr const char* kVersion = "mz-mi355x 0.1";
+
+thread_local std::string g_load_error;
+
+struct HipError {
+  hipError_t e;
+  const char* what;
+};
+
+#define HIPCHK(x)                                      \
+  do {                                                 \
+    hipError_t e_ = (x);                               \
+    if (e_ != hipSuccess) throw HipError{e_, #x};      \
+  } while (0)
+
+struct StatusError {
+  mz_status st;
+  std::string msg;
+};
+
+[[noreturn]] void fail(mz_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  throw StatusError{st, buf};
+}
+
+int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+// ---------------------------------------------------------------- Q4_0 repacking
+
+constexpr int kBlockBytes = 18;
+
+int64_t q4_row_bytes(int64_t cols) { return (cols + 31) / 32 * kBlockBytes; }
+
+int64_t gemm_packed_bytes(int64_t n, int64_t k) {
+  return round_up(n, mzk::kGemmTileN) / mzk::kGemmTileN * (round_up(k, mzk::kGemmTileK) / mzk::kGemmTileK) *
+         mzk::kGemmTileBytes;
+}
+
+// Source row r (or nullptr for a zero row) of a canonical Q4_0 matrix.
+template <typename RowFn>
+void pack_gemm_tiles(RowFn row_ptr, int64_t n, int64_t k, uint8_t* out) {
+  const int64_t n_tiles = round_up(n, mzk::kGemmTileN) / mzk::kGemmTileN;
+  const int64_t k_tiles = round_up(k, mzk::kGemmTileK) / mzk::kGemmTileK;
+  const int64_t nb_src = (k + 31) / 32;
+  for (int64_t nt = 0; nt < n_tiles; ++nt)
+    for (int64_t kt = 0; kt < k_tiles; ++kt) {
+      uint8_t* tile = out + (nt * k_tiles + kt) * mzk::kGemmTileBytes;
+      for (int r = 0; r < mzk::kGemmTileN; ++r)
+        for (int b = 0; b < 2; ++b) {
+          const int64_t row = nt * mzk::kGemmTileN + r;
+          const int64_t blk = kt * 2 + b;
+          uint8_t* nib = tile + (r * 2 + b) * 16;
+          uint8_t* sc = tile + mzk::kGemmTileN * mzk::kGemmTileK / 2 + (r * 2 + b) * 2;
+          const uint8_t* src = row < n ? row_ptr(row) : nullptr;
+          if (src && blk < nb_src) {
+            memcpy(sc, src + blk * kBlockBytes, 2);
+            memcpy(nib, src + blk * kBlockBytes + 2, 16);
+          } else {
+            memset(sc, 0, 2);          // scale 0: the padded block decodes to 0
+            memset(nib, 0x88, 16);
+          }
+        }
+    }
+}
+
+void pack_plain(const uint8_t* w, int64_t n, int64_t k, uint8_t* out) {
+  const int64_t rb = q4_row_bytes(k);
+  pack_gemm_tiles([&](int64_t r) { return w + r * rb; }, n, k, out);
+}
+
+// Gate/up interleave: packed row 32 g + i is gate row 16 g + i (i < 16) or up
+// row 16 g + i - 16, so a 32-column group of the product holds matching
+// gate and up columns.
+void pack_gateup(const uint8_t* g, const uint8_t* u, int64_t n, int64_t k, uint8_t* out) {
+  const int64_t rb = q4_row_bytes(k);
+  const int64_t n_pad = round_up(n, 64);
+  pack_gemm_tiles(
+      [&](int64_t pr) -> const uint8_t* {
+        const int64_t grp = pr / 32, i = pr % 32;
+        const int64_t src = grp * 16 + (i < 16 ? i : i - 16);
+        if (src >= n) return nullptr;
+        return (i < 16 ? g : u) + src * rb;
+      },
+      2 * n_pad, k, out);
+}
+
+// Split rows of 18-byte blocks into nibbles [rows][cols/2] and scales [rows][cols/32].
+void split_rows(const uint8_t* w, int64_t rows, int64_t cols, uint8_t* nib, uint16_t* sc) {
+  const int64_t nb = cols / 32;
+  for (int64_t r = 0; r < rows; ++r)
+    for (int64_t b = 0; b < nb; ++b) {
+      const uint8_t* blk = w + (r * nb + b) * kBlockBytes;
+      memcpy(&sc[r * nb + b], blk, 2);
+      memcpy(nib + r * (cols / 2) + b * 16, blk + 2, 16);
+    }
+}
+
+// ---------------------------------------------------------------- restore rows
+
+struct Rows {
+  std::vector<int32_t> nR, nD;
+  std::vector<std::vector<int32_t>> R;   // ascending positions per layer
+};
+
+// R_l = {p < N : chunk(p) dropped at some l' >= l} U {N..S-1} U {S-1};
+// D_l = {p < N : chunk(p) dropped at l} U {N..S-1}.
+Rows compute_rows(const uint8_t* kv_state, int L, int nc, int N, int P, int C) {
+  Rows rows;
+  const int S = N + P;
+  std::vector<int> maxdrop(nc, -1);
+  for (int l = 0; l < L; ++l)
+    for (int c = 0; c < nc; ++c)
+      if (kv_state[(size_t)l * nc + c] == MZ_DROP) maxdrop[c] = l;
+  rows.R.resize(L);
+  rows.nR.resize(L);
+  rows.nD.resize(L);
+  for (int l = 0; l < L; ++l) {
+    std::vector<int32_t>& r = rows.R[l];
+    int nd = P;
+    for (int p = 0; p < N; ++p) {
+      const int c = p / C;
+      if (maxdrop[c] >= l) r.push_back(p);
+      if (kv_state[(size_t)l * nc + c] == MZ_DROP) ++nd;
+    }
+    for (int p = N; p < S; ++p) r.push_back(p);
+    if (r.empty() || r.back() != S - 1) r.push_back(S - 1);
+    rows.nR[l] = (int32_t)r.size();
+    rows.nD[l] = nd;
+  }
+  return rows;
+}
+
+// ---------------------------------------------------------------- pools
+
+struct SlotPool {
+  int n = 0;
+  std::set<int> free;
+  void init(int count) {
+    n = count;
+    free.clear();
+    for (int i = 0; i < count; ++i) free.insert(i);
+  }
+  int alloc_one() {
+    if (free.empty()) return -1;
+    int s = *free.begin();
+    free.erase(free.begin());
+    return s;
+  }
+  // first-fit contiguous run of k slots; -1 if none
+  int alloc_run(int k) {
+    if (k <= 0) return -1;
+    int start = -1, len = 0, prev = -2;
+    for (int s : free) {
+      if (s == prev + 1) {
+        ++len;
+      } else {
+        start = s;
+        len = 1;
+      }
+      prev = s;
+      if (len == k) {
+        for (int i = 0; i < k; ++i) free.erase(start + i);
+        return start;
+      }
+    }
+    return -1;
+  }
+  void release(int s) { free.insert(s); }
+  int used() const { return n - (int)free.size(); }
+};
+
+struct ArenaEntry {
+  int seg;
+  size_t off, bytes;
+};
+
+// LIFO stack of pinned host segments (the swap space).
+struct HostArena {
+  struct Seg {
+    uint8_t* p;
+    size_t cap, used;
+  };
+  std::vector<Seg> segs;
+  int top = 0;
+  size_t seg_min = size_t(256) << 20;
+  size_t bytes_live = 0;
+
+  uint8_t* ptr(const ArenaEntry& e) const { return segs[e.seg].p + e.off; }
+
+  ArenaEntry push(size_t bytes) {
+    bytes = (size_t)round_up((int64_t)bytes, 256);
+    while (true) {
+      if (top < (int)segs.size() && segs[top].cap - segs[top].used >= bytes) {
+        ArenaEntry e{top, segs[top].used, bytes};
+        segs[top].used += bytes;
+        bytes_live += bytes;
+        return e;
+      }
+      if (top < (int)segs.size() && segs[top].used > 0) {
+        ++top;
+        continue;
+      }
+      if (top < (int)segs.size()) {   // empty but too small: replace
+        HIPCHK(hipHostFree(segs[top].p));
+        segs.erase(segs.begin() + top);
+      }
+      const size_t cap = std::max(seg_min, bytes);
+      void* p = nullptr;
+      if (hipHostMalloc(&p, cap, hipHostMallocDefault) != hipSuccess || !p)
+        fail(MZ_ENOMEM, "pinned host allocation of %zu bytes failed", cap);
+      segs.insert(segs.begin() + std::min<size_t>(top, segs.size()), Seg{(uint8_t*)p, cap, 0});
+    }
+  }
+  void reset() {
+    for (auto& s : segs) s.used = 0;
+    top = 0;
+    bytes_live = 0;
+  }
+  size_t reserved() const {
+    size_t t = 0;
+    for (auto& s : segs) t += s.cap;
+    return t;
+  }
+  void release_all() {
+    for (auto& s : segs) (void)hipHostFree(s.p);
+    segs.clear();
+    top = 0;
+  }
+};
+
+// ---------------------------------------------------------------- timing
+
+enum KernelKind {
+  kKEmbed, kKRmsnorm, kKGemmQKV, kKRopeKV, kKAttention, kKGemmO, kKGemmGateUp, kKGemmDown,
+  kKGather, kKLmHead, kKCount
+};
+const char* kKindName[kKCount] = {"embed_q4", "rmsnorm", "gemm_q4_qkv", "rope_kv", "attention",
+                                  "gemm_q4_o", "gemm_q4_gateup", "gemm_q4_down", "gather_rows",
+                                  "lm_head_argmax"};
+// HIP kernel symbol each kind launches (to line up with profiler summaries)
+const char* kKindKernel[kKCount] = {"embed_kernel", "rmsnorm_kernel", "gemm_q4_kernel<0>",
+                                    "rope_kv_kernel", "attn_kernel", "gemm_q4_kernel<1>",
+                                    "gemm_q4_kernel<2>", "gemm_q4_kernel<1>",
+                                    "gather_rows_kernel", "lm_head_kernel+argmax_kernel"};
+
+struct KindStats {
+  int64_t launches = 0;
+  double ms = 0, flops = 0, bytes = 0;
+};
+
+struct PendingTiming {
+  int kind;
+  hipEvent_t a, b;
+  double flops, bytes;
+};
+
+}  // namespace
+
+// ---------------------------------------------------------------- context
+
+struct mz_ctx {
+  mz_model_cfg cfg{};
+  int device = 0;
+  std::string err;
+  hipStream_t s_compute = nullptr, s_swap = nullptr;
+
+  // shapes
+  int L = 0, d = 0, nq = 0, nkv = 0, hd = 0, ff = 0, ffp = 0, V = 0, C = 0, max_ctx = 0;
+  int dq = 0, dkv = 0, nqkv = 0, nqkv_pad = 0, d_pad = 0;
+  int max_chunks = 0;
+  int64_t slot_bytes = 0;
+  int64_t off_qkv = 0, off_o = 0, off_gu = 0, off_dn = 0, unit_bytes = 0;
+
+  // weights
+  uint8_t* w_slab = nullptr;
+  SlotPool w_pool;
+  std::vector<int> w_slot;              // per layer, -1 when evicted
+  std::vector<uint8_t> w_state;
+  std::vector<ArenaEntry> w_entry;
+  uint8_t* w_image = nullptr;           // pinned host copy of all packed units
+  uint8_t *emb_nib = nullptr, *lm_nib = nullptr;
+  uint16_t *emb_sc = nullptr, *lm_sc = nullptr;
+  float2* rope_cs = nullptr;
+
+  // KV
+  uint8_t* kv_slab = nullptr;
+  SlotPool kv_pool;
+  std::vector<int32_t> table;           // [L][max_chunks]
+  std::vector<uint8_t> kv_state;        // [L][max_chunks]
+  std::vector<ArenaEntry> kv_entry;     // [L][max_chunks]
+  HostArena arena;
+
+  // context
+  std::vector<int32_t> tokens;
+  bool have_last = false;
+  const float* h_last = nullptr;
+
+  // activations
+  float* h[2] = {nullptr, nullptr};
+  void* xb = nullptr;      // f16 [max_ctx][max(d, dq)]: norm output / attention output
+  float* qkv = nullptr;    // [max_ctx][nqkv_pad]
+  void* q16 = nullptr;     // f16 [max_ctx][dq]
+  void* act = nullptr;     // f16 [max_ctx][ffp]
+  float* logits = nullptr;
+  float* part_val = nullptr;
+  int32_t* part_idx = nullptr;
+  int32_t* d_token = nullptr;
+
+  // restore metadata (device + pinned staging)
+  int32_t* d_tables = nullptr;
+  int32_t* d_pos = nullptr;
+  int64_t* d_kvoff = nullptr;
+  int32_t* d_gather = nullptr;
+  int32_t* d_tok = nullptr;
+  uint8_t* h_stage = nullptr;
+  size_t stage_bytes = 0;
+  int32_t* h_token = nullptr;
+
+  // events
+  std::vector<hipEvent_t> ev_w, ev_kv;
+  hipEvent_t ev_swap_start = nullptr, ev_swap_end = nullptr;
+  bool swap_timed = false;
+
+  // options / stats
+  bool overlap = true;
+  int64_t debug_swap_delay_us = 0;   // test hook: delay the swap stream before its copies
+  bool debug_poison = false;         // test hook: NaN-fill every freshly allocated unit
+  bool timing = false;
+  std::vector<hipEvent_t> ev_pool;
+  size_t ev_used = 0;
+  std::vector<PendingTiming> pending;
+  KindStats kstats[kKCount];
+  std::vector<int32_t> last_nR, last_nD;
+  int64_t last_swap_kv_bytes = 0, last_swap_w_bytes = 0, last_reload_w_bytes = 0;
+  int64_t last_copies = 0;
+  double last_swap_ms = -1;
+  double last_algo_flops = 0;
+  int last_N = 0, last_P = 0;
+
+  hipEvent_t get_event() {
+    if (ev_used == ev_pool.size()) {
+      hipEvent_t e;
+      HIPCHK(hipEventCreate(&e));
+      ev_pool.push_back(e);
+    }
+    return ev_pool[ev_used++];
+  }
+
+  template <typename F>
+  void timed(int kind, double flops, double bytes, hipStream_t s, F&& launch) {
+    if (!timing) {
+      launch();
+      HIPCHK(hipGetLastError());
+      return;
+    }
+    hipEvent_t a = get_event(), b = get_event();
+    HIPCHK(hipEventRecord(a, s));
+    launch();
+    HIPCHK(hipGetLastError());
+    HIPCHK(hipEventRecord(b, s));
+    pending.push_back({kind, a, b, flops, bytes});
+  }
+
+  void collect_timing() {
+    for (auto& p : pending) {
+      float ms = 0;
+      HIPCHK(hipEventElapsedTime(&ms, p.a, p.b));
+      KindStats& k = kstats[p.kind];
+      k.launches++;
+      k.ms += ms;
+      k.flops += p.flops;
+      k.bytes += p.bytes;
+    }
+    pending.clear();
+    ev_used = 0;
+  }
+
+  uint8_t* unit_ptr(int l) const { return w_slab + (int64_t)w_slot[l] * unit_bytes; }
+  int nchunks_of(int n_tokens) const { return (n_tokens + C - 1) / C; }
+
+  void release_context() {
+    // the arena is cleared below: swapped weight units come back from the image
+    for (int l = 0; l < L; ++l)
+      if (w_state[l] == MZ_SWAP) w_state[l] = MZ_DROP;
+    for (int l = 0; l < L; ++l)
+      for (int c = 0; c < max_chunks; ++c) {
+        int32_t& t = table[(size_t)l * max_chunks + c];
+        if (t >= 0) kv_pool.release(t);
+        t = -1;
+        kv_state[(size_t)l * max_chunks + c] = MZ_RES;
+      }
+    arena.reset();
+    tokens.clear();
+    have_last = false;
+  }
+};
+
+namespace {
+
+template <typename F>
+mz_status guarded(mz_ctx* ctx, F&& body) {
+  try {
+    if (ctx) {
+      ctx->err.clear();
+      HIPCHK(hipSetDevice(ctx->device));
+    }
+    body();
+    return MZ_OK;
+  } catch (const StatusError& e) {
+    if (ctx) ctx->err = e.msg; else g_load_error = e.msg;
+    return e.st;
+  } catch (const HipError& e) {
+    std::string m = std::string("HIP error '") + hipGetErrorString(e.e) + "' in " + e.what;
+    if (ctx) ctx->err = m; else g_load_error = m;
+    return MZ_EHIP;
+  } catch (const std::bad_alloc&) {
+    if (ctx) ctx->err = "host allocation failed"; else g_load_error = "host allocation failed";
+    return MZ_ENOMEM;
+  }
+}
+
+void* dmalloc(size_t bytes) {
+  void* p = nullptr;
+  if (hipMalloc(&p, std::max<size_t>(bytes, 256)) != hipSuccess || !p)
+    fail(MZ_ENOMEM, "device allocation of %zu bytes failed", bytes);
+  return p;
+}
+
+void validate_cfg(const mz_model_cfg* c) {
+  if (!c) fail(MZ_EINVAL, "cfg is NULL");
+  if (c->n_layers < 1 || c->d_model < 64 || c->d_model % 64) fail(MZ_EINVAL, "d_model must be a positive multiple of 64 and n_layers >= 1");
+  if (c->head_dim != 64 && c->head_dim != 128) fail(MZ_EINVAL, "head_dim must be 64 or 128");
+  if (c->n_kv_heads < 1 || c->n_q_heads < 1 || c->n_q_heads % c->n_kv_heads)
+    fail(MZ_EINVAL, "n_q_heads must be a positive multiple of n_kv_heads");
+  if (c->n_q_heads / c->n_kv_heads > 8) fail(MZ_EINVAL, "GQA group above 8 is not supported");
+  if (c->d_ffn < 1 || c->vocab < 1) fail(MZ_EINVAL, "d_ffn and vocab must be positive");
+  if (c->chunk_tokens < 1 || c->max_ctx < 1) fail(MZ_EINVAL, "chunk_tokens and max_ctx must be positive");
+  if (!(c->rope_theta > 0) || !(c->rms_eps >= 0)) fail(MZ_EINVAL, "rope_theta must be > 0 and rms_eps >= 0");
+}
+
+int64_t blob_bytes(const mz_model_cfg* c) {
+  const int64_t d = c->d_model, dq = (int64_t)c->n_q_heads * c->head_dim,
+                dkv = (int64_t)c->n_kv_heads * c->head_dim, ff = c->d_ffn;
+  const int64_t layer = dq * q4_row_bytes(d) + 2 * dkv * q4_row_bytes(d) + d * q4_row_bytes(dq) +
+                        2 * ff * q4_row_bytes(d) + d * q4_row_bytes(ff);
+  return c->n_layers * layer + 2 * (int64_t)c->vocab * q4_row_bytes(d);
+}
+
+// Run the per-layer path over the rows planned in `rows`.  Metadata must
+// already be staged (see stage_and_upload).
+struct LayerOffsets {
+  std::vector<int64_t> pos_off, gat_off;
+};
+
+}  // namespace
+
+// ---------------------------------------------------------------- restore core
+
+namespace {
+
+struct CopyJob {
+  void* dst;
+  const void* src;
+  size_t bytes;
+};
+
+// Shared by mz_restore_and_prefill and mz_prefill_context.
+void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt) {
+  const int L = x->L, C = x->C, MC = x->max_chunks;
+  if (n_prompt < 0) fail(MZ_EINVAL, "n_prompt is negative");
+  if (n_prompt > 0 && !prompt) fail(MZ_EINVAL, "prompt is NULL");
+  const int N = (int)x->tokens.size();
+  const int P = n_prompt;
+  const int S = N + P;
+  if (S == 0) fail(MZ_ESTATE, "no context and no prompt to prefill");
+  if (S > x->max_ctx) fail(MZ_EINVAL, "context + prompt (%d) exceeds max_ctx (%d)", S, x->max_ctx);
+  for (int i = 0; i < P; ++i)
+    if (prompt[i] < 0 || prompt[i] >= x->V) fail(MZ_EINVAL, "prompt token %d out of range", prompt[i]);
+  const int nc_old = x->nchunks_of(N), nc_new = x->nchunks_of(S);
+
+  // --- plan rows over the chunks of the cached context
+  std::vector<uint8_t> st((size_t)L * std::max(nc_old, 1), MZ_RES);
+  for (int l = 0; l < L; ++l)
+    for (int c = 0; c < nc_old; ++c) st[(size_t)l * nc_old + c] = x->kv_state[(size_t)l * MC + c];
+  Rows rows = compute_rows(st.data(), L, nc_old, N, P, C);
+
+  // --- allocate slots: swapped chunks first, in runs matching their arena order
+  std::vector<std::vector<CopyJob>> kv_jobs(L);
+  std::vector<int> new_slots;   // for rollback on failure
+  auto rollback = [&]() {
+    for (int s : new_slots) x->kv_pool.release(s);
+  };
+  try {
+    for (int l = 0; l < L; ++l) {
+      std::vector<int> sw;
+      for (int c = 0; c < nc_old; ++c)
+        if (x->kv_state[(size_t)l * MC + c] == MZ_SWAP) sw.push_back(c);
+      std::sort(sw.begin(), sw.end(), [&](int a, int b) {
+        const ArenaEntry &ea = x->kv_entry[(size_t)l * MC + a], &eb = x->kv_entry[(size_t)l * MC + b];
+        return ea.seg != eb.seg ? ea.seg < eb.seg : ea.off < eb.off;
+      });
+      size_t i = 0;
+      while (i < sw.size()) {
+        size_t j = i + 1;
+        while (j < sw.size()) {
+          const ArenaEntry &p = x->kv_entry[(size_t)l * MC + sw[j - 1]], &q = x->kv_entry[(size_t)l * MC + sw[j]];
+          if (q.seg != p.seg || q.off != p.off + p.bytes) break;
+          ++j;
+        }
+        // arena run sw[i..j): try one contiguous slot run, else split per chunk
+        const int k = (int)(j - i);
+        int first = x->kv_pool.alloc_run(k);
+        if (first >= 0) {
+          for (int t = 0; t < k; ++t) {
+            x->table[(size_t)l * MC + sw[i + t]] = first + t;
+            new_slots.push_back(first + t);
+          }
+          const ArenaEntry& e0 = x->kv_entry[(size_t)l * MC + sw[i]];
+          kv_jobs[l].push_back({x->kv_slab + (int64_t)first * x->slot_bytes, x->arena.ptr(e0),
+                                (size_t)k * (size_t)x->slot_bytes});
+        } else {
+          for (int t = 0; t < k; ++t) {
+            int s = x->kv_pool.alloc_one();
+            if (s < 0) fail(MZ_ENOMEM, "KV slot pool exhausted");
+            x->table[(size_t)l * MC + sw[i + t]] = s;
+            new_slots.push_back(s);
+            const ArenaEntry& e = x->kv_entry[(size_t)l * MC + sw[i + t]];
+            kv_jobs[l].push_back({x->kv_slab + (int64_t)s * x->slot_bytes, x->arena.ptr(e),
+                                  (size_t)x->slot_bytes});
+          }
+        }
+        i = j;
+      }
+    }
+    for (int l = 0; l < L; ++l) {
+      for (int c = 0; c < nc_new; ++c) {
+        int32_t& t = x->table[(size_t)l * MC + c];
+        const bool need = c >= nc_old || x->kv_state[(size_t)l * MC + c] == MZ_DROP;
+        if (need && t < 0) {
+          int s = x->kv_pool.alloc_one();
+          if (s < 0) fail(MZ_ENOMEM, "KV slot pool exhausted");
+          t = s;
+          new_slots.push_back(s);
+        }
+      }
+    }
+  } catch (...) {
+    for (int l = 0; l < L; ++l)
+      for (int c = 0; c < MC; ++c) {
+        int32_t& t = x->table[(size_t)l * MC + c];
+        if (t >= 0 && std::find(new_slots.begin(), new_slots.end(), t) != new_slots.end()) t = -1;
+      }
+    rollback();
+    throw;
+  }
+  // weight units
+  std::vector<int> w_new;
+  for (int l = 0; l < L; ++l)
+    if (x->w_state[l] != MZ_RES) {
+      int s = x->w_pool.alloc_one();
+      if (s < 0) fail(MZ_ENOMEM, "weight unit pool exhausted");
+      x->w_slot[l] = s;
+      w_new.push_back(l);
+    }
+
+  // --- metadata: tables, positions, KV destinations, compaction, tokens
+  std::vector<int64_t> pos_off(L + 1, 0), gat_off(L, 0);
+  for (int l = 0; l < L; ++l) pos_off[l + 1] = pos_off[l] + rows.nR[l];
+  int64_t n_gat = 0;
+  for (int l = 0; l + 1 < L; ++l) {
+    gat_off[l] = n_gat;
+    n_gat += rows.nR[l + 1];
+  }
+  const int64_t tot = pos_off[L];
+  const size_t b_tab = (size_t)L * MC * 4, b_pos = (size_t)tot * 4, b_off = (size_t)tot * 8,
+               b_gat = (size_t)n_gat * 4, b_tok = (size_t)rows.nR[0] * 4;
+  const size_t need = b_tab + b_pos + b_off + b_gat + b_tok + 5 * 256;
+  if (need > x->stage_bytes) fail(MZ_EINVAL, "restore metadata exceeds the staging buffer");
+  uint8_t* sp = x->h_stage;
+  int32_t* s_tab = (int32_t*)sp;
+  int32_t* s_pos = (int32_t*)(sp + round_up(b_tab, 256));
+  int64_t* s_off = (int64_t*)((uint8_t*)s_pos + round_up(b_pos, 256));
+  int32_t* s_gat = (int32_t*)((uint8_t*)s_off + round_up(b_off, 256));
+  int32_t* s_tok = (int32_t*)((uint8_t*)s_gat + round_up(b_gat, 256));
+  memcpy(s_tab, x->table.data(), b_tab);
+  for (int l = 0; l < L; ++l) {
+    const std::vector<int32_t>& R = rows.R[l];
+    for (size_t i = 0; i < R.size(); ++i) {
+      const int p = R[i];
+      s_pos[pos_off[l] + i] = p;
+      const int c = p / C;
+      const bool write = p >= N || x->kv_state[(size_t)l * MC + c] == MZ_DROP;
+      s_off[pos_off[l] + i] =
+          write ? (int64_t)x->table[(size_t)l * MC + c] * x->slot_bytes + (int64_t)(p % C) * x->dkv * 2
+                : -1;
+    }
+    if (l + 1 < L) {
+      const std::vector<int32_t>& Rn = rows.R[l + 1];
+      size_t a = 0;
+      for (size_t b = 0; b < Rn.size(); ++b) {
+        while (R[a] != Rn[b]) ++a;
+        s_gat[gat_off[l] + b] = (int32_t)a;
+      }
+    }
+  }
+  for (int i = 0; i < rows.nR[0]; ++i) {
+    const int p = rows.R[0][i];
+    s_tok[i] = p < N ? x->tokens[p] : prompt[p - N];
+  }
+  hipStream_t cs = x->s_compute, ss = x->s_swap;
+  HIPCHK(hipMemcpyAsync(x->d_tables, s_tab, b_tab, hipMemcpyHostToDevice, cs));
+  HIPCHK(hipMemcpyAsync(x->d_pos, s_pos, b_pos, hipMemcpyHostToDevice, cs));
+  HIPCHK(hipMemcpyAsync(x->d_kvoff, s_off, b_off, hipMemcpyHostToDevice, cs));
+  if (b_gat) HIPCHK(hipMemcpyAsync(x->d_gather, s_gat, b_gat, hipMemcpyHostToDevice, cs));
+  HIPCHK(hipMemcpyAsync(x->d_tok, s_tok, b_tok, hipMemcpyHostToDevice, cs));
+
+  if (x->debug_poison) {
+    // fresh slots hold fp16 NaN until restored or recomputed: a missed row or
+    // an unordered read shows up as NaN
+    std::vector<char> is_copy_dst((size_t)x->kv_pool.n, 0);
+    for (int l = 0; l < L; ++l)
+      for (int c = 0; c < nc_old; ++c)
+        if (x->kv_state[(size_t)l * MC + c] == MZ_SWAP) is_copy_dst[x->table[(size_t)l * MC + c]] = 1;
+    for (int sl : new_slots)
+      mzk::launch_fill(x->kv_slab + (int64_t)sl * x->slot_bytes, x->slot_bytes / 4, 0xFFFFFFFFu,
+                       is_copy_dst[sl] ? ss : cs);
+    for (int l : w_new) mzk::launch_fill(x->unit_ptr(l), x->unit_bytes / 4, 0xFFFFFFFFu, ss);
+    HIPCHK(hipGetLastError());
+  }
+  if (x->debug_swap_delay_us > 0) {
+    mzk::launch_spin(x->debug_swap_delay_us, ss);
+    HIPCHK(hipGetLastError());
+  }
+
+  // --- swap-in on the side stream, forward-in, one event per layer and kind
+  std::vector<char> w_copy(L, 0), kv_copy(L, 0);
+  int64_t swap_kv = 0, swap_w = 0, reload_w = 0, copies = 0;
+  x->swap_timed = false;
+  bool any_copy = false;
+  for (int l = 0; l < L; ++l) any_copy |= x->w_state[l] != MZ_RES || !kv_jobs[l].empty();
+  if (any_copy) {
+    HIPCHK(hipEventRecord(x->ev_swap_start, ss));
+    for (int l = 0; l < L; ++l) {
+      if (x->w_state[l] != MZ_RES) {
+        const void* src = x->w_state[l] == MZ_SWAP ? (const void*)x->arena.ptr(x->w_entry[l])
+                                                    : (const void*)(x->w_image + (int64_t)l * x->unit_bytes);
+        HIPCHK(hipMemcpyAsync(x->unit_ptr(l), src, x->unit_bytes, hipMemcpyHostToDevice, ss));
+        HIPCHK(hipEventRecord(x->ev_w[l], ss));
+        w_copy[l] = 1;
+        (x->w_state[l] == MZ_SWAP ? swap_w : reload_w) += x->unit_bytes;
+        ++copies;
+      }
+      for (const CopyJob& j : kv_jobs[l]) {
+        HIPCHK(hipMemcpyAsync(j.dst, j.src, j.bytes, hipMemcpyHostToDevice, ss));
+        swap_kv += j.bytes;
+        ++copies;
+      }
+      if (!kv_jobs[l].empty()) {
+        HIPCHK(hipEventRecord(x->ev_kv[l], ss));
+        kv_copy[l] = 1;
+      }
+    }
+    HIPCHK(hipEventRecord(x->ev_swap_end, ss));
+    x->swap_timed = true;
+    if (!x->overlap) HIPCHK(hipStreamWaitEvent(cs, x->ev_swap_end, 0));
+  }
+
+  // --- compute stream: embedding, layers, compaction
+  const int d = x->d;
+  const double bpe_w = 0.5625;   // Q4_0 bytes per weight
+  x->timed(kKEmbed, 0, (double)rows.nR[0] * (d * bpe_w + d * 4.0), cs, [&] {
+    mzk::launch_embed(x->emb_nib, x->emb_sc, x->d_tok, rows.nR[0], d, x->h[0], cs);
+  });
+  int cur = 0;
+  double algo = 2.0 * d * x->V;
+  for (int l = 0; l < L; ++l) {
+    const int n = rows.nR[l];
+    const int32_t* pos = x->d_pos + pos_off[l];
+    const int64_t* off = x->d_kvoff + pos_off[l];
+    if (w_copy[l]) HIPCHK(hipStreamWaitEvent(cs, x->ev_w[l], 0));
+    const uint8_t* unit = x->unit_ptr(l);
+    float* h = x->h[cur];
+    x->timed(kKRmsnorm, 0, (double)n * d * 6.0, cs,
+             [&] { mzk::launch_rmsnorm(h, n, d, x->cfg.rms_eps, x->xb, cs); });
+    x->timed(kKGemmQKV, 2.0 * n * d * x->nqkv, (double)x->nqkv * d * bpe_w + n * (d * 2.0 + x->nqkv * 4.0), cs,
+             [&] { mzk::launch_gemm_q4(x->xb, n, x->nqkv_pad, d, unit + x->off_qkv, mzk::kEpiStore, x->qkv, cs); });
+    // prompt rows appended to a partial last chunk that was swapped out land in
+    // the restored slot: its copy must be done before they are written
+    const bool early_wait = kv_copy[l] && P > 0 && N % C != 0 &&
+                            x->kv_state[(size_t)l * MC + (nc_old - 1)] == MZ_SWAP;
+    if (early_wait) HIPCHK(hipStreamWaitEvent(cs, x->ev_kv[l], 0));
+    x->timed(kKRopeKV, 0, (double)n * (x->nqkv * 4.0 + x->dq * 2.0) + rows.nD[l] * 4.0 * x->dkv, cs, [&] {
+      mzk::launch_rope_kv(x->qkv, x->nqkv_pad, n, pos, off, x->rope_cs, x->nq, x->nkv, x->hd,
+                          (int64_t)C * x->dkv * 2, x->q16, x->kv_slab, cs);
+    });
+    if (kv_copy[l] && !early_wait) HIPCHK(hipStreamWaitEvent(cs, x->ev_kv[l], 0));
+    double keys = 0;
+    for (int p : rows.R[l]) keys += p + 1.0;
+    const double att_flops = 4.0 * x->hd * x->nq * keys;
+    x->timed(kKAttention, att_flops, (double)n * x->dq * 4.0, cs, [&] {
+      mzk::launch_attention(x->q16, pos, n, x->kv_slab, x->d_tables + (size_t)l * MC, C, x->slot_bytes,
+                            x->nq, x->nkv, x->hd, x->xb, cs);
+    });
+    x->timed(kKGemmO, 2.0 * n * x->dq * d, (double)d * x->dq * bpe_w + n * (x->dq * 2.0 + d * 8.0), cs,
+             [&] { mzk::launch_gemm_q4(x->xb, n, x->d_pad, x->dq, unit + x->off_o, mzk::kEpiAdd, h, cs); });
+    x->timed(kKRmsnorm, 0, (double)n * d * 6.0, cs,
+             [&] { mzk::launch_rmsnorm(h, n, d, x->cfg.rms_eps, x->xb, cs); });
+    x->timed(kKGemmGateUp, 2.0 * n * d * 2.0 * x->ff, 2.0 * x->ff * d * bpe_w + n * (d * 2.0 + x->ff * 2.0), cs,
+             [&] { mzk::launch_gemm_q4(x->xb, n, 2 * x->ffp, d, unit + x->off_gu, mzk::kEpiSwiGLU, x->act, cs); });
+    x->timed(kKGemmDown, 2.0 * n * x->ff * d, (double)d * x->ff * bpe_w + n * (x->ffp * 2.0 + d * 8.0), cs,
+             [&] { mzk::launch_gemm_q4(x->act, n, x->d_pad, x->ffp, unit + x->off_dn, mzk::kEpiAdd, h, cs); });
+    algo += 2.0 * n * d * 2 * x->dq + 2.0 * rows.nD[l] * d * 2 * x->dkv + 2.0 * n * 3 * d * x->ff + att_flops;
+    if (l + 1 < L && rows.nR[l + 1] < n) {
+      const int nn = rows.nR[l + 1];
+      float* dst = x->h[cur ^ 1];
+      x->timed(kKGather, 0, (double)nn * d * 8.0, cs,
+               [&] { mzk::launch_gather_rows(h, x->d_gather + gat_off[l], nn, d, dst, cs); });
+      cur ^= 1;
+    }
+  }
+  x->h_last = x->h[cur] + (int64_t)(rows.nR[L - 1] - 1) * d;
+  x->have_last = true;
+
+  // --- new state: every unit resident, context extended by the prompt
+  for (int l = 0; l < L; ++l) {
+    x->w_state[l] = MZ_RES;
+    for (int c = 0; c < MC; ++c) x->kv_state[(size_t)l * MC + c] = MZ_RES;
+  }
+  x->arena.reset();
+  x->tokens.insert(x->tokens.end(), prompt, prompt + P);
+  x->last_nR = rows.nR;
+  x->last_nD = rows.nD;
+  x->last_swap_kv_bytes = swap_kv;
+  x->last_swap_w_bytes = swap_w;
+  x->last_reload_w_bytes = reload_w;
+  x->last_copies = copies;
+  x->last_algo_flops = algo;
+  x->last_N = N;
+  x->last_P = P;
+  x->last_swap_ms = -1;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- ABI
+
+extern "C" {
+
+const char* mz_version(void) { return kVersion; }
+
+const char* mz_last_error(const mz_ctx* ctx) {
+  return ctx ? ctx->err.c_str() : g_load_error.c_str();
+}
+
+mz_status mz_load_model(const mz_model_cfg* cfg, const void* blob, size_t nbytes, int32_t device,
+                        mz_ctx** out) {
+  if (out) *out = nullptr;
+  std::unique_ptr<mz_ctx> x(new (std::nothrow) mz_ctx());
+  if (!x) {
+    g_load_error = "host allocation failed";
+    return MZ_ENOMEM;
+  }
+  mz_ctx* raw = x.get();
+  mz_status st = guarded(nullptr, [&] {
+    if (!out) fail(MZ_EINVAL, "out is NULL");
+    validate_cfg(cfg);
+    if (!blob) fail(MZ_EINVAL, "blob is NULL");
+    if ((int64_t)nbytes != blob_bytes(cfg))
+      fail(MZ_EINVAL, "blob has %zu bytes, the configuration needs %lld", nbytes, (long long)blob_bytes(cfg));
+    int ndev = 0;
+    HIPCHK(hipGetDeviceCount(&ndev));
+    if (device < 0 || device >= ndev) fail(MZ_EINVAL, "device %d not present (%d devices)", device, ndev);
+    raw->device = device;
+    HIPCHK(hipSetDevice(device));
+    raw->cfg = *cfg;
+    mz_ctx& c = *raw;
+    c.L = cfg->n_layers; c.d = cfg->d_model; c.nq = cfg->n_q_heads; c.nkv = cfg->n_kv_heads;
+    c.hd = cfg->head_dim; c.ff = cfg->d_ffn; c.V = cfg->vocab; c.C = cfg->chunk_tokens;
+    c.max_ctx = cfg->max_ctx;
+    c.dq = c.nq * c.hd; c.dkv = c.nkv * c.hd; c.nqkv = c.dq + 2 * c.dkv;
+    c.nqkv_pad = (int)round_up(c.nqkv, mzk::kGemmTileN);
+    c.d_pad = (int)round_up(c.d, mzk::kGemmTileN);
+    if (c.d_pad != c.d) fail(MZ_EINVAL, "d_model must be a multiple of 128");
+    c.ffp = (int)round_up(c.ff, 64);
+    c.max_chunks = c.nchunks_of(c.max_ctx);
+    c.slot_bytes = (int64_t)c.C * c.dkv * 2 * 2;
+
+    // weight unit layout
+    const int64_t b_qkv = gemm_packed_bytes(c.nqkv, c.d), b_o = gemm_packed_bytes(c.d, c.dq),
+                  b_gu = gemm_packed_bytes(2 * (int64_t)c.ffp, c.d), b_dn = gemm_packed_bytes(c.d, c.ffp);
+    c.off_qkv = 0;
+    c.off_o = round_up(b_qkv, 256);
+    c.off_gu = c.off_o + round_up(b_o, 256);
+    c.off_dn = c.off_gu + round_up(b_gu, 256);
+    c.unit_bytes = round_up(c.off_dn + b_dn, 4096);
+
+    HIPCHK(hipStreamCreateWithFlags(&c.s_compute, hipStreamNonBlocking));
+    HIPCHK(hipStreamCreateWithFlags(&c.s_swap, hipStreamNonBlocking));
+    c.ev_w.resize(c.L);
+    c.ev_kv.resize(c.L);
+    for (int l = 0; l < c.L; ++l) {
+      HIPCHK(hipEventCreateWithFlags(&c.ev_w[l], hipEventDisableTiming));
+      HIPCHK(hipEventCreateWithFlags(&c.ev_kv[l], hipEventDisableTiming));
+    }
+    HIPCHK(hipEventCreate(&c.ev_swap_start));
+    HIPCHK(hipEventCreate(&c.ev_swap_end));
+
+    // repack layer units into a pinned host image, then upload
+    void* img = nullptr;
+    if (hipHostMalloc(&img, (size_t)c.unit_bytes * c.L, hipHostMallocDefault) != hipSuccess || !img)
+      fail(MZ_ENOMEM, "pinned host allocation for the weight image failed");
+    c.w_image = (uint8_t*)img;
+    const uint8_t* bp = (const uint8_t*)blob;
+    const int64_t rb_d = q4_row_bytes(c.d);
+    for (int l = 0; l < c.L; ++l) {
+      uint8_t* u = c.w_image + (int64_t)l * c.unit_bytes;
+      memset(u, 0, c.unit_bytes);
+      const uint8_t* wq = bp;                                  // Wq, Wk, Wv are consecutive rows
+      const uint8_t* wo = wq + (int64_t)c.nqkv * rb_d;
+      const uint8_t* wg = wo + (int64_t)c.d * q4_row_bytes(c.dq);
+      const uint8_t* wu = wg + (int64_t)c.ff * rb_d;
+      const uint8_t* wd = wu + (int64_t)c.ff * rb_d;
+      pack_plain(wq, c.nqkv, c.d, u + c.off_qkv);
+      pack_plain(wo, c.d, c.dq, u + c.off_o);
+      pack_gateup(wg, wu, c.ff, c.d, u + c.off_gu);
+      pack_plain(wd, c.d, c.ff, u + c.off_dn);
+      bp = wd + (int64_t)c.d * q4_row_bytes(c.ff);
+    }
+    c.w_slab = (uint8_t*)dmalloc((size_t)c.unit_bytes * c.L);
+    c.w_pool.init(c.L);
+    c.w_slot.resize(c.L);
+    c.w_state.assign(c.L, MZ_RES);
+    c.w_entry.resize(c.L);
+    for (int l = 0; l < c.L; ++l) c.w_slot[l] = c.w_pool.alloc_one();
+    HIPCHK(hipMemcpy(c.w_slab, c.w_image, (size_t)c.unit_bytes * c.L, hipMemcpyHostToDevice));
+
+    // embedding and output head, split into nibble and scale planes
+    {
+      const int64_t nib_b = (int64_t)c.V * c.d / 2, sc_b = (int64_t)c.V * (c.d / 32) * 2;
+      std::vector<uint8_t> nib(nib_b);
+      std::vector<uint16_t> sc((size_t)c.V * (c.d / 32));
+      c.emb_nib = (uint8_t*)dmalloc(nib_b);
+      c.emb_sc = (uint16_t*)dmalloc(sc_b);
+      c.lm_nib = (uint8_t*)dmalloc(nib_b);
+      c.lm_sc = (uint16_t*)dmalloc(sc_b);
+      split_rows(bp, c.V, c.d, nib.data(), sc.data());
+      HIPCHK(hipMemcpy(c.emb_nib, nib.data(), nib_b, hipMemcpyHostToDevice));
+      HIPCHK(hipMemcpy(c.emb_sc, sc.data(), sc_b, hipMemcpyHostToDevice));
+      split_rows(bp + (int64_t)c.V * rb_d, c.V, c.d, nib.data(), sc.data());
+      HIPCHK(hipMemcpy(c.lm_nib, nib.data(), nib_b, hipMemcpyHostToDevice));
+      HIPCHK(hipMemcpy(c.lm_sc, sc.data(), sc_b, hipMemcpyHostToDevice));
+    }
+    // RoPE table: angles in double precision, stored as float (cos, sin)
+    {
+      const int half = c.hd / 2;
+      std::vector<float2> cs((size_t)c.max_ctx * half);
+      for (int p = 0; p < c.max_ctx; ++p)
+        for (int i = 0; i < half; ++i) {
+          const double inv = std::pow((double)cfg->rope_theta, -2.0 * i / c.hd);
+          const double a = (double)p * inv;
+          cs[(size_t)p * half + i] = make_float2((float)std::cos(a), (float)std::sin(a));
+        }
+      c.rope_cs = (float2*)dmalloc(cs.size() * sizeof(float2));
+      HIPCHK(hipMemcpy(c.rope_cs, cs.data(), cs.size() * sizeof(float2), hipMemcpyHostToDevice));
+    }
+    // KV slab
+    const int n_slots = c.L * c.max_chunks;
+    c.kv_slab = (uint8_t*)dmalloc((size_t)n_slots * c.slot_bytes);
+    HIPCHK(hipMemset(c.kv_slab, 0, (size_t)n_slots * c.slot_bytes));
+    c.kv_pool.init(n_slots);
+    c.table.assign((size_t)c.L * c.max_chunks, -1);
+    c.kv_state.assign((size_t)c.L * c.max_chunks, MZ_RES);
+    c.kv_entry.resize((size_t)c.L * c.max_chunks);
+
+    // activations
+    const int64_t M = c.max_ctx;
+    c.h[0] = (float*)dmalloc((size_t)M * c.d * 4);
+    c.h[1] = (float*)dmalloc((size_t)M * c.d * 4);
+    c.xb = dmalloc((size_t)M * std::max(c.d, c.dq) * 2);
+    c.qkv = (float*)dmalloc((size_t)M * c.nqkv_pad * 4);
+    c.q16 = dmalloc((size_t)M * c.dq * 2);
+    c.act = dmalloc((size_t)M * c.ffp * 2);
+    c.logits = (float*)dmalloc((size_t)c.V * 4);
+    const int nblk = (c.V + 63) / 64;
+    c.part_val = (float*)dmalloc((size_t)nblk * 4);
+    c.part_idx = (int32_t*)dmalloc((size_t)nblk * 4);
+    c.d_token = (int32_t*)dmalloc(4);
+
+    // restore metadata
+    const int64_t tot = (int64_t)c.L * M;
+    c.d_tables = (int32_t*)dmalloc((size_t)c.L * c.max_chunks * 4);
+    c.d_pos = (int32_t*)dmalloc((size_t)tot * 4);
+    c.d_kvoff = (int64_t*)dmalloc((size_t)tot * 8);
+    c.d_gather = (int32_t*)dmalloc((size_t)tot * 4);
+    c.d_tok = (int32_t*)dmalloc((size_t)M * 4);
+    c.stage_bytes = (size_t)c.L * c.max_chunks * 4 + (size_t)tot * 16 + (size_t)M * 4 + 8 * 256;
+    void* stage = nullptr;
+    if (hipHostMalloc(&stage, c.stage_bytes, hipHostMallocDefault) != hipSuccess || !stage)
+      fail(MZ_ENOMEM, "pinned staging allocation failed");
+    c.h_stage = (uint8_t*)stage;
+    void* tokp = nullptr;
+    if (hipHostMalloc(&tokp, 64, hipHostMallocDefault) != hipSuccess || !tokp)
+      fail(MZ_ENOMEM, "pinned allocation failed");
+    c.h_token = (int32_t*)tokp;
+    HIPCHK(hipDeviceSynchronize());
+  });
+  if (st != MZ_OK) {
+    mz_free(x.release());
+    return st;
+  }
+  *out = x.release();
+  return MZ_OK;
+}
+
+void mz_free(mz_ctx* x) {
+  if (!x) return;
+  (void)hipSetDevice(x->device);
+  if (x->s_compute) (void)hipStreamSynchronize(x->s_compute);
+  if (x->s_swap) (void)hipStreamSynchronize(x->s_swap);
+  void* dptrs[] = {x->w_slab, x->emb_nib, x->emb_sc, x->lm_nib, x->lm_sc, x->rope_cs, x->kv_slab,
+                   x->h[0], x->h[1], x->xb, x->qkv, x->q16, x->act, x->logits, x->part_val,
+                   x->part_idx, x->d_token, x->d_tables, x->d_pos, x->d_kvoff, x->d_gather, x->d_tok};
+  for (void* p : dptrs)
+    if (p) (void)hipFree(p);
+  if (x->w_image) (void)hipHostFree(x->w_image);
+  if (x->h_stage) (void)hipHostFree(x->h_stage);
+  if (x->h_token) (void)hipHostFree(x->h_token);
+  x->arena.release_all();
+  for (auto e : x->ev_w) if (e) (void)hipEventDestroy(e);
+  for (auto e : x->ev_kv) if (e) (void)hipEventDestroy(e);
+  for (auto e : x->ev_pool) (void)hipEventDestroy(e);
+  if (x->ev_swap_start) (void)hipEventDestroy(x->ev_swap_start);
+  if (x->ev_swap_end) (void)hipEventDestroy(x->ev_swap_end);
+  if (x->s_compute) (void)hipStreamDestroy(x->s_compute);
+  if (x->s_swap) (void)hipStreamDestroy(x->s_swap);
+  delete x;
+}
+
+mz_status mz_set_option(mz_ctx* x, const char* key, int64_t value) {
+  if (!x) return MZ_EINVAL;
+  return guarded(x, [&] {
+    if (!key) fail(MZ_EINVAL, "key is NULL");
+    const std::string k(key);
+    if (k == "overlap") x->overlap = value != 0;
+    else if (k == "debug_swap_delay_us") x->debug_swap_delay_us = value < 0 ? 0 : value;
+    else if (k == "debug_poison") x->debug_poison = value != 0;
+    else if (k == "kernel_timing") {
+      HIPCHK(hipStreamSynchronize(x->s_compute));
+      x->collect_timing();
+      x->timing = value != 0;
+      for (auto& s : x->kstats) s = KindStats();
+    } else fail(MZ_EINVAL, "unknown option '%s'", key);
+  });
+}
+
+static void check_tokens(const mz_ctx* x, const int32_t* t, int32_t n) {
+  if (n < 0) fail(MZ_EINVAL, "token count is negative");
+  if (n > 0 && !t) fail(MZ_EINVAL, "tokens is NULL");
+  if (n > x->max_ctx) fail(MZ_EINVAL, "%d tokens exceed max_ctx (%d)", n, x->max_ctx);
+  for (int i = 0; i < n; ++i)
+    if (t[i] < 0 || t[i] >= x->V) fail(MZ_EINVAL, "token %d out of range", t[i]);
+}
+
+mz_status mz_prefill_context(mz_ctx* x, const int32_t* tokens, int32_t n) {
+  if (!x) return MZ_EINVAL;
+  return guarded(x, [&] {
+    check_tokens(x, tokens, n);
+    if (n == 0) fail(MZ_EINVAL, "empty context");
+    HIPCHK(hipStreamSynchronize(x->s_compute));
+    HIPCHK(hipStreamSynchronize(x->s_swap));
+    // weights must be resident for a clean prefill: bring evicted units back
+    x->release_context();
+    restore_and_prefill_impl(x, tokens, n);
+  });
+}
+
+mz_status mz_set_context(mz_ctx* x, const int32_t* tokens, int32_t n) {
+  if (!x) return MZ_EINVAL;
+  return guarded(x, [&] {
+    check_tokens(x, tokens, n);
+    HIPCHK(hipStreamSynchronize(x->s_compute));
+    HIPCHK(hipStreamSynchronize(x->s_swap));
+    x->release_context();
+    const int nc = x->nchunks_of(n);
+    for (int l = 0; l < x->L; ++l)
+      for (int c = 0; c < nc; ++c) {
+        int s = x->kv_pool.alloc_one();
+        if (s < 0) fail(MZ_ENOMEM, "KV slot pool exhausted");
+        x->table[(size_t)l * x->max_chunks + c] = s;
+        mzk::launch_zero(x->kv_slab + (int64_t)s * x->slot_bytes, x->slot_bytes / 4, x->s_compute);
+      }
+    HIPCHK(hipGetLastError());
+    HIPCHK(hipStreamSynchronize(x->s_compute));
+    x->tokens.assign(tokens, tokens + n);
+  });
+}
+
+mz_status mz_truncate_context(mz_ctx* x, int32_t n) {
+  if (!x) return MZ_EINVAL;
+  return guarded(x, [&] {
+    if (n < 0 || n > (int)x->tokens.size()) fail(MZ_EINVAL, "n=%d outside 0..%zu", n, x->tokens.size());
+    const int nc = x->nchunks_of((int)x->tokens.size()), keep = x->nchunks_of(n);
+    for (int l = 0; l < x->L; ++l) {
+      if (x->w_state[l] != MZ_RES) fail(MZ_ESTATE, "weights of layer %d are evicted", l);
+      for (int c = 0; c < nc; ++c)
+        if (x->kv_state[(size_t)l * x->max_chunks + c] != MZ_RES) fail(MZ_ESTATE, "KV chunks are evicted");
+    }
+    HIPCHK(hipStreamSynchronize(x->s_compute));
+    HIPCHK(hipStreamSynchronize(x->s_swap));
+    for (int l = 0; l < x->L; ++l)
+      for (int c = keep; c < nc; ++c) {
+        int32_t& t = x->table[(size_t)l * x->max_chunks + c];
+        if (t >= 0) x->kv_pool.release(t);
+        t = -1;
+      }
+    x->tokens.resize(n);
+    x->have_last = false;
+  });
+}
+
+static int32_t chunk_slot(mz_ctx* x, int32_t layer, int32_t chunk) {
+  if (layer < 0 || layer >= x->L) fail(MZ_EINVAL, "layer %d out of range", layer);
+  const int nc = x->nchunks_of((int)x->tokens.size());
+  if (chunk < 0 || chunk >= nc) fail(MZ_EINVAL, "chunk %d out of range (%d chunks)", chunk, nc);
+  const int32_t s = x->table[(size_t)layer * x->max_chunks + chunk];
+  if (s < 0 || x->kv_state[(size_t)layer * x->max_chunks + chunk] != MZ_RES)
+    fail(MZ_ESTATE, "chunk (%d, %d) is not resident", layer, chunk);
+  return s;
+}
+
+mz_status mz_import_kv(mz_ctx* x, int32_t layer, int32_t chunk, const void* k, const void* v) {
+  if (!x) return MZ_EINVAL;
+  return guarded(x, [&] {
+    if (!k || !v) fail(MZ_EINVAL, "k or v is NULL");
+    const int32_t s = chunk_slot(x, layer, chunk);
+    HIPCHK(hipStreamSynchronize(x->s_compute));
+    const size_t half = (size_t)x->slot_bytes / 2;
+    uint8_t* dst = x->kv_slab + (int64_t)s * x->slot_bytes;
+    HIPCHK(hipMemcpy(dst, k, half, hipMemcpyHostToDevice));
+    HIPCHK(hipMemcpy(dst + half, v, half, hipMemcpyHostToDevice));
+  });
+}
+
+mz_status mz_read_kv(mz_ctx* x, int32_t layer, int32_t chunk, void* k, void* v) {
+  if (!x) return MZ_EINVAL;
+  return guarded(x, [&] {
+    if (!k || !v) fail(MZ_EINVAL, "k or v is NULL");
+    const int32_t s = chunk_slot(x, layer, chunk);
+    HIPCHK(hipStreamSynchronize(x->s_compute));
+    HIPCHK(hipStreamSynchronize(x->s_swap));
+    const size_t half = (size_t)x->slot_bytes / 2;
+    const uint8_t* src = x->kv_slab + (int64_t)s * x->slot_bytes;
+    HIPCHK(hipMemcpy(k, src, half, hipMemcpyDeviceToHost));
+    HIPCHK(hipMemcpy(v, src + half, half, hipMemcpyDeviceToHost));
+  });
+}
+
+mz_status mz_evict(mz_ctx* x, const mz_evict_plan* plan) {
+  if (!x) return MZ_EINVAL;
+  return guarded(x, [&] {
+    if (!plan || !plan->kv_state) fail(MZ_EINVAL, "plan or plan->kv_state is NULL");
+    const int L = x->L, MC = x->max_chunks;
+    const int nc = x->nchunks_of((int)x->tokens.size());
+    if (x->tokens.empty()) fail(MZ_ESTATE, "no cached context to evict");
+    if (plan->n_layers != L || plan->n_chunks != nc)
+      fail(MZ_EINVAL, "plan is %dx%d, the context has %dx%d units", plan->n_layers, plan->n_chunks, L, nc);
+    const int n_units = L * nc + L;
+    auto target = [&](int u) -> int {
+      return u < L * nc ? plan->kv_state[u] : (plan->w_state ? plan->w_state[u - L * nc] : MZ_RES);
+    };
+    auto current = [&](int u) -> int {
+      return u < L * nc ? x->kv_state[(size_t)(u / nc) * MC + u % nc] : x->w_state[u - L * nc];
+    };
+    // visiting order: the given order, then every other unit backward-out
+    std::vector<int> order;
+    std::vector<char> seen(n_units, 0);
+    if (plan->order) {
+      if (plan->n_order < 0) fail(MZ_EINVAL, "n_order is negative");
+      for (int i = 0; i < plan->n_order; ++i) {
+        const int u = plan->order[i];
+        if (u < 0 || u >= n_units || seen[u]) fail(MZ_EINVAL, "order entry %d invalid or repeated", u);
+        seen[u] = 1;
+        order.push_back(u);
+      }
+    }
+    for (int l = L - 1; l >= 0; --l) {
+      for (int c = nc - 1; c >= 0; --c)
+        if (!seen[l * nc + c]) order.push_back(l * nc + c);
+      if (!seen[L * nc + l]) order.push_back(L * nc + l);
+    }
+    // validate before touching anything
+    for (int u = 0; u < n_units; ++u) {
+      const int t = target(u), cur = current(u);
+      if (t != MZ_RES && t != MZ_SWAP && t != MZ_DROP) fail(MZ_EINVAL, "unit %d: state %d invalid", u, t);
+      if (t == MZ_SWAP && cur == MZ_DROP) fail(MZ_ESTATE, "unit %d is dropped and cannot be swapped", u);
+    }
+    HIPCHK(hipStreamSynchronize(x->s_compute));
+    HIPCHK(hipStreamSynchronize(x->s_swap));
+    x->collect_timing();
+    std::vector<int> release_kv;
+    std::vector<int> release_w;
+    for (int u : order) {
+      const int t = target(u), cur = current(u);
+      if (t == MZ_RES || t == cur) continue;
+      if (u < L * nc) {
+        const int l = u / nc, c = u % nc;
+        const size_t idx = (size_t)l * MC + c;
+        if (t == MZ_SWAP) {
+          const ArenaEntry e = x->arena.push((size_t)x->slot_bytes);
+          HIPCHK(hipMemcpyAsync(x->arena.ptr(e), x->kv_slab + (int64_t)x->table[idx] * x->slot_bytes,
+                                x->slot_bytes, hipMemcpyDeviceToHost, x->s_swap));
+          x->kv_entry[idx] = e;
+        }
+        if (cur == MZ_RES) release_kv.push_back(x->table[idx]);
+        x->table[idx] = -1;
+        x->kv_state[idx] = (uint8_t)t;
+      } else {
+        const int l = u - L * nc;
+        if (t == MZ_SWAP) {
+          const ArenaEntry e = x->arena.push((size_t)x->unit_bytes);
+          HIPCHK(hipMemcpyAsync(x->arena.ptr(e), x->unit_ptr(l), x->unit_bytes, hipMemcpyDeviceToHost,
+                                x->s_swap));
+          x->w_entry[l] = e;
+        }
+        if (cur == MZ_RES) release_w.push_back(x->w_slot[l]);
+        x->w_slot[l] = -1;
+        x->w_state[l] = (uint8_t)t;
+      }
+    }
+    HIPCHK(hipStreamSynchronize(x->s_swap));
+    for (int s : release_kv) x->kv_pool.release(s);
+    for (int s : release_w) x->w_pool.release(s);
+    x->have_last = false;
+  });
+}
+
+mz_status mz_restore_and_prefill(mz_ctx* x, const int32_t* prompt, int32_t n_prompt) {
+  if (!x) return MZ_EINVAL;
+  return guarded(x, [&] {
+    if (x->tokens.empty() && n_prompt == 0) fail(MZ_ESTATE, "no cached context and no prompt");
+    if (n_prompt > 0) check_tokens(x, prompt, n_prompt);
+    restore_and_prefill_impl(x, prompt, n_prompt);
+  });
+}
+
+mz_status mz_first_token(mz_ctx* x, int32_t* token_out, float* logits_out) {
+  if (!x) return MZ_EINVAL;
+  return guarded(x, [&] {
+    if (!token_out) fail(MZ_EINVAL, "token_out is NULL");
+    if (!x->have_last) fail(MZ_ESTATE, "no prefill since the last first token");
+    hipStream_t cs = x->s_compute;
+    x->timed(kKLmHead, 2.0 * x->d * x->V, (double)x->V * x->d * 0.5625 + x->V * 4.0, cs, [&] {
+      mzk::launch_lm_head(x->h_last, x->d, x->cfg.rms_eps, x->lm_nib, x->lm_sc, x->V, x->logits,
+                          x->part_val, x->part_idx, x->d_token, cs);
+    });
+    HIPCHK(hipMemcpyAsync(x->h_token, x->d_token, 4, hipMemcpyDeviceToHost, cs));
+    if (logits_out)
+      HIPCHK(hipMemcpyAsync(logits_out, x->logits, (size_t)x->V * 4, hipMemcpyDeviceToHost, cs));
+    HIPCHK(hipStreamSynchronize(cs));
+    *token_out = *x->h_token;
+    x->have_last = false;
+    if (x->swap_timed) {
+      HIPCHK(hipEventSynchronize(x->ev_swap_end));
+      float ms = 0;
+      HIPCHK(hipEventElapsedTime(&ms, x->ev_swap_start, x->ev_swap_end));
+      x->last_swap_ms = ms;
+      x->swap_timed = false;
+    }
+    x->collect_timing();
+  });
+}
+
+mz_status mz_stats(mz_ctx* x, char* out, size_t cap) {
+  if (!x) return MZ_EINVAL;
+  return guarded(x, [&] {
+    if (!out) fail(MZ_EINVAL, "json_out is NULL");
+    std::string s = "{";
+    char buf[512];
+    snprintf(buf, sizeof buf, "\"version\": \"%s\", \"n_ctx\": %zu, \"last_N\": %d, \"last_P\": %d, ",
+             kVersion, x->tokens.size(), x->last_N, x->last_P);
+    s += buf;
+    auto arr = [&](const char* name, const std::vector<int32_t>& v) {
+      s += "\""; s += name; s += "\": [";
+      for (size_t i = 0; i < v.size(); ++i) {
+        if (i) s += ", ";
+        s += std::to_string(v[i]);
+      }
+      s += "], ";
+    };
+    arr("nR", x->last_nR);
+    arr("nD", x->last_nD);
+    snprintf(buf, sizeof buf,
+             "\"swap_kv_bytes\": %lld, \"swap_w_bytes\": %lld, \"reload_w_bytes\": %lld, \"copies\": %lld, "
+             "\"swap_ms\": %.6f, \"algo_flops\": %.6e, ",
+             (long long)x->last_swap_kv_bytes, (long long)x->last_swap_w_bytes,
+             (long long)x->last_reload_w_bytes, (long long)x->last_copies, x->last_swap_ms,
+             x->last_algo_flops);
+    s += buf;
+    snprintf(buf, sizeof buf,
+             "\"pool\": {\"kv_slots\": %d, \"kv_slots_used\": %d, \"slot_bytes\": %lld, \"w_units\": %d, "
+             "\"w_units_used\": %d, \"unit_bytes\": %lld, \"arena_reserved\": %zu}, ",
+             x->kv_pool.n, x->kv_pool.used(), (long long)x->slot_bytes, x->w_pool.n, x->w_pool.used(),
+             (long long)x->unit_bytes, x->arena.reserved());
+    s += buf;
+    s += "\"kernels\": {";
+    bool first = true;
+    for (int k = 0; k < kKCount; ++k) {
+      const KindStats& ks = x->kstats[k];
+      if (!ks.launches) continue;
+      snprintf(buf, sizeof buf,
+               "%s\"%s\": {\"kernel\": \"%s\", \"launches\": %lld, \"ms\": %.6f, \"flops\": %.6e, \"bytes\": %.6e}",
+               first ? "" : ", ", kKindName[k], kKindKernel[k], (long long)ks.launches, ks.ms, ks.flops,
+               ks.bytes);
+      s += buf;
+      first = false;
+    }
+    s += "}}";
+    if (s.size() + 1 > cap) fail(MZ_EINVAL, "json buffer needs %zu bytes", s.size() + 1);
+    memcpy(out, s.c_str(), s.size() + 1);
+  });
+}
+
+mz_status mz_plan_rows(const mz_model_cfg* cfg, const uint8_t* kv_state, int32_t n_chunks, int32_t n_ctx,
+                       int32_t n_prompt, int32_t* nR, int32_t* nD, int32_t* rows_out, int64_t rows_cap) {
+  return guarded(nullptr, [&] {
+    if (!cfg || !kv_state || !nR || !nD) fail(MZ_EINVAL, "NULL argument");
+    if (cfg->n_layers < 1 || cfg->chunk_tokens < 1) fail(MZ_EINVAL, "bad cfg");
+    if (n_ctx < 0 || n_prompt < 0 || n_ctx + n_prompt < 1) fail(MZ_EINVAL, "bad token counts");
+    if (n_chunks != (n_ctx + cfg->chunk_tokens - 1) / cfg->chunk_tokens) fail(MZ_EINVAL, "n_chunks mismatch");
+    for (int64_t i = 0; i < (int64_t)cfg->n_layers * n_chunks; ++i)
+      if (kv_state[i] > MZ_DROP) fail(MZ_EINVAL, "bad state value");
+    Rows r = compute_rows(kv_state, cfg->n_layers, n_chunks, n_ctx, n_prompt, cfg->chunk_tokens);
+    int64_t tot = 0;
+    for (int l = 0; l < cfg->n_layers; ++l) {
+      nR[l] = r.nR[l];
+      nD[l] = r.nD[l];
+      tot += r.nR[l];
+    }
+    if (rows_out) {
+      if (tot > rows_cap) fail(MZ_EINVAL, "rows_cap %lld < %lld", (long long)rows_cap, (long long)tot);
+      int64_t o = 0;
+      for (auto& v : r.R)
+        for (int32_t p : v) rows_out[o++] = p;
+    }
+  });
+}
+
+int64_t mz_q4_gemm_packed_bytes(int32_t n, int32_t k) {
+  if (n < 1 || k < 1) return 0;
+  return gemm_packed_bytes(n, k);
+}
+
+mz_status mz_q4_gemm_pack(const void* w, const void* w_up, int32_t n, int32_t k, void* out) {
+  return guarded(nullptr, [&] {
+    if (!w || !out || n < 1 || k < 1) fail(MZ_EINVAL, "bad arguments");
+    if (w_up)
+      pack_gateup((const uint8_t*)w, (const uint8_t*)w_up, n, k, (uint8_t*)out);
+    else
+      pack_plain((const uint8_t*)w, n, k, (uint8_t*)out);
+  });
+}
+
+mz_status mz_q4_gemm(const void* x_f16, int32_t m, int32_t n_pad, int32_t k, const void* w_packed,
+                     int32_t epilogue, void* y, void* stream) {
+  return guarded(nullptr, [&] {
+    if (!x_f16 || !w_packed || !y) fail(MZ_EINVAL, "NULL pointer");
+    if (m < 1 || n_pad < 1 || k < 1) fail(MZ_EINVAL, "sizes must be positive");
+    if (n_pad % mzk::kGemmTileN) fail(MZ_EINVAL, "n_pad must be a multiple of %d", mzk::kGemmTileN);
+    if (k % mzk::kGemmTileK) fail(MZ_EINVAL, "k must be a multiple of %d", mzk::kGemmTileK);
+    if (epilogue < 0 || epilogue > 2) fail(MZ_EINVAL, "bad epilogue");
+    mzk::launch_gemm_q4(x_f16, m, n_pad, k, w_packed, epilogue, y, (hipStream_t)stream);
+    HIPCHK(hipGetLastError());
+  });
+}
+
+mz_status mz_attention(const void* q, const int32_t* qpos, int32_t m, const void* slab, const int32_t* table,
+                       int32_t n_table, int32_t chunk_tokens, int32_t n_q, int32_t n_kv, int32_t head_dim,
+                       void* out, void* stream) {
+  return guarded(nullptr, [&] {
+    if (!q || !qpos || !slab || !table || !out) fail(MZ_EINVAL, "NULL pointer");
+    if (m < 1 || n_table < 1 || chunk_tokens < 1) fail(MZ_EINVAL, "sizes must be positive");
+    if (head_dim != 64 && head_dim != 128) fail(MZ_EINVAL, "head_dim must be 64 or 128");
+    if (n_kv < 1 || n_q % n_kv || n_q / n_kv > 8) fail(MZ_EINVAL, "bad head counts");
+    const int64_t slot_bytes = (int64_t)chunk_tokens * n_kv * head_dim * 2 * 2;
+    mzk::launch_attention(q, qpos, m, slab, table, chunk_tokens, slot_bytes, n_q, n_kv, head_dim, out,
+                          (hipStream_t)stream);
+    HIPCHK(hipGetLastError());
+  });
+}
+
+mz_status mz_rmsnorm(const void* h, int32_t m, int32_t d, float eps, void* x, void* stream) {
+  return guarded(nullptr, [&] {
+    if (!h || !x) fail(MZ_EINVAL, "NULL pointer");
+    if (m < 1 || d < 4 || d % 4) fail(MZ_EINVAL, "bad sizes");
+    mzk::launch_rmsnorm((const float*)h, m, d, eps, x, (hipStream_t)stream);
+    HIPCHK(hipGetLastError());
+  });
+}
+
+}  // extern "C"

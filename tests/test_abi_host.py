@@ -1,0 +1,155 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads and
+exports every function include/mz.h declares; the restore planner's rows
+match the oracle's; the GEMM repacker lays Q4_0 blocks out as documented;
+calls that need a device fail cleanly without one."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle as O
+from paper_2609_01338_amd import mz
+from paper_2609_01338_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module", autouse=True)
+def built():
+    if not os.path.exists(mz.LIB_PATH):
+        from paper_2609_01338_amd import build
+        build.build_all()
+    mz.lib()
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "mz.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(mz_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_symbol():
+    names = _declared_functions()
+    assert len(names) >= 19
+    lib = ctypes.CDLL(mz.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert mz.mz_version().startswith("mz-mi355x")
+
+
+def test_plan_rows_match_oracle():
+    rng = np.random.default_rng(1)
+    for trial in range(25):
+        L = int(rng.integers(1, 5))
+        C = int(rng.choice([4, 16, 256]))
+        N = int(rng.integers(1, 6 * C))
+        P = int(rng.integers(0, 2 * C))
+        nc = (N + C - 1) // C
+        st = rng.integers(0, 3, (L, nc)).astype(np.uint8)
+        model = W.ModelConfig("t", L, 128, 2, 1, 64, 64, 32, 1e4, C)
+        cfg = mz.make_cfg(model, N + P)
+        nR, nD, R = mz.mz_plan_rows(cfg, st, N, P)
+        oR, oD = O.restore_rows(st, N, P, C)
+        assert nR.tolist() == [r.size for r in oR]
+        assert nD.tolist() == [d.size for d in oD]
+        for l in range(L):
+            assert np.array_equal(R[l], oR[l])
+
+
+def test_plan_rows_workloads():
+    """Row counts of the five measured workloads (the sizes the bench times)."""
+    for key in W.ORDERED_KEYS:
+        w = W.WORKLOADS[key]
+        plan = W.make_plan(w)
+        cfg = mz.make_cfg(w.model, w.n_ctx + w.n_prompt)
+        nR, nD, _ = mz.mz_plan_rows(cfg, plan.kv_state, w.n_ctx, w.n_prompt, with_rows=False)
+        oR, oD = O.restore_rows(plan.kv_state, w.n_ctx, w.n_prompt, w.model.chunk_tokens)
+        assert nR.tolist() == [r.size for r in oR], key
+        assert nD.tolist() == [d.size for d in oD], key
+    w = W.WORKLOADS["8b"]
+    nR, nD, _ = mz.mz_plan_rows(mz.make_cfg(w.model, 32896), W.make_plan(w).kv_state, 32768, 128,
+                                with_rows=False)
+    assert nR[0] == 32896 and nD[0] == 128          # layers 0-7 resident: only the prompt is written
+
+
+def test_plan_rows_errors():
+    model = W.ModelConfig("t", 2, 128, 2, 1, 64, 64, 32, 1e4, 16)
+    cfg = mz.make_cfg(model, 64)
+    mz.mz_plan_rows(cfg, np.zeros((2, 3), np.uint8), 40, 0)        # 40 tokens need 3 chunks
+    with pytest.raises(mz.MzError) as e:
+        mz.mz_plan_rows(cfg, np.zeros((2, 2), np.uint8), 40, 0)
+    assert e.value.status == mz.MZ_EINVAL
+    with pytest.raises(mz.MzError):
+        mz.mz_plan_rows(cfg, np.full((2, 3), 7, np.uint8), 40, 0)
+
+
+def test_plan_rows_ok_case():
+    model = W.ModelConfig("t", 2, 128, 2, 1, 64, 64, 32, 1e4, 16)
+    cfg = mz.make_cfg(model, 64)
+    st = np.zeros((2, 3), np.uint8)
+    st[1, 1] = mz.MZ_DROP
+    nR, nD, R = mz.mz_plan_rows(cfg, st, 40, 2)
+    assert R[0].tolist() == list(range(16, 32)) + [40, 41]
+    assert R[1].tolist() == list(range(16, 32)) + [40, 41]
+    assert nD.tolist() == [2, 18]
+
+
+def test_gemm_pack_layout():
+    """Tile (nt, kt) holds rows nt*128.., blocks kt*2..: nibbles (row, block) x 16 B,
+    then the fp16 scales; padding rows/blocks carry scale 0."""
+    rng = np.random.default_rng(2)
+    n, k = 200, 96                       # n pads to 256, k to 128
+    x = rng.standard_normal((n, k)).astype(np.float32)
+    raw = W.encode_q4_0(x)               # [n, 3 blocks * 18]
+    packed = mz.mz_q4_gemm_pack(raw, n, k)
+    tiles = packed.reshape(2, 2, 4608)   # [n tiles][k tiles][bytes]
+    blocks = raw.reshape(n, 3, 18)
+    for nt in range(2):
+        for kt in range(2):
+            t = tiles[nt, kt]
+            nib = t[:4096].reshape(128, 2, 16)
+            sc = t[4096:].reshape(128, 2, 2)
+            for r in (0, 5, 71, 127):
+                row = nt * 128 + r
+                for b in range(2):
+                    blk = kt * 2 + b
+                    if row < n and blk < 3:
+                        assert bytes(nib[r, b]) == bytes(blocks[row, blk, 2:])
+                        assert bytes(sc[r, b]) == bytes(blocks[row, blk, :2])
+                    else:
+                        assert bytes(sc[r, b]) == b"\0\0"
+
+
+def test_gemm_pack_gateup_interleave():
+    rng = np.random.default_rng(3)
+    n, k = 40, 64                        # n pads to 64 per matrix -> 128 packed rows
+    g = W.encode_q4_0(rng.standard_normal((n, k)).astype(np.float32))
+    u = W.encode_q4_0(rng.standard_normal((n, k)).astype(np.float32))
+    packed = mz.mz_q4_gemm_pack(g, n, k, w_up=u)
+    assert packed.size == mz.mz_q4_gemm_packed_bytes(128, 64)
+    nib = packed[:4096].reshape(128, 2, 16)
+    gb, ub = g.reshape(n, 2, 18), u.reshape(n, 2, 18)
+    for pr in range(128):
+        grp, i = divmod(pr, 32)
+        src = grp * 16 + (i if i < 16 else i - 16)
+        if src < n:
+            ref = (gb if i < 16 else ub)[src]
+            assert bytes(nib[pr, 0]) == bytes(ref[0, 2:])
+
+
+def test_load_model_without_gpu_fails_cleanly():
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    w = W.WORKLOADS["tiny"]
+    blob = W.make_blob(w)
+    with pytest.raises(mz.MzError) as e:
+        mz.mz_load_model(mz.make_cfg(w.model, 256), blob, 0)
+    assert e.value.status in (mz.MZ_EHIP, mz.MZ_EINVAL)
+    # wrong blob size is rejected before any device call
+    with pytest.raises(mz.MzError) as e:
+        mz.mz_load_model(mz.make_cfg(w.model, 256), blob[:-1], 0)
+    assert e.value.status == mz.MZ_EINVAL

@@ -1,0 +1,236 @@
+"""End-to-end parity of evict -> restore -> first token on the GPU against the
+CPU oracle, through the model-level C ABI.
+
+Bars: restored swap chunks are byte-identical to what was evicted; resident
+chunks are untouched; every recomputed K/V element is within 2e-2 of the
+oracle's; first-token logits within 5e-2; the greedy token is equal (a
+mismatch is accepted only as a near-tie: the oracle's logits for the two
+tokens differ by less than twice the measured logit error, and it is
+reported).  Workloads: the tiny configuration as specified, and each larger
+configuration's layer shape with fewer layers and a shorter context so that
+the oracle finishes in seconds.
+"""
+
+import numpy as np
+import pytest
+
+import oracle as O
+from paper_2609_01338_amd import mz
+from paper_2609_01338_amd import workloads as W
+from gpu_util import report, torch_cuda
+
+pytestmark = pytest.mark.gpu
+
+KV_TOL = 2e-2
+LOGIT_TOL = 5e-2
+
+_blobs = {}
+
+
+def blob_for(w):
+    if w.key not in _blobs:
+        _blobs.clear()
+        _blobs[w.key] = W.make_blob(w)
+    return _blobs[w.key]
+
+
+def _chunks(S, C):
+    return (S + C - 1) // C
+
+
+def _check_token(tok, logits, otok, ologits, name):
+    err = float(np.abs(logits.astype(np.float64) - ologits).max())
+    srt = np.sort(ologits)
+    margin = float(srt[-1] - srt[-2])
+    report("  first token", gpu=tok, oracle=otok, logit_err=f"{err:.3e}", oracle_margin=f"{margin:.3e}")
+    assert err <= LOGIT_TOL, name
+    if tok != otok:
+        gap = abs(float(ologits[tok] - ologits[otok]))
+        report("  NEAR-TIE", case=name, gap=gap)
+        assert gap <= 2 * err, name
+
+
+def run_import_flow(w, kv_state, w_state, prompt, name, engine=None):
+    """Import the oracle's clean KV, evict, restore, first token; compare."""
+    torch_cuda()
+    m = w.model
+    C, dkv, L = m.chunk_tokens, m.dkv, m.n_layers
+    blob = blob_for(w)
+    ctx, _ = W.make_tokens(w)
+    hp = O.Hyper(m)
+    wts = O.Weights(hp, blob)
+    Kc, Vc, _ = O.clean_prefill(hp, wts, ctx)
+    ox = O.OracleContext(m, blob)
+    ox.set_context(ctx)
+    nc = _chunks(ctx.size, C)
+
+    def chunk_of(arr, c):
+        out = np.zeros((C, dkv), np.float16)
+        n = min(C, ctx.size - c * C)
+        out[:n] = arr[c * C:c * C + n]
+        return out
+
+    S = ctx.size + len(prompt)
+    eng = engine or mz.Engine(m, blob, max_ctx=S + 16)
+    try:
+        mz.mz_set_context(eng.ctx, ctx)
+        for l in range(L):
+            for c in range(nc):
+                k, v = chunk_of(Kc[l], c), chunk_of(Vc[l], c)
+                ox.import_kv(l, c, k, v)
+                mz.mz_import_kv(eng.ctx, l, c, k, v)
+        pre = {(l, c): mz.mz_read_kv(eng.ctx, l, c, C, dkv) for l in range(L) for c in range(nc)}
+        report("case", name=name, N=ctx.size, P=len(prompt), **{k: v for k, v in
+                                                                 W.Plan(kv_state, w_state).counts().items()})
+        mz.mz_evict(eng.ctx, kv_state, w_state)
+        ox.evict(kv_state, w_state)
+        mz.mz_restore_and_prefill(eng.ctx, prompt)
+        ox.restore_and_prefill(prompt)
+        tok, logits = mz.mz_first_token(eng.ctx, m.vocab)
+        otok, ologits = ox.first_token()
+        stats = mz.mz_stats(eng.ctx)
+        assert stats["nR"] == ox.stats["nR"] and stats["nD"] == ox.stats["nD"]
+        worst = 0.0
+        for l in range(L):
+            for c in range(_chunks(S, C)):
+                k, v = mz.mz_read_kv(eng.ctx, l, c, C, dkv)
+                ok_, ov_ = ox.read_kv(l, c)
+                n = min(C, S - c * C)
+                st = kv_state[l, c] if c < nc else O.DROP
+                if st == O.SWAP or st == O.RES:
+                    # restored or untouched rows are the evicted bytes
+                    keep = min(C, ctx.size - c * C)
+                    assert k[:keep].tobytes() == pre[(l, c)][0][:keep].tobytes(), (name, l, c)
+                    assert v[:keep].tobytes() == pre[(l, c)][1][:keep].tobytes(), (name, l, c)
+                e = max(np.abs(k[:n].astype(np.float64) - ok_[:n]).max(),
+                        np.abs(v[:n].astype(np.float64) - ov_[:n]).max())
+                worst = max(worst, float(e))
+        report("  kv", max_err=f"{worst:.3e}")
+        assert worst <= KV_TOL, name
+        _check_token(tok, logits, otok, ologits, name)
+    finally:
+        if engine is None:
+            eng.close()
+
+
+TINY = W.WORKLOADS["tiny"]
+
+
+@pytest.fixture(scope="module")
+def tiny_engine():
+    torch_cuda()
+    eng = mz.Engine(TINY.model, blob_for(TINY), max_ctx=256)
+    yield eng
+    eng.close()
+
+
+def _tiny_plans():
+    L, nc = TINY.model.n_layers, TINY.n_chunks
+    out = [("workload", W.make_plan(TINY).kv_state, None),
+           ("all-res", np.zeros((L, nc), np.uint8), None),
+           ("all-drop", np.full((L, nc), O.DROP, np.uint8), None),
+           ("all-swap", np.full((L, nc), O.SWAP, np.uint8), np.full(L, O.SWAP, np.uint8))]
+    for seed in range(4):
+        p = W.random_plan(L, nc, 0.35, 0.35, seed, w_swap=0.4, w_drop=0.3)
+        out.append((f"rand-{seed}", p.kv_state, p.w_state))
+    return out
+
+
+@pytest.mark.parametrize("P", [0, 5, 19])
+def test_tiny_import_flow_plans(tiny_engine, P):
+    prm = np.random.default_rng(11).integers(0, TINY.model.vocab, P).astype(np.int32)
+    for name, kv, ws in _tiny_plans():
+        run_import_flow(TINY, kv, ws, prm, f"tiny-{name}-P{P}", engine=tiny_engine)
+
+
+def test_tiny_prefill_flow_matches_clean_oracle(tiny_engine):
+    """GPU full prefill (the cold-start path) vs the oracle's clean prefill."""
+    m = TINY.model
+    ctx, _ = W.make_tokens(TINY)
+    hp = O.Hyper(m)
+    Kc, Vc, lc = O.clean_prefill(hp, O.Weights(hp, blob_for(TINY)), ctx)
+    mz.mz_prefill_context(tiny_engine.ctx, ctx)
+    tok, logits = mz.mz_first_token(tiny_engine.ctx, m.vocab)
+    _check_token(tok, logits, O.argmax_first(lc), lc, "tiny-prefill")
+    for l in range(m.n_layers):
+        for c in range(TINY.n_chunks):
+            k, v = mz.mz_read_kv(tiny_engine.ctx, l, c, m.chunk_tokens, m.dkv)
+            assert np.abs(k.astype(np.float64) - Kc[l][c * 16:(c + 1) * 16]).max() <= KV_TOL
+            assert np.abs(v.astype(np.float64) - Vc[l][c * 16:(c + 1) * 16]).max() <= KV_TOL
+
+
+def test_tiny_partial_chunk_and_double_evict(tiny_engine):
+    m = TINY.model
+    w = W.Workload("tiny117", 1, m, 117, 0, "all-drop", "")
+    nc = _chunks(117, 16)
+    kv = np.zeros((m.n_layers, nc), np.uint8)
+    kv[0, nc - 1] = O.SWAP
+    kv[1, 3] = O.DROP
+    kv[1, nc - 1] = O.SWAP
+    run_import_flow(w, kv, None, np.arange(9, dtype=np.int32), "tiny-partial-swap-last")
+
+
+def test_tiny_overlap_race_poisoned_and_delayed(tiny_engine):
+    """Swap-in delayed on its stream: the compute stream must still wait for it."""
+    mz.mz_set_option(tiny_engine.ctx, "debug_swap_delay_us", 20000)
+    mz.mz_set_option(tiny_engine.ctx, "debug_poison", 1)
+    try:
+        L, nc = TINY.model.n_layers, TINY.n_chunks
+        kv = np.full((L, nc), O.SWAP, np.uint8)
+        kv[1, ::3] = O.DROP
+        run_import_flow(TINY, kv, np.array([O.SWAP, O.RES], np.uint8), np.arange(4, dtype=np.int32),
+                        "tiny-delayed-swap", engine=tiny_engine)
+        mz.mz_set_option(tiny_engine.ctx, "overlap", 0)
+        run_import_flow(TINY, kv, None, np.zeros(0, np.int32), "tiny-serialized", engine=tiny_engine)
+    finally:
+        mz.mz_set_option(tiny_engine.ctx, "overlap", 1)
+        mz.mz_set_option(tiny_engine.ctx, "debug_swap_delay_us", 0)
+        mz.mz_set_option(tiny_engine.ctx, "debug_poison", 0)
+
+
+def test_tiny_error_paths(tiny_engine):
+    m = TINY.model
+    ctx, _ = W.make_tokens(TINY)
+    e = tiny_engine.ctx
+    mz.mz_prefill_context(e, ctx)
+    mz.mz_first_token(e)
+    with pytest.raises(mz.MzError) as ei:
+        mz.mz_first_token(e)
+    assert ei.value.status == mz.MZ_ESTATE
+    with pytest.raises(mz.MzError) as ei:
+        mz.mz_evict(e, np.zeros((m.n_layers, 3), np.uint8))
+    assert ei.value.status == mz.MZ_EINVAL
+    kv = np.zeros((m.n_layers, TINY.n_chunks), np.uint8)
+    kv[0, 0] = O.DROP
+    mz.mz_evict(e, kv)
+    kv[0, 0] = O.SWAP
+    with pytest.raises(mz.MzError) as ei:
+        mz.mz_evict(e, kv)                       # a dropped chunk cannot be swapped
+    assert ei.value.status == mz.MZ_ESTATE
+    with pytest.raises(mz.MzError) as ei:
+        mz.mz_read_kv(e, 0, 0, m.chunk_tokens, m.dkv)
+    assert ei.value.status == mz.MZ_ESTATE
+    with pytest.raises(mz.MzError) as ei:
+        mz.mz_restore_and_prefill(e, np.full(4, m.vocab, np.int32))
+    assert ei.value.status == mz.MZ_EINVAL
+    with pytest.raises(mz.MzError) as ei:
+        mz.mz_restore_and_prefill(e, np.zeros(200, np.int32))     # 128 + 200 > max_ctx 256
+    assert ei.value.status == mz.MZ_EINVAL
+    mz.mz_restore_and_prefill(e, np.zeros(0, np.int32))           # the failed calls changed nothing
+    mz.mz_first_token(e)
+
+
+SCALED = [
+    ("1b", dict(n_layers=2, n_ctx=512)),
+    ("3b", dict(n_layers=2, n_ctx=512, n_prompt=64)),
+    ("1p5b", dict(n_layers=2, n_ctx=768)),
+    ("8b", dict(n_layers=2, n_ctx=512, n_prompt=128)),
+]
+
+
+@pytest.mark.parametrize("key,kw", SCALED, ids=[k for k, _ in SCALED])
+def test_scaled_workload_import_flow(key, kw):
+    w = W.WORKLOADS[key].scaled(**kw)
+    plan = W.make_plan(w)
+    prm = np.random.default_rng(1).integers(0, w.model.vocab, w.n_prompt).astype(np.int32)
+    run_import_flow(w, plan.kv_state, plan.w_state, prm, w.key)

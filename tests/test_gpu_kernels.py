@@ -1,0 +1,187 @@
+"""Kernel-level parity on the GPU against the CPU oracle, through the C ABI's
+kernel entry points (device buffers allocated with torch).
+
+Tolerances follow from the kernels' arithmetic (u = 2^-11, the f16 unit
+roundoff):
+ * GEMM: weights d * (q - 8) rounded to f16 (<= u relative) on f16 activations
+   (exact inputs), fp32 accumulation: |y - y_ref| <= 2u * sum_k |x_k w_k|
+   (+ u |y| for the f16 SwiGLU output).
+ * Attention: scores in fp32 from f16 operands (exact products), P rounded to
+   f16 (<= u relative), output rounded to f16: |o - o_ref| <= 2u |o_ref| +
+   2u max|v|.
+ * RMSNorm: fp32 sum of squares, f16 output: 2u relative.
+"""
+
+import numpy as np
+import pytest
+
+import oracle as O
+from paper_2609_01338_amd import mz
+from paper_2609_01338_amd import workloads as W
+from gpu_util import F16_REL, report, stream, torch_cuda
+
+REL = 2 * F16_REL
+
+pytestmark = pytest.mark.gpu
+
+
+def _gemm_case(M, N, K, epi, seed, sample_rows=None):
+    torch = torch_cuda()
+    rng = np.random.default_rng(seed)
+    report("gemm", M=M, N=N, K=K, epi=epi, seed=seed)
+    if epi == 2:
+        g = W.encode_q4_0((rng.standard_normal((N, K)) * 0.02).astype(np.float32))
+        u = W.encode_q4_0((rng.standard_normal((N, K)) * 0.02).astype(np.float32))
+        packed = mz.mz_q4_gemm_pack(g, N, K, w_up=u)
+        n64 = (N + 63) // 64 * 64
+        n_pad = 2 * n64
+    else:
+        raw = W.encode_q4_0((rng.standard_normal((N, K)) * 0.02).astype(np.float32))
+        packed = mz.mz_q4_gemm_pack(raw, N, K)
+        n_pad = (N + 127) // 128 * 128
+    gen = torch.Generator(device="cuda").manual_seed(seed)
+    x = torch.randn(M, K, device="cuda", generator=gen).to(torch.float16)
+    w = torch.from_numpy(packed).cuda()
+    if epi == 2:
+        y = torch.zeros(M, n_pad // 2, device="cuda", dtype=torch.float16)
+    else:
+        y = torch.randn(M, n_pad, device="cuda", generator=gen) if epi == 1 else \
+            torch.zeros(M, n_pad, device="cuda")
+    y0 = y.float().cpu().numpy().astype(np.float64)
+    mz.mz_q4_gemm(x.data_ptr(), M, n_pad, K, w.data_ptr(), epi, y.data_ptr(), stream())
+    torch.cuda.synchronize()
+    rows = np.arange(M) if sample_rows is None else sample_rows
+    xs = x[torch.from_numpy(rows).cuda()].float().cpu().numpy().astype(np.float64)
+    ys = y.float().cpu().numpy()[rows].astype(np.float64)
+    if epi == 2:
+        G = O.q4_0_decode(g.reshape(-1), N, K)
+        U = O.q4_0_decode(u.reshape(-1), N, K)
+        gr, ur = xs @ G.T, xs @ U.T
+        bg = REL * (np.abs(xs) @ np.abs(G).T) + 1e-6
+        bu = REL * (np.abs(xs) @ np.abs(U).T) + 1e-6
+        ref = O.silu(gr) * ur
+        bound = 1.1 * bg * (np.abs(ur) + bu) + np.abs(O.silu(gr)) * bu + REL * np.abs(ref) + 1e-6
+        got = ys[:, :N]
+        assert np.all(ys[:, N:] == 0)          # padded gate/up columns give silu(0) * 0
+    else:
+        Wd = O.q4_0_decode(raw.reshape(-1), N, K)
+        ref = xs @ Wd.T + (y0[rows, :N] if epi == 1 else 0.0)
+        bound = REL * (np.abs(xs) @ np.abs(Wd).T) + 1e-5 * (1 + np.abs(ref))
+        got = ys[:, :N]
+    err = np.abs(got - ref)
+    report("  err", max=float(err.max()), worst_ratio=float((err / bound).max()))
+    assert np.all(err <= bound)
+
+
+@pytest.mark.parametrize("M,N,K,epi", [
+    (1, 128, 64, 0), (200, 256, 128, 0), (333, 512, 704, 0), (129, 384, 256, 1),
+    (77, 688, 256, 2), (300, 1408, 256, 2)])
+def test_gemm_small(M, N, K, epi):
+    _gemm_case(M, N, K, epi, seed=M + N + K)
+
+
+def _layer_gemms(key):
+    w = W.WORKLOADS[key]
+    m = w.model
+    M = w.n_ctx + w.n_prompt
+    ffp = (m.d_ffn + 63) // 64 * 64
+    return [(M, m.dq + 2 * m.dkv, m.d_model, 0), (M, m.d_model, m.dq, 1),
+            (M, m.d_ffn, m.d_model, 2), (M, m.d_model, ffp, 1)]
+
+
+@pytest.mark.parametrize("key", ["tiny", "1b", "3b", "1p5b", "8b"])
+def test_gemm_full_layer_shapes(key):
+    """Every projection of the workload at its full row count (the launch the
+    benchmark times), checked on sampled rows including the ragged tail."""
+    for i, (M, N, K, epi) in enumerate(_layer_gemms(key)):
+        rng = np.random.default_rng(i)
+        rows = np.unique(np.concatenate([rng.choice(M, min(M, 24), replace=False), [0, M - 1]]))
+        _gemm_case(M, N, K, epi, seed=100 + i, sample_rows=rows)
+
+
+def _attn_case(nq, nkv, hd, C, S, qpos, seed, sample=None):
+    torch = torch_cuda()
+    report("attention", nq=nq, nkv=nkv, hd=hd, C=C, S=S, m=len(qpos), seed=seed)
+    rng = np.random.default_rng(seed)
+    dkv = nkv * hd
+    nch = (S + C - 1) // C
+    n_slots = nch + 3
+    table = rng.permutation(n_slots)[:nch].astype(np.int32)
+    K = rng.standard_normal((S, dkv)).astype(np.float16)
+    V = rng.standard_normal((S, dkv)).astype(np.float16)
+    slab = np.full((n_slots, 2, C, dkv), np.nan, np.float16)     # unused rows are NaN
+    for c in range(nch):
+        n = min(C, S - c * C)
+        slab[table[c], 0, :n] = K[c * C:c * C + n]
+        slab[table[c], 1, :n] = V[c * C:c * C + n]
+    qpos = np.asarray(qpos, np.int32)
+    M = qpos.size
+    q = (rng.standard_normal((M, nq, hd)) * 1.0).astype(np.float16)
+    d_q = torch.from_numpy(q).cuda()
+    d_pos = torch.from_numpy(qpos).cuda()
+    d_slab = torch.from_numpy(slab).cuda()
+    d_tab = torch.from_numpy(table).cuda()
+    out = torch.empty(M, nq * hd, device="cuda", dtype=torch.float16)
+    mz.mz_attention(d_q.data_ptr(), d_pos.data_ptr(), M, d_slab.data_ptr(), d_tab.data_ptr(), nch, C,
+                    nq, nkv, hd, out.data_ptr(), stream())
+    torch.cuda.synchronize()
+    got = out.float().cpu().numpy().reshape(M, nq, hd).astype(np.float64)
+    rows = np.arange(M) if sample is None else sample
+    ref = O.causal_gqa_attention(q[rows].astype(np.float64), qpos[rows],
+                                 K.astype(np.float64).reshape(S, nkv, hd),
+                                 V.astype(np.float64).reshape(S, nkv, hd))
+    g = got[rows]
+    bound = REL * np.abs(ref) + 2.0 ** -10 * float(np.abs(V).max())
+    err = np.abs(g - ref)
+    report("  err", max=float(err.max()), worst_ratio=float((err / bound).max()))
+    assert np.all(np.isfinite(g))
+    assert np.all(err <= bound)
+
+
+@pytest.mark.parametrize("nq,nkv,hd,C,S", [
+    (4, 2, 64, 16, 128), (4, 2, 64, 16, 117), (32, 8, 64, 256, 600), (24, 8, 128, 256, 700),
+    (12, 2, 128, 256, 530), (32, 8, 128, 256, 400), (8, 8, 128, 64, 200), (6, 1, 64, 32, 90)])
+def test_attention_small(nq, nkv, hd, C, S):
+    rng = np.random.default_rng(S)
+    dense = np.arange(S)
+    gappy = np.sort(rng.choice(S, max(1, S // 3), replace=False))
+    _attn_case(nq, nkv, hd, C, S, dense, seed=1)
+    _attn_case(nq, nkv, hd, C, S, gappy, seed=2)
+    _attn_case(nq, nkv, hd, C, S, [0], seed=3)
+    _attn_case(nq, nkv, hd, C, S, [S - 1], seed=4)
+
+
+@pytest.mark.parametrize("key", ["1b", "3b", "1p5b", "8b"])
+def test_attention_full_context(key):
+    """All S query rows of the workload (the benchmark's launch), sampled check."""
+    w = W.WORKLOADS[key]
+    m = w.model
+    S = w.n_ctx + w.n_prompt
+    rng = np.random.default_rng(7)
+    sample = np.unique(np.concatenate([rng.choice(S, 12, replace=False), [0, S - 1]]))
+    _attn_case(m.n_q_heads, m.n_kv_heads, m.head_dim, m.chunk_tokens, S, np.arange(S), seed=5,
+               sample=sample)
+
+
+@pytest.mark.parametrize("M,d", [(1, 256), (300, 2048), (77, 4096), (5, 1536)])
+def test_rmsnorm(M, d):
+    torch = torch_cuda()
+    rng = np.random.default_rng(M * d)
+    h = (rng.standard_normal((M, d)) * 3).astype(np.float32)
+    h[0, :] *= 1e-3
+    x = torch.empty(M, d, device="cuda", dtype=torch.float16)
+    dh = torch.from_numpy(h).cuda()
+    mz.mz_rmsnorm(dh.data_ptr(), M, d, 1e-5, x.data_ptr(), stream())
+    torch.cuda.synchronize()
+    ref = O.rmsnorm(h.astype(np.float64), 1e-5)
+    got = x.float().cpu().numpy()
+    assert np.all(np.abs(got - ref) <= REL * np.abs(ref) + 1e-6)
+
+
+def test_kernel_entry_validation():
+    torch_cuda()
+    with pytest.raises(mz.MzError) as e:
+        mz.mz_q4_gemm(1, 10, 100, 64, 1, 0, 1)          # n_pad not a multiple of 128
+    assert e.value.status == mz.MZ_EINVAL
+    with pytest.raises(mz.MzError):
+        mz.mz_attention(1, 1, 4, 1, 1, 1, 16, 6, 4, 64, 1)   # 6 q heads over 4 kv heads
