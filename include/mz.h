@@ -43,7 +43,7 @@ typedef enum {
 /* State of one unit (a layer's weights, or one KV chunk of one layer). */
 typedef enum { MZ_RES = 0, MZ_SWAP = 1, MZ_DROP = 2 } mz_unit_state;
 
-/* Model shape.  d_model must be a multiple of 128; d_ffn need not be a
+/* Model shape.  d_model must be a multiple of 256; d_ffn need not be a
  * multiple of 32 (Q4_0 rows of W_down are zero-padded); head_dim must be 64 or
  * 128; n_q_heads a multiple of n_kv_heads with a group of at most 8;
  * max_ctx bounds context + prompt tokens. */
@@ -164,15 +164,18 @@ mz_status mz_plan_rows(const mz_model_cfg *cfg, const uint8_t *kv_state, int32_t
                        int32_t n_ctx, int32_t n_prompt, int32_t *nR, int32_t *nD,
                        int32_t *rows, int64_t rows_cap);
 
-/* Bytes of the device GEMM layout of a Q4_0 matrix [n][k] (n padded to 128,
+/* Bytes of the device GEMM layout of a Q4_0 matrix [n][k] (n padded to 256,
  * k to 64). */
 int64_t mz_q4_gemm_packed_bytes(int32_t n, int32_t k);
 
 /* Repack a Q4_0 matrix [n][k] (host, blob row format) into the device GEMM
- * layout (host out, mz_q4_gemm_packed_bytes(n, k) bytes).  If w_up is not
- * NULL, w and w_up are the gate and up matrices [n][k] and are interleaved
- * in groups of 16 rows (gate group i, then up group i) for the SwiGLU
- * epilogue; out then needs mz_q4_gemm_packed_bytes(2 * n_pad64, k) bytes. */
+ * layout (host out, mz_q4_gemm_packed_bytes(n, k) bytes): tiles of 256 rows x
+ * 64 columns holding 16-byte code blocks (codes re-ordered for the
+ * dequantizer) and then their fp16 scales.  If w_up is not NULL, w and w_up
+ * are the gate and up matrices [n][k], each padded to n128 = 128 * ceil(n/128)
+ * rows and interleaved in groups of 16 rows (gate group i, then up group i)
+ * for the SwiGLU epilogue; out then needs mz_q4_gemm_packed_bytes(2 * n128, k)
+ * bytes. */
 mz_status mz_q4_gemm_pack(const void *w, const void *w_up, int32_t n, int32_t k, void *out);
 
 /* ---- kernel-level calls (device pointers, enqueue on `stream`) --------- */
@@ -180,8 +183,9 @@ mz_status mz_q4_gemm_pack(const void *w, const void *w_up, int32_t n, int32_t k,
  * a hipStream_t (NULL = default stream).  They validate shapes and return
  * EINVAL without launching on a mismatch. */
 
-/* Y = X . W^T with X f16 [m][k] row-major and W packed by mz_q4_gemm_pack
- * (weights dequantized to f16, fp32 accumulation).
+/* Y = X . W^T with X f16 [m][k] row-major (k a multiple of 64) and W packed
+ * by mz_q4_gemm_pack (n_pad a multiple of 256; weights dequantized to f16,
+ * fp32 accumulation).
  * epilogue 0: y float [m][n_pad] = acc;  1: y float [m][n_pad] += acc;
  * 2: y f16 [m][n_pad/2] = silu(gate) * up (W packed with w_up). */
 mz_status mz_q4_gemm(const void *x_f16, int32_t m, int32_t n_pad, int32_t k,

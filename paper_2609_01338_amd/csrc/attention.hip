@@ -10,13 +10,21 @@
 // A workgroup serves one KV head and a tile of query rows for all of that
 // head's G query heads; each wave owns 32 queries of one query head.  Per
 // 64-key tile the keys (K rows) and the values, transposed (V^T: keys
-// contiguous per dimension), are staged in LDS once for the whole group.
-// Scores are computed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_f16 so
-// that each lane holds 32 scores of a single query: the row max needs one
-// cross-lane exchange (lane l and l ^ 32), and the exponentiated scores are
-// already laid out as the B operand of O^T += V^T P^T.  Softmax in fp32 with
-// exp2 and the log2(e)/sqrt(hd) scale folded in; P is rounded to f16 for the
+// contiguous per dimension), are staged in LDS once for the whole group,
+// double buffered: the next tile's global loads are in flight while the
+// current one is multiplied.  Scores are computed transposed, S^T = K Q^T,
+// with v_mfma_f32_32x32x16_f16 so that each lane holds 32 scores of a single
+// query: the row max needs one cross-lane exchange (lane l and l ^ 32), and
+// the exponentiated scores are already laid out as the B operand of
+// O^T += V^T P^T.  Softmax in fp32 with exp2 (the log2(e)/sqrt(hd) scale folded
+// into one FMA); the running max is only raised when a tile exceeds it by more
+// than 8 (log2 units), so rescaling the accumulators is rare and skipped
+// wave-wide when no lane needs it; P (at most 2^8) is rounded to f16 for the
 // MFMA; the row sums are kept per lane half and combined at the end.
+//
+// Workgroup numbering: query tiles are dealt to the 8 XCDs round-robin,
+// heaviest (latest positions) first, and the KV heads of one query tile run
+// back to back on the same XCD so they share the K/V rows in its L2.
 //
 // MFMA 32x32x16 layout (checked on gfx950): lane l feeds row/column l % 32 with
 // the 8 consecutive k of group l / 32; the accumulator element r of lane l is
@@ -33,29 +41,46 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int KT = 64;             // keys per tile
 constexpr int VT_STRIDE = KT + 4;  // halves per V^T row (136 B): conflict-free b64 reads
+constexpr float kMaxSlack = 8.0f;  // log2 headroom before the running max is raised
 
 template <int HD>
-__global__ __launch_bounds__(512) void attn_kernel(const _Float16* __restrict__ Q,
-                                                   const int32_t* __restrict__ qpos, int M,
-                                                   const uint8_t* __restrict__ slab,
-                                                   const int32_t* __restrict__ table, int C,
-                                                   int64_t slot_bytes, int nq, int nkv, int group,
-                                                   int qw, float scale_log2,
-                                                   _Float16* __restrict__ O) {
-  constexpr int K_STRIDE = HD + 8;  // halves per K row
-  __shared__ __attribute__((aligned(16))) _Float16 Ks[KT * K_STRIDE];
-  __shared__ __attribute__((aligned(16))) _Float16 Vt[HD * VT_STRIDE];
+constexpr int k_stride() { return HD + 8; }   // halves per K row in LDS
+
+template <int HD>
+constexpr size_t stage_halves() { return (size_t)KT * k_stride<HD>() + (size_t)HD * VT_STRIDE; }
+
+template <int HD, int NW>
+__global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restrict__ Q,
+                                                       const int32_t* __restrict__ qpos, int M,
+                                                       const uint8_t* __restrict__ slab,
+                                                       const int32_t* __restrict__ table, int C,
+                                                       int64_t slot_bytes, int nq, int nkv,
+                                                       int group, int qw, int n_qtiles,
+                                                       float scale_log2, _Float16* __restrict__ O) {
+  constexpr int NTH = 64 * NW;
+  constexpr int KS = k_stride<HD>();
+  constexpr int K_SEGS = KT * (HD / 8);             // 16-byte segments of a K tile
+  constexpr int V_SEGS = (KT / 2) * (HD / 8);       // key pairs x 8-dim groups of a V tile
+  constexpr int K_PER = (K_SEGS + NTH - 1) / NTH;
+  constexpr int V_PER = (V_SEGS + NTH - 1) / NTH;
+  extern __shared__ __attribute__((aligned(16))) _Float16 lds[];
 
   const int tid = threadIdx.x;
-  const int nthreads = blockDim.x;
   const int lane = tid & 63;
   const int w = tid >> 6;
   const int half = lane >> 5;       // lane group (0/1)
   const int col = lane & 31;        // query column of this lane
   const int dkv = nkv * HD;
-  const int kvh = blockIdx.y;
+
+  // block -> (query tile, kv head): XCD x = b % 8 takes tiles x, x+8, ... in
+  // heaviest-first order, all kv heads of a tile consecutively
+  const int b = blockIdx.x;
+  const int j = b / 8;
+  const int tile_rank = (j / nkv) * 8 + (b % 8);
+  if (tile_rank >= n_qtiles) return;
+  const int kvh = j % nkv;
+  const int tile = n_qtiles - 1 - tile_rank;
   const int bq = 32 * qw;
-  const int tile = gridDim.x - 1 - blockIdx.x;     // heaviest tiles first
   const int row0 = tile * bq;
   const int row_end = min(row0 + bq, M);
   const int kmax = qpos[row_end - 1];              // positions ascend
@@ -63,14 +88,15 @@ __global__ __launch_bounds__(512) void attn_kernel(const _Float16* __restrict__ 
   const int n_kt = kmax / KT + 1;
 
   const int h = kvh * group + (w % group);
+  const bool wave_active = w < group * qw;
   const int qi = row0 + (w / group) * 32 + col;
-  const bool qvalid = qi < M;
-  const int qc = qvalid ? qi : M - 1;
+  const bool qvalid = wave_active && qi < M;
+  const int qc = min(qi, M - 1);
   const int p = qpos[qc];
 
   f16x8 qf[HD / 16];
   {
-    const _Float16* qrow = Q + (size_t)qc * nq * HD + h * HD + half * 8;
+    const _Float16* qrow = Q + (size_t)qc * nq * HD + (wave_active ? h : 0) * HD + half * 8;
 #pragma unroll
     for (int ks = 0; ks < HD / 16; ++ks) qf[ks] = *reinterpret_cast<const f16x8*>(qrow + ks * 16);
   }
@@ -82,111 +108,144 @@ __global__ __launch_bounds__(512) void attn_kernel(const _Float16* __restrict__ 
     for (int r = 0; r < 16; ++r) o[t][r] = 0.f;
   float m_i = -INFINITY, l_i = 0.f;
 
-  const uint8_t* vbase_off = slab + (int64_t)C * dkv * 2;   // V follows K inside a slot
+  const uint8_t* kbase = slab + (int64_t)kvh * HD * 2;
+  const uint8_t* vbase = slab + (int64_t)C * dkv * 2 + (int64_t)kvh * HD * 2;   // V follows K
+  uint4 rk[K_PER], rv0[V_PER], rv1[V_PER];
 
-  for (int kt = 0; kt < n_kt; ++kt) {
-    __syncthreads();
-    // K rows of this tile: 64 keys x HD halves in 16-byte segments
-    for (int seg = tid; seg < KT * (HD / 8); seg += nthreads) {
+  auto gload = [&](int kt) {
+#pragma unroll
+    for (int i = 0; i < K_PER; ++i) {
+      const int seg = tid + i * NTH;
       const int key = seg / (HD / 8), c8 = seg % (HD / 8);
-      const int j = kt * KT + key;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (j <= kmax) {
-        const int64_t slot = table[j / C];
-        v = *reinterpret_cast<const uint4*>(slab + slot * slot_bytes +
-                                            ((int64_t)(j % C) * dkv + kvh * HD + c8 * 8) * 2);
-      }
-      *reinterpret_cast<uint4*>(&Ks[key * K_STRIDE + c8 * 8]) = v;
+      const int jj = kt * KT + key;
+      rk[i] = make_uint4(0, 0, 0, 0);
+      if (seg < K_SEGS && jj <= kmax)
+        rk[i] = *reinterpret_cast<const uint4*>(kbase + (int64_t)table[jj / C] * slot_bytes +
+                                                ((int64_t)(jj % C) * dkv + c8 * 8) * 2);
     }
-    // V rows, two keys at a time, written transposed as key pairs
-    for (int seg = tid; seg < (KT / 2) * (HD / 8); seg += nthreads) {
+#pragma unroll
+    for (int i = 0; i < V_PER; ++i) {
+      const int seg = tid + i * NTH;
       const int kp = seg % (KT / 2), dg = seg / (KT / 2);
       const int j0 = kt * KT + 2 * kp;
-      uint4 v0 = make_uint4(0, 0, 0, 0), v1 = make_uint4(0, 0, 0, 0);
-      if (j0 <= kmax) {
-        const int64_t slot = table[j0 / C];
-        v0 = *reinterpret_cast<const uint4*>(vbase_off + slot * slot_bytes +
-                                             ((int64_t)(j0 % C) * dkv + kvh * HD + dg * 8) * 2);
-      }
-      if (j0 + 1 <= kmax) {
-        const int64_t slot = table[(j0 + 1) / C];
-        v1 = *reinterpret_cast<const uint4*>(
-            vbase_off + slot * slot_bytes + ((int64_t)((j0 + 1) % C) * dkv + kvh * HD + dg * 8) * 2);
-      }
-      const uint32_t a[4] = {v0.x, v0.y, v0.z, v0.w};
-      const uint32_t b[4] = {v1.x, v1.y, v1.z, v1.w};
+      rv0[i] = make_uint4(0, 0, 0, 0);
+      rv1[i] = make_uint4(0, 0, 0, 0);
+      if (seg < V_SEGS && j0 <= kmax)
+        rv0[i] = *reinterpret_cast<const uint4*>(vbase + (int64_t)table[j0 / C] * slot_bytes +
+                                                 ((int64_t)(j0 % C) * dkv + dg * 8) * 2);
+      if (seg < V_SEGS && j0 + 1 <= kmax)
+        rv1[i] = *reinterpret_cast<const uint4*>(vbase + (int64_t)table[(j0 + 1) / C] * slot_bytes +
+                                                 ((int64_t)((j0 + 1) % C) * dkv + dg * 8) * 2);
+    }
+  };
+  auto lstore = [&](int st) {
+    _Float16* Ks = lds + st * stage_halves<HD>();
+    _Float16* Vt = Ks + KT * KS;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        // dims dg*8 + 2i (low halves) and dg*8 + 2i + 1 (high halves)
-        const uint32_t lo = (a[i] & 0xFFFFu) | (b[i] << 16);
-        const uint32_t hi = (a[i] >> 16) | (b[i] & 0xFFFF0000u);
-        *reinterpret_cast<uint32_t*>(&Vt[(dg * 8 + 2 * i) * VT_STRIDE + 2 * kp]) = lo;
-        *reinterpret_cast<uint32_t*>(&Vt[(dg * 8 + 2 * i + 1) * VT_STRIDE + 2 * kp]) = hi;
+    for (int i = 0; i < K_PER; ++i) {
+      const int seg = tid + i * NTH;
+      if (seg < K_SEGS)
+        *reinterpret_cast<uint4*>(&Ks[(seg / (HD / 8)) * KS + (seg % (HD / 8)) * 8]) = rk[i];
+    }
+#pragma unroll
+    for (int i = 0; i < V_PER; ++i) {
+      const int seg = tid + i * NTH;
+      if (seg >= V_SEGS) continue;
+      const int kp = seg % (KT / 2), dg = seg / (KT / 2);
+      const uint32_t a[4] = {rv0[i].x, rv0[i].y, rv0[i].z, rv0[i].w};
+      const uint32_t bb[4] = {rv1[i].x, rv1[i].y, rv1[i].z, rv1[i].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        // dims dg*8 + 2e (low halves) and dg*8 + 2e + 1 (high halves), keys 2kp, 2kp+1
+        *reinterpret_cast<uint32_t*>(&Vt[(dg * 8 + 2 * e) * VT_STRIDE + 2 * kp]) =
+            (a[e] & 0xFFFFu) | (bb[e] << 16);
+        *reinterpret_cast<uint32_t*>(&Vt[(dg * 8 + 2 * e + 1) * VT_STRIDE + 2 * kp]) =
+            (a[e] >> 16) | (bb[e] & 0xFFFF0000u);
       }
     }
+  };
+
+  gload(0);
+  lstore(0);
+  __syncthreads();
+
+  for (int kt = 0; kt < n_kt; ++kt) {
+    const int st = kt & 1;
+    if (kt + 1 < n_kt) gload(kt + 1);
+    if (wave_active) {
+      const _Float16* Ks = lds + st * stage_halves<HD>();
+      const _Float16* Vt = Ks + KT * KS;
+      // S^T = K Q^T: keys on rows, this wave's 32 queries on columns
+      f32x16 s[2];
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[kk][r] = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < HD / 16; ++ks) {
+          const f16x8 a =
+              *reinterpret_cast<const f16x8*>(&Ks[(kk * 32 + col) * KS + ks * 16 + half * 8]);
+          s[kk] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, qf[ks], s[kk], 0, 0, 0);
+        }
+      }
+      // causal mask (only tiles that reach past the smallest query position)
+      if (kt * KT + KT - 1 > kmin) {
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = kt * KT + kk * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+            if (key > p) s[kk][r] = -INFINITY;
+          }
+      }
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kk][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32)) * scale_log2;
+      // raise the running max only when this tile exceeds it by more than the slack
+      const bool raise = mx > m_i + kMaxSlack;
+      const float m_new = raise ? mx : m_i;   // finite after tile 0: key 0 is visible to all
+      if (__any(raise)) {
+        const float alpha = exp2f(m_i - m_new);
+        l_i *= alpha;
+#pragma unroll
+        for (int t = 0; t < HD / 32; ++t)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
+      }
+      m_i = m_new;
+      float psum = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float e = exp2f(__builtin_fmaf(s[kk][r], scale_log2, -m_new));
+          s[kk][r] = e;
+          psum += e;
+        }
+      l_i += psum;
+
+      // O^T += V^T P^T over 4 steps of 16 keys.  Slot sl of lane group `half`
+      // carries key 16*ks + 8*(sl/4) + 4*half + sl%4 in both operands.
+#pragma unroll
+      for (int ks = 0; ks < KT / 16; ++ks) {
+        f16x8 pb;
+#pragma unroll
+        for (int sl = 0; sl < 8; ++sl) pb[sl] = (_Float16)s[ks >> 1][(ks & 1) * 8 + sl];
+#pragma unroll
+        for (int t = 0; t < HD / 32; ++t) {
+          const _Float16* vrow = &Vt[(t * 32 + col) * VT_STRIDE + 16 * ks + 4 * half];
+          const f16x4 lo = *reinterpret_cast<const f16x4*>(vrow);
+          const f16x4 hi = *reinterpret_cast<const f16x4*>(vrow + 8);
+          const f16x8 a = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          o[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, pb, o[t], 0, 0, 0);
+        }
+      }
+    }
+    if (kt + 1 < n_kt) lstore(st ^ 1);
     __syncthreads();
-
-    // S^T = K Q^T: keys on rows, this wave's 32 queries on columns
-    f32x16 s[2];
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s[kk][r] = 0.f;
-#pragma unroll
-      for (int ks = 0; ks < HD / 16; ++ks) {
-        const f16x8 a =
-            *reinterpret_cast<const f16x8*>(&Ks[(kk * 32 + col) * K_STRIDE + ks * 16 + half * 8]);
-        s[kk] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, qf[ks], s[kk], 0, 0, 0);
-      }
-    }
-    // scale, causal mask, tile max
-    const bool need_mask = kt * KT + KT - 1 > kmin;
-    float mx = -INFINITY;
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float v = s[kk][r] * scale_log2;
-        const int key = kt * KT + kk * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-        if (need_mask && key > p) v = -INFINITY;
-        s[kk][r] = v;
-        mx = fmaxf(mx, v);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_i, mx);       // finite: key 0 is visible to every query
-    const float alpha = exp2f(m_i - m_new);
-    float psum = 0.f;
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float e = exp2f(s[kk][r] - m_new);
-        s[kk][r] = e;
-        psum += e;
-      }
-    l_i = l_i * alpha + psum;
-    m_i = m_new;
-#pragma unroll
-    for (int t = 0; t < HD / 32; ++t)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
-
-    // O^T += V^T P^T over 4 steps of 16 keys.  Slot sl of lane group `half`
-    // carries key 16*ks + 8*(sl/4) + 4*half + sl%4 in both operands.
-#pragma unroll
-    for (int ks = 0; ks < KT / 16; ++ks) {
-      f16x8 pb;
-#pragma unroll
-      for (int sl = 0; sl < 8; ++sl) pb[sl] = (_Float16)s[ks >> 1][(ks & 1) * 8 + sl];
-#pragma unroll
-      for (int t = 0; t < HD / 32; ++t) {
-        const _Float16* vrow = &Vt[(t * 32 + col) * VT_STRIDE + 16 * ks + 4 * half];
-        const f16x4 lo = *reinterpret_cast<const f16x4*>(vrow);
-        const f16x4 hi = *reinterpret_cast<const f16x4*>(vrow + 8);
-        const f16x8 a = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-        o[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, pb, o[t], 0, 0, 0);
-      }
-    }
   }
 
   const float l = l_i + __shfl_xor(l_i, 32);
@@ -205,26 +264,51 @@ __global__ __launch_bounds__(512) void attn_kernel(const _Float16* __restrict__ 
   }
 }
 
+template <int HD, int NW>
+void launch_nw(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S, const int32_t* table,
+               int C, int64_t slot_bytes, int nq, int nkv, int group, int qw, float scale_log2,
+               _Float16* O, hipStream_t s) {
+  const size_t lds_bytes = 2 * stage_halves<HD>() * sizeof(_Float16);
+  static const bool attr = [&] {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<HD, NW>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
+    return true;
+  }();
+  (void)attr;
+  const int bq = 32 * qw;
+  const int n_qtiles = (m + bq - 1) / bq;
+  const int blocks = 8 * ((n_qtiles + 7) / 8) * nkv;
+  hipLaunchKernelGGL((attn_kernel<HD, NW>), dim3(blocks), dim3(64 * NW), lds_bytes, s, Q, qpos, m, S,
+                     table, C, slot_bytes, nq, nkv, group, qw, n_qtiles, scale_log2, O);
+}
+
+template <int HD>
+void launch_hd(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S, const int32_t* table,
+               int C, int64_t slot_bytes, int nq, int nkv, int group, int qw, float scale_log2,
+               _Float16* O, hipStream_t s) {
+  switch (group * qw) {
+    case 5: launch_nw<HD, 5>(Q, qpos, m, S, table, C, slot_bytes, nq, nkv, group, qw, scale_log2, O, s); break;
+    case 6: launch_nw<HD, 6>(Q, qpos, m, S, table, C, slot_bytes, nq, nkv, group, qw, scale_log2, O, s); break;
+    case 7: launch_nw<HD, 7>(Q, qpos, m, S, table, C, slot_bytes, nq, nkv, group, qw, scale_log2, O, s); break;
+    default: launch_nw<HD, 8>(Q, qpos, m, S, table, C, slot_bytes, nq, nkv, group, qw, scale_log2, O, s); break;
+  }
+}
+
 }  // namespace
 
 void launch_attention(const void* q, const int32_t* qpos, int m, const void* slab,
                       const int32_t* table, int chunk_tokens, int64_t slot_bytes, int n_q,
                       int n_kv, int head_dim, void* out, hipStream_t s) {
-  const int group = n_q / n_kv;
-  const int qw = group >= 8 ? 1 : 8 / group;        // 32-query row groups per workgroup
-  const int waves = group * qw;
-  const int bq = 32 * qw;
-  dim3 grid((m + bq - 1) / bq, n_kv);
+  const int group = n_q / n_kv;          // 1..8
+  const int qw = 8 / group;              // 32-query row groups per workgroup: 5..8 waves
   const float scale_log2 = 1.4426950408889634f / __builtin_sqrtf((float)head_dim);
   const _Float16* Q = reinterpret_cast<const _Float16*>(q);
   const uint8_t* S = reinterpret_cast<const uint8_t*>(slab);
   _Float16* O = reinterpret_cast<_Float16*>(out);
   if (head_dim == 128)
-    hipLaunchKernelGGL(attn_kernel<128>, grid, dim3(64 * waves), 0, s, Q, qpos, m, S, table,
-                       chunk_tokens, slot_bytes, n_q, n_kv, group, qw, scale_log2, O);
+    launch_hd<128>(Q, qpos, m, S, table, chunk_tokens, slot_bytes, n_q, n_kv, group, qw, scale_log2, O, s);
   else
-    hipLaunchKernelGGL(attn_kernel<64>, grid, dim3(64 * waves), 0, s, Q, qpos, m, S, table,
-                       chunk_tokens, slot_bytes, n_q, n_kv, group, qw, scale_log2, O);
+    launch_hd<64>(Q, qpos, m, S, table, chunk_tokens, slot_bytes, n_q, n_kv, group, qw, scale_log2, O, s);
 }
 
 }  // namespace mzk

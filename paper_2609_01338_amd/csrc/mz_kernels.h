@@ -7,10 +7,12 @@
 
 namespace mzk {
 
-// Device GEMM layout of a Q4_0 matrix [n][k]: tiles of 128 rows x 64 columns,
-// ordered n-tile major, k-tile minor.  A tile holds 128*2 blocks of 16 nibble
-// bytes (row-major over (row, block)), then their 128*2 fp16 scales.
-constexpr int kGemmTileN = 128;
+// Device GEMM layout of a Q4_0 matrix [n][k]: tiles of 256 rows x 64 columns,
+// ordered n-tile major, k-tile minor.  A tile holds 256*2 blocks of 16 nibble
+// bytes (row-major over (row, block)), then their 256*2 fp16 scales.  Within
+// a block the 32 codes are re-ordered: dword i carries elements 8i..8i+7 with
+// element 8i+2m at bits 4m..4m+3 and element 8i+2m+1 at bits 16+4m..19+4m.
+constexpr int kGemmTileN = 256;
 constexpr int kGemmTileK = 64;
 constexpr int kGemmTileBytes = kGemmTileN * kGemmTileK / 2 + kGemmTileN * (kGemmTileK / 32) * 2;
 

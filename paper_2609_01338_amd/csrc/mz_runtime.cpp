@@ -77,6 +77,26 @@ int64_t gemm_packed_bytes(int64_t n, int64_t k) {
          mzk::kGemmTileBytes;
 }
 
+// Codes of one block (element j in the low nibble of byte j, element j+16 in
+// its high nibble) re-ordered for the GEMM's dequantizer: dword i carries
+// elements 8i..8i+7, element 8i+2m at bits 4m and element 8i+2m+1 at bits
+// 16+4m (little-endian dwords).
+void reorder_codes(const uint8_t* qs, uint8_t* out) {
+  uint8_t q[32];
+  for (int j = 0; j < 16; ++j) {
+    q[j] = qs[j] & 15;
+    q[j + 16] = qs[j] >> 4;
+  }
+  for (int i = 0; i < 4; ++i) {
+    uint32_t w = 0;
+    for (int m = 0; m < 4; ++m) {
+      w |= (uint32_t)q[8 * i + 2 * m] << (4 * m);
+      w |= (uint32_t)q[8 * i + 2 * m + 1] << (16 + 4 * m);
+    }
+    memcpy(out + 4 * i, &w, 4);
+  }
+}
+
 // Source row r (or nullptr for a zero row) of a canonical Q4_0 matrix.
 template <typename RowFn>
 void pack_gemm_tiles(RowFn row_ptr, int64_t n, int64_t k, uint8_t* out) {
@@ -95,7 +115,7 @@ void pack_gemm_tiles(RowFn row_ptr, int64_t n, int64_t k, uint8_t* out) {
           const uint8_t* src = row < n ? row_ptr(row) : nullptr;
           if (src && blk < nb_src) {
             memcpy(sc, src + blk * kBlockBytes, 2);
-            memcpy(nib, src + blk * kBlockBytes + 2, 16);
+            reorder_codes(src + blk * kBlockBytes + 2, nib);
           } else {
             memset(sc, 0, 2);          // scale 0: the padded block decodes to 0
             memset(nib, 0x88, 16);
@@ -111,10 +131,10 @@ void pack_plain(const uint8_t* w, int64_t n, int64_t k, uint8_t* out) {
 
 // Gate/up interleave: packed row 32 g + i is gate row 16 g + i (i < 16) or up
 // row 16 g + i - 16, so a 32-column group of the product holds matching
-// gate and up columns.
+// gate and up columns.  Each matrix is padded to a multiple of 128 rows.
 void pack_gateup(const uint8_t* g, const uint8_t* u, int64_t n, int64_t k, uint8_t* out) {
   const int64_t rb = q4_row_bytes(k);
-  const int64_t n_pad = round_up(n, 64);
+  const int64_t n_pad = round_up(n, mzk::kGemmTileN / 2);
   pack_gemm_tiles(
       [&](int64_t pr) -> const uint8_t* {
         const int64_t grp = pr / 32, i = pr % 32;
@@ -469,7 +489,7 @@ void* dmalloc(size_t bytes) {
 
 void validate_cfg(const mz_model_cfg* c) {
   if (!c) fail(MZ_EINVAL, "cfg is NULL");
-  if (c->n_layers < 1 || c->d_model < 64 || c->d_model % 64) fail(MZ_EINVAL, "d_model must be a positive multiple of 64 and n_layers >= 1");
+  if (c->n_layers < 1 || c->d_model < 256 || c->d_model % 256) fail(MZ_EINVAL, "d_model must be a positive multiple of 256 and n_layers >= 1");
   if (c->head_dim != 64 && c->head_dim != 128) fail(MZ_EINVAL, "head_dim must be 64 or 128");
   if (c->n_kv_heads < 1 || c->n_q_heads < 1 || c->n_q_heads % c->n_kv_heads)
     fail(MZ_EINVAL, "n_q_heads must be a positive multiple of n_kv_heads");
@@ -821,8 +841,8 @@ mz_status mz_load_model(const mz_model_cfg* cfg, const void* blob, size_t nbytes
     c.dq = c.nq * c.hd; c.dkv = c.nkv * c.hd; c.nqkv = c.dq + 2 * c.dkv;
     c.nqkv_pad = (int)round_up(c.nqkv, mzk::kGemmTileN);
     c.d_pad = (int)round_up(c.d, mzk::kGemmTileN);
-    if (c.d_pad != c.d) fail(MZ_EINVAL, "d_model must be a multiple of 128");
-    c.ffp = (int)round_up(c.ff, 64);
+    if (c.d_pad != c.d) fail(MZ_EINVAL, "d_model must be a multiple of %d", mzk::kGemmTileN);
+    c.ffp = (int)round_up(c.ff, mzk::kGemmTileN / 2);
     c.max_chunks = c.nchunks_of(c.max_ctx);
     c.slot_bytes = (int64_t)c.C * c.dkv * 2 * 2;
 

@@ -215,8 +215,8 @@ def mz_q4_gemm_pack(w: np.ndarray, n: int, k: int, w_up: Optional[np.ndarray] = 
         out = np.empty(mz_q4_gemm_packed_bytes(n, k), np.uint8)
     else:
         w_up = np.ascontiguousarray(w_up, dtype=np.uint8)
-        n64 = (n + 63) // 64 * 64
-        out = np.empty(mz_q4_gemm_packed_bytes(2 * n64, k), np.uint8)
+        n128 = (n + 127) // 128 * 128
+        out = np.empty(mz_q4_gemm_packed_bytes(2 * n128, k), np.uint8)
     _check(lib().mz_q4_gemm_pack(w.ctypes.data, _ptr(w_up), n, k, out.ctypes.data), None)
     return out
 

@@ -97,27 +97,44 @@ def test_plan_rows_ok_case():
     assert nD.tolist() == [2, 18]
 
 
+def _codes_from_packed(nib16: np.ndarray) -> list:
+    """The 32 codes of one packed block: dword i holds elements 8i..8i+7, element
+    8i+2m at bits 4m and element 8i+2m+1 at bits 16+4m."""
+    words = np.frombuffer(bytes(nib16), "<u4")
+    out = [0] * 32
+    for i in range(4):
+        for m in range(4):
+            out[8 * i + 2 * m] = int(words[i] >> (4 * m)) & 15
+            out[8 * i + 2 * m + 1] = int(words[i] >> (16 + 4 * m)) & 15
+    return out
+
+
+def _codes_from_blob(block18: np.ndarray) -> list:
+    qs = bytes(block18[2:])
+    return [qs[j] & 15 for j in range(16)] + [qs[j] >> 4 for j in range(16)]
+
+
 def test_gemm_pack_layout():
-    """Tile (nt, kt) holds rows nt*128.., blocks kt*2..: nibbles (row, block) x 16 B,
+    """Tile (nt, kt) holds rows nt*256.., blocks kt*2..: code blocks (row, block) x 16 B,
     then the fp16 scales; padding rows/blocks carry scale 0."""
     rng = np.random.default_rng(2)
-    n, k = 200, 96                       # n pads to 256, k to 128
+    n, k = 300, 96                       # n pads to 512, k to 128
     x = rng.standard_normal((n, k)).astype(np.float32)
     raw = W.encode_q4_0(x)               # [n, 3 blocks * 18]
     packed = mz.mz_q4_gemm_pack(raw, n, k)
-    tiles = packed.reshape(2, 2, 4608)   # [n tiles][k tiles][bytes]
+    tiles = packed.reshape(2, 2, 9216)   # [n tiles][k tiles][bytes]
     blocks = raw.reshape(n, 3, 18)
     for nt in range(2):
         for kt in range(2):
             t = tiles[nt, kt]
-            nib = t[:4096].reshape(128, 2, 16)
-            sc = t[4096:].reshape(128, 2, 2)
-            for r in (0, 5, 71, 127):
-                row = nt * 128 + r
+            nib = t[:8192].reshape(256, 2, 16)
+            sc = t[8192:].reshape(256, 2, 2)
+            for r in (0, 5, 43, 44, 71, 255):
+                row = nt * 256 + r
                 for b in range(2):
                     blk = kt * 2 + b
                     if row < n and blk < 3:
-                        assert bytes(nib[r, b]) == bytes(blocks[row, blk, 2:])
+                        assert _codes_from_packed(nib[r, b]) == _codes_from_blob(blocks[row, blk])
                         assert bytes(sc[r, b]) == bytes(blocks[row, blk, :2])
                     else:
                         assert bytes(sc[r, b]) == b"\0\0"
@@ -125,19 +142,19 @@ def test_gemm_pack_layout():
 
 def test_gemm_pack_gateup_interleave():
     rng = np.random.default_rng(3)
-    n, k = 40, 64                        # n pads to 64 per matrix -> 128 packed rows
+    n, k = 40, 64                        # n pads to 128 per matrix -> 256 packed rows
     g = W.encode_q4_0(rng.standard_normal((n, k)).astype(np.float32))
     u = W.encode_q4_0(rng.standard_normal((n, k)).astype(np.float32))
     packed = mz.mz_q4_gemm_pack(g, n, k, w_up=u)
-    assert packed.size == mz.mz_q4_gemm_packed_bytes(128, 64)
-    nib = packed[:4096].reshape(128, 2, 16)
+    assert packed.size == mz.mz_q4_gemm_packed_bytes(256, 64)
+    nib = packed[:8192].reshape(256, 2, 16)
     gb, ub = g.reshape(n, 2, 18), u.reshape(n, 2, 18)
-    for pr in range(128):
+    for pr in range(256):
         grp, i = divmod(pr, 32)
         src = grp * 16 + (i if i < 16 else i - 16)
         if src < n:
             ref = (gb if i < 16 else ub)[src]
-            assert bytes(nib[pr, 0]) == bytes(ref[0, 2:])
+            assert _codes_from_packed(nib[pr, 1]) == _codes_from_blob(ref[1])
 
 
 def test_load_model_without_gpu_fails_cleanly():

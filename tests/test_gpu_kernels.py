@@ -33,12 +33,11 @@ def _gemm_case(M, N, K, epi, seed, sample_rows=None):
         g = W.encode_q4_0((rng.standard_normal((N, K)) * 0.02).astype(np.float32))
         u = W.encode_q4_0((rng.standard_normal((N, K)) * 0.02).astype(np.float32))
         packed = mz.mz_q4_gemm_pack(g, N, K, w_up=u)
-        n64 = (N + 63) // 64 * 64
-        n_pad = 2 * n64
+        n_pad = 2 * ((N + 127) // 128 * 128)
     else:
         raw = W.encode_q4_0((rng.standard_normal((N, K)) * 0.02).astype(np.float32))
         packed = mz.mz_q4_gemm_pack(raw, N, K)
-        n_pad = (N + 127) // 128 * 128
+        n_pad = (N + 255) // 256 * 256
     gen = torch.Generator(device="cuda").manual_seed(seed)
     x = torch.randn(M, K, device="cuda", generator=gen).to(torch.float16)
     w = torch.from_numpy(packed).cuda()
@@ -84,7 +83,7 @@ def _layer_gemms(key):
     w = W.WORKLOADS[key]
     m = w.model
     M = w.n_ctx + w.n_prompt
-    ffp = (m.d_ffn + 63) // 64 * 64
+    ffp = (m.d_ffn + 127) // 128 * 128
     return [(M, m.dq + 2 * m.dkv, m.d_model, 0), (M, m.d_model, m.dq, 1),
             (M, m.d_ffn, m.d_model, 2), (M, m.d_model, ffp, 1)]
 
@@ -181,7 +180,7 @@ def test_rmsnorm(M, d):
 def test_kernel_entry_validation():
     torch_cuda()
     with pytest.raises(mz.MzError) as e:
-        mz.mz_q4_gemm(1, 10, 100, 64, 1, 0, 1)          # n_pad not a multiple of 128
+        mz.mz_q4_gemm(1, 10, 128, 64, 1, 0, 1)          # n_pad not a multiple of 256
     assert e.value.status == mz.MZ_EINVAL
     with pytest.raises(mz.MzError):
         mz.mz_attention(1, 1, 4, 1, 1, 1, 16, 6, 4, 64, 1)   # 6 q heads over 4 kv heads
