@@ -16,15 +16,17 @@
 // with v_mfma_f32_32x32x16_f16 so that each lane holds 32 scores of a single
 // query: the row max needs one cross-lane exchange (lane l and l ^ 32), and
 // the exponentiated scores are already laid out as the B operand of
-// O^T += V^T P^T.  Softmax in fp32 with exp2 (the log2(e)/sqrt(hd) scale folded
-// into one FMA); the running max is only raised when a tile exceeds it by more
-// than 8 (log2 units), so rescaling the accumulators is rare and skipped
-// wave-wide when no lane needs it; P (at most 2^8) is rounded to f16 for the
-// MFMA; the row sums are kept per lane half and combined at the end.
+// O^T += V^T P^T.  Softmax in fp32 with the hardware exp2 (the
+// log2(e)/sqrt(hd) scale folded into one FMA); the running max is only raised
+// when a tile exceeds it by more than 8 (log2 units), so rescaling the
+// accumulators is rare and skipped wave-wide when no lane needs it; P (at most
+// 2^8) is rounded to f16 for the MFMA, and the row sums add those same f16
+// values (v_dot2 with ones, fp32 accumulation), kept per lane half and
+// combined at the end.  Chunk sizes are powers of two (shift addressing).
 //
-// Workgroup numbering: query tiles are dealt to the 8 XCDs round-robin,
-// heaviest (latest positions) first, and the KV heads of one query tile run
-// back to back on the same XCD so they share the K/V rows in its L2.
+// Workgroup numbering: each XCD serves one KV head (when the head count
+// divides 8) and walks its query tiles heaviest (latest positions) first, so
+// the 32 CUs of an XCD stream the same keys through its L2.
 //
 // MFMA 32x32x16 layout (checked on gfx950): lane l feeds row/column l % 32 with
 // the 8 consecutive k of group l / 32; the accumulator element r of lane l is
@@ -37,6 +39,7 @@ namespace {
 
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int KT = 64;             // keys per tile
@@ -48,13 +51,14 @@ constexpr int k_stride() { return HD + 8; }   // halves per K row in LDS
 
 template <int HD>
 constexpr size_t stage_halves() { return (size_t)KT * k_stride<HD>() + (size_t)HD * VT_STRIDE; }
+// two K buffers and two V buffers
 
 template <int HD, int NW>
 __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restrict__ Q,
                                                        const int32_t* __restrict__ qpos, int M,
                                                        const uint8_t* __restrict__ slab,
                                                        const int32_t* __restrict__ table, int C,
-                                                       int64_t slot_bytes, int nq, int nkv,
+                                                       int cshift, int64_t slot_bytes, int nq, int nkv,
                                                        int group, int qw, int n_qtiles,
                                                        float scale_log2, _Float16* __restrict__ O) {
   constexpr int NTH = 64 * NW;
@@ -72,13 +76,22 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
   const int col = lane & 31;        // query column of this lane
   const int dkv = nkv * HD;
 
-  // block -> (query tile, kv head): XCD x = b % 8 takes tiles x, x+8, ... in
-  // heaviest-first order, all kv heads of a tile consecutively
+  // block -> (query tile, kv head).  Workgroups are dealt to the 8 XCDs
+  // round-robin (x = b % 8).  When nkv divides 8, XCD x serves kv head x % nkv
+  // only, taking every (8/nkv)-th query tile heaviest first, so the CUs of an
+  // XCD stream the same keys and share them in its L2; otherwise XCD x takes
+  // tiles x, x+8, ... with all kv heads of a tile in a row.
   const int b = blockIdx.x;
-  const int j = b / 8;
-  const int tile_rank = (j / nkv) * 8 + (b % 8);
+  const int xcd = b % 8, j = b / 8;
+  int kvh, tile_rank;
+  if (8 % nkv == 0) {
+    kvh = xcd % nkv;
+    tile_rank = j * (8 / nkv) + xcd / nkv;
+  } else {
+    kvh = j % nkv;
+    tile_rank = (j / nkv) * 8 + xcd;
+  }
   if (tile_rank >= n_qtiles) return;
-  const int kvh = j % nkv;
   const int tile = n_qtiles - 1 - tile_rank;
   const int bq = 32 * qw;
   const int row0 = tile * bq;
@@ -110,43 +123,51 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
 
   const uint8_t* kbase = slab + (int64_t)kvh * HD * 2;
   const uint8_t* vbase = slab + (int64_t)C * dkv * 2 + (int64_t)kvh * HD * 2;   // V follows K
+  const int cmask = C - 1;                    // C is a power of two
+  const int row_bytes = dkv * 2;
   uint4 rk[K_PER], rv0[V_PER], rv1[V_PER];
 
-  auto gload = [&](int kt) {
+  // global -> registers for K tile kt / V tile kt
+  auto gload_k = [&](int kt) {
 #pragma unroll
     for (int i = 0; i < K_PER; ++i) {
       const int seg = tid + i * NTH;
-      const int key = seg / (HD / 8), c8 = seg % (HD / 8);
-      const int jj = kt * KT + key;
+      const int jj = kt * KT + seg / (HD / 8);
       rk[i] = make_uint4(0, 0, 0, 0);
       if (seg < K_SEGS && jj <= kmax)
-        rk[i] = *reinterpret_cast<const uint4*>(kbase + (int64_t)table[jj / C] * slot_bytes +
-                                                ((int64_t)(jj % C) * dkv + c8 * 8) * 2);
+        rk[i] = *reinterpret_cast<const uint4*>(kbase + (uint64_t)(uint32_t)table[jj >> cshift] * slot_bytes +
+                                                (uint32_t)((jj & cmask) * row_bytes + (seg % (HD / 8)) * 16));
     }
+  };
+  auto gload_v = [&](int kt) {
 #pragma unroll
     for (int i = 0; i < V_PER; ++i) {
       const int seg = tid + i * NTH;
-      const int kp = seg % (KT / 2), dg = seg / (KT / 2);
-      const int j0 = kt * KT + 2 * kp;
+      const int j0 = kt * KT + 2 * (seg % (KT / 2));
+      const uint32_t col = (seg / (KT / 2)) * 16;
       rv0[i] = make_uint4(0, 0, 0, 0);
       rv1[i] = make_uint4(0, 0, 0, 0);
-      if (seg < V_SEGS && j0 <= kmax)
-        rv0[i] = *reinterpret_cast<const uint4*>(vbase + (int64_t)table[j0 / C] * slot_bytes +
-                                                 ((int64_t)(j0 % C) * dkv + dg * 8) * 2);
-      if (seg < V_SEGS && j0 + 1 <= kmax)
-        rv1[i] = *reinterpret_cast<const uint4*>(vbase + (int64_t)table[(j0 + 1) / C] * slot_bytes +
-                                                 ((int64_t)((j0 + 1) % C) * dkv + dg * 8) * 2);
+      if (seg < V_SEGS && j0 <= kmax) {
+        // j0 is even and C >= 2, so keys j0 and j0 + 1 share a chunk
+        const uint8_t* src = vbase + (uint64_t)(uint32_t)table[j0 >> cshift] * slot_bytes +
+                             (uint32_t)((j0 & cmask) * row_bytes) + col;
+        rv0[i] = *reinterpret_cast<const uint4*>(src);
+        if (j0 + 1 <= kmax) rv1[i] = *reinterpret_cast<const uint4*>(src + row_bytes);
+      }
     }
   };
-  auto lstore = [&](int st) {
-    _Float16* Ks = lds + st * stage_halves<HD>();
-    _Float16* Vt = Ks + KT * KS;
+  // registers -> LDS buffers (K: [key][dim], V transposed: [dim][key])
+  auto Kbuf = [&](int i) { return lds + (i & 1) * (KT * KS); };
+  auto Vbuf = [&](int i) { return lds + 2 * KT * KS + (i & 1) * (HD * VT_STRIDE); };
+  auto lstore_k = [&](_Float16* Ks) {
 #pragma unroll
     for (int i = 0; i < K_PER; ++i) {
       const int seg = tid + i * NTH;
       if (seg < K_SEGS)
         *reinterpret_cast<uint4*>(&Ks[(seg / (HD / 8)) * KS + (seg % (HD / 8)) * 8]) = rk[i];
     }
+  };
+  auto lstore_v = [&](_Float16* Vt) {
 #pragma unroll
     for (int i = 0; i < V_PER; ++i) {
       const int seg = tid + i * NTH;
@@ -164,30 +185,46 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
       }
     }
   };
+  // S^T = K Q^T: keys on rows, this wave's 32 queries on columns
+  auto qk = [&](const _Float16* Ks, f32x16* sc) {
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sc[kk][r] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < HD / 16; ++ks) {
+        const f16x8 a = *reinterpret_cast<const f16x8*>(&Ks[(kk * 32 + col) * KS + ks * 16 + half * 8]);
+        sc[kk] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, qf[ks], sc[kk], 0, 0, 0);
+      }
+    }
+  };
 
-  gload(0);
-  lstore(0);
+  // Pipeline: K runs one tile ahead of V.  In iteration kt the LDS holds K of
+  // tile kt+1 and V of tile kt; the wave issues the score MFMAs of tile kt+1,
+  // then runs the softmax of tile kt (whose scores it already holds) while
+  // those MFMAs execute, then the PV MFMAs of tile kt.  Global loads of K
+  // tile kt+2 and V tile kt+1 are in flight across the iteration and land in
+  // the buffers freed in iteration kt-1; one barrier per iteration.
+  gload_k(0);
+  gload_v(0);
+  lstore_k(Kbuf(0));
+  lstore_v(Vbuf(0));
+  if (n_kt > 1) {
+    gload_k(1);
+    lstore_k(Kbuf(1));
+  }
   __syncthreads();
+  f32x16 s_cur[2], s_nxt[2];
+  qk(Kbuf(0), s_cur);
 
   for (int kt = 0; kt < n_kt; ++kt) {
-    const int st = kt & 1;
-    if (kt + 1 < n_kt) gload(kt + 1);
-    if (wave_active) {
-      const _Float16* Ks = lds + st * stage_halves<HD>();
-      const _Float16* Vt = Ks + KT * KS;
-      // S^T = K Q^T: keys on rows, this wave's 32 queries on columns
-      f32x16 s[2];
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[kk][r] = 0.f;
-#pragma unroll
-        for (int ks = 0; ks < HD / 16; ++ks) {
-          const f16x8 a =
-              *reinterpret_cast<const f16x8*>(&Ks[(kk * 32 + col) * KS + ks * 16 + half * 8]);
-          s[kk] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, qf[ks], s[kk], 0, 0, 0);
-        }
-      }
+    if (kt + 2 < n_kt) gload_k(kt + 2);
+    if (kt + 1 < n_kt) {
+      gload_v(kt + 1);
+      qk(Kbuf(kt + 1), s_nxt);
+    }
+    {
+      f32x16* s = s_cur;
       // causal mask (only tiles that reach past the smallest query position)
       if (kt * KT + KT - 1 > kmin) {
 #pragma unroll
@@ -216,24 +253,27 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
           for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
       }
       m_i = m_new;
-      float psum = 0.f;
+      // P = 2^(s * scale - m) with the raw hardware exp2 (arguments are <= 8;
+      // underflow to 0 is harmless), rounded to f16 in pairs; the row sum adds
+      // the same f16 values (v_dot2 with ones, fp32 accumulate)
+      f16x2 ph[2][8];
+      const f16x2 ones = {(_Float16)1.0f, (_Float16)1.0f};
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float e = exp2f(__builtin_fmaf(s[kk][r], scale_log2, -m_new));
-          s[kk][r] = e;
-          psum += e;
+        for (int r2 = 0; r2 < 8; ++r2) {
+          const float e0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kk][2 * r2], scale_log2, -m_new));
+          const float e1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kk][2 * r2 + 1], scale_log2, -m_new));
+          ph[kk][r2] = f16x2{(_Float16)e0, (_Float16)e1};
+          l_i = __builtin_amdgcn_fdot2(ph[kk][r2], ones, l_i, false);
         }
-      l_i += psum;
-
       // O^T += V^T P^T over 4 steps of 16 keys.  Slot sl of lane group `half`
       // carries key 16*ks + 8*(sl/4) + 4*half + sl%4 in both operands.
+      const _Float16* Vt = Vbuf(kt);
 #pragma unroll
       for (int ks = 0; ks < KT / 16; ++ks) {
-        f16x8 pb;
-#pragma unroll
-        for (int sl = 0; sl < 8; ++sl) pb[sl] = (_Float16)s[ks >> 1][(ks & 1) * 8 + sl];
+        const f16x2* pp = &ph[ks >> 1][(ks & 1) * 4];
+        const f16x8 pb = {pp[0][0], pp[0][1], pp[1][0], pp[1][1], pp[2][0], pp[2][1], pp[3][0], pp[3][1]};
 #pragma unroll
         for (int t = 0; t < HD / 32; ++t) {
           const _Float16* vrow = &Vt[(t * 32 + col) * VT_STRIDE + 16 * ks + 4 * half];
@@ -244,8 +284,11 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
         }
       }
     }
-    if (kt + 1 < n_kt) lstore(st ^ 1);
+    if (kt + 2 < n_kt) lstore_k(Kbuf(kt));
+    if (kt + 1 < n_kt) lstore_v(Vbuf(kt + 1));
     __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) s_cur[kk] = s_nxt[kk];
   }
 
   const float l = l_i + __shfl_xor(l_i, 32);
@@ -266,7 +309,7 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
 
 template <int HD, int NW>
 void launch_nw(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S, const int32_t* table,
-               int C, int64_t slot_bytes, int nq, int nkv, int group, int qw, float scale_log2,
+               int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group, int qw, float scale_log2,
                _Float16* O, hipStream_t s) {
   const size_t lds_bytes = 2 * stage_halves<HD>() * sizeof(_Float16);
   static const bool attr = [&] {
@@ -277,20 +320,21 @@ void launch_nw(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S, 
   (void)attr;
   const int bq = 32 * qw;
   const int n_qtiles = (m + bq - 1) / bq;
-  const int blocks = 8 * ((n_qtiles + 7) / 8) * nkv;
+  const int blocks = (8 % nkv == 0) ? 8 * ((n_qtiles + 8 / nkv - 1) / (8 / nkv))
+                                    : 8 * ((n_qtiles + 7) / 8) * nkv;
   hipLaunchKernelGGL((attn_kernel<HD, NW>), dim3(blocks), dim3(64 * NW), lds_bytes, s, Q, qpos, m, S,
-                     table, C, slot_bytes, nq, nkv, group, qw, n_qtiles, scale_log2, O);
+                     table, C, cshift, slot_bytes, nq, nkv, group, qw, n_qtiles, scale_log2, O);
 }
 
 template <int HD>
 void launch_hd(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S, const int32_t* table,
-               int C, int64_t slot_bytes, int nq, int nkv, int group, int qw, float scale_log2,
+               int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group, int qw, float scale_log2,
                _Float16* O, hipStream_t s) {
   switch (group * qw) {
-    case 5: launch_nw<HD, 5>(Q, qpos, m, S, table, C, slot_bytes, nq, nkv, group, qw, scale_log2, O, s); break;
-    case 6: launch_nw<HD, 6>(Q, qpos, m, S, table, C, slot_bytes, nq, nkv, group, qw, scale_log2, O, s); break;
-    case 7: launch_nw<HD, 7>(Q, qpos, m, S, table, C, slot_bytes, nq, nkv, group, qw, scale_log2, O, s); break;
-    default: launch_nw<HD, 8>(Q, qpos, m, S, table, C, slot_bytes, nq, nkv, group, qw, scale_log2, O, s); break;
+    case 5: launch_nw<HD, 5>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, s); break;
+    case 6: launch_nw<HD, 6>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, s); break;
+    case 7: launch_nw<HD, 7>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, s); break;
+    default: launch_nw<HD, 8>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, s); break;
   }
 }
 
@@ -305,10 +349,12 @@ void launch_attention(const void* q, const int32_t* qpos, int m, const void* sla
   const _Float16* Q = reinterpret_cast<const _Float16*>(q);
   const uint8_t* S = reinterpret_cast<const uint8_t*>(slab);
   _Float16* O = reinterpret_cast<_Float16*>(out);
+  int cshift = 0;
+  while ((1 << cshift) < chunk_tokens) ++cshift;   // chunk_tokens is a power of two
   if (head_dim == 128)
-    launch_hd<128>(Q, qpos, m, S, table, chunk_tokens, slot_bytes, n_q, n_kv, group, qw, scale_log2, O, s);
+    launch_hd<128>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, scale_log2, O, s);
   else
-    launch_hd<64>(Q, qpos, m, S, table, chunk_tokens, slot_bytes, n_q, n_kv, group, qw, scale_log2, O, s);
+    launch_hd<64>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, scale_log2, O, s);
 }
 
 }  // namespace mzk

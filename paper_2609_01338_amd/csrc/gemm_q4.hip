@@ -1,17 +1,24 @@
 // Q4_0-weight GEMM for gfx950: Y = X . W^T, X f16 [m][k], W Q4_0 [n][k].
 //
-// A 512-thread workgroup computes a 256 x 256 tile of Y.  Each 64-wide K step
-// stages the activation tile (f16) and the weight tile in LDS (double
-// buffered, one barrier a step); the weight tile arrives as Q4_0 (2 blocks of
-// 32 per row: 16 nibble bytes + an fp16 scale each) and is dequantized on the
-// way into LDS.  The nibbles are pre-ordered (at load time) so that one
-// and-or per pair of codes builds two halves 1024 + q; a packed subtract of
-// 1032 gives q - 8 exactly and a packed multiply by the scale gives
-// d * (q - 8) rounded once to f16 (2^-11 relative).  Eight waves in a 4 x 2
-// grid each own a 64 x 128 sub-tile as 4 x 8 tiles of v_mfma_f32_16x16x32_f16
-// with fp32 accumulation.  (f16 rather than bf16 operands: same MFMA rate on
-// this chip, three more mantissa bits, and the activations of this model stay
-// far inside the f16 range.)
+// A 512-thread workgroup computes a 256 x 256 tile of Y in 64-wide K steps.
+// Eight waves in a 4 x 2 grid each own a 64 x 128 sub-tile as 4 x 8 tiles of
+// v_mfma_f32_16x16x32_f16 with fp32 accumulation.  (f16 rather than bf16
+// operands: same MFMA rate on this chip, three more mantissa bits, and the
+// activations of this model stay far inside the f16 range.)
+//
+// Staging: the activation tile goes from global memory straight into LDS
+// (global_load_lds_dwordx4, no registers), requested a full step before it is
+// needed, in three LDS stages.  The weight tile arrives as Q4_0 (2 blocks of 32 per row: 16 code
+// bytes + an fp16 scale) one step ahead in registers and is dequantized into
+// one of two LDS stages: the codes are pre-ordered (at load time) so that one
+// and-or per pair builds two halves 1024 + q, a packed subtract of 1032 gives
+// q - 8 exactly, and a packed multiply by the scale gives d * (q - 8) rounded
+// once to f16 (2^-11 relative).  One barrier per step.
+//
+// LDS rows are 128 B with the 16-byte column c of row r stored at column
+// c ^ ((r >> 1) & 7): the MFMA fragment reads (rows l % 16, column l / 16),
+// the direct loads (8 lanes per row) and the dequantized stores (8 lanes on
+// 8 rows) are all bank-conflict free (measured on gfx950).
 //
 // Workgroups are numbered so that each XCD (workgroups are dealt to the 8 XCDs
 // round-robin) walks a contiguous run of tiles, M-major: neighbouring tiles on
@@ -28,13 +35,20 @@ namespace {
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) void glb_void;
 
 constexpr int BM = 256, BN = kGemmTileN, BK = kGemmTileK;
-constexpr int NT = 512;                     // threads
-constexpr int LDS_STRIDE = BK + 8;          // halves per LDS row: 144 B, conflict-free b128 reads
-constexpr int NIB_BYTES = BN * BK / 2;      // 8192
+constexpr int NT = 512;                      // threads
+constexpr int ROW = BK;                      // halves per LDS row (128 B, swizzled)
+constexpr int TILE_HALVES = BM * ROW;        // one 32 KB stage (A and B tiles are both 256 x 64)
+constexpr int A_STAGES = 3, B_STAGES = 2;
+constexpr int NIB_BYTES = BN * BK / 2;       // 8192
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
+
+// LDS offset (halves) of logical 16-byte column c of row r
+__device__ __forceinline__ int swz(int r, int c) { return r * ROW + ((c ^ ((r >> 1) & 7)) << 3); }
 
 __device__ __forceinline__ uint32_t pair_code(uint32_t w, int shift) {
   // two 4-bit codes at bits [shift, shift+4) and [16+shift, 20+shift) -> halves 1024 + q
@@ -47,9 +61,10 @@ __device__ __forceinline__ uint32_t dequant_pair(uint32_t w, int shift, f16x2 d2
   return __builtin_bit_cast(uint32_t, (c - off) * d2);
 }
 
-// One pre-ordered Q4_0 block (4 dwords; dword i holds elements 8i..8i+7) ->
-// 32 halves in LDS.
-__device__ __forceinline__ void dequant_block_to_lds(uint4 nib, uint16_t dbits, _Float16* dst) {
+// One pre-ordered Q4_0 block (4 dwords; dword i holds elements 8i..8i+7) of
+// row `row`, block `blk` -> 32 halves (logical columns 4 blk .. 4 blk + 3).
+__device__ __forceinline__ void dequant_block_to_lds(uint4 nib, uint16_t dbits, _Float16* stage,
+                                                     int row, int blk) {
   const _Float16 d = __builtin_bit_cast(_Float16, dbits);
   const f16x2 d2 = {d, d};
   const uint32_t w[4] = {nib.x, nib.y, nib.z, nib.w};
@@ -60,7 +75,7 @@ __device__ __forceinline__ void dequant_block_to_lds(uint4 nib, uint16_t dbits, 
     o.y = dequant_pair(w[i], 4, d2);
     o.z = dequant_pair(w[i], 8, d2);
     o.w = dequant_pair(w[i], 12, d2);
-    *reinterpret_cast<uint4*>(dst + 8 * i) = o;
+    *reinterpret_cast<uint4*>(stage + swz(row, blk * 4 + i)) = o;
   }
 }
 
@@ -69,8 +84,8 @@ __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict_
                                                      const uint8_t* __restrict__ Wp, int N,
                                                      void* __restrict__ Y) {
   extern __shared__ __attribute__((aligned(16))) _Float16 lds[];
-  _Float16* As = lds;                              // [2][BM * LDS_STRIDE]
-  _Float16* Bs = lds + 2 * BM * LDS_STRIDE;        // [2][BN * LDS_STRIDE]
+  _Float16* As = lds;                                  // [A_STAGES][TILE_HALVES]
+  _Float16* Bs = lds + A_STAGES * TILE_HALVES;         // [B_STAGES][TILE_HALVES]
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -85,16 +100,21 @@ __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict_
   const int mt = t / n_tiles, nt = t % n_tiles;
   const int nk = K / BK;
 
-  // activation loads: 4 segments of 16 B per thread (rows tid/8 + 64 i, column tid%8)
-  const int a_row = tid >> 3, a_c16 = tid & 7;
-  const _Float16* x0 = X + (size_t)min(mt * BM + a_row, M - 1) * K + a_c16 * 8;
-  const _Float16* x1 = X + (size_t)min(mt * BM + a_row + 64, M - 1) * K + a_c16 * 8;
-  const _Float16* x2 = X + (size_t)min(mt * BM + a_row + 128, M - 1) * K + a_c16 * 8;
-  const _Float16* x3 = X + (size_t)min(mt * BM + a_row + 192, M - 1) * K + a_c16 * 8;
-  const int a_lds = a_row * LDS_STRIDE + a_c16 * 8;
-  // weight loads: one Q4_0 block (row tid/2, block tid%2) per thread
+  // direct A loads: wave w fills rows 32w .. 32w+31 with 4 instructions of 8
+  // rows; lane l lands at LDS (row 8i + l/8, physical column l%8), which holds
+  // logical column (l%8) ^ ((row >> 1) & 7)
+  const _Float16* a_src[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int pr = wave * 32 + i * 8 + (lane >> 3);
+    const int lc = (lane & 7) ^ ((pr >> 1) & 7);
+    a_src[i] = X + (size_t)min(mt * BM + pr, M - 1) * K + lc * 8;
+  }
+  // weight loads: one Q4_0 block per thread; 8 consecutive lanes take 8 rows of
+  // the same block so their LDS stores land in distinct banks
   const uint8_t* wtile = Wp + (size_t)nt * nk * kGemmTileBytes;
-  const int b_lds = (tid >> 1) * LDS_STRIDE + (tid & 1) * 32;
+  const int b_row = (tid & 7) | ((tid >> 4) << 3), b_blk = (tid >> 3) & 1;
+  const int b_idx = b_row * 2 + b_blk;
 
   f32x4 acc[4][8];
 #pragma unroll
@@ -102,59 +122,73 @@ __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict_
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  uint4 ra0, ra1, ra2, ra3, rnib;
-  uint16_t rsc;
-#define MZ_GLOAD(kt)                                                                    \
-  do {                                                                                  \
-    const int ko_ = (kt) * BK;                                                          \
-    ra0 = *reinterpret_cast<const uint4*>(x0 + ko_);                                    \
-    ra1 = *reinterpret_cast<const uint4*>(x1 + ko_);                                    \
-    ra2 = *reinterpret_cast<const uint4*>(x2 + ko_);                                    \
-    ra3 = *reinterpret_cast<const uint4*>(x3 + ko_);                                    \
-    const uint8_t* t_ = wtile + (size_t)(kt) * kGemmTileBytes;                          \
-    rnib = *reinterpret_cast<const uint4*>(t_ + tid * 16);                              \
-    rsc = *reinterpret_cast<const uint16_t*>(t_ + NIB_BYTES + tid * 2);                 \
-  } while (0)
-#define MZ_LSTORE(st)                                                                   \
-  do {                                                                                  \
-    _Float16* a_ = As + (st) * BM * LDS_STRIDE + a_lds;                                 \
-    *reinterpret_cast<uint4*>(a_) = ra0;                                                \
-    *reinterpret_cast<uint4*>(a_ + 64 * LDS_STRIDE) = ra1;                              \
-    *reinterpret_cast<uint4*>(a_ + 128 * LDS_STRIDE) = ra2;                             \
-    *reinterpret_cast<uint4*>(a_ + 192 * LDS_STRIDE) = ra3;                             \
-    dequant_block_to_lds(rnib, rsc, Bs + (st) * BN * LDS_STRIDE + b_lds);               \
-  } while (0)
+  // All vector-memory loads of the main loop are issued and waited for
+  // explicitly.  Completion order between the direct-to-LDS loads and the
+  // register loads is not relied on: every wait is a full vmcnt(0), placed
+  // where only the loads about to be consumed are in flight.  The register
+  // results pass through the wait as in/out operands so nothing reads them
+  // before it.
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  u32x4 rnib;
+  uint32_t rsc;
+  const uint32_t a_lds0 = (uint32_t)(uintptr_t)(lds_void*)(As + wave * 32 * ROW);
+  auto load_a = [&](int kt) {            // 4 direct global -> LDS loads per lane
+    const uint32_t base = __builtin_amdgcn_readfirstlane(a_lds0 + (kt % A_STAGES) * TILE_HALVES * 2);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      // one wait state between the M0 write and the LDS-DMA load that reads it
+      asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+                   :: "s"(base + i * 8 * ROW * 2), "v"(a_src[i] + kt * BK) : "memory", "m0");
+  };
+  auto load_b = [&](int kt) {
+    const uint8_t* t_ = wtile + (size_t)kt * kGemmTileBytes;
+    asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(rnib) : "v"(t_ + b_idx * 16) : "memory");
+    asm volatile("global_load_ushort %0, %1, off" : "=v"(rsc) : "v"(t_ + NIB_BYTES + b_idx * 2) : "memory");
+  };
+  auto dequant = [&](_Float16* stage) {
+    dequant_block_to_lds(uint4{rnib.x, rnib.y, rnib.z, rnib.w}, (uint16_t)rsc, stage, b_row, b_blk);
+  };
 
-  MZ_GLOAD(0);
-  MZ_LSTORE(0);
+  // prologue: A of steps 0 and 1 requested, B of step 0 dequantized
+  load_a(0);
+  load_b(0);
+  if (nk > 1) load_a(1);
+  asm volatile("s_waitcnt vmcnt(0)" : "+v"(rnib), "+v"(rsc) :: "memory");
+  dequant(Bs);
   __syncthreads();
 
+  // step kt: B codes of kt+1 requested, MFMAs on stage kt, then wait for
+  // B(kt+1) and A(kt+1) (requested at the end of step kt-1), dequantize
+  // B(kt+1), request A(kt+2) into the stage freed by step kt-1, barrier.
   const int frag_row = lane & 15;
-  const int frag_k = (lane >> 4) * 8;
+  const int frag_c = lane >> 4;
   for (int kt = 0; kt < nk; ++kt) {
-    const int st = kt & 1;
-    if (kt + 1 < nk) MZ_GLOAD(kt + 1);
-    const _Float16* Ab = As + st * BM * LDS_STRIDE + (wm * 64 + frag_row) * LDS_STRIDE + frag_k;
-    const _Float16* Bb = Bs + st * BN * LDS_STRIDE + (wn * 128 + frag_row) * LDS_STRIDE + frag_k;
+    const bool more_b = kt + 1 < nk, more_a = kt + 2 < nk;
+    if (more_b) load_b(kt + 1);
+    const _Float16* Ab = As + (kt % A_STAGES) * TILE_HALVES;
+    const _Float16* Bb = Bs + (kt & 1) * TILE_HALVES;
 #pragma unroll
     for (int ks = 0; ks < BK / 32; ++ks) {
       f16x8 a[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        a[i] = *reinterpret_cast<const f16x8*>(Ab + i * 16 * LDS_STRIDE + ks * 32);
+        a[i] = *reinterpret_cast<const f16x8*>(Ab + swz(wm * 64 + i * 16 + frag_row, ks * 4 + frag_c));
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const f16x8 bf = *reinterpret_cast<const f16x8*>(Bb + j * 16 * LDS_STRIDE + ks * 32);
+        const f16x8 bf =
+            *reinterpret_cast<const f16x8*>(Bb + swz(wn * 128 + j * 16 + frag_row, ks * 4 + frag_c));
 #pragma unroll
         for (int i = 0; i < 4; ++i)
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[i], bf, acc[i][j], 0, 0, 0);
       }
     }
-    if (kt + 1 < nk) MZ_LSTORE(st ^ 1);
+    if (more_b) {
+      asm volatile("s_waitcnt vmcnt(0)" : "+v"(rnib), "+v"(rsc) :: "memory");
+      dequant(Bs + ((kt + 1) & 1) * TILE_HALVES);
+    }
+    if (more_a) load_a(kt + 2);
     __syncthreads();
   }
-#undef MZ_GLOAD
-#undef MZ_LSTORE
 
   // epilogue
   const int col_in = lane & 15;
@@ -188,7 +222,7 @@ __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict_
   }
 }
 
-constexpr size_t kLdsBytes = (size_t)2 * (BM + BN) * LDS_STRIDE * sizeof(_Float16);
+constexpr size_t kLdsBytes = (size_t)(A_STAGES + B_STAGES) * TILE_HALVES * sizeof(_Float16);
 
 }  // namespace
 

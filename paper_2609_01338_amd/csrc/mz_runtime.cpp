@@ -495,7 +495,8 @@ void validate_cfg(const mz_model_cfg* c) {
     fail(MZ_EINVAL, "n_q_heads must be a positive multiple of n_kv_heads");
   if (c->n_q_heads / c->n_kv_heads > 8) fail(MZ_EINVAL, "GQA group above 8 is not supported");
   if (c->d_ffn < 1 || c->vocab < 1) fail(MZ_EINVAL, "d_ffn and vocab must be positive");
-  if (c->chunk_tokens < 1 || c->max_ctx < 1) fail(MZ_EINVAL, "chunk_tokens and max_ctx must be positive");
+  if (c->chunk_tokens < 2 || (c->chunk_tokens & (c->chunk_tokens - 1)) || c->max_ctx < 1)
+    fail(MZ_EINVAL, "chunk_tokens must be a power of two >= 2 and max_ctx positive");
   if (!(c->rope_theta > 0) || !(c->rms_eps >= 0)) fail(MZ_EINVAL, "rope_theta must be > 0 and rms_eps >= 0");
 }
 
@@ -1339,7 +1340,8 @@ mz_status mz_attention(const void* q, const int32_t* qpos, int32_t m, const void
                        void* out, void* stream) {
   return guarded(nullptr, [&] {
     if (!q || !qpos || !slab || !table || !out) fail(MZ_EINVAL, "NULL pointer");
-    if (m < 1 || n_table < 1 || chunk_tokens < 1) fail(MZ_EINVAL, "sizes must be positive");
+    if (m < 1 || n_table < 1) fail(MZ_EINVAL, "sizes must be positive");
+    if (chunk_tokens < 2 || (chunk_tokens & (chunk_tokens - 1))) fail(MZ_EINVAL, "chunk_tokens must be a power of two >= 2");
     if (head_dim != 64 && head_dim != 128) fail(MZ_EINVAL, "head_dim must be 64 or 128");
     if (n_kv < 1 || n_q % n_kv || n_q / n_kv > 8) fail(MZ_EINVAL, "bad head counts");
     const int64_t slot_bytes = (int64_t)chunk_tokens * n_kv * head_dim * 2 * 2;
