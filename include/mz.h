@@ -46,7 +46,7 @@ typedef enum { MZ_RES = 0, MZ_SWAP = 1, MZ_DROP = 2 } mz_unit_state;
 /* Model shape.  d_model must be a multiple of 256; d_ffn need not be a
  * multiple of 32 (Q4_0 rows of W_down are zero-padded); head_dim must be 64 or
  * 128; n_q_heads a multiple of n_kv_heads with a group of at most 8;
- * chunk_tokens a power of two (>= 2); max_ctx bounds context + prompt tokens. */
+ * chunk_tokens a power of two (>= 8); max_ctx bounds context + prompt tokens. */
 typedef struct {
   int32_t n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ffn, vocab;
   int32_t chunk_tokens, max_ctx;
@@ -94,8 +94,9 @@ mz_status mz_prefill_context(mz_ctx *ctx, const int32_t *tokens, int32_t n);
 mz_status mz_set_context(mz_ctx *ctx, const int32_t *tokens, int32_t n);
 
 /* Write chunk `chunk` of layer `layer` from host arrays k, v, each
- * [chunk_tokens][n_kv_heads * head_dim] IEEE half, hidden index innermost.
- * ESTATE if the chunk is not resident. */
+ * [chunk_tokens][n_kv_heads * head_dim] IEEE half, hidden index innermost
+ * (the exchange layout; the device slot keeps V transposed).  ESTATE if the
+ * chunk is not resident. */
 mz_status mz_import_kv(mz_ctx *ctx, int32_t layer, int32_t chunk, const void *k_f16,
                        const void *v_f16);
 
@@ -193,11 +194,11 @@ mz_status mz_q4_gemm(const void *x_f16, int32_t m, int32_t n_pad, int32_t k,
 
 /* Causal GQA attention of q (f16 [m][n_q_heads][head_dim], rotated) at
  * positions qpos (int32 [m], ascending) over the KV chunks of one layer:
- * chunk c of the layer lives in slot table[c] of slab (each slot: K then V,
- * each [chunk_tokens][n_kv_heads * head_dim] f16; chunk_tokens a power of
- * two).  Keys 0..qpos[i] are read;
- * table must cover chunk (qpos[m-1] / chunk_tokens).  out: f16
- * [m][n_q_heads * head_dim]. */
+ * chunk c of the layer lives in slot table[c] of slab.  A slot holds K
+ * token-major ([chunk_tokens][n_kv_heads * head_dim] f16) followed by V
+ * dimension-major ([n_kv_heads * head_dim][chunk_tokens] f16); chunk_tokens is
+ * a power of two and a multiple of 8.  Keys 0..qpos[i] are read; table must
+ * cover chunk (qpos[m-1] / chunk_tokens).  out: f16 [m][n_q_heads * head_dim]. */
 mz_status mz_attention(const void *q_f16, const int32_t *qpos, int32_t m, const void *slab,
                        const int32_t *table, int32_t n_table, int32_t chunk_tokens,
                        int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, void *out_f16,

@@ -7,12 +7,13 @@
 // pass with an online softmax over non-contiguous chunks (paper Sec. 4.2),
 // here on MFMA.
 //
-// A workgroup serves one KV head and a tile of query rows for all of that
-// head's G query heads; each wave owns 32 queries of one query head.  Per
-// 64-key tile the keys (K rows) and the values, transposed (V^T: keys
-// contiguous per dimension), are staged in LDS once for the whole group,
-// double buffered: the next tile's global loads are in flight while the
-// current one is multiplied.  Scores are computed transposed, S^T = K Q^T,
+// A chunk slot stores K token-major ([C][dkv]) and V dimension-major
+// ([dkv][C], "hidden-dimension-first"), so both tiles load as plain 16-byte
+// rows.  A workgroup serves one KV head and a tile of query rows for all of
+// that head's G query heads; each wave owns 32 queries of one query head.  Per
+// 64-key tile K and V^T are staged in LDS once for the whole group, double
+// buffered: the next tile's global loads are in flight while the current one
+// is multiplied.  Scores are computed transposed, S^T = K Q^T,
 // with v_mfma_f32_32x32x16_f16 so that each lane holds 32 scores of a single
 // query: the row max needs one cross-lane exchange (lane l and l ^ 32), and
 // the exponentiated scores are already laid out as the B operand of
@@ -43,15 +44,31 @@ typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int KT = 64;             // keys per tile
-constexpr int VT_STRIDE = KT + 4;  // halves per V^T row (136 B): conflict-free b64 reads
 constexpr float kMaxSlack = 8.0f;  // log2 headroom before the running max is raised
 
-template <int HD>
-constexpr int k_stride() { return HD + 8; }   // halves per K row in LDS
+// LDS tiles are unpadded and XOR-swizzled on 16-byte columns.  K tile: KT rows
+// (keys) of HD halves; V^T tile: HD rows (dimensions) of KT halves (128 B).
+// Row r's logical column c sits at column c ^ g(r), with g(r) = r & 15 for
+// 256-byte rows and (r >> 1) & 7 for 128-byte rows: the fragment reads below
+// (lane groups {0-7, 24-31}, {8-15, 16-23}, ... on 16 slots of 16 B) and the
+// staging writes (8 lanes on 8 columns of one row) are bank-conflict free.
+template <int ROW_HALVES>
+__device__ __forceinline__ int swz(int r, int c) {
+  if constexpr (ROW_HALVES == 128)
+    return r * 128 + ((c ^ (r & 15)) << 3);
+  else
+    return r * 64 + ((c ^ ((r >> 1) & 7)) << 3);
+}
+
+// Key permutation of the score tile: MFMA row i holds key pi(i) (bits 2 and 3
+// swapped), so the accumulator slots a lane turns into the P operand are 8
+// consecutive keys and each V^T fragment is a single 16-byte read.
+__device__ __forceinline__ int pi_key(int i) { return (i & ~0xC) | ((i & 8) >> 1) | ((i & 4) << 1); }
 
 template <int HD>
-constexpr size_t stage_halves() { return (size_t)KT * k_stride<HD>() + (size_t)HD * VT_STRIDE; }
-// two K buffers and two V buffers
+constexpr int k_tile_halves() { return KT * HD; }
+template <int HD>
+constexpr int v_tile_halves() { return HD * KT; }
 
 template <int HD, int NW>
 __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restrict__ Q,
@@ -62,9 +79,9 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
                                                        int group, int qw, int n_qtiles,
                                                        float scale_log2, _Float16* __restrict__ O) {
   constexpr int NTH = 64 * NW;
-  constexpr int KS = k_stride<HD>();
-  constexpr int K_SEGS = KT * (HD / 8);             // 16-byte segments of a K tile
-  constexpr int V_SEGS = (KT / 2) * (HD / 8);       // key pairs x 8-dim groups of a V tile
+  constexpr int KC = HD / 8;                        // 16-byte columns of a K row
+  constexpr int K_SEGS = KT * KC;                   // 16-byte pieces of a K tile
+  constexpr int V_SEGS = HD * (KT / 8);             // 16-byte pieces of a V^T tile
   constexpr int K_PER = (K_SEGS + NTH - 1) / NTH;
   constexpr int V_PER = (V_SEGS + NTH - 1) / NTH;
   extern __shared__ __attribute__((aligned(16))) _Float16 lds[];
@@ -121,71 +138,67 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
     for (int r = 0; r < 16; ++r) o[t][r] = 0.f;
   float m_i = -INFINITY, l_i = 0.f;
 
+  // slot layout: K [C][dkv] (token-major), then V^T [dkv][C] (dimension-major)
   const uint8_t* kbase = slab + (int64_t)kvh * HD * 2;
-  const uint8_t* vbase = slab + (int64_t)C * dkv * 2 + (int64_t)kvh * HD * 2;   // V follows K
+  const uint8_t* vbase = slab + (int64_t)C * dkv * 2 + (int64_t)kvh * HD * C * 2;
   const int cmask = C - 1;                    // C is a power of two
-  const int row_bytes = dkv * 2;
-  uint4 rk[K_PER], rv0[V_PER], rv1[V_PER];
+  const int krow_bytes = dkv * 2, vrow_bytes = C * 2;
+  uint4 rk[K_PER], rv[V_PER];
 
-  // global -> registers for K tile kt / V tile kt
+  // global -> registers for K tile kt / V^T tile kt (keys past kmax are zero)
   auto gload_k = [&](int kt) {
 #pragma unroll
     for (int i = 0; i < K_PER; ++i) {
       const int seg = tid + i * NTH;
-      const int jj = kt * KT + seg / (HD / 8);
+      const int jj = kt * KT + seg / KC;
       rk[i] = make_uint4(0, 0, 0, 0);
       if (seg < K_SEGS && jj <= kmax)
         rk[i] = *reinterpret_cast<const uint4*>(kbase + (uint64_t)(uint32_t)table[jj >> cshift] * slot_bytes +
-                                                (uint32_t)((jj & cmask) * row_bytes + (seg % (HD / 8)) * 16));
+                                                (uint32_t)((jj & cmask) * krow_bytes + (seg % KC) * 16));
     }
   };
   auto gload_v = [&](int kt) {
 #pragma unroll
     for (int i = 0; i < V_PER; ++i) {
       const int seg = tid + i * NTH;
-      const int j0 = kt * KT + 2 * (seg % (KT / 2));
-      const uint32_t col = (seg / (KT / 2)) * 16;
-      rv0[i] = make_uint4(0, 0, 0, 0);
-      rv1[i] = make_uint4(0, 0, 0, 0);
+      const int dim = seg / (KT / 8), j0 = kt * KT + (seg % (KT / 8)) * 8;
+      uint4 v = make_uint4(0, 0, 0, 0);
       if (seg < V_SEGS && j0 <= kmax) {
-        // j0 is even and C >= 2, so keys j0 and j0 + 1 share a chunk
-        const uint8_t* src = vbase + (uint64_t)(uint32_t)table[j0 >> cshift] * slot_bytes +
-                             (uint32_t)((j0 & cmask) * row_bytes) + col;
-        rv0[i] = *reinterpret_cast<const uint4*>(src);
-        if (j0 + 1 <= kmax) rv1[i] = *reinterpret_cast<const uint4*>(src + row_bytes);
+        // 8 keys of one chunk (C is a multiple of 8)
+        v = *reinterpret_cast<const uint4*>(vbase + (uint64_t)(uint32_t)table[j0 >> cshift] * slot_bytes +
+                                            (uint32_t)(dim * vrow_bytes + (j0 & cmask) * 2));
+        const int nv = kmax - j0 + 1;           // keys of this group that exist
+        if (nv < 8) {
+          uint32_t e[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            if (2 * q >= nv) e[q] = 0u;
+            else if (2 * q + 1 >= nv) e[q] &= 0xFFFFu;
+          }
+          v = make_uint4(e[0], e[1], e[2], e[3]);
+        }
       }
+      rv[i] = v;
     }
   };
-  // registers -> LDS buffers (K: [key][dim], V transposed: [dim][key])
-  auto Kbuf = [&](int i) { return lds + (i & 1) * (KT * KS); };
-  auto Vbuf = [&](int i) { return lds + 2 * KT * KS + (i & 1) * (HD * VT_STRIDE); };
+  auto Kbuf = [&](int i) { return lds + (i & 1) * k_tile_halves<HD>(); };
+  auto Vbuf = [&](int i) { return lds + 2 * k_tile_halves<HD>() + (i & 1) * v_tile_halves<HD>(); };
   auto lstore_k = [&](_Float16* Ks) {
 #pragma unroll
     for (int i = 0; i < K_PER; ++i) {
       const int seg = tid + i * NTH;
-      if (seg < K_SEGS)
-        *reinterpret_cast<uint4*>(&Ks[(seg / (HD / 8)) * KS + (seg % (HD / 8)) * 8]) = rk[i];
+      if (seg < K_SEGS) *reinterpret_cast<uint4*>(&Ks[swz<HD>(seg / KC, seg % KC)]) = rk[i];
     }
   };
   auto lstore_v = [&](_Float16* Vt) {
 #pragma unroll
     for (int i = 0; i < V_PER; ++i) {
       const int seg = tid + i * NTH;
-      if (seg >= V_SEGS) continue;
-      const int kp = seg % (KT / 2), dg = seg / (KT / 2);
-      const uint32_t a[4] = {rv0[i].x, rv0[i].y, rv0[i].z, rv0[i].w};
-      const uint32_t bb[4] = {rv1[i].x, rv1[i].y, rv1[i].z, rv1[i].w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        // dims dg*8 + 2e (low halves) and dg*8 + 2e + 1 (high halves), keys 2kp, 2kp+1
-        *reinterpret_cast<uint32_t*>(&Vt[(dg * 8 + 2 * e) * VT_STRIDE + 2 * kp]) =
-            (a[e] & 0xFFFFu) | (bb[e] << 16);
-        *reinterpret_cast<uint32_t*>(&Vt[(dg * 8 + 2 * e + 1) * VT_STRIDE + 2 * kp]) =
-            (a[e] >> 16) | (bb[e] & 0xFFFF0000u);
-      }
+      if (seg < V_SEGS) *reinterpret_cast<uint4*>(&Vt[swz<KT>(seg / (KT / 8), seg % (KT / 8))]) = rv[i];
     }
   };
-  // S^T = K Q^T: keys on rows, this wave's 32 queries on columns
+  // S^T = K Q^T: keys (permuted by pi) on rows, this wave's 32 queries on columns
+  const int krow = pi_key(col);
   auto qk = [&](const _Float16* Ks, f32x16* sc) {
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
@@ -193,14 +206,14 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
       for (int r = 0; r < 16; ++r) sc[kk][r] = 0.f;
 #pragma unroll
       for (int ks = 0; ks < HD / 16; ++ks) {
-        const f16x8 a = *reinterpret_cast<const f16x8*>(&Ks[(kk * 32 + col) * KS + ks * 16 + half * 8]);
+        const f16x8 a = *reinterpret_cast<const f16x8*>(&Ks[swz<HD>(kk * 32 + krow, ks * 2 + half)]);
         sc[kk] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, qf[ks], sc[kk], 0, 0, 0);
       }
     }
   };
 
   // Pipeline: K runs one tile ahead of V.  In iteration kt the LDS holds K of
-  // tile kt+1 and V of tile kt; the wave issues the score MFMAs of tile kt+1,
+  // tile kt+1 and V^T of tile kt; the wave issues the score MFMAs of tile kt+1,
   // then runs the softmax of tile kt (whose scores it already holds) while
   // those MFMAs execute, then the PV MFMAs of tile kt.  Global loads of K
   // tile kt+2 and V tile kt+1 are in flight across the iteration and land in
@@ -231,7 +244,7 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
         for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            const int key = kt * KT + kk * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+            const int key = kt * KT + kk * 32 + pi_key(8 * (r >> 2) + 4 * half + (r & 3));
             if (key > p) s[kk][r] = -INFINITY;
           }
       }
@@ -267,8 +280,8 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
           ph[kk][r2] = f16x2{(_Float16)e0, (_Float16)e1};
           l_i = __builtin_amdgcn_fdot2(ph[kk][r2], ones, l_i, false);
         }
-      // O^T += V^T P^T over 4 steps of 16 keys.  Slot sl of lane group `half`
-      // carries key 16*ks + 8*(sl/4) + 4*half + sl%4 in both operands.
+      // O^T += V^T P^T over 4 steps of 16 keys: slot sl of lane group `half`
+      // carries key 16*ks + 8*half + sl in both operands (through pi)
       const _Float16* Vt = Vbuf(kt);
 #pragma unroll
       for (int ks = 0; ks < KT / 16; ++ks) {
@@ -276,10 +289,7 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
         const f16x8 pb = {pp[0][0], pp[0][1], pp[1][0], pp[1][1], pp[2][0], pp[2][1], pp[3][0], pp[3][1]};
 #pragma unroll
         for (int t = 0; t < HD / 32; ++t) {
-          const _Float16* vrow = &Vt[(t * 32 + col) * VT_STRIDE + 16 * ks + 4 * half];
-          const f16x4 lo = *reinterpret_cast<const f16x4*>(vrow);
-          const f16x4 hi = *reinterpret_cast<const f16x4*>(vrow + 8);
-          const f16x8 a = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          const f16x8 a = *reinterpret_cast<const f16x8*>(&Vt[swz<KT>(t * 32 + col, 2 * ks + half)]);
           o[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, pb, o[t], 0, 0, 0);
         }
       }
@@ -311,7 +321,7 @@ template <int HD, int NW>
 void launch_nw(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S, const int32_t* table,
                int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group, int qw, float scale_log2,
                _Float16* O, hipStream_t s) {
-  const size_t lds_bytes = 2 * stage_halves<HD>() * sizeof(_Float16);
+  const size_t lds_bytes = 2 * (k_tile_halves<HD>() + v_tile_halves<HD>()) * sizeof(_Float16);
   static const bool attr = [&] {
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<HD, NW>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
@@ -344,7 +354,9 @@ void launch_attention(const void* q, const int32_t* qpos, int m, const void* sla
                       const int32_t* table, int chunk_tokens, int64_t slot_bytes, int n_q,
                       int n_kv, int head_dim, void* out, hipStream_t s) {
   const int group = n_q / n_kv;          // 1..8
-  const int qw = 8 / group;              // 32-query row groups per workgroup: 5..8 waves
+  // 32-query row groups per workgroup: 5..8 waves, so one staged K/V tile
+  // serves as many queries as the registers allow
+  const int qw = group >= 8 ? 1 : 8 / group;
   const float scale_log2 = 1.4426950408889634f / __builtin_sqrtf((float)head_dim);
   const _Float16* Q = reinterpret_cast<const _Float16*>(q);
   const uint8_t* S = reinterpret_cast<const uint8_t*>(slab);

@@ -43,45 +43,102 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ 
   }
 }
 
-// One block per row.  Rotate-half RoPE on the nq query heads and nkv key heads;
-// q goes to q_out (f16), k and v to the row's slot (f16) when kv_off >= 0.
+constexpr int ROPE_ROWS = 16;   // rows of R_l per block
+
+// Rotate-half RoPE on the nq query heads and nkv key heads of ROPE_ROWS rows;
+// q goes to q_out (f16).  Rows with kv_off >= 0 write their K (f16,
+// token-major) at slab + kv_off and their V (f16) into the slot's V^T part
+// (dimension-major: V^T[d][p % C] at slot + C*dkv*2 + (d*C + p % C)*2).  The
+// V values are staged in LDS; a group of 8 rows that are 8 consecutive
+// positions from a multiple of 8, all written to one slot, leaves as one
+// 16-byte store per dimension, any other row as 2-byte stores.  Blocks are
+// renumbered so that the row blocks one XCD runs at a time are adjacent and
+// their partial V^T lines meet in that XCD's L2.
 __global__ __launch_bounds__(256) void rope_kv_kernel(const float* __restrict__ qkv, int qkv_stride,
-                                                      const int32_t* __restrict__ pos,
+                                                      int M, const int32_t* __restrict__ pos,
                                                       const int64_t* __restrict__ kv_off,
                                                       const float2* __restrict__ cs, int nq,
-                                                      int nkv, int hd, int64_t v_delta,
+                                                      int nkv, int hd, int C,
                                                       _Float16* __restrict__ q_out,
                                                       uint8_t* __restrict__ slab) {
-  const int row = blockIdx.x;
-  const int halfd = hd / 2;
+  extern __shared__ _Float16 vstage[];     // [ROPE_ROWS][dkv]
+  __shared__ int s_pos[ROPE_ROWS];         // position of the row
+  __shared__ int s_pc[ROPE_ROWS];          // p % C, or -1 when the row writes no KV
+  __shared__ int64_t s_k[ROPE_ROWS];       // byte offset of the row's K
+  __shared__ int64_t s_vt[ROPE_ROWS];      // byte offset of V^T[0][p % C]
+  __shared__ int s_fast[ROPE_ROWS / 8];
+  const int nb = gridDim.x, b = blockIdx.x, per = nb / 8;
+  const int blk = b < per * 8 ? (b % 8) * per + b / 8 : b;
+  const int row0 = blk * ROPE_ROWS;
+  const int nrows = min(ROPE_ROWS, M - row0);
+  const int halfd = hd / 2, hq = hd / 8;   // quads per half head
   const int dq = nq * hd, dkv = nkv * hd;
-  const float* src = qkv + (size_t)row * qkv_stride;
-  const int p = pos[row];
-  const int64_t off = kv_off[row];
-  const float2* c = cs + (size_t)p * halfd;
-  _Float16* qo = q_out + (size_t)row * dq;
-  _Float16* ko = off >= 0 ? reinterpret_cast<_Float16*>(slab + off) : nullptr;
-  const int n_pairs = (nq + nkv) * halfd;
-  for (int idx = threadIdx.x; idx < n_pairs; idx += blockDim.x) {
-    const int head = idx / halfd, i = idx % halfd;
-    const float2 t = c[i];
-    const float* x = src + head * hd;   // q heads then k heads are contiguous
-    const float x1 = x[i], x2 = x[i + halfd];
-    const float y1 = x1 * t.x - x2 * t.y;
-    const float y2 = x2 * t.x + x1 * t.y;
-    if (head < nq) {
-      qo[head * hd + i] = (_Float16)y1;
-      qo[head * hd + i + halfd] = (_Float16)y2;
-    } else if (ko) {
-      const int g = head - nq;
-      ko[g * hd + i] = (_Float16)y1;
-      ko[g * hd + i + halfd] = (_Float16)y2;
-    }
+  if (threadIdx.x < ROPE_ROWS) {
+    const int row = row0 + threadIdx.x;
+    const int64_t off = row < M ? kv_off[row] : -1;
+    const int p = row < M ? pos[row] : 0;
+    const int pc = off >= 0 ? (p & (C - 1)) : -1;
+    s_pos[threadIdx.x] = p;
+    s_pc[threadIdx.x] = pc;
+    s_k[threadIdx.x] = off;
+    s_vt[threadIdx.x] = off >= 0 ? off - (int64_t)pc * dkv * 2 + (int64_t)C * dkv * 2 + pc * 2 : 0;
   }
-  if (ko) {
-    _Float16* vo = reinterpret_cast<_Float16*>(slab + off + v_delta);
-    const float* v = src + dq + dkv;
-    for (int i = threadIdx.x; i < dkv; i += blockDim.x) vo[i] = (_Float16)v[i];
+  __syncthreads();
+  // rotate 4 pairs (i..i+3, i+hd/2..i+hd/2+3) per item: float4 loads, 8-byte stores
+  typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+  const int n_quads = (nq + nkv) * hq;
+#pragma unroll 4
+  for (int idx = threadIdx.x; idx < nrows * n_quads; idx += blockDim.x) {
+    const int rr = idx / n_quads, qd = idx - rr * n_quads;
+    const int head = qd / hq, i = (qd - head * hq) * 4;
+    const float* x = qkv + (size_t)(row0 + rr) * qkv_stride + head * hd;  // q then k heads
+    const float4 x1 = *reinterpret_cast<const float4*>(x + i);
+    const float4 x2 = *reinterpret_cast<const float4*>(x + i + halfd);
+    const float4* c = reinterpret_cast<const float4*>(cs + (size_t)s_pos[rr] * halfd + i);
+    const float4 c01 = c[0], c23 = c[1];   // (cos, sin) of pairs i, i+1 and i+2, i+3
+    const f16x4 y1 = {(_Float16)(x1.x * c01.x - x2.x * c01.y), (_Float16)(x1.y * c01.z - x2.y * c01.w),
+                      (_Float16)(x1.z * c23.x - x2.z * c23.y), (_Float16)(x1.w * c23.z - x2.w * c23.w)};
+    const f16x4 y2 = {(_Float16)(x2.x * c01.x + x1.x * c01.y), (_Float16)(x2.y * c01.z + x1.y * c01.w),
+                      (_Float16)(x2.z * c23.x + x1.z * c23.y), (_Float16)(x2.w * c23.z + x1.w * c23.w)};
+    _Float16* dst;
+    if (head < nq) {
+      dst = q_out + (size_t)(row0 + rr) * dq + head * hd;
+    } else {
+      if (s_pc[rr] < 0) continue;
+      dst = reinterpret_cast<_Float16*>(slab + s_k[rr]) + (head - nq) * hd;
+    }
+    *reinterpret_cast<f16x4*>(dst + i) = y1;
+    *reinterpret_cast<f16x4*>(dst + i + halfd) = y2;
+  }
+  const int vq = dkv / 4;
+#pragma unroll 4
+  for (int idx = threadIdx.x; idx < nrows * vq; idx += blockDim.x) {
+    const int rr = idx / vq, d = (idx - rr * vq) * 4;
+    const float4 v = *reinterpret_cast<const float4*>(qkv + (size_t)(row0 + rr) * qkv_stride + dq + dkv + d);
+    *reinterpret_cast<f16x4*>(&vstage[rr * dkv + d]) = f16x4{(_Float16)v.x, (_Float16)v.y, (_Float16)v.z, (_Float16)v.w};
+  }
+  __syncthreads();
+  if (threadIdx.x < ROPE_ROWS / 8) {
+    const int g0 = threadIdx.x * 8;
+    bool fast = s_pc[g0] >= 0 && (s_pc[g0] & 7) == 0;
+    for (int i = 1; i < 8 && fast; ++i)
+      fast = s_pc[g0 + i] == s_pc[g0] + i && s_vt[g0 + i] == s_vt[g0] + 2 * i;
+    s_fast[threadIdx.x] = fast;
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < (ROPE_ROWS / 8) * dkv; idx += blockDim.x) {
+    const int g = idx / dkv, d = idx % dkv, g0 = g * 8;
+    if (s_fast[g]) {
+      typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+      f16x8 v;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = vstage[(g0 + i) * dkv + d];
+      *reinterpret_cast<f16x8*>(slab + s_vt[g0] + (int64_t)d * C * 2) = v;
+    } else {
+      for (int i = 0; i < 8; ++i)
+        if (s_pc[g0 + i] >= 0)
+          *reinterpret_cast<_Float16*>(slab + s_vt[g0 + i] + (int64_t)d * C * 2) = vstage[(g0 + i) * dkv + d];
+    }
   }
 }
 
@@ -244,11 +301,12 @@ void launch_rmsnorm(const float* h, int m, int d, float eps, void* x, hipStream_
 }
 
 void launch_rope_kv(const float* qkv, int qkv_stride, int m, const int32_t* pos,
-                    const int64_t* kv_off, const float2* rope_cs, int nq, int nkv, int hd,
-                    int64_t v_delta, void* q_out, void* slab, hipStream_t s) {
-  hipLaunchKernelGGL(rope_kv_kernel, dim3(m), dim3(256), 0, s, qkv, qkv_stride, pos, kv_off, rope_cs, nq, nkv,
-                     hd, v_delta, reinterpret_cast<_Float16*>(q_out),
-                     reinterpret_cast<uint8_t*>(slab));
+                    const int64_t* kv_off, const float2* rope_cs, int nq, int nkv, int hd, int C,
+                    void* q_out, void* slab, hipStream_t s) {
+  const size_t lds = (size_t)ROPE_ROWS * nkv * hd * sizeof(_Float16);
+  hipLaunchKernelGGL(rope_kv_kernel, dim3((m + ROPE_ROWS - 1) / ROPE_ROWS), dim3(256), lds, s, qkv,
+                     qkv_stride, m, pos, kv_off, rope_cs, nq, nkv, hd, C,
+                     reinterpret_cast<_Float16*>(q_out), reinterpret_cast<uint8_t*>(slab));
 }
 
 void launch_embed(const uint8_t* e_nib, const uint16_t* e_scale, const int32_t* tok, int m, int d,

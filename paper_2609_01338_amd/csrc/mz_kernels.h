@@ -33,12 +33,12 @@ void launch_attention(const void* q, const int32_t* qpos, int m, const void* sla
 void launch_rmsnorm(const float* h, int m, int d, float eps, void* x, hipStream_t s);
 
 // Rotary embedding + KV scatter.  qkv float [m][qkv_stride] holding q, k, v; rope_cs
-// float2 [max_pos][hd/2] (cos, sin); kv_off int64 [m]: byte offset of the
-// row's K in slab (its V is kv_bytes_half later) or -1 to skip.
-// q_out f16 [m][nq*hd].
+// float2 [max_pos][hd/2] (cos, sin); kv_off int64 [m]: byte offset in slab of
+// the row's K (token-major [C][dkv] slot half) or -1 to skip; the row's V goes
+// to the slot's V^T half ([dkv][C]).  q_out f16 [m][nq*hd].  C is a power of two.
 void launch_rope_kv(const float* qkv, int qkv_stride, int m, const int32_t* pos,
-                    const int64_t* kv_off, const float2* rope_cs, int nq, int nkv, int hd,
-                    int64_t v_delta, void* q_out, void* slab, hipStream_t s);
+                    const int64_t* kv_off, const float2* rope_cs, int nq, int nkv, int hd, int C,
+                    void* q_out, void* slab, hipStream_t s);
 
 // h float [m][d] = dequant(E[tok[i]]) with E split into nibbles [V][d/2] and
 // fp16 scales [V][d/32].

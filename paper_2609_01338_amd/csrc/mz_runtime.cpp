@@ -2,7 +2,9 @@
 //
 // Memory (paper Sec. 4.2, re-targeted to a discrete GPU):
 //  - KV: one HBM slab of fixed-size slots, one slot per (layer, chunk), each
-//    holding K then V of chunk_tokens tokens ([C][dkv] f16 each).  A per-layer
+//    holding K of chunk_tokens tokens token-major ([C][dkv] f16) and then V
+//    dimension-major ([dkv][C] f16: the chunk is "hidden-dimension-first" for
+//    the values, which the attention kernel stages without transposing).  A per-layer
 //    chunk table maps chunk -> slot; free slots sit in an ordered set so that
 //    contiguous runs can be handed out for coalesced copies.  Allocation at
 //    restore time is O(log n) with no driver call.
@@ -495,8 +497,8 @@ void validate_cfg(const mz_model_cfg* c) {
     fail(MZ_EINVAL, "n_q_heads must be a positive multiple of n_kv_heads");
   if (c->n_q_heads / c->n_kv_heads > 8) fail(MZ_EINVAL, "GQA group above 8 is not supported");
   if (c->d_ffn < 1 || c->vocab < 1) fail(MZ_EINVAL, "d_ffn and vocab must be positive");
-  if (c->chunk_tokens < 2 || (c->chunk_tokens & (c->chunk_tokens - 1)) || c->max_ctx < 1)
-    fail(MZ_EINVAL, "chunk_tokens must be a power of two >= 2 and max_ctx positive");
+  if (c->chunk_tokens < 8 || (c->chunk_tokens & (c->chunk_tokens - 1)) || c->max_ctx < 1)
+    fail(MZ_EINVAL, "chunk_tokens must be a power of two >= 8 and max_ctx positive");
   if (!(c->rope_theta > 0) || !(c->rms_eps >= 0)) fail(MZ_EINVAL, "rope_theta must be > 0 and rms_eps >= 0");
 }
 
@@ -752,8 +754,8 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
                             x->kv_state[(size_t)l * MC + (nc_old - 1)] == MZ_SWAP;
     if (early_wait) HIPCHK(hipStreamWaitEvent(cs, x->ev_kv[l], 0));
     x->timed(kKRopeKV, 0, (double)n * (x->nqkv * 4.0 + x->dq * 2.0) + rows.nD[l] * 4.0 * x->dkv, cs, [&] {
-      mzk::launch_rope_kv(x->qkv, x->nqkv_pad, n, pos, off, x->rope_cs, x->nq, x->nkv, x->hd,
-                          (int64_t)C * x->dkv * 2, x->q16, x->kv_slab, cs);
+      mzk::launch_rope_kv(x->qkv, x->nqkv_pad, n, pos, off, x->rope_cs, x->nq, x->nkv, x->hd, C,
+                          x->q16, x->kv_slab, cs);
     });
     if (kv_copy[l] && !early_wait) HIPCHK(hipStreamWaitEvent(cs, x->ev_kv[l], 0));
     double keys = 0;
@@ -1090,6 +1092,14 @@ static int32_t chunk_slot(mz_ctx* x, int32_t layer, int32_t chunk) {
   return s;
 }
 
+// The exchange layout of a chunk is K [C][dkv] and V [C][dkv]; the slot keeps
+// V dimension-major (V^T [dkv][C]) for the attention kernel, so V is
+// transposed on the way in and out.
+static void transpose_f16(const uint16_t* in, int rows, int cols, uint16_t* out) {
+  for (int r = 0; r < rows; ++r)
+    for (int c = 0; c < cols; ++c) out[(size_t)c * rows + r] = in[(size_t)r * cols + c];
+}
+
 mz_status mz_import_kv(mz_ctx* x, int32_t layer, int32_t chunk, const void* k, const void* v) {
   if (!x) return MZ_EINVAL;
   return guarded(x, [&] {
@@ -1097,9 +1107,11 @@ mz_status mz_import_kv(mz_ctx* x, int32_t layer, int32_t chunk, const void* k, c
     const int32_t s = chunk_slot(x, layer, chunk);
     HIPCHK(hipStreamSynchronize(x->s_compute));
     const size_t half = (size_t)x->slot_bytes / 2;
+    std::vector<uint16_t> vt((size_t)x->C * x->dkv);
+    transpose_f16((const uint16_t*)v, x->C, x->dkv, vt.data());
     uint8_t* dst = x->kv_slab + (int64_t)s * x->slot_bytes;
     HIPCHK(hipMemcpy(dst, k, half, hipMemcpyHostToDevice));
-    HIPCHK(hipMemcpy(dst + half, v, half, hipMemcpyHostToDevice));
+    HIPCHK(hipMemcpy(dst + half, vt.data(), half, hipMemcpyHostToDevice));
   });
 }
 
@@ -1111,9 +1123,11 @@ mz_status mz_read_kv(mz_ctx* x, int32_t layer, int32_t chunk, void* k, void* v) 
     HIPCHK(hipStreamSynchronize(x->s_compute));
     HIPCHK(hipStreamSynchronize(x->s_swap));
     const size_t half = (size_t)x->slot_bytes / 2;
+    std::vector<uint16_t> vt((size_t)x->C * x->dkv);
     const uint8_t* src = x->kv_slab + (int64_t)s * x->slot_bytes;
     HIPCHK(hipMemcpy(k, src, half, hipMemcpyDeviceToHost));
-    HIPCHK(hipMemcpy(v, src + half, half, hipMemcpyDeviceToHost));
+    HIPCHK(hipMemcpy(vt.data(), src + half, half, hipMemcpyDeviceToHost));
+    transpose_f16(vt.data(), x->dkv, x->C, (uint16_t*)v);
   });
 }
 
@@ -1341,7 +1355,7 @@ mz_status mz_attention(const void* q, const int32_t* qpos, int32_t m, const void
   return guarded(nullptr, [&] {
     if (!q || !qpos || !slab || !table || !out) fail(MZ_EINVAL, "NULL pointer");
     if (m < 1 || n_table < 1) fail(MZ_EINVAL, "sizes must be positive");
-    if (chunk_tokens < 2 || (chunk_tokens & (chunk_tokens - 1))) fail(MZ_EINVAL, "chunk_tokens must be a power of two >= 2");
+    if (chunk_tokens < 8 || (chunk_tokens & (chunk_tokens - 1))) fail(MZ_EINVAL, "chunk_tokens must be a power of two >= 8");
     if (head_dim != 64 && head_dim != 128) fail(MZ_EINVAL, "head_dim must be 64 or 128");
     if (n_kv < 1 || n_q % n_kv || n_q / n_kv > 8) fail(MZ_EINVAL, "bad head counts");
     const int64_t slot_bytes = (int64_t)chunk_tokens * n_kv * head_dim * 2 * 2;

@@ -108,11 +108,14 @@ def _attn_case(nq, nkv, hd, C, S, qpos, seed, sample=None):
     table = rng.permutation(n_slots)[:nch].astype(np.int32)
     K = rng.standard_normal((S, dkv)).astype(np.float16)
     V = rng.standard_normal((S, dkv)).astype(np.float16)
-    slab = np.full((n_slots, 2, C, dkv), np.nan, np.float16)     # unused rows are NaN
+    # slot: K [C][dkv] token-major, then V^T [dkv][C]; unused rows are NaN
+    kpart = np.full((n_slots, C, dkv), np.nan, np.float16)
+    vpart = np.full((n_slots, dkv, C), np.nan, np.float16)
     for c in range(nch):
         n = min(C, S - c * C)
-        slab[table[c], 0, :n] = K[c * C:c * C + n]
-        slab[table[c], 1, :n] = V[c * C:c * C + n]
+        kpart[table[c], :n] = K[c * C:c * C + n]
+        vpart[table[c], :, :n] = V[c * C:c * C + n].T
+    slab = np.concatenate([kpart.reshape(n_slots, -1), vpart.reshape(n_slots, -1)], axis=1)
     qpos = np.asarray(qpos, np.int32)
     M = qpos.size
     q = (rng.standard_normal((M, nq, hd)) * 1.0).astype(np.float16)
@@ -139,7 +142,8 @@ def _attn_case(nq, nkv, hd, C, S, qpos, seed, sample=None):
 
 @pytest.mark.parametrize("nq,nkv,hd,C,S", [
     (4, 2, 64, 16, 128), (4, 2, 64, 16, 117), (32, 8, 64, 256, 600), (24, 8, 128, 256, 700),
-    (12, 2, 128, 256, 530), (32, 8, 128, 256, 400), (8, 8, 128, 64, 200), (6, 1, 64, 32, 90)])
+    (12, 2, 128, 256, 530), (32, 8, 128, 256, 400), (8, 8, 128, 64, 200), (6, 1, 64, 32, 90),
+    (4, 4, 128, 8, 77)])
 def test_attention_small(nq, nkv, hd, C, S):
     rng = np.random.default_rng(S)
     dense = np.arange(S)
