@@ -70,7 +70,7 @@ constexpr int k_tile_halves() { return KT * HD; }
 template <int HD>
 constexpr int v_tile_halves() { return HD * KT; }
 
-template <int HD, int NW>
+template <int HD, int NW, bool DIRECT>
 __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restrict__ Q,
                                                        const int32_t* __restrict__ qpos, int M,
                                                        const uint8_t* __restrict__ slab,
@@ -197,6 +197,77 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
       if (seg < V_SEGS) *reinterpret_cast<uint4*>(&Vt[swz<KT>(seg / (KT / 8), seg % (KT / 8))]) = rv[i];
     }
   };
+  // Direct path (C >= KT, so a tile lies in one chunk): the tile's slot comes
+  // from one scalar table read, and each wave moves whole 1 KB stretches of
+  // the swizzled LDS tile with global_load_lds_dwordx4 (lane l fills bytes
+  // 16l .. 16l+15 of the stretch, so it fetches the 16 global bytes that the
+  // swizzle puts there).  Per-lane offsets within a tile are loop invariant.
+  constexpr int KQ = K_SEGS / 64, VQ = V_SEGS / 64;           // 1 KB stretches per tile
+  constexpr int KQ_PER = (KQ + NW - 1) / NW, VQ_PER = (VQ + NW - 1) / NW;
+  const int wu = __builtin_amdgcn_readfirstlane(w);
+  uint32_t kofs[KQ_PER], vofs[VQ_PER];
+#pragma unroll
+  for (int i = 0; i < KQ_PER; ++i) {
+    const int pc = (i * NW + wu) * 64 + lane;                 // 16-byte piece of the tile
+    const int r = pc / KC;
+    const int c = (pc % KC) ^ (HD == 128 ? (r & 15) : ((r >> 1) & 7));
+    kofs[i] = (uint32_t)(r * krow_bytes + c * 16);
+  }
+#pragma unroll
+  for (int i = 0; i < VQ_PER; ++i) {
+    const int pc = (i * NW + wu) * 64 + lane;
+    const int r = pc / (KT / 8);
+    const int c = (pc % (KT / 8)) ^ ((r >> 1) & 7);
+    vofs[i] = (uint32_t)(r * vrow_bytes + c * 16);
+  }
+  typedef __attribute__((address_space(3))) void lds_void;
+  auto lds_addr = [&](const _Float16* p_) { return (uint32_t)(uintptr_t)(lds_void*)p_; };
+  auto dload = [&](const uint8_t* gbase, uint32_t lds0, const uint32_t* ofs, int nq_, int per) {
+#pragma unroll
+    for (int i = 0; i < per; ++i) {
+      const int q = i * NW + wu;
+      if (q < nq_)
+        // one wait state between the M0 write and the load that reads it
+        asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+                     :: "s"(lds0 + q * 1024), "v"(ofs[i]), "s"(gbase) : "memory", "m0");
+    }
+  };
+  auto dload_k = [&](int t, const _Float16* Ks) {
+    const int j0 = t * KT;
+    const uint8_t* g = kbase + (uint64_t)(uint32_t)table[j0 >> cshift] * slot_bytes + (uint32_t)((j0 & cmask) * krow_bytes);
+    dload(g, __builtin_amdgcn_readfirstlane(lds_addr(Ks)), kofs, KQ, KQ_PER);
+  };
+  auto dload_v = [&](int t, const _Float16* Vt) {
+    const int j0 = t * KT;
+    const uint8_t* g = vbase + (uint64_t)(uint32_t)table[j0 >> cshift] * slot_bytes + (uint32_t)((j0 & cmask) * 2);
+    dload(g, __builtin_amdgcn_readfirstlane(lds_addr(Vt)), vofs, VQ, VQ_PER);
+  };
+  // After the wave's own loads of V^T tile t have landed: zero the keys past
+  // kmax in the pieces this lane fetched (P is 0 there, but the slot rows past
+  // the last written position may hold anything).
+  auto vfix = [&](int t, _Float16* Vt) {
+#pragma unroll
+    for (int i = 0; i < VQ_PER; ++i) {
+      const int q = i * NW + wu;
+      if (q >= VQ) continue;
+      const int pc = q * 64 + lane;
+      const int r = pc / (KT / 8);
+      const int c = (pc % (KT / 8)) ^ ((r >> 1) & 7);
+      const int nv = kmax - (t * KT + c * 8) + 1;            // keys of this piece that exist
+      if (nv < 8) {
+        uint4* d = reinterpret_cast<uint4*>(Vt + pc * 8);
+        uint4 v = *d;
+        uint32_t e[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          if (2 * k >= nv) e[k] = 0u;
+          else if (2 * k + 1 >= nv) e[k] &= 0xFFFFu;
+        }
+        *d = make_uint4(e[0], e[1], e[2], e[3]);
+      }
+    }
+  };
+
   // S^T = K Q^T: keys (permuted by pi) on rows, this wave's 32 queries on columns
   const int krow = pi_key(col);
   auto qk = [&](const _Float16* Ks, f32x16* sc) {
@@ -212,94 +283,179 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
     }
   };
 
+  // causal mask of tile kt (keys past the lane's query position -> -inf).
+  // Score slot (kk, r) of lane group `half` holds key
+  // kt*KT + 8*half + kk*32 + 16*(r/8) + 4*((r/4)%2) + r%4 (the pi order).
+  auto mask_tile = [&](f32x16* sc, int kt) {
+    const int th = p - kt * KT - 8 * half;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int c = kk * 32 + 16 * (r >> 3) + 4 * ((r >> 2) & 1) + (r & 3);
+        if (c > th) sc[kk][r] = -INFINITY;
+      }
+  };
+  auto tile_max = [&](const f32x16* sc) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[kk][r]);
+    return fmaxf(mx, __shfl_xor(mx, 32)) * scale_log2;
+  };
+  // raise the running max only when a tile exceeds it by more than the slack;
+  // the accumulators are rescaled then (rare, skipped wave-wide otherwise)
+  auto update_max = [&](float mx) {
+    const bool raise = mx > m_i + kMaxSlack;
+    const float m_new = raise ? mx : m_i;   // finite after tile 0: key 0 is visible to all
+    if (__any(raise)) {
+      const float alpha = exp2f(m_i - m_new);
+      l_i *= alpha;
+#pragma unroll
+      for (int t = 0; t < HD / 32; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
+    }
+    m_i = m_new;
+  };
+  // P = 2^(s * scale - m) with the raw hardware exp2 (arguments are <= 8;
+  // underflow to 0 is harmless), rounded to f16 in pairs straight into the
+  // MFMA B operand (pk[j] holds keys 16*j .. 16*j+15 of this lane group's
+  // half, pair r of it in elements 2r, 2r+1); the row sum adds the same f16
+  // values (v_dot2 with ones, fp32 accumulation).
+  const f16x2 ones = {(_Float16)1.0f, (_Float16)1.0f};
+  auto exp_pair = [&](const f32x16* sc, int r2, f16x8* pk) {
+    const int kk = r2 >> 3, rr = r2 & 7;     // score slots 2rr, 2rr+1 of half kk
+    const float e0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[kk][2 * rr], scale_log2, -m_i));
+    const float e1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[kk][2 * rr + 1], scale_log2, -m_i));
+    f16x8& dst = pk[r2 >> 2];
+    dst[2 * (r2 & 3)] = (_Float16)e0;
+    dst[2 * (r2 & 3) + 1] = (_Float16)e1;
+    l_i = __builtin_amdgcn_fdot2(f16x2{dst[2 * (r2 & 3)], dst[2 * (r2 & 3) + 1]}, ones, l_i, false);
+  };
+  constexpr int TN = HD / 32;          // output accumulators (32 dimensions each)
+  constexpr int NQK = 2 * (HD / 16);   // score MFMAs per tile (8 or 16)
+  constexpr int NPV = 4 * TN;          // PV MFMAs per tile (8 or 16)
+  // operand fragments: score MFMA i reads K rows of half i % 2 at k-step i / 2;
+  // PV MFMA i reads V^T rows 32 * (i % TN) .. at key step i / TN
+  auto kfrag = [&](const _Float16* Ks, int i) {
+    return *reinterpret_cast<const f16x8*>(&Ks[swz<HD>((i & 1) * 32 + krow, (i >> 1) * 2 + half)]);
+  };
+  auto vfrag = [&](const _Float16* Vt, int i) {
+    return *reinterpret_cast<const f16x8*>(&Vt[swz<KT>((i % TN) * 32 + col, 2 * (i / TN) + half)]);
+  };
+  const f32x16 zero16 = {};
+
   // Pipeline: K runs one tile ahead of V.  In iteration kt the LDS holds K of
-  // tile kt+1 and V^T of tile kt; the wave issues the score MFMAs of tile kt+1,
-  // then runs the softmax of tile kt (whose scores it already holds) while
-  // those MFMAs execute, then the PV MFMAs of tile kt.  Global loads of K
-  // tile kt+2 and V tile kt+1 are in flight across the iteration and land in
-  // the buffers freed in iteration kt-1; one barrier per iteration.
-  gload_k(0);
-  gload_v(0);
-  lstore_k(Kbuf(0));
-  lstore_v(Vbuf(0));
-  if (n_kt > 1) {
-    gload_k(1);
-    lstore_k(Kbuf(1));
+  // tile kt+1 and V^T of tile kt, and the wave holds the masked scores of tile
+  // kt and its running max.  Phase A issues the score MFMAs of tile kt+1, one
+  // per slot, each slot also carrying a share of the exponentials of keys
+  // 0-31 of tile kt; phase B issues the PV MFMAs of tile kt with the
+  // exponentials of keys 32-63 and then the max of tile kt+1.  Slots are
+  // fenced so the compiler keeps this order: the MFMAs of a wave then run
+  // under its own VALU work.  Fragment reads run two slots ahead.  Global
+  // loads of K tile kt+2 and V tile kt+1 are in flight across the iteration
+  // and land in the buffers freed in iteration kt-1; one barrier per
+  // iteration.
+  if constexpr (DIRECT) {
+    dload_k(0, Kbuf(0));
+    dload_v(0, Vbuf(0));
+    if (n_kt > 1) dload_k(1, Kbuf(1));
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    if (n_kt == 1) vfix(0, Vbuf(0));
+  } else {
+    gload_k(0);
+    gload_v(0);
+    lstore_k(Kbuf(0));
+    lstore_v(Vbuf(0));
+    if (n_kt > 1) {
+      gload_k(1);
+      lstore_k(Kbuf(1));
+    }
   }
   __syncthreads();
-  f32x16 s_cur[2], s_nxt[2];
-  qk(Kbuf(0), s_cur);
+  f32x16 s0[2], s1[2];
+  qk(Kbuf(0), s0);
+  if (KT - 1 > kmin) mask_tile(s0, 0);
+  update_max(tile_max(s0));
 
-  for (int kt = 0; kt < n_kt; ++kt) {
-    if (kt + 2 < n_kt) gload_k(kt + 2);
-    if (kt + 1 < n_kt) {
-      gload_v(kt + 1);
-      qk(Kbuf(kt + 1), s_nxt);
+  auto step = [&](int kt, f32x16* sc, f32x16* sn) {
+    if constexpr (DIRECT) {
+      if (kt + 2 < n_kt) dload_k(kt + 2, Kbuf(kt));
+      if (kt + 1 < n_kt) dload_v(kt + 1, Vbuf(kt + 1));
+    } else {
+      if (kt + 2 < n_kt) gload_k(kt + 2);
+      if (kt + 1 < n_kt) gload_v(kt + 1);
     }
+    f16x8 pk[4];
+    // phase A (the score MFMAs of the last iteration read a stale buffer and
+    // are discarded)
     {
-      f32x16* s = s_cur;
-      // causal mask (only tiles that reach past the smallest query position)
-      if (kt * KT + KT - 1 > kmin) {
+      const _Float16* Kn = Kbuf(kt + 1);
+      f16x8 fa = kfrag(Kn, 0), fb = kfrag(Kn, 1);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int key = kt * KT + kk * 32 + pi_key(8 * (r >> 2) + 4 * half + (r & 3));
-            if (key > p) s[kk][r] = -INFINITY;
-          }
+      for (int i = 0; i < NQK; ++i) {
+        const f16x8 fc = i + 2 < NQK ? kfrag(Kn, i + 2) : fb;
+        sn[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa, qf[i >> 1], i < 2 ? zero16 : sn[i & 1], 0, 0, 0);
+        fa = fb;
+        fb = fc;
+        // 8 exponential pairs over the slots
+        if (i % (NQK / 8) == 0) exp_pair(sc, i / (NQK / 8), pk);
+        __builtin_amdgcn_sched_barrier(0);
       }
-      float mx = -INFINITY;
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kk][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32)) * scale_log2;
-      // raise the running max only when this tile exceeds it by more than the slack
-      const bool raise = mx > m_i + kMaxSlack;
-      const float m_new = raise ? mx : m_i;   // finite after tile 0: key 0 is visible to all
-      if (__any(raise)) {
-        const float alpha = exp2f(m_i - m_new);
-        l_i *= alpha;
-#pragma unroll
-        for (int t = 0; t < HD / 32; ++t)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
-      }
-      m_i = m_new;
-      // P = 2^(s * scale - m) with the raw hardware exp2 (arguments are <= 8;
-      // underflow to 0 is harmless), rounded to f16 in pairs; the row sum adds
-      // the same f16 values (v_dot2 with ones, fp32 accumulate)
-      f16x2 ph[2][8];
-      const f16x2 ones = {(_Float16)1.0f, (_Float16)1.0f};
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-        for (int r2 = 0; r2 < 8; ++r2) {
-          const float e0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kk][2 * r2], scale_log2, -m_new));
-          const float e1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kk][2 * r2 + 1], scale_log2, -m_new));
-          ph[kk][r2] = f16x2{(_Float16)e0, (_Float16)e1};
-          l_i = __builtin_amdgcn_fdot2(ph[kk][r2], ones, l_i, false);
-        }
-      // O^T += V^T P^T over 4 steps of 16 keys: slot sl of lane group `half`
-      // carries key 16*ks + 8*half + sl in both operands (through pi)
+      // keep those exponentials here: they are only read in phase B
+      asm volatile("" : "+v"(pk[0]), "+v"(pk[1]));
+    }
+    const bool more = kt + 1 < n_kt;
+    if (more && (kt + 1) * KT + KT - 1 > kmin) {
+      asm volatile("");   // a real branch: only the last tiles of a query block need the mask
+      mask_tile(sn, kt + 1);
+    }
+    // phase B
+    float mx = -INFINITY;
+    {
       const _Float16* Vt = Vbuf(kt);
+      f16x8 fa = vfrag(Vt, 0), fb = vfrag(Vt, 1);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int ks = 0; ks < KT / 16; ++ks) {
-        const f16x2* pp = &ph[ks >> 1][(ks & 1) * 4];
-        const f16x8 pb = {pp[0][0], pp[0][1], pp[1][0], pp[1][1], pp[2][0], pp[2][1], pp[3][0], pp[3][1]};
+      for (int i = 0; i < NPV; ++i) {
+        const f16x8 fc = i + 2 < NPV ? vfrag(Vt, i + 2) : fb;
+        o[i % TN] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa, pk[i / TN], o[i % TN], 0, 0, 0);
+        fa = fb;
+        fb = fc;
+        if (i < NPV / 2) {
+          // keys 32-63 (pk[2], pk[3]) are needed from slot NPV/2 on
 #pragma unroll
-        for (int t = 0; t < HD / 32; ++t) {
-          const f16x8 a = *reinterpret_cast<const f16x8*>(&Vt[swz<KT>(t * 32 + col, 2 * ks + half)]);
-          o[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, pb, o[t], 0, 0, 0);
+          for (int j = 0; j < 16 / NPV; ++j) exp_pair(sc, 8 + i * (16 / NPV) + j, pk);
+        } else {
+          // max of the next tile's 32 scores over the remaining slots
+          constexpr int PER = 32 / (NPV / 2);
+          const int b0 = (i - NPV / 2) * PER;
+#pragma unroll
+          for (int e = 0; e < PER; ++e) mx = fmaxf(mx, sn[(b0 + e) >> 4][(b0 + e) & 15]);
         }
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
-    if (kt + 2 < n_kt) lstore_k(Kbuf(kt));
-    if (kt + 1 < n_kt) lstore_v(Vbuf(kt + 1));
+    mx = fmaxf(mx, __shfl_xor(mx, 32)) * scale_log2;
+    if (more) update_max(mx);
+    if constexpr (DIRECT) {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      if (kt + 2 == n_kt) vfix(kt + 1, Vbuf(kt + 1));
+    } else {
+      if (kt + 2 < n_kt) lstore_k(Kbuf(kt));
+      if (more) lstore_v(Vbuf(kt + 1));
+    }
     __syncthreads();
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) s_cur[kk] = s_nxt[kk];
+  };
+  int kt = 0;
+  for (; kt + 1 < n_kt; kt += 2) {
+    step(kt, s0, s1);
+    step(kt + 1, s1, s0);
   }
+  if (kt < n_kt) step(kt, s0, s1);
 
   const float l = l_i + __shfl_xor(l_i, 32);
   const float inv = 1.0f / l;
@@ -317,13 +473,13 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
   }
 }
 
-template <int HD, int NW>
-void launch_nw(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S, const int32_t* table,
+template <int HD, int NW, bool DIRECT>
+void launch_nwd(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S, const int32_t* table,
                int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group, int qw, float scale_log2,
                _Float16* O, hipStream_t s) {
   const size_t lds_bytes = 2 * (k_tile_halves<HD>() + v_tile_halves<HD>()) * sizeof(_Float16);
   static const bool attr = [&] {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<HD, NW>),
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<HD, NW, DIRECT>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
     return true;
   }();
@@ -332,8 +488,18 @@ void launch_nw(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S, 
   const int n_qtiles = (m + bq - 1) / bq;
   const int blocks = (8 % nkv == 0) ? 8 * ((n_qtiles + 8 / nkv - 1) / (8 / nkv))
                                     : 8 * ((n_qtiles + 7) / 8) * nkv;
-  hipLaunchKernelGGL((attn_kernel<HD, NW>), dim3(blocks), dim3(64 * NW), lds_bytes, s, Q, qpos, m, S,
+  hipLaunchKernelGGL((attn_kernel<HD, NW, DIRECT>), dim3(blocks), dim3(64 * NW), lds_bytes, s, Q, qpos, m, S,
                      table, C, cshift, slot_bytes, nq, nkv, group, qw, n_qtiles, scale_log2, O);
+}
+
+template <int HD, int NW>
+void launch_nw(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S, const int32_t* table,
+               int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group, int qw, float scale_log2,
+               _Float16* O, hipStream_t s) {
+  if (C >= KT)
+    launch_nwd<HD, NW, true>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, s);
+  else
+    launch_nwd<HD, NW, false>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, s);
 }
 
 template <int HD>
