@@ -75,7 +75,7 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(const float* __restrict__ 
   const int dq = nq * hd, dkv = nkv * hd;
   if (threadIdx.x < ROPE_ROWS) {
     const int row = row0 + threadIdx.x;
-    const int64_t off = row < M ? kv_off[row] : -1;
+    const int64_t off = row < M && kv_off ? kv_off[row] : -1;
     const int p = row < M ? pos[row] : 0;
     const int pc = off >= 0 ? (p & (C - 1)) : -1;
     s_pos[threadIdx.x] = p;

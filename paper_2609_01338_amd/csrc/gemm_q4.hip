@@ -1,4 +1,5 @@
-// Q4_0-weight GEMM for gfx950: Y = X . W^T, X f16 [m][k], W Q4_0 [n][k].
+// Q4_0-weight GEMM for gfx950: Y = X . W^T, X f16 [m][k], W Q4_0 [n][k]; optionally
+// Y[r] = X[a_rows[r]] . W^T (the rows of a layer that need this projection).
 //
 // A 512-thread workgroup computes a 256 x 256 tile of Y in 64-wide K steps.
 // Eight waves in a 4 x 2 grid each own a 64 x 128 sub-tile as 4 x 8 tiles of
@@ -80,7 +81,8 @@ __device__ __forceinline__ void dequant_block_to_lds(uint4 nib, uint16_t dbits, 
 }
 
 template <int EPI>
-__global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict__ X, int M, int K,
+__global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict__ X,
+                                                     const int32_t* __restrict__ a_rows, int M, int K,
                                                      const uint8_t* __restrict__ Wp, int N,
                                                      void* __restrict__ Y) {
   extern __shared__ __attribute__((aligned(16))) _Float16 lds[];
@@ -102,13 +104,15 @@ __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict_
 
   // direct A loads: wave w fills rows 32w .. 32w+31 with 4 instructions of 8
   // rows; lane l lands at LDS (row 8i + l/8, physical column l%8), which holds
-  // logical column (l%8) ^ ((row >> 1) & 7)
+  // logical column (l%8) ^ ((row >> 1) & 7).  Output row r reads activation
+  // row a_rows[r] when a row list is given, else row r.
   const _Float16* a_src[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int pr = wave * 32 + i * 8 + (lane >> 3);
     const int lc = (lane & 7) ^ ((pr >> 1) & 7);
-    a_src[i] = X + (size_t)min(mt * BM + pr, M - 1) * K + lc * 8;
+    const int r = min(mt * BM + pr, M - 1);
+    a_src[i] = X + (size_t)(a_rows ? a_rows[r] : r) * K + lc * 8;
   }
   // weight loads: one Q4_0 block per thread; 8 consecutive lanes take 8 rows of
   // the same block so their LDS stores land in distinct banks
@@ -227,7 +231,7 @@ constexpr size_t kLdsBytes = (size_t)(A_STAGES + B_STAGES) * TILE_HALVES * sizeo
 }  // namespace
 
 void launch_gemm_q4(const void* x, int m, int n, int k, const void* w, int epilogue, void* y,
-                    hipStream_t s) {
+                    hipStream_t s, const int32_t* a_rows) {
   static const bool lds_ok = [] {   // allow more than 64 KB of dynamic LDS, once per process
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_q4_kernel<kEpiStore>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
@@ -243,15 +247,15 @@ void launch_gemm_q4(const void* x, int m, int n, int k, const void* w, int epilo
   const uint8_t* W = reinterpret_cast<const uint8_t*>(w);
   switch (epilogue) {
     case kEpiStore:
-      hipLaunchKernelGGL(gemm_q4_kernel<kEpiStore>, dim3(tiles), dim3(NT), kLdsBytes, s, X, m, k, W,
+      hipLaunchKernelGGL(gemm_q4_kernel<kEpiStore>, dim3(tiles), dim3(NT), kLdsBytes, s, X, a_rows, m, k, W,
                          n, y);
       break;
     case kEpiAdd:
-      hipLaunchKernelGGL(gemm_q4_kernel<kEpiAdd>, dim3(tiles), dim3(NT), kLdsBytes, s, X, m, k, W, n,
+      hipLaunchKernelGGL(gemm_q4_kernel<kEpiAdd>, dim3(tiles), dim3(NT), kLdsBytes, s, X, a_rows, m, k, W, n,
                          y);
       break;
     default:
-      hipLaunchKernelGGL(gemm_q4_kernel<kEpiSwiGLU>, dim3(tiles), dim3(NT), kLdsBytes, s, X, m, k,
+      hipLaunchKernelGGL(gemm_q4_kernel<kEpiSwiGLU>, dim3(tiles), dim3(NT), kLdsBytes, s, X, a_rows, m, k,
                          W, n, y);
       break;
   }

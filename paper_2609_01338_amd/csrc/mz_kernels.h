@@ -21,8 +21,9 @@ enum GemmEpilogue { kEpiStore = 0, kEpiAdd = 1, kEpiSwiGLU = 2 };
 // Y = X . W^T: X f16 [m][k], W packed [n][k] (n % 128 == 0, k % 64 == 0).
 // kEpiStore: Y float [m][n] = acc; kEpiAdd: Y float [m][n] += acc;
 // kEpiSwiGLU: Y f16 [m][n/2] = silu(gate) * up for the interleaved layout.
+// With a_rows (device, m entries), output row r is computed from X row a_rows[r].
 void launch_gemm_q4(const void* x, int m, int n, int k, const void* w, int epilogue, void* y,
-                    hipStream_t s);
+                    hipStream_t s, const int32_t* a_rows = nullptr);
 
 // Causal GQA attention over chunked KV (see mz.h, mz_attention).
 void launch_attention(const void* q, const int32_t* qpos, int m, const void* slab,
@@ -32,10 +33,12 @@ void launch_attention(const void* q, const int32_t* qpos, int m, const void* sla
 // x f16 [m][d] = RMSNorm(h float [m][d]).
 void launch_rmsnorm(const float* h, int m, int d, float eps, void* x, hipStream_t s);
 
-// Rotary embedding + KV scatter.  qkv float [m][qkv_stride] holding q, k, v; rope_cs
-// float2 [max_pos][hd/2] (cos, sin); kv_off int64 [m]: byte offset in slab of
-// the row's K (token-major [C][dkv] slot half) or -1 to skip; the row's V goes
-// to the slot's V^T half ([dkv][C]).  q_out f16 [m][nq*hd].  C is a power of two.
+// Rotary embedding + KV scatter.  qkv float [m][qkv_stride] holding nq query
+// heads, then nkv key heads and nkv value heads (either group may be empty);
+// rope_cs float2 [max_pos][hd/2] (cos, sin); kv_off int64 [m] (may be null when
+// nkv is 0): byte offset in slab of the row's K (token-major [C][dkv] slot
+// half) or -1 to skip; the row's V goes to the slot's V^T half ([dkv][C]).
+// q_out f16 [m][nq*hd].  C is a power of two.
 void launch_rope_kv(const float* qkv, int qkv_stride, int m, const int32_t* pos,
                     const int64_t* kv_off, const float2* rope_cs, int nq, int nkv, int hd, int C,
                     void* q_out, void* slab, hipStream_t s);

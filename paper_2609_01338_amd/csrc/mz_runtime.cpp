@@ -294,17 +294,18 @@ struct HostArena {
 // ---------------------------------------------------------------- timing
 
 enum KernelKind {
-  kKEmbed, kKRmsnorm, kKGemmQKV, kKRopeKV, kKAttention, kKGemmO, kKGemmGateUp, kKGemmDown,
-  kKGather, kKLmHead, kKCount
+  kKEmbed, kKRmsnorm, kKGemmKV, kKRopeKV, kKGemmQ, kKRopeQ, kKGather, kKAttention, kKGemmO,
+  kKGemmGateUp, kKGemmDown, kKLmHead, kKCount
 };
-const char* kKindName[kKCount] = {"embed_q4", "rmsnorm", "gemm_q4_qkv", "rope_kv", "attention",
-                                  "gemm_q4_o", "gemm_q4_gateup", "gemm_q4_down", "gather_rows",
-                                  "lm_head_argmax"};
+const char* kKindName[kKCount] = {"embed_q4", "rmsnorm", "gemm_q4_kv", "rope_kv", "gemm_q4_q",
+                                  "rope_q", "gather_rows", "attention", "gemm_q4_o",
+                                  "gemm_q4_gateup", "gemm_q4_down", "lm_head_argmax"};
 // HIP kernel symbol each kind launches (to line up with profiler summaries)
 const char* kKindKernel[kKCount] = {"embed_kernel", "rmsnorm_kernel", "gemm_q4_kernel<0>",
-                                    "rope_kv_kernel", "attn_kernel", "gemm_q4_kernel<1>",
+                                    "rope_kv_kernel", "gemm_q4_kernel<0>", "rope_kv_kernel",
+                                    "gather_rows_kernel", "attn_kernel", "gemm_q4_kernel<1>",
                                     "gemm_q4_kernel<2>", "gemm_q4_kernel<1>",
-                                    "gather_rows_kernel", "lm_head_kernel+argmax_kernel"};
+                                    "lm_head_kernel+argmax_kernel"};
 
 struct KindStats {
   int64_t launches = 0;
@@ -329,10 +330,10 @@ struct mz_ctx {
 
   // shapes
   int L = 0, d = 0, nq = 0, nkv = 0, hd = 0, ff = 0, ffp = 0, V = 0, C = 0, max_ctx = 0;
-  int dq = 0, dkv = 0, nqkv = 0, nqkv_pad = 0, d_pad = 0;
+  int dq = 0, dkv = 0, dq_pad = 0, kv_pad = 0, d_pad = 0;
   int max_chunks = 0;
   int64_t slot_bytes = 0;
-  int64_t off_qkv = 0, off_o = 0, off_gu = 0, off_dn = 0, unit_bytes = 0;
+  int64_t off_q = 0, off_kv = 0, off_o = 0, off_gu = 0, off_dn = 0, unit_bytes = 0;
 
   // weights
   uint8_t* w_slab = nullptr;
@@ -361,7 +362,8 @@ struct mz_ctx {
   // activations
   float* h[2] = {nullptr, nullptr};
   void* xb = nullptr;      // f16 [max_ctx][max(d, dq)]: norm output / attention output
-  float* qkv = nullptr;    // [max_ctx][nqkv_pad]
+  float* qf = nullptr;     // [max_ctx][dq_pad]: query projection
+  float* kvf = nullptr;    // [max_ctx][kv_pad]: key and value projections
   void* q16 = nullptr;     // f16 [max_ctx][dq]
   void* act = nullptr;     // f16 [max_ctx][ffp]
   float* logits = nullptr;
@@ -371,9 +373,13 @@ struct mz_ctx {
 
   // restore metadata (device + pinned staging)
   int32_t* d_tables = nullptr;
+  // per layer: rows whose K/V are written (positions, slot offsets, indices
+  // into the layer's input rows) and rows carried on (positions, indices)
   int32_t* d_pos = nullptr;
   int64_t* d_kvoff = nullptr;
-  int32_t* d_gather = nullptr;
+  int32_t* d_dix = nullptr;
+  int32_t* d_posq = nullptr;
+  int32_t* d_qix = nullptr;
   int32_t* d_tok = nullptr;
   uint8_t* h_stage = nullptr;
   size_t stage_bytes = 0;
@@ -393,7 +399,7 @@ struct mz_ctx {
   size_t ev_used = 0;
   std::vector<PendingTiming> pending;
   KindStats kstats[kKCount];
-  std::vector<int32_t> last_nR, last_nD;
+  std::vector<int32_t> last_nR, last_nD, last_nQ;
   int64_t last_swap_kv_bytes = 0, last_swap_w_bytes = 0, last_reload_w_bytes = 0;
   int64_t last_copies = 0;
   double last_swap_ms = -1;
@@ -510,12 +516,6 @@ int64_t blob_bytes(const mz_model_cfg* c) {
   return c->n_layers * layer + 2 * (int64_t)c->vocab * q4_row_bytes(d);
 }
 
-// Run the per-layer path over the rows planned in `rows`.  Metadata must
-// already be staged (see stage_and_upload).
-struct LayerOffsets {
-  std::vector<int64_t> pos_off, gat_off;
-};
-
 }  // namespace
 
 // ---------------------------------------------------------------- restore core
@@ -627,44 +627,56 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
       w_new.push_back(l);
     }
 
-  // --- metadata: tables, positions, KV destinations, compaction, tokens
-  std::vector<int64_t> pos_off(L + 1, 0), gat_off(L, 0);
-  for (int l = 0; l < L; ++l) pos_off[l + 1] = pos_off[l] + rows.nR[l];
-  int64_t n_gat = 0;
-  for (int l = 0; l + 1 < L; ++l) {
-    gat_off[l] = n_gat;
-    n_gat += rows.nR[l + 1];
+  // --- metadata: tables; per layer the rows whose K/V are written (D_l:
+  // position, slot offset, index among the layer's input rows R_l) and the
+  // rows carried on (R_{l+1}, or the last position after the last layer:
+  // position, index in R_l); tokens
+  std::vector<int64_t> dofs(L + 1, 0), qofs(L + 1, 0);
+  std::vector<int32_t> nQ(L);
+  for (int l = 0; l < L; ++l) {
+    nQ[l] = l + 1 < L ? rows.nR[l + 1] : 1;
+    dofs[l + 1] = dofs[l] + rows.nD[l];
+    qofs[l + 1] = qofs[l] + nQ[l];
   }
-  const int64_t tot = pos_off[L];
-  const size_t b_tab = (size_t)L * MC * 4, b_pos = (size_t)tot * 4, b_off = (size_t)tot * 8,
-               b_gat = (size_t)n_gat * 4, b_tok = (size_t)rows.nR[0] * 4;
-  const size_t need = b_tab + b_pos + b_off + b_gat + b_tok + 5 * 256;
+  const size_t b_tab = (size_t)L * MC * 4, b_pos = (size_t)dofs[L] * 4, b_off = (size_t)dofs[L] * 8,
+               b_dix = (size_t)dofs[L] * 4, b_posq = (size_t)qofs[L] * 4, b_qix = (size_t)qofs[L] * 4,
+               b_tok = (size_t)rows.nR[0] * 4;
+  const size_t need = b_tab + b_pos + b_off + b_dix + b_posq + b_qix + b_tok + 7 * 256;
   if (need > x->stage_bytes) fail(MZ_EINVAL, "restore metadata exceeds the staging buffer");
   uint8_t* sp = x->h_stage;
   int32_t* s_tab = (int32_t*)sp;
   int32_t* s_pos = (int32_t*)(sp + round_up(b_tab, 256));
   int64_t* s_off = (int64_t*)((uint8_t*)s_pos + round_up(b_pos, 256));
-  int32_t* s_gat = (int32_t*)((uint8_t*)s_off + round_up(b_off, 256));
-  int32_t* s_tok = (int32_t*)((uint8_t*)s_gat + round_up(b_gat, 256));
+  int32_t* s_dix = (int32_t*)((uint8_t*)s_off + round_up(b_off, 256));
+  int32_t* s_posq = (int32_t*)((uint8_t*)s_dix + round_up(b_dix, 256));
+  int32_t* s_qix = (int32_t*)((uint8_t*)s_posq + round_up(b_posq, 256));
+  int32_t* s_tok = (int32_t*)((uint8_t*)s_qix + round_up(b_qix, 256));
   memcpy(s_tab, x->table.data(), b_tab);
   for (int l = 0; l < L; ++l) {
     const std::vector<int32_t>& R = rows.R[l];
+    int64_t j = dofs[l];
     for (size_t i = 0; i < R.size(); ++i) {
       const int p = R[i];
-      s_pos[pos_off[l] + i] = p;
       const int c = p / C;
-      const bool write = p >= N || x->kv_state[(size_t)l * MC + c] == MZ_DROP;
-      s_off[pos_off[l] + i] =
-          write ? (int64_t)x->table[(size_t)l * MC + c] * x->slot_bytes + (int64_t)(p % C) * x->dkv * 2
-                : -1;
+      if (p >= N || x->kv_state[(size_t)l * MC + c] == MZ_DROP) {
+        s_pos[j] = p;
+        s_off[j] = (int64_t)x->table[(size_t)l * MC + c] * x->slot_bytes + (int64_t)(p % C) * x->dkv * 2;
+        s_dix[j] = (int32_t)i;
+        ++j;
+      }
     }
+    if (j != dofs[l + 1]) fail(MZ_EINVAL, "internal: written-row count mismatch at layer %d", l);
     if (l + 1 < L) {
       const std::vector<int32_t>& Rn = rows.R[l + 1];
       size_t a = 0;
       for (size_t b = 0; b < Rn.size(); ++b) {
         while (R[a] != Rn[b]) ++a;
-        s_gat[gat_off[l] + b] = (int32_t)a;
+        s_posq[qofs[l] + b] = Rn[b];
+        s_qix[qofs[l] + b] = (int32_t)a;
       }
+    } else {
+      s_posq[qofs[l]] = R.back();             // S - 1
+      s_qix[qofs[l]] = (int32_t)R.size() - 1;
     }
   }
   for (int i = 0; i < rows.nR[0]; ++i) {
@@ -673,9 +685,13 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
   }
   hipStream_t cs = x->s_compute, ss = x->s_swap;
   HIPCHK(hipMemcpyAsync(x->d_tables, s_tab, b_tab, hipMemcpyHostToDevice, cs));
-  HIPCHK(hipMemcpyAsync(x->d_pos, s_pos, b_pos, hipMemcpyHostToDevice, cs));
-  HIPCHK(hipMemcpyAsync(x->d_kvoff, s_off, b_off, hipMemcpyHostToDevice, cs));
-  if (b_gat) HIPCHK(hipMemcpyAsync(x->d_gather, s_gat, b_gat, hipMemcpyHostToDevice, cs));
+  if (b_pos) {
+    HIPCHK(hipMemcpyAsync(x->d_pos, s_pos, b_pos, hipMemcpyHostToDevice, cs));
+    HIPCHK(hipMemcpyAsync(x->d_kvoff, s_off, b_off, hipMemcpyHostToDevice, cs));
+    HIPCHK(hipMemcpyAsync(x->d_dix, s_dix, b_dix, hipMemcpyHostToDevice, cs));
+  }
+  HIPCHK(hipMemcpyAsync(x->d_posq, s_posq, b_posq, hipMemcpyHostToDevice, cs));
+  HIPCHK(hipMemcpyAsync(x->d_qix, s_qix, b_qix, hipMemcpyHostToDevice, cs));
   HIPCHK(hipMemcpyAsync(x->d_tok, s_tok, b_tok, hipMemcpyHostToDevice, cs));
 
   if (x->debug_poison) {
@@ -738,52 +754,68 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
   int cur = 0;
   double algo = 2.0 * d * x->V;
   for (int l = 0; l < L; ++l) {
-    const int n = rows.nR[l];
-    const int32_t* pos = x->d_pos + pos_off[l];
-    const int64_t* off = x->d_kvoff + pos_off[l];
+    const int n = rows.nR[l], nd = rows.nD[l], nq = nQ[l];
     if (w_copy[l]) HIPCHK(hipStreamWaitEvent(cs, x->ev_w[l], 0));
     const uint8_t* unit = x->unit_ptr(l);
     float* h = x->h[cur];
     x->timed(kKRmsnorm, 0, (double)n * d * 6.0, cs,
              [&] { mzk::launch_rmsnorm(h, n, d, x->cfg.rms_eps, x->xb, cs); });
-    x->timed(kKGemmQKV, 2.0 * n * d * x->nqkv, (double)x->nqkv * d * bpe_w + n * (d * 2.0 + x->nqkv * 4.0), cs,
-             [&] { mzk::launch_gemm_q4(x->xb, n, x->nqkv_pad, d, unit + x->off_qkv, mzk::kEpiStore, x->qkv, cs); });
     // prompt rows appended to a partial last chunk that was swapped out land in
     // the restored slot: its copy must be done before they are written
     const bool early_wait = kv_copy[l] && P > 0 && N % C != 0 &&
                             x->kv_state[(size_t)l * MC + (nc_old - 1)] == MZ_SWAP;
     if (early_wait) HIPCHK(hipStreamWaitEvent(cs, x->ev_kv[l], 0));
-    x->timed(kKRopeKV, 0, (double)n * (x->nqkv * 4.0 + x->dq * 2.0) + rows.nD[l] * 4.0 * x->dkv, cs, [&] {
-      mzk::launch_rope_kv(x->qkv, x->nqkv_pad, n, pos, off, x->rope_cs, x->nq, x->nkv, x->hd, C,
-                          x->q16, x->kv_slab, cs);
-    });
+    // keys and values of the rows written at this layer (D_l)
+    if (nd > 0) {
+      const int32_t* dix = x->d_dix + dofs[l];
+      x->timed(kKGemmKV, 2.0 * nd * d * 2 * x->dkv, 2.0 * x->dkv * d * bpe_w + nd * (d * 2.0 + 2 * x->dkv * 4.0), cs,
+               [&] { mzk::launch_gemm_q4(x->xb, nd, x->kv_pad, d, unit + x->off_kv, mzk::kEpiStore, x->kvf, cs, dix); });
+      x->timed(kKRopeKV, 0, nd * (2 * x->dkv * 4.0 + 2 * x->dkv * 2.0), cs, [&] {
+        mzk::launch_rope_kv(x->kvf, x->kv_pad, nd, x->d_pos + dofs[l], x->d_kvoff + dofs[l], x->rope_cs, 0,
+                            x->nkv, x->hd, C, nullptr, x->kv_slab, cs);
+      });
+    }
     if (kv_copy[l] && !early_wait) HIPCHK(hipStreamWaitEvent(cs, x->ev_kv[l], 0));
+    // queries, attention and MLP of the rows carried on (R_{l+1}; the last
+    // position after the last layer)
+    const int32_t* qix = x->d_qix + qofs[l];
+    const int32_t* posq = x->d_posq + qofs[l];
+    x->timed(kKGemmQ, 2.0 * nq * d * x->dq, (double)x->dq * d * bpe_w + nq * (d * 2.0 + x->dq * 4.0), cs,
+             [&] { mzk::launch_gemm_q4(x->xb, nq, x->dq_pad, d, unit + x->off_q, mzk::kEpiStore, x->qf, cs, qix); });
+    x->timed(kKRopeQ, 0, nq * (x->dq * 4.0 + x->dq * 2.0), cs, [&] {
+      mzk::launch_rope_kv(x->qf, x->dq_pad, nq, posq, nullptr, x->rope_cs, x->nq, 0, x->hd, C, x->q16,
+                          x->kv_slab, cs);
+    });
+    if (nq < n) {
+      float* dst = x->h[cur ^ 1];
+      x->timed(kKGather, 0, (double)nq * d * 8.0, cs,
+               [&] { mzk::launch_gather_rows(h, qix, nq, d, dst, cs); });
+      cur ^= 1;
+      h = dst;
+    }
     double keys = 0;
-    for (int p : rows.R[l]) keys += p + 1.0;
+    if (l + 1 < L)
+      for (int p : rows.R[l + 1]) keys += p + 1.0;
+    else
+      keys = S;
     const double att_flops = 4.0 * x->hd * x->nq * keys;
-    x->timed(kKAttention, att_flops, (double)n * x->dq * 4.0, cs, [&] {
-      mzk::launch_attention(x->q16, pos, n, x->kv_slab, x->d_tables + (size_t)l * MC, C, x->slot_bytes,
+    x->timed(kKAttention, att_flops, (double)nq * x->dq * 4.0, cs, [&] {
+      mzk::launch_attention(x->q16, posq, nq, x->kv_slab, x->d_tables + (size_t)l * MC, C, x->slot_bytes,
                             x->nq, x->nkv, x->hd, x->xb, cs);
     });
-    x->timed(kKGemmO, 2.0 * n * x->dq * d, (double)d * x->dq * bpe_w + n * (x->dq * 2.0 + d * 8.0), cs,
-             [&] { mzk::launch_gemm_q4(x->xb, n, x->d_pad, x->dq, unit + x->off_o, mzk::kEpiAdd, h, cs); });
-    x->timed(kKRmsnorm, 0, (double)n * d * 6.0, cs,
-             [&] { mzk::launch_rmsnorm(h, n, d, x->cfg.rms_eps, x->xb, cs); });
-    x->timed(kKGemmGateUp, 2.0 * n * d * 2.0 * x->ff, 2.0 * x->ff * d * bpe_w + n * (d * 2.0 + x->ff * 2.0), cs,
-             [&] { mzk::launch_gemm_q4(x->xb, n, 2 * x->ffp, d, unit + x->off_gu, mzk::kEpiSwiGLU, x->act, cs); });
-    x->timed(kKGemmDown, 2.0 * n * x->ff * d, (double)d * x->ff * bpe_w + n * (x->ffp * 2.0 + d * 8.0), cs,
-             [&] { mzk::launch_gemm_q4(x->act, n, x->d_pad, x->ffp, unit + x->off_dn, mzk::kEpiAdd, h, cs); });
-    algo += 2.0 * n * d * 2 * x->dq + 2.0 * rows.nD[l] * d * 2 * x->dkv + 2.0 * n * 3 * d * x->ff + att_flops;
-    if (l + 1 < L && rows.nR[l + 1] < n) {
-      const int nn = rows.nR[l + 1];
-      float* dst = x->h[cur ^ 1];
-      x->timed(kKGather, 0, (double)nn * d * 8.0, cs,
-               [&] { mzk::launch_gather_rows(h, x->d_gather + gat_off[l], nn, d, dst, cs); });
-      cur ^= 1;
-    }
+    x->timed(kKGemmO, 2.0 * nq * x->dq * d, (double)d * x->dq * bpe_w + nq * (x->dq * 2.0 + d * 8.0), cs,
+             [&] { mzk::launch_gemm_q4(x->xb, nq, x->d_pad, x->dq, unit + x->off_o, mzk::kEpiAdd, h, cs); });
+    x->timed(kKRmsnorm, 0, (double)nq * d * 6.0, cs,
+             [&] { mzk::launch_rmsnorm(h, nq, d, x->cfg.rms_eps, x->xb, cs); });
+    x->timed(kKGemmGateUp, 2.0 * nq * d * 2.0 * x->ff, 2.0 * x->ff * d * bpe_w + nq * (d * 2.0 + x->ff * 2.0), cs,
+             [&] { mzk::launch_gemm_q4(x->xb, nq, 2 * x->ffp, d, unit + x->off_gu, mzk::kEpiSwiGLU, x->act, cs); });
+    x->timed(kKGemmDown, 2.0 * nq * x->ff * d, (double)d * x->ff * bpe_w + nq * (x->ffp * 2.0 + d * 8.0), cs,
+             [&] { mzk::launch_gemm_q4(x->act, nq, x->d_pad, x->ffp, unit + x->off_dn, mzk::kEpiAdd, h, cs); });
+    algo += 2.0 * nd * d * 2 * x->dkv + 2.0 * nq * d * 2 * x->dq + 2.0 * nq * 3 * d * x->ff + att_flops;
   }
-  x->h_last = x->h[cur] + (int64_t)(rows.nR[L - 1] - 1) * d;
+  x->h_last = x->h[cur];
   x->have_last = true;
+  x->last_nQ = nQ;
 
   // --- new state: every unit resident, context extended by the prompt
   for (int l = 0; l < L; ++l) {
@@ -841,8 +873,9 @@ mz_status mz_load_model(const mz_model_cfg* cfg, const void* blob, size_t nbytes
     c.L = cfg->n_layers; c.d = cfg->d_model; c.nq = cfg->n_q_heads; c.nkv = cfg->n_kv_heads;
     c.hd = cfg->head_dim; c.ff = cfg->d_ffn; c.V = cfg->vocab; c.C = cfg->chunk_tokens;
     c.max_ctx = cfg->max_ctx;
-    c.dq = c.nq * c.hd; c.dkv = c.nkv * c.hd; c.nqkv = c.dq + 2 * c.dkv;
-    c.nqkv_pad = (int)round_up(c.nqkv, mzk::kGemmTileN);
+    c.dq = c.nq * c.hd; c.dkv = c.nkv * c.hd;
+    c.dq_pad = (int)round_up(c.dq, mzk::kGemmTileN);
+    c.kv_pad = (int)round_up(2 * c.dkv, mzk::kGemmTileN);
     c.d_pad = (int)round_up(c.d, mzk::kGemmTileN);
     if (c.d_pad != c.d) fail(MZ_EINVAL, "d_model must be a multiple of %d", mzk::kGemmTileN);
     c.ffp = (int)round_up(c.ff, mzk::kGemmTileN / 2);
@@ -850,10 +883,12 @@ mz_status mz_load_model(const mz_model_cfg* cfg, const void* blob, size_t nbytes
     c.slot_bytes = (int64_t)c.C * c.dkv * 2 * 2;
 
     // weight unit layout
-    const int64_t b_qkv = gemm_packed_bytes(c.nqkv, c.d), b_o = gemm_packed_bytes(c.d, c.dq),
-                  b_gu = gemm_packed_bytes(2 * (int64_t)c.ffp, c.d), b_dn = gemm_packed_bytes(c.d, c.ffp);
-    c.off_qkv = 0;
-    c.off_o = round_up(b_qkv, 256);
+    const int64_t b_q = gemm_packed_bytes(c.dq, c.d), b_kv = gemm_packed_bytes(2 * c.dkv, c.d),
+                  b_o = gemm_packed_bytes(c.d, c.dq), b_gu = gemm_packed_bytes(2 * (int64_t)c.ffp, c.d),
+                  b_dn = gemm_packed_bytes(c.d, c.ffp);
+    c.off_q = 0;
+    c.off_kv = round_up(b_q, 256);
+    c.off_o = c.off_kv + round_up(b_kv, 256);
     c.off_gu = c.off_o + round_up(b_o, 256);
     c.off_dn = c.off_gu + round_up(b_gu, 256);
     c.unit_bytes = round_up(c.off_dn + b_dn, 4096);
@@ -880,11 +915,12 @@ mz_status mz_load_model(const mz_model_cfg* cfg, const void* blob, size_t nbytes
       uint8_t* u = c.w_image + (int64_t)l * c.unit_bytes;
       memset(u, 0, c.unit_bytes);
       const uint8_t* wq = bp;                                  // Wq, Wk, Wv are consecutive rows
-      const uint8_t* wo = wq + (int64_t)c.nqkv * rb_d;
+      const uint8_t* wo = wq + (int64_t)(c.dq + 2 * c.dkv) * rb_d;
       const uint8_t* wg = wo + (int64_t)c.d * q4_row_bytes(c.dq);
       const uint8_t* wu = wg + (int64_t)c.ff * rb_d;
       const uint8_t* wd = wu + (int64_t)c.ff * rb_d;
-      pack_plain(wq, c.nqkv, c.d, u + c.off_qkv);
+      pack_plain(wq, c.dq, c.d, u + c.off_q);
+      pack_plain(wq + (int64_t)c.dq * rb_d, 2 * c.dkv, c.d, u + c.off_kv);
       pack_plain(wo, c.d, c.dq, u + c.off_o);
       pack_gateup(wg, wu, c.ff, c.d, u + c.off_gu);
       pack_plain(wd, c.d, c.ff, u + c.off_dn);
@@ -941,7 +977,8 @@ mz_status mz_load_model(const mz_model_cfg* cfg, const void* blob, size_t nbytes
     c.h[0] = (float*)dmalloc((size_t)M * c.d * 4);
     c.h[1] = (float*)dmalloc((size_t)M * c.d * 4);
     c.xb = dmalloc((size_t)M * std::max(c.d, c.dq) * 2);
-    c.qkv = (float*)dmalloc((size_t)M * c.nqkv_pad * 4);
+    c.qf = (float*)dmalloc((size_t)M * c.dq_pad * 4);
+    c.kvf = (float*)dmalloc((size_t)M * c.kv_pad * 4);
     c.q16 = dmalloc((size_t)M * c.dq * 2);
     c.act = dmalloc((size_t)M * c.ffp * 2);
     c.logits = (float*)dmalloc((size_t)c.V * 4);
@@ -955,9 +992,11 @@ mz_status mz_load_model(const mz_model_cfg* cfg, const void* blob, size_t nbytes
     c.d_tables = (int32_t*)dmalloc((size_t)c.L * c.max_chunks * 4);
     c.d_pos = (int32_t*)dmalloc((size_t)tot * 4);
     c.d_kvoff = (int64_t*)dmalloc((size_t)tot * 8);
-    c.d_gather = (int32_t*)dmalloc((size_t)tot * 4);
+    c.d_dix = (int32_t*)dmalloc((size_t)tot * 4);
+    c.d_posq = (int32_t*)dmalloc((size_t)tot * 4);
+    c.d_qix = (int32_t*)dmalloc((size_t)tot * 4);
     c.d_tok = (int32_t*)dmalloc((size_t)M * 4);
-    c.stage_bytes = (size_t)c.L * c.max_chunks * 4 + (size_t)tot * 16 + (size_t)M * 4 + 8 * 256;
+    c.stage_bytes = (size_t)c.L * c.max_chunks * 4 + (size_t)tot * 24 + (size_t)M * 4 + 8 * 256;
     void* stage = nullptr;
     if (hipHostMalloc(&stage, c.stage_bytes, hipHostMallocDefault) != hipSuccess || !stage)
       fail(MZ_ENOMEM, "pinned staging allocation failed");
@@ -982,8 +1021,9 @@ void mz_free(mz_ctx* x) {
   if (x->s_compute) (void)hipStreamSynchronize(x->s_compute);
   if (x->s_swap) (void)hipStreamSynchronize(x->s_swap);
   void* dptrs[] = {x->w_slab, x->emb_nib, x->emb_sc, x->lm_nib, x->lm_sc, x->rope_cs, x->kv_slab,
-                   x->h[0], x->h[1], x->xb, x->qkv, x->q16, x->act, x->logits, x->part_val,
-                   x->part_idx, x->d_token, x->d_tables, x->d_pos, x->d_kvoff, x->d_gather, x->d_tok};
+                   x->h[0], x->h[1], x->xb, x->qf, x->kvf, x->q16, x->act, x->logits, x->part_val,
+                   x->part_idx, x->d_token, x->d_tables, x->d_pos, x->d_kvoff, x->d_dix, x->d_posq,
+                   x->d_qix, x->d_tok};
   for (void* p : dptrs)
     if (p) (void)hipFree(p);
   if (x->w_image) (void)hipHostFree(x->w_image);
@@ -1265,6 +1305,7 @@ mz_status mz_stats(mz_ctx* x, char* out, size_t cap) {
     };
     arr("nR", x->last_nR);
     arr("nD", x->last_nD);
+    arr("nQ", x->last_nQ);
     snprintf(buf, sizeof buf,
              "\"swap_kv_bytes\": %lld, \"swap_w_bytes\": %lld, \"reload_w_bytes\": %lld, \"copies\": %lld, "
              "\"swap_ms\": %.6f, \"algo_flops\": %.6e, ",
