@@ -39,10 +39,10 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) void glb_void;
 
-constexpr int BM = 256, BN = kGemmTileN, BK = kGemmTileK;
+constexpr int BN = kGemmTileN, BK = kGemmTileK;
 constexpr int NT = 512;                      // threads
 constexpr int ROW = BK;                      // halves per LDS row (128 B, swizzled)
-constexpr int TILE_HALVES = BM * ROW;        // one 32 KB stage (A and B tiles are both 256 x 64)
+constexpr int B_TILE = BN * ROW;             // one 32 KB weight stage (256 x 64)
 constexpr int A_STAGES = 3, B_STAGES = 2;
 constexpr int NIB_BYTES = BN * BK / 2;       // 8192
 
@@ -80,14 +80,20 @@ __device__ __forceinline__ void dequant_block_to_lds(uint4 nib, uint16_t dbits, 
   }
 }
 
-template <int EPI>
+// BM = 256 (large m) or 64 (few row tiles: four times as many workgroups; the
+// arithmetic of every output element is the same, so results do not depend
+// on the choice).
+template <int EPI, int BM>
 __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict__ X,
                                                      const int32_t* __restrict__ a_rows, int M, int K,
                                                      const uint8_t* __restrict__ Wp, int N,
                                                      void* __restrict__ Y) {
   extern __shared__ __attribute__((aligned(16))) _Float16 lds[];
-  _Float16* As = lds;                                  // [A_STAGES][TILE_HALVES]
-  _Float16* Bs = lds + A_STAGES * TILE_HALVES;         // [B_STAGES][TILE_HALVES]
+  constexpr int A_TILE = BM * ROW;                     // one activation stage
+  constexpr int MI = BM / 64;                          // 16-row MFMA tiles per wave
+  constexpr int RW = BM / 8;                           // activation rows loaded per wave
+  _Float16* As = lds;                                  // [A_STAGES][A_TILE]
+  _Float16* Bs = lds + A_STAGES * A_TILE;              // [B_STAGES][B_TILE]
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -102,14 +108,14 @@ __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict_
   const int mt = t / n_tiles, nt = t % n_tiles;
   const int nk = K / BK;
 
-  // direct A loads: wave w fills rows 32w .. 32w+31 with 4 instructions of 8
-  // rows; lane l lands at LDS (row 8i + l/8, physical column l%8), which holds
-  // logical column (l%8) ^ ((row >> 1) & 7).  Output row r reads activation
-  // row a_rows[r] when a row list is given, else row r.
-  const _Float16* a_src[4];
+  // direct A loads: wave w fills rows RW*w .. RW*w+RW-1 with MI instructions
+  // of 8 rows; lane l lands at LDS (row 8i + l/8, physical column l%8), which
+  // holds logical column (l%8) ^ ((row >> 1) & 7).  Output row r reads
+  // activation row a_rows[r] when a row list is given, else row r.
+  const _Float16* a_src[MI];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int pr = wave * 32 + i * 8 + (lane >> 3);
+  for (int i = 0; i < MI; ++i) {
+    const int pr = wave * RW + i * 8 + (lane >> 3);
     const int lc = (lane & 7) ^ ((pr >> 1) & 7);
     const int r = min(mt * BM + pr, M - 1);
     a_src[i] = X + (size_t)(a_rows ? a_rows[r] : r) * K + lc * 8;
@@ -120,9 +126,9 @@ __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict_
   const int b_row = (tid & 7) | ((tid >> 4) << 3), b_blk = (tid >> 3) & 1;
   const int b_idx = b_row * 2 + b_blk;
 
-  f32x4 acc[4][8];
+  f32x4 acc[MI][8];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < MI; ++i)
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
@@ -135,11 +141,11 @@ __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict_
   typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
   u32x4 rnib;
   uint32_t rsc;
-  const uint32_t a_lds0 = (uint32_t)(uintptr_t)(lds_void*)(As + wave * 32 * ROW);
-  auto load_a = [&](int kt) {            // 4 direct global -> LDS loads per lane
-    const uint32_t base = __builtin_amdgcn_readfirstlane(a_lds0 + (kt % A_STAGES) * TILE_HALVES * 2);
+  const uint32_t a_lds0 = (uint32_t)(uintptr_t)(lds_void*)(As + wave * RW * ROW);
+  auto load_a = [&](int kt) {            // MI direct global -> LDS loads per lane
+    const uint32_t base = __builtin_amdgcn_readfirstlane(a_lds0 + (kt % A_STAGES) * A_TILE * 2);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < MI; ++i)
       // one wait state between the M0 write and the LDS-DMA load that reads it
       asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
                    :: "s"(base + i * 8 * ROW * 2), "v"(a_src[i] + kt * BK) : "memory", "m0");
@@ -169,26 +175,26 @@ __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict_
   for (int kt = 0; kt < nk; ++kt) {
     const bool more_b = kt + 1 < nk, more_a = kt + 2 < nk;
     if (more_b) load_b(kt + 1);
-    const _Float16* Ab = As + (kt % A_STAGES) * TILE_HALVES;
-    const _Float16* Bb = Bs + (kt & 1) * TILE_HALVES;
+    const _Float16* Ab = As + (kt % A_STAGES) * A_TILE;
+    const _Float16* Bb = Bs + (kt & 1) * B_TILE;
 #pragma unroll
     for (int ks = 0; ks < BK / 32; ++ks) {
-      f16x8 a[4];
+      f16x8 a[MI];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        a[i] = *reinterpret_cast<const f16x8*>(Ab + swz(wm * 64 + i * 16 + frag_row, ks * 4 + frag_c));
+      for (int i = 0; i < MI; ++i)
+        a[i] = *reinterpret_cast<const f16x8*>(Ab + swz(wm * (BM / 4) + i * 16 + frag_row, ks * 4 + frag_c));
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const f16x8 bf =
             *reinterpret_cast<const f16x8*>(Bb + swz(wn * 128 + j * 16 + frag_row, ks * 4 + frag_c));
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < MI; ++i)
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[i], bf, acc[i][j], 0, 0, 0);
       }
     }
     if (more_b) {
       asm volatile("s_waitcnt vmcnt(0)" : "+v"(rnib), "+v"(rsc) :: "memory");
-      dequant(Bs + ((kt + 1) & 1) * TILE_HALVES);
+      dequant(Bs + ((kt + 1) & 1) * B_TILE);
     }
     if (more_a) load_a(kt + 2);
     __syncthreads();
@@ -198,10 +204,10 @@ __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict_
   const int col_in = lane & 15;
   const int row_in = (lane >> 4) * 4;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < MI; ++i) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int row = mt * BM + wm * 64 + i * 16 + row_in + r;
+      const int row = mt * BM + wm * (BM / 4) + i * 16 + row_in + r;
       if (row >= M) continue;
       if (EPI == kEpiSwiGLU) {
         _Float16* y = reinterpret_cast<_Float16*>(Y) + (size_t)row * (N / 2);
@@ -226,38 +232,45 @@ __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict_
   }
 }
 
-constexpr size_t kLdsBytes = (size_t)(A_STAGES + B_STAGES) * TILE_HALVES * sizeof(_Float16);
+template <int BM>
+constexpr size_t lds_bytes() {
+  return ((size_t)A_STAGES * BM * ROW + (size_t)B_STAGES * B_TILE) * sizeof(_Float16);
+}
+
+template <int EPI, int BM>
+void launch_bm(const _Float16* X, const int32_t* a_rows, int m, int n, int k, const uint8_t* W, void* y,
+               hipStream_t s) {
+  static const bool lds_ok = [] {   // more than 64 KB of dynamic LDS, once per instantiation
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_q4_kernel<EPI, BM>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes<BM>());
+    return true;
+  }();
+  (void)lds_ok;
+  const int tiles = (n / BN) * ((m + BM - 1) / BM);
+  hipLaunchKernelGGL((gemm_q4_kernel<EPI, BM>), dim3(tiles), dim3(NT), lds_bytes<BM>(), s, X, a_rows, m, k,
+                     W, n, y);
+}
+
+template <int EPI>
+void launch_epi(const _Float16* X, const int32_t* a_rows, int m, int n, int k, const uint8_t* W, void* y,
+                hipStream_t s) {
+  // 256-row tiles unless they leave most of the 256 CUs idle
+  if ((n / BN) * ((m + 255) / 256) < 128)
+    launch_bm<EPI, 64>(X, a_rows, m, n, k, W, y, s);
+  else
+    launch_bm<EPI, 256>(X, a_rows, m, n, k, W, y, s);
+}
 
 }  // namespace
 
 void launch_gemm_q4(const void* x, int m, int n, int k, const void* w, int epilogue, void* y,
                     hipStream_t s, const int32_t* a_rows) {
-  static const bool lds_ok = [] {   // allow more than 64 KB of dynamic LDS, once per process
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_q4_kernel<kEpiStore>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_q4_kernel<kEpiAdd>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_q4_kernel<kEpiSwiGLU>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
-    return true;
-  }();
-  (void)lds_ok;
-  const int tiles = (n / BN) * ((m + BM - 1) / BM);
   const _Float16* X = reinterpret_cast<const _Float16*>(x);
   const uint8_t* W = reinterpret_cast<const uint8_t*>(w);
   switch (epilogue) {
-    case kEpiStore:
-      hipLaunchKernelGGL(gemm_q4_kernel<kEpiStore>, dim3(tiles), dim3(NT), kLdsBytes, s, X, a_rows, m, k, W,
-                         n, y);
-      break;
-    case kEpiAdd:
-      hipLaunchKernelGGL(gemm_q4_kernel<kEpiAdd>, dim3(tiles), dim3(NT), kLdsBytes, s, X, a_rows, m, k, W, n,
-                         y);
-      break;
-    default:
-      hipLaunchKernelGGL(gemm_q4_kernel<kEpiSwiGLU>, dim3(tiles), dim3(NT), kLdsBytes, s, X, a_rows, m, k,
-                         W, n, y);
-      break;
+    case kEpiStore: launch_epi<kEpiStore>(X, a_rows, m, n, k, W, y, s); break;
+    case kEpiAdd: launch_epi<kEpiAdd>(X, a_rows, m, n, k, W, y, s); break;
+    default: launch_epi<kEpiSwiGLU>(X, a_rows, m, n, k, W, y, s); break;
   }
 }
 

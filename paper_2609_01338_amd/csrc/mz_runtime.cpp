@@ -23,6 +23,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <chrono>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -404,6 +405,9 @@ struct mz_ctx {
   int64_t last_copies = 0;
   double last_swap_ms = -1;
   double last_algo_flops = 0;
+  // host time of the last restore: planning + metadata staging until the
+  // first kernel is queued, and the whole call (everything queued)
+  double last_plan_ms = 0, last_enqueue_ms = 0;
   int last_N = 0, last_P = 0;
 
   hipEvent_t get_event() {
@@ -530,6 +534,10 @@ struct CopyJob {
 
 // Shared by mz_restore_and_prefill and mz_prefill_context.
 void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt) {
+  const auto t_entry = std::chrono::steady_clock::now();
+  auto ms_since = [&](std::chrono::steady_clock::time_point t) {
+    return std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t).count();
+  };
   const int L = x->L, C = x->C, MC = x->max_chunks;
   if (n_prompt < 0) fail(MZ_EINVAL, "n_prompt is negative");
   if (n_prompt > 0 && !prompt) fail(MZ_EINVAL, "prompt is NULL");
@@ -745,6 +753,7 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
     if (!x->overlap) HIPCHK(hipStreamWaitEvent(cs, x->ev_swap_end, 0));
   }
 
+  x->last_plan_ms = ms_since(t_entry);
   // --- compute stream: embedding, layers, compaction
   const int d = x->d;
   const double bpe_w = 0.5625;   // Q4_0 bytes per weight
@@ -831,6 +840,7 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
   x->last_reload_w_bytes = reload_w;
   x->last_copies = copies;
   x->last_algo_flops = algo;
+  x->last_enqueue_ms = ms_since(t_entry);
   x->last_N = N;
   x->last_P = P;
   x->last_swap_ms = -1;
@@ -1308,10 +1318,10 @@ mz_status mz_stats(mz_ctx* x, char* out, size_t cap) {
     arr("nQ", x->last_nQ);
     snprintf(buf, sizeof buf,
              "\"swap_kv_bytes\": %lld, \"swap_w_bytes\": %lld, \"reload_w_bytes\": %lld, \"copies\": %lld, "
-             "\"swap_ms\": %.6f, \"algo_flops\": %.6e, ",
+             "\"swap_ms\": %.6f, \"algo_flops\": %.6e, \"host_plan_ms\": %.4f, \"host_enqueue_ms\": %.4f, ",
              (long long)x->last_swap_kv_bytes, (long long)x->last_swap_w_bytes,
              (long long)x->last_reload_w_bytes, (long long)x->last_copies, x->last_swap_ms,
-             x->last_algo_flops);
+             x->last_algo_flops, x->last_plan_ms, x->last_enqueue_ms);
     s += buf;
     snprintf(buf, sizeof buf,
              "\"pool\": {\"kv_slots\": %d, \"kv_slots_used\": %d, \"slot_bytes\": %lld, \"w_units\": %d, "
