@@ -93,6 +93,66 @@ def cpu_baseline(w, blob, plan_nR, sample_rows=64):
                        f"(est. {total:.1f} s per restore)")}
 
 
+def tp_shard_kernels(w, tp):
+    """Row GEMMs and attention at the per-GPU shapes of a tp-way split by KV
+    head (n_q/tp query heads, n_kv/tp KV heads, d_ffn/tp FFN columns; O and
+    down row-split), all S rows, timed through the kernel-level C ABI with HIP
+    events on one stream.  Random Q4_0 weights and activations."""
+    import torch
+    from paper_2609_01338_amd import mz
+    from paper_2609_01338_amd import workloads as W
+    m = w.model
+    S = w.n_ctx + w.n_prompt
+    nq, nkv, ff = m.n_q_heads // tp, m.n_kv_heads // tp, m.d_ffn // tp
+    hd, d, C = m.head_dim, m.d_model, m.chunk_tokens
+    rng = np.random.default_rng(0)
+    st = torch.cuda.current_stream()
+    sp = st.cuda_stream
+    out = {"tp": tp, "rows": S, "n_q_heads": nq, "n_kv_heads": nkv, "ffn_cols": ff}
+
+    def timed(fn, reps=3):
+        fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        for _ in range(reps):
+            fn()
+        e1.record(st)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    x = (torch.randn(S, max(d, ff, nq * hd), device="cuda") * 0.5).to(torch.float16)
+    for name, n, k, epi in [("q", nq * hd, d, 0), ("kv", 2 * nkv * hd, d, 0), ("o", d, nq * hd, 1),
+                            ("gateup", ff, d, 2), ("down", d, ff, 1)]:
+        if epi == 2:
+            g = W.encode_q4_0((rng.standard_normal((n, k)) * 0.02).astype(np.float32))
+            u = W.encode_q4_0((rng.standard_normal((n, k)) * 0.02).astype(np.float32))
+            packed = mz.mz_q4_gemm_pack(g, n, k, w_up=u)
+            n_pad = 2 * ((n + 127) // 128 * 128)
+            y = torch.zeros(S, n_pad // 2, device="cuda", dtype=torch.float16)
+        else:
+            packed = mz.mz_q4_gemm_pack(W.encode_q4_0((rng.standard_normal((n, k)) * 0.02).astype(np.float32)), n, k)
+            n_pad = (n + 255) // 256 * 256
+            y = torch.zeros(S, n_pad, device="cuda")
+        wt = torch.from_numpy(packed).cuda()
+        xa = x[:, :k].contiguous()
+        ms = timed(lambda: mz.mz_q4_gemm(xa.data_ptr(), S, n_pad, k, wt.data_ptr(), epi, y.data_ptr(), sp))
+        flops = 2.0 * S * (2 * n if epi == 2 else n) * k
+        out[f"gemm_{name}"] = {"N": int(2 * n if epi == 2 else n), "K": int(k), "ms": round(ms, 4),
+                               "TFLOPs": round(flops / ms / 1e9, 1)}
+        del wt, y, xa
+    nch = (S + C - 1) // C
+    slab = (torch.randn(nch, 2 * C * nkv * hd, device="cuda") * 1.0).to(torch.float16)
+    table = torch.arange(nch, device="cuda", dtype=torch.int32)
+    q = torch.randn(S, nq * hd, device="cuda").to(torch.float16)
+    pos = torch.arange(S, device="cuda", dtype=torch.int32)
+    o = torch.empty(S, nq * hd, device="cuda", dtype=torch.float16)
+    ms = timed(lambda: mz.mz_attention(q.data_ptr(), pos.data_ptr(), S, slab.data_ptr(), table.data_ptr(), nch, C,
+                                       nq, nkv, hd, o.data_ptr(), sp))
+    flops = 4.0 * nq * hd * S * (S + 1) / 2
+    out["attention"] = {"ms": round(ms, 4), "TFLOPs": round(flops / ms / 1e9, 1)}
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -101,6 +161,7 @@ def main():
     ap.add_argument("--workload", default="8b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-overlap", action="store_true")
+    ap.add_argument("--no-shard", action="store_true", help="skip the per-GPU shard kernel timings")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one plain 1 GiB device copy first (reference for profiler byte counters)")
     args = ap.parse_args()
@@ -109,11 +170,16 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
+    # torch (device buffers of the calibration copy and the shard-kernel
+    # timings) brings its own HIP runtime; initialising it before libmz is
+    # first used makes libmz bind to that same runtime, so one runtime serves
+    # the whole process.
+    import torch
+    torch.cuda.init()
     from paper_2609_01338_amd import mz
     from paper_2609_01338_amd import workloads as W
 
     if args.calibrate_copy:
-        import torch
         src = torch.ones(1 << 28, device="cuda", dtype=torch.float32)
         dst = torch.empty_like(src)
         dst.copy_(src)
@@ -124,6 +190,8 @@ def main():
     w = W.WORKLOADS[args.workload]
     m = w.model
     S = w.n_ctx + w.n_prompt
+    ceilings = mz.mz_probe_ceilings(0)
+    log(f"[bench] measured ceilings: {ceilings}")
     t = time.perf_counter()
     blob = W.make_blob(w)
     log(f"[bench] {w.key}: blob {blob.nbytes / 1e9:.2f} GB in {time.perf_counter() - t:.1f} s")
@@ -184,12 +252,16 @@ def main():
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_MFMA_TFLOPS, 4),
                 "traffic": measured_traffic(dom_name, w.key),
                 "kernel": dom_name, "roles": dom["roles"],
+                "measured_peak": ceilings["mfma_f16_tflops"],
+                "frac_of_measured_peak": round(achieved / ceilings["mfma_f16_tflops"], 4),
                 "avg_launch_ms": round(dom["ms"] / dom["launches"], 5),
                 "flops_per_launch": dom["flops"] / dom["launches"]}
     else:
         achieved = dom["bytes"] / (dom["ms"] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": None, "kernel": dom_name,
+                "measured_peak": ceilings["hbm_copy_gbps"],
+                "frac_of_measured_peak": round(achieved / ceilings["hbm_copy_gbps"], 4),
                 "avg_launch_ms": round(dom["ms"] / dom["launches"], 5)}
     steps = len(ttft)
     kernels_ms_per_step = {k: round(v["ms"] / steps, 3) for k, v in stats["kernels"].items()}
@@ -215,6 +287,7 @@ def main():
                     "copies": stats["copies"], "ms": stats["swap_ms"],
                     "GBps": (round((stats["swap_kv_bytes"] + stats["swap_w_bytes"]) / stats["swap_ms"] / 1e6, 2)
                              if stats["swap_ms"] and stats["swap_ms"] > 0 else None)},
+        "ceilings_measured": ceilings,
         "kernel_ms_per_step": kernels_ms_per_step,
         "kernel_tflops": kernel_tflops,
         "invariant": {"clean_token": clean_tok, "tokens": toks,
@@ -222,6 +295,10 @@ def main():
         "roofline": roof,
     }
     eng.close()
+    if w.model.n_kv_heads % 8 == 0 and not args.no_shard:
+        t = time.perf_counter()
+        out["tp8_shard_kernels"] = tp_shard_kernels(w, 8)
+        log(f"[bench] tp8 shard kernels in {time.perf_counter() - t:.1f} s: {out['tp8_shard_kernels']}")
     if not args.no_cpu_baseline:
         t = time.perf_counter()
         out["cpu_baseline"] = cpu_baseline(w, blob, nR)

@@ -208,6 +208,17 @@ mz_status mz_attention(const void *q_f16, const int32_t *qpos, int32_t m, const 
 mz_status mz_rmsnorm(const void *h_f32, int32_t m, int32_t d, float eps, void *x_f16,
                      void *stream);
 
+/* Ceilings this GPU actually sustains, measured on the spot (not part of the
+ * restore path; for stating measured rates against them): f16 MFMA
+ * throughput with operand bits that keep changing as real data does, a plain
+ * 1 GiB device copy (bytes read + written), and 1 GiB pinned host -> device
+ * and device -> host copies.  Writes JSON
+ * {"mfma_f16_tflops", "hbm_copy_gbps", "h2d_pinned_gbps", "d2h_pinned_gbps"}
+ * into json_out (cap bytes, NUL-terminated).  Allocates and frees about
+ * 2 GiB of device memory and 1 GiB of pinned host memory; takes about a
+ * second.  Errors: MZ_EINVAL (buffer), MZ_ENOMEM / MZ_EHIP (device). */
+mz_status mz_probe_ceilings(int32_t device, char *json_out, size_t cap);
+
 #ifdef __cplusplus
 }
 #endif

@@ -69,4 +69,10 @@ void launch_fill(void* p, int64_t n_words, uint32_t value, hipStream_t s);
 // delays a stream).  Bounded: always exits.
 void launch_spin(int64_t us, hipStream_t s);
 
+// Ceiling probes: blocks x 512 threads of f16 MFMAs with changing operands
+// (out: blocks*512 floats), and a plain copy of `bytes` (multiple of 16).
+double mfma_probe_flops_per_launch(int blocks, int iters);
+void launch_mfma_probe(float* out, int blocks, int iters, hipStream_t s);
+void launch_copy_probe(const void* src, void* dst, int64_t bytes, hipStream_t s);
+
 }  // namespace mzk

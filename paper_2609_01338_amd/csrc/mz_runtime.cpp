@@ -1425,4 +1425,70 @@ mz_status mz_rmsnorm(const void* h, int32_t m, int32_t d, float eps, void* x, vo
   });
 }
 
+mz_status mz_probe_ceilings(int32_t device, char* json_out, size_t cap) {
+  return guarded(nullptr, [&] {
+    if (!json_out || cap < 2) fail(MZ_EINVAL, "json_out is NULL or too small");
+    HIPCHK(hipSetDevice(device));
+    hipStream_t s = nullptr;
+    HIPCHK(hipStreamCreateWithFlags(&s, hipStreamNonBlocking));
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    float* out = nullptr;
+    void *a = nullptr, *b = nullptr, *host = nullptr;
+    auto cleanup = [&] {
+      if (out) (void)hipFree(out);
+      if (a) (void)hipFree(a);
+      if (b) (void)hipFree(b);
+      if (host) (void)hipHostFree(host);
+      if (e0) (void)hipEventDestroy(e0);
+      if (e1) (void)hipEventDestroy(e1);
+      if (s) (void)hipStreamDestroy(s);
+    };
+    try {
+      HIPCHK(hipEventCreate(&e0));
+      HIPCHK(hipEventCreate(&e1));
+      // best of a few timed runs of f(), in ms
+      auto best_ms = [&](int reps, auto&& f) {
+        float best = 1e30f;
+        f();   // warm-up (clocks, code load)
+        for (int r = 0; r < reps; ++r) {
+          HIPCHK(hipEventRecord(e0, s));
+          f();
+          HIPCHK(hipEventRecord(e1, s));
+          HIPCHK(hipEventSynchronize(e1));
+          float ms = 0;
+          HIPCHK(hipEventElapsedTime(&ms, e0, e1));
+          best = std::min(best, ms);
+        }
+        return (double)best;
+      };
+      const int blocks = 2048, iters = 16000;   // ~45 ms per run: long enough for the clock to settle
+      HIPCHK(hipMalloc((void**)&out, (size_t)blocks * 512 * sizeof(float)));
+      const double mfma_ms = best_ms(3, [&] { mzk::launch_mfma_probe(out, blocks, iters, s); });
+      const double tflops = mzk::mfma_probe_flops_per_launch(blocks, iters) / (mfma_ms * 1e-3) / 1e12;
+      const size_t bytes = (size_t)1 << 30;
+      HIPCHK(hipMalloc(&a, bytes));
+      HIPCHK(hipMalloc(&b, bytes));
+      mzk::launch_fill(a, bytes / 4, 0x3C003C00u, s);
+      const double copy_ms = best_ms(3, [&] { mzk::launch_copy_probe(a, b, (int64_t)bytes, s); });
+      HIPCHK(hipHostMalloc(&host, bytes, hipHostMallocDefault));
+      memset(host, 1, bytes);
+      const double h2d_ms = best_ms(3, [&] { HIPCHK(hipMemcpyAsync(a, host, bytes, hipMemcpyHostToDevice, s)); });
+      const double d2h_ms = best_ms(3, [&] { HIPCHK(hipMemcpyAsync(host, b, bytes, hipMemcpyDeviceToHost, s)); });
+      HIPCHK(hipStreamSynchronize(s));
+      char buf[512];
+      snprintf(buf, sizeof buf,
+               "{\"mfma_f16_tflops\": %.1f, \"hbm_copy_gbps\": %.1f, \"h2d_pinned_gbps\": %.2f, "
+               "\"d2h_pinned_gbps\": %.2f}",
+               tflops, 2.0 * bytes / (copy_ms * 1e-3) / 1e9, bytes / (h2d_ms * 1e-3) / 1e9,
+               bytes / (d2h_ms * 1e-3) / 1e9);
+      if (strlen(buf) + 1 > cap) fail(MZ_EINVAL, "json_out buffer too small");
+      memcpy(json_out, buf, strlen(buf) + 1);
+    } catch (...) {
+      cleanup();
+      throw;
+    }
+    cleanup();
+  });
+}
+
 }  // extern "C"

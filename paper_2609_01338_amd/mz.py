@@ -75,6 +75,7 @@ def lib() -> ctypes.CDLL:
         "mz_q4_gemm": ([vp, i32, i32, i32, vp, i32, vp, vp], i32),
         "mz_attention": ([vp, vp, i32, vp, vp, i32, i32, i32, i32, i32, vp, vp], i32),
         "mz_rmsnorm": ([vp, i32, i32, ctypes.c_float, vp, vp], i32),
+        "mz_probe_ceilings": ([i32, ctypes.c_char_p, sz], i32),
     }
     for name, (args, res) in sigs.items():
         f = getattr(L, name)
@@ -239,6 +240,12 @@ def mz_attention(q_ptr: int, qpos_ptr: int, m: int, slab_ptr: int, table_ptr: in
 
 def mz_rmsnorm(h_ptr: int, m: int, d: int, eps: float, x_ptr: int, stream: Optional[int] = None) -> None:
     _check(lib().mz_rmsnorm(h_ptr, m, d, eps, x_ptr, stream), None)
+
+
+def mz_probe_ceilings(device: int = 0) -> dict:
+    buf = ctypes.create_string_buffer(1024)
+    _check(lib().mz_probe_ceilings(device, buf, len(buf)), None)
+    return json.loads(buf.value.decode())
 
 
 class Engine:

@@ -464,3 +464,27 @@ def test_chunk_bytes_match_paper():
     # an 8B-class KV cache at 32K context: 32 layers x 32768 x 1024 x 2 (K,V) x 2 bytes
     m = W.M8B
     assert m.n_layers * 32768 * m.dkv * 2 * 2 == g["kv_bytes_8b_32k"]
+
+
+# ----------------------------------------------------------------------------- f16 operand floor
+
+def test_f16_floor_reduces_to_fp64_oracle():
+    """With the half-precision operand roundings switched off, the floor's
+    prefill is the oracle's clean prefill bit for bit; with them on, it moves
+    the keys and values (so the rounding is really applied) but stays within
+    a few half ulps at this depth."""
+    from oracle.f16_floor import f16_operand_floor, prefix_kv
+    hp = O.Hyper(TINY_W.model)
+    wts = O.Weights(hp, W.make_blob(TINY_W))
+    ctx, _ = W.make_tokens(TINY_W)
+    toks = ctx[:40]
+    K0, V0, h0 = prefix_kv(hp, wts, toks, False)
+    Kc, Vc, lc = O.clean_prefill(hp, wts, toks)
+    for l in range(hp.n_layers):
+        assert np.array_equal(K0[l], Kc[l].astype(np.float64))
+        assert np.array_equal(V0[l], Vc[l].astype(np.float64))
+    assert np.allclose(O.output_logits(hp, wts, h0), lc, rtol=0, atol=0)
+    fl = f16_operand_floor(hp, wts, toks)
+    kmax = max(np.abs(K0[l]).max() for l in range(hp.n_layers))
+    assert fl.shape == (hp.n_layers,) and fl.max() > 0
+    assert fl.max() <= 8 * 2.0 ** -11 * max(1.0, kmax)
