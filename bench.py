@@ -153,6 +153,58 @@ def tp_shard_kernels(w, tp):
     return out
 
 
+def run_ablation(mz, W, eng, w, prompt, clean_logits, recompute_tflops, link_gbps, steps=3):
+    """TTFT of every eviction order x placement at the workload's evicted amount
+    (as many KV chunks and weight units as its own plan evicts), with the
+    planner's estimate beside each, then overlap on/off for two plans."""
+    m = w.model
+    e = eng.ctx
+    base = W.make_plan(w)
+    n_kv = int((base.kv_state != W.RES).sum())
+    n_w = int((base.w_state != W.RES).sum())
+    cfg = mz.make_cfg(m, w.n_ctx + w.n_prompt)
+
+    def ttft_of(kv, ws):
+        ts, err = [], 0.0
+        for step in range(steps + 1):
+            mz.mz_evict(e, kv, ws)
+            t0 = time.perf_counter()
+            mz.mz_restore_and_prefill(e, prompt)
+            tok, logits = mz.mz_first_token(e, m.vocab)
+            dt = time.perf_counter() - t0
+            mz.mz_truncate_context(e, w.n_ctx)
+            if step:
+                ts.append(dt * 1e3)
+            err = max(err, float(np.abs(logits - clean_logits).max()))
+        return statistics.median(ts), err
+
+    rows = []
+    for order in mz.ORDERS:
+        for placement in mz.PLACEMENTS:
+            kv, ws, est = mz.mz_plan_evict(cfg, w.n_ctx, w.n_prompt, n_kv, n_w, order, placement, 1,
+                                           link_gbps * 1e9, recompute_tflops * 1e12)
+            t, err = ttft_of(kv, ws)
+            rows.append({"order": order, "placement": placement, "swap_chunks": int((kv == W.SWAP).sum()),
+                         "drop_chunks": int((kv == W.DROP).sum()), "ttft_ms": round(t, 2),
+                         "est_link_ms": round(est["link_s"] * 1e3, 2),
+                         "est_recompute_ms": round(est["recompute_s"] * 1e3, 2), "max_logit_err_vs_clean": err})
+            log(f"[ablation] {order:14s} {placement:15s} TTFT {t:8.2f} ms (est link {est['link_s'] * 1e3:7.1f}, "
+                f"recompute {est['recompute_s'] * 1e3:7.1f}) swap/drop {rows[-1]['swap_chunks']}/{rows[-1]['drop_chunks']}")
+    overlap = []
+    for placement in ("interleave-2-1", "balanced"):
+        kv, ws, _ = mz.mz_plan_evict(cfg, w.n_ctx, w.n_prompt, n_kv, n_w, "backward-out", placement, 1,
+                                     link_gbps * 1e9, recompute_tflops * 1e12)
+        res = {"placement": placement}
+        for ov in (1, 0):
+            mz.mz_set_option(e, "overlap", ov)
+            res["ttft_ms_overlap" if ov else "ttft_ms_serialized"] = round(ttft_of(kv, ws)[0], 2)
+        mz.mz_set_option(e, "overlap", 1)
+        overlap.append(res)
+        log(f"[ablation] overlap {res}")
+    return {"n_kv_evicted": n_kv, "n_w_evicted": n_w, "link_gbps": link_gbps,
+            "recompute_tflops": recompute_tflops, "plans": rows, "overlap": overlap}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -162,6 +214,11 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-overlap", action="store_true")
     ap.add_argument("--no-shard", action="store_true", help="skip the per-GPU shard kernel timings")
+    ap.add_argument("--ablation", action="store_true",
+                    help="instead of the timed steps: TTFT per eviction order x placement (one JSON line)")
+    ap.add_argument("--recompute-tflops", type=float, default=400.0,
+                    help="recompute rate the balanced placement assumes (partial-layer recompute of a "
+                         "balanced plan runs at about 400 TFLOP/s on MI355X: few rows per GEMM)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one plain 1 GiB device copy first (reference for profiler byte counters)")
     args = ap.parse_args()
@@ -211,6 +268,13 @@ def main():
     clean_tok, clean_logits = mz.mz_first_token(e, m.vocab)
     mz.mz_truncate_context(e, w.n_ctx)
     log(f"[bench] clean prefill of {S} tokens in {time.perf_counter() - t:.2f} s, token {clean_tok}")
+
+    if args.ablation:
+        res = run_ablation(mz, W, eng, w, prompt, clean_logits, args.recompute_tflops,
+                           ceilings["h2d_pinned_gbps"])
+        eng.close()
+        print(json.dumps({"ablation": res, "workload": w.key, "ceilings_measured": ceilings}), flush=True)
+        return
 
     ttft, toks, logit_err = [], [], []
     stats = None

@@ -165,6 +165,55 @@ mz_status mz_plan_rows(const mz_model_cfg *cfg, const uint8_t *kv_state, int32_t
                        int32_t n_ctx, int32_t n_prompt, int32_t *nR, int32_t *nD,
                        int32_t *rows, int64_t rows_cap);
 
+/* ---- eviction planning (host only) ------------------------------------ */
+
+/* Order in which units are evicted (paper Sec. 4.4 for backward-out). */
+typedef enum {
+  MZ_ORDER_BACKWARD_OUT = 0,   /* layer descending, chunk descending */
+  MZ_ORDER_FORWARD_OUT = 1,    /* layer ascending, chunk ascending */
+  MZ_ORDER_RANDOM_OUT = 2,     /* uniform shuffle (Fisher-Yates driven by splitmix64(seed)) */
+  MZ_ORDER_TOKEN_ALIGNED = 3   /* chunk column descending, all layers of a column together */
+} mz_evict_order;
+
+/* Restore path of each evicted KV chunk. */
+typedef enum {
+  MZ_PLACE_BALANCED = 0,       /* each chunk to the path that keeps max(link, recompute) time smallest */
+  MZ_PLACE_ALL_SWAP = 1,
+  MZ_PLACE_ALL_DROP = 2,
+  MZ_PLACE_INTERLEAVE_2_1 = 3  /* rank r in the order dropped iff r mod 3 = 2 */
+} mz_placement;
+
+typedef struct {
+  int32_t n_ctx;               /* cached tokens; chunks per layer = ceil(n_ctx / chunk_tokens) */
+  int32_t n_prompt;            /* prompt tokens of the coming restore (they enter the work model) */
+  int32_t n_kv_evict;          /* KV chunks to evict, the first ones of `order` */
+  int32_t n_w_evict;           /* weight units to evict (always swapped): the last layers, the
+                                  first for MZ_ORDER_FORWARD_OUT */
+  int32_t order;               /* mz_evict_order */
+  int32_t placement;           /* mz_placement */
+  uint64_t seed;               /* MZ_ORDER_RANDOM_OUT */
+  double link_bytes_per_s;     /* host link rate (MZ_PLACE_BALANCED) */
+  double recompute_flops_per_s;/* effective recompute rate (MZ_PLACE_BALANCED) */
+} mz_evict_request;
+
+/* Eviction plan for mz_evict: the paper's hybrid-swap balance (Sec. 4.3)
+ * re-targeted to this engine's two restore paths, the host link (weights and
+ * KV chunks) and GPU recompute (KV chunks), with its forward-in restore
+ * (Sec. 4.4).  The balanced placement walks the evicted KV chunks in order
+ * and gives each to the path that finishes the restore earlier under the
+ * restore's schedule: units arrive over the link layer by layer, and layer
+ * l computes once layer l-1 is done and layer l's units have arrived, its
+ * work being the restore's exact FLOP count for the plan so far (dropping a
+ * chunk at layer l pulls its rows through every layer <= l, so its cost
+ * depends on the rest of the plan).  Outputs (host, caller-owned):
+ * kv_state [n_layers][ceil(n_ctx / chunk_tokens)], w_state [n_layers]
+ * (MZ_RES / MZ_SWAP / MZ_DROP), and est (NULL or 5 doubles: swapped bytes,
+ * restore FLOPs, link seconds, recompute seconds, and the schedule's finish
+ * time in seconds; the times need both rates).  Errors: EINVAL (sizes,
+ * unknown order or placement, non-positive rates for the balanced placement). */
+mz_status mz_plan_evict(const mz_model_cfg *cfg, const mz_evict_request *req, uint8_t *kv_state,
+                        uint8_t *w_state, double *est);
+
 /* Bytes of the device GEMM layout of a Q4_0 matrix [n][k] (n padded to 256,
  * k to 64). */
 int64_t mz_q4_gemm_packed_bytes(int32_t n, int32_t k);

@@ -34,6 +34,7 @@
 #include <vector>
 
 #include "../../include/mz.h"
+#include "mz_internal.h"
 #include "mz_kernels.h"
 
 namespace {
@@ -68,6 +69,31 @@ struct StatusError {
 }
 
 int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+// ---------------------------------------------------------------- weight unit layout
+
+struct UnitLayout {
+  int64_t off_q, off_kv, off_o, off_gu, off_dn, unit_bytes;
+};
+
+int64_t gemm_packed_bytes(int64_t n, int64_t k);
+
+UnitLayout unit_layout(const mz_model_cfg& cfg) {
+  const int64_t d = cfg.d_model, dq = (int64_t)cfg.n_q_heads * cfg.head_dim,
+                dkv = (int64_t)cfg.n_kv_heads * cfg.head_dim,
+                ffp = round_up(cfg.d_ffn, mzk::kGemmTileN / 2);
+  const int64_t b_q = gemm_packed_bytes(dq, d), b_kv = gemm_packed_bytes(2 * dkv, d),
+                b_o = gemm_packed_bytes(d, dq), b_gu = gemm_packed_bytes(2 * ffp, d),
+                b_dn = gemm_packed_bytes(d, ffp);
+  UnitLayout u;
+  u.off_q = 0;
+  u.off_kv = round_up(b_q, 256);
+  u.off_o = u.off_kv + round_up(b_kv, 256);
+  u.off_gu = u.off_o + round_up(b_o, 256);
+  u.off_dn = u.off_gu + round_up(b_gu, 256);
+  u.unit_bytes = round_up(u.off_dn + b_dn, 4096);
+  return u;
+}
 
 // ---------------------------------------------------------------- Q4_0 repacking
 
@@ -522,6 +548,14 @@ int64_t blob_bytes(const mz_model_cfg* c) {
 
 }  // namespace
 
+namespace mzrt {
+int64_t weight_unit_bytes(const mz_model_cfg& cfg) { return unit_layout(cfg).unit_bytes; }
+int64_t kv_slot_bytes(const mz_model_cfg& cfg) {
+  return (int64_t)cfg.chunk_tokens * cfg.n_kv_heads * cfg.head_dim * 2 * 2;
+}
+void set_error(const char* msg) { g_load_error = msg; }
+}  // namespace mzrt
+
 // ---------------------------------------------------------------- restore core
 
 namespace {
@@ -893,15 +927,13 @@ mz_status mz_load_model(const mz_model_cfg* cfg, const void* blob, size_t nbytes
     c.slot_bytes = (int64_t)c.C * c.dkv * 2 * 2;
 
     // weight unit layout
-    const int64_t b_q = gemm_packed_bytes(c.dq, c.d), b_kv = gemm_packed_bytes(2 * c.dkv, c.d),
-                  b_o = gemm_packed_bytes(c.d, c.dq), b_gu = gemm_packed_bytes(2 * (int64_t)c.ffp, c.d),
-                  b_dn = gemm_packed_bytes(c.d, c.ffp);
-    c.off_q = 0;
-    c.off_kv = round_up(b_q, 256);
-    c.off_o = c.off_kv + round_up(b_kv, 256);
-    c.off_gu = c.off_o + round_up(b_o, 256);
-    c.off_dn = c.off_gu + round_up(b_gu, 256);
-    c.unit_bytes = round_up(c.off_dn + b_dn, 4096);
+    const UnitLayout ul = unit_layout(*cfg);
+    c.off_q = ul.off_q;
+    c.off_kv = ul.off_kv;
+    c.off_o = ul.off_o;
+    c.off_gu = ul.off_gu;
+    c.off_dn = ul.off_dn;
+    c.unit_bytes = ul.unit_bytes;
 
     HIPCHK(hipStreamCreateWithFlags(&c.s_compute, hipStreamNonBlocking));
     HIPCHK(hipStreamCreateWithFlags(&c.s_swap, hipStreamNonBlocking));

@@ -1,0 +1,241 @@
+// Eviction planning: which units to evict, in what order, and which restore
+// path each evicted KV chunk takes.
+//
+// The paper balances its two restore paths (in-memory decompression and
+// storage reads) by giving each increment of eviction to the path that keeps
+// both finishing together, with weight layers restricted to one of the paths
+// (Sec. 4.3, hybrid swap and balance preservation), and evicts in
+// backward-out order (Sec. 4.4).  On this engine the two paths are the host
+// link (swap: weights and KV chunks) and GPU recompute (drop: KV chunks
+// only), so the same structure applies with one change: the cost of
+// recomputing a chunk is not a fixed per-unit time.  Dropping chunk c at
+// layer l pulls the rows of c through every layer up to l (they are in R_l'
+// for all l' <= l), so its marginal cost depends on what else of column c is
+// dropped.  The balanced placement therefore prices each candidate with the
+// restore's exact FLOP count for the plan so far.
+//
+// Work model (integers, the restore path's own arithmetic):
+//   R_l = {p < N : column(p) dropped at some l' >= l} U {N..S-1} U {S-1},
+//   D_l = {p < N : column(p) dropped at l} U {N..S-1},
+//   Q_l = R_{l+1} (l < L-1), {S-1} (l = L-1),
+//   F_l = 2|Q_l| d 2dq + 2|D_l| d 2dkv + 2|Q_l| 3 d ff + 4 dq sum_{p in Q_l} (p+1).
+// Time model (the restore's own schedule): the link copies forward-in, layer
+// by layer (the weight unit, then the swapped chunks), so layer l's units
+// have all arrived at A_l = (bytes of layers 0..l) / link rate; layer l's
+// compute starts when layer l-1 is done and its units have arrived:
+//   end_l = max(end_{l-1}, A_l) + F_l / recompute rate,  TTFT ~ end_{L-1}.
+// A KV chunk goes to recompute when that gives the smaller end_{L-1}, else
+// to the link (ties: link).  Times are exact integers in units of
+// 1 / (link rate x recompute rate) seconds (rates rounded to whole bytes/s
+// and FLOP/s, 128-bit arithmetic).
+#include <algorithm>
+#include <cstdint>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/mz.h"
+#include "mz_internal.h"
+
+namespace {
+
+typedef __int128 i128;
+
+struct PlanError {
+  mz_status st;
+  const char* msg;
+};
+
+// splitmix64: the random-out order's generator (published constants).
+uint64_t splitmix64(uint64_t& x) {
+  uint64_t z = (x += 0x9E3779B97F4A7C15ull);
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+struct Work {
+  int L, nc, C, N, P, S;
+  int64_t d, dq, dkv, ff;
+  std::vector<int64_t> rows, psum;   // per column: context rows, sum of (p+1)
+  std::vector<int> md;               // per column: deepest layer that drops it, -1 if none
+  std::vector<int64_t> drop_rows;    // per layer: context rows of columns dropped there
+  int64_t prompt_psum = 0;           // sum of (p+1) over the prompt positions
+
+  Work(const mz_model_cfg& c, int n_ctx, int n_prompt)
+      : L(c.n_layers), nc((n_ctx + c.chunk_tokens - 1) / c.chunk_tokens), C(c.chunk_tokens), N(n_ctx),
+        P(n_prompt), S(n_ctx + n_prompt), d(c.d_model), dq((int64_t)c.n_q_heads * c.head_dim),
+        dkv((int64_t)c.n_kv_heads * c.head_dim), ff(c.d_ffn) {
+    rows.resize(nc);
+    psum.resize(nc);
+    for (int k = 0; k < nc; ++k) {
+      const int64_t p0 = (int64_t)k * C, n = std::min<int64_t>(C, N - p0);
+      rows[k] = n;
+      psum[k] = n * (p0 + 1) + n * (n - 1) / 2;
+    }
+    md.assign(nc, -1);
+    drop_rows.assign(L, 0);
+    for (int64_t p = N; p < S; ++p) prompt_psum += p + 1;
+  }
+
+  // |R_l| and sum_{p in R_l} (p+1)
+  void rset(int l, int64_t& n, int64_t& ps) const {
+    n = P;
+    ps = prompt_psum;
+    for (int k = 0; k < nc; ++k)
+      if (md[k] >= l) {
+        n += rows[k];
+        ps += psum[k];
+      }
+    if (P == 0 && nc > 0 && md[nc - 1] < l) {   // the last position joins every R_l
+      n += 1;
+      ps += S;
+    }
+  }
+
+  int64_t layer_flops(int l) const {
+    int64_t nq, aq;
+    if (l + 1 < L) {
+      rset(l + 1, nq, aq);
+    } else {
+      nq = 1;
+      aq = S;
+    }
+    const int64_t nd = drop_rows[l] + P;
+    return 2 * nq * d * 2 * dq + 2 * nd * d * 2 * dkv + 2 * nq * 3 * d * ff + 4 * dq * aq;
+  }
+  int64_t flops() const {
+    int64_t f = 0;
+    for (int l = 0; l < L; ++l) f += layer_flops(l);
+    return f;
+  }
+  // end of the last layer in units of 1 / (BW * RF) s, given the bytes each
+  // layer brings over the link
+  i128 pipeline_end(const std::vector<int64_t>& layer_bytes, i128 BW, i128 RF) const {
+    i128 arrive = 0, end = 0;
+    for (int l = 0; l < L; ++l) {
+      arrive += (i128)layer_bytes[l] * RF;
+      end = std::max(end, arrive) + (i128)layer_flops(l) * BW;
+    }
+    return end;
+  }
+
+  void drop(int l, int k) {
+    md[k] = std::max(md[k], l);
+    drop_rows[l] += rows[k];
+  }
+  void undrop(int l, int k, int old_md) {
+    md[k] = old_md;
+    drop_rows[l] -= rows[k];
+  }
+};
+
+}  // namespace
+
+extern "C" {
+
+mz_status mz_plan_evict(const mz_model_cfg* cfg, const mz_evict_request* req, uint8_t* kv_state,
+                        uint8_t* w_state, double* est) {
+  try {
+    if (!cfg || !req || !kv_state || !w_state) throw PlanError{MZ_EINVAL, "NULL pointer"};
+    const mz_model_cfg& c = *cfg;
+    if (c.n_layers < 1 || c.chunk_tokens < 1 || req->n_ctx < 1 || req->n_prompt < 0)
+      throw PlanError{MZ_EINVAL, "bad sizes"};
+    Work w(c, req->n_ctx, req->n_prompt);
+    const int L = w.L, nc = w.nc;
+    if (req->n_kv_evict < 0 || req->n_kv_evict > L * nc) throw PlanError{MZ_EINVAL, "n_kv_evict out of range"};
+    if (req->n_w_evict < 0 || req->n_w_evict > L) throw PlanError{MZ_EINVAL, "n_w_evict out of range"};
+    if (req->placement == MZ_PLACE_BALANCED && !(req->link_bytes_per_s >= 1.0 && req->recompute_flops_per_s >= 1.0))
+      throw PlanError{MZ_EINVAL, "balanced placement needs positive rates"};
+
+    // eviction order over the KV units (layer, column)
+    std::vector<std::pair<int, int>> seq;
+    seq.reserve((size_t)L * nc);
+    switch (req->order) {
+      case MZ_ORDER_BACKWARD_OUT:
+        for (int l = L - 1; l >= 0; --l)
+          for (int k = nc - 1; k >= 0; --k) seq.push_back({l, k});
+        break;
+      case MZ_ORDER_FORWARD_OUT:
+        for (int l = 0; l < L; ++l)
+          for (int k = 0; k < nc; ++k) seq.push_back({l, k});
+        break;
+      case MZ_ORDER_TOKEN_ALIGNED:
+        for (int k = nc - 1; k >= 0; --k)
+          for (int l = L - 1; l >= 0; --l) seq.push_back({l, k});
+        break;
+      case MZ_ORDER_RANDOM_OUT: {
+        for (int l = L - 1; l >= 0; --l)
+          for (int k = nc - 1; k >= 0; --k) seq.push_back({l, k});
+        uint64_t x = req->seed;
+        for (size_t i = seq.size() - 1; i > 0; --i) {   // Fisher-Yates
+          const size_t j = (size_t)(splitmix64(x) % (uint64_t)(i + 1));
+          std::swap(seq[i], seq[j]);
+        }
+        break;
+      }
+      default:
+        throw PlanError{MZ_EINVAL, "unknown order"};
+    }
+
+    memset(kv_state, MZ_RES, (size_t)L * nc);
+    memset(w_state, MZ_RES, (size_t)L);
+    const int64_t slot = mzrt::kv_slot_bytes(c), unit = mzrt::weight_unit_bytes(c);
+    int64_t link_bytes = 0;
+    std::vector<int64_t> layer_bytes(L, 0);
+    // weight units ride the link: the last layers, or the first for forward-out
+    for (int i = 0; i < req->n_w_evict; ++i) {
+      const int l = req->order == MZ_ORDER_FORWARD_OUT ? i : L - 1 - i;
+      w_state[l] = MZ_SWAP;
+      link_bytes += unit;
+      layer_bytes[l] += unit;
+    }
+    const i128 BW = (i128)(int64_t)(req->link_bytes_per_s + 0.5);
+    const i128 RF = (i128)(int64_t)(req->recompute_flops_per_s + 0.5);
+    int64_t f_cur = w.flops();
+    for (int r = 0; r < req->n_kv_evict; ++r) {
+      const int l = seq[r].first, k = seq[r].second;
+      bool drop = false;
+      switch (req->placement) {
+        case MZ_PLACE_ALL_SWAP: drop = false; break;
+        case MZ_PLACE_ALL_DROP: drop = true; break;
+        case MZ_PLACE_INTERLEAVE_2_1: drop = r % 3 == 2; break;
+        case MZ_PLACE_BALANCED: {
+          layer_bytes[l] += slot;
+          const i128 if_swap = w.pipeline_end(layer_bytes, BW, RF);
+          layer_bytes[l] -= slot;
+          const int old = w.md[k];
+          w.drop(l, k);
+          const i128 if_drop = w.pipeline_end(layer_bytes, BW, RF);
+          w.undrop(l, k, old);
+          drop = if_drop < if_swap;
+          break;
+        }
+        default:
+          throw PlanError{MZ_EINVAL, "unknown placement"};
+      }
+      if (drop) {
+        kv_state[(size_t)l * nc + k] = MZ_DROP;
+        w.drop(l, k);
+        f_cur = w.flops();
+      } else {
+        kv_state[(size_t)l * nc + k] = MZ_SWAP;
+        link_bytes += slot;
+        layer_bytes[l] += slot;
+      }
+    }
+    if (est) {
+      est[0] = (double)link_bytes;
+      est[1] = (double)f_cur;
+      est[2] = BW > 0 ? (double)link_bytes / (double)BW : 0.0;
+      est[3] = RF > 0 ? (double)f_cur / (double)RF : 0.0;
+      est[4] = BW > 0 && RF > 0 ? (double)w.pipeline_end(layer_bytes, BW, RF) / ((double)BW * (double)RF) : 0.0;
+    }
+    return MZ_OK;
+  } catch (const PlanError& e) {
+    mzrt::set_error(e.msg);
+    return e.st;
+  }
+}
+
+}  // extern "C"

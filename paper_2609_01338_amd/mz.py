@@ -43,6 +43,16 @@ class mz_evict_plan(ctypes.Structure):
                 ("order", ctypes.c_void_p), ("n_order", ctypes.c_int32)]
 
 
+class mz_evict_request(ctypes.Structure):
+    _fields_ = [("n_ctx", ctypes.c_int32), ("n_prompt", ctypes.c_int32), ("n_kv_evict", ctypes.c_int32),
+                ("n_w_evict", ctypes.c_int32), ("order", ctypes.c_int32), ("placement", ctypes.c_int32),
+                ("seed", ctypes.c_uint64), ("link_bytes_per_s", ctypes.c_double),
+                ("recompute_flops_per_s", ctypes.c_double)]
+
+
+ORDERS = {"backward-out": 0, "forward-out": 1, "random-out": 2, "token-aligned": 3}
+PLACEMENTS = {"balanced": 0, "all-swap": 1, "all-drop": 2, "interleave-2-1": 3}
+
 _lib = None
 
 
@@ -76,6 +86,7 @@ def lib() -> ctypes.CDLL:
         "mz_attention": ([vp, vp, i32, vp, vp, i32, i32, i32, i32, i32, vp, vp], i32),
         "mz_rmsnorm": ([vp, i32, i32, ctypes.c_float, vp, vp], i32),
         "mz_probe_ceilings": ([i32, ctypes.c_char_p, sz], i32),
+        "mz_plan_evict": ([ctypes.POINTER(mz_model_cfg), ctypes.POINTER(mz_evict_request), vp, vp, vp], i32),
     }
     for name, (args, res) in sigs.items():
         f = getattr(L, name)
@@ -186,6 +197,24 @@ def mz_last_error(ctx=None) -> str:
 
 
 # ----------------------------------------------------------------------------- host helpers
+
+def mz_plan_evict(cfg: mz_model_cfg, n_ctx: int, n_prompt: int, n_kv_evict: int, n_w_evict: int,
+                  order: str = "backward-out", placement: str = "balanced", seed: int = 0,
+                  link_bytes_per_s: float = 0.0, recompute_flops_per_s: float = 0.0):
+    """Eviction plan (kv_state [L][n_chunks] uint8, w_state [L] uint8) and the
+    estimate dict {swap_bytes, restore_flops, link_s, recompute_s, pipeline_s}."""
+    L = cfg.n_layers
+    nc = (n_ctx + cfg.chunk_tokens - 1) // cfg.chunk_tokens
+    req = mz_evict_request(n_ctx, n_prompt, n_kv_evict, n_w_evict, ORDERS[order], PLACEMENTS[placement],
+                           seed, link_bytes_per_s, recompute_flops_per_s)
+    kv = np.empty((L, nc), np.uint8)
+    ws = np.empty(L, np.uint8)
+    est = np.empty(5, np.float64)
+    _check(lib().mz_plan_evict(ctypes.byref(cfg), ctypes.byref(req), kv.ctypes.data, ws.ctypes.data,
+                               est.ctypes.data), None)
+    return kv, ws, {"swap_bytes": est[0], "restore_flops": est[1], "link_s": est[2], "recompute_s": est[3],
+                    "pipeline_s": est[4]}
+
 
 def mz_plan_rows(cfg: mz_model_cfg, kv_state: np.ndarray, n_ctx: int, n_prompt: int,
                  with_rows: bool = True):
