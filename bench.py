@@ -190,6 +190,21 @@ def run_ablation(mz, W, eng, w, prompt, clean_logits, recompute_tflops, link_gbp
                          "est_recompute_ms": round(est["recompute_s"] * 1e3, 2), "max_logit_err_vs_clean": err})
             log(f"[ablation] {order:14s} {placement:15s} TTFT {t:8.2f} ms (est link {est['link_s'] * 1e3:7.1f}, "
                 f"recompute {est['recompute_s'] * 1e3:7.1f}) swap/drop {rows[-1]['swap_chunks']}/{rows[-1]['drop_chunks']}")
+    codec_rows = []
+    mz.mz_set_option(e, "kv_codec", 1)
+    for placement in ("balanced", "all-swap", "interleave-2-1"):
+        kv, ws, est = mz.mz_plan_evict(cfg, w.n_ctx, w.n_prompt, n_kv, n_w, "backward-out", placement, 1,
+                                       link_gbps * 1e9, recompute_tflops * 1e12, kv_codec=True)
+        t, err = ttft_of(kv, ws)
+        codec_rows.append({"order": "backward-out", "placement": placement, "kv_codec": True,
+                           "swap_chunks": int((kv == W.SWAP).sum()), "drop_chunks": int((kv == W.DROP).sum()),
+                           "ttft_ms": round(t, 2), "est_link_ms": round(est["link_s"] * 1e3, 2),
+                           "est_recompute_ms": round(est["recompute_s"] * 1e3, 2),
+                           "max_logit_err_vs_clean": err})
+        log(f"[ablation] codec backward-out {placement:15s} TTFT {t:8.2f} ms (est link {est['link_s'] * 1e3:7.1f}, "
+            f"recompute {est['recompute_s'] * 1e3:7.1f}) swap/drop {codec_rows[-1]['swap_chunks']}/"
+            f"{codec_rows[-1]['drop_chunks']} max|logit - clean| {err:.3e}")
+    mz.mz_set_option(e, "kv_codec", 0)
     overlap = []
     for placement in ("interleave-2-1", "balanced"):
         kv, ws, _ = mz.mz_plan_evict(cfg, w.n_ctx, w.n_prompt, n_kv, n_w, "backward-out", placement, 1,
@@ -202,7 +217,7 @@ def run_ablation(mz, W, eng, w, prompt, clean_logits, recompute_tflops, link_gbp
         overlap.append(res)
         log(f"[ablation] overlap {res}")
     return {"n_kv_evicted": n_kv, "n_w_evicted": n_w, "link_gbps": link_gbps,
-            "recompute_tflops": recompute_tflops, "plans": rows, "overlap": overlap}
+            "recompute_tflops": recompute_tflops, "plans": rows, "codec_plans": codec_rows, "overlap": overlap}
 
 
 def main():

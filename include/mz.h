@@ -132,7 +132,12 @@ mz_status mz_first_token(mz_ctx *ctx, int32_t *token_out, float *logits_out);
 /* Engine options: "overlap" (1: swap-in overlapped with compute, default;
  * 0: every copy finishes before compute starts), "kernel_timing" (1: time
  * every kernel launch with HIP events on its stream; setting it clears the
- * accumulated kernel statistics).  Test hooks: "debug_poison" (1: fill every
+ * accumulated kernel statistics), "kv_codec" (1: mz_evict compresses every
+ * full swapped KV chunk with the 8-bit codec of mz_kv_compress and restores
+ * it through mz_kv_decompress -- about half the host-link bytes, values
+ * rounded to the codec's grid; partial chunks and weight units move raw;
+ * enabling it the first time allocates a device staging ring of one layer's
+ * chunks).  Test hooks: "debug_poison" (1: fill every
  * slot and weight unit allocated by a restore with NaN before it is
  * restored or recomputed), "debug_swap_delay_us" (delay the swap stream by a
  * bounded busy wait before its copies).  EINVAL for an unknown key. */
@@ -194,6 +199,7 @@ typedef struct {
   uint64_t seed;               /* MZ_ORDER_RANDOM_OUT */
   double link_bytes_per_s;     /* host link rate (MZ_PLACE_BALANCED) */
   double recompute_flops_per_s;/* effective recompute rate (MZ_PLACE_BALANCED) */
+  int32_t kv_codec;            /* 1: full chunks cross the link compressed (option "kv_codec") */
 } mz_evict_request;
 
 /* Eviction plan for mz_evict: the paper's hybrid-swap balance (Sec. 4.3)
@@ -256,6 +262,17 @@ mz_status mz_attention(const void *q_f16, const int32_t *qpos, int32_t m, const 
 /* x = h / sqrt(mean(h^2) + eps) per row: h float [m][d] -> x f16 [m][d]. */
 mz_status mz_rmsnorm(const void *h_f32, int32_t m, int32_t d, float eps, void *x_f16,
                      void *stream);
+
+/* 8-bit group-wise codec of the swap path (paper Sec. 5: 8-bit quantization
+ * as the default KV codec).  On n_halves IEEE halves (a positive multiple of
+ * 64), in groups of 64 consecutive values: mn, mx = min, max;
+ * d = half(fp32(mx - mn) / 255); q = d == 0 ? 0 : clamp(rint(fp32(x - mn) /
+ * fp32(d)), 0, 255) (correctly rounded division, ties to even);
+ * x^ = half(fp32(q) * fp32(d) + fp32(mn)).  Compressed layout (device, caller
+ * owned): n_halves code bytes, then (mn, d) as two halves per group, i.e.
+ * n_halves + n_halves / 16 bytes.  Enqueued on stream. */
+mz_status mz_kv_compress(const void *src_f16, int64_t n_halves, void *out, void *stream);
+mz_status mz_kv_decompress(const void *in, int64_t n_halves, void *dst_f16, void *stream);
 
 /* Ceilings this GPU actually sustains, measured on the spot (not part of the
  * restore path; for stating measured rates against them): f16 MFMA

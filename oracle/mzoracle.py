@@ -359,10 +359,13 @@ class OracleContext:
 
     # -- eviction (idle phase)
     def evict(self, kv_state: np.ndarray, w_state: Optional[np.ndarray] = None,
-              order: Optional[Sequence[Tuple[str, int, int]]] = None):
+              order: Optional[Sequence[Tuple[str, int, int]]] = None, codec: bool = False):
         """Apply a plan.  Units are visited in `order` (default backward-out:
         last layer first; within a layer its KV chunks from the last, then its
-        weight unit), each moving RES -> SWAP / DROP or SWAP -> DROP."""
+        weight unit), each moving RES -> SWAP / DROP or SWAP -> DROP.  With
+        codec, a swapped chunk holding chunk_tokens positions is kept in the
+        8-bit swap codec's form (oracle/kv_codec.py) and comes back as its
+        round trip; partial chunks are kept as they are."""
         L = self.hp.n_layers
         nc = self.kv_state.shape[1]
         kv_state = np.asarray(kv_state, dtype=np.uint8)
@@ -382,7 +385,11 @@ class OracleContext:
                 if tgt == SWAP and cur == DROP:
                     raise RuntimeError("cannot swap a dropped chunk")
                 if tgt == SWAP:
-                    self.host_kv[(l, c)] = (self.chunks[l][c][0].copy(), self.chunks[l][c][1].copy())
+                    k, v = self.chunks[l][c][0].copy(), self.chunks[l][c][1].copy()
+                    if codec and (c + 1) * self.C <= self.n_ctx:
+                        from .kv_codec import roundtrip_chunk
+                        k, v = roundtrip_chunk(k, v)
+                    self.host_kv[(l, c)] = (k, v)
                     self.swap_log.append(("kv", l, c))
                 else:
                     self.host_kv.pop((l, c), None)

@@ -101,7 +101,7 @@ def eviction_sequence(L: int, nc: int, order: str, seed: int = 0) -> List[Tuple[
 
 def plan_evict(L: int, d: int, dq: int, dkv: int, ff: int, chunk: int, n_ctx: int, n_prompt: int,
                n_kv: int, n_w: int, order: str, placement: str, seed: int, link_rate: float,
-               recompute_rate: float, slot_bytes: int, unit_bytes: int):
+               recompute_rate: float, slot_bytes: int, unit_bytes: int, codec: bool = False):
     """(kv_state [L][nc], w_state [L], swapped bytes, restore FLOPs)."""
     nc = (n_ctx + chunk - 1) // chunk
     kv = np.full((L, nc), RES, np.uint8)
@@ -116,6 +116,10 @@ def plan_evict(L: int, d: int, dq: int, dkv: int, ff: int, chunk: int, n_ctx: in
     bw = int(link_rate + 0.5)
     rf = int(recompute_rate + 0.5)
     seq = eviction_sequence(L, nc, order, seed)
+    # a full chunk crosses the link compressed with the codec: n halves take
+    # n + n / 16 bytes (oracle/kv_codec.py)
+    chunk_bytes = lambda c: (slot_bytes // 2 + slot_bytes // 32
+                             if codec and (c + 1) * chunk <= n_ctx else slot_bytes)
     per_layer = lambda plan: layer_flops(L, d, dq, dkv, ff, plan, n_ctx, n_prompt, chunk)
     f_cur = sum(per_layer(kv))
     for r in range(n_kv):
@@ -128,7 +132,7 @@ def plan_evict(L: int, d: int, dq: int, dkv: int, ff: int, chunk: int, n_ctx: in
             drop = r % 3 == 2
         elif placement == "balanced":
             with_swap = list(layer_bytes)
-            with_swap[l] += slot_bytes
+            with_swap[l] += chunk_bytes(c)
             if_swap = schedule_end(with_swap, per_layer(kv), bw, rf)
             trial = kv.copy()
             trial[l, c] = DROP
@@ -141,6 +145,6 @@ def plan_evict(L: int, d: int, dq: int, dkv: int, ff: int, chunk: int, n_ctx: in
             f_cur = sum(per_layer(kv))
         else:
             kv[l, c] = SWAP
-            link += slot_bytes
-            layer_bytes[l] += slot_bytes
+            link += chunk_bytes(c)
+            layer_bytes[l] += chunk_bytes(c)
     return kv, ws, link, f_cur

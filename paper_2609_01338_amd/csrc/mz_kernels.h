@@ -75,4 +75,15 @@ double mfma_probe_flops_per_launch(int blocks, int iters);
 void launch_mfma_probe(float* out, int blocks, int iters, hipStream_t s);
 void launch_copy_probe(const void* src, void* dst, int64_t bytes, hipStream_t s);
 
+// 8-bit group-wise KV codec (groups of 64 halves; compressed run = n code
+// bytes, then (min, step) halves per group).  n_runs runs of n_halves each:
+// run r is read from src_base + (src_slots ? src_slots[r] : r) * src_stride
+// and written to dst + r * kv_compressed_bytes(n_halves); decompression the
+// other way round (dst_base + (dst_slots ? dst_slots[r] : r) * dst_stride).
+int64_t kv_compressed_bytes(int64_t n_halves);
+void launch_kv_compress(const void* src_base, const int32_t* src_slots, int64_t src_stride, int64_t n_halves,
+                        int n_runs, void* dst, hipStream_t s);
+void launch_kv_decompress(const void* src, int64_t n_halves, int n_runs, void* dst_base,
+                          const int32_t* dst_slots, int64_t dst_stride, hipStream_t s);
+
 }  // namespace mzk

@@ -421,6 +421,14 @@ struct mz_ctx {
   bool overlap = true;
   int64_t debug_swap_delay_us = 0;   // test hook: delay the swap stream before its copies
   bool debug_poison = false;         // test hook: NaN-fill every freshly allocated unit
+  // 8-bit codec on the swap path (option kv_codec): full chunks are compressed
+  // into a device staging ring before the copy to host and decompressed from
+  // it after the copy back
+  bool kv_codec = false;
+  int64_t comp_bytes = 0;            // compressed size of one chunk
+  uint8_t* codec_stage = nullptr;    // [max_chunks][comp_bytes]
+  int32_t* d_codec_slots = nullptr;  // per restore: destination slot of each compressed chunk
+  hipEvent_t ev_meta = nullptr;      // restore metadata uploaded (the swap stream reads some)
   bool timing = false;
   std::vector<hipEvent_t> ev_pool;
   size_t ev_used = 0;
@@ -592,19 +600,45 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
 
   // --- allocate slots: swapped chunks first, in runs matching their arena order
   std::vector<std::vector<CopyJob>> kv_jobs(L);
+  // compressed chunks: copies of arena runs into the staging ring (in the
+  // layer's compressed order) and the slot each one decompresses into
+  std::vector<std::vector<CopyJob>> codec_jobs(L);
+  std::vector<std::vector<int32_t>> codec_slots(L);
   std::vector<int> new_slots;   // for rollback on failure
   auto rollback = [&]() {
     for (int s : new_slots) x->kv_pool.release(s);
   };
   try {
     for (int l = 0; l < L; ++l) {
-      std::vector<int> sw;
+      std::vector<int> sw, swc;
       for (int c = 0; c < nc_old; ++c)
-        if (x->kv_state[(size_t)l * MC + c] == MZ_SWAP) sw.push_back(c);
-      std::sort(sw.begin(), sw.end(), [&](int a, int b) {
+        if (x->kv_state[(size_t)l * MC + c] == MZ_SWAP)
+          (x->kv_entry[(size_t)l * MC + c].bytes == (size_t)x->slot_bytes ? sw : swc).push_back(c);
+      auto by_arena = [&](int a, int b) {
         const ArenaEntry &ea = x->kv_entry[(size_t)l * MC + a], &eb = x->kv_entry[(size_t)l * MC + b];
         return ea.seg != eb.seg ? ea.seg < eb.seg : ea.off < eb.off;
-      });
+      };
+      std::sort(swc.begin(), swc.end(), by_arena);
+      for (size_t i = 0; i < swc.size();) {
+        size_t j = i + 1;
+        while (j < swc.size()) {
+          const ArenaEntry &p = x->kv_entry[(size_t)l * MC + swc[j - 1]], &q = x->kv_entry[(size_t)l * MC + swc[j]];
+          if (q.seg != p.seg || q.off != p.off + p.bytes) break;
+          ++j;
+        }
+        codec_jobs[l].push_back({x->codec_stage + (int64_t)i * x->comp_bytes,
+                                 x->arena.ptr(x->kv_entry[(size_t)l * MC + swc[i]]),
+                                 (size_t)(j - i) * (size_t)x->comp_bytes});
+        i = j;
+      }
+      for (int c : swc) {
+        const int sl = x->kv_pool.alloc_one();
+        if (sl < 0) fail(MZ_ENOMEM, "KV slot pool exhausted");
+        x->table[(size_t)l * MC + c] = sl;
+        new_slots.push_back(sl);
+        codec_slots[l].push_back(sl);
+      }
+      std::sort(sw.begin(), sw.end(), by_arena);
       size_t i = 0;
       while (i < sw.size()) {
         size_t j = i + 1;
@@ -673,7 +707,8 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
   // position, slot offset, index among the layer's input rows R_l) and the
   // rows carried on (R_{l+1}, or the last position after the last layer:
   // position, index in R_l); tokens
-  std::vector<int64_t> dofs(L + 1, 0), qofs(L + 1, 0);
+  std::vector<int64_t> dofs(L + 1, 0), qofs(L + 1, 0), cofs(L + 1, 0);
+  for (int l = 0; l < L; ++l) cofs[l + 1] = cofs[l] + (int64_t)codec_slots[l].size();
   std::vector<int32_t> nQ(L);
   for (int l = 0; l < L; ++l) {
     nQ[l] = l + 1 < L ? rows.nR[l + 1] : 1;
@@ -682,8 +717,8 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
   }
   const size_t b_tab = (size_t)L * MC * 4, b_pos = (size_t)dofs[L] * 4, b_off = (size_t)dofs[L] * 8,
                b_dix = (size_t)dofs[L] * 4, b_posq = (size_t)qofs[L] * 4, b_qix = (size_t)qofs[L] * 4,
-               b_tok = (size_t)rows.nR[0] * 4;
-  const size_t need = b_tab + b_pos + b_off + b_dix + b_posq + b_qix + b_tok + 7 * 256;
+               b_tok = (size_t)rows.nR[0] * 4, b_cs = (size_t)cofs[L] * 4;
+  const size_t need = b_tab + b_pos + b_off + b_dix + b_posq + b_qix + b_tok + b_cs + 8 * 256;
   if (need > x->stage_bytes) fail(MZ_EINVAL, "restore metadata exceeds the staging buffer");
   uint8_t* sp = x->h_stage;
   int32_t* s_tab = (int32_t*)sp;
@@ -693,6 +728,10 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
   int32_t* s_posq = (int32_t*)((uint8_t*)s_dix + round_up(b_dix, 256));
   int32_t* s_qix = (int32_t*)((uint8_t*)s_posq + round_up(b_posq, 256));
   int32_t* s_tok = (int32_t*)((uint8_t*)s_qix + round_up(b_qix, 256));
+  int32_t* s_cs = (int32_t*)((uint8_t*)s_tok + round_up(b_tok, 256));
+  for (int l = 0; l < L; ++l)
+    if (!codec_slots[l].empty())
+      memcpy(s_cs + cofs[l], codec_slots[l].data(), codec_slots[l].size() * 4);
   memcpy(s_tab, x->table.data(), b_tab);
   for (int l = 0; l < L; ++l) {
     const std::vector<int32_t>& R = rows.R[l];
@@ -735,6 +774,10 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
   HIPCHK(hipMemcpyAsync(x->d_posq, s_posq, b_posq, hipMemcpyHostToDevice, cs));
   HIPCHK(hipMemcpyAsync(x->d_qix, s_qix, b_qix, hipMemcpyHostToDevice, cs));
   HIPCHK(hipMemcpyAsync(x->d_tok, s_tok, b_tok, hipMemcpyHostToDevice, cs));
+  if (b_cs) {
+    HIPCHK(hipMemcpyAsync(x->d_codec_slots, s_cs, b_cs, hipMemcpyHostToDevice, cs));
+    HIPCHK(hipEventRecord(x->ev_meta, cs));
+  }
 
   if (x->debug_poison) {
     // fresh slots hold fp16 NaN until restored or recomputed: a missed row or
@@ -759,9 +802,11 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
   int64_t swap_kv = 0, swap_w = 0, reload_w = 0, copies = 0;
   x->swap_timed = false;
   bool any_copy = false;
-  for (int l = 0; l < L; ++l) any_copy |= x->w_state[l] != MZ_RES || !kv_jobs[l].empty();
+  for (int l = 0; l < L; ++l)
+    any_copy |= x->w_state[l] != MZ_RES || !kv_jobs[l].empty() || !codec_jobs[l].empty();
   if (any_copy) {
     HIPCHK(hipEventRecord(x->ev_swap_start, ss));
+    if (b_cs) HIPCHK(hipStreamWaitEvent(ss, x->ev_meta, 0));   // slot lists of the decompressions
     for (int l = 0; l < L; ++l) {
       if (x->w_state[l] != MZ_RES) {
         const void* src = x->w_state[l] == MZ_SWAP ? (const void*)x->arena.ptr(x->w_entry[l])
@@ -777,7 +822,17 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
         swap_kv += j.bytes;
         ++copies;
       }
-      if (!kv_jobs[l].empty()) {
+      for (const CopyJob& j : codec_jobs[l]) {
+        HIPCHK(hipMemcpyAsync(j.dst, j.src, j.bytes, hipMemcpyHostToDevice, ss));
+        swap_kv += j.bytes;
+        ++copies;
+      }
+      if (!codec_slots[l].empty()) {
+        mzk::launch_kv_decompress(x->codec_stage, x->slot_bytes / 2, (int)codec_slots[l].size(), x->kv_slab,
+                                  x->d_codec_slots + cofs[l], x->slot_bytes, ss);
+        HIPCHK(hipGetLastError());
+      }
+      if (!kv_jobs[l].empty() || !codec_slots[l].empty()) {
         HIPCHK(hipEventRecord(x->ev_kv[l], ss));
         kv_copy[l] = 1;
       }
@@ -1038,7 +1093,9 @@ mz_status mz_load_model(const mz_model_cfg* cfg, const void* blob, size_t nbytes
     c.d_posq = (int32_t*)dmalloc((size_t)tot * 4);
     c.d_qix = (int32_t*)dmalloc((size_t)tot * 4);
     c.d_tok = (int32_t*)dmalloc((size_t)M * 4);
-    c.stage_bytes = (size_t)c.L * c.max_chunks * 4 + (size_t)tot * 24 + (size_t)M * 4 + 8 * 256;
+    c.stage_bytes = (size_t)c.L * c.max_chunks * 8 + (size_t)tot * 24 + (size_t)M * 4 + 9 * 256;
+    c.comp_bytes = mzk::kv_compressed_bytes(c.slot_bytes / 2);
+    HIPCHK(hipEventCreateWithFlags(&c.ev_meta, hipEventDisableTiming));
     void* stage = nullptr;
     if (hipHostMalloc(&stage, c.stage_bytes, hipHostMallocDefault) != hipSuccess || !stage)
       fail(MZ_ENOMEM, "pinned staging allocation failed");
@@ -1062,7 +1119,8 @@ void mz_free(mz_ctx* x) {
   (void)hipSetDevice(x->device);
   if (x->s_compute) (void)hipStreamSynchronize(x->s_compute);
   if (x->s_swap) (void)hipStreamSynchronize(x->s_swap);
-  void* dptrs[] = {x->w_slab, x->emb_nib, x->emb_sc, x->lm_nib, x->lm_sc, x->rope_cs, x->kv_slab,
+  void* dptrs[] = {x->codec_stage, x->d_codec_slots, x->w_slab, x->emb_nib, x->emb_sc, x->lm_nib, x->lm_sc,
+                   x->rope_cs, x->kv_slab,
                    x->h[0], x->h[1], x->xb, x->qf, x->kvf, x->q16, x->act, x->logits, x->part_val,
                    x->part_idx, x->d_token, x->d_tables, x->d_pos, x->d_kvoff, x->d_dix, x->d_posq,
                    x->d_qix, x->d_tok};
@@ -1077,6 +1135,7 @@ void mz_free(mz_ctx* x) {
   for (auto e : x->ev_pool) (void)hipEventDestroy(e);
   if (x->ev_swap_start) (void)hipEventDestroy(x->ev_swap_start);
   if (x->ev_swap_end) (void)hipEventDestroy(x->ev_swap_end);
+  if (x->ev_meta) (void)hipEventDestroy(x->ev_meta);
   if (x->s_compute) (void)hipStreamDestroy(x->s_compute);
   if (x->s_swap) (void)hipStreamDestroy(x->s_swap);
   delete x;
@@ -1090,6 +1149,13 @@ mz_status mz_set_option(mz_ctx* x, const char* key, int64_t value) {
     if (k == "overlap") x->overlap = value != 0;
     else if (k == "debug_swap_delay_us") x->debug_swap_delay_us = value < 0 ? 0 : value;
     else if (k == "debug_poison") x->debug_poison = value != 0;
+    else if (k == "kv_codec") {
+      if (value && !x->codec_stage) {
+        HIPCHK(hipMalloc((void**)&x->codec_stage, (size_t)x->max_chunks * (size_t)x->comp_bytes));
+        HIPCHK(hipMalloc((void**)&x->d_codec_slots, (size_t)x->L * x->max_chunks * sizeof(int32_t)));
+      }
+      x->kv_codec = value != 0;
+    }
     else if (k == "kernel_timing") {
       HIPCHK(hipStreamSynchronize(x->s_compute));
       x->collect_timing();
@@ -1257,6 +1323,7 @@ mz_status mz_evict(mz_ctx* x, const mz_evict_plan* plan) {
     x->collect_timing();
     std::vector<int> release_kv;
     std::vector<int> release_w;
+    int64_t n_comp = 0;
     for (int u : order) {
       const int t = target(u), cur = current(u);
       if (t == MZ_RES || t == cur) continue;
@@ -1264,10 +1331,21 @@ mz_status mz_evict(mz_ctx* x, const mz_evict_plan* plan) {
         const int l = u / nc, c = u % nc;
         const size_t idx = (size_t)l * MC + c;
         if (t == MZ_SWAP) {
-          const ArenaEntry e = x->arena.push((size_t)x->slot_bytes);
-          HIPCHK(hipMemcpyAsync(x->arena.ptr(e), x->kv_slab + (int64_t)x->table[idx] * x->slot_bytes,
-                                x->slot_bytes, hipMemcpyDeviceToHost, x->s_swap));
-          x->kv_entry[idx] = e;
+          const uint8_t* slot = x->kv_slab + (int64_t)x->table[idx] * x->slot_bytes;
+          const bool full = (int64_t)(c + 1) * x->C <= (int64_t)x->tokens.size();
+          if (x->kv_codec && full) {
+            // compress into the staging ring, then copy the compressed bytes out
+            uint8_t* stage = x->codec_stage + (n_comp++ % x->max_chunks) * x->comp_bytes;
+            mzk::launch_kv_compress(slot, nullptr, 0, x->slot_bytes / 2, 1, stage, x->s_swap);
+            HIPCHK(hipGetLastError());
+            const ArenaEntry e = x->arena.push((size_t)x->comp_bytes);
+            HIPCHK(hipMemcpyAsync(x->arena.ptr(e), stage, x->comp_bytes, hipMemcpyDeviceToHost, x->s_swap));
+            x->kv_entry[idx] = e;
+          } else {
+            const ArenaEntry e = x->arena.push((size_t)x->slot_bytes);
+            HIPCHK(hipMemcpyAsync(x->arena.ptr(e), slot, x->slot_bytes, hipMemcpyDeviceToHost, x->s_swap));
+            x->kv_entry[idx] = e;
+          }
         }
         if (cur == MZ_RES) release_kv.push_back(x->table[idx]);
         x->table[idx] = -1;
@@ -1453,6 +1531,24 @@ mz_status mz_rmsnorm(const void* h, int32_t m, int32_t d, float eps, void* x, vo
     if (!h || !x) fail(MZ_EINVAL, "NULL pointer");
     if (m < 1 || d < 4 || d % 4) fail(MZ_EINVAL, "bad sizes");
     mzk::launch_rmsnorm((const float*)h, m, d, eps, x, (hipStream_t)stream);
+    HIPCHK(hipGetLastError());
+  });
+}
+
+mz_status mz_kv_compress(const void* src, int64_t n_halves, void* out, void* stream) {
+  return guarded(nullptr, [&] {
+    if (!src || !out) fail(MZ_EINVAL, "NULL pointer");
+    if (n_halves < 64 || n_halves % 64) fail(MZ_EINVAL, "n_halves must be a positive multiple of 64");
+    mzk::launch_kv_compress(src, nullptr, 0, n_halves, 1, out, (hipStream_t)stream);
+    HIPCHK(hipGetLastError());
+  });
+}
+
+mz_status mz_kv_decompress(const void* in, int64_t n_halves, void* dst, void* stream) {
+  return guarded(nullptr, [&] {
+    if (!in || !dst) fail(MZ_EINVAL, "NULL pointer");
+    if (n_halves < 64 || n_halves % 64) fail(MZ_EINVAL, "n_halves must be a positive multiple of 64");
+    mzk::launch_kv_decompress(in, n_halves, 1, dst, nullptr, 0, (hipStream_t)stream);
     HIPCHK(hipGetLastError());
   });
 }

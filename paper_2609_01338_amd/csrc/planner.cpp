@@ -181,6 +181,12 @@ mz_status mz_plan_evict(const mz_model_cfg* cfg, const mz_evict_request* req, ui
     memset(kv_state, MZ_RES, (size_t)L * nc);
     memset(w_state, MZ_RES, (size_t)L);
     const int64_t slot = mzrt::kv_slot_bytes(c), unit = mzrt::weight_unit_bytes(c);
+    // link bytes of a swapped chunk: compressed when the codec is on and the
+    // chunk is full (n halves -> n + n/16 bytes), else the raw slot
+    const int64_t comp = slot / 2 + slot / 32;
+    auto chunk_link_bytes = [&](int k) {
+      return req->kv_codec && (int64_t)(k + 1) * c.chunk_tokens <= req->n_ctx ? comp : slot;
+    };
     int64_t link_bytes = 0;
     std::vector<int64_t> layer_bytes(L, 0);
     // weight units ride the link: the last layers, or the first for forward-out
@@ -201,9 +207,9 @@ mz_status mz_plan_evict(const mz_model_cfg* cfg, const mz_evict_request* req, ui
         case MZ_PLACE_ALL_DROP: drop = true; break;
         case MZ_PLACE_INTERLEAVE_2_1: drop = r % 3 == 2; break;
         case MZ_PLACE_BALANCED: {
-          layer_bytes[l] += slot;
+          layer_bytes[l] += chunk_link_bytes(k);
           const i128 if_swap = w.pipeline_end(layer_bytes, BW, RF);
-          layer_bytes[l] -= slot;
+          layer_bytes[l] -= chunk_link_bytes(k);
           const int old = w.md[k];
           w.drop(l, k);
           const i128 if_drop = w.pipeline_end(layer_bytes, BW, RF);
@@ -220,8 +226,8 @@ mz_status mz_plan_evict(const mz_model_cfg* cfg, const mz_evict_request* req, ui
         f_cur = w.flops();
       } else {
         kv_state[(size_t)l * nc + k] = MZ_SWAP;
-        link_bytes += slot;
-        layer_bytes[l] += slot;
+        link_bytes += chunk_link_bytes(k);
+        layer_bytes[l] += chunk_link_bytes(k);
       }
     }
     if (est) {

@@ -47,7 +47,7 @@ class mz_evict_request(ctypes.Structure):
     _fields_ = [("n_ctx", ctypes.c_int32), ("n_prompt", ctypes.c_int32), ("n_kv_evict", ctypes.c_int32),
                 ("n_w_evict", ctypes.c_int32), ("order", ctypes.c_int32), ("placement", ctypes.c_int32),
                 ("seed", ctypes.c_uint64), ("link_bytes_per_s", ctypes.c_double),
-                ("recompute_flops_per_s", ctypes.c_double)]
+                ("recompute_flops_per_s", ctypes.c_double), ("kv_codec", ctypes.c_int32)]
 
 
 ORDERS = {"backward-out": 0, "forward-out": 1, "random-out": 2, "token-aligned": 3}
@@ -87,6 +87,8 @@ def lib() -> ctypes.CDLL:
         "mz_rmsnorm": ([vp, i32, i32, ctypes.c_float, vp, vp], i32),
         "mz_probe_ceilings": ([i32, ctypes.c_char_p, sz], i32),
         "mz_plan_evict": ([ctypes.POINTER(mz_model_cfg), ctypes.POINTER(mz_evict_request), vp, vp, vp], i32),
+        "mz_kv_compress": ([vp, i64, vp, vp], i32),
+        "mz_kv_decompress": ([vp, i64, vp, vp], i32),
     }
     for name, (args, res) in sigs.items():
         f = getattr(L, name)
@@ -200,13 +202,13 @@ def mz_last_error(ctx=None) -> str:
 
 def mz_plan_evict(cfg: mz_model_cfg, n_ctx: int, n_prompt: int, n_kv_evict: int, n_w_evict: int,
                   order: str = "backward-out", placement: str = "balanced", seed: int = 0,
-                  link_bytes_per_s: float = 0.0, recompute_flops_per_s: float = 0.0):
+                  link_bytes_per_s: float = 0.0, recompute_flops_per_s: float = 0.0, kv_codec: bool = False):
     """Eviction plan (kv_state [L][n_chunks] uint8, w_state [L] uint8) and the
     estimate dict {swap_bytes, restore_flops, link_s, recompute_s, pipeline_s}."""
     L = cfg.n_layers
     nc = (n_ctx + cfg.chunk_tokens - 1) // cfg.chunk_tokens
     req = mz_evict_request(n_ctx, n_prompt, n_kv_evict, n_w_evict, ORDERS[order], PLACEMENTS[placement],
-                           seed, link_bytes_per_s, recompute_flops_per_s)
+                           seed, link_bytes_per_s, recompute_flops_per_s, int(kv_codec))
     kv = np.empty((L, nc), np.uint8)
     ws = np.empty(L, np.uint8)
     est = np.empty(5, np.float64)
@@ -269,6 +271,14 @@ def mz_attention(q_ptr: int, qpos_ptr: int, m: int, slab_ptr: int, table_ptr: in
 
 def mz_rmsnorm(h_ptr: int, m: int, d: int, eps: float, x_ptr: int, stream: Optional[int] = None) -> None:
     _check(lib().mz_rmsnorm(h_ptr, m, d, eps, x_ptr, stream), None)
+
+
+def mz_kv_compress(src_ptr: int, n_halves: int, out_ptr: int, stream: Optional[int] = None) -> None:
+    _check(lib().mz_kv_compress(src_ptr, n_halves, out_ptr, stream), None)
+
+
+def mz_kv_decompress(in_ptr: int, n_halves: int, dst_ptr: int, stream: Optional[int] = None) -> None:
+    _check(lib().mz_kv_decompress(in_ptr, n_halves, dst_ptr, stream), None)
 
 
 def mz_probe_ceilings(device: int = 0) -> dict:

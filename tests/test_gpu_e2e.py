@@ -50,8 +50,10 @@ def _check_token(tok, logits, otok, ologits, name):
         assert gap <= 2 * err, name
 
 
-def run_import_flow(w, kv_state, w_state, prompt, name, engine=None):
-    """Import the oracle's clean KV, evict, restore, first token; compare."""
+def run_import_flow(w, kv_state, w_state, prompt, name, engine=None, codec=False):
+    """Import the oracle's clean KV, evict, restore, first token; compare.
+    With codec, both sides swap full chunks through the 8-bit codec and the
+    restored chunks must equal the oracle's round trip bit for bit."""
     torch_cuda()
     m = w.model
     C, dkv, L = m.chunk_tokens, m.dkv, m.n_layers
@@ -82,8 +84,9 @@ def run_import_flow(w, kv_state, w_state, prompt, name, engine=None):
         pre = {(l, c): mz.mz_read_kv(eng.ctx, l, c, C, dkv) for l in range(L) for c in range(nc)}
         report("case", name=name, N=ctx.size, P=len(prompt), **{k: v for k, v in
                                                                  W.Plan(kv_state, w_state).counts().items()})
+        mz.mz_set_option(eng.ctx, "kv_codec", int(codec))
         mz.mz_evict(eng.ctx, kv_state, w_state)
-        ox.evict(kv_state, w_state)
+        ox.evict(kv_state, w_state, codec=codec)
         mz.mz_restore_and_prefill(eng.ctx, prompt)
         ox.restore_and_prefill(prompt)
         tok, logits = mz.mz_first_token(eng.ctx, m.vocab)
@@ -97,9 +100,13 @@ def run_import_flow(w, kv_state, w_state, prompt, name, engine=None):
                 ok_, ov_ = ox.read_kv(l, c)
                 n = min(C, S - c * C)
                 st = kv_state[l, c] if c < nc else O.DROP
-                if st == O.SWAP or st == O.RES:
+                keep = min(C, ctx.size - c * C)
+                if st == O.SWAP and codec and keep == C:
+                    # through the codec: the oracle's round trip, bit for bit
+                    assert k.tobytes() == ok_.astype(np.float16).tobytes(), (name, l, c)
+                    assert v.tobytes() == ov_.astype(np.float16).tobytes(), (name, l, c)
+                elif st == O.SWAP or st == O.RES:
                     # restored or untouched rows are the evicted bytes
-                    keep = min(C, ctx.size - c * C)
                     assert k[:keep].tobytes() == pre[(l, c)][0][:keep].tobytes(), (name, l, c)
                     assert v[:keep].tobytes() == pre[(l, c)][1][:keep].tobytes(), (name, l, c)
                 e = max(np.abs(k[:n].astype(np.float64) - ok_[:n]).max(),
@@ -234,3 +241,34 @@ def test_scaled_workload_import_flow(key, kw):
     plan = W.make_plan(w)
     prm = np.random.default_rng(1).integers(0, w.model.vocab, w.n_prompt).astype(np.int32)
     run_import_flow(w, plan.kv_state, plan.w_state, prm, w.key)
+
+
+@pytest.mark.parametrize("P", [0, 7])
+def test_tiny_swap_codec(tiny_engine, P):
+    """Swapped chunks through the 8-bit codec (full chunks compressed, the
+    partial last chunk raw), mixed with drops and resident chunks."""
+    prm = np.random.default_rng(3).integers(0, TINY.model.vocab, P).astype(np.int32)
+    for name, kv, ws in _tiny_plans():
+        if (kv == O.SWAP).any():
+            run_import_flow(TINY, kv, ws, prm, f"tiny-codec-{name}-P{P}", engine=tiny_engine, codec=True)
+    mz.mz_set_option(tiny_engine.ctx, "kv_codec", 0)
+
+
+def test_tiny_codec_partial_last_chunk():
+    m = TINY.model
+    w = W.Workload("tiny117c", 1, m, 117, 0, "all-drop", "")
+    nc = _chunks(117, 16)
+    kv = np.full((m.n_layers, nc), O.SWAP, np.uint8)
+    kv[1, 2] = O.DROP
+    run_import_flow(w, kv, None, np.arange(5, dtype=np.int32), "tiny-codec-partial", codec=True)
+
+
+def test_scaled_8b_swap_codec():
+    """Layer shape of the 8B workload (256-token chunks, 1 MiB slots) with the
+    codec on its own plan."""
+    w = W.WORKLOADS["8b"].scaled(n_layers=2, n_ctx=1024, n_prompt=64)
+    kv = np.full((2, w.n_chunks), O.SWAP, np.uint8)
+    kv[1, 1] = O.DROP
+    kv[0, 3] = O.RES
+    prm = np.random.default_rng(2).integers(0, w.model.vocab, w.n_prompt).astype(np.int32)
+    run_import_flow(w, kv, np.array([O.SWAP, O.RES], np.uint8), prm, "8b-codec", codec=True)

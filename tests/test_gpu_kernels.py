@@ -188,3 +188,41 @@ def test_kernel_entry_validation():
     assert e.value.status == mz.MZ_EINVAL
     with pytest.raises(mz.MzError):
         mz.mz_attention(1, 1, 4, 1, 1, 1, 16, 6, 4, 64, 1)   # 6 q heads over 4 kv heads
+
+
+@pytest.mark.parametrize("n,scale_kind", [(64, "normal"), (4096, "normal"), (64 * 1237, "mixed"),
+                                          (524288, "normal"), (640, "special")])
+def test_kv_codec_bit_exact(n, scale_kind):
+    """Swap-path codec: codes, per-group (min, step) and reconstruction equal
+    the oracle's bit for bit (same fp32 steps, correctly rounded division)."""
+    from oracle import kv_codec as Q
+    torch = torch_cuda()
+    rng = np.random.default_rng(n)
+    if scale_kind == "normal":
+        x = (rng.standard_normal(n) * 1.7).astype(np.float16)
+    elif scale_kind == "mixed":        # per-group scales from 1e-4 to 3e3, offsets
+        g = n // 64
+        x = (rng.standard_normal((g, 64)) * 10.0 ** rng.uniform(-4, 3.5, (g, 1))
+             + rng.uniform(-100, 100, (g, 1))).astype(np.float16).reshape(-1)
+    else:                              # constant, two-valued, subnormal, +-0, huge range, ties
+        x = np.zeros(n, np.float16)
+        x[64:128] = 2.5
+        x[128:192] = np.where(np.arange(64) % 2, 1.0, -1.0)
+        x[192:256] = np.float16(2.0 ** -20) * np.arange(64)
+        x[256:320] = np.where(np.arange(64) % 3 == 0, -0.0, 0.0)
+        x[320:384] = np.linspace(-60000, 60000, 64)
+        x[384:448] = (np.arange(64) * 0.5 / 16).astype(np.float16)
+        x[448:640] = rng.standard_normal(192)
+    report("codec", n=n, kind=scale_kind)
+    ref = Q.compress(x)
+    d_x = torch.from_numpy(x.view(np.int16)).cuda()
+    d_c = torch.empty(Q.compressed_bytes(n), dtype=torch.uint8, device="cuda")
+    d_y = torch.empty(n, dtype=torch.int16, device="cuda")
+    mz.mz_kv_compress(d_x.data_ptr(), n, d_c.data_ptr(), stream())
+    mz.mz_kv_decompress(d_c.data_ptr(), n, d_y.data_ptr(), stream())
+    torch.cuda.synchronize()
+    got = d_c.cpu().numpy()
+    assert np.array_equal(got[:n], ref[:n]), "codes"
+    assert np.array_equal(got[n:], ref[n:]), "group parameters"
+    assert np.array_equal(d_y.cpu().numpy().view(np.float16).view(np.uint16),
+                          Q.decompress(ref, n).view(np.uint16)), "reconstruction"

@@ -488,3 +488,60 @@ def test_f16_floor_reduces_to_fp64_oracle():
     kmax = max(np.abs(K0[l]).max() for l in range(hp.n_layers))
     assert fl.shape == (hp.n_layers,) and fl.max() > 0
     assert fl.max() <= 8 * 2.0 ** -11 * max(1.0, kmax)
+
+
+# ----------------------------------------------------------------------------- KV codec
+
+def test_kv_codec_exact_grid_group():
+    """A group lying on the grid m + j/16 with range 255/16: step, minimum
+    and codes are known in closed form and the round trip is exact."""
+    from oracle import kv_codec as Q
+    codes = np.array(list(range(0, 252, 4)) + [255], np.int64)          # 64 codes, max 255
+    x = (-8.0 + codes / 16.0).astype(np.float16)
+    b = Q.compress(x)
+    assert b.size == Q.compressed_bytes(64) == 68
+    assert b[:64].tolist() == codes.tolist()
+    m, d = b[64:].view(np.float16).tolist()
+    assert m == -8.0 and d == 0.0625
+    assert np.array_equal(Q.decompress(b, 64), x)
+
+
+def test_kv_codec_special_groups():
+    from oracle import kv_codec as Q
+    const = np.full(64, 3.25, np.float16)                    # zero range: step 0, codes 0
+    b = Q.compress(const)
+    assert not b[:64].any() and b[64:].view(np.float16).tolist() == [3.25, 0.0]
+    assert np.array_equal(Q.decompress(b, 64), const)
+    # ties round to even: x - m = 0.5 d -> 0, 1.5 d -> 2 (d = 1/16, range 255/16)
+    x = np.zeros(64, np.float16)
+    x[1], x[2], x[3] = 0.5 / 16, 1.5 / 16, 255 / 16
+    q = Q.compress(x)[:64]
+    assert q[0] == 0 and q[1] == 0 and q[2] == 2 and q[3] == 255
+
+
+def test_kv_codec_error_bound_and_no_accumulation():
+    """|x^ - x| <= d/2 + half an ulp of x^ per element (one rounding to the
+    grid, one to half precision); further swap cycles stay within that bound
+    of the original (the codec does not accumulate error)."""
+    from oracle import kv_codec as Q
+    rng = np.random.default_rng(0)
+    x = (rng.standard_normal(64 * 2048) * np.repeat(rng.uniform(0.01, 30, 2048), 64)).astype(np.float16)
+    b = Q.compress(x)
+    d = np.repeat(b[x.size:].view(np.float16).reshape(-1, 2)[:, 1].astype(np.float64), 64)
+    cur = x
+    for cycle in range(4):
+        cur = Q.decompress(Q.compress(cur), x.size)
+        ulp = np.spacing(np.abs(cur).astype(np.float16)).astype(np.float64)
+        err = np.abs(cur.astype(np.float64) - x.astype(np.float64))
+        assert np.all(err <= 0.5 * d + 0.5 * ulp + 1e-12), cycle
+
+
+def test_kv_codec_chunk_order_round_trip():
+    from oracle import kv_codec as Q
+    rng = np.random.default_rng(1)
+    k = rng.standard_normal((16, 128)).astype(np.float16)
+    v = rng.standard_normal((16, 128)).astype(np.float16)
+    flat = Q.chunk_device_order(k, v)
+    assert np.array_equal(flat[16 * 128 + 5], v[5, 0]) and np.array_equal(flat[16 * 128 + 16], v[0, 1])
+    k2, v2 = Q.chunk_from_device_order(flat, 16, 128)
+    assert np.array_equal(k2, k) and np.array_equal(v2, v)

@@ -64,15 +64,17 @@ def test_matches_reference_planner(shape, order, placement):
     unit, slot = _unit_and_slot(cfg, n_ctx)
     nc = (n_ctx + C - 1) // C
     rng = np.random.default_rng(L * 1000 + n_ctx)
-    for trial in range(3):
+    for trial in range(4):
+        codec = trial % 2 == 1
         n_kv = int(rng.integers(0, L * nc + 1))
         n_w = int(rng.integers(0, L + 1))
         seed = int(rng.integers(0, 2 ** 63))
         link = float(rng.uniform(1e6, 1e8))          # bytes/s and FLOP/s scaled so both paths matter
         rec = float(rng.uniform(1e9, 1e11))
-        kv, ws, est = mz.mz_plan_evict(cfg, n_ctx, n_prompt, n_kv, n_w, order, placement, seed, link, rec)
+        kv, ws, est = mz.mz_plan_evict(cfg, n_ctx, n_prompt, n_kv, n_w, order, placement, seed, link, rec,
+                                       kv_codec=codec)
         rkv, rws, rlink, rflops = ref_plan(L, d, nq * hd, nkv * hd, ff, C, n_ctx, n_prompt, n_kv, n_w, order,
-                                           placement, seed, link, rec, slot, unit)
+                                           placement, seed, link, rec, slot, unit, codec=codec)
         assert np.array_equal(kv, rkv), (order, placement, trial)
         assert np.array_equal(ws, rws)
         assert est["swap_bytes"] == rlink
