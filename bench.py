@@ -153,7 +153,8 @@ def tp_shard_kernels(w, tp):
     return out
 
 
-def run_ablation(mz, W, eng, w, prompt, clean_logits, recompute_tflops, link_gbps, steps=3):
+def run_ablation(mz, W, eng, w, prompt, clean_logits, recompute_tflops, link_gbps, steps=3,
+                 parts=("plans", "codec", "overlap", "size")):
     """TTFT of every eviction order x placement at the workload's evicted amount
     (as many KV chunks and weight units as its own plan evicts), with the
     planner's estimate beside each, then overlap on/off for two plans."""
@@ -179,7 +180,7 @@ def run_ablation(mz, W, eng, w, prompt, clean_logits, recompute_tflops, link_gbp
         return statistics.median(ts), err
 
     rows = []
-    for order in mz.ORDERS:
+    for order in (mz.ORDERS if "plans" in parts else ()):
         for placement in mz.PLACEMENTS:
             kv, ws, est = mz.mz_plan_evict(cfg, w.n_ctx, w.n_prompt, n_kv, n_w, order, placement, 1,
                                            link_gbps * 1e9, recompute_tflops * 1e12)
@@ -192,7 +193,7 @@ def run_ablation(mz, W, eng, w, prompt, clean_logits, recompute_tflops, link_gbp
                 f"recompute {est['recompute_s'] * 1e3:7.1f}) swap/drop {rows[-1]['swap_chunks']}/{rows[-1]['drop_chunks']}")
     codec_rows = []
     mz.mz_set_option(e, "kv_codec", 1)
-    for placement in ("balanced", "all-swap", "interleave-2-1"):
+    for placement in (("balanced", "all-swap", "interleave-2-1") if "codec" in parts else ()):
         kv, ws, est = mz.mz_plan_evict(cfg, w.n_ctx, w.n_prompt, n_kv, n_w, "backward-out", placement, 1,
                                        link_gbps * 1e9, recompute_tflops * 1e12, kv_codec=True)
         t, err = ttft_of(kv, ws)
@@ -206,7 +207,7 @@ def run_ablation(mz, W, eng, w, prompt, clean_logits, recompute_tflops, link_gbp
             f"{codec_rows[-1]['drop_chunks']} max|logit - clean| {err:.3e}")
     mz.mz_set_option(e, "kv_codec", 0)
     overlap = []
-    for placement in ("interleave-2-1", "balanced"):
+    for placement in (("interleave-2-1", "balanced") if "overlap" in parts else ()):
         kv, ws, _ = mz.mz_plan_evict(cfg, w.n_ctx, w.n_prompt, n_kv, n_w, "backward-out", placement, 1,
                                      link_gbps * 1e9, recompute_tflops * 1e12)
         res = {"placement": placement}
@@ -216,8 +217,52 @@ def run_ablation(mz, W, eng, w, prompt, clean_logits, recompute_tflops, link_gbp
         mz.mz_set_option(e, "overlap", 1)
         overlap.append(res)
         log(f"[ablation] overlap {res}")
+    # size-driven eviction (hybrid-swap state machine) at fractions of the
+    # context's device bytes (every KV slot and weight unit), codec on, with
+    # the balanced plan for the same numbers of units beside it
+    size_rows = []
+    nc = w.n_chunks
+    slot = m.chunk_tokens * m.dkv * 4
+    _, _, e1 = mz.mz_plan_evict(cfg, w.n_ctx, w.n_prompt, 0, 1, "backward-out", "all-swap")
+    total = m.n_layers * nc * slot + m.n_layers * int(e1["swap_bytes"])
+    mz.mz_set_option(e, "kv_codec", 1)
+    for frac in ((0.25, 0.5, 0.75, 1.0) if "size" in parts else ()):
+        want = int(total * frac)
+        kv0 = np.zeros((m.n_layers, nc), np.uint8)
+        ws0 = np.zeros(m.n_layers, np.uint8)
+        kv, ws, _, stg, info = mz.mz_plan_evict_size(cfg, w.n_ctx, kv0, ws0, want, link_gbps * 1e9,
+                                                     recompute_tflops * 1e12, m.n_layers, w.n_prompt, True)
+        ts, err = [], 0.0
+        for step in range(steps + 1):
+            got = mz.mz_evict_size(e, want, link_gbps * 1e9, recompute_tflops * 1e12, m.n_layers, w.n_prompt)
+            assert got["released"] == info["released"]
+            t0 = time.perf_counter()
+            mz.mz_restore_and_prefill(e, prompt)
+            tok, logits = mz.mz_first_token(e, m.vocab)
+            dt = time.perf_counter() - t0
+            mz.mz_truncate_context(e, w.n_ctx)
+            if step:
+                ts.append(dt * 1e3)
+            err = max(err, float(np.abs(logits - clean_logits).max()))
+        t = statistics.median(ts)
+        n_kv_s, n_w_s = int((kv != W.RES).sum()), int((ws != W.RES).sum())
+        kvb, wsb, _ = mz.mz_plan_evict(cfg, w.n_ctx, w.n_prompt, n_kv_s, n_w_s, "backward-out", "balanced", 1,
+                                       link_gbps * 1e9, recompute_tflops * 1e12, kv_codec=True)
+        tb, _ = ttft_of(kvb, wsb)
+        counts = np.bincount(stg, minlength=4)
+        size_rows.append({"fraction": frac, "released_bytes": info["released"], "T": info["T"],
+                          "stage_units": {"kv_only": int(counts[0]), "kv_and_w": int(counts[1]),
+                                          "w_only": int(counts[2])},
+                          "swap_chunks": int((kv == W.SWAP).sum()), "drop_chunks": int((kv == W.DROP).sum()),
+                          "weight_layers": n_w_s, "ttft_ms": round(t, 2), "max_logit_err_vs_clean": err,
+                          "balanced_plan_same_units_ttft_ms": round(tb, 2)})
+        log(f"[ablation] evict_size {frac:4.2f} of {total / 1e9:.2f} GB: T {info['T']} stages {counts[:3].tolist()} "
+            f"swap/drop {size_rows[-1]['swap_chunks']}/{size_rows[-1]['drop_chunks']} weights {n_w_s} "
+            f"TTFT {t:8.2f} ms (balanced plan, same units: {tb:8.2f} ms) max|logit - clean| {err:.3e}")
+    mz.mz_set_option(e, "kv_codec", 0)
     return {"n_kv_evicted": n_kv, "n_w_evicted": n_w, "link_gbps": link_gbps,
-            "recompute_tflops": recompute_tflops, "plans": rows, "codec_plans": codec_rows, "overlap": overlap}
+            "recompute_tflops": recompute_tflops, "plans": rows, "codec_plans": codec_rows, "overlap": overlap,
+            "evict_size": size_rows}
 
 
 def main():
@@ -231,6 +276,8 @@ def main():
     ap.add_argument("--no-shard", action="store_true", help="skip the per-GPU shard kernel timings")
     ap.add_argument("--ablation", action="store_true",
                     help="instead of the timed steps: TTFT per eviction order x placement (one JSON line)")
+    ap.add_argument("--ablation-parts", default="plans,codec,overlap,size",
+                    help="comma list of ablation parts: plans, codec, overlap, size")
     ap.add_argument("--recompute-tflops", type=float, default=400.0,
                     help="recompute rate the balanced placement assumes (partial-layer recompute of a "
                          "balanced plan runs at about 400 TFLOP/s on MI355X: few rows per GEMM)")
@@ -286,7 +333,7 @@ def main():
 
     if args.ablation:
         res = run_ablation(mz, W, eng, w, prompt, clean_logits, args.recompute_tflops,
-                           ceilings["h2d_pinned_gbps"])
+                           ceilings["h2d_pinned_gbps"], parts=tuple(args.ablation_parts.split(",")))
         eng.close()
         print(json.dumps({"ablation": res, "workload": w.key, "ceilings_measured": ceilings}), flush=True)
         return

@@ -220,6 +220,69 @@ typedef struct {
 mz_status mz_plan_evict(const mz_model_cfg *cfg, const mz_evict_request *req, uint8_t *kv_state,
                         uint8_t *w_state, double *est);
 
+/* ---- size-driven eviction (host planning + mz_evict) ------------------ */
+
+/* Stage of the hybrid-swap eviction policy (paper Sec. 4.3, Alg. 1). */
+typedef enum {
+  MZ_STAGE_KV_ONLY = 0,        /* KV chunks only, each to the path that keeps both totals level */
+  MZ_STAGE_KV_AND_W = 1,       /* weight layers, with the KV chunks their reload time covers dropped */
+  MZ_STAGE_W_ONLY = 2,         /* weight layers only (no KV chunk left) */
+  MZ_STAGE_EXHAUSTED = 3       /* nothing resident is left to evict */
+} mz_evict_stage;
+
+typedef struct {
+  int64_t bytes;               /* device bytes to release: KV slots and weight units */
+  int32_t n_prompt;            /* expected prompt length of the coming restore (0 if unknown) */
+  int32_t n_w_total;           /* evictable weight layers N_W^total (the last ones), 0..n_layers */
+  double link_bytes_per_s;     /* host link rate */
+  double recompute_flops_per_s;/* GPU recompute rate */
+  int32_t kv_codec;            /* 1: full swapped chunks are priced at their compressed size */
+} mz_evict_size_request;
+
+/* Plan the next increment of size-driven eviction from the current unit
+ * states (the paper's evict(size), Sec. 5, driven by its hybrid-swap policy,
+ * Sec. 4.3 and Alg. 1, and its backward-out order, Sec. 4.4).  The two
+ * restore paths are the host link (weight layers and swapped KV chunks: a
+ * unit costs its link bytes / link rate) and GPU recompute (dropped KV
+ * chunks: a chunk costs the growth of the restore's exact FLOP count when it
+ * is dropped, / recompute rate; this depends on the rest of the plan).
+ * Totals: link = every non-resident weight unit and swapped chunk, recompute
+ * = FLOPs(plan) - FLOPs(nothing dropped).  Threshold T = the largest n such
+ * that dropping the n front-most chunks (the last n of the backward-out
+ * order, nothing else dropped) costs no more recompute time than reloading
+ * all n_w_total weight layers over the link.  Units are taken one at a time,
+ * rearmost first, until `bytes` are released:
+ *   N_KV > T          KV_ONLY: the next chunk is dropped iff the recompute
+ *                     total with it stays below the link total with it
+ *                     swapped, else swapped;
+ *   N_KV > 0, N_W > 0 KV_AND_W: the next chunk is dropped if the recompute
+ *                     total with it does not pass the link total, else the
+ *                     next weight layer is evicted;
+ *   N_KV > 0, N_W = 0 the KV_ONLY rule (no weight layer left to pair with);
+ *   N_W > 0           W_ONLY: the next weight layer;
+ *   otherwise         EXHAUSTED: stop short of `bytes`.
+ * Weight layers are evicted as MZ_DROP (reloaded from the library's pinned
+ * weight image).  kv_state [n_layers][ceil(n_ctx / chunk_tokens)] and
+ * w_state [n_layers] (host) are read as the current states and updated in
+ * place.  order (host, NULL or n_layers * (n_chunks + 1) entries) receives
+ * the evicted units in eviction order (chunk (l, c) as l * n_chunks + c,
+ * weight layer l as n_layers * n_chunks + l), stage (NULL or as many
+ * entries) the stage that took each, *n_evicted their count.  info (NULL or
+ * 8 doubles): released bytes, T, stage after the call, link total (s),
+ * recompute total (s), N_KV, N_W, whether `bytes` was reached (1/0).
+ * Errors: EINVAL (sizes, states, non-positive rates). */
+mz_status mz_plan_evict_size(const mz_model_cfg *cfg, int32_t n_ctx, const mz_evict_size_request *req,
+                             uint8_t *kv_state, uint8_t *w_state, int32_t *order, int32_t *stage,
+                             int32_t *n_evicted, double *info);
+
+/* Release at least req->bytes of device memory from ctx's cached context by
+ * the policy of mz_plan_evict_size (its kv_codec field is replaced by the
+ * context's "kv_codec" option), then mz_evict the planned units in eviction
+ * order.  Repeated calls continue from the state the previous ones left.
+ * info as in mz_plan_evict_size.  Errors: those of mz_plan_evict_size and
+ * mz_evict; ESTATE without a cached context. */
+mz_status mz_evict_size(mz_ctx *ctx, const mz_evict_size_request *req, double *info);
+
 /* Bytes of the device GEMM layout of a Q4_0 matrix [n][k] (n padded to 256,
  * k to 64). */
 int64_t mz_q4_gemm_packed_bytes(int32_t n, int32_t k);

@@ -148,3 +148,132 @@ def plan_evict(L: int, d: int, dq: int, dkv: int, ff: int, chunk: int, n_ctx: in
             link += chunk_bytes(c)
             layer_bytes[l] += chunk_bytes(c)
     return kv, ws, link, f_cur
+
+
+# --------------------------------------------------------------------------
+# Size-driven eviction: the hybrid-swap policy (Sec. 4.3, Alg. 1), taken one
+# unit at a time in backward-out order (Sec. 4.4) until the requested bytes
+# are released (the evict(size) interface of Sec. 5).
+#
+# Paths: the link (weight layers, swapped chunks) plays the storage path of
+# the paper, the one weights are tied to; recompute (dropped chunks) plays
+# the in-memory decompression path, which takes KV chunks only.  A chunk's
+# recompute time is not a constant here, so every time below is a path
+# total: link = sum of link times of non-resident units, recompute = time of
+# the plan's extra restore work.  Stages, from the counts of resident units:
+#   N_KV > T              KV_ONLY   chunk to the path that stays behind
+#   N_KV > 0 and N_W > 0  KV_AND_W  chunk dropped if recompute stays within
+#                                   the link total, else a weight layer
+#   N_KV > 0, N_W = 0               the KV_ONLY rule (no weight left)
+#   N_W > 0               W_ONLY    a weight layer
+#   else                  EXHAUSTED (the paper's CompKV has no counterpart:
+#                                    nothing compressed stays on the device)
+# T = the largest n for which dropping the n front-most chunks costs no more
+# recompute than reloading all N_W^total weight layers; with a constant
+# per-chunk time t_d this is floor(N_W^total * t_W / t_d).
+
+KV_ONLY, KV_AND_W, W_ONLY, EXHAUSTED = 0, 1, 2, 3
+
+
+def size_threshold(kv_seq, rec_time, n_w_total, t_w):
+    """T: front-most chunks (the tail of kv_seq) that the weight reload covers."""
+    T = 0
+    budget = n_w_total * t_w
+    for n in range(1, len(kv_seq) + 1):
+        if rec_time(set(kv_seq[len(kv_seq) - n:])) > budget:
+            break
+        T = n
+    return T
+
+
+def hybrid_swap_evict(kv_seq, w_seq, kv_state, w_state, T, request, kv_release, w_release, kv_link, w_link,
+                      rec_time):
+    """One evict(size) call.
+
+    kv_seq / w_seq: every evictable chunk / weight id in eviction order;
+    kv_state / w_state: dicts id -> RES / SWAP / DROP, updated in place;
+    kv_link(id), w_link: link time of a unit; rec_time(set of dropped chunk
+    ids): recompute time of that plan's extra work.  Returns (evicted ids with
+    their stage, released bytes)."""
+    dropped = {u for u, s in kv_state.items() if s == DROP}
+    link = sum((kv_link(u) for u, s in kv_state.items() if s == SWAP), Fraction(0))
+    link += sum((w_link for s in w_state.values() if s != RES), Fraction(0))
+    taken, released = [], 0
+
+    def counts():
+        return (sum(1 for u in kv_seq if kv_state[u] == RES), sum(1 for u in w_seq if w_state[u] == RES))
+
+    def stage():
+        n_kv, n_w = counts()
+        if n_kv > T:
+            return KV_ONLY
+        if n_kv > 0 and n_w > 0:
+            return KV_AND_W
+        if n_kv > 0:
+            return KV_ONLY
+        return W_ONLY if n_w > 0 else EXHAUSTED
+
+    def evict_weight(st):
+        nonlocal link, released
+        u = next(u for u in w_seq if w_state[u] == RES)
+        w_state[u] = DROP
+        link += w_link
+        released += w_release
+        taken.append((("w", u), st))
+
+    while released < request:
+        st = stage()
+        if st == EXHAUSTED:
+            break
+        if st == W_ONLY:
+            evict_weight(st)
+            continue
+        u = next(u for u in kv_seq if kv_state[u] == RES)
+        rec_with = rec_time(dropped | {u})
+        if st == KV_AND_W and rec_with > link:
+            evict_weight(st)
+            continue
+        if st == KV_AND_W or rec_with < link + kv_link(u):
+            kv_state[u] = DROP
+            dropped.add(u)
+        else:
+            kv_state[u] = SWAP
+            link += kv_link(u)
+        released += kv_release
+        taken.append((("kv", u), st))
+    return taken, released
+
+
+def plan_evict_size(L: int, d: int, dq: int, dkv: int, ff: int, chunk: int, n_ctx: int, n_prompt: int,
+                    kv_state: np.ndarray, w_state: np.ndarray, request: int, n_w_total: int, link_rate: float,
+                    recompute_rate: float, slot_bytes: int, unit_bytes: int, codec: bool = False):
+    """The policy on this engine's restore: chunk (l, c) and weight layer l,
+    link times from bytes, recompute time from the restore's FLOP count.
+    Returns (kv_state, w_state, unit ids in order with stages, released, T)."""
+    nc = (n_ctx + chunk - 1) // chunk
+    bw = int(link_rate + 0.5)
+    rf = int(recompute_rate + 0.5)
+    kv_seq = [(l, c) for l in range(L - 1, -1, -1) for c in range(nc - 1, -1, -1)]
+    w_seq = list(range(L - 1, L - 1 - n_w_total, -1))
+
+    def flops_of(dropped):
+        plan = np.full((L, nc), RES, np.uint8)
+        for l, c in dropped:
+            plan[l, c] = DROP
+        return restore_flops(L, d, dq, dkv, ff, plan, n_ctx, n_prompt, chunk)
+
+    f0 = flops_of(set())
+    rec_time = lambda dropped: Fraction(flops_of(dropped) - f0, rf)
+    kv_link = lambda u: Fraction(slot_bytes // 2 + slot_bytes // 32
+                                 if codec and (u[1] + 1) * chunk <= n_ctx else slot_bytes, bw)
+    w_link = Fraction(unit_bytes, bw)
+    T = size_threshold(kv_seq, rec_time, n_w_total, w_link)
+    kvs = {(l, c): int(kv_state[l, c]) for l in range(L) for c in range(nc)}
+    ws = {l: int(w_state[l]) for l in range(L)}
+    taken, released = hybrid_swap_evict(kv_seq, w_seq, kvs, ws, T, request, slot_bytes, unit_bytes, kv_link,
+                                        w_link, rec_time)
+    out_kv = np.array([[kvs[(l, c)] for c in range(nc)] for l in range(L)], np.uint8)
+    out_w = np.array([ws[l] for l in range(L)], np.uint8)
+    ids = [u[0] * nc + u[1] if kind == "kv" else L * nc + u for (kind, u), _ in taken]
+    stages = [st for _, st in taken]
+    return out_kv, out_w, ids, stages, released, T

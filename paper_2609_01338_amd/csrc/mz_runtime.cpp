@@ -316,6 +316,15 @@ struct HostArena {
     segs.clear();
     top = 0;
   }
+  // after a restore has consumed the stack: give every segment back
+  void trim() {
+    for (auto& s : segs)
+      if (s.used) fail(MZ_ESTATE, "swap segment still in use");
+    for (auto& s : segs) HIPCHK(hipHostFree(s.p));
+    segs.clear();
+    top = 0;
+    bytes_live = 0;
+  }
 };
 
 // ---------------------------------------------------------------- timing
@@ -419,6 +428,7 @@ struct mz_ctx {
 
   // options / stats
   bool overlap = true;
+  bool swap_trim = false;               // option swap_trim: free the swap segments after a restore
   int64_t debug_swap_delay_us = 0;   // test hook: delay the swap stream before its copies
   bool debug_poison = false;         // test hook: NaN-fill every freshly allocated unit
   // 8-bit codec on the swap path (option kv_codec): full chunks are compressed
@@ -921,6 +931,10 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
     for (int c = 0; c < MC; ++c) x->kv_state[(size_t)l * MC + c] = MZ_RES;
   }
   x->arena.reset();
+  if (x->swap_trim) {   // the copies out of the segments must be done before they are freed
+    HIPCHK(hipStreamSynchronize(x->s_swap));
+    x->arena.trim();
+  }
   x->tokens.insert(x->tokens.end(), prompt, prompt + P);
   x->last_nR = rows.nR;
   x->last_nD = rows.nD;
@@ -1149,6 +1163,7 @@ mz_status mz_set_option(mz_ctx* x, const char* key, int64_t value) {
     if (k == "overlap") x->overlap = value != 0;
     else if (k == "debug_swap_delay_us") x->debug_swap_delay_us = value < 0 ? 0 : value;
     else if (k == "debug_poison") x->debug_poison = value != 0;
+    else if (k == "swap_trim") x->swap_trim = value != 0;
     else if (k == "kv_codec") {
       if (value && !x->codec_stage) {
         HIPCHK(hipMalloc((void**)&x->codec_stage, (size_t)x->max_chunks * (size_t)x->comp_bytes));
@@ -1368,6 +1383,39 @@ mz_status mz_evict(mz_ctx* x, const mz_evict_plan* plan) {
     for (int s : release_w) x->w_pool.release(s);
     x->have_last = false;
   });
+}
+
+mz_status mz_evict_size(mz_ctx* x, const mz_evict_size_request* req, double* info) {
+  if (!x) return MZ_EINVAL;
+  std::vector<uint8_t> kv, ws;
+  std::vector<int32_t> order;
+  int32_t n_ev = 0;
+  int32_t L = 0, nc = 0;
+  mz_status st = guarded(x, [&] {
+    if (!req) fail(MZ_EINVAL, "req is NULL");
+    if (x->tokens.empty()) fail(MZ_ESTATE, "no cached context to evict");
+    L = x->L;
+    nc = x->nchunks_of((int)x->tokens.size());
+    kv.resize((size_t)L * nc);
+    for (int l = 0; l < L; ++l)
+      for (int c = 0; c < nc; ++c) kv[(size_t)l * nc + c] = x->kv_state[(size_t)l * x->max_chunks + c];
+    ws.assign(x->w_state.begin(), x->w_state.end());
+    order.resize((size_t)L * (nc + 1));
+    mz_evict_size_request r = *req;
+    r.kv_codec = x->kv_codec ? 1 : 0;
+    if (mz_plan_evict_size(&x->cfg, (int32_t)x->tokens.size(), &r, kv.data(), ws.data(), order.data(), nullptr,
+                           &n_ev, info) != MZ_OK)
+      fail(MZ_EINVAL, "%s", mz_last_error(nullptr));
+  });
+  if (st != MZ_OK || n_ev == 0) return st;
+  mz_evict_plan plan{};
+  plan.n_layers = L;
+  plan.n_chunks = nc;
+  plan.kv_state = kv.data();
+  plan.w_state = ws.data();
+  plan.order = order.data();
+  plan.n_order = n_ev;
+  return mz_evict(x, &plan);
 }
 
 mz_status mz_restore_and_prefill(mz_ctx* x, const int32_t* prompt, int32_t n_prompt) {

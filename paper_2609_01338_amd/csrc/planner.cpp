@@ -244,4 +244,159 @@ mz_status mz_plan_evict(const mz_model_cfg* cfg, const mz_evict_request* req, ui
   }
 }
 
+// Size-driven eviction: the hybrid-swap state machine (paper Alg. 1) over
+// the two restore paths, one unit at a time, rearmost first.  Totals are
+// kept in units of 1 / (BW * RF) seconds: link bytes * RF, recompute FLOPs *
+// BW.  Every decision reads only the current unit states, so a sequence of
+// calls takes the same units as one call asking for their sum.
+mz_status mz_plan_evict_size(const mz_model_cfg* cfg, int32_t n_ctx, const mz_evict_size_request* req,
+                             uint8_t* kv_state, uint8_t* w_state, int32_t* order, int32_t* stage,
+                             int32_t* n_evicted, double* info) {
+  try {
+    if (!cfg || !req || !kv_state || !w_state) throw PlanError{MZ_EINVAL, "NULL pointer"};
+    const mz_model_cfg& c = *cfg;
+    if (c.n_layers < 1 || c.chunk_tokens < 1 || n_ctx < 1 || req->n_prompt < 0 || req->bytes < 0)
+      throw PlanError{MZ_EINVAL, "bad sizes"};
+    if (req->n_w_total < 0 || req->n_w_total > c.n_layers) throw PlanError{MZ_EINVAL, "n_w_total out of range"};
+    if (!(req->link_bytes_per_s >= 1.0 && req->recompute_flops_per_s >= 1.0))
+      throw PlanError{MZ_EINVAL, "size-driven eviction needs positive rates"};
+    Work w(c, n_ctx, req->n_prompt);
+    const int L = w.L, nc = w.nc, total = L * nc;
+    for (int u = 0; u < total; ++u)
+      if (kv_state[u] > MZ_DROP) throw PlanError{MZ_EINVAL, "invalid kv_state entry"};
+    for (int l = 0; l < L; ++l)
+      if (w_state[l] > MZ_DROP) throw PlanError{MZ_EINVAL, "invalid w_state entry"};
+    const i128 BW = (i128)(int64_t)(req->link_bytes_per_s + 0.5);
+    const i128 RF = (i128)(int64_t)(req->recompute_flops_per_s + 0.5);
+    const int64_t slot = mzrt::kv_slot_bytes(c), unit = mzrt::weight_unit_bytes(c);
+    const int64_t comp = slot / 2 + slot / 32;
+    auto chunk_link_bytes = [&](int k) {
+      return req->kv_codec && (int64_t)(k + 1) * c.chunk_tokens <= n_ctx ? comp : slot;
+    };
+    const int64_t F0 = w.flops();
+
+    // backward-out order over every chunk; weights rearmost first
+    std::vector<std::pair<int, int>> seq;
+    seq.reserve(total);
+    for (int l = L - 1; l >= 0; --l)
+      for (int k = nc - 1; k >= 0; --k) seq.push_back({l, k});
+
+    // threshold T: the front-most chunks whose recompute fits the reload of
+    // all evictable weight layers
+    const i128 budget = (i128)req->n_w_total * unit * RF;
+    auto tail_fits = [&](int n) {
+      Work t(c, n_ctx, req->n_prompt);
+      for (int i = total - n; i < total; ++i) t.drop(seq[i].first, seq[i].second);
+      return (i128)(t.flops() - F0) * BW <= budget;
+    };
+    int lo = 0, hi = total;   // the cost grows with n
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) / 2;
+      if (tail_fits(mid)) lo = mid; else hi = mid - 1;
+    }
+    const int T = lo;
+
+    // current state
+    int64_t link = 0;
+    int n_kv = 0, n_w = 0;
+    for (int l = 0; l < L; ++l)
+      for (int k = 0; k < nc; ++k) {
+        const uint8_t st = kv_state[(size_t)l * nc + k];
+        if (st == MZ_RES) ++n_kv;
+        else if (st == MZ_SWAP) link += chunk_link_bytes(k);
+        else w.drop(l, k);
+      }
+    for (int l = 0; l < L; ++l) {
+      if (w_state[l] != MZ_RES) link += unit;
+      else if (l >= L - req->n_w_total) ++n_w;
+    }
+    int64_t F = w.flops();
+    size_t kv_cur = 0;
+    int w_cur = L - 1;
+    auto next_kv = [&]() {
+      while (kv_state[(size_t)seq[kv_cur].first * nc + seq[kv_cur].second] != MZ_RES) ++kv_cur;
+      return seq[kv_cur];
+    };
+    auto next_w = [&]() {
+      while (w_state[w_cur] != MZ_RES) --w_cur;
+      return w_cur;
+    };
+    auto stage_now = [&]() {
+      if (n_kv > T) return (int)MZ_STAGE_KV_ONLY;
+      if (n_kv > 0 && n_w > 0) return (int)MZ_STAGE_KV_AND_W;
+      if (n_kv > 0) return (int)MZ_STAGE_KV_ONLY;
+      if (n_w > 0) return (int)MZ_STAGE_W_ONLY;
+      return (int)MZ_STAGE_EXHAUSTED;
+    };
+
+    int64_t released = 0;
+    int n_out = 0;
+    int st = stage_now();
+    while (released < req->bytes && st != MZ_STAGE_EXHAUSTED) {
+      int unit_id;
+      if (st == MZ_STAGE_W_ONLY) {
+        const int l = next_w();
+        w_state[l] = MZ_DROP;
+        link += unit;
+        --n_w;
+        released += unit;
+        unit_id = total + l;
+      } else {
+        const auto lk = next_kv();
+        const int l = lk.first, k = lk.second, old = w.md[k];
+        w.drop(l, k);
+        const int64_t Fd = w.flops();
+        const i128 rec_with = (i128)(Fd - F0) * BW;
+        bool drop, take_weight = false;
+        if (st == MZ_STAGE_KV_ONLY) {
+          drop = rec_with < (i128)(link + chunk_link_bytes(k)) * RF;
+        } else {
+          drop = rec_with <= (i128)link * RF;
+          take_weight = !drop;
+        }
+        if (take_weight) {
+          w.undrop(l, k, old);
+          const int lw = next_w();
+          w_state[lw] = MZ_DROP;
+          link += unit;
+          --n_w;
+          released += unit;
+          unit_id = total + lw;
+        } else {
+          if (drop) {
+            F = Fd;
+            kv_state[(size_t)l * nc + k] = MZ_DROP;
+          } else {
+            w.undrop(l, k, old);
+            kv_state[(size_t)l * nc + k] = MZ_SWAP;
+            link += chunk_link_bytes(k);
+          }
+          --n_kv;
+          released += slot;
+          unit_id = l * nc + k;
+        }
+      }
+      if (order) order[n_out] = unit_id;
+      if (stage) stage[n_out] = st;
+      ++n_out;
+      st = stage_now();
+    }
+    if (n_evicted) *n_evicted = n_out;
+    if (info) {
+      info[0] = (double)released;
+      info[1] = (double)T;
+      info[2] = (double)st;
+      info[3] = (double)link / (double)BW;
+      info[4] = (double)(F - F0) / (double)RF;
+      info[5] = (double)n_kv;
+      info[6] = (double)n_w;
+      info[7] = released >= req->bytes ? 1.0 : 0.0;
+    }
+    return MZ_OK;
+  } catch (const PlanError& e) {
+    mzrt::set_error(e.msg);
+    return e.st;
+  }
+}
+
 }  // extern "C"

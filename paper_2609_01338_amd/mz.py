@@ -50,6 +50,25 @@ class mz_evict_request(ctypes.Structure):
                 ("recompute_flops_per_s", ctypes.c_double), ("kv_codec", ctypes.c_int32)]
 
 
+class mz_evict_size_request(ctypes.Structure):
+    _fields_ = [("bytes", ctypes.c_int64), ("n_prompt", ctypes.c_int32), ("n_w_total", ctypes.c_int32),
+                ("link_bytes_per_s", ctypes.c_double), ("recompute_flops_per_s", ctypes.c_double),
+                ("kv_codec", ctypes.c_int32)]
+
+
+STAGES = ("kv-only", "kv-and-w", "w-only", "exhausted")
+_INFO_KEYS = ("released", "T", "stage", "link_s", "recompute_s", "n_kv", "n_w", "reached")
+
+
+def _size_info(info: np.ndarray) -> dict:
+    d = dict(zip(_INFO_KEYS, (float(v) for v in info)))
+    for k in ("released", "T", "n_kv", "n_w"):
+        d[k] = int(d[k])
+    d["stage"] = STAGES[int(d["stage"])]
+    d["reached"] = bool(d["reached"])
+    return d
+
+
 ORDERS = {"backward-out": 0, "forward-out": 1, "random-out": 2, "token-aligned": 3}
 PLACEMENTS = {"balanced": 0, "all-swap": 1, "all-drop": 2, "interleave-2-1": 3}
 
@@ -89,6 +108,9 @@ def lib() -> ctypes.CDLL:
         "mz_plan_evict": ([ctypes.POINTER(mz_model_cfg), ctypes.POINTER(mz_evict_request), vp, vp, vp], i32),
         "mz_kv_compress": ([vp, i64, vp, vp], i32),
         "mz_kv_decompress": ([vp, i64, vp, vp], i32),
+        "mz_plan_evict_size": ([ctypes.POINTER(mz_model_cfg), i32, ctypes.POINTER(mz_evict_size_request),
+                                vp, vp, vp, vp, vp, vp], i32),
+        "mz_evict_size": ([vp, ctypes.POINTER(mz_evict_size_request), vp], i32),
     }
     for name, (args, res) in sigs.items():
         f = getattr(L, name)
@@ -170,6 +192,17 @@ def mz_evict(ctx, kv_state: np.ndarray, w_state: Optional[np.ndarray] = None,
     _check(lib().mz_evict(ctx, ctypes.byref(plan)), ctx)
 
 
+def mz_evict_size(ctx, nbytes: int, link_bytes_per_s: float, recompute_flops_per_s: float,
+                  n_w_total: int, n_prompt: int = 0) -> dict:
+    """Release at least nbytes of device memory by the hybrid-swap policy;
+    returns {released, T, stage, link_s, recompute_s, n_kv, n_w, reached}."""
+    req = mz_evict_size_request(int(nbytes), int(n_prompt), int(n_w_total), float(link_bytes_per_s),
+                                float(recompute_flops_per_s), 0)
+    info = np.zeros(8, np.float64)
+    _check(lib().mz_evict_size(ctx, ctypes.byref(req), info.ctypes.data), ctx)
+    return _size_info(info)
+
+
 def mz_restore_and_prefill(ctx, prompt: Optional[np.ndarray] = None) -> None:
     p = np.zeros(0, np.int32) if prompt is None else np.ascontiguousarray(prompt, dtype=np.int32)
     _check(lib().mz_restore_and_prefill(ctx, _ptr(p) if p.size else None, p.size), ctx)
@@ -216,6 +249,27 @@ def mz_plan_evict(cfg: mz_model_cfg, n_ctx: int, n_prompt: int, n_kv_evict: int,
                                est.ctypes.data), None)
     return kv, ws, {"swap_bytes": est[0], "restore_flops": est[1], "link_s": est[2], "recompute_s": est[3],
                     "pipeline_s": est[4]}
+
+
+def mz_plan_evict_size(cfg: mz_model_cfg, n_ctx: int, kv_state: np.ndarray, w_state: np.ndarray, nbytes: int,
+                       link_bytes_per_s: float, recompute_flops_per_s: float, n_w_total: int,
+                       n_prompt: int = 0, kv_codec: bool = False):
+    """Next increment of size-driven eviction from the given states:
+    (kv_state, w_state updated copies, evicted unit ids in order, their
+    stages, info dict)."""
+    kv = np.array(kv_state, dtype=np.uint8, order="C", copy=True)
+    ws = np.array(w_state, dtype=np.uint8, order="C", copy=True)
+    L, nc = kv.shape
+    order = np.empty(L * (nc + 1), np.int32)
+    stage = np.empty(L * (nc + 1), np.int32)
+    n = ctypes.c_int32()
+    info = np.zeros(8, np.float64)
+    req = mz_evict_size_request(int(nbytes), int(n_prompt), int(n_w_total), float(link_bytes_per_s),
+                                float(recompute_flops_per_s), int(kv_codec))
+    _check(lib().mz_plan_evict_size(ctypes.byref(cfg), n_ctx, ctypes.byref(req), kv.ctypes.data, ws.ctypes.data,
+                                    order.ctypes.data, stage.ctypes.data, ctypes.byref(n), info.ctypes.data),
+           None)
+    return kv, ws, order[:n.value].copy(), stage[:n.value].copy(), _size_info(info)
 
 
 def mz_plan_rows(cfg: mz_model_cfg, kv_state: np.ndarray, n_ctx: int, n_prompt: int,

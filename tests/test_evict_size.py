@@ -1,0 +1,272 @@
+"""Size-driven eviction (mz_plan_evict_size): the hybrid-swap state machine
+(Sec. 4.3, Alg. 1) pinned on its closed forms, and the library's planner
+against the reference in oracle/ decision for decision.  CPU only."""
+
+import math
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle as O
+from oracle.planner import (EXHAUSTED, KV_AND_W, KV_ONLY, W_ONLY, hybrid_swap_evict, plan_evict_size,
+                            restore_flops, size_threshold)
+from paper_2609_01338_amd import mz
+from paper_2609_01338_amd import workloads as W
+
+# ---------------------------------------------------------------------------
+# the state machine with constant per-unit times: the paper's own model
+
+
+def _const_machine(n_kv, n_w_total, t_l, t_d, t_w, L_w=None):
+    kv_seq = list(range(n_kv))
+    w_seq = list(range(n_w_total))
+    rec = lambda s: len(s) * t_d
+    T = size_threshold(kv_seq, rec, n_w_total, t_w)
+    kvs = {u: O.RES for u in kv_seq}
+    ws = {u: O.RES for u in range(L_w or n_w_total)}
+    return kv_seq, w_seq, rec, T, kvs, ws
+
+
+def _run(kv_seq, w_seq, kvs, ws, T, request, t_l, t_w, rec):
+    return hybrid_swap_evict(kv_seq, w_seq, kvs, ws, T, request, 1, 1, lambda u: t_l, t_w, rec)
+
+
+CONST = [  # n_kv, n_w_total, t_l, t_d, t_w
+    (200, 8, Fraction(1), Fraction(3), Fraction(10)),
+    (200, 8, Fraction(5), Fraction(2), Fraction(7)),
+    (50, 10, Fraction(1), Fraction(1), Fraction(9)),       # n_kv <= T: starts in KV_AND_W
+    (300, 4, Fraction(2, 3), Fraction(7, 5), Fraction(17, 2)),
+    (120, 0, Fraction(1), Fraction(2), Fraction(5)),       # no evictable weights: T = 0
+]
+
+
+@pytest.mark.parametrize("n_kv,n_w,t_l,t_d,t_w", CONST)
+def test_threshold_closed_form(n_kv, n_w, t_l, t_d, t_w):
+    """With a constant chunk time, T = floor(N_W^total t_W / t_d), capped by
+    the number of chunks."""
+    *_, T, _, _ = _const_machine(n_kv, n_w, t_l, t_d, t_w)
+    assert T == min(n_kv, math.floor(n_w * t_w / t_d))
+
+
+@pytest.mark.parametrize("n_kv,n_w,t_l,t_d,t_w", CONST)
+def test_stage_sequence_and_split(n_kv, n_w, t_l, t_d, t_w):
+    kv_seq, w_seq, rec, T, kvs, ws = _const_machine(n_kv, n_w, t_l, t_d, t_w)
+    taken, released = _run(kv_seq, w_seq, kvs, ws, T, 10 ** 9, t_l, t_w, rec)
+    stages = [st for _, st in taken]
+    # everything evictable is taken, each unit once
+    assert released == n_kv + n_w and len(taken) == n_kv + n_w
+    assert all(kvs[u] != O.RES for u in kv_seq) and all(ws[u] != O.RES for u in w_seq)
+    # weights leave only as the rearmost first
+    w_order = [u for (k, u), _ in taken if k == "w"]
+    assert w_order == w_seq
+    # KV_ONLY while more than T chunks remain, KV_AND_W from N_KV = T on
+    n_kv_only = max(0, n_kv - T)
+    assert stages[:n_kv_only] == [KV_ONLY] * n_kv_only
+    assert all(k == "kv" for (k, _), _ in taken[:n_kv_only])          # weights untouched
+    # KV_ONLY split in inverse proportion to the unit times: the two totals
+    # stay within one unit of each other
+    drops = sum(1 for (k, u), _ in taken[:n_kv_only] if kvs[u] == O.DROP)
+    swaps = n_kv_only - drops
+    assert abs(drops * t_d - swaps * t_l) <= max(t_l, t_d)
+    if n_kv_only:
+        expect = n_kv_only * t_l / (t_l + t_d)
+        assert abs(drops - expect) <= 1
+    # in KV_AND_W every chunk goes to recompute
+    assert all(kvs[u] == O.DROP for (k, u), st in taken if k == "kv" and st == KV_AND_W)
+    if n_w and n_kv > T:
+        assert stages[n_kv_only] == KV_AND_W
+    if n_kv <= T and n_w:
+        # the chunks run out first; the rest are weights alone
+        assert stages[0] == KV_AND_W
+        last_kv = max(i for i, ((k, _), _) in enumerate(taken) if k == "kv")
+        assert all(st == W_ONLY for _, st in taken[last_kv + 1:])
+    if n_kv > T and n_w:
+        # both run out together: whichever kind outlasts the other does so by
+        # about one weight layer's share (a weight layer is paired with the
+        # chunks its reload covers, which follow it)
+        last_w = max(i for i, ((k, _), _) in enumerate(taken) if k == "w")
+        last_kv = max(i for i, ((k, _), _) in enumerate(taken) if k == "kv")
+        m = max(t_l, t_d)
+        if last_kv > last_w:
+            assert last_kv - last_w <= math.ceil((t_w + m) / t_d) + 1
+            assert all(kvs[u] == O.DROP for (k, u), _ in taken[last_w + 1:])
+        else:
+            assert last_w - last_kv <= math.ceil(m / t_w) + 1
+    if n_w == 0:
+        assert T == 0 and set(stages) == {KV_ONLY}
+
+
+@pytest.mark.parametrize("n_kv,n_w,t_l,t_d,t_w", CONST[:4])
+def test_balance_preserved_wherever_eviction_stops(n_kv, n_w, t_l, t_d, t_w):
+    """Through KV_ONLY the two path totals stay within one chunk of each
+    other; through KV_AND_W, whose increment is a weight layer and the chunks
+    its reload covers, within one weight layer and one chunk.  Any stopping
+    point is balanced to that grain."""
+    kv_seq, w_seq, rec, T, kvs, ws = _const_machine(n_kv, n_w, t_l, t_d, t_w)
+    link = Fraction(0)
+    rec_t = Fraction(0)
+    m = max(t_l, t_d)
+    while True:
+        taken, _ = _run(kv_seq, w_seq, kvs, ws, T, 1, t_l, t_w, rec)
+        if not taken:
+            break
+        (kind, u), st = taken[0]
+        if kind == "w":
+            link += t_w
+        elif kvs[u] == O.SWAP:
+            link += t_l
+        else:
+            rec_t += t_d
+        if st == KV_ONLY and sum(1 for v in kv_seq if kvs[v] == O.RES) > T:
+            assert abs(link - rec_t) <= m
+        if st == KV_AND_W:
+            assert abs(link - rec_t) <= t_w + m
+
+
+def test_calls_continue_where_the_last_stopped():
+    """A sequence of calls takes exactly the units of one call for their
+    total: the state machine keeps no state beside the units' states."""
+    args = (200, 8, Fraction(1), Fraction(3), Fraction(10))
+    kv_seq, w_seq, rec, T, kvs, ws = _const_machine(*args)
+    full, _ = _run(kv_seq, w_seq, kvs, ws, T, 10 ** 9, args[2], args[4], rec)
+    kv_seq, w_seq, rec, T, kvs, ws = _const_machine(*args)
+    got = []
+    for req in (3, 1, 17, 60, 2, 10 ** 9):
+        t, r = _run(kv_seq, w_seq, kvs, ws, T, req, args[2], args[4], rec)
+        assert r >= min(req, len(full) - len(got))
+        got += t
+    assert got == full
+    t, r = _run(kv_seq, w_seq, kvs, ws, T, 5, args[2], args[4], rec)
+    assert t == [] and r == 0                                           # exhausted
+
+
+# ---------------------------------------------------------------------------
+# the work model that prices a dropped chunk
+
+
+def test_front_chunk_costs_its_layer0_kv_projection():
+    """Dropping a chunk of layer 0 alone adds exactly its rows' K/V
+    projection at layer 0: 2 rows d 2dkv FLOPs (R_1 and every later set are
+    unchanged, so nothing else is recomputed)."""
+    L, d, dq, dkv, ff, C, N = 4, 256, 256, 128, 512, 64, 200
+    base = np.zeros((L, (N + C - 1) // C), np.uint8)
+    f0 = restore_flops(L, d, dq, dkv, ff, base, N, 0, C)
+    for c, rows in [(0, 64), (3, N - 3 * C)]:
+        p = base.copy()
+        p[0, c] = O.DROP
+        assert restore_flops(L, d, dq, dkv, ff, p, N, 0, C) - f0 == 2 * rows * d * 2 * dkv
+
+
+# ---------------------------------------------------------------------------
+# library planner vs the reference, decision for decision
+
+
+def _setup(shape):
+    L, d, nq, nkv, hd, ff, C, n_ctx, n_prompt = shape
+    m = W.ModelConfig("t", L, d, nq, nkv, hd, ff, 1024, 1e4, C)
+    cfg = mz.make_cfg(m, n_ctx + n_prompt)
+    _, _, e = mz.mz_plan_evict(cfg, n_ctx, 0, 0, 1, "backward-out", "all-swap")
+    unit = int(e["swap_bytes"])
+    slot = C * nkv * hd * 4
+    return m, cfg, unit, slot
+
+
+SHAPES = [
+    # L, d, nq, nkv, hd, ff, C, n_ctx, n_prompt
+    (3, 256, 4, 2, 64, 688, 64, 700, 0),
+    (4, 512, 8, 2, 64, 1024, 128, 1024, 16),
+    (5, 256, 4, 4, 64, 512, 64, 448, 5),
+]
+RATES = [(1e7, 1e10), (1e8, 1e9), (3e6, 1e11), (5.5e7, 2.5e10)]
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+@pytest.mark.parametrize("rates", RATES)
+def test_matches_reference_over_calls(shape, rates):
+    L, d, nq, nkv, hd, ff, C, n_ctx, n_prompt = shape
+    m, cfg, unit, slot = _setup(shape)
+    nc = (n_ctx + C - 1) // C
+    link, rec = rates
+    rng = np.random.default_rng(hash((shape, rates)) % 2 ** 32)
+    for trial in range(2):
+        codec = trial == 1
+        n_w_total = int(rng.integers(0, L + 1))
+        kv = np.zeros((L, nc), np.uint8)
+        ws = np.zeros(L, np.uint8)
+        okv, ows = kv.copy(), ws.copy()
+        total = 0
+        while True:
+            req = int(rng.integers(1, 6)) * slot + int(rng.integers(0, 2)) * unit
+            kv, ws, order, stage, info = mz.mz_plan_evict_size(cfg, n_ctx, kv, ws, req, link, rec, n_w_total,
+                                                                n_prompt, codec)
+            okv, ows, oids, ost, orel, oT = plan_evict_size(L, d, nq * hd, nkv * hd, ff, C, n_ctx, n_prompt, okv,
+                                                            ows, req, n_w_total, link, rec, slot, unit, codec)
+            assert np.array_equal(kv, okv) and np.array_equal(ws, ows)
+            assert list(order) == oids and list(stage) == ost
+            assert info["released"] == orel and info["T"] == oT
+            assert info["reached"] == (orel >= req)
+            total += orel
+            if not info["reached"]:
+                assert info["stage"] == "exhausted" and info["n_kv"] == 0 and info["n_w"] == 0
+                break
+        # everything evictable is gone; weights beyond n_w_total never move
+        assert not (kv == O.RES).any()
+        assert list(ws) == [O.RES] * (L - n_w_total) + [O.DROP] * n_w_total
+        assert total == L * nc * slot + n_w_total * unit
+
+
+def test_matches_reference_from_a_mixed_state():
+    """Starting from a state left by an explicit plan (swapped and dropped
+    chunks, a swapped weight layer) the totals include what is already out."""
+    shape = (4, 512, 8, 2, 64, 1024, 128, 1024, 16)
+    L, d, nq, nkv, hd, ff, C, n_ctx, n_prompt = shape
+    m, cfg, unit, slot = _setup(shape)
+    p = W.random_plan(L, (n_ctx + C - 1) // C, 0.3, 0.2, 4, w_swap=0.3, w_drop=0.0)
+    for req in (slot, 7 * slot, 10 ** 12):
+        a = mz.mz_plan_evict_size(cfg, n_ctx, p.kv_state, p.w_state, req, 2e7, 3e10, L, n_prompt)
+        b = plan_evict_size(L, d, nq * hd, nkv * hd, ff, C, n_ctx, n_prompt, p.kv_state, p.w_state, req, L,
+                            2e7, 3e10, slot, unit)
+        assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1]) and list(a[2]) == b[2]
+        assert list(a[3]) == b[3] and a[4]["released"] == b[4]
+
+
+def test_workload_8b_stages():
+    """On the 8B context the policy starts in KV_ONLY (the front-most chunks
+    that the weight reload covers are a few of the 4096) and reaches
+    KV_AND_W before the context is gone."""
+    w = W.WORKLOADS["8b"]
+    cfg = mz.make_cfg(w.model, w.n_ctx + w.n_prompt)
+    L, nc = w.model.n_layers, w.n_chunks
+    kv = np.zeros((L, nc), np.uint8)
+    ws = np.zeros(L, np.uint8)
+    slot = w.model.chunk_tokens * w.model.dkv * 4
+    kv2, ws2, order, stage, info = mz.mz_plan_evict_size(cfg, w.n_ctx, kv, ws, 10 ** 13, 56e9, 4e14, L,
+                                                         w.n_prompt, True)
+    assert 0 < info["T"] < L * nc
+    assert stage[0] == KV_ONLY and KV_AND_W in set(stage.tolist())
+    assert info["stage"] == "exhausted" and not info["reached"]
+    kv3, ws3, order3, _, info3 = mz.mz_plan_evict_size(cfg, w.n_ctx, kv, ws, 100 * slot, 56e9, 4e14, L,
+                                                       w.n_prompt, True)
+    assert list(order3) == list(order[:100]) and info3["released"] == 100 * slot
+
+
+def test_errors():
+    w = W.WORKLOADS["tiny"]
+    cfg = mz.make_cfg(w.model, w.n_ctx)
+    L, nc = w.model.n_layers, w.n_chunks
+    kv = np.zeros((L, nc), np.uint8)
+    ws = np.zeros(L, np.uint8)
+    with pytest.raises(mz.MzError):
+        mz.mz_plan_evict_size(cfg, w.n_ctx, kv, ws, 100, 0.0, 1e9, L)           # no link rate
+    with pytest.raises(mz.MzError):
+        mz.mz_plan_evict_size(cfg, w.n_ctx, kv, ws, 100, 1e9, 1e9, L + 1)       # n_w_total
+    with pytest.raises(mz.MzError):
+        mz.mz_plan_evict_size(cfg, w.n_ctx, kv, ws, -1, 1e9, 1e9, L)            # bytes
+    bad = kv.copy()
+    bad[0, 0] = 7
+    with pytest.raises(mz.MzError):
+        mz.mz_plan_evict_size(cfg, w.n_ctx, bad, ws, 100, 1e9, 1e9, L)
+    # nothing requested: nothing taken
+    kv2, ws2, order, _, info = mz.mz_plan_evict_size(cfg, w.n_ctx, kv, ws, 0, 1e9, 1e9, L)
+    assert order.size == 0 and info["released"] == 0 and info["reached"]

@@ -50,7 +50,7 @@ def _check_token(tok, logits, otok, ologits, name):
         assert gap <= 2 * err, name
 
 
-def run_import_flow(w, kv_state, w_state, prompt, name, engine=None, codec=False):
+def run_import_flow(w, kv_state, w_state, prompt, name, engine=None, codec=False, evict_fn=None):
     """Import the oracle's clean KV, evict, restore, first token; compare.
     With codec, both sides swap full chunks through the 8-bit codec and the
     restored chunks must equal the oracle's round trip bit for bit."""
@@ -85,7 +85,10 @@ def run_import_flow(w, kv_state, w_state, prompt, name, engine=None, codec=False
         report("case", name=name, N=ctx.size, P=len(prompt), **{k: v for k, v in
                                                                  W.Plan(kv_state, w_state).counts().items()})
         mz.mz_set_option(eng.ctx, "kv_codec", int(codec))
-        mz.mz_evict(eng.ctx, kv_state, w_state)
+        if evict_fn is None:
+            mz.mz_evict(eng.ctx, kv_state, w_state)
+        else:
+            evict_fn(eng)
         ox.evict(kv_state, w_state, codec=codec)
         mz.mz_restore_and_prefill(eng.ctx, prompt)
         ox.restore_and_prefill(prompt)
@@ -272,3 +275,59 @@ def test_scaled_8b_swap_codec():
     kv[0, 3] = O.RES
     prm = np.random.default_rng(2).integers(0, w.model.vocab, w.n_prompt).astype(np.int32)
     run_import_flow(w, kv, np.array([O.SWAP, O.RES], np.uint8), prm, "8b-codec", codec=True)
+
+
+def _size_flow(w, requests, link, rec, n_w_total, prompt, name, codec=False, engine=None):
+    """mz_evict_size over several calls; the oracle side evicts the states
+    that the reference planner reaches for the same calls."""
+    from oracle.planner import plan_evict_size
+    m = w.model
+    L, C, nc = m.n_layers, m.chunk_tokens, w.n_chunks
+    slot = C * m.dkv * 4
+    cfg = mz.make_cfg(m, w.n_ctx + len(prompt))
+    _, _, e = mz.mz_plan_evict(cfg, w.n_ctx, 0, 0, 1, "backward-out", "all-swap")
+    unit = int(e["swap_bytes"])
+    kv = np.zeros((L, nc), np.uint8)
+    ws = np.zeros(L, np.uint8)
+    expect = []
+    for req in requests:
+        kv, ws, _, stages, rel, T = plan_evict_size(L, m.d_model, m.dq, m.dkv, m.d_ffn, C, w.n_ctx, len(prompt),
+                                                    kv, ws, req, n_w_total, link, rec, slot, unit, codec)
+        expect.append((rel, T))
+    report("size plan", case=name, T=expect[0][1], swap=int((kv == O.SWAP).sum()), drop=int((kv == O.DROP).sum()),
+           w_out=int((ws != O.RES).sum()))
+
+    def evict_fn(eng):
+        for req, (rel, T) in zip(requests, expect):
+            info = mz.mz_evict_size(eng.ctx, req, link, rec, n_w_total, len(prompt))
+            assert info["released"] == rel and info["T"] == T, (name, info, rel, T)
+
+    run_import_flow(w, kv, ws, prompt, name, engine=engine, codec=codec, evict_fn=evict_fn)
+    return kv, ws
+
+
+@pytest.mark.parametrize("codec", [False, True])
+def test_tiny_evict_size_calls(tiny_engine, codec):
+    """Size-driven eviction in three calls, down to exhaustion, with rates
+    that exercise KV_ONLY, KV_AND_W and W_ONLY on the tiny model."""
+    m = TINY.model
+    slot = m.chunk_tokens * m.dkv * 4
+    prm = np.arange(6, dtype=np.int32)
+    # (KV_ONLY + KV_AND_W, swaps and drops), (KV_ONLY then W_ONLY, T = 0),
+    # (KV_AND_W then W_ONLY, T = every chunk)
+    for link, rec, n_w in [(1e8, 1e10, 2), (1e9, 1e9, 2), (1e8, 1e11, 2)]:
+        kv, ws = _size_flow(TINY, [3 * slot, 5 * slot, 10 ** 12], link, rec, n_w, prm,
+                            f"tiny-size-{link:g}-{rec:g}-{n_w}-codec{int(codec)}", codec, tiny_engine)
+        assert not (kv == O.RES).any()
+
+
+def test_scaled_8b_evict_size():
+    """The 8B layer shape (4 layers, 2K context): half the context's device
+    bytes released in two calls, then everything (swaps, drops, two weight
+    layers)."""
+    w = W.WORKLOADS["8b"].scaled(n_layers=4, n_ctx=2048, n_prompt=32)
+    m = w.model
+    slot = m.chunk_tokens * m.dkv * 4
+    half = m.n_layers * w.n_chunks * slot // 2
+    prm = np.random.default_rng(5).integers(0, m.vocab, w.n_prompt).astype(np.int32)
+    _size_flow(w, [half // 2, half - half // 2, 10 ** 13], 56e9, 1e13, 2, prm, "8b-size", codec=True)
