@@ -137,7 +137,11 @@ mz_status mz_first_token(mz_ctx *ctx, int32_t *token_out, float *logits_out);
  * it through mz_kv_decompress -- about half the host-link bytes, values
  * rounded to the codec's grid; partial chunks and weight units move raw;
  * enabling it the first time allocates a device staging ring of one layer's
- * chunks).  Test hooks: "debug_poison" (1: fill every
+ * chunks), "attn_split" (1: attention of few query rows against a long
+ * context runs split over the keys, as mz_attention_split, default; 0: always
+ * one pass), "swap_trim" (1: free the pinned swap segments after each restore,
+ * as the paper's growing swap stack does; 0: keep them for the next
+ * eviction, default).  Test hooks: "debug_poison" (1: fill every
  * slot and weight unit allocated by a restore with NaN before it is
  * restored or recomputed), "debug_swap_delay_us" (delay the swap stream by a
  * bounded busy wait before its copies).  EINVAL for an unknown key. */
@@ -321,6 +325,38 @@ mz_status mz_attention(const void *q_f16, const int32_t *qpos, int32_t m, const 
                        const int32_t *table, int32_t n_table, int32_t chunk_tokens,
                        int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, void *out_f16,
                        void *stream);
+
+/* Split-key form of mz_attention for few query rows against a long context
+ * (the paper's short requests, Sec. 6; the attention of its custom kernel,
+ * Sec. 4.2, is one pass over the chunks, which leaves most of the GPU idle
+ * when there are few queries).  The keys 0..max_pos are cut into n_split
+ * ranges of whole 64-key tiles, ceil((max_pos / 64 + 1) / n_split) tiles
+ * each; every range runs as its own workgroups and leaves, per query row and
+ * head, its output normalised by its own softmax sum (f16) with that sum and
+ * the running max (fp32) in workspace; a second kernel merges the ranges
+ * with weights 2^(max_s - max) * sum_s.  The result equals mz_attention's to
+ * the f16 rounding of the partial outputs.  max_pos (host value) must be >=
+ * qpos[m-1], and table must cover chunk max_pos / chunk_tokens.  workspace:
+ * device, caller-owned, at least mz_attention_split_workspace_bytes(m,
+ * n_q_heads, head_dim, n_split) bytes; it must not be shared by calls in
+ * flight at the same time.  Other arguments and errors as mz_attention;
+ * EINVAL also for n_split outside 1..1024 or a short workspace. */
+mz_status mz_attention_split(const void *q_f16, const int32_t *qpos, int32_t m, int32_t max_pos,
+                             const void *slab, const int32_t *table, int32_t n_table,
+                             int32_t chunk_tokens, int32_t n_q_heads, int32_t n_kv_heads,
+                             int32_t head_dim, int32_t n_split, void *workspace,
+                             int64_t workspace_bytes, void *out_f16, void *stream);
+
+/* Workspace bytes of mz_attention_split (-1 for invalid arguments). */
+int64_t mz_attention_split_workspace_bytes(int32_t m, int32_t n_q_heads, int32_t head_dim,
+                                           int32_t n_split);
+
+/* The split count the restore uses for m query rows up to max_pos with
+ * workspace_bytes of workspace: enough workgroups for two per compute unit,
+ * at least 4 key tiles per split, at most 64 splits; 1 when the unsplit
+ * kernel already fills the GPU. */
+int32_t mz_attention_auto_splits(int32_t m, int32_t max_pos, int32_t n_q_heads, int32_t n_kv_heads,
+                                 int32_t head_dim, int64_t workspace_bytes);
 
 /* x = h / sqrt(mean(h^2) + eps) per row: h float [m][d] -> x f16 [m][d]. */
 mz_status mz_rmsnorm(const void *h_f32, int32_t m, int32_t d, float eps, void *x_f16,

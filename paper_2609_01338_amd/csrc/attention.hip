@@ -33,6 +33,8 @@
 // the 8 consecutive k of group l / 32; the accumulator element r of lane l is
 // row 8 * (r / 4) + 4 * (l / 32) + r % 4, column l % 32.  Both operands of a
 // product only need to agree on which logical k sits in (lane group, slot).
+#include <algorithm>
+
 #include "mz_kernels.h"
 
 namespace mzk {
@@ -70,14 +72,22 @@ constexpr int k_tile_halves() { return KT * HD; }
 template <int HD>
 constexpr int v_tile_halves() { return HD * KT; }
 
-template <int HD, int NW, bool DIRECT>
+// SPLIT: blockIdx.y is a key split.  The workgroup covers key tiles
+// [y * tps, min((y + 1) * tps, n_kt)) of its query tile and writes, per query
+// row and head, the partial output normalised by its own row sum (f16, into
+// Opart [split][M][nq][HD]) and (running max, row sum) (into MLpart
+// [split][M][nq]; max -inf and sum 0 for a query that sees no key of the
+// split).  Without SPLIT the whole key range is one pass and O is final.
+template <int HD, int NW, bool DIRECT, bool SPLIT>
 __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restrict__ Q,
                                                        const int32_t* __restrict__ qpos, int M,
                                                        const uint8_t* __restrict__ slab,
                                                        const int32_t* __restrict__ table, int C,
                                                        int cshift, int64_t slot_bytes, int nq, int nkv,
                                                        int group, int qw, int n_qtiles,
-                                                       float scale_log2, _Float16* __restrict__ O) {
+                                                       float scale_log2, _Float16* __restrict__ O, int tps,
+                                                       _Float16* __restrict__ Opart,
+                                                       float2* __restrict__ MLpart) {
   constexpr int NTH = 64 * NW;
   constexpr int KC = HD / 8;                        // 16-byte columns of a K row
   constexpr int K_SEGS = KT * KC;                   // 16-byte pieces of a K tile
@@ -116,6 +126,11 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
   const int kmax = qpos[row_end - 1];              // positions ascend
   const int kmin = qpos[row0];
   const int n_kt = kmax / KT + 1;
+  // key tiles of this workgroup: [kt0, kt_end)
+  const int split = SPLIT ? (int)blockIdx.y : 0;
+  const int kt0 = SPLIT ? split * tps : 0;
+  const int kt_end = SPLIT ? min(kt0 + tps, n_kt) : n_kt;
+  if (kt0 >= kt_end) return;   // no query of this tile reaches the split
 
   const int h = kvh * group + (w % group);
   const bool wave_active = w < group * qw;
@@ -359,34 +374,39 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
   // and land in the buffers freed in iteration kt-1; one barrier per
   // iteration.
   if constexpr (DIRECT) {
-    dload_k(0, Kbuf(0));
-    dload_v(0, Vbuf(0));
-    if (n_kt > 1) dload_k(1, Kbuf(1));
+    dload_k(kt0, Kbuf(kt0));
+    dload_v(kt0, Vbuf(kt0));
+    if (kt0 + 1 < kt_end) dload_k(kt0 + 1, Kbuf(kt0 + 1));
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    if (n_kt == 1) vfix(0, Vbuf(0));
+    if (kt0 + 1 == kt_end) vfix(kt0, Vbuf(kt0));
   } else {
-    gload_k(0);
-    gload_v(0);
-    lstore_k(Kbuf(0));
-    lstore_v(Vbuf(0));
-    if (n_kt > 1) {
-      gload_k(1);
-      lstore_k(Kbuf(1));
+    gload_k(kt0);
+    gload_v(kt0);
+    lstore_k(Kbuf(kt0));
+    lstore_v(Vbuf(kt0));
+    if (kt0 + 1 < kt_end) {
+      gload_k(kt0 + 1);
+      lstore_k(Kbuf(kt0 + 1));
     }
   }
   __syncthreads();
   f32x16 s0[2], s1[2];
-  qk(Kbuf(0), s0);
-  if (KT - 1 > kmin) mask_tile(s0, 0);
+  qk(Kbuf(kt0), s0);
+  if (kt0 * KT + KT - 1 > kmin) mask_tile(s0, kt0);
   update_max(tile_max(s0));
+  // a query before the split's first key sees nothing here: a finite max
+  // keeps its exponentials at 0 instead of NaN (its row sum stays 0)
+  if constexpr (SPLIT) {
+    if (m_i == -INFINITY) m_i = 0.f;
+  }
 
   auto step = [&](int kt, f32x16* sc, f32x16* sn) {
     if constexpr (DIRECT) {
-      if (kt + 2 < n_kt) dload_k(kt + 2, Kbuf(kt));
-      if (kt + 1 < n_kt) dload_v(kt + 1, Vbuf(kt + 1));
+      if (kt + 2 < kt_end) dload_k(kt + 2, Kbuf(kt));
+      if (kt + 1 < kt_end) dload_v(kt + 1, Vbuf(kt + 1));
     } else {
-      if (kt + 2 < n_kt) gload_k(kt + 2);
-      if (kt + 1 < n_kt) gload_v(kt + 1);
+      if (kt + 2 < kt_end) gload_k(kt + 2);
+      if (kt + 1 < kt_end) gload_v(kt + 1);
     }
     f16x8 pk[4];
     // phase A (the score MFMAs of the last iteration read a stale buffer and
@@ -408,7 +428,7 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
       // keep those exponentials here: they are only read in phase B
       asm volatile("" : "+v"(pk[0]), "+v"(pk[1]));
     }
-    const bool more = kt + 1 < n_kt;
+    const bool more = kt + 1 < kt_end;
     if (more && (kt + 1) * KT + KT - 1 > kmin) {
       asm volatile("");   // a real branch: only the last tiles of a query block need the mask
       mask_tile(sn, kt + 1);
@@ -443,24 +463,27 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
     if (more) update_max(mx);
     if constexpr (DIRECT) {
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      if (kt + 2 == n_kt) vfix(kt + 1, Vbuf(kt + 1));
+      if (kt + 2 == kt_end) vfix(kt + 1, Vbuf(kt + 1));
     } else {
-      if (kt + 2 < n_kt) lstore_k(Kbuf(kt));
+      if (kt + 2 < kt_end) lstore_k(Kbuf(kt));
       if (more) lstore_v(Vbuf(kt + 1));
     }
     __syncthreads();
   };
-  int kt = 0;
-  for (; kt + 1 < n_kt; kt += 2) {
+  int kt = kt0;
+  for (; kt + 1 < kt_end; kt += 2) {
     step(kt, s0, s1);
     step(kt + 1, s1, s0);
   }
-  if (kt < n_kt) step(kt, s0, s1);
+  if (kt < kt_end) step(kt, s0, s1);
 
   const float l = l_i + __shfl_xor(l_i, 32);
-  const float inv = 1.0f / l;
+  const float inv = SPLIT ? (l > 0.f ? 1.0f / l : 0.f) : 1.0f / l;
+  if constexpr (SPLIT) {
+    if (qvalid && half == 0) MLpart[(size_t)(split * M + qi) * nq + h] = make_float2(l > 0.f ? m_i : -INFINITY, l);
+  }
   if (qvalid) {
-    _Float16* orow = O + (size_t)qi * nq * HD + h * HD;
+    _Float16* orow = SPLIT ? Opart + ((size_t)(split * M + qi) * nq + h) * HD : O + (size_t)qi * nq * HD + h * HD;
 #pragma unroll
     for (int t = 0; t < HD / 32; ++t)
 #pragma unroll
@@ -473,52 +496,96 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
   }
 }
 
-template <int HD, int NW, bool DIRECT>
+// Merge of the key splits: one wave per (query row, head).  With m_s, l_s
+// and the normalised partial o_s of split s, and M = max m_s over the splits
+// that hold keys of the query: O = sum_s 2^(m_s - M) l_s o_s / sum_s
+// 2^(m_s - M) l_s.  Split 0 always holds key 0, so the denominator is
+// positive.  Splits past the one holding the query's own position were not
+// written for it and are not read.
+template <int HD>
+__global__ __launch_bounds__(256) void attn_merge_kernel(const _Float16* __restrict__ Opart,
+                                                         const float2* __restrict__ MLpart,
+                                                         const int32_t* __restrict__ qpos, int M, int nq,
+                                                         int n_split, int tps, _Float16* __restrict__ O) {
+  constexpr int DPL = HD / 64;   // dimensions per lane (1 or 2)
+  const int wv = (int)((blockIdx.x * blockDim.x + threadIdx.x) >> 6);
+  const int lane = threadIdx.x & 63;
+  if (wv >= M * nq) return;      // whole waves leave together
+  const int qi = wv / nq, h = wv % nq;
+  const int nv = min(n_split, (qpos[qi] / KT) / tps + 1);
+  float mx = -INFINITY;
+  for (int sp = 0; sp < nv; ++sp) mx = fmaxf(mx, MLpart[(size_t)(sp * M + qi) * nq + h].x);
+  float acc[DPL] = {};
+  float den = 0.f;
+  for (int sp = 0; sp < nv; ++sp) {
+    const float2 ml = MLpart[(size_t)(sp * M + qi) * nq + h];
+    if (!(ml.y > 0.f)) continue;
+    const float wgt = exp2f(ml.x - mx) * ml.y;
+    den += wgt;
+    const _Float16* src = Opart + ((size_t)(sp * M + qi) * nq + h) * HD + lane * DPL;
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) acc[e] = __builtin_fmaf(wgt, (float)src[e], acc[e]);
+  }
+  const float inv = 1.0f / den;
+  _Float16* dst = O + (size_t)qi * nq * HD + h * HD + lane * DPL;
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) dst[e] = (_Float16)(acc[e] * inv);
+}
+
+struct SplitArgs {
+  int tps = 0, n_split = 1;
+  _Float16* opart = nullptr;
+  float2* ml = nullptr;
+};
+
+template <int HD, int NW, bool DIRECT, bool SPLIT>
 void launch_nwd(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S, const int32_t* table,
                int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group, int qw, float scale_log2,
-               _Float16* O, hipStream_t s) {
+               _Float16* O, const SplitArgs& sa, hipStream_t s) {
   const size_t lds_bytes = 2 * (k_tile_halves<HD>() + v_tile_halves<HD>()) * sizeof(_Float16);
   static const bool attr = [&] {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<HD, NW, DIRECT>),
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<HD, NW, DIRECT, SPLIT>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
     return true;
   }();
   (void)attr;
   const int bq = 32 * qw;
   const int n_qtiles = (m + bq - 1) / bq;
+  // a multiple of 8, so a split's workgroups keep the XCD mapping of blockIdx.x
   const int blocks = (8 % nkv == 0) ? 8 * ((n_qtiles + 8 / nkv - 1) / (8 / nkv))
                                     : 8 * ((n_qtiles + 7) / 8) * nkv;
-  hipLaunchKernelGGL((attn_kernel<HD, NW, DIRECT>), dim3(blocks), dim3(64 * NW), lds_bytes, s, Q, qpos, m, S,
-                     table, C, cshift, slot_bytes, nq, nkv, group, qw, n_qtiles, scale_log2, O);
+  hipLaunchKernelGGL((attn_kernel<HD, NW, DIRECT, SPLIT>), dim3(blocks, SPLIT ? sa.n_split : 1), dim3(64 * NW),
+                     lds_bytes, s, Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, n_qtiles,
+                     scale_log2, O, sa.tps, sa.opart, sa.ml);
 }
 
-template <int HD, int NW>
+template <int HD, int NW, bool SPLIT>
 void launch_nw(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S, const int32_t* table,
                int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group, int qw, float scale_log2,
-               _Float16* O, hipStream_t s) {
+               _Float16* O, const SplitArgs& sa, hipStream_t s) {
   if (C >= KT)
-    launch_nwd<HD, NW, true>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, s);
+    launch_nwd<HD, NW, true, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2,
+                                    O, sa, s);
   else
-    launch_nwd<HD, NW, false>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, s);
+    launch_nwd<HD, NW, false, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2,
+                                     O, sa, s);
 }
 
-template <int HD>
+template <int HD, bool SPLIT>
 void launch_hd(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S, const int32_t* table,
                int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group, int qw, float scale_log2,
-               _Float16* O, hipStream_t s) {
+               _Float16* O, const SplitArgs& sa, hipStream_t s) {
   switch (group * qw) {
-    case 5: launch_nw<HD, 5>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, s); break;
-    case 6: launch_nw<HD, 6>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, s); break;
-    case 7: launch_nw<HD, 7>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, s); break;
-    default: launch_nw<HD, 8>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, s); break;
+    case 5: launch_nw<HD, 5, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, sa, s); break;
+    case 6: launch_nw<HD, 6, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, sa, s); break;
+    case 7: launch_nw<HD, 7, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, sa, s); break;
+    default: launch_nw<HD, 8, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, sa, s); break;
   }
 }
 
-}  // namespace
-
-void launch_attention(const void* q, const int32_t* qpos, int m, const void* slab,
-                      const int32_t* table, int chunk_tokens, int64_t slot_bytes, int n_q,
-                      int n_kv, int head_dim, void* out, hipStream_t s) {
+void launch_any(const void* q, const int32_t* qpos, int m, const void* slab, const int32_t* table,
+                int chunk_tokens, int64_t slot_bytes, int n_q, int n_kv, int head_dim, void* out,
+                const SplitArgs& sa, bool split, hipStream_t s) {
   const int group = n_q / n_kv;          // 1..8
   // 32-query row groups per workgroup: 5..8 waves, so one staged K/V tile
   // serves as many queries as the registers allow
@@ -529,10 +596,70 @@ void launch_attention(const void* q, const int32_t* qpos, int m, const void* sla
   _Float16* O = reinterpret_cast<_Float16*>(out);
   int cshift = 0;
   while ((1 << cshift) < chunk_tokens) ++cshift;   // chunk_tokens is a power of two
+  if (head_dim == 128) {
+    if (split) launch_hd<128, true>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, scale_log2, O, sa, s);
+    else launch_hd<128, false>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, scale_log2, O, sa, s);
+  } else {
+    if (split) launch_hd<64, true>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, scale_log2, O, sa, s);
+    else launch_hd<64, false>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, scale_log2, O, sa, s);
+  }
+}
+
+}  // namespace
+
+void launch_attention(const void* q, const int32_t* qpos, int m, const void* slab,
+                      const int32_t* table, int chunk_tokens, int64_t slot_bytes, int n_q,
+                      int n_kv, int head_dim, void* out, hipStream_t s) {
+  launch_any(q, qpos, m, slab, table, chunk_tokens, slot_bytes, n_q, n_kv, head_dim, out, SplitArgs(), false, s);
+}
+
+int64_t attention_split_ws_bytes(int m, int n_q, int head_dim, int n_split) {
+  const int64_t o = (int64_t)n_split * m * n_q * head_dim * 2;
+  return ((o + 255) / 256) * 256 + (int64_t)n_split * m * n_q * 8;
+}
+
+int attention_split_tiles(int max_pos, int n_split) {
+  const int n_kt = max_pos / KT + 1;
+  return (n_kt + n_split - 1) / n_split;
+}
+
+int attention_auto_splits(int m, int max_pos, int n_q, int n_kv, int head_dim, int64_t ws_cap) {
+  const int group = n_q / n_kv;
+  const int qw = group >= 8 ? 1 : 8 / group;
+  const int n_qtiles = (m + 32 * qw - 1) / (32 * qw);
+  const int wgs = n_qtiles * n_kv;
+  const int n_kt = max_pos / KT + 1;
+  // two workgroups per CU (their LDS fits twice) over 256 CUs, at least 4
+  // key tiles per split, and partials that fit the workspace
+  constexpr int kTarget = 512, kMinTiles = 4, kMaxSplits = 64;
+  if (wgs >= kTarget / 2 || n_kt < 2 * kMinTiles) return 1;
+  int ns = std::min({(kTarget + wgs - 1) / wgs, n_kt / kMinTiles, kMaxSplits});
+  while (ns > 1 && attention_split_ws_bytes(m, n_q, head_dim, ns) > ws_cap) --ns;
+  if (ns <= 1) return 1;
+  const int tps = (n_kt + ns - 1) / ns;
+  return (n_kt + tps - 1) / tps;   // no empty trailing split
+}
+
+void launch_attention_split(const void* q, const int32_t* qpos, int m, int max_pos, const void* slab,
+                            const int32_t* table, int chunk_tokens, int64_t slot_bytes, int n_q, int n_kv,
+                            int head_dim, int n_split, void* ws, void* out, hipStream_t s) {
+  SplitArgs sa;
+  sa.tps = attention_split_tiles(max_pos, n_split);
+  const int n_kt = max_pos / KT + 1;
+  sa.n_split = (n_kt + sa.tps - 1) / sa.tps;
+  sa.opart = reinterpret_cast<_Float16*>(ws);
+  const int64_t o = (int64_t)sa.n_split * m * n_q * head_dim * 2;
+  sa.ml = reinterpret_cast<float2*>(reinterpret_cast<uint8_t*>(ws) + ((o + 255) / 256) * 256);
+  launch_any(q, qpos, m, slab, table, chunk_tokens, slot_bytes, n_q, n_kv, head_dim, out, sa, true, s);
+  const int waves = m * n_q;
+  const dim3 grid((unsigned)((waves + 3) / 4));
+  _Float16* O = reinterpret_cast<_Float16*>(out);
   if (head_dim == 128)
-    launch_hd<128>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, scale_log2, O, s);
+    hipLaunchKernelGGL(attn_merge_kernel<128>, grid, dim3(256), 0, s, sa.opart, sa.ml, qpos, m, n_q, sa.n_split,
+                       sa.tps, O);
   else
-    launch_hd<64>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, scale_log2, O, s);
+    hipLaunchKernelGGL(attn_merge_kernel<64>, grid, dim3(256), 0, s, sa.opart, sa.ml, qpos, m, n_q, sa.n_split,
+                       sa.tps, O);
 }
 
 }  // namespace mzk

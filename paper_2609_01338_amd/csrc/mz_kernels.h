@@ -30,6 +30,18 @@ void launch_attention(const void* q, const int32_t* qpos, int m, const void* sla
                       const int32_t* table, int chunk_tokens, int64_t slot_bytes, int n_q,
                       int n_kv, int head_dim, void* out, hipStream_t s);
 
+// Split-key attention for few query rows: n_split key ranges of whole 64-key
+// tiles (tiles per split = ceil((max_pos / 64 + 1) / n_split)) run as separate
+// workgroups writing partials into ws, then a merge kernel writes out.
+// max_pos >= qpos[m - 1]; ws holds attention_split_ws_bytes(m, n_q,
+// head_dim, n_split) bytes.
+void launch_attention_split(const void* q, const int32_t* qpos, int m, int max_pos, const void* slab,
+                            const int32_t* table, int chunk_tokens, int64_t slot_bytes, int n_q, int n_kv,
+                            int head_dim, int n_split, void* ws, void* out, hipStream_t s);
+int64_t attention_split_ws_bytes(int m, int n_q, int head_dim, int n_split);
+// Splits that fill the chip for this shape within ws_cap bytes (1: no split).
+int attention_auto_splits(int m, int max_pos, int n_q, int n_kv, int head_dim, int64_t ws_cap);
+
 // x f16 [m][d] = RMSNorm(h float [m][d]).
 void launch_rmsnorm(const float* h, int m, int d, float eps, void* x, hipStream_t s);
 

@@ -437,6 +437,10 @@ struct mz_ctx {
   bool kv_codec = false;
   int64_t comp_bytes = 0;            // compressed size of one chunk
   uint8_t* codec_stage = nullptr;    // [max_chunks][comp_bytes]
+  // split-key attention partials (few query rows against a long context)
+  uint8_t* att_ws = nullptr;
+  int64_t att_ws_bytes = 0;
+  bool attn_split = true;            // option attn_split
   int32_t* d_codec_slots = nullptr;  // per restore: destination slot of each compressed chunk
   hipEvent_t ev_meta = nullptr;      // restore metadata uploaded (the swap stream reads some)
   bool timing = false;
@@ -907,9 +911,17 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
     else
       keys = S;
     const double att_flops = 4.0 * x->hd * x->nq * keys;
+    // few query rows against a long context: split the keys over the chip
+    const int max_pos = l + 1 < L ? rows.R[l + 1].back() : S - 1;
+    const int n_split =
+        x->attn_split ? mzk::attention_auto_splits(nq, max_pos, x->nq, x->nkv, x->hd, x->att_ws_bytes) : 1;
     x->timed(kKAttention, att_flops, (double)nq * x->dq * 4.0, cs, [&] {
-      mzk::launch_attention(x->q16, posq, nq, x->kv_slab, x->d_tables + (size_t)l * MC, C, x->slot_bytes,
-                            x->nq, x->nkv, x->hd, x->xb, cs);
+      if (n_split > 1)
+        mzk::launch_attention_split(x->q16, posq, nq, max_pos, x->kv_slab, x->d_tables + (size_t)l * MC, C,
+                                    x->slot_bytes, x->nq, x->nkv, x->hd, n_split, x->att_ws, x->xb, cs);
+      else
+        mzk::launch_attention(x->q16, posq, nq, x->kv_slab, x->d_tables + (size_t)l * MC, C, x->slot_bytes,
+                              x->nq, x->nkv, x->hd, x->xb, cs);
     });
     x->timed(kKGemmO, 2.0 * nq * x->dq * d, (double)d * x->dq * bpe_w + nq * (x->dq * 2.0 + d * 8.0), cs,
              [&] { mzk::launch_gemm_q4(x->xb, nq, x->d_pad, x->dq, unit + x->off_o, mzk::kEpiAdd, h, cs); });
@@ -1109,6 +1121,9 @@ mz_status mz_load_model(const mz_model_cfg* cfg, const void* blob, size_t nbytes
     c.d_tok = (int32_t*)dmalloc((size_t)M * 4);
     c.stage_bytes = (size_t)c.L * c.max_chunks * 8 + (size_t)tot * 24 + (size_t)M * 4 + 9 * 256;
     c.comp_bytes = mzk::kv_compressed_bytes(c.slot_bytes / 2);
+    c.att_ws_bytes = std::min<int64_t>(int64_t(64) << 20,
+                                       mzk::attention_split_ws_bytes(std::min<int64_t>(M, 4096), c.nq, c.hd, 64));
+    c.att_ws = (uint8_t*)dmalloc((size_t)c.att_ws_bytes);
     HIPCHK(hipEventCreateWithFlags(&c.ev_meta, hipEventDisableTiming));
     void* stage = nullptr;
     if (hipHostMalloc(&stage, c.stage_bytes, hipHostMallocDefault) != hipSuccess || !stage)
@@ -1133,7 +1148,7 @@ void mz_free(mz_ctx* x) {
   (void)hipSetDevice(x->device);
   if (x->s_compute) (void)hipStreamSynchronize(x->s_compute);
   if (x->s_swap) (void)hipStreamSynchronize(x->s_swap);
-  void* dptrs[] = {x->codec_stage, x->d_codec_slots, x->w_slab, x->emb_nib, x->emb_sc, x->lm_nib, x->lm_sc,
+  void* dptrs[] = {x->codec_stage, x->d_codec_slots, x->att_ws, x->w_slab, x->emb_nib, x->emb_sc, x->lm_nib, x->lm_sc,
                    x->rope_cs, x->kv_slab,
                    x->h[0], x->h[1], x->xb, x->qf, x->kvf, x->q16, x->act, x->logits, x->part_val,
                    x->part_idx, x->d_token, x->d_tables, x->d_pos, x->d_kvoff, x->d_dix, x->d_posq,
@@ -1164,6 +1179,7 @@ mz_status mz_set_option(mz_ctx* x, const char* key, int64_t value) {
     else if (k == "debug_swap_delay_us") x->debug_swap_delay_us = value < 0 ? 0 : value;
     else if (k == "debug_poison") x->debug_poison = value != 0;
     else if (k == "swap_trim") x->swap_trim = value != 0;
+    else if (k == "attn_split") x->attn_split = value != 0;
     else if (k == "kv_codec") {
       if (value && !x->codec_stage) {
         HIPCHK(hipMalloc((void**)&x->codec_stage, (size_t)x->max_chunks * (size_t)x->comp_bytes));
@@ -1570,6 +1586,38 @@ mz_status mz_attention(const void* q, const int32_t* qpos, int32_t m, const void
     const int64_t slot_bytes = (int64_t)chunk_tokens * n_kv * head_dim * 2 * 2;
     mzk::launch_attention(q, qpos, m, slab, table, chunk_tokens, slot_bytes, n_q, n_kv, head_dim, out,
                           (hipStream_t)stream);
+    HIPCHK(hipGetLastError());
+  });
+}
+
+int64_t mz_attention_split_workspace_bytes(int32_t m, int32_t n_q, int32_t head_dim, int32_t n_split) {
+  if (m < 1 || n_q < 1 || (head_dim != 64 && head_dim != 128) || n_split < 1) return -1;
+  return mzk::attention_split_ws_bytes(m, n_q, head_dim, n_split);
+}
+
+int32_t mz_attention_auto_splits(int32_t m, int32_t max_pos, int32_t n_q, int32_t n_kv, int32_t head_dim,
+                                 int64_t workspace_bytes) {
+  if (m < 1 || max_pos < 0 || n_kv < 1 || n_q % n_kv || (head_dim != 64 && head_dim != 128)) return 1;
+  return mzk::attention_auto_splits(m, max_pos, n_q, n_kv, head_dim, workspace_bytes);
+}
+
+mz_status mz_attention_split(const void* q, const int32_t* qpos, int32_t m, int32_t max_pos, const void* slab,
+                             const int32_t* table, int32_t n_table, int32_t chunk_tokens, int32_t n_q,
+                             int32_t n_kv, int32_t head_dim, int32_t n_split, void* workspace,
+                             int64_t workspace_bytes, void* out, void* stream) {
+  return guarded(nullptr, [&] {
+    if (!q || !qpos || !slab || !table || !out || !workspace) fail(MZ_EINVAL, "NULL pointer");
+    if (m < 1 || n_table < 1 || max_pos < 0) fail(MZ_EINVAL, "sizes must be positive");
+    if (chunk_tokens < 8 || (chunk_tokens & (chunk_tokens - 1))) fail(MZ_EINVAL, "chunk_tokens must be a power of two >= 8");
+    if (head_dim != 64 && head_dim != 128) fail(MZ_EINVAL, "head_dim must be 64 or 128");
+    if (n_kv < 1 || n_q % n_kv || n_q / n_kv > 8) fail(MZ_EINVAL, "bad head counts");
+    if (max_pos / chunk_tokens >= n_table) fail(MZ_EINVAL, "table does not cover max_pos");
+    if (n_split < 1 || n_split > 1024) fail(MZ_EINVAL, "n_split must be 1..1024");
+    if (workspace_bytes < mzk::attention_split_ws_bytes(m, n_q, head_dim, n_split))
+      fail(MZ_EINVAL, "workspace too small for %d splits", n_split);
+    const int64_t slot_bytes = (int64_t)chunk_tokens * n_kv * head_dim * 2 * 2;
+    mzk::launch_attention_split(q, qpos, m, max_pos, slab, table, chunk_tokens, slot_bytes, n_q, n_kv, head_dim,
+                                n_split, workspace, out, (hipStream_t)stream);
     HIPCHK(hipGetLastError());
   });
 }

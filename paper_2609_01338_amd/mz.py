@@ -108,6 +108,9 @@ def lib() -> ctypes.CDLL:
         "mz_plan_evict": ([ctypes.POINTER(mz_model_cfg), ctypes.POINTER(mz_evict_request), vp, vp, vp], i32),
         "mz_kv_compress": ([vp, i64, vp, vp], i32),
         "mz_kv_decompress": ([vp, i64, vp, vp], i32),
+        "mz_attention_split": ([vp, vp, i32, i32, vp, vp, i32, i32, i32, i32, i32, i32, vp, i64, vp, vp], i32),
+        "mz_attention_split_workspace_bytes": ([i32, i32, i32, i32], i64),
+        "mz_attention_auto_splits": ([i32, i32, i32, i32, i32, i64], i32),
         "mz_plan_evict_size": ([ctypes.POINTER(mz_model_cfg), i32, ctypes.POINTER(mz_evict_size_request),
                                 vp, vp, vp, vp, vp, vp], i32),
         "mz_evict_size": ([vp, ctypes.POINTER(mz_evict_size_request), vp], i32),
@@ -321,6 +324,21 @@ def mz_attention(q_ptr: int, qpos_ptr: int, m: int, slab_ptr: int, table_ptr: in
                  stream: Optional[int] = None) -> None:
     _check(lib().mz_attention(q_ptr, qpos_ptr, m, slab_ptr, table_ptr, n_table, chunk_tokens, n_q,
                               n_kv, head_dim, out_ptr, stream), None)
+
+
+def mz_attention_split(q_ptr: int, qpos_ptr: int, m: int, max_pos: int, slab_ptr: int, table_ptr: int,
+                       n_table: int, chunk_tokens: int, n_q: int, n_kv: int, head_dim: int, n_split: int,
+                       ws_ptr: int, ws_bytes: int, out_ptr: int, stream: Optional[int] = None) -> None:
+    _check(lib().mz_attention_split(q_ptr, qpos_ptr, m, max_pos, slab_ptr, table_ptr, n_table, chunk_tokens, n_q,
+                                    n_kv, head_dim, n_split, ws_ptr, ws_bytes, out_ptr, stream), None)
+
+
+def mz_attention_split_workspace_bytes(m: int, n_q: int, head_dim: int, n_split: int) -> int:
+    return int(lib().mz_attention_split_workspace_bytes(m, n_q, head_dim, n_split))
+
+
+def mz_attention_auto_splits(m: int, max_pos: int, n_q: int, n_kv: int, head_dim: int, ws_bytes: int) -> int:
+    return int(lib().mz_attention_auto_splits(m, max_pos, n_q, n_kv, head_dim, ws_bytes))
 
 
 def mz_rmsnorm(h_ptr: int, m: int, d: int, eps: float, x_ptr: int, stream: Optional[int] = None) -> None:

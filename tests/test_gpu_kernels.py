@@ -98,9 +98,11 @@ def test_gemm_full_layer_shapes(key):
         _gemm_case(M, N, K, epi, seed=100 + i, sample_rows=rows)
 
 
-def _attn_case(nq, nkv, hd, C, S, qpos, seed, sample=None):
+def _attn_case(nq, nkv, hd, C, S, qpos, seed, sample=None, n_split=None):
+    """n_split: None for mz_attention, else mz_attention_split with that many
+    key splits ("auto": the restore's choice)."""
     torch = torch_cuda()
-    report("attention", nq=nq, nkv=nkv, hd=hd, C=C, S=S, m=len(qpos), seed=seed)
+    report("attention", nq=nq, nkv=nkv, hd=hd, C=C, S=S, m=len(qpos), seed=seed, n_split=n_split)
     rng = np.random.default_rng(seed)
     dkv = nkv * hd
     nch = (S + C - 1) // C
@@ -124,8 +126,18 @@ def _attn_case(nq, nkv, hd, C, S, qpos, seed, sample=None):
     d_slab = torch.from_numpy(slab).cuda()
     d_tab = torch.from_numpy(table).cuda()
     out = torch.empty(M, nq * hd, device="cuda", dtype=torch.float16)
-    mz.mz_attention(d_q.data_ptr(), d_pos.data_ptr(), M, d_slab.data_ptr(), d_tab.data_ptr(), nch, C,
-                    nq, nkv, hd, out.data_ptr(), stream())
+    max_pos = int(qpos[-1])
+    if n_split is None:
+        mz.mz_attention(d_q.data_ptr(), d_pos.data_ptr(), M, d_slab.data_ptr(), d_tab.data_ptr(), nch, C,
+                        nq, nkv, hd, out.data_ptr(), stream())
+    else:
+        if n_split == "auto":
+            n_split = mz.mz_attention_auto_splits(M, max_pos, nq, nkv, hd, 64 << 20)
+            report("  auto splits", n_split=n_split)
+        wsb = mz.mz_attention_split_workspace_bytes(M, nq, hd, n_split)
+        ws = torch.empty(wsb, device="cuda", dtype=torch.uint8)
+        mz.mz_attention_split(d_q.data_ptr(), d_pos.data_ptr(), M, max_pos, d_slab.data_ptr(), d_tab.data_ptr(),
+                              nch, C, nq, nkv, hd, n_split, ws.data_ptr(), wsb, out.data_ptr(), stream())
     torch.cuda.synchronize()
     got = out.float().cpu().numpy().reshape(M, nq, hd).astype(np.float64)
     rows = np.arange(M) if sample is None else sample
@@ -134,6 +146,11 @@ def _attn_case(nq, nkv, hd, C, S, qpos, seed, sample=None):
                                  V.astype(np.float64).reshape(S, nkv, hd))
     g = got[rows]
     bound = REL * np.abs(ref) + 2.0 ** -10 * float(np.abs(V).max())
+    if n_split is not None:
+        # each split's normalised output is a convex combination of V rows,
+        # rounded to f16 (half an ulp: 2^-11 max|V|); the merge is again a
+        # convex combination of those
+        bound = bound + 2.0 ** -11 * float(np.abs(V).max())
     err = np.abs(g - ref)
     report("  err", max=float(err.max()), worst_ratio=float((err / bound).max()))
     assert np.all(np.isfinite(g))
@@ -164,6 +181,44 @@ def test_attention_full_context(key):
     sample = np.unique(np.concatenate([rng.choice(S, 12, replace=False), [0, S - 1]]))
     _attn_case(m.n_q_heads, m.n_kv_heads, m.head_dim, m.chunk_tokens, S, np.arange(S), seed=5,
                sample=sample)
+
+
+@pytest.mark.parametrize("nq,nkv,hd,C,S", [
+    (4, 2, 64, 16, 700), (32, 8, 128, 256, 2000), (24, 8, 128, 256, 1500), (12, 2, 128, 256, 1100),
+    (8, 8, 128, 64, 900), (6, 1, 64, 32, 800), (4, 4, 128, 8, 333)])
+def test_attention_split(nq, nkv, hd, C, S):
+    """Split-key attention against the exact definition: prompt-like tails,
+    one row, rows far apart (early rows see no key of the later splits), and
+    a row at position 0; 2..64 splits (one tile per split at the top)."""
+    rng = np.random.default_rng(S + nq)
+    cases = [np.arange(S - 9, S), [S - 1], [3, S // 2, S - 1], np.concatenate([[10], np.arange(S - 70, S)]),
+             np.sort(rng.choice(S, 40, replace=False)), [0]]
+    for i, qp in enumerate(cases):
+        for n_split in (2, 5, "auto", 64):
+            _attn_case(nq, nkv, hd, C, S, qp, seed=20 + i, n_split=n_split)
+
+
+@pytest.mark.parametrize("m", [1, 129])
+def test_attention_split_8b_context(m):
+    """The 8B layer at its full context (32768 cached + 128 prompt tokens):
+    the last m rows, as the restore runs them when nothing before the prompt
+    is recomputed, with the restore's split choice; every row checked."""
+    w = W.WORKLOADS["8b"]
+    mdl = w.model
+    S = w.n_ctx + w.n_prompt
+    _attn_case(mdl.n_q_heads, mdl.n_kv_heads, mdl.head_dim, mdl.chunk_tokens, S, np.arange(S - m, S), seed=9,
+               n_split="auto")
+
+
+def test_attention_split_validation():
+    torch_cuda()
+    with pytest.raises(mz.MzError):
+        mz.mz_attention_split(1, 1, 4, 100, 1, 1, 1, 16, 8, 2, 64, 2, 1, 10, 1)   # table short of max_pos
+    with pytest.raises(mz.MzError):
+        mz.mz_attention_split(1, 1, 4, 10, 1, 1, 1, 16, 8, 2, 64, 2, 1, 10, 1)    # workspace too small
+    assert mz.mz_attention_auto_splits(40000, 40000, 32, 8, 128, 64 << 20) == 1   # the chip is full already
+    assert 32 <= mz.mz_attention_auto_splits(1, 32895, 32, 8, 128, 64 << 20) <= 64
+    assert mz.mz_attention_auto_splits(129, 32895, 32, 8, 128, 64 << 20) > 8
 
 
 @pytest.mark.parametrize("M,d", [(1, 256), (300, 2048), (77, 4096), (5, 1536)])
