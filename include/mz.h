@@ -139,7 +139,8 @@ mz_status mz_first_token(mz_ctx *ctx, int32_t *token_out, float *logits_out);
  * enabling it the first time allocates a device staging ring of one layer's
  * chunks), "attn_split" (1: attention of few query rows against a long
  * context runs split over the keys, as mz_attention_split, default; 0: always
- * one pass), "swap_trim" (1: free the pinned swap segments after each restore,
+ * one pass), "gemm_split" (1: GEMMs of few rows run split over K, as
+ * mz_q4_gemm_split, default; 0: never), "swap_trim" (1: free the pinned swap segments after each restore,
  * as the paper's growing swap stack does; 0: keep them for the next
  * eviction, default).  Test hooks: "debug_poison" (1: fill every
  * slot and weight unit allocated by a restore with NaN before it is
@@ -313,6 +314,29 @@ mz_status mz_q4_gemm_pack(const void *w, const void *w_up, int32_t n, int32_t k,
  * 2: y f16 [m][n_pad/2] = silu(gate) * up (W packed with w_up). */
 mz_status mz_q4_gemm(const void *x_f16, int32_t m, int32_t n_pad, int32_t k,
                      const void *w_packed, int32_t epilogue, void *y, void *stream);
+
+/* Split-K form of mz_q4_gemm for few rows (the short requests of the
+ * paper's evaluation, Sec. 6, and every decode step): a grid of 256-column
+ * tiles alone leaves most of the GPU idle there.  The k / 64 steps are cut
+ * into n_split ranges of ceil((k / 64) / n_split) steps; each range runs as
+ * its own workgroups and leaves its fp32 sums in workspace; a second kernel
+ * adds the ranges in order and applies the epilogue, so results are
+ * deterministic and equal mz_q4_gemm's up to the order of the fp32 sums.
+ * workspace: device, caller-owned, at least
+ * mz_q4_gemm_split_workspace_bytes(m, n_pad, n_split) bytes, not shared by
+ * calls in flight together.  Other arguments and errors as mz_q4_gemm; EINVAL
+ * also for n_split outside 1..1024 or a short workspace. */
+mz_status mz_q4_gemm_split(const void *x_f16, int32_t m, int32_t n_pad, int32_t k,
+                           const void *w_packed, int32_t epilogue, void *y, int32_t n_split,
+                           void *workspace, int64_t workspace_bytes, void *stream);
+
+/* Workspace bytes of mz_q4_gemm_split (-1 for invalid arguments). */
+int64_t mz_q4_gemm_split_workspace_bytes(int32_t m, int32_t n_pad, int32_t n_split);
+
+/* The split count the restore uses for this shape with workspace_bytes of
+ * workspace: about two workgroups per compute unit, at least 4 K steps per
+ * split, at most 32 splits; 1 when the tile grid already fills the GPU. */
+int32_t mz_q4_gemm_auto_splits(int32_t m, int32_t n_pad, int32_t k, int64_t workspace_bytes);
 
 /* Causal GQA attention of q (f16 [m][n_q_heads][head_dim], rotated) at
  * positions qpos (int32 [m], ascending) over the KV chunks of one layer:

@@ -28,6 +28,8 @@
 // MFMA 16x16x32 operand layout (checked on gfx950): lane l feeds row/column
 // l % 16 with the 8 consecutive k of group l / 16; the accumulator holds rows
 // 4 * (l / 16) + r (r = 0..3) of column l % 16.
+#include <algorithm>
+
 #include "mz_kernels.h"
 
 namespace mzk {
@@ -83,11 +85,16 @@ __device__ __forceinline__ void dequant_block_to_lds(uint4 nib, uint16_t dbits, 
 // BM = 256 (large m) or 64 (few row tiles: four times as many workgroups; the
 // arithmetic of every output element is the same, so results do not depend
 // on the choice).
+//
+// Split K (EPI == kEpiPartial): blockIdx.y is a split that takes K steps
+// [y * k_steps, min((y + 1) * k_steps, K / 64)) and stores its fp32 sums in
+// Y as [split][M][N]; gemm_splitk_reduce adds the splits in order and applies
+// the real epilogue.
 template <int EPI, int BM>
 __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict__ X,
                                                      const int32_t* __restrict__ a_rows, int M, int K,
                                                      const uint8_t* __restrict__ Wp, int N,
-                                                     void* __restrict__ Y) {
+                                                     void* __restrict__ Y, int k_steps) {
   extern __shared__ __attribute__((aligned(16))) _Float16 lds[];
   constexpr int A_TILE = BM * ROW;                     // one activation stage
   constexpr int MI = BM / 64;                          // 16-row MFMA tiles per wave
@@ -106,7 +113,9 @@ __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict_
   const int per = total / 8;
   const int t = b < per * 8 ? (b % 8) * per + b / 8 : b;
   const int mt = t / n_tiles, nt = t % n_tiles;
-  const int nk = K / BK;
+  const int split = EPI == kEpiPartial ? (int)blockIdx.y : 0;
+  const int ks0 = EPI == kEpiPartial ? split * k_steps : 0;
+  const int nk = EPI == kEpiPartial ? min(k_steps, K / BK - ks0) : K / BK;
 
   // direct A loads: wave w fills rows RW*w .. RW*w+RW-1 with MI instructions
   // of 8 rows; lane l lands at LDS (row 8i + l/8, physical column l%8), which
@@ -118,11 +127,11 @@ __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict_
     const int pr = wave * RW + i * 8 + (lane >> 3);
     const int lc = (lane & 7) ^ ((pr >> 1) & 7);
     const int r = min(mt * BM + pr, M - 1);
-    a_src[i] = X + (size_t)(a_rows ? a_rows[r] : r) * K + lc * 8;
+    a_src[i] = X + (size_t)(a_rows ? a_rows[r] : r) * K + (size_t)ks0 * BK + lc * 8;
   }
   // weight loads: one Q4_0 block per thread; 8 consecutive lanes take 8 rows of
   // the same block so their LDS stores land in distinct banks
-  const uint8_t* wtile = Wp + (size_t)nt * nk * kGemmTileBytes;
+  const uint8_t* wtile = Wp + ((size_t)nt * (K / BK) + ks0) * kGemmTileBytes;
   const int b_row = (tid & 7) | ((tid >> 4) << 3), b_blk = (tid >> 3) & 1;
   const int b_idx = b_row * 2 + b_blk;
 
@@ -218,7 +227,7 @@ __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict_
           y[col] = (_Float16)(silu(g) * u);
         }
       } else {
-        float* y = reinterpret_cast<float*>(Y) + (size_t)row * N;
+        float* y = reinterpret_cast<float*>(Y) + ((size_t)split * M + row) * N;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           const int col = nt * BN + wn * 128 + j * 16 + col_in;
@@ -232,6 +241,49 @@ __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict_
   }
 }
 
+// Sum of the K splits in split order, then the epilogue; 4 columns per
+// thread (SwiGLU: 4 output columns, whose gate and up sums are 4 consecutive
+// columns each: output column o takes gate column 32 (o / 16) + o % 16 and the
+// up column 16 after it).
+template <int EPI>
+__global__ __launch_bounds__(256) void gemm_splitk_reduce(const float* __restrict__ part, int ns, int M, int N,
+                                                          void* __restrict__ Y) {
+  const int NO = EPI == kEpiSwiGLU ? N / 2 : N;       // output columns
+  const int64_t i4 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i4 * 4 >= (int64_t)M * NO) return;
+  const int row = (int)(i4 * 4 / NO), o = (int)(i4 * 4 % NO);
+  const size_t plane = (size_t)M * N;
+  if constexpr (EPI == kEpiSwiGLU) {
+    const int cg = 32 * (o / 16) + o % 16;
+    const float* pg = part + (size_t)row * N + cg;
+    float4 g = *reinterpret_cast<const float4*>(pg), u = *reinterpret_cast<const float4*>(pg + 16);
+    for (int sp = 1; sp < ns; ++sp) {
+      const float4 g2 = *reinterpret_cast<const float4*>(pg + sp * plane);
+      const float4 u2 = *reinterpret_cast<const float4*>(pg + sp * plane + 16);
+      g.x += g2.x; g.y += g2.y; g.z += g2.z; g.w += g2.w;
+      u.x += u2.x; u.y += u2.y; u.z += u2.z; u.w += u2.w;
+    }
+    _Float16* y = reinterpret_cast<_Float16*>(Y) + (size_t)row * NO + o;
+    y[0] = (_Float16)(silu(g.x) * u.x);
+    y[1] = (_Float16)(silu(g.y) * u.y);
+    y[2] = (_Float16)(silu(g.z) * u.z);
+    y[3] = (_Float16)(silu(g.w) * u.w);
+  } else {
+    const float* pp = part + (size_t)row * N + o;
+    float4 a = *reinterpret_cast<const float4*>(pp);
+    for (int sp = 1; sp < ns; ++sp) {
+      const float4 b = *reinterpret_cast<const float4*>(pp + sp * plane);
+      a.x += b.x; a.y += b.y; a.z += b.z; a.w += b.w;
+    }
+    float4* y = reinterpret_cast<float4*>(reinterpret_cast<float*>(Y) + (size_t)row * N + o);
+    if (EPI == kEpiAdd) {
+      const float4 c = *y;
+      a.x += c.x; a.y += c.y; a.z += c.z; a.w += c.w;
+    }
+    *y = a;
+  }
+}
+
 template <int BM>
 constexpr size_t lds_bytes() {
   return ((size_t)A_STAGES * BM * ROW + (size_t)B_STAGES * B_TILE) * sizeof(_Float16);
@@ -239,7 +291,7 @@ constexpr size_t lds_bytes() {
 
 template <int EPI, int BM>
 void launch_bm(const _Float16* X, const int32_t* a_rows, int m, int n, int k, const uint8_t* W, void* y,
-               hipStream_t s) {
+               hipStream_t s, int n_split = 1, int k_steps = 0) {
   static const bool lds_ok = [] {   // more than 64 KB of dynamic LDS, once per instantiation
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_q4_kernel<EPI, BM>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes<BM>());
@@ -247,21 +299,64 @@ void launch_bm(const _Float16* X, const int32_t* a_rows, int m, int n, int k, co
   }();
   (void)lds_ok;
   const int tiles = (n / BN) * ((m + BM - 1) / BM);
-  hipLaunchKernelGGL((gemm_q4_kernel<EPI, BM>), dim3(tiles), dim3(NT), lds_bytes<BM>(), s, X, a_rows, m, k,
-                     W, n, y);
+  hipLaunchKernelGGL((gemm_q4_kernel<EPI, BM>), dim3(tiles, n_split), dim3(NT), lds_bytes<BM>(), s, X, a_rows,
+                     m, k, W, n, y, k_steps);
 }
+
+int gemm_row_tile(int m, int n) { return (n / BN) * ((m + 255) / 256) < 128 ? 64 : 256; }
 
 template <int EPI>
 void launch_epi(const _Float16* X, const int32_t* a_rows, int m, int n, int k, const uint8_t* W, void* y,
                 hipStream_t s) {
   // 256-row tiles unless they leave most of the 256 CUs idle
-  if ((n / BN) * ((m + 255) / 256) < 128)
+  if (gemm_row_tile(m, n) == 64)
     launch_bm<EPI, 64>(X, a_rows, m, n, k, W, y, s);
   else
     launch_bm<EPI, 256>(X, a_rows, m, n, k, W, y, s);
 }
 
+int gemm_k_steps(int k, int n_split) {
+  const int nk = k / BK;
+  return (nk + n_split - 1) / n_split;
+}
+
 }  // namespace
+
+int64_t gemm_splitk_ws_bytes(int m, int n, int n_split) { return (int64_t)n_split * m * n * 4; }
+
+int gemm_auto_splits(int m, int n, int k, int64_t ws_cap) {
+  const int bm = gemm_row_tile(m, n);
+  const int tiles = (n / BN) * ((m + bm - 1) / bm);
+  const int nk = k / BK;
+  // about two workgroups per CU, at least 4 K steps per split
+  constexpr int kTarget = 512, kMinSteps = 4, kMaxSplits = 32;
+  if (tiles >= kTarget / 2 || nk < 2 * kMinSteps) return 1;
+  int ns = std::min({(kTarget + tiles - 1) / tiles, nk / kMinSteps, kMaxSplits});
+  while (ns > 1 && gemm_splitk_ws_bytes(m, n, ns) > ws_cap) --ns;
+  if (ns <= 1) return 1;
+  const int ks = gemm_k_steps(k, ns);
+  return (nk + ks - 1) / ks;   // no empty trailing split
+}
+
+void launch_gemm_q4_splitk(const void* x, int m, int n, int k, const void* w, int epilogue, void* y, int n_split,
+                           void* ws, hipStream_t s, const int32_t* a_rows) {
+  const _Float16* X = reinterpret_cast<const _Float16*>(x);
+  const uint8_t* W = reinterpret_cast<const uint8_t*>(w);
+  const int ks = gemm_k_steps(k, n_split);
+  const int ns = (k / BK + ks - 1) / ks;
+  if (gemm_row_tile(m, n) == 64)
+    launch_bm<kEpiPartial, 64>(X, a_rows, m, n, k, W, ws, s, ns, ks);
+  else
+    launch_bm<kEpiPartial, 256>(X, a_rows, m, n, k, W, ws, s, ns, ks);
+  const int64_t outs = (int64_t)m * (epilogue == kEpiSwiGLU ? n / 2 : n) / 4;
+  const dim3 grid((unsigned)((outs + 255) / 256));
+  const float* part = reinterpret_cast<const float*>(ws);
+  switch (epilogue) {
+    case kEpiStore: hipLaunchKernelGGL(gemm_splitk_reduce<kEpiStore>, grid, dim3(256), 0, s, part, ns, m, n, y); break;
+    case kEpiAdd: hipLaunchKernelGGL(gemm_splitk_reduce<kEpiAdd>, grid, dim3(256), 0, s, part, ns, m, n, y); break;
+    default: hipLaunchKernelGGL(gemm_splitk_reduce<kEpiSwiGLU>, grid, dim3(256), 0, s, part, ns, m, n, y); break;
+  }
+}
 
 void launch_gemm_q4(const void* x, int m, int n, int k, const void* w, int epilogue, void* y,
                     hipStream_t s, const int32_t* a_rows) {

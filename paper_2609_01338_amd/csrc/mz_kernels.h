@@ -16,7 +16,7 @@ constexpr int kGemmTileN = 256;
 constexpr int kGemmTileK = 64;
 constexpr int kGemmTileBytes = kGemmTileN * kGemmTileK / 2 + kGemmTileN * (kGemmTileK / 32) * 2;
 
-enum GemmEpilogue { kEpiStore = 0, kEpiAdd = 1, kEpiSwiGLU = 2 };
+enum GemmEpilogue { kEpiStore = 0, kEpiAdd = 1, kEpiSwiGLU = 2, kEpiPartial = 3 };
 
 // Y = X . W^T: X f16 [m][k], W packed [n][k] (n % 128 == 0, k % 64 == 0).
 // kEpiStore: Y float [m][n] = acc; kEpiAdd: Y float [m][n] += acc;
@@ -24,6 +24,16 @@ enum GemmEpilogue { kEpiStore = 0, kEpiAdd = 1, kEpiSwiGLU = 2 };
 // With a_rows (device, m entries), output row r is computed from X row a_rows[r].
 void launch_gemm_q4(const void* x, int m, int n, int k, const void* w, int epilogue, void* y,
                     hipStream_t s, const int32_t* a_rows = nullptr);
+
+// Split-K form for few rows: n_split ranges of whole 64-wide K steps
+// (ceil((k / 64) / n_split) steps each) write fp32 partials into ws
+// (gemm_splitk_ws_bytes(m, n, n_split) bytes), then one kernel adds them in
+// split order and applies the epilogue.
+void launch_gemm_q4_splitk(const void* x, int m, int n, int k, const void* w, int epilogue, void* y, int n_split,
+                           void* ws, hipStream_t s, const int32_t* a_rows = nullptr);
+int64_t gemm_splitk_ws_bytes(int m, int n, int n_split);
+// Splits that fill the chip for this shape within ws_cap bytes (1: no split).
+int gemm_auto_splits(int m, int n, int k, int64_t ws_cap);
 
 // Causal GQA attention over chunked KV (see mz.h, mz_attention).
 void launch_attention(const void* q, const int32_t* qpos, int m, const void* slab,

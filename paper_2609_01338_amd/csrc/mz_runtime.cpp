@@ -437,10 +437,23 @@ struct mz_ctx {
   bool kv_codec = false;
   int64_t comp_bytes = 0;            // compressed size of one chunk
   uint8_t* codec_stage = nullptr;    // [max_chunks][comp_bytes]
-  // split-key attention partials (few query rows against a long context)
-  uint8_t* att_ws = nullptr;
-  int64_t att_ws_bytes = 0;
+  // partials of split-key attention and split-K GEMMs (few rows: the
+  // kernels of one layer run in order on the compute stream and share it)
+  uint8_t* split_ws = nullptr;
+  int64_t split_ws_bytes = 0;
   bool attn_split = true;            // option attn_split
+  bool gemm_split = true;            // option gemm_split
+
+  // Y = X W^T on the compute stream, split over K when the tile grid alone
+  // would leave most of the GPU idle
+  void gemm(const void* X, int m, int n, int k, const uint8_t* W, int epi, void* Y, hipStream_t s,
+            const int32_t* rows = nullptr) {
+    const int ns = gemm_split ? mzk::gemm_auto_splits(m, n, k, split_ws_bytes) : 1;
+    if (ns > 1)
+      mzk::launch_gemm_q4_splitk(X, m, n, k, W, epi, Y, ns, split_ws, s, rows);
+    else
+      mzk::launch_gemm_q4(X, m, n, k, W, epi, Y, s, rows);
+  }
   int32_t* d_codec_slots = nullptr;  // per restore: destination slot of each compressed chunk
   hipEvent_t ev_meta = nullptr;      // restore metadata uploaded (the swap stream reads some)
   bool timing = false;
@@ -881,7 +894,7 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
     if (nd > 0) {
       const int32_t* dix = x->d_dix + dofs[l];
       x->timed(kKGemmKV, 2.0 * nd * d * 2 * x->dkv, 2.0 * x->dkv * d * bpe_w + nd * (d * 2.0 + 2 * x->dkv * 4.0), cs,
-               [&] { mzk::launch_gemm_q4(x->xb, nd, x->kv_pad, d, unit + x->off_kv, mzk::kEpiStore, x->kvf, cs, dix); });
+               [&] { x->gemm(x->xb, nd, x->kv_pad, d, unit + x->off_kv, mzk::kEpiStore, x->kvf, cs, dix); });
       x->timed(kKRopeKV, 0, nd * (2 * x->dkv * 4.0 + 2 * x->dkv * 2.0), cs, [&] {
         mzk::launch_rope_kv(x->kvf, x->kv_pad, nd, x->d_pos + dofs[l], x->d_kvoff + dofs[l], x->rope_cs, 0,
                             x->nkv, x->hd, C, nullptr, x->kv_slab, cs);
@@ -893,7 +906,7 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
     const int32_t* qix = x->d_qix + qofs[l];
     const int32_t* posq = x->d_posq + qofs[l];
     x->timed(kKGemmQ, 2.0 * nq * d * x->dq, (double)x->dq * d * bpe_w + nq * (d * 2.0 + x->dq * 4.0), cs,
-             [&] { mzk::launch_gemm_q4(x->xb, nq, x->dq_pad, d, unit + x->off_q, mzk::kEpiStore, x->qf, cs, qix); });
+             [&] { x->gemm(x->xb, nq, x->dq_pad, d, unit + x->off_q, mzk::kEpiStore, x->qf, cs, qix); });
     x->timed(kKRopeQ, 0, nq * (x->dq * 4.0 + x->dq * 2.0), cs, [&] {
       mzk::launch_rope_kv(x->qf, x->dq_pad, nq, posq, nullptr, x->rope_cs, x->nq, 0, x->hd, C, x->q16,
                           x->kv_slab, cs);
@@ -914,23 +927,23 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
     // few query rows against a long context: split the keys over the chip
     const int max_pos = l + 1 < L ? rows.R[l + 1].back() : S - 1;
     const int n_split =
-        x->attn_split ? mzk::attention_auto_splits(nq, max_pos, x->nq, x->nkv, x->hd, x->att_ws_bytes) : 1;
+        x->attn_split ? mzk::attention_auto_splits(nq, max_pos, x->nq, x->nkv, x->hd, x->split_ws_bytes) : 1;
     x->timed(kKAttention, att_flops, (double)nq * x->dq * 4.0, cs, [&] {
       if (n_split > 1)
         mzk::launch_attention_split(x->q16, posq, nq, max_pos, x->kv_slab, x->d_tables + (size_t)l * MC, C,
-                                    x->slot_bytes, x->nq, x->nkv, x->hd, n_split, x->att_ws, x->xb, cs);
+                                    x->slot_bytes, x->nq, x->nkv, x->hd, n_split, x->split_ws, x->xb, cs);
       else
         mzk::launch_attention(x->q16, posq, nq, x->kv_slab, x->d_tables + (size_t)l * MC, C, x->slot_bytes,
                               x->nq, x->nkv, x->hd, x->xb, cs);
     });
     x->timed(kKGemmO, 2.0 * nq * x->dq * d, (double)d * x->dq * bpe_w + nq * (x->dq * 2.0 + d * 8.0), cs,
-             [&] { mzk::launch_gemm_q4(x->xb, nq, x->d_pad, x->dq, unit + x->off_o, mzk::kEpiAdd, h, cs); });
+             [&] { x->gemm(x->xb, nq, x->d_pad, x->dq, unit + x->off_o, mzk::kEpiAdd, h, cs); });
     x->timed(kKRmsnorm, 0, (double)nq * d * 6.0, cs,
              [&] { mzk::launch_rmsnorm(h, nq, d, x->cfg.rms_eps, x->xb, cs); });
     x->timed(kKGemmGateUp, 2.0 * nq * d * 2.0 * x->ff, 2.0 * x->ff * d * bpe_w + nq * (d * 2.0 + x->ff * 2.0), cs,
-             [&] { mzk::launch_gemm_q4(x->xb, nq, 2 * x->ffp, d, unit + x->off_gu, mzk::kEpiSwiGLU, x->act, cs); });
+             [&] { x->gemm(x->xb, nq, 2 * x->ffp, d, unit + x->off_gu, mzk::kEpiSwiGLU, x->act, cs); });
     x->timed(kKGemmDown, 2.0 * nq * x->ff * d, (double)d * x->ff * bpe_w + nq * (x->ffp * 2.0 + d * 8.0), cs,
-             [&] { mzk::launch_gemm_q4(x->act, nq, x->d_pad, x->ffp, unit + x->off_dn, mzk::kEpiAdd, h, cs); });
+             [&] { x->gemm(x->act, nq, x->d_pad, x->ffp, unit + x->off_dn, mzk::kEpiAdd, h, cs); });
     algo += 2.0 * nd * d * 2 * x->dkv + 2.0 * nq * d * 2 * x->dq + 2.0 * nq * 3 * d * x->ff + att_flops;
   }
   x->h_last = x->h[cur];
@@ -1121,9 +1134,10 @@ mz_status mz_load_model(const mz_model_cfg* cfg, const void* blob, size_t nbytes
     c.d_tok = (int32_t*)dmalloc((size_t)M * 4);
     c.stage_bytes = (size_t)c.L * c.max_chunks * 8 + (size_t)tot * 24 + (size_t)M * 4 + 9 * 256;
     c.comp_bytes = mzk::kv_compressed_bytes(c.slot_bytes / 2);
-    c.att_ws_bytes = std::min<int64_t>(int64_t(64) << 20,
-                                       mzk::attention_split_ws_bytes(std::min<int64_t>(M, 4096), c.nq, c.hd, 64));
-    c.att_ws = (uint8_t*)dmalloc((size_t)c.att_ws_bytes);
+    c.split_ws_bytes = std::min<int64_t>(
+        int64_t(64) << 20, std::max(mzk::attention_split_ws_bytes(std::min<int64_t>(M, 4096), c.nq, c.hd, 64),
+                                    mzk::gemm_splitk_ws_bytes(std::min<int64_t>(M, 512), 2 * c.ffp, 8)));
+    c.split_ws = (uint8_t*)dmalloc((size_t)c.split_ws_bytes);
     HIPCHK(hipEventCreateWithFlags(&c.ev_meta, hipEventDisableTiming));
     void* stage = nullptr;
     if (hipHostMalloc(&stage, c.stage_bytes, hipHostMallocDefault) != hipSuccess || !stage)
@@ -1148,7 +1162,7 @@ void mz_free(mz_ctx* x) {
   (void)hipSetDevice(x->device);
   if (x->s_compute) (void)hipStreamSynchronize(x->s_compute);
   if (x->s_swap) (void)hipStreamSynchronize(x->s_swap);
-  void* dptrs[] = {x->codec_stage, x->d_codec_slots, x->att_ws, x->w_slab, x->emb_nib, x->emb_sc, x->lm_nib, x->lm_sc,
+  void* dptrs[] = {x->codec_stage, x->d_codec_slots, x->split_ws, x->w_slab, x->emb_nib, x->emb_sc, x->lm_nib, x->lm_sc,
                    x->rope_cs, x->kv_slab,
                    x->h[0], x->h[1], x->xb, x->qf, x->kvf, x->q16, x->act, x->logits, x->part_val,
                    x->part_idx, x->d_token, x->d_tables, x->d_pos, x->d_kvoff, x->d_dix, x->d_posq,
@@ -1180,6 +1194,7 @@ mz_status mz_set_option(mz_ctx* x, const char* key, int64_t value) {
     else if (k == "debug_poison") x->debug_poison = value != 0;
     else if (k == "swap_trim") x->swap_trim = value != 0;
     else if (k == "attn_split") x->attn_split = value != 0;
+    else if (k == "gemm_split") x->gemm_split = value != 0;
     else if (k == "kv_codec") {
       if (value && !x->codec_stage) {
         HIPCHK(hipMalloc((void**)&x->codec_stage, (size_t)x->max_chunks * (size_t)x->comp_bytes));
@@ -1570,6 +1585,34 @@ mz_status mz_q4_gemm(const void* x_f16, int32_t m, int32_t n_pad, int32_t k, con
     if (k % mzk::kGemmTileK) fail(MZ_EINVAL, "k must be a multiple of %d", mzk::kGemmTileK);
     if (epilogue < 0 || epilogue > 2) fail(MZ_EINVAL, "bad epilogue");
     mzk::launch_gemm_q4(x_f16, m, n_pad, k, w_packed, epilogue, y, (hipStream_t)stream);
+    HIPCHK(hipGetLastError());
+  });
+}
+
+int64_t mz_q4_gemm_split_workspace_bytes(int32_t m, int32_t n_pad, int32_t n_split) {
+  if (m < 1 || n_pad < 1 || n_split < 1) return -1;
+  return mzk::gemm_splitk_ws_bytes(m, n_pad, n_split);
+}
+
+int32_t mz_q4_gemm_auto_splits(int32_t m, int32_t n_pad, int32_t k, int64_t workspace_bytes) {
+  if (m < 1 || n_pad < mzk::kGemmTileN || k < mzk::kGemmTileK) return 1;
+  return mzk::gemm_auto_splits(m, n_pad, k, workspace_bytes);
+}
+
+mz_status mz_q4_gemm_split(const void* x_f16, int32_t m, int32_t n_pad, int32_t k, const void* w_packed,
+                           int32_t epilogue, void* y, int32_t n_split, void* workspace, int64_t workspace_bytes,
+                           void* stream) {
+  return guarded(nullptr, [&] {
+    if (!x_f16 || !w_packed || !y || !workspace) fail(MZ_EINVAL, "NULL pointer");
+    if (m < 1 || n_pad < 1 || k < 1) fail(MZ_EINVAL, "sizes must be positive");
+    if (n_pad % mzk::kGemmTileN) fail(MZ_EINVAL, "n_pad must be a multiple of %d", mzk::kGemmTileN);
+    if (k % mzk::kGemmTileK) fail(MZ_EINVAL, "k must be a multiple of %d", mzk::kGemmTileK);
+    if (epilogue < 0 || epilogue > 2) fail(MZ_EINVAL, "bad epilogue");
+    if (n_split < 1 || n_split > 1024) fail(MZ_EINVAL, "n_split must be 1..1024");
+    if (workspace_bytes < mzk::gemm_splitk_ws_bytes(m, n_pad, n_split))
+      fail(MZ_EINVAL, "workspace too small for %d splits", n_split);
+    mzk::launch_gemm_q4_splitk(x_f16, m, n_pad, k, w_packed, epilogue, y, n_split, workspace,
+                               (hipStream_t)stream);
     HIPCHK(hipGetLastError());
   });
 }

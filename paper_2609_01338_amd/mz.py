@@ -108,6 +108,9 @@ def lib() -> ctypes.CDLL:
         "mz_plan_evict": ([ctypes.POINTER(mz_model_cfg), ctypes.POINTER(mz_evict_request), vp, vp, vp], i32),
         "mz_kv_compress": ([vp, i64, vp, vp], i32),
         "mz_kv_decompress": ([vp, i64, vp, vp], i32),
+        "mz_q4_gemm_split": ([vp, i32, i32, i32, vp, i32, vp, i32, vp, i64, vp], i32),
+        "mz_q4_gemm_split_workspace_bytes": ([i32, i32, i32], i64),
+        "mz_q4_gemm_auto_splits": ([i32, i32, i32, i64], i32),
         "mz_attention_split": ([vp, vp, i32, i32, vp, vp, i32, i32, i32, i32, i32, i32, vp, i64, vp, vp], i32),
         "mz_attention_split_workspace_bytes": ([i32, i32, i32, i32], i64),
         "mz_attention_auto_splits": ([i32, i32, i32, i32, i32, i64], i32),
@@ -324,6 +327,20 @@ def mz_attention(q_ptr: int, qpos_ptr: int, m: int, slab_ptr: int, table_ptr: in
                  stream: Optional[int] = None) -> None:
     _check(lib().mz_attention(q_ptr, qpos_ptr, m, slab_ptr, table_ptr, n_table, chunk_tokens, n_q,
                               n_kv, head_dim, out_ptr, stream), None)
+
+
+def mz_q4_gemm_split(x_ptr: int, m: int, n_pad: int, k: int, w_ptr: int, epilogue: int, y_ptr: int,
+                     n_split: int, ws_ptr: int, ws_bytes: int, stream: Optional[int] = None) -> None:
+    _check(lib().mz_q4_gemm_split(x_ptr, m, n_pad, k, w_ptr, epilogue, y_ptr, n_split, ws_ptr, ws_bytes, stream),
+           None)
+
+
+def mz_q4_gemm_split_workspace_bytes(m: int, n_pad: int, n_split: int) -> int:
+    return int(lib().mz_q4_gemm_split_workspace_bytes(m, n_pad, n_split))
+
+
+def mz_q4_gemm_auto_splits(m: int, n_pad: int, k: int, ws_bytes: int) -> int:
+    return int(lib().mz_q4_gemm_auto_splits(m, n_pad, k, ws_bytes))
 
 
 def mz_attention_split(q_ptr: int, qpos_ptr: int, m: int, max_pos: int, slab_ptr: int, table_ptr: int,

@@ -25,10 +25,12 @@ REL = 2 * F16_REL
 pytestmark = pytest.mark.gpu
 
 
-def _gemm_case(M, N, K, epi, seed, sample_rows=None):
+def _gemm_case(M, N, K, epi, seed, sample_rows=None, n_split=None):
+    """n_split: None for mz_q4_gemm, else mz_q4_gemm_split with that many K
+    splits ("auto": the restore's choice)."""
     torch = torch_cuda()
     rng = np.random.default_rng(seed)
-    report("gemm", M=M, N=N, K=K, epi=epi, seed=seed)
+    report("gemm", M=M, N=N, K=K, epi=epi, seed=seed, n_split=n_split)
     if epi == 2:
         g = W.encode_q4_0((rng.standard_normal((N, K)) * 0.02).astype(np.float32))
         u = W.encode_q4_0((rng.standard_normal((N, K)) * 0.02).astype(np.float32))
@@ -47,7 +49,16 @@ def _gemm_case(M, N, K, epi, seed, sample_rows=None):
         y = torch.randn(M, n_pad, device="cuda", generator=gen) if epi == 1 else \
             torch.zeros(M, n_pad, device="cuda")
     y0 = y.float().cpu().numpy().astype(np.float64)
-    mz.mz_q4_gemm(x.data_ptr(), M, n_pad, K, w.data_ptr(), epi, y.data_ptr(), stream())
+    if n_split is None:
+        mz.mz_q4_gemm(x.data_ptr(), M, n_pad, K, w.data_ptr(), epi, y.data_ptr(), stream())
+    else:
+        if n_split == "auto":
+            n_split = mz.mz_q4_gemm_auto_splits(M, n_pad, K, 64 << 20)
+            report("  auto splits", n_split=n_split)
+        wsb = mz.mz_q4_gemm_split_workspace_bytes(M, n_pad, n_split)
+        ws = torch.full((wsb // 4,), float("nan"), device="cuda")      # stale partials must not leak in
+        mz.mz_q4_gemm_split(x.data_ptr(), M, n_pad, K, w.data_ptr(), epi, y.data_ptr(), n_split, ws.data_ptr(),
+                            wsb, stream())
     torch.cuda.synchronize()
     rows = np.arange(M) if sample_rows is None else sample_rows
     xs = x[torch.from_numpy(rows).cuda()].float().cpu().numpy().astype(np.float64)
@@ -77,6 +88,40 @@ def _gemm_case(M, N, K, epi, seed, sample_rows=None):
     (77, 688, 256, 2), (300, 1408, 256, 2)])
 def test_gemm_small(M, N, K, epi):
     _gemm_case(M, N, K, epi, seed=M + N + K)
+
+
+@pytest.mark.parametrize("M,N,K,epi", [
+    (1, 256, 640, 0), (5, 512, 1024, 1), (64, 384, 960, 2), (129, 1024, 4096, 1), (200, 688, 512, 2),
+    (1, 1408, 2048, 2), (33, 256, 4096, 0)])
+def test_gemm_split(M, N, K, epi):
+    """Split-K against the exact product: splits that divide the K steps,
+    ragged last splits, one step per split, and the restore's choice."""
+    nk = K // 64
+    for ns in sorted({2, 3, nk, "auto"} - {1}, key=str):
+        if ns != "auto" and ns > nk:
+            continue
+        _gemm_case(M, N, K, epi, seed=M + N + K, n_split=ns)
+
+
+@pytest.mark.parametrize("M", [1, 129])
+def test_gemm_split_8b_layer(M):
+    """The 8B projections at a decode step (1 row) and a 128-token prompt
+    (129 rows), with the restore's split choice."""
+    m = W.WORKLOADS["8b"].model
+    ffp = (m.d_ffn + 127) // 128 * 128
+    for i, (N, K, epi) in enumerate([(m.dq, m.d_model, 0), (2 * m.dkv, m.d_model, 0), (m.d_model, m.dq, 1),
+                                     (m.d_ffn, m.d_model, 2), (m.d_model, ffp, 1)]):
+        _gemm_case(M, N, K, epi, seed=300 + i, n_split="auto")
+
+
+def test_gemm_split_validation():
+    torch_cuda()
+    with pytest.raises(mz.MzError):
+        mz.mz_q4_gemm_split(1, 4, 256, 640, 1, 0, 1, 2, 1, 100, None)     # workspace too small
+    with pytest.raises(mz.MzError):
+        mz.mz_q4_gemm_split(1, 4, 256, 640, 1, 0, 1, 0, 1, 1 << 20, None)  # n_split 0
+    assert mz.mz_q4_gemm_auto_splits(32896, 4096, 4096, 64 << 20) == 1
+    assert mz.mz_q4_gemm_auto_splits(1, 4096, 14336, 64 << 20) > 8
 
 
 def _layer_gemms(key):
