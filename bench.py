@@ -217,6 +217,47 @@ def run_ablation(mz, W, eng, w, prompt, clean_logits, recompute_tflops, link_gbp
         mz.mz_set_option(e, "overlap", 1)
         overlap.append(res)
         log(f"[ablation] overlap {res}")
+    # short requests: all units resident, a 128-token prompt and a single
+    # token, then the size-driven 25 % restore, each with the split paths
+    # (split-key attention, split-K GEMMs) on and off, per-kind kernel time
+    short_rows = []
+    if "short" in parts:
+        mz.mz_set_option(e, "kv_codec", 1)
+        slot_ = m.chunk_tokens * m.dkv * 4
+        _, _, eu = mz.mz_plan_evict(cfg, w.n_ctx, w.n_prompt, 0, 1, "backward-out", "all-swap")
+        quarter = (m.n_layers * w.n_chunks * slot_ + m.n_layers * int(eu["swap_bytes"])) // 4
+        cases = [("resident, 128-token prompt", None, prompt), ("resident, one token", None, prompt[:1]),
+                 ("size-driven 25 %, codec",
+                  lambda: mz.mz_evict_size(e, quarter, link_gbps * 1e9, recompute_tflops * 1e12, m.n_layers,
+                                           w.n_prompt), prompt)]
+        for name, evict, prm in cases:
+            for split in (1, 0):
+                mz.mz_set_option(e, "attn_split", split)
+                mz.mz_set_option(e, "gemm_split", split)
+                ts = []
+                for step in range(steps + 1):
+                    if evict:
+                        evict()
+                    if step == 1:
+                        mz.mz_set_option(e, "kernel_timing", 1)
+                    t0 = time.perf_counter()
+                    mz.mz_restore_and_prefill(e, prm)
+                    mz.mz_first_token(e)
+                    dt = time.perf_counter() - t0
+                    mz.mz_truncate_context(e, w.n_ctx)
+                    if step:
+                        ts.append(dt * 1e3)
+                st = mz.mz_stats(e)
+                mz.mz_set_option(e, "kernel_timing", 0)
+                kms = {k: round(v["ms"] / steps, 3) for k, v in st["kernels"].items() if v["ms"] > 0}
+                t = statistics.median(ts)
+                short_rows.append({"request": name, "split": bool(split), "ttft_ms": round(t, 2),
+                                   "kernel_ms": kms})
+                log(f"[ablation] short {name:28s} split={split} TTFT {t:8.2f} ms kernels {kms}")
+        mz.mz_set_option(e, "attn_split", 1)
+        mz.mz_set_option(e, "gemm_split", 1)
+        mz.mz_set_option(e, "kv_codec", 0)
+
     # size-driven eviction (hybrid-swap state machine) at fractions of the
     # context's device bytes (every KV slot and weight unit), codec on, with
     # the balanced plan for the same numbers of units beside it
@@ -262,7 +303,7 @@ def run_ablation(mz, W, eng, w, prompt, clean_logits, recompute_tflops, link_gbp
     mz.mz_set_option(e, "kv_codec", 0)
     return {"n_kv_evicted": n_kv, "n_w_evicted": n_w, "link_gbps": link_gbps,
             "recompute_tflops": recompute_tflops, "plans": rows, "codec_plans": codec_rows, "overlap": overlap,
-            "evict_size": size_rows}
+            "evict_size": size_rows, "short": short_rows}
 
 
 def main():
@@ -274,10 +315,12 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-overlap", action="store_true")
     ap.add_argument("--no-shard", action="store_true", help="skip the per-GPU shard kernel timings")
+    ap.add_argument("--no-decode", action="store_true",
+                    help="skip the decode steps after the timed restores (profiler runs of the restore alone)")
     ap.add_argument("--ablation", action="store_true",
                     help="instead of the timed steps: TTFT per eviction order x placement (one JSON line)")
-    ap.add_argument("--ablation-parts", default="plans,codec,overlap,size",
-                    help="comma list of ablation parts: plans, codec, overlap, size")
+    ap.add_argument("--ablation-parts", default="plans,codec,overlap,size,short",
+                    help="comma list of ablation parts: plans, codec, overlap, size, short")
     ap.add_argument("--recompute-tflops", type=float, default=400.0,
                     help="recompute rate the balanced placement assumes (partial-layer recompute of a "
                          "balanced plan runs at about 400 TFLOP/s on MI355X: few rows per GEMM)")
@@ -318,7 +361,7 @@ def main():
     plan = W.make_plan(w)
 
     t = time.perf_counter()
-    eng = mz.Engine(m, blob, max_ctx=S)
+    eng = mz.Engine(m, blob, max_ctx=S + 64)   # room for the decode steps after the restore
     e = eng.ctx
     log(f"[bench] model loaded in {time.perf_counter() - t:.1f} s")
     if args.no_overlap:
@@ -420,6 +463,23 @@ def main():
                       "max_logit_err_vs_clean": max(logit_err)},
         "roofline": roof,
     }
+    # past the first token: after the same restore, greedy decode steps
+    # (one row each: split-key attention over the whole context and split-K
+    # projections), timed as a whole
+    mz.mz_set_option(e, "kernel_timing", 0)
+    n_dec = 0 if args.no_decode else 32
+    mz.mz_evict(e, plan.kv_state, plan.w_state)
+    mz.mz_restore_and_prefill(e, prompt)
+    tok = mz.mz_first_token(e)
+    if n_dec:
+        mz.mz_generate(e, tok, 4)                      # warm
+        t = time.perf_counter()
+        mz.mz_generate(e, int(tok), n_dec)
+        dt = time.perf_counter() - t
+        out["decode_after_restore"] = {"tokens": n_dec, "ms_per_token": round(dt * 1e3 / n_dec, 3),
+                                       "tokens_per_s": round(n_dec / dt, 1), "context": S + 4}
+        log(f"[bench] decode after restore: {dt * 1e3 / n_dec:.2f} ms/token over {n_dec} tokens")
+    mz.mz_truncate_context(e, w.n_ctx)
     eng.close()
     if w.model.n_kv_heads % 8 == 0 and not args.no_shard:
         t = time.perf_counter()

@@ -129,6 +129,17 @@ mz_status mz_restore_and_prefill(mz_ctx *ctx, const int32_t *prompt, int32_t n_p
  * be NULL.  ESTATE if nothing was prefilled since the last first token. */
 mz_status mz_first_token(mz_ctx *ctx, int32_t *token_out, float *logits_out);
 
+/* Greedy generation past the first token: append `token` to the context,
+ * run it through every layer (one row; its attention reads the whole
+ * context, split over the keys), take the argmax of its logits as
+ * tokens_out[0]; then append that and continue, n tokens in all (host,
+ * caller-owned tokens_out [n]).  The last generated token is not appended,
+ * as with mz_first_token.  Any evicted units are restored by the first step
+ * (it is a restore with a one-token prompt).  Errors: EINVAL (n < 0, NULL
+ * tokens_out, token out of range, or a context that would pass max_ctx),
+ * and those of mz_restore_and_prefill. */
+mz_status mz_generate(mz_ctx *ctx, int32_t token, int32_t n, int32_t *tokens_out);
+
 /* Engine options: "overlap" (1: swap-in overlapped with compute, default;
  * 0: every copy finishes before compute starts), "kernel_timing" (1: time
  * every kernel launch with HIP events on its stream; setting it clears the

@@ -1485,6 +1485,19 @@ mz_status mz_first_token(mz_ctx* x, int32_t* token_out, float* logits_out) {
   });
 }
 
+mz_status mz_generate(mz_ctx* x, int32_t token, int32_t n, int32_t* tokens_out) {
+  if (!x) return MZ_EINVAL;
+  if (n < 0 || (n > 0 && !tokens_out)) return guarded(x, [&] { fail(MZ_EINVAL, "bad n or tokens_out"); });
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t t = i == 0 ? token : tokens_out[i - 1];
+    mz_status st = mz_restore_and_prefill(x, &t, 1);
+    if (st != MZ_OK) return st;
+    st = mz_first_token(x, &tokens_out[i], nullptr);
+    if (st != MZ_OK) return st;
+  }
+  return MZ_OK;
+}
+
 mz_status mz_stats(mz_ctx* x, char* out, size_t cap) {
   if (!x) return MZ_EINVAL;
   return guarded(x, [&] {

@@ -94,6 +94,7 @@ def lib() -> ctypes.CDLL:
         "mz_restore_and_prefill": ([vp, vp, i32], i32),
         "mz_first_token": ([vp, vp, vp], i32),
         "mz_set_option": ([vp, ctypes.c_char_p, i64], i32),
+        "mz_generate": ([vp, i32, i32, vp], i32),
         "mz_stats": ([vp, ctypes.c_char_p, sz], i32),
         "mz_last_error": ([vp], ctypes.c_char_p),
         "mz_free": ([vp], None),
@@ -220,6 +221,13 @@ def mz_first_token(ctx, vocab: Optional[int] = None):
     logits = None if vocab is None else np.empty(vocab, np.float32)
     _check(lib().mz_first_token(ctx, ctypes.byref(tok), _ptr(logits)), ctx)
     return (tok.value, logits) if vocab is not None else tok.value
+
+
+def mz_generate(ctx, token: int, n: int) -> np.ndarray:
+    """Append token and decode n more tokens greedily."""
+    out = np.zeros(max(n, 1), np.int32)
+    _check(lib().mz_generate(ctx, int(token), int(n), out.ctypes.data), ctx)
+    return out[:n]
 
 
 def mz_set_option(ctx, key: str, value: int) -> None:

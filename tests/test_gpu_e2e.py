@@ -50,7 +50,7 @@ def _check_token(tok, logits, otok, ologits, name):
         assert gap <= 2 * err, name
 
 
-def run_import_flow(w, kv_state, w_state, prompt, name, engine=None, codec=False, evict_fn=None):
+def run_import_flow(w, kv_state, w_state, prompt, name, engine=None, codec=False, evict_fn=None, generate=0):
     """Import the oracle's clean KV, evict, restore, first token; compare.
     With codec, both sides swap full chunks through the 8-bit codec and the
     restored chunks must equal the oracle's round trip bit for bit."""
@@ -118,9 +118,38 @@ def run_import_flow(w, kv_state, w_state, prompt, name, engine=None, codec=False
         report("  kv", max_err=f"{worst:.3e}")
         assert worst <= KV_TOL, name
         _check_token(tok, logits, otok, ologits, name)
+        if generate:
+            _check_generate(eng, ox, m, tok, generate, S, name)
     finally:
         if engine is None:
             eng.close()
+
+
+def _check_generate(eng, ox, m, tok, n, S, name):
+    """mz_generate for n tokens; the oracle takes the same steps with the
+    GPU's tokens forced in (so a near-tie cannot fork the two sequences):
+    each GPU token is the oracle's argmax or within twice the logit bar of
+    it, and the K/V of every generated row is within the K/V bar."""
+    toks = mz.mz_generate(eng.ctx, tok, n)
+    prev = tok
+    for i in range(n):
+        ox.restore_and_prefill(np.array([prev], np.int32))
+        otok, ologits = ox.first_token()
+        gap = float(ologits[otok] - ologits[toks[i]])
+        report("  generate", step=i, gpu=int(toks[i]), oracle=int(otok), gap=f"{gap:.3e}")
+        assert toks[i] == otok or gap <= 2 * LOGIT_TOL, (name, i)
+        prev = int(toks[i])
+    C, dkv = m.chunk_tokens, m.dkv
+    worst = 0.0
+    for p in range(S, S + n):
+        c, r = divmod(p, C)
+        for l in range(m.n_layers):
+            k, v = mz.mz_read_kv(eng.ctx, l, c, C, dkv)
+            ok_, ov_ = ox.read_kv(l, c)
+            worst = max(worst, float(np.abs(k[r].astype(np.float64) - ok_[r]).max()),
+                        float(np.abs(v[r].astype(np.float64) - ov_[r]).max()))
+    report("  generated kv", max_err=f"{worst:.3e}")
+    assert worst <= KV_TOL, name
 
 
 TINY = W.WORKLOADS["tiny"]
@@ -331,3 +360,24 @@ def test_scaled_8b_evict_size():
     half = m.n_layers * w.n_chunks * slot // 2
     prm = np.random.default_rng(5).integers(0, m.vocab, w.n_prompt).astype(np.int32)
     _size_flow(w, [half // 2, half - half // 2, 10 ** 13], 56e9, 1e13, 2, prm, "8b-size", codec=True)
+
+
+def test_tiny_generate_after_restore(tiny_engine):
+    """Restore of a mixed plan, first token, then 12 generated tokens (they
+    cross into a new chunk)."""
+    L, nc = TINY.model.n_layers, TINY.n_chunks
+    p = W.random_plan(L, nc, 0.35, 0.35, 7, w_swap=0.5, w_drop=0.0)
+    run_import_flow(TINY, p.kv_state, p.w_state, np.arange(3, dtype=np.int32), "tiny-generate",
+                    engine=tiny_engine, generate=12)
+
+
+def test_scaled_8b_generate():
+    """The 8B layer shape (4 layers, 2K context): all-swap restore of the
+    back half with the codec, 128-token prompt, then 6 generated tokens
+    (split-key attention and split-K projections on every step)."""
+    w = W.WORKLOADS["8b"].scaled(n_layers=4, n_ctx=2048, n_prompt=128)
+    m = w.model
+    kv = np.zeros((m.n_layers, w.n_chunks), np.uint8)
+    kv[2:, :] = O.SWAP
+    prm = np.random.default_rng(8).integers(0, m.vocab, w.n_prompt).astype(np.int32)
+    run_import_flow(w, kv, None, prm, "8b-generate", codec=True, generate=6)
