@@ -468,10 +468,10 @@ def main():
     # projections), timed as a whole
     mz.mz_set_option(e, "kernel_timing", 0)
     n_dec = 0 if args.no_decode else 32
-    mz.mz_evict(e, plan.kv_state, plan.w_state)
-    mz.mz_restore_and_prefill(e, prompt)
-    tok = mz.mz_first_token(e)
     if n_dec:
+        mz.mz_evict(e, plan.kv_state, plan.w_state)
+        mz.mz_restore_and_prefill(e, prompt)
+        tok = mz.mz_first_token(e)
         mz.mz_generate(e, tok, 4)                      # warm
         t = time.perf_counter()
         mz.mz_generate(e, int(tok), n_dec)
@@ -479,7 +479,7 @@ def main():
         out["decode_after_restore"] = {"tokens": n_dec, "ms_per_token": round(dt * 1e3 / n_dec, 3),
                                        "tokens_per_s": round(n_dec / dt, 1), "context": S + 4}
         log(f"[bench] decode after restore: {dt * 1e3 / n_dec:.2f} ms/token over {n_dec} tokens")
-    mz.mz_truncate_context(e, w.n_ctx)
+        mz.mz_truncate_context(e, w.n_ctx)
     eng.close()
     if w.model.n_kv_heads % 8 == 0 and not args.no_shard:
         t = time.perf_counter()

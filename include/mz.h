@@ -375,7 +375,7 @@ mz_status mz_attention(const void *q_f16, const int32_t *qpos, int32_t m, const 
  * device, caller-owned, at least mz_attention_split_workspace_bytes(m,
  * n_q_heads, head_dim, n_split) bytes; it must not be shared by calls in
  * flight at the same time.  Other arguments and errors as mz_attention;
- * EINVAL also for n_split outside 1..1024 or a short workspace. */
+ * EINVAL also for n_split outside 1..64 or a short workspace. */
 mz_status mz_attention_split(const void *q_f16, const int32_t *qpos, int32_t m, int32_t max_pos,
                              const void *slab, const int32_t *table, int32_t n_table,
                              int32_t chunk_tokens, int32_t n_q_heads, int32_t n_kv_heads,

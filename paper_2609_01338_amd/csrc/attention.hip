@@ -501,7 +501,10 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
 // that hold keys of the query: O = sum_s 2^(m_s - M) l_s o_s / sum_s
 // 2^(m_s - M) l_s.  Split 0 always holds key 0, so the denominator is
 // positive.  Splits past the one holding the query's own position were not
-// written for it and are not read.
+// written for it and are not read.  Lane s reads split s's (m, l) (at most
+// 64 splits); M and the denominator are wave reductions, and the output sum
+// walks the splits with independent loads, each weight broadcast from its
+// lane.
 template <int HD>
 __global__ __launch_bounds__(256) void attn_merge_kernel(const _Float16* __restrict__ Opart,
                                                          const float2* __restrict__ MLpart,
@@ -513,18 +516,26 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(const _Float16* __restr
   if (wv >= M * nq) return;      // whole waves leave together
   const int qi = wv / nq, h = wv % nq;
   const int nv = min(n_split, (qpos[qi] / KT) / tps + 1);
-  float mx = -INFINITY;
-  for (int sp = 0; sp < nv; ++sp) mx = fmaxf(mx, MLpart[(size_t)(sp * M + qi) * nq + h].x);
-  float acc[DPL] = {};
-  float den = 0.f;
-  for (int sp = 0; sp < nv; ++sp) {
-    const float2 ml = MLpart[(size_t)(sp * M + qi) * nq + h];
-    if (!(ml.y > 0.f)) continue;
-    const float wgt = exp2f(ml.x - mx) * ml.y;
-    den += wgt;
-    const _Float16* src = Opart + ((size_t)(sp * M + qi) * nq + h) * HD + lane * DPL;
+  const size_t stride = (size_t)M * nq;          // between splits, in (row, head) entries
+  const size_t e0 = (size_t)qi * nq + h;
+  float2 ml = make_float2(-INFINITY, 0.f);
+  if (lane < nv) ml = MLpart[lane * stride + e0];
+  if (!(ml.y > 0.f)) ml.x = -INFINITY;            // no key of this split: weight 0
+  float mx = ml.x;
 #pragma unroll
-    for (int e = 0; e < DPL; ++e) acc[e] = __builtin_fmaf(wgt, (float)src[e], acc[e]);
+  for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+  const float wgt = ml.x == -INFINITY ? 0.f : exp2f(ml.x - mx) * ml.y;
+  float den = wgt;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) den += __shfl_xor(den, o);
+  float acc[DPL] = {};
+  const _Float16* src = Opart + e0 * HD + lane * DPL;
+#pragma unroll 8
+  for (int j = 0; j < nv; ++j) {
+    const float wj = __shfl(wgt, j);
+    const _Float16* p = src + (size_t)j * stride * HD;
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) acc[e] = __builtin_fmaf(wj, (float)p[e], acc[e]);
   }
   const float inv = 1.0f / den;
   _Float16* dst = O + (size_t)qi * nq * HD + h * HD + lane * DPL;

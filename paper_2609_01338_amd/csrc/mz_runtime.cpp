@@ -331,17 +331,17 @@ struct HostArena {
 
 enum KernelKind {
   kKEmbed, kKRmsnorm, kKGemmKV, kKRopeKV, kKGemmQ, kKRopeQ, kKGather, kKAttention, kKGemmO,
-  kKGemmGateUp, kKGemmDown, kKLmHead, kKCount
+  kKGemmGateUp, kKGemmDown, kKLmHead, kKAttentionSplit, kKCount
 };
 const char* kKindName[kKCount] = {"embed_q4", "rmsnorm", "gemm_q4_kv", "rope_kv", "gemm_q4_q",
                                   "rope_q", "gather_rows", "attention", "gemm_q4_o",
-                                  "gemm_q4_gateup", "gemm_q4_down", "lm_head_argmax"};
+                                  "gemm_q4_gateup", "gemm_q4_down", "lm_head_argmax", "attention_split"};
 // HIP kernel symbol each kind launches (to line up with profiler summaries)
 const char* kKindKernel[kKCount] = {"embed_kernel", "rmsnorm_kernel", "gemm_q4_kernel<0>",
                                     "rope_kv_kernel", "gemm_q4_kernel<0>", "rope_kv_kernel",
                                     "gather_rows_kernel", "attn_kernel", "gemm_q4_kernel<1>",
                                     "gemm_q4_kernel<2>", "gemm_q4_kernel<1>",
-                                    "lm_head_kernel+argmax_kernel"};
+                                    "lm_head_kernel+argmax_kernel", "attn_kernel<split>+attn_merge_kernel"};
 
 struct KindStats {
   int64_t launches = 0;
@@ -928,7 +928,7 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
     const int max_pos = l + 1 < L ? rows.R[l + 1].back() : S - 1;
     const int n_split =
         x->attn_split ? mzk::attention_auto_splits(nq, max_pos, x->nq, x->nkv, x->hd, x->split_ws_bytes) : 1;
-    x->timed(kKAttention, att_flops, (double)nq * x->dq * 4.0, cs, [&] {
+    x->timed(n_split > 1 ? kKAttentionSplit : kKAttention, att_flops, (double)nq * x->dq * 4.0, cs, [&] {
       if (n_split > 1)
         mzk::launch_attention_split(x->q16, posq, nq, max_pos, x->kv_slab, x->d_tables + (size_t)l * MC, C,
                                     x->slot_bytes, x->nq, x->nkv, x->hd, n_split, x->split_ws, x->xb, cs);
@@ -1668,7 +1668,7 @@ mz_status mz_attention_split(const void* q, const int32_t* qpos, int32_t m, int3
     if (head_dim != 64 && head_dim != 128) fail(MZ_EINVAL, "head_dim must be 64 or 128");
     if (n_kv < 1 || n_q % n_kv || n_q / n_kv > 8) fail(MZ_EINVAL, "bad head counts");
     if (max_pos / chunk_tokens >= n_table) fail(MZ_EINVAL, "table does not cover max_pos");
-    if (n_split < 1 || n_split > 1024) fail(MZ_EINVAL, "n_split must be 1..1024");
+    if (n_split < 1 || n_split > 64) fail(MZ_EINVAL, "n_split must be 1..64");
     if (workspace_bytes < mzk::attention_split_ws_bytes(m, n_q, head_dim, n_split))
       fail(MZ_EINVAL, "workspace too small for %d splits", n_split);
     const int64_t slot_bytes = (int64_t)chunk_tokens * n_kv * head_dim * 2 * 2;

@@ -261,6 +261,8 @@ def test_attention_split_validation():
         mz.mz_attention_split(1, 1, 4, 100, 1, 1, 1, 16, 8, 2, 64, 2, 1, 10, 1)   # table short of max_pos
     with pytest.raises(mz.MzError):
         mz.mz_attention_split(1, 1, 4, 10, 1, 1, 1, 16, 8, 2, 64, 2, 1, 10, 1)    # workspace too small
+    with pytest.raises(mz.MzError):
+        mz.mz_attention_split(1, 1, 4, 10, 1, 1, 1, 16, 8, 2, 64, 65, 1, 1 << 30, 1)   # more than 64 splits
     assert mz.mz_attention_auto_splits(40000, 40000, 32, 8, 128, 64 << 20) == 1   # the chip is full already
     assert 32 <= mz.mz_attention_auto_splits(1, 32895, 32, 8, 128, 64 << 20) <= 64
     assert mz.mz_attention_auto_splits(129, 32895, 32, 8, 128, 64 << 20) > 8
