@@ -251,9 +251,12 @@ def run_ablation(mz, W, eng, w, prompt, clean_logits, recompute_tflops, link_gbp
                 mz.mz_set_option(e, "kernel_timing", 0)
                 kms = {k: round(v["ms"] / steps, 3) for k, v in st["kernels"].items() if v["ms"] > 0}
                 t = statistics.median(ts)
+                host = {"plan_and_stage_ms": round(st["host_plan_ms"], 3),
+                        "enqueue_ms": round(st["host_enqueue_ms"], 3)}
                 short_rows.append({"request": name, "split": bool(split), "ttft_ms": round(t, 2),
-                                   "kernel_ms": kms})
-                log(f"[ablation] short {name:28s} split={split} TTFT {t:8.2f} ms kernels {kms}")
+                                   "kernel_ms": kms, "kernel_sum_ms": round(sum(kms.values()), 3), "host": host})
+                log(f"[ablation] short {name:28s} split={split} TTFT {t:8.2f} ms kernel sum "
+                    f"{sum(kms.values()):7.2f} ms host {host} kernels {kms}")
         mz.mz_set_option(e, "attn_split", 1)
         mz.mz_set_option(e, "gemm_split", 1)
         mz.mz_set_option(e, "kv_codec", 0)

@@ -241,6 +241,74 @@ __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict_
   }
 }
 
+// One activation row (m = 1: a decode step, the last layer's single row): the
+// product of gemm_q4_kernel<kEpiPartial> without matrix cores.  Thread r of
+// a 256-thread workgroup owns output column (tile row) r of n tile
+// blockIdx.x; over K tiles [y * k_steps, ...) it reads that row's two code
+// blocks (32 contiguous bytes: 256 threads read the tile's 8 KB of codes in
+// one coalesced sweep) and two scales, up to 8 tiles ahead, decodes each code
+// pair to f16 exactly as the GEMM does (one rounding of d * (q - 8)), and
+// accumulates products with the f16 activations in fp32 (v_dot2).  The
+// activations of each batch of tiles are staged in LDS (one pair per
+// thread) and read as broadcasts.  Partials go to part [split][N] for
+// gemm_splitk_reduce.
+constexpr int kGemvAhead = 8;     // K tiles whose codes are in flight per thread
+
+__global__ __launch_bounds__(256) void gemv_q4_kernel(const _Float16* __restrict__ X,
+                                                      const int32_t* __restrict__ a_rows, int K,
+                                                      const uint8_t* __restrict__ Wp, int N,
+                                                      float* __restrict__ part, int k_steps) {
+  __shared__ f16x2 xs[kGemvAhead * 32];   // 256 pairs: one per thread and batch
+  const int nk = K / BK;
+  const int split = blockIdx.y;
+  const int kt0 = split * k_steps;
+  const int kt_n = min(k_steps, nk - kt0);
+  const int nt = blockIdx.x;
+  const int r = threadIdx.x;
+  const _Float16* xrow = X + (size_t)(a_rows ? a_rows[0] : 0) * K + (size_t)kt0 * BK;
+  const uint8_t* tile0 = Wp + ((size_t)nt * nk + kt0) * kGemmTileBytes;
+  const f16x2 off = {(_Float16)1032.0f, (_Float16)1032.0f};
+  float acc = 0.f;
+  for (int t0 = 0; t0 < kt_n; t0 += kGemvAhead) {
+    uint4 nb[kGemvAhead][2];
+    uint32_t sc[kGemvAhead];
+#pragma unroll
+    for (int j = 0; j < kGemvAhead; ++j) {
+      if (t0 + j < kt_n) {
+        const uint8_t* t = tile0 + (size_t)(t0 + j) * kGemmTileBytes;
+        nb[j][0] = *reinterpret_cast<const uint4*>(t + r * 32);
+        nb[j][1] = *reinterpret_cast<const uint4*>(t + r * 32 + 16);
+        sc[j] = *reinterpret_cast<const uint32_t*>(t + NIB_BYTES + r * 4);
+      }
+    }
+    __syncthreads();   // the previous batch is done with xs
+    if (r < (kt_n - t0) * 32) xs[r] = *reinterpret_cast<const f16x2*>(xrow + (size_t)t0 * BK + 2 * r);
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kGemvAhead; ++j) {
+      if (t0 + j < kt_n) {
+        const f16x2* xp = xs + j * 32;
+#pragma unroll
+        for (int blk = 0; blk < 2; ++blk) {
+          const _Float16 d = __builtin_bit_cast(_Float16, (uint16_t)(sc[j] >> (16 * blk)));
+          const f16x2 d2 = {d, d};
+          const uint4 q = nb[j][blk];
+          const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int mm = 0; mm < 4; ++mm) {
+              const f16x2 c = __builtin_bit_cast(f16x2, pair_code(w[i], 4 * mm));
+              const f16x2 wv = (c - off) * d2;
+              acc = __builtin_amdgcn_fdot2(wv, xp[blk * 16 + 4 * i + mm], acc, false);
+            }
+        }
+      }
+    }
+  }
+  part[(size_t)split * N + (size_t)nt * BN + r] = acc;
+}
+
 // Sum of the K splits in split order, then the epilogue; 4 columns per
 // thread (SwiGLU: 4 output columns, whose gate and up sums are 4 consecutive
 // columns each: output column o takes gate column 32 (o / 16) + o % 16 and the
@@ -344,7 +412,10 @@ void launch_gemm_q4_splitk(const void* x, int m, int n, int k, const void* w, in
   const uint8_t* W = reinterpret_cast<const uint8_t*>(w);
   const int ks = gemm_k_steps(k, n_split);
   const int ns = (k / BK + ks - 1) / ks;
-  if (gemm_row_tile(m, n) == 64)
+  if (m == 1)
+    hipLaunchKernelGGL(gemv_q4_kernel, dim3(n / BN, ns), dim3(256), 0, s, X, a_rows, k, W, n,
+                       reinterpret_cast<float*>(ws), ks);
+  else if (gemm_row_tile(m, n) == 64)
     launch_bm<kEpiPartial, 64>(X, a_rows, m, n, k, W, ws, s, ns, ks);
   else
     launch_bm<kEpiPartial, 256>(X, a_rows, m, n, k, W, ws, s, ns, ks);

@@ -204,13 +204,16 @@ Rows compute_rows(const uint8_t* kv_state, int L, int nc, int N, int P, int C) {
   rows.R.resize(L);
   rows.nR.resize(L);
   rows.nD.resize(L);
+  // walked by chunk: the cost is the rows produced, not the cached context
+  // (a decode step carries one row per layer of a 32K context)
   for (int l = 0; l < L; ++l) {
     std::vector<int32_t>& r = rows.R[l];
     int nd = P;
-    for (int p = 0; p < N; ++p) {
-      const int c = p / C;
-      if (maxdrop[c] >= l) r.push_back(p);
-      if (kv_state[(size_t)l * nc + c] == MZ_DROP) ++nd;
+    for (int c = 0; c < nc; ++c) {
+      const int p0 = c * C, p1 = std::min(N, p0 + C);
+      if (maxdrop[c] >= l)
+        for (int p = p0; p < p1; ++p) r.push_back(p);
+      if (kv_state[(size_t)l * nc + c] == MZ_DROP) nd += p1 - p0;
     }
     for (int p = N; p < S; ++p) r.push_back(p);
     if (r.empty() || r.back() != S - 1) r.push_back(S - 1);
