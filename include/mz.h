@@ -43,7 +43,7 @@ typedef enum {
 /* State of one unit (a layer's weights, or one KV chunk of one layer). */
 typedef enum { MZ_RES = 0, MZ_SWAP = 1, MZ_DROP = 2 } mz_unit_state;
 
-/* Model shape.  d_model must be a multiple of 256; d_ffn need not be a
+/* Model shape.  d_model must be a multiple of 256, at most 8192; d_ffn need not be a
  * multiple of 32 (Q4_0 rows of W_down are zero-padded); head_dim must be 64 or
  * 128; n_q_heads a multiple of n_kv_heads with a group of at most 8;
  * chunk_tokens a power of two (>= 8); max_ctx bounds context + prompt tokens. */

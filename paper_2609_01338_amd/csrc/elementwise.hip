@@ -175,61 +175,113 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const float* __restric
   for (int i = threadIdx.x; i < d / 4; i += 256) t[i] = s[i];
 }
 
-constexpr int LM_ROWS = 64;   // vocabulary rows per block (16 per wave)
+constexpr int LM_ROWS = 256;   // vocabulary rows per block (64 per wave)
+constexpr int LM_GROUP = 4;    // rows whose codes are in flight together per wave
 
-// logits[v] = x . W_lm[v] with x = RMSNorm(h_last) staged in LDS; per-block
-// (max, lowest index) partials.
+// logits[v] = x . W_lm[v] with x = RMSNorm(h_last); per-block (max, lowest
+// index) partials.  Lane l of every wave owns the 32-element blocks b = l,
+// l + 64, ... of a row (NBL of them): their x values live in its registers
+// (read once from global memory), so the row loop touches no LDS.  With
+// codes q in 0..15, x . d (q - 8) over a block = d (sum x q - 8 sum x), the
+// block's sum of x being precomputed; nibbles become floats with the
+// byte-to-float conversions.  A wave takes its 64 rows LM_GROUP at a time,
+// issuing the loads of the group before any arithmetic.
+// byte K of v as a float (one v_cvt_f32_ubyteK)
+template <int K>
+__device__ __forceinline__ float ubyte_f32(uint32_t v) { return (float)((v >> (8 * K)) & 0xFFu); }
+
+template <int NBL>
 __global__ __launch_bounds__(256) void lm_head_kernel(const float* __restrict__ h_last, int d,
                                                       float eps, const uint8_t* __restrict__ nib,
                                                       const uint16_t* __restrict__ scale,
                                                       int vocab, float* __restrict__ logits,
                                                       float* __restrict__ part_val,
                                                       int32_t* __restrict__ part_idx) {
-  extern __shared__ float xs[];
   __shared__ float red[4];
   __shared__ float bval[4];
   __shared__ int32_t bidx[4];
   float ss = 0.f;
   for (int i = threadIdx.x; i < d; i += 256) {
     const float v = h_last[i];
-    xs[i] = v;
     ss += v * v;
   }
   ss = block_sum256(ss, red);
-  const float r = 1.0f / __builtin_sqrtf(ss / (float)d + eps);
-  for (int i = threadIdx.x; i < d; i += 256) xs[i] *= r;
-  __syncthreads();
+  const float rn = 1.0f / __builtin_sqrtf(ss / (float)d + eps);
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int nb = d / 32;
+  // this lane's blocks: x (normalised) and the sums of x over the low-nibble
+  // half (elements 0..15) and the high-nibble half (16..31)
+  float xv[NBL][32];
+  float sx[NBL];
+#pragma unroll
+  for (int j = 0; j < NBL; ++j) {
+    const int b = lane + 64 * j;
+    sx[j] = 0.f;
+#pragma unroll
+    for (int e = 0; e < 32; e += 4) {
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (b < nb) v = *reinterpret_cast<const float4*>(h_last + b * 32 + e);
+      xv[j][e] = v.x * rn;
+      xv[j][e + 1] = v.y * rn;
+      xv[j][e + 2] = v.z * rn;
+      xv[j][e + 3] = v.w * rn;
+      sx[j] += xv[j][e] + xv[j][e + 1] + xv[j][e + 2] + xv[j][e + 3];
+    }
+  }
   float best = -INFINITY;
   int32_t best_i = 0x7fffffff;
-  for (int k = 0; k < LM_ROWS / 4; ++k) {
-    const int v = blockIdx.x * LM_ROWS + w * (LM_ROWS / 4) + k;
-    if (v >= vocab) break;
-    float acc = 0.f;
-    for (int b = lane; b < nb; b += 64) {
-      const uint4 q = *reinterpret_cast<const uint4*>(nib + (int64_t)v * (d / 2) + b * 16);
-      const float dd = (float)__builtin_bit_cast(_Float16, scale[(int64_t)v * nb + b]);
-      const uint32_t wd[4] = {q.x, q.y, q.z, q.w};
-      const float* xb = xs + b * 32;
-      float sl = 0.f, sh = 0.f;
+  const int v0 = blockIdx.x * LM_ROWS + w * (LM_ROWS / 4);
+  for (int g = 0; g < LM_ROWS / 4; g += LM_GROUP) {
+    uint4 q[LM_GROUP][NBL];
+    uint16_t sc[LM_GROUP][NBL];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+    for (int k = 0; k < LM_GROUP; ++k) {
+      const int v = min(v0 + g + k, vocab - 1);
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-          const uint32_t byte = (wd[i] >> (8 * kk)) & 0xFFu;
-          sl += xb[4 * i + kk] * (float)((int)(byte & 15u) - 8);
-          sh += xb[16 + 4 * i + kk] * (float)((int)(byte >> 4) - 8);
+      for (int j = 0; j < NBL; ++j) {
+        const int b = lane + 64 * j;
+        q[k][j] = make_uint4(0, 0, 0, 0);
+        sc[k][j] = 0;
+        if (b < nb) {
+          q[k][j] = *reinterpret_cast<const uint4*>(nib + (int64_t)v * (d / 2) + b * 16);
+          sc[k][j] = scale[(int64_t)v * nb + b];
         }
-      acc += dd * (sl + sh);
+      }
     }
-    acc = wave_sum(acc);
-    if (acc > best) {   // rows ascend, so the first maximum keeps the lowest index
-      best = acc;
-      best_i = v;
+#pragma unroll
+    for (int k = 0; k < LM_GROUP; ++k) {
+      float acc = 0.f;
+#pragma unroll
+      for (int j = 0; j < NBL; ++j) {
+        const uint32_t wd[4] = {q[k][j].x, q[k][j].y, q[k][j].z, q[k][j].w};
+        float dot = 0.f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const uint32_t lo = wd[i] & 0x0F0F0F0Fu, hi = (wd[i] >> 4) & 0x0F0F0F0Fu;
+          // byte kk of dword i: low nibble -> element 4i+kk, high -> 16+4i+kk
+          dot = __builtin_fmaf(xv[j][4 * i + 0], ubyte_f32<0>(lo), dot);
+          dot = __builtin_fmaf(xv[j][4 * i + 1], ubyte_f32<1>(lo), dot);
+          dot = __builtin_fmaf(xv[j][4 * i + 2], ubyte_f32<2>(lo), dot);
+          dot = __builtin_fmaf(xv[j][4 * i + 3], ubyte_f32<3>(lo), dot);
+          dot = __builtin_fmaf(xv[j][16 + 4 * i + 0], ubyte_f32<0>(hi), dot);
+          dot = __builtin_fmaf(xv[j][16 + 4 * i + 1], ubyte_f32<1>(hi), dot);
+          dot = __builtin_fmaf(xv[j][16 + 4 * i + 2], ubyte_f32<2>(hi), dot);
+          dot = __builtin_fmaf(xv[j][16 + 4 * i + 3], ubyte_f32<3>(hi), dot);
+        }
+        const float dd = (float)__builtin_bit_cast(_Float16, sc[k][j]);
+        acc = __builtin_fmaf(dd, __builtin_fmaf(-8.0f, sx[j], dot), acc);
+      }
+      acc = wave_sum(acc);
+      const int v = v0 + g + k;
+      if (v < vocab) {
+        if (acc > best) {   // rows ascend, so the first maximum keeps the lowest index
+          best = acc;
+          best_i = v;
+        }
+        if (lane == 0) logits[v] = acc;
+      }
     }
-    if (lane == 0) logits[v] = acc;
   }
   if (lane == 0) {
     bval[w] = best;
@@ -323,8 +375,17 @@ void launch_lm_head(const float* h_last, int d, float eps, const uint8_t* w_nib,
                     const uint16_t* w_scale, int vocab, float* logits, float* part_val,
                     int32_t* part_idx, int32_t* token, hipStream_t s) {
   const int nblk = (vocab + LM_ROWS - 1) / LM_ROWS;
-  hipLaunchKernelGGL(lm_head_kernel, dim3(nblk), dim3(256), d * sizeof(float), s, h_last, d, eps,
-                     w_nib, w_scale, vocab, logits, part_val, part_idx);
+  const int nbl = (d / 32 + 63) / 64;   // 32-element blocks per lane (d <= 8192)
+  switch (nbl) {
+    case 1: hipLaunchKernelGGL(lm_head_kernel<1>, dim3(nblk), dim3(256), 0, s, h_last, d, eps, w_nib, w_scale,
+                               vocab, logits, part_val, part_idx); break;
+    case 2: hipLaunchKernelGGL(lm_head_kernel<2>, dim3(nblk), dim3(256), 0, s, h_last, d, eps, w_nib, w_scale,
+                               vocab, logits, part_val, part_idx); break;
+    case 3: hipLaunchKernelGGL(lm_head_kernel<3>, dim3(nblk), dim3(256), 0, s, h_last, d, eps, w_nib, w_scale,
+                               vocab, logits, part_val, part_idx); break;
+    default: hipLaunchKernelGGL(lm_head_kernel<4>, dim3(nblk), dim3(256), 0, s, h_last, d, eps, w_nib, w_scale,
+                                vocab, logits, part_val, part_idx); break;
+  }
   hipLaunchKernelGGL(argmax_kernel, dim3(1), dim3(256), 0, s, part_val, part_idx, nblk, token);
 }
 

@@ -565,7 +565,8 @@ void* dmalloc(size_t bytes) {
 
 void validate_cfg(const mz_model_cfg* c) {
   if (!c) fail(MZ_EINVAL, "cfg is NULL");
-  if (c->n_layers < 1 || c->d_model < 256 || c->d_model % 256) fail(MZ_EINVAL, "d_model must be a positive multiple of 256 and n_layers >= 1");
+  if (c->n_layers < 1 || c->d_model < 256 || c->d_model % 256 || c->d_model > 8192)
+    fail(MZ_EINVAL, "d_model must be a multiple of 256 in 256..8192 and n_layers >= 1");
   if (c->head_dim != 64 && c->head_dim != 128) fail(MZ_EINVAL, "head_dim must be 64 or 128");
   if (c->n_kv_heads < 1 || c->n_q_heads < 1 || c->n_q_heads % c->n_kv_heads)
     fail(MZ_EINVAL, "n_q_heads must be a positive multiple of n_kv_heads");
