@@ -11,10 +11,13 @@
 // (global_load_lds_dwordx4, no registers), requested a full step before it is
 // needed, in three LDS stages.  The weight tile arrives as Q4_0 (2 blocks of 32 per row: 16 code
 // bytes + an fp16 scale) one step ahead in registers and is dequantized into
-// one of two LDS stages: the codes are pre-ordered (at load time) so that one
-// and-or per pair builds two halves 1024 + q, a packed subtract of 1032 gives
-// q - 8 exactly, and a packed multiply by the scale gives d * (q - 8) rounded
-// once to f16 (2^-11 relative).  One barrier per step.
+// one of two LDS stages.  The codes are pre-ordered (at load time) so that a
+// code pair sits at bits (4m, 16 + 4m) of a dword: one v_and_or_b32 per pair
+// builds two halves, 1024 + q for the pair at bits 0-3 (exponent with ulp 1)
+// and 64 + q for the pair at bits 4-7 (exponent with ulp 1/16), one shift by 8
+// serves the other two pairs, a packed subtract of 1032 or 72 gives q - 8
+// exactly and a packed multiply by the scale gives d * (q - 8) rounded once to
+// f16 (2^-11 relative): 13 VALU operations per 8 codes.  One barrier per step.
 //
 // LDS rows are 128 B with the 16-byte column c of row r stored at column
 // c ^ ((r >> 1) & 7): the MFMA fragment reads (rows l % 16, column l / 16),
@@ -29,6 +32,7 @@
 // l % 16 with the 8 consecutive k of group l / 16; the accumulator holds rows
 // 4 * (l / 16) + r (r = 0..3) of column l % 16.
 #include <algorithm>
+#include <type_traits>
 
 #include "mz_kernels.h"
 
@@ -58,10 +62,32 @@ __device__ __forceinline__ uint32_t pair_code(uint32_t w, int shift) {
   return ((w >> shift) & 0x000F000Fu) | 0x64006400u;
 }
 
-__device__ __forceinline__ uint32_t dequant_pair(uint32_t w, int shift, f16x2 d2) {
-  const f16x2 c = __builtin_bit_cast(f16x2, pair_code(w, shift));
-  const f16x2 off = {(_Float16)1032.0f, (_Float16)1032.0f};
-  return __builtin_bit_cast(uint32_t, (c - off) * d2);
+// (x & mask) | magic in one instruction (the mask from a scalar register, the
+// magic from a vector register: one scalar operand per VOP3 on this chip)
+__device__ __forceinline__ uint32_t and_or(uint32_t x, uint32_t mask, uint32_t magic) {
+  uint32_t r;
+  asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "s"(mask), "v"(magic));
+  return r;
+}
+
+// The 8 codes of one pre-ordered dword (pair m at bits 4m and 16 + 4m) ->
+// 4 f16x2 of d * (q - 8), pair m in component m.
+__device__ __forceinline__ uint4 dequant_dword(uint32_t w, f16x2 d2) {
+  const uint32_t mag_lo = 0x64006400u;   // 1024: code bits 0-3 add q
+  const uint32_t mag_hi = 0x54005400u;   // 64: code bits 4-7 add q (ulp 1/16)
+  const f16x2 off_lo = {(_Float16)1032.0f, (_Float16)1032.0f};
+  const f16x2 off_hi = {(_Float16)72.0f, (_Float16)72.0f};
+  const uint32_t w8 = w >> 8;
+  const f16x2 c0 = __builtin_bit_cast(f16x2, and_or(w, 0x000F000Fu, mag_lo));
+  const f16x2 c1 = __builtin_bit_cast(f16x2, and_or(w, 0x00F000F0u, mag_hi));
+  const f16x2 c2 = __builtin_bit_cast(f16x2, and_or(w8, 0x000F000Fu, mag_lo));
+  const f16x2 c3 = __builtin_bit_cast(f16x2, and_or(w8, 0x00F000F0u, mag_hi));
+  uint4 o;
+  o.x = __builtin_bit_cast(uint32_t, (c0 - off_lo) * d2);
+  o.y = __builtin_bit_cast(uint32_t, (c1 - off_hi) * d2);
+  o.z = __builtin_bit_cast(uint32_t, (c2 - off_lo) * d2);
+  o.w = __builtin_bit_cast(uint32_t, (c3 - off_hi) * d2);
+  return o;
 }
 
 // One pre-ordered Q4_0 block (4 dwords; dword i holds elements 8i..8i+7) of
@@ -72,13 +98,81 @@ __device__ __forceinline__ void dequant_block_to_lds(uint4 nib, uint16_t dbits, 
   const f16x2 d2 = {d, d};
   const uint32_t w[4] = {nib.x, nib.y, nib.z, nib.w};
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    uint4 o;
-    o.x = dequant_pair(w[i], 0, d2);
-    o.y = dequant_pair(w[i], 4, d2);
-    o.z = dequant_pair(w[i], 8, d2);
-    o.w = dequant_pair(w[i], 12, d2);
-    *reinterpret_cast<uint4*>(stage + swz(row, blk * 4 + i)) = o;
+  for (int i = 0; i < 4; ++i)
+    *reinterpret_cast<uint4*>(stage + swz(row, blk * 4 + i)) = dequant_dword(w[i], d2);
+}
+
+// Rotary-embedding epilogue of a wave's 64 x 128 (BM 256) or 16 x 128 (BM 64)
+// accumulator block.  Pair partners c and c + hd/2 of a head sit in tiles j
+// and j + JO (JO = hd / 32) of the same lane.  Row positions (and slot
+// offsets) are read first, then the (cos, sin) of two 16-row groups at once,
+// then the rotated values are stored: the table reads never wait behind the
+// stores of earlier rows.
+template <int EPI, int BM, int JO>
+__device__ __forceinline__ void rope_epilogue(const f32x4 (&acc)[BM / 64][8], const GemmRope& ea, void* Y, int M,
+                                              int mt, int nt, int wm, int wn, int col_in, int row_in) {
+  constexpr int MI = BM / 64, IB = (MI >= 2 && EPI == kEpiRopeQ) ? 2 : 1;   // row groups per table read
+  constexpr int HALF = JO * 16, HD = 2 * HALF;
+  const int rot_end = EPI == kEpiRopeQ ? ea.n_valid : ea.n_valid >> 1;   // rotated columns
+  const int col0 = nt * BN + wn * 128 + col_in;
+  int pos[MI][4];
+#pragma unroll
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = mt * BM + wm * (BM / 4) + i * 16 + row_in + r;
+      pos[i][r] = ea.pos[min(row, M - 1)];
+    }
+#pragma unroll
+  for (int i0 = 0; i0 < MI; i0 += IB) {
+    int64_t off[IB][4];
+    float2 cv[IB][4][4];
+#pragma unroll
+    for (int ii = 0; ii < IB; ++ii)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = mt * BM + wm * (BM / 4) + (i0 + ii) * 16 + row_in + r;
+        off[ii][r] = EPI == kEpiRopeKV ? ea.kv_off[min(row, M - 1)] : 0;
+        const float2* cs = ea.rope_cs + (size_t)pos[i0 + ii][r] * HALF;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int j = (q / JO) * 2 * JO + q % JO;   // first-half tiles: 0..JO-1, 2JO..3JO-1, ...
+          const int col = col0 + j * 16;
+          cv[ii][r][q] = col < rot_end ? cs[col & (HD - 1)] : float2{0.f, 0.f};
+        }
+      }
+#pragma unroll
+    for (int ii = 0; ii < IB; ++ii)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int i = i0 + ii;
+        const int row = mt * BM + wm * (BM / 4) + i * 16 + row_in + r;
+        if (row >= M || off[ii][r] < 0) continue;  // past the rows, or a row that writes no KV
+        _Float16* yr = EPI == kEpiRopeQ ? reinterpret_cast<_Float16*>(Y) + (size_t)row * ea.n_valid
+                                        : reinterpret_cast<_Float16*>(ea.slab + off[ii][r]);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int j = (q / JO) * 2 * JO + q % JO;
+          const int col = col0 + j * 16;
+          if (col < rot_end) {
+            const float x1 = acc[i][j][r], x2 = acc[i][j + JO][r];
+            const float2 c = cv[ii][r][q];
+            yr[col] = (_Float16)(x1 * c.x - x2 * c.y);
+            yr[col + HALF] = (_Float16)(x2 * c.x + x1 * c.y);
+          }
+        }
+        if constexpr (EPI == kEpiRopeKV) {
+          // values: V^T[c][pos % C] of the row's slot
+          const int pc = pos[i][r] & (ea.C - 1);
+          uint8_t* vt = ea.slab + off[ii][r] - (int64_t)pc * ea.n_valid + (int64_t)ea.C * ea.n_valid + pc * 2;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const int col = col0 + j * 16;
+            if (col >= rot_end && col < ea.n_valid)
+              *reinterpret_cast<_Float16*>(vt + (int64_t)(col - rot_end) * ea.C * 2) = (_Float16)acc[i][j][r];
+          }
+        }
+      }
   }
 }
 
@@ -94,7 +188,7 @@ template <int EPI, int BM>
 __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict__ X,
                                                      const int32_t* __restrict__ a_rows, int M, int K,
                                                      const uint8_t* __restrict__ Wp, int N,
-                                                     void* __restrict__ Y, int k_steps) {
+                                                     void* __restrict__ Y, int k_steps, GemmRope ea) {
   extern __shared__ __attribute__((aligned(16))) _Float16 lds[];
   constexpr int A_TILE = BM * ROW;                     // one activation stage
   constexpr int MI = BM / 64;                          // 16-row MFMA tiles per wave
@@ -212,6 +306,15 @@ __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict_
   // epilogue
   const int col_in = lane & 15;
   const int row_in = (lane >> 4) * 4;
+  if constexpr (EPI == kEpiRopeQ || EPI == kEpiRopeKV) {
+    if (ea.hd == 128)
+      rope_epilogue<EPI, BM, 4>(acc, ea, Y, M, mt, nt, wm, wn, col_in, row_in);
+    else if (ea.hd == 64)
+      rope_epilogue<EPI, BM, 2>(acc, ea, Y, M, mt, nt, wm, wn, col_in, row_in);
+    else
+      rope_epilogue<EPI, BM, 1>(acc, ea, Y, M, mt, nt, wm, wn, col_in, row_in);
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < MI; ++i) {
 #pragma unroll
@@ -359,7 +462,7 @@ constexpr size_t lds_bytes() {
 
 template <int EPI, int BM>
 void launch_bm(const _Float16* X, const int32_t* a_rows, int m, int n, int k, const uint8_t* W, void* y,
-               hipStream_t s, int n_split = 1, int k_steps = 0) {
+               hipStream_t s, int n_split = 1, int k_steps = 0, const GemmRope& ea = GemmRope{}) {
   static const bool lds_ok = [] {   // more than 64 KB of dynamic LDS, once per instantiation
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_q4_kernel<EPI, BM>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes<BM>());
@@ -368,19 +471,19 @@ void launch_bm(const _Float16* X, const int32_t* a_rows, int m, int n, int k, co
   (void)lds_ok;
   const int tiles = (n / BN) * ((m + BM - 1) / BM);
   hipLaunchKernelGGL((gemm_q4_kernel<EPI, BM>), dim3(tiles, n_split), dim3(NT), lds_bytes<BM>(), s, X, a_rows,
-                     m, k, W, n, y, k_steps);
+                     m, k, W, n, y, k_steps, ea);
 }
 
 int gemm_row_tile(int m, int n) { return (n / BN) * ((m + 255) / 256) < 128 ? 64 : 256; }
 
 template <int EPI>
 void launch_epi(const _Float16* X, const int32_t* a_rows, int m, int n, int k, const uint8_t* W, void* y,
-                hipStream_t s) {
+                hipStream_t s, const GemmRope& ea = GemmRope{}) {
   // 256-row tiles unless they leave most of the 256 CUs idle
   if (gemm_row_tile(m, n) == 64)
-    launch_bm<EPI, 64>(X, a_rows, m, n, k, W, y, s);
+    launch_bm<EPI, 64>(X, a_rows, m, n, k, W, y, s, 1, 0, ea);
   else
-    launch_bm<EPI, 256>(X, a_rows, m, n, k, W, y, s);
+    launch_bm<EPI, 256>(X, a_rows, m, n, k, W, y, s, 1, 0, ea);
 }
 
 int gemm_k_steps(int k, int n_split) {
@@ -438,6 +541,21 @@ void launch_gemm_q4(const void* x, int m, int n, int k, const void* w, int epilo
     case kEpiAdd: launch_epi<kEpiAdd>(X, a_rows, m, n, k, W, y, s); break;
     default: launch_epi<kEpiSwiGLU>(X, a_rows, m, n, k, W, y, s); break;
   }
+}
+
+bool gemm_rope_fusable(int head_dim, int chunk_tokens) {
+  return (head_dim == 32 || head_dim == 64 || head_dim == 128) && chunk_tokens > 0 &&
+         (chunk_tokens & (chunk_tokens - 1)) == 0;
+}
+
+void launch_gemm_q4_rope(const void* x, int m, int n, int k, const void* w, int epilogue, const GemmRope& ea,
+                         void* y, hipStream_t s, const int32_t* a_rows) {
+  const _Float16* X = reinterpret_cast<const _Float16*>(x);
+  const uint8_t* W = reinterpret_cast<const uint8_t*>(w);
+  if (epilogue == kEpiRopeQ)
+    launch_epi<kEpiRopeQ>(X, a_rows, m, n, k, W, y, s, ea);
+  else
+    launch_epi<kEpiRopeKV>(X, a_rows, m, n, k, W, y, s, ea);
 }
 
 }  // namespace mzk

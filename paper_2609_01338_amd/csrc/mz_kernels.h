@@ -16,7 +16,23 @@ constexpr int kGemmTileN = 256;
 constexpr int kGemmTileK = 64;
 constexpr int kGemmTileBytes = kGemmTileN * kGemmTileK / 2 + kGemmTileN * (kGemmTileK / 32) * 2;
 
-enum GemmEpilogue { kEpiStore = 0, kEpiAdd = 1, kEpiSwiGLU = 2, kEpiPartial = 3 };
+enum GemmEpilogue { kEpiStore = 0, kEpiAdd = 1, kEpiSwiGLU = 2, kEpiPartial = 3, kEpiRopeQ = 4, kEpiRopeKV = 5 };
+
+// Rotary-embedding epilogues (rotate-half pairs c, c + hd/2 of each head at
+// the row's position, (cos, sin) from rope_cs [pos][hd/2], rounded to f16).
+// kEpiRopeQ: y f16 [m][n_valid] holds the rotated queries (n_valid = q
+// columns).  kEpiRopeKV: output columns [0, n_valid/2) are keys, rotated and
+// written to slab + kv_off[r] (the row's token-major K row of its chunk
+// slot); [n_valid/2, n_valid) are values, written to the slot's V^T half
+// (V^T[c][pos % C] at slot + C * (n_valid/2) * 2 + (c * C + pos % C) * 2);
+// rows with kv_off < 0 write nothing.  pos is indexed by output row.
+struct GemmRope {
+  const int32_t* pos = nullptr;
+  const int64_t* kv_off = nullptr;
+  const float2* rope_cs = nullptr;
+  uint8_t* slab = nullptr;
+  int hd = 0, n_valid = 0, C = 0;
+};
 
 // Y = X . W^T: X f16 [m][k], W packed [n][k] (n % 128 == 0, k % 64 == 0).
 // kEpiStore: Y float [m][n] = acc; kEpiAdd: Y float [m][n] += acc;
@@ -24,6 +40,13 @@ enum GemmEpilogue { kEpiStore = 0, kEpiAdd = 1, kEpiSwiGLU = 2, kEpiPartial = 3 
 // With a_rows (device, m entries), output row r is computed from X row a_rows[r].
 void launch_gemm_q4(const void* x, int m, int n, int k, const void* w, int epilogue, void* y,
                     hipStream_t s, const int32_t* a_rows = nullptr);
+
+// Y = X . W^T with a rotary-embedding epilogue (kEpiRopeQ / kEpiRopeKV, see
+// GemmRope); n_valid <= n.  Only for gemm_rope_fusable(hd, C): head
+// dimension 32, 64 or 128, C a power of two.
+bool gemm_rope_fusable(int head_dim, int chunk_tokens);
+void launch_gemm_q4_rope(const void* x, int m, int n, int k, const void* w, int epilogue, const GemmRope& ea,
+                         void* y, hipStream_t s, const int32_t* a_rows = nullptr);
 
 // Split-K form for few rows: n_split ranges of whole 64-wide K steps
 // (ceil((k / 64) / n_split) steps each) write fp32 partials into ws

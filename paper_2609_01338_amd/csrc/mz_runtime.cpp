@@ -446,6 +446,7 @@ struct mz_ctx {
   int64_t split_ws_bytes = 0;
   bool attn_split = true;            // option attn_split
   bool gemm_split = true;            // option gemm_split
+  bool fuse_rope = true;             // option fuse_rope: RoPE (and the KV slot writes) in the GEMM epilogue
 
   // Y = X W^T on the compute stream, split over K when the tile grid alone
   // would leave most of the GPU idle
@@ -456,6 +457,16 @@ struct mz_ctx {
       mzk::launch_gemm_q4_splitk(X, m, n, k, W, epi, Y, ns, split_ws, s, rows);
     else
       mzk::launch_gemm_q4(X, m, n, k, W, epi, Y, s, rows);
+  }
+  // The projection with rotary embedding fused into its epilogue, when it
+  // runs unsplit and the shape allows it (false: the caller runs the
+  // projection and the RoPE kernel separately).
+  bool gemm_rope(const void* X, int m, int n, int k, const uint8_t* W, int epi, const mzk::GemmRope& ea, void* Y,
+                 hipStream_t s, const int32_t* rows) {
+    if (!fuse_rope || !mzk::gemm_rope_fusable(ea.hd, ea.C)) return false;
+    if (gemm_split && mzk::gemm_auto_splits(m, n, k, split_ws_bytes) > 1) return false;
+    mzk::launch_gemm_q4_rope(X, m, n, k, W, epi, ea, Y, s, rows);
+    return true;
   }
   int32_t* d_codec_slots = nullptr;  // per restore: destination slot of each compressed chunk
   hipEvent_t ev_meta = nullptr;      // restore metadata uploaded (the swap stream reads some)
@@ -897,24 +908,50 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
     // keys and values of the rows written at this layer (D_l)
     if (nd > 0) {
       const int32_t* dix = x->d_dix + dofs[l];
-      x->timed(kKGemmKV, 2.0 * nd * d * 2 * x->dkv, 2.0 * x->dkv * d * bpe_w + nd * (d * 2.0 + 2 * x->dkv * 4.0), cs,
-               [&] { x->gemm(x->xb, nd, x->kv_pad, d, unit + x->off_kv, mzk::kEpiStore, x->kvf, cs, dix); });
-      x->timed(kKRopeKV, 0, nd * (2 * x->dkv * 4.0 + 2 * x->dkv * 2.0), cs, [&] {
-        mzk::launch_rope_kv(x->kvf, x->kv_pad, nd, x->d_pos + dofs[l], x->d_kvoff + dofs[l], x->rope_cs, 0,
-                            x->nkv, x->hd, C, nullptr, x->kv_slab, cs);
-      });
+      mzk::GemmRope ea;
+      ea.pos = x->d_pos + dofs[l];
+      ea.kv_off = x->d_kvoff + dofs[l];
+      ea.rope_cs = x->rope_cs;
+      ea.slab = x->kv_slab;
+      ea.hd = x->hd;
+      ea.n_valid = 2 * x->dkv;
+      ea.C = C;
+      bool fused = false;
+      x->timed(kKGemmKV, 2.0 * nd * d * 2 * x->dkv, 2.0 * x->dkv * d * bpe_w + nd * (d * 2.0 + 2 * x->dkv * 2.0), cs,
+               [&] {
+                 fused = x->gemm_rope(x->xb, nd, x->kv_pad, d, unit + x->off_kv, mzk::kEpiRopeKV, ea, nullptr, cs,
+                                      dix);
+                 if (!fused) x->gemm(x->xb, nd, x->kv_pad, d, unit + x->off_kv, mzk::kEpiStore, x->kvf, cs, dix);
+               });
+      if (!fused)
+        x->timed(kKRopeKV, 0, nd * (2 * x->dkv * 4.0 + 2 * x->dkv * 2.0), cs, [&] {
+          mzk::launch_rope_kv(x->kvf, x->kv_pad, nd, x->d_pos + dofs[l], x->d_kvoff + dofs[l], x->rope_cs, 0,
+                              x->nkv, x->hd, C, nullptr, x->kv_slab, cs);
+        });
     }
     if (kv_copy[l] && !early_wait) HIPCHK(hipStreamWaitEvent(cs, x->ev_kv[l], 0));
     // queries, attention and MLP of the rows carried on (R_{l+1}; the last
     // position after the last layer)
     const int32_t* qix = x->d_qix + qofs[l];
     const int32_t* posq = x->d_posq + qofs[l];
-    x->timed(kKGemmQ, 2.0 * nq * d * x->dq, (double)x->dq * d * bpe_w + nq * (d * 2.0 + x->dq * 4.0), cs,
-             [&] { x->gemm(x->xb, nq, x->dq_pad, d, unit + x->off_q, mzk::kEpiStore, x->qf, cs, qix); });
-    x->timed(kKRopeQ, 0, nq * (x->dq * 4.0 + x->dq * 2.0), cs, [&] {
-      mzk::launch_rope_kv(x->qf, x->dq_pad, nq, posq, nullptr, x->rope_cs, x->nq, 0, x->hd, C, x->q16,
-                          x->kv_slab, cs);
-    });
+    {
+      mzk::GemmRope ea;
+      ea.pos = posq;
+      ea.rope_cs = x->rope_cs;
+      ea.hd = x->hd;
+      ea.n_valid = x->dq;
+      ea.C = C;
+      bool fused = false;
+      x->timed(kKGemmQ, 2.0 * nq * d * x->dq, (double)x->dq * d * bpe_w + nq * (d * 2.0 + x->dq * 2.0), cs, [&] {
+        fused = x->gemm_rope(x->xb, nq, x->dq_pad, d, unit + x->off_q, mzk::kEpiRopeQ, ea, x->q16, cs, qix);
+        if (!fused) x->gemm(x->xb, nq, x->dq_pad, d, unit + x->off_q, mzk::kEpiStore, x->qf, cs, qix);
+      });
+      if (!fused)
+        x->timed(kKRopeQ, 0, nq * (x->dq * 4.0 + x->dq * 2.0), cs, [&] {
+          mzk::launch_rope_kv(x->qf, x->dq_pad, nq, posq, nullptr, x->rope_cs, x->nq, 0, x->hd, C, x->q16,
+                              x->kv_slab, cs);
+        });
+    }
     if (nq < n) {
       float* dst = x->h[cur ^ 1];
       x->timed(kKGather, 0, (double)nq * d * 8.0, cs,
@@ -1199,6 +1236,7 @@ mz_status mz_set_option(mz_ctx* x, const char* key, int64_t value) {
     else if (k == "swap_trim") x->swap_trim = value != 0;
     else if (k == "attn_split") x->attn_split = value != 0;
     else if (k == "gemm_split") x->gemm_split = value != 0;
+    else if (k == "fuse_rope") x->fuse_rope = value != 0;
     else if (k == "kv_codec") {
       if (value && !x->codec_stage) {
         HIPCHK(hipMalloc((void**)&x->codec_stage, (size_t)x->max_chunks * (size_t)x->comp_bytes));

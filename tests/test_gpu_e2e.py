@@ -50,10 +50,12 @@ def _check_token(tok, logits, otok, ologits, name):
         assert gap <= 2 * err, name
 
 
-def run_import_flow(w, kv_state, w_state, prompt, name, engine=None, codec=False, evict_fn=None, generate=0):
+def run_import_flow(w, kv_state, w_state, prompt, name, engine=None, codec=False, evict_fn=None, generate=0,
+                    options=None):
     """Import the oracle's clean KV, evict, restore, first token; compare.
     With codec, both sides swap full chunks through the 8-bit codec and the
-    restored chunks must equal the oracle's round trip bit for bit."""
+    restored chunks must equal the oracle's round trip bit for bit.
+    options: engine options set before the restore (mz_set_option)."""
     torch_cuda()
     m = w.model
     C, dkv, L = m.chunk_tokens, m.dkv, m.n_layers
@@ -85,6 +87,8 @@ def run_import_flow(w, kv_state, w_state, prompt, name, engine=None, codec=False
         report("case", name=name, N=ctx.size, P=len(prompt), **{k: v for k, v in
                                                                  W.Plan(kv_state, w_state).counts().items()})
         mz.mz_set_option(eng.ctx, "kv_codec", int(codec))
+        for key, val in (options or {}).items():
+            mz.mz_set_option(eng.ctx, key, val)
         if evict_fn is None:
             mz.mz_evict(eng.ctx, kv_state, w_state)
         else:
@@ -273,6 +277,22 @@ def test_scaled_workload_import_flow(key, kw):
     plan = W.make_plan(w)
     prm = np.random.default_rng(1).integers(0, w.model.vocab, w.n_prompt).astype(np.int32)
     run_import_flow(w, plan.kv_state, plan.w_state, prm, w.key)
+
+
+@pytest.mark.parametrize("key,kw", SCALED, ids=[k for k, _ in SCALED])
+@pytest.mark.parametrize("fuse", [1, 0])
+def test_scaled_unsplit_rope_epilogue(key, kw, fuse):
+    """Every projection unsplit (gemm_split 0), so the query and key/value
+    projections run with the rotary embedding in their epilogue (fuse 1: keys
+    straight into their slot rows, values into the V^T halves) or as the
+    projection followed by the separate RoPE kernel (fuse 0); both against
+    the oracle at each layer shape (head dim 64 and 128, 256-token chunks,
+    prompts that start a partial chunk)."""
+    w = W.WORKLOADS[key].scaled(**kw)
+    plan = W.make_plan(w)
+    prm = np.random.default_rng(2).integers(0, w.model.vocab, w.n_prompt).astype(np.int32)
+    run_import_flow(w, plan.kv_state, plan.w_state, prm, f"{w.key}-unsplit-fuse{fuse}",
+                    options={"gemm_split": 0, "fuse_rope": fuse})
 
 
 @pytest.mark.parametrize("P", [0, 7])
