@@ -20,9 +20,13 @@
 // f16 (2^-11 relative): 13 VALU operations per 8 codes.  One barrier per step.
 //
 // LDS rows are 128 B with the 16-byte column c of row r stored at column
-// c ^ ((r >> 1) & 7): the MFMA fragment reads (rows l % 16, column l / 16),
-// the direct loads (8 lanes per row) and the dequantized stores (8 lanes on
-// 8 rows) are all bank-conflict free (measured on gfx950).
+// c ^ ((r >> 1) & 7).  The MFMA fragment reads (rows l % 16, column l / 16)
+// are conflict free.  A 16-byte store is written 8 lanes at a time into one
+// 128-byte half of the 64 banks (even or odd rows), so each group of 8 lanes
+// of the dequantized stores takes the two blocks of 4 rows of one parity:
+// the swizzle puts their 8 pieces in 8 distinct columns (measured on gfx950:
+// 8 LDS cycles per store instruction, against 16 for 8 lanes on 8
+// consecutive rows).
 //
 // Workgroups are numbered so that each XCD (workgroups are dealt to the 8 XCDs
 // round-robin) walks a contiguous run of tiles, M-major: neighbouring tiles on
@@ -223,10 +227,12 @@ __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict_
     const int r = min(mt * BM + pr, M - 1);
     a_src[i] = X + (size_t)(a_rows ? a_rows[r] : r) * K + (size_t)ks0 * BK + lc * 8;
   }
-  // weight loads: one Q4_0 block per thread; 8 consecutive lanes take 8 rows of
-  // the same block so their LDS stores land in distinct banks
+  // weight loads: one Q4_0 block per thread.  Lanes 8g..8g+7 take blocks 0
+  // and 1 of rows 8 (g / 2) + (g % 2) + {0, 2, 4, 6} (one row parity, so their
+  // stores stay in one bank half); a wave's loads cover 32 consecutive rows,
+  // one contiguous kilobyte of codes.
   const uint8_t* wtile = Wp + ((size_t)nt * (K / BK) + ks0) * kGemmTileBytes;
-  const int b_row = (tid & 7) | ((tid >> 4) << 3), b_blk = (tid >> 3) & 1;
+  const int b_row = 8 * (tid >> 4) + ((tid >> 3) & 1) + 2 * ((tid & 7) >> 1), b_blk = tid & 1;
   const int b_idx = b_row * 2 + b_blk;
 
   f32x4 acc[MI][8];
@@ -280,19 +286,43 @@ __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict_
     if (more_b) load_b(kt + 1);
     const _Float16* Ab = As + (kt % A_STAGES) * A_TILE;
     const _Float16* Bb = Bs + (kt & 1) * B_TILE;
+    if constexpr (EPI != kEpiRopeKV) {
+      // every fragment of the step is requested before the first MFMA, so the
+      // LDS latency of the second 32-wide half hides under the first half
+      f16x8 a[BK / 32][MI], bq[BK / 32][8];
 #pragma unroll
-    for (int ks = 0; ks < BK / 32; ++ks) {
-      f16x8 a[MI];
-#pragma unroll
-      for (int i = 0; i < MI; ++i)
-        a[i] = *reinterpret_cast<const f16x8*>(Ab + swz(wm * (BM / 4) + i * 16 + frag_row, ks * 4 + frag_c));
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const f16x8 bf =
-            *reinterpret_cast<const f16x8*>(Bb + swz(wn * 128 + j * 16 + frag_row, ks * 4 + frag_c));
+      for (int ks = 0; ks < BK / 32; ++ks) {
 #pragma unroll
         for (int i = 0; i < MI; ++i)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[i], bf, acc[i][j], 0, 0, 0);
+          a[ks][i] = *reinterpret_cast<const f16x8*>(Ab + swz(wm * (BM / 4) + i * 16 + frag_row, ks * 4 + frag_c));
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          bq[ks][j] = *reinterpret_cast<const f16x8*>(Bb + swz(wn * 128 + j * 16 + frag_row, ks * 4 + frag_c));
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int ks = 0; ks < BK / 32; ++ks)
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+#pragma unroll
+          for (int i = 0; i < MI; ++i)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[ks][i], bq[ks][j], acc[i][j], 0, 0, 0);
+    } else {
+      // the key/value epilogue needs the registers: one half at a time
+#pragma unroll
+      for (int ks = 0; ks < BK / 32; ++ks) {
+        f16x8 a[MI];
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+          a[i] = *reinterpret_cast<const f16x8*>(Ab + swz(wm * (BM / 4) + i * 16 + frag_row, ks * 4 + frag_c));
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const f16x8 bf =
+              *reinterpret_cast<const f16x8*>(Bb + swz(wn * 128 + j * 16 + frag_row, ks * 4 + frag_c));
+#pragma unroll
+          for (int i = 0; i < MI; ++i)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[i], bf, acc[i][j], 0, 0, 0);
+        }
       }
     }
     if (more_b) {
