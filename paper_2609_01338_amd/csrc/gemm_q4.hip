@@ -506,14 +506,66 @@ void launch_bm(const _Float16* X, const int32_t* a_rows, int m, int n, int k, co
 
 int gemm_row_tile(int m, int n) { return (n / BN) * ((m + 255) / 256) < 128 ? 64 : 256; }
 
+int device_cus() {
+  static const int cus = [] {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    return n;
+  }();
+  return cus;
+}
+
+// Output rows [r0, r0 + m) of the product: the row-indexed pointers (row
+// list or activations, output, RoPE positions and slot offsets) are shifted.
+template <int EPI, int BM>
+void launch_rows(const _Float16* X, const int32_t* a_rows, int r0, int m, int n, int k, const uint8_t* W, void* y,
+                 hipStream_t s, const GemmRope& ea) {
+  const _Float16* x = a_rows ? X : X + (size_t)r0 * k;
+  const int32_t* ar = a_rows ? a_rows + r0 : nullptr;
+  GemmRope e = ea;
+  if (e.pos) e.pos += r0;
+  if (e.kv_off) e.kv_off += r0;
+  void* yy = y;
+  if (EPI == kEpiSwiGLU)
+    yy = reinterpret_cast<_Float16*>(y) + (size_t)r0 * (n / 2);
+  else if (EPI == kEpiRopeQ)
+    yy = reinterpret_cast<_Float16*>(y) + (size_t)r0 * ea.n_valid;
+  else if (EPI == kEpiStore || EPI == kEpiAdd)
+    yy = reinterpret_cast<float*>(y) + (size_t)r0 * n;
+  launch_bm<EPI, BM>(x, ar, m, n, k, W, yy, s, 1, 0, e);
+}
+
+// Relative duration of a 64-row tile against a 256-row one (a quarter of the
+// MFMA work, the same weight traffic and dequantization).
+constexpr double kTile64Cost = 0.35;
+
 template <int EPI>
 void launch_epi(const _Float16* X, const int32_t* a_rows, int m, int n, int k, const uint8_t* W, void* y,
                 hipStream_t s, const GemmRope& ea = GemmRope{}) {
   // 256-row tiles unless they leave most of the 256 CUs idle
-  if (gemm_row_tile(m, n) == 64)
+  if (gemm_row_tile(m, n) == 64) {
     launch_bm<EPI, 64>(X, a_rows, m, n, k, W, y, s, 1, 0, ea);
-  else
-    launch_bm<EPI, 256>(X, a_rows, m, n, k, W, y, s, 1, 0, ea);
+    return;
+  }
+  // A ragged last row of 256-row tiles can make a final round of workgroups
+  // that occupies few CUs (16 column tiles x 129 row tiles = 8 rounds + 16
+  // workgroups on 256 CUs).  Then the whole 256-row tiles run in one launch
+  // and the remaining rows as 64-row tiles in a second one.
+  const int nt = n / BN, cus = device_cus();
+  const int full = m / 256, rem = m - full * 256;
+  if (rem > 0 && full > 0) {
+    auto rounds = [&](int tiles) { return (double)((tiles + cus - 1) / cus); };
+    const double one = rounds(nt * (full + 1));
+    const double two = rounds(nt * full) + kTile64Cost * rounds(nt * ((rem + 63) / 64));
+    if (two < one) {
+      launch_rows<EPI, 256>(X, a_rows, 0, full * 256, n, k, W, y, s, ea);
+      launch_rows<EPI, 64>(X, a_rows, full * 256, rem, n, k, W, y, s, ea);
+      return;
+    }
+  }
+  launch_bm<EPI, 256>(X, a_rows, m, n, k, W, y, s, 1, 0, ea);
 }
 
 int gemm_k_steps(int k, int n_split) {
