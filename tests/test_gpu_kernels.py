@@ -268,7 +268,7 @@ def test_attention_split_validation():
     assert mz.mz_attention_auto_splits(129, 32895, 32, 8, 128, 64 << 20) > 8
 
 
-@pytest.mark.parametrize("M,d", [(1, 256), (300, 2048), (77, 4096), (5, 1536)])
+@pytest.mark.parametrize("M,d", [(1, 256), (300, 2048), (77, 4096), (5, 1536), (3, 8196), (2, 12292)])
 def test_rmsnorm(M, d):
     torch = torch_cuda()
     rng = np.random.default_rng(M * d)
