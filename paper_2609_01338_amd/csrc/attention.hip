@@ -369,7 +369,8 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
   // 0-31 of tile kt; phase B issues the PV MFMAs of tile kt with the
   // exponentials of keys 32-63 and then the max of tile kt+1.  Slots are
   // fenced so the compiler keeps this order: the MFMAs of a wave then run
-  // under its own VALU work.  Fragment reads run two slots ahead.  Global
+  // under its own VALU work.  Fragment reads run three slots ahead, each
+  // issued before its slot's MFMA.  Global
   // loads of K tile kt+2 and V tile kt+1 are in flight across the iteration
   // and land in the buffers freed in iteration kt-1; one barrier per
   // iteration.
@@ -413,14 +414,16 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
     // are discarded)
     {
       const _Float16* Kn = Kbuf(kt + 1);
-      f16x8 fa = kfrag(Kn, 0), fb = kfrag(Kn, 1);
+      f16x8 fa = kfrag(Kn, 0), fb = kfrag(Kn, 1), fc = kfrag(Kn, 2);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < NQK; ++i) {
-        const f16x8 fc = i + 2 < NQK ? kfrag(Kn, i + 2) : fb;
+        const f16x8 fd = i + 3 < NQK ? kfrag(Kn, i + 3) : fc;
+        __builtin_amdgcn_sched_barrier(0);   // the read goes out ahead of the MFMA
         sn[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa, qf[i >> 1], i < 2 ? zero16 : sn[i & 1], 0, 0, 0);
         fa = fb;
         fb = fc;
+        fc = fd;
         // 8 exponential pairs over the slots
         if (i % (NQK / 8) == 0) exp_pair(sc, i / (NQK / 8), pk);
         __builtin_amdgcn_sched_barrier(0);
@@ -437,14 +440,16 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
     float mx = -INFINITY;
     {
       const _Float16* Vt = Vbuf(kt);
-      f16x8 fa = vfrag(Vt, 0), fb = vfrag(Vt, 1);
+      f16x8 fa = vfrag(Vt, 0), fb = vfrag(Vt, 1), fc = vfrag(Vt, 2);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < NPV; ++i) {
-        const f16x8 fc = i + 2 < NPV ? vfrag(Vt, i + 2) : fb;
+        const f16x8 fd = i + 3 < NPV ? vfrag(Vt, i + 3) : fc;
+        __builtin_amdgcn_sched_barrier(0);   // the read goes out ahead of the MFMA
         o[i % TN] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa, pk[i / TN], o[i % TN], 0, 0, 0);
         fa = fb;
         fb = fc;
+        fc = fd;
         if (i < NPV / 2) {
           // keys 32-63 (pk[2], pk[3]) are needed from slot NPV/2 on
 #pragma unroll
