@@ -205,18 +205,27 @@ Rows compute_rows(const uint8_t* kv_state, int L, int nc, int N, int P, int C) {
   rows.nR.resize(L);
   rows.nD.resize(L);
   // walked by chunk: the cost is the rows produced, not the cached context
-  // (a decode step carries one row per layer of a 32K context)
+  // (a decode step carries one row per layer of a 32K context); each layer's
+  // list is sized first and filled by whole chunk runs
   for (int l = 0; l < L; ++l) {
     std::vector<int32_t>& r = rows.R[l];
     int nd = P;
+    size_t n = (size_t)(S - N);
     for (int c = 0; c < nc; ++c) {
       const int p0 = c * C, p1 = std::min(N, p0 + C);
-      if (maxdrop[c] >= l)
-        for (int p = p0; p < p1; ++p) r.push_back(p);
+      if (maxdrop[c] >= l) n += (size_t)(p1 - p0);
       if (kv_state[(size_t)l * nc + c] == MZ_DROP) nd += p1 - p0;
     }
-    for (int p = N; p < S; ++p) r.push_back(p);
-    if (r.empty() || r.back() != S - 1) r.push_back(S - 1);
+    const bool last_extra = P == 0 && (N == 0 || maxdrop[nc - 1] < l);   // S - 1 not among the rows yet
+    r.resize(n + (last_extra ? 1 : 0));
+    int32_t* o = r.data();
+    for (int c = 0; c < nc; ++c) {
+      if (maxdrop[c] < l) continue;
+      const int p0 = c * C, p1 = std::min(N, p0 + C);
+      for (int p = p0; p < p1; ++p) *o++ = p;
+    }
+    for (int p = N; p < S; ++p) *o++ = p;
+    if (last_extra) *o++ = S - 1;
     rows.nR[l] = (int32_t)r.size();
     rows.nD[l] = nd;
   }
