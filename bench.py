@@ -437,6 +437,14 @@ def main():
                 "avg_launch_ms": round(dom["ms"] / dom["launches"], 5)}
     steps = len(ttft)
     kernels_ms_per_step = {k: round(v["ms"] / steps, 3) for k, v in stats["kernels"].items()}
+    # the recompute projections together (Q, K/V, O, gate/up, down; their
+    # split-K forms included): total FLOPs over total kernel time
+    proj = [v for k, v in stats["kernels"].items() if k.startswith("gemm_q4")]
+    proj_ms, proj_flops = sum(v["ms"] for v in proj), sum(v["flops"] for v in proj)
+    proj_tflops = proj_flops / (proj_ms * 1e-3) / 1e12 if proj_ms > 0 else 0.0
+    projections = {"ms_per_step": round(proj_ms / steps, 3), "tflops": round(proj_tflops, 1),
+                   "frac": round(proj_tflops / PEAK_MFMA_TFLOPS, 4),
+                   "frac_of_measured_peak": round(proj_tflops / ceilings["mfma_f16_tflops"], 4)}
     kernel_tflops = {k: round(v["flops"] / (v["ms"] * 1e-3) / 1e12, 1)
                      for k, v in stats["kernels"].items() if v["flops"] > 0}
     algo = stats["algo_flops"]
@@ -462,6 +470,7 @@ def main():
         "ceilings_measured": ceilings,
         "kernel_ms_per_step": kernels_ms_per_step,
         "kernel_tflops": kernel_tflops,
+        "projections": projections,
         "invariant": {"clean_token": clean_tok, "tokens": toks,
                       "max_logit_err_vs_clean": max(logit_err)},
         "roofline": roof,

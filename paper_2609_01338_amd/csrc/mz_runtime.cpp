@@ -28,9 +28,11 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <exception>
 #include <memory>
 #include <set>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "../../include/mz.h"
@@ -192,10 +194,40 @@ struct Rows {
   std::vector<std::vector<int32_t>> R;   // ascending positions per layer
 };
 
+// fn(l) for l in [0, L): on host threads when the work (rows to produce) is
+// large enough to repay starting them, else in this thread.  fn must only
+// touch data of its own layer.
+template <class F>
+void for_layers(int L, int64_t work, F&& fn) {
+  constexpr int64_t kMinWork = 1 << 16;
+  const int hw = (int)std::thread::hardware_concurrency();
+  const int T = std::min({L, 8, std::max(hw, 1)});
+  if (work < kMinWork || T < 2) {
+    for (int l = 0; l < L; ++l) fn(l);
+    return;
+  }
+  std::vector<std::exception_ptr> err(T);
+  auto run = [&](int t) {
+    try {
+      for (int l = t; l < L; l += T) fn(l);
+    } catch (...) {
+      err[t] = std::current_exception();
+    }
+  };
+  std::vector<std::thread> th;
+  th.reserve(T - 1);
+  for (int t = 1; t < T; ++t) th.emplace_back(run, t);
+  run(0);
+  for (auto& x : th) x.join();
+  for (auto& e : err)
+    if (e) std::rethrow_exception(e);
+}
+
 // R_l = {p < N : chunk(p) dropped at some l' >= l} U {N..S-1} U {S-1};
 // D_l = {p < N : chunk(p) dropped at l} U {N..S-1}.
-Rows compute_rows(const uint8_t* kv_state, int L, int nc, int N, int P, int C) {
-  Rows rows;
+// Fills `rows`, reusing the capacity of its vectors (a restore's lists are
+// megabytes: fresh allocations would fault their pages in on every call).
+void compute_rows_into(Rows& rows, const uint8_t* kv_state, int L, int nc, int N, int P, int C) {
   const int S = N + P;
   std::vector<int> maxdrop(nc, -1);
   for (int l = 0; l < L; ++l)
@@ -207,17 +239,23 @@ Rows compute_rows(const uint8_t* kv_state, int L, int nc, int N, int P, int C) {
   // walked by chunk: the cost is the rows produced, not the cached context
   // (a decode step carries one row per layer of a 32K context); each layer's
   // list is sized first and filled by whole chunk runs
+  int64_t total = 0;
   for (int l = 0; l < L; ++l) {
-    std::vector<int32_t>& r = rows.R[l];
     int nd = P;
-    size_t n = (size_t)(S - N);
+    int64_t n = S - N;
     for (int c = 0; c < nc; ++c) {
       const int p0 = c * C, p1 = std::min(N, p0 + C);
-      if (maxdrop[c] >= l) n += (size_t)(p1 - p0);
+      if (maxdrop[c] >= l) n += p1 - p0;
       if (kv_state[(size_t)l * nc + c] == MZ_DROP) nd += p1 - p0;
     }
     const bool last_extra = P == 0 && (N == 0 || maxdrop[nc - 1] < l);   // S - 1 not among the rows yet
-    r.resize(n + (last_extra ? 1 : 0));
+    rows.nR[l] = (int32_t)(n + (last_extra ? 1 : 0));
+    rows.nD[l] = nd;
+    total += rows.nR[l];
+  }
+  for_layers(L, total, [&](int l) {
+    std::vector<int32_t>& r = rows.R[l];
+    r.resize((size_t)rows.nR[l]);
     int32_t* o = r.data();
     for (int c = 0; c < nc; ++c) {
       if (maxdrop[c] < l) continue;
@@ -225,10 +263,13 @@ Rows compute_rows(const uint8_t* kv_state, int L, int nc, int N, int P, int C) {
       for (int p = p0; p < p1; ++p) *o++ = p;
     }
     for (int p = N; p < S; ++p) *o++ = p;
-    if (last_extra) *o++ = S - 1;
-    rows.nR[l] = (int32_t)r.size();
-    rows.nD[l] = nd;
-  }
+    if (o != r.data() + r.size()) *o++ = S - 1;
+  });
+}
+
+Rows compute_rows(const uint8_t* kv_state, int L, int nc, int N, int P, int C) {
+  Rows rows;
+  compute_rows_into(rows, kv_state, L, nc, N, P, C);
   return rows;
 }
 
@@ -348,9 +389,10 @@ enum KernelKind {
 const char* kKindName[kKCount] = {"embed_q4", "rmsnorm", "gemm_q4_kv", "rope_kv", "gemm_q4_q",
                                   "rope_q", "gather_rows", "attention", "gemm_q4_o",
                                   "gemm_q4_gateup", "gemm_q4_down", "lm_head_argmax", "attention_split"};
-// HIP kernel symbol each kind launches (to line up with profiler summaries)
-const char* kKindKernel[kKCount] = {"embed_kernel", "rmsnorm_kernel", "gemm_q4_kernel<0>",
-                                    "rope_kv_kernel", "gemm_q4_kernel<0>", "rope_kv_kernel",
+// HIP kernel symbol each kind launches (to line up with profiler summaries;
+// the Q and K/V projections name their unsplit RoPE-epilogue form)
+const char* kKindKernel[kKCount] = {"embed_kernel", "rmsnorm_kernel", "gemm_q4_kernel<5>",
+                                    "rope_kv_kernel", "gemm_q4_kernel<4>", "rope_kv_kernel",
                                     "gather_rows_kernel", "attn_kernel", "gemm_q4_kernel<1>",
                                     "gemm_q4_kernel<2>", "gemm_q4_kernel<1>",
                                     "lm_head_kernel+argmax_kernel", "attn_kernel<split>+attn_merge_kernel"};
@@ -485,6 +527,7 @@ struct mz_ctx {
   std::vector<PendingTiming> pending;
   KindStats kstats[kKCount];
   std::vector<int32_t> last_nR, last_nD, last_nQ;
+  Rows rows_buf;                     // row lists of the last restore (capacity kept)
   int64_t last_swap_kv_bytes = 0, last_swap_w_bytes = 0, last_reload_w_bytes = 0;
   int64_t last_copies = 0;
   double last_swap_ms = -1;
@@ -647,7 +690,8 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
   std::vector<uint8_t> st((size_t)L * std::max(nc_old, 1), MZ_RES);
   for (int l = 0; l < L; ++l)
     for (int c = 0; c < nc_old; ++c) st[(size_t)l * nc_old + c] = x->kv_state[(size_t)l * MC + c];
-  Rows rows = compute_rows(st.data(), L, nc_old, N, P, C);
+  Rows& rows = x->rows_buf;
+  compute_rows_into(rows, st.data(), L, nc_old, N, P, C);
 
   // --- allocate slots: swapped chunks first, in runs matching their arena order
   std::vector<std::vector<CopyJob>> kv_jobs(L);
@@ -784,7 +828,10 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
     if (!codec_slots[l].empty())
       memcpy(s_cs + cofs[l], codec_slots[l].data(), codec_slots[l].size() * 4);
   memcpy(s_tab, x->table.data(), b_tab);
-  for (int l = 0; l < L; ++l) {
+  int64_t total_rows = 0;
+  for (int l = 0; l < L; ++l) total_rows += rows.nR[l];
+  std::vector<char> count_ok(L, 1);
+  for_layers(L, total_rows, [&](int l) {
     const std::vector<int32_t>& R = rows.R[l];
     int64_t j = dofs[l];
     for (size_t i = 0; i < R.size(); ++i) {
@@ -797,7 +844,7 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
         ++j;
       }
     }
-    if (j != dofs[l + 1]) fail(MZ_EINVAL, "internal: written-row count mismatch at layer %d", l);
+    if (j != dofs[l + 1]) count_ok[l] = 0;
     if (l + 1 < L) {
       const std::vector<int32_t>& Rn = rows.R[l + 1];
       size_t a = 0;
@@ -810,7 +857,9 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
       s_posq[qofs[l]] = R.back();             // S - 1
       s_qix[qofs[l]] = (int32_t)R.size() - 1;
     }
-  }
+  });
+  for (int l = 0; l < L; ++l)
+    if (!count_ok[l]) fail(MZ_EINVAL, "internal: written-row count mismatch at layer %d", l);
   for (int i = 0; i < rows.nR[0]; ++i) {
     const int p = rows.R[0][i];
     s_tok[i] = p < N ? x->tokens[p] : prompt[p - N];
