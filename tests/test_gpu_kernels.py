@@ -136,10 +136,13 @@ def _layer_gemms(key):
 @pytest.mark.parametrize("key", ["tiny", "1b", "3b", "1p5b", "8b"])
 def test_gemm_full_layer_shapes(key):
     """Every projection of the workload at its full row count (the launch the
-    benchmark times), checked on sampled rows including the ragged tail."""
+    benchmark times), checked on sampled rows including the ragged tail and
+    both sides of the row where whole 256-row tiles end (a ragged remainder
+    may run as 64-row tiles in a second launch)."""
     for i, (M, N, K, epi) in enumerate(_layer_gemms(key)):
         rng = np.random.default_rng(i)
-        rows = np.unique(np.concatenate([rng.choice(M, min(M, 24), replace=False), [0, M - 1]]))
+        edge = [r for r in (M // 256 * 256 - 1, M // 256 * 256) if 0 <= r < M]
+        rows = np.unique(np.concatenate([rng.choice(M, min(M, 24), replace=False), [0, M - 1], edge]))
         _gemm_case(M, N, K, epi, seed=100 + i, sample_rows=rows)
 
 
