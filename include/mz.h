@@ -152,9 +152,9 @@ mz_status mz_generate(mz_ctx *ctx, int32_t token, int32_t n, int32_t *tokens_out
  * context runs split over the keys, as mz_attention_split, default; 0: always
  * one pass), "gemm_split" (1: GEMMs of few rows run split over K, as
  * mz_q4_gemm_split, default; 0: never), "fuse_rope" (1: the query and
- * key/value projections apply the rotary embedding in their epilogue and
- * write f16 queries and the chunk slots directly whenever they run unsplit,
- * default; 0: projection, then a separate RoPE pass), "swap_trim" (1: free the pinned swap segments after each restore,
+ * key/value projections apply the rotary embedding in their epilogue, or in
+ * the reduce of their K splits, and write f16 queries and the chunk slots
+ * directly, default; 0: projection, then a separate RoPE pass), "swap_trim" (1: free the pinned swap segments after each restore,
  * as the paper's growing swap stack does; 0: keep them for the next
  * eviction, default).  Test hooks: "debug_poison" (1: fill every
  * slot and weight unit allocated by a restore with NaN before it is

@@ -485,6 +485,46 @@ __global__ __launch_bounds__(256) void gemm_splitk_reduce(const float* __restric
   }
 }
 
+// Sum of the K splits in split order, then the rotary embedding of
+// kEpiRopeQ / kEpiRopeKV (see GemmRope): one thread per (row, rotated pair
+// c, c + hd/2) and, for keys and values, per (row, value column).
+template <int EPI>
+__global__ __launch_bounds__(256) void gemm_splitk_reduce_rope(const float* __restrict__ part, int ns, int M, int N,
+                                                               GemmRope ea, void* __restrict__ Y) {
+  const int half = ea.hd >> 1;
+  const int rot = EPI == kEpiRopeQ ? ea.n_valid : ea.n_valid >> 1;   // rotated columns
+  const int pairs = rot >> 1;
+  const int per_row = pairs + (EPI == kEpiRopeKV ? ea.n_valid >> 1 : 0);
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)M * per_row) return;
+  const int row = (int)(t / per_row), j = (int)(t % per_row);
+  const int64_t off = EPI == kEpiRopeKV ? ea.kv_off[row] : 0;
+  if (off < 0) return;                       // a row that writes no KV
+  const int p = ea.pos[row];
+  const size_t plane = (size_t)M * N;
+  const float* pr = part + (size_t)row * N;
+  if (j < pairs) {
+    const int i = j % half, c = (j / half) * ea.hd + i;
+    float x1 = pr[c], x2 = pr[c + half];
+    for (int sp = 1; sp < ns; ++sp) {
+      x1 += pr[sp * plane + c];
+      x2 += pr[sp * plane + c + half];
+    }
+    const float2 cv = ea.rope_cs[(size_t)p * half + i];
+    _Float16* yr = EPI == kEpiRopeQ ? reinterpret_cast<_Float16*>(Y) + (size_t)row * ea.n_valid
+                                    : reinterpret_cast<_Float16*>(ea.slab + off);
+    yr[c] = (_Float16)(x1 * cv.x - x2 * cv.y);
+    yr[c + half] = (_Float16)(x2 * cv.x + x1 * cv.y);
+  } else {
+    const int v = j - pairs;
+    float a = pr[rot + v];
+    for (int sp = 1; sp < ns; ++sp) a += pr[sp * plane + rot + v];
+    const int pc = p & (ea.C - 1);
+    uint8_t* vt = ea.slab + off - (int64_t)pc * ea.n_valid + (int64_t)ea.C * ea.n_valid + pc * 2;
+    *reinterpret_cast<_Float16*>(vt + (int64_t)v * ea.C * 2) = (_Float16)a;
+  }
+}
+
 template <int BM>
 constexpr size_t lds_bytes() {
   return ((size_t)A_STAGES * BM * ROW + (size_t)B_STAGES * B_TILE) * sizeof(_Float16);
@@ -591,8 +631,11 @@ int gemm_auto_splits(int m, int n, int k, int64_t ws_cap) {
   return (nk + ks - 1) / ks;   // no empty trailing split
 }
 
-void launch_gemm_q4_splitk(const void* x, int m, int n, int k, const void* w, int epilogue, void* y, int n_split,
-                           void* ws, hipStream_t s, const int32_t* a_rows) {
+namespace {
+// The fp32 partials [split][m][n] of a split-K product; returns the number of
+// splits written.
+int launch_partials(const void* x, int m, int n, int k, const void* w, int n_split, void* ws, hipStream_t s,
+                    const int32_t* a_rows) {
   const _Float16* X = reinterpret_cast<const _Float16*>(x);
   const uint8_t* W = reinterpret_cast<const uint8_t*>(w);
   const int ks = gemm_k_steps(k, n_split);
@@ -604,6 +647,26 @@ void launch_gemm_q4_splitk(const void* x, int m, int n, int k, const void* w, in
     launch_bm<kEpiPartial, 64>(X, a_rows, m, n, k, W, ws, s, ns, ks);
   else
     launch_bm<kEpiPartial, 256>(X, a_rows, m, n, k, W, ws, s, ns, ks);
+  return ns;
+}
+}  // namespace
+
+void launch_gemm_q4_splitk_rope(const void* x, int m, int n, int k, const void* w, int epilogue, const GemmRope& ea,
+                                void* y, int n_split, void* ws, hipStream_t s, const int32_t* a_rows) {
+  const int ns = launch_partials(x, m, n, k, w, n_split, ws, s, a_rows);
+  const int rot = epilogue == kEpiRopeQ ? ea.n_valid : ea.n_valid / 2;
+  const int64_t per_row = rot / 2 + (epilogue == kEpiRopeKV ? ea.n_valid / 2 : 0);
+  const dim3 grid((unsigned)(((int64_t)m * per_row + 255) / 256));
+  const float* part = reinterpret_cast<const float*>(ws);
+  if (epilogue == kEpiRopeQ)
+    hipLaunchKernelGGL(gemm_splitk_reduce_rope<kEpiRopeQ>, grid, dim3(256), 0, s, part, ns, m, n, ea, y);
+  else
+    hipLaunchKernelGGL(gemm_splitk_reduce_rope<kEpiRopeKV>, grid, dim3(256), 0, s, part, ns, m, n, ea, y);
+}
+
+void launch_gemm_q4_splitk(const void* x, int m, int n, int k, const void* w, int epilogue, void* y, int n_split,
+                           void* ws, hipStream_t s, const int32_t* a_rows) {
+  const int ns = launch_partials(x, m, n, k, w, n_split, ws, s, a_rows);
   const int64_t outs = (int64_t)m * (epilogue == kEpiSwiGLU ? n / 2 : n) / 4;
   const dim3 grid((unsigned)((outs + 255) / 256));
   const float* part = reinterpret_cast<const float*>(ws);

@@ -55,6 +55,11 @@ void launch_gemm_q4_rope(const void* x, int m, int n, int k, const void* w, int 
 void launch_gemm_q4_splitk(const void* x, int m, int n, int k, const void* w, int epilogue, void* y, int n_split,
                            void* ws, hipStream_t s, const int32_t* a_rows = nullptr);
 int64_t gemm_splitk_ws_bytes(int m, int n, int n_split);
+// Split-K form with a rotary-embedding epilogue (kEpiRopeQ / kEpiRopeKV): the
+// splits are added in order, then rotated and written as the unsplit
+// epilogues do.
+void launch_gemm_q4_splitk_rope(const void* x, int m, int n, int k, const void* w, int epilogue, const GemmRope& ea,
+                                void* y, int n_split, void* ws, hipStream_t s, const int32_t* a_rows = nullptr);
 // Splits that fill the chip for this shape within ws_cap bytes (1: no split).
 int gemm_auto_splits(int m, int n, int k, int64_t ws_cap);
 

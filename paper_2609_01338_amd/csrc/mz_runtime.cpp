@@ -509,14 +509,17 @@ struct mz_ctx {
     else
       mzk::launch_gemm_q4(X, m, n, k, W, epi, Y, s, rows);
   }
-  // The projection with rotary embedding fused into its epilogue, when it
-  // runs unsplit and the shape allows it (false: the caller runs the
-  // projection and the RoPE kernel separately).
+  // The projection with rotary embedding fused into its epilogue (or into
+  // the reduce of its K splits), when the shape allows it (false: the caller
+  // runs the projection and the RoPE kernel separately).
   bool gemm_rope(const void* X, int m, int n, int k, const uint8_t* W, int epi, const mzk::GemmRope& ea, void* Y,
                  hipStream_t s, const int32_t* rows) {
     if (!fuse_rope || !mzk::gemm_rope_fusable(ea.hd, ea.C)) return false;
-    if (gemm_split && mzk::gemm_auto_splits(m, n, k, split_ws_bytes) > 1) return false;
-    mzk::launch_gemm_q4_rope(X, m, n, k, W, epi, ea, Y, s, rows);
+    const int ns = gemm_split ? mzk::gemm_auto_splits(m, n, k, split_ws_bytes) : 1;
+    if (ns > 1)
+      mzk::launch_gemm_q4_splitk_rope(X, m, n, k, W, epi, ea, Y, ns, split_ws, s, rows);
+    else
+      mzk::launch_gemm_q4_rope(X, m, n, k, W, epi, ea, Y, s, rows);
     return true;
   }
   int32_t* d_codec_slots = nullptr;  // per restore: destination slot of each compressed chunk

@@ -287,7 +287,9 @@ def test_scaled_unsplit_rope_epilogue(key, kw, fuse):
     straight into their slot rows, values into the V^T halves) or as the
     projection followed by the separate RoPE kernel (fuse 0); both against
     the oracle at each layer shape (head dim 64 and 128, 256-token chunks,
-    prompts that start a partial chunk)."""
+    prompts that start a partial chunk).  With the default options these
+    few-row shapes run split over K, the rotary embedding then in the
+    reduce (test_scaled_workload_import_flow)."""
     w = W.WORKLOADS[key].scaled(**kw)
     plan = W.make_plan(w)
     prm = np.random.default_rng(2).integers(0, w.model.vocab, w.n_prompt).astype(np.int32)
