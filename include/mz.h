@@ -154,7 +154,11 @@ mz_status mz_generate(mz_ctx *ctx, int32_t token, int32_t n, int32_t *tokens_out
  * mz_q4_gemm_split, default; 0: never), "fuse_rope" (1: the query and
  * key/value projections apply the rotary embedding in their epilogue, or in
  * the reduce of their K splits, and write f16 queries and the chunk slots
- * directly, default; 0: projection, then a separate RoPE pass), "swap_trim" (1: free the pinned swap segments after each restore,
+ * directly, default; 0: projection, then a separate RoPE pass), "fuse_norm"
+ * (1: a layer step of a single row whose projections all run split over K
+ * forms that row's RMSNorm inside them, the same f16 values the RMSNorm
+ * pass writes, and leaves that pass out, default; 0: always a separate
+ * pass), "swap_trim" (1: free the pinned swap segments after each restore,
  * as the paper's growing swap stack does; 0: keep them for the next
  * eviction, default).  Test hooks: "debug_poison" (1: fill every
  * slot and weight unit allocated by a restore with NaN before it is

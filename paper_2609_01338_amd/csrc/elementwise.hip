@@ -2,59 +2,32 @@
 // rotary embedding with KV scatter into chunk slots, embedding gather with
 // Q4_0 dequantization, row compaction, and the output head with argmax.
 #include "mz_kernels.h"
+#include "rownorm.h"
 
 namespace mzk {
 namespace {
 
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
-
-// Sum over a 256-thread block; every thread gets the result.
-__device__ __forceinline__ float block_sum256(float v, float* red) {
-  v = wave_sum(v);
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  __syncthreads();
-  if (lane == 0) red[w] = v;
-  __syncthreads();
-  return red[0] + red[1] + red[2] + red[3];
-}
-
 // One 256-thread block per row; d % 4 == 0.  The row is read once: each
-// thread keeps its up to RN_MAX float4 pieces in registers between the sum of
-// squares and the scaled store (rows longer than 256 * RN_MAX * 4 read the
-// rest twice).
-constexpr int RN_MAX = 8;
+// thread keeps its up to kRowNormRegs float4 pieces in registers between the
+// sum of squares and the scaled store (rows longer than 256 * kRowNormRegs * 4
+// read the rest twice).
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ h, int d, float eps,
                                                       _Float16* __restrict__ x) {
   __shared__ float red[4];
   const int row = blockIdx.x;
   const int n4 = d / 4;
-  const float4* hr = reinterpret_cast<const float4*>(h + (size_t)row * d);
-  float4 v[RN_MAX];
-  float ss = 0.f;
-#pragma unroll
-  for (int k = 0; k < RN_MAX; ++k) {
-    const int i = threadIdx.x + k * 256;
-    v[k] = i < n4 ? hr[i] : float4{0.f, 0.f, 0.f, 0.f};
-    ss += v[k].x * v[k].x + v[k].y * v[k].y + v[k].z * v[k].z + v[k].w * v[k].w;
-  }
-  for (int i = threadIdx.x + RN_MAX * 256; i < n4; i += 256) {
-    const float4 u = hr[i];
-    ss += u.x * u.x + u.y * u.y + u.z * u.z + u.w * u.w;
-  }
-  ss = block_sum256(ss, red);
-  const float r = 1.0f / __builtin_sqrtf(ss / (float)d + eps);
+  const float* hrow = h + (size_t)row * d;
+  float4 v[kRowNormRegs];
+  const float r = row_inv_rms(hrow, d, eps, v, red);
   typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
   f16x4* xr = reinterpret_cast<f16x4*>(x + (size_t)row * d);
 #pragma unroll
-  for (int k = 0; k < RN_MAX; ++k) {
+  for (int k = 0; k < kRowNormRegs; ++k) {
     const int i = threadIdx.x + k * 256;
     if (i < n4) xr[i] = f16x4{(_Float16)(v[k].x * r), (_Float16)(v[k].y * r), (_Float16)(v[k].z * r), (_Float16)(v[k].w * r)};
   }
-  for (int i = threadIdx.x + RN_MAX * 256; i < n4; i += 256) {
+  const float4* hr = reinterpret_cast<const float4*>(hrow);
+  for (int i = threadIdx.x + kRowNormRegs * 256; i < n4; i += 256) {
     const float4 u = hr[i];
     xr[i] = f16x4{(_Float16)(u.x * r), (_Float16)(u.y * r), (_Float16)(u.z * r), (_Float16)(u.w * r)};
   }

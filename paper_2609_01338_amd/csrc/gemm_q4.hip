@@ -39,6 +39,7 @@
 #include <type_traits>
 
 #include "mz_kernels.h"
+#include "rownorm.h"
 
 namespace mzk {
 namespace {
@@ -384,10 +385,14 @@ __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict_
 // accumulates products with the f16 activations in fp32 (v_dot2).  The
 // activations of each batch of tiles are staged in LDS (one pair per
 // thread) and read as broadcasts.  Partials go to part [split][N] for
-// gemm_splitk_reduce.
+// gemm_splitk_reduce.  NORM: the row is RMSNorm's input, fp32 H [.][K]; each
+// workgroup first takes its scale r through the norm kernel's own routine
+// and stages (f16)(h * r), the values the norm kernel would have written.
 constexpr int kGemvAhead = 8;     // K tiles whose codes are in flight per thread
 
+template <bool NORM>
 __global__ __launch_bounds__(256) void gemv_q4_kernel(const _Float16* __restrict__ X,
+                                                      const float* __restrict__ H, float eps,
                                                       const int32_t* __restrict__ a_rows, int K,
                                                       const uint8_t* __restrict__ Wp, int N,
                                                       float* __restrict__ part, int k_steps) {
@@ -398,7 +403,16 @@ __global__ __launch_bounds__(256) void gemv_q4_kernel(const _Float16* __restrict
   const int kt_n = min(k_steps, nk - kt0);
   const int nt = blockIdx.x;
   const int r = threadIdx.x;
-  const _Float16* xrow = X + (size_t)(a_rows ? a_rows[0] : 0) * K + (size_t)kt0 * BK;
+  const size_t row = a_rows ? a_rows[0] : 0;
+  const _Float16* xrow = X + row * K + (size_t)kt0 * BK;
+  const float* hrow = H + row * K;
+  float rn = 0.f;
+  if constexpr (NORM) {
+    __shared__ float red[4];
+    float4 v[kRowNormRegs];
+    rn = row_inv_rms(hrow, K, eps, v, red);
+    hrow += (size_t)kt0 * BK;
+  }
   const uint8_t* tile0 = Wp + ((size_t)nt * nk + kt0) * kGemmTileBytes;
   const f16x2 off = {(_Float16)1032.0f, (_Float16)1032.0f};
   float acc = 0.f;
@@ -415,7 +429,14 @@ __global__ __launch_bounds__(256) void gemv_q4_kernel(const _Float16* __restrict
       }
     }
     __syncthreads();   // the previous batch is done with xs
-    if (r < (kt_n - t0) * 32) xs[r] = *reinterpret_cast<const f16x2*>(xrow + (size_t)t0 * BK + 2 * r);
+    if (r < (kt_n - t0) * 32) {
+      if constexpr (NORM) {
+        const float2 hv = *reinterpret_cast<const float2*>(hrow + (size_t)t0 * BK + 2 * r);
+        xs[r] = f16x2{(_Float16)(hv.x * rn), (_Float16)(hv.y * rn)};
+      } else {
+        xs[r] = *reinterpret_cast<const f16x2*>(xrow + (size_t)t0 * BK + 2 * r);
+      }
+    }
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < kGemvAhead; ++j) {
@@ -635,14 +656,17 @@ namespace {
 // The fp32 partials [split][m][n] of a split-K product; returns the number of
 // splits written.
 int launch_partials(const void* x, int m, int n, int k, const void* w, int n_split, void* ws, hipStream_t s,
-                    const int32_t* a_rows) {
+                    const int32_t* a_rows, const float* h_norm, float eps) {
   const _Float16* X = reinterpret_cast<const _Float16*>(x);
   const uint8_t* W = reinterpret_cast<const uint8_t*>(w);
   const int ks = gemm_k_steps(k, n_split);
   const int ns = (k / BK + ks - 1) / ks;
-  if (m == 1)
-    hipLaunchKernelGGL(gemv_q4_kernel, dim3(n / BN, ns), dim3(256), 0, s, X, a_rows, k, W, n,
+  if (h_norm)
+    hipLaunchKernelGGL(gemv_q4_kernel<true>, dim3(n / BN, ns), dim3(256), 0, s, X, h_norm, eps, a_rows, k, W, n,
                        reinterpret_cast<float*>(ws), ks);
+  else if (m == 1)
+    hipLaunchKernelGGL(gemv_q4_kernel<false>, dim3(n / BN, ns), dim3(256), 0, s, X, nullptr, 0.f, a_rows, k, W,
+                       n, reinterpret_cast<float*>(ws), ks);
   else if (gemm_row_tile(m, n) == 64)
     launch_bm<kEpiPartial, 64>(X, a_rows, m, n, k, W, ws, s, ns, ks);
   else
@@ -652,8 +676,9 @@ int launch_partials(const void* x, int m, int n, int k, const void* w, int n_spl
 }  // namespace
 
 void launch_gemm_q4_splitk_rope(const void* x, int m, int n, int k, const void* w, int epilogue, const GemmRope& ea,
-                                void* y, int n_split, void* ws, hipStream_t s, const int32_t* a_rows) {
-  const int ns = launch_partials(x, m, n, k, w, n_split, ws, s, a_rows);
+                                void* y, int n_split, void* ws, hipStream_t s, const int32_t* a_rows,
+                                const float* h_norm, float eps) {
+  const int ns = launch_partials(x, m, n, k, w, n_split, ws, s, a_rows, h_norm, eps);
   const int rot = epilogue == kEpiRopeQ ? ea.n_valid : ea.n_valid / 2;
   const int64_t per_row = rot / 2 + (epilogue == kEpiRopeKV ? ea.n_valid / 2 : 0);
   const dim3 grid((unsigned)(((int64_t)m * per_row + 255) / 256));
@@ -665,8 +690,8 @@ void launch_gemm_q4_splitk_rope(const void* x, int m, int n, int k, const void* 
 }
 
 void launch_gemm_q4_splitk(const void* x, int m, int n, int k, const void* w, int epilogue, void* y, int n_split,
-                           void* ws, hipStream_t s, const int32_t* a_rows) {
-  const int ns = launch_partials(x, m, n, k, w, n_split, ws, s, a_rows);
+                           void* ws, hipStream_t s, const int32_t* a_rows, const float* h_norm, float eps) {
+  const int ns = launch_partials(x, m, n, k, w, n_split, ws, s, a_rows, h_norm, eps);
   const int64_t outs = (int64_t)m * (epilogue == kEpiSwiGLU ? n / 2 : n) / 4;
   const dim3 grid((unsigned)((outs + 255) / 256));
   const float* part = reinterpret_cast<const float*>(ws);

@@ -51,15 +51,19 @@ void launch_gemm_q4_rope(const void* x, int m, int n, int k, const void* w, int 
 // Split-K form for few rows: n_split ranges of whole 64-wide K steps
 // (ceil((k / 64) / n_split) steps each) write fp32 partials into ws
 // (gemm_splitk_ws_bytes(m, n, n_split) bytes), then one kernel adds them in
-// split order and applies the epilogue.
+// split order and applies the epilogue.  h_norm (m == 1 only): x is not read;
+// the row is RMSNorm(h_norm row, eps) formed inside the product, the same
+// f16 values launch_rmsnorm writes.
 void launch_gemm_q4_splitk(const void* x, int m, int n, int k, const void* w, int epilogue, void* y, int n_split,
-                           void* ws, hipStream_t s, const int32_t* a_rows = nullptr);
+                           void* ws, hipStream_t s, const int32_t* a_rows = nullptr,
+                           const float* h_norm = nullptr, float eps = 0.f);
 int64_t gemm_splitk_ws_bytes(int m, int n, int n_split);
 // Split-K form with a rotary-embedding epilogue (kEpiRopeQ / kEpiRopeKV): the
 // splits are added in order, then rotated and written as the unsplit
 // epilogues do.
 void launch_gemm_q4_splitk_rope(const void* x, int m, int n, int k, const void* w, int epilogue, const GemmRope& ea,
-                                void* y, int n_split, void* ws, hipStream_t s, const int32_t* a_rows = nullptr);
+                                void* y, int n_split, void* ws, hipStream_t s, const int32_t* a_rows = nullptr,
+                                const float* h_norm = nullptr, float eps = 0.f);
 // Splits that fill the chip for this shape within ws_cap bytes (1: no split).
 int gemm_auto_splits(int m, int n, int k, int64_t ws_cap);
 

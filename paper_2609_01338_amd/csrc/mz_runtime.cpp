@@ -498,14 +498,16 @@ struct mz_ctx {
   bool attn_split = true;            // option attn_split
   bool gemm_split = true;            // option gemm_split
   bool fuse_rope = true;             // option fuse_rope: RoPE (and the KV slot writes) in the GEMM epilogue
+  bool fuse_norm = true;             // option fuse_norm: a single row's RMSNorm inside its split-K GEMVs
 
   // Y = X W^T on the compute stream, split over K when the tile grid alone
-  // would leave most of the GPU idle
+  // would leave most of the GPU idle.  hn: X is RMSNorm(hn) formed inside the
+  // product (only where norm_in_gemv(m, n, k)).
   void gemm(const void* X, int m, int n, int k, const uint8_t* W, int epi, void* Y, hipStream_t s,
-            const int32_t* rows = nullptr) {
+            const int32_t* rows = nullptr, const float* hn = nullptr) {
     const int ns = gemm_split ? mzk::gemm_auto_splits(m, n, k, split_ws_bytes) : 1;
     if (ns > 1)
-      mzk::launch_gemm_q4_splitk(X, m, n, k, W, epi, Y, ns, split_ws, s, rows);
+      mzk::launch_gemm_q4_splitk(X, m, n, k, W, epi, Y, ns, split_ws, s, rows, hn, cfg.rms_eps);
     else
       mzk::launch_gemm_q4(X, m, n, k, W, epi, Y, s, rows);
   }
@@ -513,14 +515,19 @@ struct mz_ctx {
   // the reduce of its K splits), when the shape allows it (false: the caller
   // runs the projection and the RoPE kernel separately).
   bool gemm_rope(const void* X, int m, int n, int k, const uint8_t* W, int epi, const mzk::GemmRope& ea, void* Y,
-                 hipStream_t s, const int32_t* rows) {
+                 hipStream_t s, const int32_t* rows, const float* hn = nullptr) {
     if (!fuse_rope || !mzk::gemm_rope_fusable(ea.hd, ea.C)) return false;
     const int ns = gemm_split ? mzk::gemm_auto_splits(m, n, k, split_ws_bytes) : 1;
     if (ns > 1)
-      mzk::launch_gemm_q4_splitk_rope(X, m, n, k, W, epi, ea, Y, ns, split_ws, s, rows);
+      mzk::launch_gemm_q4_splitk_rope(X, m, n, k, W, epi, ea, Y, ns, split_ws, s, rows, hn, cfg.rms_eps);
     else
       mzk::launch_gemm_q4_rope(X, m, n, k, W, epi, ea, Y, s, rows);
     return true;
+  }
+  // A one-row product that runs as the split-K GEMV, which can normalize its
+  // own input row (a decode step: the RMSNorm launch is then left out)
+  bool norm_in_gemv(int m, int n, int k) const {
+    return fuse_norm && gemm_split && m == 1 && mzk::gemm_auto_splits(m, n, k, split_ws_bytes) > 1;
   }
   int32_t* d_codec_slots = nullptr;  // per restore: destination slot of each compressed chunk
   hipEvent_t ev_meta = nullptr;      // restore metadata uploaded (the swap stream reads some)
@@ -959,8 +966,13 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
     if (w_copy[l]) HIPCHK(hipStreamWaitEvent(cs, x->ev_w[l], 0));
     const uint8_t* unit = x->unit_ptr(l);
     float* h = x->h[cur];
-    x->timed(kKRmsnorm, 0, (double)n * d * 6.0, cs,
-             [&] { mzk::launch_rmsnorm(h, n, d, x->cfg.rms_eps, x->xb, cs); });
+    // a single row whose projections all run as GEMVs normalizes inside them
+    const bool norm1_fused = n == 1 && (nd == 0 || x->norm_in_gemv(nd, x->kv_pad, d)) &&
+                             (nq == 0 || x->norm_in_gemv(nq, x->dq_pad, d));
+    const float* hn1 = norm1_fused ? h : nullptr;
+    if (!norm1_fused)
+      x->timed(kKRmsnorm, 0, (double)n * d * 6.0, cs,
+               [&] { mzk::launch_rmsnorm(h, n, d, x->cfg.rms_eps, x->xb, cs); });
     // prompt rows appended to a partial last chunk that was swapped out land in
     // the restored slot: its copy must be done before they are written
     const bool early_wait = kv_copy[l] && P > 0 && N % C != 0 &&
@@ -981,8 +993,9 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
       x->timed(kKGemmKV, 2.0 * nd * d * 2 * x->dkv, 2.0 * x->dkv * d * bpe_w + nd * (d * 2.0 + 2 * x->dkv * 2.0), cs,
                [&] {
                  fused = x->gemm_rope(x->xb, nd, x->kv_pad, d, unit + x->off_kv, mzk::kEpiRopeKV, ea, nullptr, cs,
-                                      dix);
-                 if (!fused) x->gemm(x->xb, nd, x->kv_pad, d, unit + x->off_kv, mzk::kEpiStore, x->kvf, cs, dix);
+                                      dix, hn1);
+                 if (!fused)
+                   x->gemm(x->xb, nd, x->kv_pad, d, unit + x->off_kv, mzk::kEpiStore, x->kvf, cs, dix, hn1);
                });
       if (!fused)
         x->timed(kKRopeKV, 0, nd * (2 * x->dkv * 4.0 + 2 * x->dkv * 2.0), cs, [&] {
@@ -1004,8 +1017,8 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
       ea.C = C;
       bool fused = false;
       x->timed(kKGemmQ, 2.0 * nq * d * x->dq, (double)x->dq * d * bpe_w + nq * (d * 2.0 + x->dq * 2.0), cs, [&] {
-        fused = x->gemm_rope(x->xb, nq, x->dq_pad, d, unit + x->off_q, mzk::kEpiRopeQ, ea, x->q16, cs, qix);
-        if (!fused) x->gemm(x->xb, nq, x->dq_pad, d, unit + x->off_q, mzk::kEpiStore, x->qf, cs, qix);
+        fused = x->gemm_rope(x->xb, nq, x->dq_pad, d, unit + x->off_q, mzk::kEpiRopeQ, ea, x->q16, cs, qix, hn1);
+        if (!fused) x->gemm(x->xb, nq, x->dq_pad, d, unit + x->off_q, mzk::kEpiStore, x->qf, cs, qix, hn1);
       });
       if (!fused)
         x->timed(kKRopeQ, 0, nq * (x->dq * 4.0 + x->dq * 2.0), cs, [&] {
@@ -1040,10 +1053,12 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
     });
     x->timed(kKGemmO, 2.0 * nq * x->dq * d, (double)d * x->dq * bpe_w + nq * (x->dq * 2.0 + d * 8.0), cs,
              [&] { x->gemm(x->xb, nq, x->d_pad, x->dq, unit + x->off_o, mzk::kEpiAdd, h, cs); });
-    x->timed(kKRmsnorm, 0, (double)nq * d * 6.0, cs,
-             [&] { mzk::launch_rmsnorm(h, nq, d, x->cfg.rms_eps, x->xb, cs); });
+    const float* hn2 = x->norm_in_gemv(nq, 2 * x->ffp, d) ? h : nullptr;
+    if (!hn2)
+      x->timed(kKRmsnorm, 0, (double)nq * d * 6.0, cs,
+               [&] { mzk::launch_rmsnorm(h, nq, d, x->cfg.rms_eps, x->xb, cs); });
     x->timed(kKGemmGateUp, 2.0 * nq * d * 2.0 * x->ff, 2.0 * x->ff * d * bpe_w + nq * (d * 2.0 + x->ff * 2.0), cs,
-             [&] { x->gemm(x->xb, nq, 2 * x->ffp, d, unit + x->off_gu, mzk::kEpiSwiGLU, x->act, cs); });
+             [&] { x->gemm(x->xb, nq, 2 * x->ffp, d, unit + x->off_gu, mzk::kEpiSwiGLU, x->act, cs, nullptr, hn2); });
     x->timed(kKGemmDown, 2.0 * nq * x->ff * d, (double)d * x->ff * bpe_w + nq * (x->ffp * 2.0 + d * 8.0), cs,
              [&] { x->gemm(x->act, nq, x->d_pad, x->ffp, unit + x->off_dn, mzk::kEpiAdd, h, cs); });
     algo += 2.0 * nd * d * 2 * x->dkv + 2.0 * nq * d * 2 * x->dq + 2.0 * nq * 3 * d * x->ff + att_flops;
@@ -1297,6 +1312,7 @@ mz_status mz_set_option(mz_ctx* x, const char* key, int64_t value) {
     else if (k == "swap_trim") x->swap_trim = value != 0;
     else if (k == "attn_split") x->attn_split = value != 0;
     else if (k == "gemm_split") x->gemm_split = value != 0;
+    else if (k == "fuse_norm") x->fuse_norm = value != 0;
     else if (k == "fuse_rope") x->fuse_rope = value != 0;
     else if (k == "kv_codec") {
       if (value && !x->codec_stage) {

@@ -384,6 +384,44 @@ def test_scaled_8b_evict_size():
     _size_flow(w, [half // 2, half - half // 2, 10 ** 13], 56e9, 1e13, 2, prm, "8b-size", codec=True)
 
 
+@pytest.mark.parametrize("key", ["8b", "tiny"])
+def test_decode_norm_in_gemv_same_bits(key):
+    """Decode steps with each single row's RMSNorm formed inside its split-K
+    GEMVs (fuse_norm 1) against the separate RMSNorm pass (fuse_norm 0):
+    the same tokens, and K/V rows and logits equal bit for bit, since both
+    take the norm scale through one routine (the oracle comparison of decode
+    is test_scaled_8b_generate / test_tiny_generate_after_restore)."""
+    torch_cuda()
+    w = W.WORKLOADS[key]
+    if key == "8b":
+        w = w.scaled(n_layers=2, n_ctx=512, n_prompt=16)
+    m = w.model
+    C, dkv = m.chunk_tokens, m.dkv
+    ctx, prm = W.make_tokens(w)
+    S, n = ctx.size + len(prm), 5   # n generated tokens, then one more step
+    outs = []
+    for fuse in (1, 0):
+        eng = mz.Engine(m, blob_for(w), max_ctx=S + n + 9)
+        try:
+            mz.mz_set_option(eng.ctx, "fuse_norm", fuse)
+            mz.mz_prefill_context(eng.ctx, np.concatenate([ctx, prm]))
+            tok, _ = mz.mz_first_token(eng.ctx, m.vocab)
+            toks = mz.mz_generate(eng.ctx, tok, n)
+            mz.mz_restore_and_prefill(eng.ctx, toks[-1:].astype(np.int32))
+            _, logits = mz.mz_first_token(eng.ctx, m.vocab)
+            kv = [mz.mz_read_kv(eng.ctx, l, c, C, dkv) for l in range(m.n_layers)
+                  for c in range(S // C, (S + n) // C + 1)]
+            outs.append((toks, logits, kv))
+        finally:
+            eng.close()
+    (t1, g1, kv1), (t0, g0, kv0) = outs
+    report("case", name=f"{key}-fuse-norm-bits", tokens=list(map(int, t1)))
+    assert (t1 == t0).all(), key
+    assert g1.tobytes() == g0.tobytes(), key
+    for (k1, v1), (k0, v0) in zip(kv1, kv0):
+        assert k1.tobytes() == k0.tobytes() and v1.tobytes() == v0.tobytes(), key
+
+
 def test_tiny_generate_after_restore(tiny_engine):
     """Restore of a mixed plan, first token, then 12 generated tokens (they
     cross into a new chunk)."""
