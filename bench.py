@@ -38,6 +38,57 @@ PEAK_MFMA_TFLOPS = 2500.0      # MI355X dense bf16 / fp16 MFMA
 PEAK_HBM_GBPS = 8000.0
 
 
+class BoardMonitor:
+    """Socket power and per-XCD shader clocks, read by a host thread through
+    amdsmi (read-only metrics) every `period_s` while `active` is set; the
+    summary is None where amdsmi is unavailable."""
+
+    def __init__(self, period_s=0.02):
+        import threading
+        self.active, self.samples, self.stop, self.err = False, [], False, None
+        try:
+            import amdsmi
+            amdsmi.amdsmi_init()
+            self.amdsmi = amdsmi
+            self.h = amdsmi.amdsmi_get_processor_handles()[0]
+            self.cap_w = amdsmi.amdsmi_get_power_cap_info(self.h)["power_cap"] / 1e6
+        except Exception as e:   # no amdsmi, no device access
+            self.err = f"{type(e).__name__}: {e}"
+            return
+        self.period = period_s
+        self.th = threading.Thread(target=self._run, daemon=True)
+        self.th.start()
+
+    def _run(self):
+        while not self.stop:
+            if self.active:
+                try:
+                    m = self.amdsmi.amdsmi_get_gpu_metrics_info(self.h)
+                    clk = [c for c in (m.get("current_gfxclks") or []) if isinstance(c, (int, float)) and c < 10000]
+                    pw = m.get("current_socket_power")
+                    if isinstance(pw, (int, float)) and clk:
+                        self.samples.append((float(pw), clk))
+                except Exception as e:
+                    self.err = f"{type(e).__name__}: {e}"
+            time.sleep(self.period)
+
+    def summary(self):
+        self.stop = True
+        if self.err and not self.samples:
+            return {"error": self.err}
+        if not self.samples:
+            return None
+        pw = np.array([s[0] for s in self.samples])
+        n = min(len(s[1]) for s in self.samples)
+        clk = np.array([s[1][:n] for s in self.samples], dtype=np.float64)
+        return {"socket_power_w_mean": round(float(pw.mean()), 1), "socket_power_w_max": round(float(pw.max()), 1),
+                "power_cap_w": round(self.cap_w, 1), "gfxclk_mhz_mean": round(float(clk.mean()), 1),
+                "gfxclk_mhz_per_xcd": [round(float(c), 1) for c in clk.mean(axis=0)],
+                "samples": len(self.samples),
+                "source": f"amdsmi current_socket_power / current_gfxclks every {self.period * 1e3:.0f} ms "
+                          "inside the timed steps (GPU busy and idle parts alike)"}
+
+
 def measured_traffic(kernel, workload):
     """The recorded counter traffic if it still describes this kernel's source, else None."""
     import hashlib
@@ -386,15 +437,18 @@ def main():
 
     ttft, toks, logit_err = [], [], []
     stats = None
+    board = BoardMonitor()
     for step in range(args.warmup + args.steps):
         timed = step >= args.warmup
         if step == args.warmup:
             mz.mz_set_option(e, "kernel_timing", 1)
         mz.mz_evict(e, plan.kv_state, plan.w_state)
+        board.active = timed
         t0 = time.perf_counter()
         mz.mz_restore_and_prefill(e, prompt)
         tok, logits = mz.mz_first_token(e, m.vocab)
         dt = time.perf_counter() - t0
+        board.active = False
         if timed:
             ttft.append(dt)
         toks.append(tok)
@@ -468,6 +522,7 @@ def main():
                     "GBps": (round((stats["swap_kv_bytes"] + stats["swap_w_bytes"]) / stats["swap_ms"] / 1e6, 2)
                              if stats["swap_ms"] and stats["swap_ms"] > 0 else None)},
         "ceilings_measured": ceilings,
+        "board_during_timed_steps": board.summary(),
         "kernel_ms_per_step": kernels_ms_per_step,
         "kernel_tflops": kernel_tflops,
         "projections": projections,

@@ -150,7 +150,9 @@ mz_status mz_generate(mz_ctx *ctx, int32_t token, int32_t n, int32_t *tokens_out
  * enabling it the first time allocates a device staging ring of one layer's
  * chunks), "attn_split" (1: attention of few query rows against a long
  * context runs split over the keys, as mz_attention_split, default; 0: always
- * one pass), "gemm_split" (1: GEMMs of few rows run split over K, as
+ * one pass), "attn_queue" (1: the attention of many rows runs as
+ * mz_attention_queued with queues owned by the context, default; 0: as
+ * mz_attention), "gemm_split" (1: GEMMs of few rows run split over K, as
  * mz_q4_gemm_split, default; 0: never), "fuse_rope" (1: the query and
  * key/value projections apply the rotary embedding in their epilogue, or in
  * the reduce of their K splits, and write f16 queries and the chunk slots
@@ -367,6 +369,20 @@ mz_status mz_attention(const void *q_f16, const int32_t *qpos, int32_t m, const 
                        const int32_t *table, int32_t n_table, int32_t chunk_tokens,
                        int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, void *out_f16,
                        void *stream);
+
+/* mz_attention with persistent workgroups that take the query tiles from
+ * per-KV-head work queues (same arguments, same result bits).  Each XCD first
+ * serves the queue of its own KV head, heaviest tiles first, then takes the
+ * lightest tiles left in the others, so XCDs that run at a higher clock take
+ * more of the work.  work_queues: device, caller-owned, 16 int32 that are
+ * zero before the first call; each call leaves them zero.  Calls that share
+ * them must not be in flight at the same time.  Where n_kv_heads does not
+ * divide 8 or chunk_tokens < 64 this runs as mz_attention.  EINVAL as
+ * mz_attention, and for a NULL work_queues. */
+mz_status mz_attention_queued(const void *q_f16, const int32_t *qpos, int32_t m, const void *slab,
+                              const int32_t *table, int32_t n_table, int32_t chunk_tokens,
+                              int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, void *out_f16,
+                              int32_t *work_queues, void *stream);
 
 /* Split-key form of mz_attention for few query rows against a long context
  * (the paper's short requests, Sec. 6; the attention of its custom kernel,

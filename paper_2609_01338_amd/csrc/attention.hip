@@ -78,16 +78,14 @@ constexpr int v_tile_halves() { return HD * KT; }
 // Opart [split][M][nq][HD]) and (running max, row sum) (into MLpart
 // [split][M][nq]; max -inf and sum 0 for a query that sees no key of the
 // split).  Without SPLIT the whole key range is one pass and O is final.
+// One work item: query tile `tile` (rows 32 * qw * tile ..) against KV head kvh.
 template <int HD, int NW, bool DIRECT, bool SPLIT>
-__global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restrict__ Q,
-                                                       const int32_t* __restrict__ qpos, int M,
-                                                       const uint8_t* __restrict__ slab,
-                                                       const int32_t* __restrict__ table, int C,
-                                                       int cshift, int64_t slot_bytes, int nq, int nkv,
-                                                       int group, int qw, int n_qtiles,
-                                                       float scale_log2, _Float16* __restrict__ O, int tps,
-                                                       _Float16* __restrict__ Opart,
-                                                       float2* __restrict__ MLpart) {
+__device__ __forceinline__ void attn_tile(const _Float16* __restrict__ Q, const int32_t* __restrict__ qpos, int M,
+                                          const uint8_t* __restrict__ slab, const int32_t* __restrict__ table,
+                                          int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group,
+                                          int qw, float scale_log2, _Float16* __restrict__ O, int tps,
+                                          _Float16* __restrict__ Opart, float2* __restrict__ MLpart, int tile,
+                                          int kvh) {
   constexpr int NTH = 64 * NW;
   constexpr int KC = HD / 8;                        // 16-byte columns of a K row
   constexpr int K_SEGS = KT * KC;                   // 16-byte pieces of a K tile
@@ -103,23 +101,6 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
   const int col = lane & 31;        // query column of this lane
   const int dkv = nkv * HD;
 
-  // block -> (query tile, kv head).  Workgroups are dealt to the 8 XCDs
-  // round-robin (x = b % 8).  When nkv divides 8, XCD x serves kv head x % nkv
-  // only, taking every (8/nkv)-th query tile heaviest first, so the CUs of an
-  // XCD stream the same keys and share them in its L2; otherwise XCD x takes
-  // tiles x, x+8, ... with all kv heads of a tile in a row.
-  const int b = blockIdx.x;
-  const int xcd = b % 8, j = b / 8;
-  int kvh, tile_rank;
-  if (8 % nkv == 0) {
-    kvh = xcd % nkv;
-    tile_rank = j * (8 / nkv) + xcd / nkv;
-  } else {
-    kvh = j % nkv;
-    tile_rank = (j / nkv) * 8 + xcd;
-  }
-  if (tile_rank >= n_qtiles) return;
-  const int tile = n_qtiles - 1 - tile_rank;
   const int bq = 32 * qw;
   const int row0 = tile * bq;
   const int row_end = min(row0 + bq, M);
@@ -501,6 +482,116 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
   }
 }
 
+// Work queues of the persistent form: wq[k] (k < nkv) counts the query tiles
+// of KV head k handed out so far, heaviest first; wq[kWqDone] counts the
+// workgroups that have finished.  They are zero when a launch starts and the
+// last workgroup to finish zeroes them again.
+constexpr int kWqDone = 15;
+static_assert(kWqDone < kAttnQueueInts, "done counter inside the queue block");
+
+// Next item of a persistent workgroup (thread 0): a tile of its home KV head
+// while that queue lasts, then the lightest tiles left in the other queues
+// (home + 1, home + 2, ...); -1 when every queue is exhausted.
+__device__ __forceinline__ int attn_pop(int* wq, int home, int nkv, int n_qtiles) {
+  for (int k = 0; k < nkv; ++k) {
+    int qk = home + k;
+    if (qk >= nkv) qk -= nkv;
+    if (__hip_atomic_load(&wq[qk], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= n_qtiles) continue;
+    const int i = atomicAdd(&wq[qk], 1);
+    if (i < n_qtiles) return qk * n_qtiles + i;
+  }
+  return -1;
+}
+
+// Scheduling of the work items (tile, kvh) over the workgroups.
+//
+// Static form (wq == nullptr, and every split launch): workgroup b takes one
+// item.  Workgroups are dealt to the 8 XCDs round-robin (x = b % 8).  When nkv
+// divides 8, XCD x serves kv head x % nkv only, taking every (8/nkv)-th query
+// tile heaviest first, so the CUs of an XCD stream the same keys and share
+// them in its L2; otherwise XCD x takes tiles x, x+8, ... with all kv heads of
+// a tile in a row.
+//
+// Persistent form (wq != nullptr, nkv divides 8, chunks of at least 64
+// tokens, no key split; one workgroup per resident slot): each workgroup pops items from the queue of its XCD's KV head
+// (hardware XCC id % nkv), heaviest first, so the same L2 sharing holds; an
+// XCD whose queue runs dry takes the lightest tiles left in the others.  The
+// XCDs run at different clocks under the power limit, and with a fixed share
+// each the slowest one sets the end of the launch.
+template <int HD, int NW, bool DIRECT, bool SPLIT>
+__global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restrict__ Q,
+                                                       const int32_t* __restrict__ qpos, int M,
+                                                       const uint8_t* __restrict__ slab,
+                                                       const int32_t* __restrict__ table, int C,
+                                                       int cshift, int64_t slot_bytes, int nq, int nkv,
+                                                       int group, int qw, int n_qtiles,
+                                                       float scale_log2, _Float16* __restrict__ O, int tps,
+                                                       _Float16* __restrict__ Opart,
+                                                       float2* __restrict__ MLpart, int* __restrict__ wq) {
+  // only the direct-load, unsplit instances have the persistent form
+  constexpr bool kCanPersist = DIRECT && !SPLIT;
+  if constexpr (!kCanPersist) {
+    const int b = blockIdx.x;
+    const int xcd = b % 8, j = b / 8;
+    int kvh, tile_rank;
+    if (8 % nkv == 0) {
+      kvh = xcd % nkv;
+      tile_rank = j * (8 / nkv) + xcd / nkv;
+    } else {
+      kvh = j % nkv;
+      tile_rank = (j / nkv) * 8 + xcd;
+    }
+    if (tile_rank >= n_qtiles) return;
+    attn_tile<HD, NW, DIRECT, SPLIT>(Q, qpos, M, slab, table, C, cshift, slot_bytes, nq, nkv, group, qw,
+                                     scale_log2, O, tps, Opart, MLpart, n_qtiles - 1 - tile_rank, kvh);
+    return;
+  }
+  const bool persistent = wq != nullptr;
+  // the item is broadcast through the int past the K/V tiles (a static LDS
+  // variable would move the tiles off their aligned base)
+  extern __shared__ __attribute__((aligned(16))) _Float16 lds[];
+  int& s_item = *reinterpret_cast<int*>(lds + 2 * (k_tile_halves<HD>() + v_tile_halves<HD>()));
+  int home = 0;
+  if (persistent) {
+    unsigned xcc;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+    home = (int)(xcc & 7) % nkv;
+  }
+  for (int round = 0;; ++round) {
+    int kvh, tile_rank;
+    if (persistent) {
+      if (threadIdx.x == 0) s_item = attn_pop(wq, home, nkv, n_qtiles);
+      __syncthreads();
+      const int item = s_item;
+      __syncthreads();   // every thread has the item before thread 0 pops again
+      if (item < 0) break;
+      kvh = item / n_qtiles;
+      tile_rank = item - kvh * n_qtiles;
+    } else {
+      if (round > 0) break;
+      const int b = blockIdx.x;
+      const int xcd = b % 8, j = b / 8;
+      if (8 % nkv == 0) {
+        kvh = xcd % nkv;
+        tile_rank = j * (8 / nkv) + xcd / nkv;
+      } else {
+        kvh = j % nkv;
+        tile_rank = (j / nkv) * 8 + xcd;
+      }
+      if (tile_rank >= n_qtiles) break;
+    }
+    attn_tile<HD, NW, DIRECT, SPLIT>(Q, qpos, M, slab, table, C, cshift, slot_bytes, nq, nkv, group, qw,
+                                     scale_log2, O, tps, Opart, MLpart, n_qtiles - 1 - tile_rank, kvh);
+  }
+  if (persistent && threadIdx.x == 0) {
+    // no pop of this launch follows: the last workgroup zeroes the queues
+    if (atomicAdd(&wq[kWqDone], 1) == (int)gridDim.x - 1) {
+      for (int k = 0; k < nkv; ++k) atomicExch(&wq[k], 0);
+      atomicExch(&wq[kWqDone], 0);
+    }
+  }
+}
+
 // Merge of the key splits: one wave per (query row, head).  With m_s, l_s
 // and the normalised partial o_s of split s, and M = max m_s over the splits
 // that hold keys of the query: O = sum_s 2^(m_s - M) l_s o_s / sum_s
@@ -554,11 +645,29 @@ struct SplitArgs {
   float2* ml = nullptr;
 };
 
+// Workgroups of one kernel instance that the whole GPU holds at once.
+template <int HD, int NW, bool DIRECT, bool SPLIT>
+int resident_wgs(size_t lds_bytes) {
+  static const int n = [&] {
+    int dev = 0, cus = 0, per = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+      cus = 256;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &per, reinterpret_cast<const void*>(&attn_kernel<HD, NW, DIRECT, SPLIT>), 64 * NW, lds_bytes) !=
+            hipSuccess || per <= 0)
+      per = 1;
+    return cus * per;
+  }();
+  return n;
+}
+
 template <int HD, int NW, bool DIRECT, bool SPLIT>
 void launch_nwd(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S, const int32_t* table,
                int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group, int qw, float scale_log2,
-               _Float16* O, const SplitArgs& sa, hipStream_t s) {
-  const size_t lds_bytes = 2 * (k_tile_halves<HD>() + v_tile_halves<HD>()) * sizeof(_Float16);
+               _Float16* O, const SplitArgs& sa, int* wq, hipStream_t s) {
+  // the K/V tiles, double buffered, and the item of the persistent form
+  const size_t lds_bytes = 2 * (k_tile_halves<HD>() + v_tile_halves<HD>()) * sizeof(_Float16) + 16;
   static const bool attr = [&] {
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<HD, NW, DIRECT, SPLIT>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
@@ -567,41 +676,47 @@ void launch_nwd(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S,
   (void)attr;
   const int bq = 32 * qw;
   const int n_qtiles = (m + bq - 1) / bq;
-  // a multiple of 8, so a split's workgroups keep the XCD mapping of blockIdx.x
-  const int blocks = (8 % nkv == 0) ? 8 * ((n_qtiles + 8 / nkv - 1) / (8 / nkv))
-                                    : 8 * ((n_qtiles + 7) / 8) * nkv;
+  int blocks;
+  if (DIRECT && !SPLIT && wq && 8 % nkv == 0) {
+    // persistent: one workgroup per resident slot, at most one per item
+    blocks = (int)std::min<int64_t>((int64_t)n_qtiles * nkv, resident_wgs<HD, NW, DIRECT, SPLIT>(lds_bytes));
+  } else {
+    wq = nullptr;
+    // a multiple of 8, so a split's workgroups keep the XCD mapping of blockIdx.x
+    blocks = (8 % nkv == 0) ? 8 * ((n_qtiles + 8 / nkv - 1) / (8 / nkv)) : 8 * ((n_qtiles + 7) / 8) * nkv;
+  }
   hipLaunchKernelGGL((attn_kernel<HD, NW, DIRECT, SPLIT>), dim3(blocks, SPLIT ? sa.n_split : 1), dim3(64 * NW),
                      lds_bytes, s, Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, n_qtiles,
-                     scale_log2, O, sa.tps, sa.opart, sa.ml);
+                     scale_log2, O, sa.tps, sa.opart, sa.ml, wq);
 }
 
 template <int HD, int NW, bool SPLIT>
 void launch_nw(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S, const int32_t* table,
                int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group, int qw, float scale_log2,
-               _Float16* O, const SplitArgs& sa, hipStream_t s) {
+               _Float16* O, const SplitArgs& sa, int* wq, hipStream_t s) {
   if (C >= KT)
     launch_nwd<HD, NW, true, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2,
-                                    O, sa, s);
+                                    O, sa, wq, s);
   else
     launch_nwd<HD, NW, false, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2,
-                                     O, sa, s);
+                                     O, sa, wq, s);
 }
 
 template <int HD, bool SPLIT>
 void launch_hd(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S, const int32_t* table,
                int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group, int qw, float scale_log2,
-               _Float16* O, const SplitArgs& sa, hipStream_t s) {
+               _Float16* O, const SplitArgs& sa, int* wq, hipStream_t s) {
   switch (group * qw) {
-    case 5: launch_nw<HD, 5, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, sa, s); break;
-    case 6: launch_nw<HD, 6, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, sa, s); break;
-    case 7: launch_nw<HD, 7, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, sa, s); break;
-    default: launch_nw<HD, 8, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, sa, s); break;
+    case 5: launch_nw<HD, 5, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, sa, wq, s); break;
+    case 6: launch_nw<HD, 6, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, sa, wq, s); break;
+    case 7: launch_nw<HD, 7, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, sa, wq, s); break;
+    default: launch_nw<HD, 8, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, sa, wq, s); break;
   }
 }
 
 void launch_any(const void* q, const int32_t* qpos, int m, const void* slab, const int32_t* table,
                 int chunk_tokens, int64_t slot_bytes, int n_q, int n_kv, int head_dim, void* out,
-                const SplitArgs& sa, bool split, hipStream_t s) {
+                const SplitArgs& sa, bool split, int* wq, hipStream_t s) {
   const int group = n_q / n_kv;          // 1..8
   // 32-query row groups per workgroup: 5..8 waves, so one staged K/V tile
   // serves as many queries as the registers allow
@@ -613,11 +728,11 @@ void launch_any(const void* q, const int32_t* qpos, int m, const void* slab, con
   int cshift = 0;
   while ((1 << cshift) < chunk_tokens) ++cshift;   // chunk_tokens is a power of two
   if (head_dim == 128) {
-    if (split) launch_hd<128, true>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, scale_log2, O, sa, s);
-    else launch_hd<128, false>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, scale_log2, O, sa, s);
+    if (split) launch_hd<128, true>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, scale_log2, O, sa, nullptr, s);
+    else launch_hd<128, false>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, scale_log2, O, sa, wq, s);
   } else {
-    if (split) launch_hd<64, true>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, scale_log2, O, sa, s);
-    else launch_hd<64, false>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, scale_log2, O, sa, s);
+    if (split) launch_hd<64, true>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, scale_log2, O, sa, nullptr, s);
+    else launch_hd<64, false>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, scale_log2, O, sa, wq, s);
   }
 }
 
@@ -625,8 +740,9 @@ void launch_any(const void* q, const int32_t* qpos, int m, const void* slab, con
 
 void launch_attention(const void* q, const int32_t* qpos, int m, const void* slab,
                       const int32_t* table, int chunk_tokens, int64_t slot_bytes, int n_q,
-                      int n_kv, int head_dim, void* out, hipStream_t s) {
-  launch_any(q, qpos, m, slab, table, chunk_tokens, slot_bytes, n_q, n_kv, head_dim, out, SplitArgs(), false, s);
+                      int n_kv, int head_dim, void* out, hipStream_t s, int* work_queues) {
+  launch_any(q, qpos, m, slab, table, chunk_tokens, slot_bytes, n_q, n_kv, head_dim, out, SplitArgs(), false,
+             work_queues, s);
 }
 
 int64_t attention_split_ws_bytes(int m, int n_q, int head_dim, int n_split) {
@@ -666,7 +782,7 @@ void launch_attention_split(const void* q, const int32_t* qpos, int m, int max_p
   sa.opart = reinterpret_cast<_Float16*>(ws);
   const int64_t o = (int64_t)sa.n_split * m * n_q * head_dim * 2;
   sa.ml = reinterpret_cast<float2*>(reinterpret_cast<uint8_t*>(ws) + ((o + 255) / 256) * 256);
-  launch_any(q, qpos, m, slab, table, chunk_tokens, slot_bytes, n_q, n_kv, head_dim, out, sa, true, s);
+  launch_any(q, qpos, m, slab, table, chunk_tokens, slot_bytes, n_q, n_kv, head_dim, out, sa, true, nullptr, s);
   const int waves = m * n_q;
   const dim3 grid((unsigned)((waves + 3) / 4));
   _Float16* O = reinterpret_cast<_Float16*>(out);

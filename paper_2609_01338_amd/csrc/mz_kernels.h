@@ -67,10 +67,15 @@ void launch_gemm_q4_splitk_rope(const void* x, int m, int n, int k, const void* 
 // Splits that fill the chip for this shape within ws_cap bytes (1: no split).
 int gemm_auto_splits(int m, int n, int k, int64_t ws_cap);
 
-// Causal GQA attention over chunked KV (see mz.h, mz_attention).
+// Causal GQA attention over chunked KV (see mz.h, mz_attention).  With
+// work_queues (device, kAttnQueueInts int32, zero on entry and left zero on
+// return; not shared by launches in flight together) and n_kv dividing 8,
+// persistent workgroups take the query tiles from per-KV-head queues, so
+// XCDs that run faster take more of them; otherwise one workgroup per tile.
+constexpr int kAttnQueueInts = 16;
 void launch_attention(const void* q, const int32_t* qpos, int m, const void* slab,
                       const int32_t* table, int chunk_tokens, int64_t slot_bytes, int n_q,
-                      int n_kv, int head_dim, void* out, hipStream_t s);
+                      int n_kv, int head_dim, void* out, hipStream_t s, int* work_queues = nullptr);
 
 // Split-key attention for few query rows: n_split key ranges of whole 64-key
 // tiles (tiles per split = ceil((max_pos / 64 + 1) / n_split)) run as separate

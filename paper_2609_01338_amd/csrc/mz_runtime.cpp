@@ -496,6 +496,10 @@ struct mz_ctx {
   uint8_t* split_ws = nullptr;
   int64_t split_ws_bytes = 0;
   bool attn_split = true;            // option attn_split
+  // work queues of the persistent attention (zero between launches; the
+  // launches run in order on the compute stream)
+  int32_t* attn_wq = nullptr;
+  bool attn_queue = true;            // option attn_queue
   bool gemm_split = true;            // option gemm_split
   bool fuse_rope = true;             // option fuse_rope: RoPE (and the KV slot writes) in the GEMM epilogue
   bool fuse_norm = true;             // option fuse_norm: a single row's RMSNorm inside its split-K GEMVs
@@ -1049,7 +1053,7 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
                                     x->slot_bytes, x->nq, x->nkv, x->hd, n_split, x->split_ws, x->xb, cs);
       else
         mzk::launch_attention(x->q16, posq, nq, x->kv_slab, x->d_tables + (size_t)l * MC, C, x->slot_bytes,
-                              x->nq, x->nkv, x->hd, x->xb, cs);
+                              x->nq, x->nkv, x->hd, x->xb, cs, x->attn_queue ? x->attn_wq : nullptr);
     });
     x->timed(kKGemmO, 2.0 * nq * x->dq * d, (double)d * x->dq * bpe_w + nq * (x->dq * 2.0 + d * 8.0), cs,
              [&] { x->gemm(x->xb, nq, x->d_pad, x->dq, unit + x->off_o, mzk::kEpiAdd, h, cs); });
@@ -1255,6 +1259,8 @@ mz_status mz_load_model(const mz_model_cfg* cfg, const void* blob, size_t nbytes
         int64_t(64) << 20, std::max(mzk::attention_split_ws_bytes(std::min<int64_t>(M, 4096), c.nq, c.hd, 64),
                                     mzk::gemm_splitk_ws_bytes(std::min<int64_t>(M, 512), 2 * c.ffp, 8)));
     c.split_ws = (uint8_t*)dmalloc((size_t)c.split_ws_bytes);
+    c.attn_wq = (int32_t*)dmalloc(mzk::kAttnQueueInts * sizeof(int32_t));
+    HIPCHK(hipMemset(c.attn_wq, 0, mzk::kAttnQueueInts * sizeof(int32_t)));
     HIPCHK(hipEventCreateWithFlags(&c.ev_meta, hipEventDisableTiming));
     void* stage = nullptr;
     if (hipHostMalloc(&stage, c.stage_bytes, hipHostMallocDefault) != hipSuccess || !stage)
@@ -1279,7 +1285,7 @@ void mz_free(mz_ctx* x) {
   (void)hipSetDevice(x->device);
   if (x->s_compute) (void)hipStreamSynchronize(x->s_compute);
   if (x->s_swap) (void)hipStreamSynchronize(x->s_swap);
-  void* dptrs[] = {x->codec_stage, x->d_codec_slots, x->split_ws, x->w_slab, x->emb_nib, x->emb_sc, x->lm_nib, x->lm_sc,
+  void* dptrs[] = {x->codec_stage, x->d_codec_slots, x->split_ws, x->attn_wq, x->w_slab, x->emb_nib, x->emb_sc, x->lm_nib, x->lm_sc,
                    x->rope_cs, x->kv_slab,
                    x->h[0], x->h[1], x->xb, x->qf, x->kvf, x->q16, x->act, x->logits, x->part_val,
                    x->part_idx, x->d_token, x->d_tables, x->d_pos, x->d_kvoff, x->d_dix, x->d_posq,
@@ -1311,6 +1317,7 @@ mz_status mz_set_option(mz_ctx* x, const char* key, int64_t value) {
     else if (k == "debug_poison") x->debug_poison = value != 0;
     else if (k == "swap_trim") x->swap_trim = value != 0;
     else if (k == "attn_split") x->attn_split = value != 0;
+    else if (k == "attn_queue") x->attn_queue = value != 0;
     else if (k == "gemm_split") x->gemm_split = value != 0;
     else if (k == "fuse_norm") x->fuse_norm = value != 0;
     else if (k == "fuse_rope") x->fuse_rope = value != 0;
@@ -1749,9 +1756,9 @@ mz_status mz_q4_gemm_split(const void* x_f16, int32_t m, int32_t n_pad, int32_t 
   });
 }
 
-mz_status mz_attention(const void* q, const int32_t* qpos, int32_t m, const void* slab, const int32_t* table,
-                       int32_t n_table, int32_t chunk_tokens, int32_t n_q, int32_t n_kv, int32_t head_dim,
-                       void* out, void* stream) {
+static mz_status attention_entry(const void* q, const int32_t* qpos, int32_t m, const void* slab,
+                                 const int32_t* table, int32_t n_table, int32_t chunk_tokens, int32_t n_q,
+                                 int32_t n_kv, int32_t head_dim, void* out, int32_t* queues, void* stream) {
   return guarded(nullptr, [&] {
     if (!q || !qpos || !slab || !table || !out) fail(MZ_EINVAL, "NULL pointer");
     if (m < 1 || n_table < 1) fail(MZ_EINVAL, "sizes must be positive");
@@ -1760,9 +1767,24 @@ mz_status mz_attention(const void* q, const int32_t* qpos, int32_t m, const void
     if (n_kv < 1 || n_q % n_kv || n_q / n_kv > 8) fail(MZ_EINVAL, "bad head counts");
     const int64_t slot_bytes = (int64_t)chunk_tokens * n_kv * head_dim * 2 * 2;
     mzk::launch_attention(q, qpos, m, slab, table, chunk_tokens, slot_bytes, n_q, n_kv, head_dim, out,
-                          (hipStream_t)stream);
+                          (hipStream_t)stream, queues);
     HIPCHK(hipGetLastError());
   });
+}
+
+mz_status mz_attention(const void* q, const int32_t* qpos, int32_t m, const void* slab, const int32_t* table,
+                       int32_t n_table, int32_t chunk_tokens, int32_t n_q, int32_t n_kv, int32_t head_dim,
+                       void* out, void* stream) {
+  return attention_entry(q, qpos, m, slab, table, n_table, chunk_tokens, n_q, n_kv, head_dim, out, nullptr,
+                         stream);
+}
+
+mz_status mz_attention_queued(const void* q, const int32_t* qpos, int32_t m, const void* slab,
+                              const int32_t* table, int32_t n_table, int32_t chunk_tokens, int32_t n_q,
+                              int32_t n_kv, int32_t head_dim, void* out, int32_t* work_queues, void* stream) {
+  if (!work_queues) return guarded(nullptr, [&] { fail(MZ_EINVAL, "work_queues is NULL"); });
+  return attention_entry(q, qpos, m, slab, table, n_table, chunk_tokens, n_q, n_kv, head_dim, out, work_queues,
+                         stream);
 }
 
 int64_t mz_attention_split_workspace_bytes(int32_t m, int32_t n_q, int32_t head_dim, int32_t n_split) {

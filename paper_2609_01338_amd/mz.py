@@ -104,6 +104,7 @@ def lib() -> ctypes.CDLL:
         "mz_q4_gemm_pack": ([vp, vp, i32, i32, vp], i32),
         "mz_q4_gemm": ([vp, i32, i32, i32, vp, i32, vp, vp], i32),
         "mz_attention": ([vp, vp, i32, vp, vp, i32, i32, i32, i32, i32, vp, vp], i32),
+        "mz_attention_queued": ([vp, vp, i32, vp, vp, i32, i32, i32, i32, i32, vp, vp, vp], i32),
         "mz_rmsnorm": ([vp, i32, i32, ctypes.c_float, vp, vp], i32),
         "mz_probe_ceilings": ([i32, ctypes.c_char_p, sz], i32),
         "mz_plan_evict": ([ctypes.POINTER(mz_model_cfg), ctypes.POINTER(mz_evict_request), vp, vp, vp], i32),
@@ -335,6 +336,13 @@ def mz_attention(q_ptr: int, qpos_ptr: int, m: int, slab_ptr: int, table_ptr: in
                  stream: Optional[int] = None) -> None:
     _check(lib().mz_attention(q_ptr, qpos_ptr, m, slab_ptr, table_ptr, n_table, chunk_tokens, n_q,
                               n_kv, head_dim, out_ptr, stream), None)
+
+
+def mz_attention_queued(q_ptr: int, qpos_ptr: int, m: int, slab_ptr: int, table_ptr: int, n_table: int,
+                        chunk_tokens: int, n_q: int, n_kv: int, head_dim: int, out_ptr: int, queues_ptr: int,
+                        stream: Optional[int] = None) -> None:
+    _check(lib().mz_attention_queued(q_ptr, qpos_ptr, m, slab_ptr, table_ptr, n_table, chunk_tokens, n_q,
+                                     n_kv, head_dim, out_ptr, queues_ptr, stream), None)
 
 
 def mz_q4_gemm_split(x_ptr: int, m: int, n_pad: int, k: int, w_ptr: int, epilogue: int, y_ptr: int,

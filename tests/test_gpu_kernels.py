@@ -147,8 +147,10 @@ def test_gemm_full_layer_shapes(key):
 
 
 def _attn_case(nq, nkv, hd, C, S, qpos, seed, sample=None, n_split=None):
-    """n_split: None for mz_attention, else mz_attention_split with that many
-    key splits ("auto": the restore's choice)."""
+    """n_split: None for mz_attention, "queued" for mz_attention_queued (run
+    twice on the same queues, which must come back zero, and equal to
+    mz_attention bit for bit), else mz_attention_split with that many key
+    splits ("auto": the restore's choice)."""
     torch = torch_cuda()
     report("attention", nq=nq, nkv=nkv, hd=hd, C=C, S=S, m=len(qpos), seed=seed, n_split=n_split)
     rng = np.random.default_rng(seed)
@@ -178,6 +180,18 @@ def _attn_case(nq, nkv, hd, C, S, qpos, seed, sample=None, n_split=None):
     if n_split is None:
         mz.mz_attention(d_q.data_ptr(), d_pos.data_ptr(), M, d_slab.data_ptr(), d_tab.data_ptr(), nch, C,
                         nq, nkv, hd, out.data_ptr(), stream())
+    elif n_split == "queued":
+        queues = torch.zeros(16, device="cuda", dtype=torch.int32)
+        plain = torch.empty_like(out)
+        mz.mz_attention(d_q.data_ptr(), d_pos.data_ptr(), M, d_slab.data_ptr(), d_tab.data_ptr(), nch, C,
+                        nq, nkv, hd, plain.data_ptr(), stream())
+        for rep in range(2):
+            out.fill_(float("nan"))
+            mz.mz_attention_queued(d_q.data_ptr(), d_pos.data_ptr(), M, d_slab.data_ptr(), d_tab.data_ptr(), nch,
+                                   C, nq, nkv, hd, out.data_ptr(), queues.data_ptr(), stream())
+            torch.cuda.synchronize()
+            assert int(queues.abs().sum()) == 0, "work queues not left at zero"
+            assert torch.equal(out.view(torch.int16), plain.view(torch.int16)), "queued != mz_attention"
     else:
         if n_split == "auto":
             n_split = mz.mz_attention_auto_splits(M, max_pos, nq, nkv, hd, 64 << 20)
@@ -221,14 +235,30 @@ def test_attention_small(nq, nkv, hd, C, S):
 
 @pytest.mark.parametrize("key", ["1b", "3b", "1p5b", "8b"])
 def test_attention_full_context(key):
-    """All S query rows of the workload (the benchmark's launch), sampled check."""
+    """All S query rows of the workload, sampled check, through the work
+    queues (the restore's launch) and bit-equal to the one-tile-per-workgroup
+    form."""
     w = W.WORKLOADS[key]
     m = w.model
     S = w.n_ctx + w.n_prompt
     rng = np.random.default_rng(7)
     sample = np.unique(np.concatenate([rng.choice(S, 12, replace=False), [0, S - 1]]))
     _attn_case(m.n_q_heads, m.n_kv_heads, m.head_dim, m.chunk_tokens, S, np.arange(S), seed=5,
-               sample=sample)
+               sample=sample, n_split="queued")
+
+
+@pytest.mark.parametrize("nq,nkv,hd,C,S", [
+    (32, 8, 128, 256, 3000), (24, 8, 128, 256, 1700), (12, 2, 128, 256, 1030), (16, 4, 64, 64, 900),
+    (8, 8, 128, 64, 200), (6, 1, 64, 128, 700), (12, 3, 64, 256, 600), (4, 4, 128, 8, 77)])
+def test_attention_queued(nq, nkv, hd, C, S):
+    """The work-queue form: 1, 2, 4 and 8 KV heads (queues shared by 8, 4, 2
+    and 1 XCDs), more tiles than workgroups and fewer, gappy query rows; 3
+    KV heads and 8-token chunks take the one-tile-per-workgroup form."""
+    rng = np.random.default_rng(S + 1)
+    gappy = np.sort(rng.choice(S, max(1, S // 3), replace=False))
+    _attn_case(nq, nkv, hd, C, S, np.arange(S), seed=11, n_split="queued")
+    _attn_case(nq, nkv, hd, C, S, gappy, seed=12, n_split="queued")
+    _attn_case(nq, nkv, hd, C, S, [S - 1], seed=13, n_split="queued")
 
 
 @pytest.mark.parametrize("nq,nkv,hd,C,S", [
@@ -266,6 +296,8 @@ def test_attention_split_validation():
         mz.mz_attention_split(1, 1, 4, 10, 1, 1, 1, 16, 8, 2, 64, 2, 1, 10, 1)    # workspace too small
     with pytest.raises(mz.MzError):
         mz.mz_attention_split(1, 1, 4, 10, 1, 1, 1, 16, 8, 2, 64, 65, 1, 1 << 30, 1)   # more than 64 splits
+    with pytest.raises(mz.MzError):
+        mz.mz_attention_queued(1, 1, 4, 1, 1, 1, 16, 8, 2, 64, 1, 0, 1)   # no work queues
     assert mz.mz_attention_auto_splits(40000, 40000, 32, 8, 128, 64 << 20) == 1   # the chip is full already
     assert 32 <= mz.mz_attention_auto_splits(1, 32895, 32, 8, 128, 64 << 20) <= 64
     assert mz.mz_attention_auto_splits(129, 32895, 32, 8, 128, 64 << 20) > 8
