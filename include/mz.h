@@ -152,7 +152,9 @@ mz_status mz_generate(mz_ctx *ctx, int32_t token, int32_t n, int32_t *tokens_out
  * context runs split over the keys, as mz_attention_split, default; 0: always
  * one pass), "attn_queue" (1: the attention of many rows runs as
  * mz_attention_queued with queues owned by the context, default; 0: as
- * mz_attention), "gemm_split" (1: GEMMs of few rows run split over K, as
+ * mz_attention), "gemm_queue" (1: the unsplit projections with a store,
+ * residual-add or SwiGLU epilogue run as mz_q4_gemm_queued, default; 0: one
+ * workgroup per tile), "gemm_split" (1: GEMMs of few rows run split over K, as
  * mz_q4_gemm_split, default; 0: never), "fuse_rope" (1: the query and
  * key/value projections apply the rotary embedding in their epilogue, or in
  * the reduce of their K splits, and write f16 queries and the chunk slots
@@ -334,6 +336,20 @@ mz_status mz_q4_gemm_pack(const void *w, const void *w_up, int32_t n, int32_t k,
  * 2: y f16 [m][n_pad/2] = silu(gate) * up (W packed with w_up). */
 mz_status mz_q4_gemm(const void *x_f16, int32_t m, int32_t n_pad, int32_t k,
                      const void *w_packed, int32_t epilogue, void *y, void *stream);
+
+/* mz_q4_gemm with persistent workgroups (same arguments, same result bits).
+ * The output tiles are cut into 8 contiguous ranges, one per XCD; each
+ * workgroup takes tiles of its XCD's range from a counter, then those left
+ * in the other ranges, so XCDs that run at a higher clock take more of them.
+ * Launches of fewer than 16 rounds of resident workgroups (4096 256-row
+ * tiles on 256 compute units) run one workgroup per tile, as mz_q4_gemm.
+ * work_queues: device, caller-owned, 16 int32 that are zero before the first
+ * call; each call leaves them zero.  Calls that share them must not be in
+ * flight at the same time.  EINVAL as mz_q4_gemm, and for a NULL
+ * work_queues. */
+mz_status mz_q4_gemm_queued(const void *x_f16, int32_t m, int32_t n_pad, int32_t k,
+                            const void *w_packed, int32_t epilogue, void *y, int32_t *work_queues,
+                            void *stream);
 
 /* Split-K form of mz_q4_gemm for few rows (the short requests of the
  * paper's evaluation, Sec. 6, and every decode step): a grid of 256-column

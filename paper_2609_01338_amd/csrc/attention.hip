@@ -562,7 +562,7 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
     if (persistent) {
       if (threadIdx.x == 0) s_item = attn_pop(wq, home, nkv, n_qtiles);
       __syncthreads();
-      const int item = s_item;
+      const int item = __builtin_amdgcn_readfirstlane(s_item);   // uniform: item addressing stays scalar
       __syncthreads();   // every thread has the item before thread 0 pops again
       if (item < 0) break;
       kvh = item / n_qtiles;

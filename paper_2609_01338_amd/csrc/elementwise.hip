@@ -2,6 +2,7 @@
 // rotary embedding with KV scatter into chunk slots, embedding gather with
 // Q4_0 dequantization, row compaction, and the output head with argmax.
 #include "mz_kernels.h"
+#include "rope.h"
 #include "rownorm.h"
 
 namespace mzk {
@@ -24,12 +25,13 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ 
 #pragma unroll
   for (int k = 0; k < kRowNormRegs; ++k) {
     const int i = threadIdx.x + k * 256;
-    if (i < n4) xr[i] = f16x4{(_Float16)(v[k].x * r), (_Float16)(v[k].y * r), (_Float16)(v[k].z * r), (_Float16)(v[k].w * r)};
+    if (i < n4)
+      xr[i] = f16x4{norm_to_f16(v[k].x, r), norm_to_f16(v[k].y, r), norm_to_f16(v[k].z, r), norm_to_f16(v[k].w, r)};
   }
   const float4* hr = reinterpret_cast<const float4*>(hrow);
   for (int i = threadIdx.x + kRowNormRegs * 256; i < n4; i += 256) {
     const float4 u = hr[i];
-    xr[i] = f16x4{(_Float16)(u.x * r), (_Float16)(u.y * r), (_Float16)(u.z * r), (_Float16)(u.w * r)};
+    xr[i] = f16x4{norm_to_f16(u.x, r), norm_to_f16(u.y, r), norm_to_f16(u.z, r), norm_to_f16(u.w, r)};
   }
 }
 
@@ -86,10 +88,10 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(const float* __restrict__ 
     const float4 x2 = *reinterpret_cast<const float4*>(x + i + halfd);
     const float4* c = reinterpret_cast<const float4*>(cs + (size_t)s_pos[rr] * halfd + i);
     const float4 c01 = c[0], c23 = c[1];   // (cos, sin) of pairs i, i+1 and i+2, i+3
-    const f16x4 y1 = {(_Float16)(x1.x * c01.x - x2.x * c01.y), (_Float16)(x1.y * c01.z - x2.y * c01.w),
-                      (_Float16)(x1.z * c23.x - x2.z * c23.y), (_Float16)(x1.w * c23.z - x2.w * c23.w)};
-    const f16x4 y2 = {(_Float16)(x2.x * c01.x + x1.x * c01.y), (_Float16)(x2.y * c01.z + x1.y * c01.w),
-                      (_Float16)(x2.z * c23.x + x1.z * c23.y), (_Float16)(x2.w * c23.z + x1.w * c23.w)};
+    const float2 r0 = rope_rotate(x1.x, x2.x, c01.x, c01.y), r1 = rope_rotate(x1.y, x2.y, c01.z, c01.w);
+    const float2 r2 = rope_rotate(x1.z, x2.z, c23.x, c23.y), r3 = rope_rotate(x1.w, x2.w, c23.z, c23.w);
+    const f16x4 y1 = {(_Float16)r0.x, (_Float16)r1.x, (_Float16)r2.x, (_Float16)r3.x};
+    const f16x4 y2 = {(_Float16)r0.y, (_Float16)r1.y, (_Float16)r2.y, (_Float16)r3.y};
     _Float16* dst;
     if (head < nq) {
       dst = q_out + (size_t)(row0 + rr) * dq + head * hd;

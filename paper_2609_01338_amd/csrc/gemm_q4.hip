@@ -28,9 +28,9 @@
 // 8 LDS cycles per store instruction, against 16 for 8 lanes on 8
 // consecutive rows).
 //
-// Workgroups are numbered so that each XCD (workgroups are dealt to the 8 XCDs
-// round-robin) walks a contiguous run of tiles, M-major: neighbouring tiles on
-// one XCD share the activation rows in that XCD's L2.
+// Each XCD walks a contiguous run of tiles, M-major: neighbouring tiles on one
+// XCD share the activation rows in that XCD's L2 (see gemm_q4_kernel for the
+// static and the persistent, work-queue form).
 //
 // MFMA 16x16x32 operand layout (checked on gfx950): lane l feeds row/column
 // l % 16 with the 8 consecutive k of group l / 16; the accumulator holds rows
@@ -39,6 +39,7 @@
 #include <type_traits>
 
 #include "mz_kernels.h"
+#include "rope.h"
 #include "rownorm.h"
 
 namespace mzk {
@@ -162,8 +163,9 @@ __device__ __forceinline__ void rope_epilogue(const f32x4 (&acc)[BM / 64][8], co
           if (col < rot_end) {
             const float x1 = acc[i][j][r], x2 = acc[i][j + JO][r];
             const float2 c = cv[ii][r][q];
-            yr[col] = (_Float16)(x1 * c.x - x2 * c.y);
-            yr[col + HALF] = (_Float16)(x2 * c.x + x1 * c.y);
+            const float2 y = rope_rotate(x1, x2, c.x, c.y);
+            yr[col] = (_Float16)y.x;
+            yr[col + HALF] = (_Float16)y.y;
           }
         }
         if constexpr (EPI == kEpiRopeKV) {
@@ -190,10 +192,9 @@ __device__ __forceinline__ void rope_epilogue(const f32x4 (&acc)[BM / 64][8], co
 // Y as [split][M][N]; gemm_splitk_reduce adds the splits in order and applies
 // the real epilogue.
 template <int EPI, int BM>
-__global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict__ X,
-                                                     const int32_t* __restrict__ a_rows, int M, int K,
-                                                     const uint8_t* __restrict__ Wp, int N,
-                                                     void* __restrict__ Y, int k_steps, GemmRope ea) {
+__device__ __forceinline__ void gemm_tile(const _Float16* __restrict__ X, const int32_t* __restrict__ a_rows,
+                                          int M, int K, const uint8_t* __restrict__ Wp, int N,
+                                          void* __restrict__ Y, int k_steps, const GemmRope& ea, int mt, int nt) {
   extern __shared__ __attribute__((aligned(16))) _Float16 lds[];
   constexpr int A_TILE = BM * ROW;                     // one activation stage
   constexpr int MI = BM / 64;                          // 16-row MFMA tiles per wave
@@ -205,13 +206,6 @@ __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict_
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int wm = wave & 3, wn = wave >> 2;
-  const int n_tiles = N / BN;
-  // XCD-contiguous tile order
-  const int total = gridDim.x;
-  const int b = blockIdx.x;
-  const int per = total / 8;
-  const int t = b < per * 8 ? (b % 8) * per + b / 8 : b;
-  const int mt = t / n_tiles, nt = t % n_tiles;
   const int split = EPI == kEpiPartial ? (int)blockIdx.y : 0;
   const int ks0 = EPI == kEpiPartial ? split * k_steps : 0;
   const int nk = EPI == kEpiPartial ? min(k_steps, K / BK - ks0) : K / BK;
@@ -375,6 +369,88 @@ __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict_
   }
 }
 
+// Work queues of the persistent form: wq[x] counts the takers of range x so
+// far, wq[kGemmWqDone] the workgroups that have finished; zero when a launch
+// starts, zeroed again by the last workgroup to finish.
+constexpr int kGemmWqDone = 15;
+static_assert(kGemmWqDone < kGemmQueueInts, "done counter inside the queue block");
+
+// Tile range x of the 8 XCD ranges of `total` tiles.
+__device__ __forceinline__ int xcd_range_lo(int x, int total) { return (int)((int64_t)x * total / 8); }
+
+// Next tile of a persistent workgroup (thread 0): from its XCD's own range
+// while that lasts, then from the ranges of the others (home + 1, ...); -1
+// when all are taken.  A counter may run past its range's length (a taker
+// that found it empty); only values below the length hand out tiles.
+__device__ __forceinline__ int gemm_pop(int* wq, int home, int total) {
+  for (int k = 0; k < 8; ++k) {
+    const int x = (home + k) & 7;
+    const int lo = xcd_range_lo(x, total), len = xcd_range_lo(x + 1, total) - lo;
+    const int i = atomicAdd(&wq[x], 1);
+    if (i < len) return lo + i;
+  }
+  return -1;
+}
+
+// Scheduling of the output tiles over the workgroups.  Tile t is row tile
+// t / (N / 256), column tile t % (N / 256) (M-major), and the tiles are cut
+// into 8 contiguous ranges, one per XCD, so that the tiles an XCD runs at one
+// time share activation rows in its L2.
+//
+// Static form (wq == nullptr, and every split-K launch): workgroup b takes one
+// tile; workgroups are dealt to the XCDs round-robin, so XCD b % 8 walks its
+// range in order.  Persistent form (wq != nullptr; one workgroup per resident
+// slot): each workgroup takes the tiles of its XCD's range (hardware XCC id)
+// from a counter, then those left in the other ranges.  Under the power limit
+// the XCDs run at clocks several percent apart; with a fixed share each, the
+// slowest one sets the end of the launch.  (Store, add and SwiGLU epilogues;
+// the others always run static.)
+template <int EPI, int BM>
+__global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict__ X,
+                                                     const int32_t* __restrict__ a_rows, int M, int K,
+                                                     const uint8_t* __restrict__ Wp, int N,
+                                                     void* __restrict__ Y, int k_steps, GemmRope ea,
+                                                     int* __restrict__ wq) {
+  const int n_tiles = N / BN;
+  const int total = n_tiles * ((M + BM - 1) / BM);
+  // the persistent form for the store, add and SwiGLU epilogues only: with
+  // the RoPE epilogues the extra loop state spills inside the K loop
+  constexpr bool kCanPersist = EPI == kEpiStore || EPI == kEpiAdd || EPI == kEpiSwiGLU;
+  const bool persistent = kCanPersist && wq != nullptr;
+  // the tile number of the persistent form passes through the first word of
+  // activation stage 0, which no wave reads between tiles
+  extern __shared__ __attribute__((aligned(16))) _Float16 lds[];
+  int& s_item = *reinterpret_cast<int*>(lds);
+  int home = 0;
+  if (persistent) {
+    unsigned xcc;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+    home = (int)(xcc & 7);
+  }
+  for (int round = 0;; ++round) {
+    int t;
+    if (persistent) {
+      __syncthreads();   // the previous tile is done with the LDS
+      if (threadIdx.x == 0) s_item = gemm_pop(wq, home, total);
+      __syncthreads();
+      t = __builtin_amdgcn_readfirstlane(s_item);
+      __syncthreads();   // read by every thread before the next loads land there
+      if (t < 0) break;
+    } else {
+      if (round > 0) break;
+      const int b = blockIdx.x;
+      const int per = (int)gridDim.x / 8;
+      t = b < per * 8 ? (b % 8) * per + b / 8 : b;
+    }
+    gemm_tile<EPI, BM>(X, a_rows, M, K, Wp, N, Y, k_steps, ea, t / n_tiles, t % n_tiles);
+  }
+  if (!persistent) return;
+  if (threadIdx.x == 0 && atomicAdd(&wq[kGemmWqDone], 1) == (int)gridDim.x - 1) {
+    for (int x = 0; x < 8; ++x) atomicExch(&wq[x], 0);
+    atomicExch(&wq[kGemmWqDone], 0);
+  }
+}
+
 // One activation row (m = 1: a decode step, the last layer's single row): the
 // product of gemm_q4_kernel<kEpiPartial> without matrix cores.  Thread r of
 // a 256-thread workgroup owns output column (tile row) r of n tile
@@ -432,7 +508,7 @@ __global__ __launch_bounds__(256) void gemv_q4_kernel(const _Float16* __restrict
     if (r < (kt_n - t0) * 32) {
       if constexpr (NORM) {
         const float2 hv = *reinterpret_cast<const float2*>(hrow + (size_t)t0 * BK + 2 * r);
-        xs[r] = f16x2{(_Float16)(hv.x * rn), (_Float16)(hv.y * rn)};
+        xs[r] = f16x2{norm_to_f16(hv.x, rn), norm_to_f16(hv.y, rn)};
       } else {
         xs[r] = *reinterpret_cast<const f16x2*>(xrow + (size_t)t0 * BK + 2 * r);
       }
@@ -534,8 +610,9 @@ __global__ __launch_bounds__(256) void gemm_splitk_reduce_rope(const float* __re
     const float2 cv = ea.rope_cs[(size_t)p * half + i];
     _Float16* yr = EPI == kEpiRopeQ ? reinterpret_cast<_Float16*>(Y) + (size_t)row * ea.n_valid
                                     : reinterpret_cast<_Float16*>(ea.slab + off);
-    yr[c] = (_Float16)(x1 * cv.x - x2 * cv.y);
-    yr[c + half] = (_Float16)(x2 * cv.x + x1 * cv.y);
+    const float2 y = rope_rotate(x1, x2, cv.x, cv.y);
+    yr[c] = (_Float16)y.x;
+    yr[c + half] = (_Float16)y.y;
   } else {
     const int v = j - pairs;
     float a = pr[rot + v];
@@ -551,9 +628,14 @@ constexpr size_t lds_bytes() {
   return ((size_t)A_STAGES * BM * ROW + (size_t)B_STAGES * B_TILE) * sizeof(_Float16);
 }
 
+// Rounds of resident workgroups from which a launch takes its tiles from the
+// work queues (measured on the 8B projections: +3.6 % at 56 rounds, none at 8).
+constexpr int kQueueMinRounds = 16;
+
 template <int EPI, int BM>
 void launch_bm(const _Float16* X, const int32_t* a_rows, int m, int n, int k, const uint8_t* W, void* y,
-               hipStream_t s, int n_split = 1, int k_steps = 0, const GemmRope& ea = GemmRope{}) {
+               hipStream_t s, int n_split = 1, int k_steps = 0, const GemmRope& ea = GemmRope{},
+               int* wq = nullptr) {
   static const bool lds_ok = [] {   // more than 64 KB of dynamic LDS, once per instantiation
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_q4_kernel<EPI, BM>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes<BM>());
@@ -561,8 +643,30 @@ void launch_bm(const _Float16* X, const int32_t* a_rows, int m, int n, int k, co
   }();
   (void)lds_ok;
   const int tiles = (n / BN) * ((m + BM - 1) / BM);
-  hipLaunchKernelGGL((gemm_q4_kernel<EPI, BM>), dim3(tiles, n_split), dim3(NT), lds_bytes<BM>(), s, X, a_rows,
-                     m, k, W, n, y, k_steps, ea);
+  int blocks = tiles;
+  if (!(EPI == kEpiStore || EPI == kEpiAdd || EPI == kEpiSwiGLU) || n_split != 1) wq = nullptr;
+  if (wq) {
+    // persistent: one workgroup per resident slot, at most one per tile
+    static const int resident = [] {
+      int dev = 0, cus = 0, per = 0;
+      if (hipGetDevice(&dev) != hipSuccess ||
+          hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+        cus = 256;
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+              &per, reinterpret_cast<const void*>(&gemm_q4_kernel<EPI, BM>), NT, lds_bytes<BM>()) != hipSuccess ||
+          per <= 0)
+        per = 1;
+      return cus * per;
+    }();
+    // a launch of few rounds leaves the slowest XCD less than a tile behind,
+    // which moving whole tiles cannot even out: one workgroup per tile there
+    if (tiles < kQueueMinRounds * resident)
+      wq = nullptr;
+    else
+      blocks = resident;
+  }
+  hipLaunchKernelGGL((gemm_q4_kernel<EPI, BM>), dim3(blocks, n_split), dim3(NT), lds_bytes<BM>(), s, X, a_rows,
+                     m, k, W, n, y, k_steps, ea, wq);
 }
 
 int gemm_row_tile(int m, int n) { return (n / BN) * ((m + 255) / 256) < 128 ? 64 : 256; }
@@ -582,7 +686,7 @@ int device_cus() {
 // list or activations, output, RoPE positions and slot offsets) are shifted.
 template <int EPI, int BM>
 void launch_rows(const _Float16* X, const int32_t* a_rows, int r0, int m, int n, int k, const uint8_t* W, void* y,
-                 hipStream_t s, const GemmRope& ea) {
+                 hipStream_t s, const GemmRope& ea, int* wq) {
   const _Float16* x = a_rows ? X : X + (size_t)r0 * k;
   const int32_t* ar = a_rows ? a_rows + r0 : nullptr;
   GemmRope e = ea;
@@ -595,7 +699,7 @@ void launch_rows(const _Float16* X, const int32_t* a_rows, int r0, int m, int n,
     yy = reinterpret_cast<_Float16*>(y) + (size_t)r0 * ea.n_valid;
   else if (EPI == kEpiStore || EPI == kEpiAdd)
     yy = reinterpret_cast<float*>(y) + (size_t)r0 * n;
-  launch_bm<EPI, BM>(x, ar, m, n, k, W, yy, s, 1, 0, e);
+  launch_bm<EPI, BM>(x, ar, m, n, k, W, yy, s, 1, 0, e, wq);
 }
 
 // Relative duration of a 64-row tile against a 256-row one (a quarter of the
@@ -604,10 +708,10 @@ constexpr double kTile64Cost = 0.35;
 
 template <int EPI>
 void launch_epi(const _Float16* X, const int32_t* a_rows, int m, int n, int k, const uint8_t* W, void* y,
-                hipStream_t s, const GemmRope& ea = GemmRope{}) {
+                hipStream_t s, const GemmRope& ea = GemmRope{}, int* wq = nullptr) {
   // 256-row tiles unless they leave most of the 256 CUs idle
   if (gemm_row_tile(m, n) == 64) {
-    launch_bm<EPI, 64>(X, a_rows, m, n, k, W, y, s, 1, 0, ea);
+    launch_bm<EPI, 64>(X, a_rows, m, n, k, W, y, s, 1, 0, ea, wq);
     return;
   }
   // A ragged last row of 256-row tiles can make a final round of workgroups
@@ -621,12 +725,12 @@ void launch_epi(const _Float16* X, const int32_t* a_rows, int m, int n, int k, c
     const double one = rounds(nt * (full + 1));
     const double two = rounds(nt * full) + kTile64Cost * rounds(nt * ((rem + 63) / 64));
     if (two < one) {
-      launch_rows<EPI, 256>(X, a_rows, 0, full * 256, n, k, W, y, s, ea);
-      launch_rows<EPI, 64>(X, a_rows, full * 256, rem, n, k, W, y, s, ea);
+      launch_rows<EPI, 256>(X, a_rows, 0, full * 256, n, k, W, y, s, ea, wq);
+      launch_rows<EPI, 64>(X, a_rows, full * 256, rem, n, k, W, y, s, ea, wq);
       return;
     }
   }
-  launch_bm<EPI, 256>(X, a_rows, m, n, k, W, y, s, 1, 0, ea);
+  launch_bm<EPI, 256>(X, a_rows, m, n, k, W, y, s, 1, 0, ea, wq);
 }
 
 int gemm_k_steps(int k, int n_split) {
@@ -703,13 +807,13 @@ void launch_gemm_q4_splitk(const void* x, int m, int n, int k, const void* w, in
 }
 
 void launch_gemm_q4(const void* x, int m, int n, int k, const void* w, int epilogue, void* y,
-                    hipStream_t s, const int32_t* a_rows) {
+                    hipStream_t s, const int32_t* a_rows, int* work_queues) {
   const _Float16* X = reinterpret_cast<const _Float16*>(x);
   const uint8_t* W = reinterpret_cast<const uint8_t*>(w);
   switch (epilogue) {
-    case kEpiStore: launch_epi<kEpiStore>(X, a_rows, m, n, k, W, y, s); break;
-    case kEpiAdd: launch_epi<kEpiAdd>(X, a_rows, m, n, k, W, y, s); break;
-    default: launch_epi<kEpiSwiGLU>(X, a_rows, m, n, k, W, y, s); break;
+    case kEpiStore: launch_epi<kEpiStore>(X, a_rows, m, n, k, W, y, s, GemmRope{}, work_queues); break;
+    case kEpiAdd: launch_epi<kEpiAdd>(X, a_rows, m, n, k, W, y, s, GemmRope{}, work_queues); break;
+    default: launch_epi<kEpiSwiGLU>(X, a_rows, m, n, k, W, y, s, GemmRope{}, work_queues); break;
   }
 }
 
@@ -719,13 +823,13 @@ bool gemm_rope_fusable(int head_dim, int chunk_tokens) {
 }
 
 void launch_gemm_q4_rope(const void* x, int m, int n, int k, const void* w, int epilogue, const GemmRope& ea,
-                         void* y, hipStream_t s, const int32_t* a_rows) {
+                         void* y, hipStream_t s, const int32_t* a_rows, int* work_queues) {
   const _Float16* X = reinterpret_cast<const _Float16*>(x);
   const uint8_t* W = reinterpret_cast<const uint8_t*>(w);
   if (epilogue == kEpiRopeQ)
-    launch_epi<kEpiRopeQ>(X, a_rows, m, n, k, W, y, s, ea);
+    launch_epi<kEpiRopeQ>(X, a_rows, m, n, k, W, y, s, ea, work_queues);
   else
-    launch_epi<kEpiRopeKV>(X, a_rows, m, n, k, W, y, s, ea);
+    launch_epi<kEpiRopeKV>(X, a_rows, m, n, k, W, y, s, ea, work_queues);
 }
 
 }  // namespace mzk

@@ -38,15 +38,21 @@ struct GemmRope {
 // kEpiStore: Y float [m][n] = acc; kEpiAdd: Y float [m][n] += acc;
 // kEpiSwiGLU: Y f16 [m][n/2] = silu(gate) * up for the interleaved layout.
 // With a_rows (device, m entries), output row r is computed from X row a_rows[r].
+// With work_queues (device, kGemmQueueInts int32, zero on entry and left zero
+// on return; not shared by launches in flight together), persistent
+// workgroups take the tiles from per-XCD queues, so XCDs that run faster take
+// more of them; the results are the same bits.  (launch_gemm_q4_rope takes
+// the argument but always runs one workgroup per tile.)
+constexpr int kGemmQueueInts = 16;
 void launch_gemm_q4(const void* x, int m, int n, int k, const void* w, int epilogue, void* y,
-                    hipStream_t s, const int32_t* a_rows = nullptr);
+                    hipStream_t s, const int32_t* a_rows = nullptr, int* work_queues = nullptr);
 
 // Y = X . W^T with a rotary-embedding epilogue (kEpiRopeQ / kEpiRopeKV, see
 // GemmRope); n_valid <= n.  Only for gemm_rope_fusable(hd, C): head
 // dimension 32, 64 or 128, C a power of two.
 bool gemm_rope_fusable(int head_dim, int chunk_tokens);
 void launch_gemm_q4_rope(const void* x, int m, int n, int k, const void* w, int epilogue, const GemmRope& ea,
-                         void* y, hipStream_t s, const int32_t* a_rows = nullptr);
+                         void* y, hipStream_t s, const int32_t* a_rows = nullptr, int* work_queues = nullptr);
 
 // Split-K form for few rows: n_split ranges of whole 64-wide K steps
 // (ceil((k / 64) / n_split) steps each) write fp32 partials into ws

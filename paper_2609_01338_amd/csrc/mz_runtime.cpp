@@ -500,6 +500,8 @@ struct mz_ctx {
   // launches run in order on the compute stream)
   int32_t* attn_wq = nullptr;
   bool attn_queue = true;            // option attn_queue
+  int32_t* gemm_wq = nullptr;        // the same for the unsplit projections
+  bool gemm_queue = true;            // option gemm_queue
   bool gemm_split = true;            // option gemm_split
   bool fuse_rope = true;             // option fuse_rope: RoPE (and the KV slot writes) in the GEMM epilogue
   bool fuse_norm = true;             // option fuse_norm: a single row's RMSNorm inside its split-K GEMVs
@@ -513,7 +515,7 @@ struct mz_ctx {
     if (ns > 1)
       mzk::launch_gemm_q4_splitk(X, m, n, k, W, epi, Y, ns, split_ws, s, rows, hn, cfg.rms_eps);
     else
-      mzk::launch_gemm_q4(X, m, n, k, W, epi, Y, s, rows);
+      mzk::launch_gemm_q4(X, m, n, k, W, epi, Y, s, rows, gemm_queue ? gemm_wq : nullptr);
   }
   // The projection with rotary embedding fused into its epilogue (or into
   // the reduce of its K splits), when the shape allows it (false: the caller
@@ -1261,6 +1263,8 @@ mz_status mz_load_model(const mz_model_cfg* cfg, const void* blob, size_t nbytes
     c.split_ws = (uint8_t*)dmalloc((size_t)c.split_ws_bytes);
     c.attn_wq = (int32_t*)dmalloc(mzk::kAttnQueueInts * sizeof(int32_t));
     HIPCHK(hipMemset(c.attn_wq, 0, mzk::kAttnQueueInts * sizeof(int32_t)));
+    c.gemm_wq = (int32_t*)dmalloc(mzk::kGemmQueueInts * sizeof(int32_t));
+    HIPCHK(hipMemset(c.gemm_wq, 0, mzk::kGemmQueueInts * sizeof(int32_t)));
     HIPCHK(hipEventCreateWithFlags(&c.ev_meta, hipEventDisableTiming));
     void* stage = nullptr;
     if (hipHostMalloc(&stage, c.stage_bytes, hipHostMallocDefault) != hipSuccess || !stage)
@@ -1285,7 +1289,7 @@ void mz_free(mz_ctx* x) {
   (void)hipSetDevice(x->device);
   if (x->s_compute) (void)hipStreamSynchronize(x->s_compute);
   if (x->s_swap) (void)hipStreamSynchronize(x->s_swap);
-  void* dptrs[] = {x->codec_stage, x->d_codec_slots, x->split_ws, x->attn_wq, x->w_slab, x->emb_nib, x->emb_sc, x->lm_nib, x->lm_sc,
+  void* dptrs[] = {x->codec_stage, x->d_codec_slots, x->split_ws, x->attn_wq, x->gemm_wq, x->w_slab, x->emb_nib, x->emb_sc, x->lm_nib, x->lm_sc,
                    x->rope_cs, x->kv_slab,
                    x->h[0], x->h[1], x->xb, x->qf, x->kvf, x->q16, x->act, x->logits, x->part_val,
                    x->part_idx, x->d_token, x->d_tables, x->d_pos, x->d_kvoff, x->d_dix, x->d_posq,
@@ -1318,6 +1322,7 @@ mz_status mz_set_option(mz_ctx* x, const char* key, int64_t value) {
     else if (k == "swap_trim") x->swap_trim = value != 0;
     else if (k == "attn_split") x->attn_split = value != 0;
     else if (k == "attn_queue") x->attn_queue = value != 0;
+    else if (k == "gemm_queue") x->gemm_queue = value != 0;
     else if (k == "gemm_split") x->gemm_split = value != 0;
     else if (k == "fuse_norm") x->fuse_norm = value != 0;
     else if (k == "fuse_rope") x->fuse_rope = value != 0;
@@ -1715,17 +1720,28 @@ mz_status mz_q4_gemm_pack(const void* w, const void* w_up, int32_t n, int32_t k,
   });
 }
 
-mz_status mz_q4_gemm(const void* x_f16, int32_t m, int32_t n_pad, int32_t k, const void* w_packed,
-                     int32_t epilogue, void* y, void* stream) {
+static mz_status gemm_entry(const void* x_f16, int32_t m, int32_t n_pad, int32_t k, const void* w_packed,
+                            int32_t epilogue, void* y, int32_t* queues, void* stream) {
   return guarded(nullptr, [&] {
     if (!x_f16 || !w_packed || !y) fail(MZ_EINVAL, "NULL pointer");
     if (m < 1 || n_pad < 1 || k < 1) fail(MZ_EINVAL, "sizes must be positive");
     if (n_pad % mzk::kGemmTileN) fail(MZ_EINVAL, "n_pad must be a multiple of %d", mzk::kGemmTileN);
     if (k % mzk::kGemmTileK) fail(MZ_EINVAL, "k must be a multiple of %d", mzk::kGemmTileK);
     if (epilogue < 0 || epilogue > 2) fail(MZ_EINVAL, "bad epilogue");
-    mzk::launch_gemm_q4(x_f16, m, n_pad, k, w_packed, epilogue, y, (hipStream_t)stream);
+    mzk::launch_gemm_q4(x_f16, m, n_pad, k, w_packed, epilogue, y, (hipStream_t)stream, nullptr, queues);
     HIPCHK(hipGetLastError());
   });
+}
+
+mz_status mz_q4_gemm(const void* x_f16, int32_t m, int32_t n_pad, int32_t k, const void* w_packed,
+                     int32_t epilogue, void* y, void* stream) {
+  return gemm_entry(x_f16, m, n_pad, k, w_packed, epilogue, y, nullptr, stream);
+}
+
+mz_status mz_q4_gemm_queued(const void* x_f16, int32_t m, int32_t n_pad, int32_t k, const void* w_packed,
+                            int32_t epilogue, void* y, int32_t* work_queues, void* stream) {
+  if (!work_queues) return guarded(nullptr, [&] { fail(MZ_EINVAL, "work_queues is NULL"); });
+  return gemm_entry(x_f16, m, n_pad, k, w_packed, epilogue, y, work_queues, stream);
 }
 
 int64_t mz_q4_gemm_split_workspace_bytes(int32_t m, int32_t n_pad, int32_t n_split) {

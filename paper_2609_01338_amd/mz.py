@@ -105,6 +105,7 @@ def lib() -> ctypes.CDLL:
         "mz_q4_gemm": ([vp, i32, i32, i32, vp, i32, vp, vp], i32),
         "mz_attention": ([vp, vp, i32, vp, vp, i32, i32, i32, i32, i32, vp, vp], i32),
         "mz_attention_queued": ([vp, vp, i32, vp, vp, i32, i32, i32, i32, i32, vp, vp, vp], i32),
+        "mz_q4_gemm_queued": ([vp, i32, i32, i32, vp, i32, vp, vp, vp], i32),
         "mz_rmsnorm": ([vp, i32, i32, ctypes.c_float, vp, vp], i32),
         "mz_probe_ceilings": ([i32, ctypes.c_char_p, sz], i32),
         "mz_plan_evict": ([ctypes.POINTER(mz_model_cfg), ctypes.POINTER(mz_evict_request), vp, vp, vp], i32),
@@ -329,6 +330,11 @@ def mz_q4_gemm_pack(w: np.ndarray, n: int, k: int, w_up: Optional[np.ndarray] = 
 def mz_q4_gemm(x_ptr: int, m: int, n_pad: int, k: int, w_ptr: int, epilogue: int, y_ptr: int,
                stream: Optional[int] = None) -> None:
     _check(lib().mz_q4_gemm(x_ptr, m, n_pad, k, w_ptr, epilogue, y_ptr, stream), None)
+
+
+def mz_q4_gemm_queued(x_ptr: int, m: int, n_pad: int, k: int, w_ptr: int, epilogue: int, y_ptr: int,
+                      queues_ptr: int, stream: Optional[int] = None) -> None:
+    _check(lib().mz_q4_gemm_queued(x_ptr, m, n_pad, k, w_ptr, epilogue, y_ptr, queues_ptr, stream), None)
 
 
 def mz_attention(q_ptr: int, qpos_ptr: int, m: int, slab_ptr: int, table_ptr: int, n_table: int,

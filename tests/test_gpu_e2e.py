@@ -422,6 +422,43 @@ def test_decode_norm_in_gemv_same_bits(key):
         assert k1.tobytes() == k0.tobytes() and v1.tobytes() == v0.tobytes(), key
 
 
+@pytest.mark.parametrize("gemm_split", [1, 0])
+def test_rope_fused_same_bits(gemm_split):
+    """The rotary embedding in the projection epilogues and split-K reduces
+    (fuse_rope 1) against the projection followed by the separate RoPE pass
+    (fuse_rope 0): a clean prefill (many rows) and decode steps (one row; split
+    over K unless gemm_split is 0) give the same tokens, K/V and logits bit
+    for bit, since every path rotates through one routine."""
+    torch_cuda()
+    w = W.WORKLOADS["8b"].scaled(n_layers=2, n_ctx=512, n_prompt=16)
+    m = w.model
+    C, dkv = m.chunk_tokens, m.dkv
+    ctx, prm = W.make_tokens(w)
+    S, n = ctx.size + len(prm), 4
+    outs = []
+    for fuse in (1, 0):
+        eng = mz.Engine(m, blob_for(w), max_ctx=S + n + 9)
+        try:
+            mz.mz_set_option(eng.ctx, "gemm_split", gemm_split)
+            mz.mz_set_option(eng.ctx, "fuse_rope", fuse)
+            mz.mz_prefill_context(eng.ctx, np.concatenate([ctx, prm]))
+            tok, first = mz.mz_first_token(eng.ctx, m.vocab)
+            toks = mz.mz_generate(eng.ctx, tok, n)
+            mz.mz_restore_and_prefill(eng.ctx, toks[-1:].astype(np.int32))
+            _, logits = mz.mz_first_token(eng.ctx, m.vocab)
+            kv = [mz.mz_read_kv(eng.ctx, l, c, C, dkv) for l in range(m.n_layers) for c in range((S + n) // C + 1)]
+            outs.append((first, toks, logits, kv))
+        finally:
+            eng.close()
+    (f1, t1, g1, kv1), (f0, t0, g0, kv0) = outs
+    report("case", name=f"rope-fused-bits-split{gemm_split}", tokens=list(map(int, t1)))
+    assert f1.tobytes() == f0.tobytes()
+    assert (t1 == t0).all()
+    assert g1.tobytes() == g0.tobytes()
+    for (k1, v1), (k0, v0) in zip(kv1, kv0):
+        assert k1.tobytes() == k0.tobytes() and v1.tobytes() == v0.tobytes()
+
+
 def test_tiny_generate_after_restore(tiny_engine):
     """Restore of a mixed plan, first token, then 12 generated tokens (they
     cross into a new chunk)."""

@@ -26,11 +26,15 @@ pytestmark = pytest.mark.gpu
 
 
 def _gemm_case(M, N, K, epi, seed, sample_rows=None, n_split=None):
-    """n_split: None for mz_q4_gemm, else mz_q4_gemm_split with that many K
-    splits ("auto": the restore's choice)."""
+    """n_split: None for mz_q4_gemm, "queued" for mz_q4_gemm_queued (run
+    twice from the same initial output on the same queues, which must come
+    back zero, and equal to mz_q4_gemm bit for bit), else mz_q4_gemm_split with
+    that many K splits ("auto": the restore's choice)."""
     torch = torch_cuda()
     rng = np.random.default_rng(seed)
     report("gemm", M=M, N=N, K=K, epi=epi, seed=seed, n_split=n_split)
+    if sample_rows is not None:   # checked on the host: the gather below must stay in bounds
+        assert 0 <= int(np.min(sample_rows)) and int(np.max(sample_rows)) < M, "sample rows out of range"
     if epi == 2:
         g = W.encode_q4_0((rng.standard_normal((N, K)) * 0.02).astype(np.float32))
         u = W.encode_q4_0((rng.standard_normal((N, K)) * 0.02).astype(np.float32))
@@ -51,6 +55,18 @@ def _gemm_case(M, N, K, epi, seed, sample_rows=None, n_split=None):
     y0 = y.float().cpu().numpy().astype(np.float64)
     if n_split is None:
         mz.mz_q4_gemm(x.data_ptr(), M, n_pad, K, w.data_ptr(), epi, y.data_ptr(), stream())
+    elif n_split == "queued":
+        y_init = y.clone()
+        mz.mz_q4_gemm(x.data_ptr(), M, n_pad, K, w.data_ptr(), epi, y.data_ptr(), stream())
+        plain = y.clone()
+        queues = torch.zeros(16, device="cuda", dtype=torch.int32)
+        for rep in range(2):
+            y.copy_(y_init)
+            mz.mz_q4_gemm_queued(x.data_ptr(), M, n_pad, K, w.data_ptr(), epi, y.data_ptr(), queues.data_ptr(),
+                                 stream())
+            torch.cuda.synchronize()
+            assert int(queues.abs().sum()) == 0, "work queues not left at zero"
+            assert torch.equal(y.view(torch.uint8), plain.view(torch.uint8)), "queued != mz_q4_gemm"
     else:
         if n_split == "auto":
             n_split = mz.mz_q4_gemm_auto_splits(M, n_pad, K, 64 << 20)
@@ -120,6 +136,8 @@ def test_gemm_split_validation():
         mz.mz_q4_gemm_split(1, 4, 256, 640, 1, 0, 1, 2, 1, 100, None)     # workspace too small
     with pytest.raises(mz.MzError):
         mz.mz_q4_gemm_split(1, 4, 256, 640, 1, 0, 1, 0, 1, 1 << 20, None)  # n_split 0
+    with pytest.raises(mz.MzError):
+        mz.mz_q4_gemm_queued(1, 4, 256, 640, 1, 0, 1, 0, None)            # no work queues
     assert mz.mz_q4_gemm_auto_splits(32896, 4096, 4096, 64 << 20) == 1
     assert mz.mz_q4_gemm_auto_splits(1, 4096, 14336, 64 << 20) > 8
 
@@ -143,7 +161,25 @@ def test_gemm_full_layer_shapes(key):
         rng = np.random.default_rng(i)
         edge = [r for r in (M // 256 * 256 - 1, M // 256 * 256) if 0 <= r < M]
         rows = np.unique(np.concatenate([rng.choice(M, min(M, 24), replace=False), [0, M - 1], edge]))
-        _gemm_case(M, N, K, epi, seed=100 + i, sample_rows=rows)
+        _gemm_case(M, N, K, epi, seed=100 + i, sample_rows=rows, n_split="queued")
+
+
+@pytest.mark.parametrize("M,N,K,epi", [
+    (20000, 14336, 128, 0), (16640, 16384, 64, 1), (20000, 7168, 128, 2), (33000, 8192, 64, 1),
+    (1000, 2048, 512, 0), (9000, 4096, 512, 1), (300, 512, 128, 1)])
+def test_gemm_queued(M, N, K, epi):
+    """mz_q4_gemm_queued for every plain epilogue: launches of at least 16
+    rounds (4096 and more 256-row tiles) take the work queues, with and
+    without a ragged remainder of 64-row tiles; shorter ones run one
+    workgroup per tile.  Against the exact product on sampled rows and
+    bit-equal to mz_q4_gemm."""
+    rows = None
+    if M > 4000:
+        rng = np.random.default_rng(M)
+        rows = np.unique(np.concatenate([rng.choice(M, 40, replace=False),
+                                         [0, M // 256 * 256 - 1, M // 256 * 256, M - 1]]))
+        rows = rows[rows < M]   # M // 256 * 256 is M itself when M is a multiple of 256
+    _gemm_case(M, N, K, epi, seed=M + 7, sample_rows=rows, n_split="queued")
 
 
 def _attn_case(nq, nkv, hd, C, S, qpos, seed, sample=None, n_split=None):
@@ -153,6 +189,8 @@ def _attn_case(nq, nkv, hd, C, S, qpos, seed, sample=None, n_split=None):
     splits ("auto": the restore's choice)."""
     torch = torch_cuda()
     report("attention", nq=nq, nkv=nkv, hd=hd, C=C, S=S, m=len(qpos), seed=seed, n_split=n_split)
+    if sample is not None:
+        assert 0 <= int(np.min(sample)) and int(np.max(sample)) < len(qpos), "sample rows out of range"
     rng = np.random.default_rng(seed)
     dkv = nkv * hd
     nch = (S + C - 1) // C
