@@ -32,8 +32,8 @@ METRIC = "KV-recompute prefill tokens/s + TTFT ms from evicted state, 1 MI355X"
 # valid only for the kernel source they were taken on and the 8B workload.
 MEASURED_TRAFFIC = {"kernel": "attn_kernel", "workload": "8b",
                     "source": "paper_2609_01338_amd/csrc/attention.hip",
-                    "sha256": "2493df82ca235614c2d76418109c376f7a4a8a8ce8e98a935d6d0a51038c1341",
-                    "bytes_per_launch": 1.642e9}
+                    "sha256": "d951c04492062eb71d0da0615efbd2a5f443306b753f2f8a87f7618257b5be2d",
+                    "bytes_per_launch": 1.660e9}
 PEAK_MFMA_TFLOPS = 2500.0      # MI355X dense bf16 / fp16 MFMA
 PEAK_HBM_GBPS = 8000.0
 
