@@ -38,55 +38,95 @@ PEAK_MFMA_TFLOPS = 2500.0      # MI355X dense bf16 / fp16 MFMA
 PEAK_HBM_GBPS = 8000.0
 
 
+# Child process that samples the board through amdsmi (read-only metrics):
+# one line "time power clk0 clk1 ..." every period, appended to a file.
+_SAMPLER = r"""
+import sys, time
+out, period = sys.argv[1], float(sys.argv[2])
+try:
+    import amdsmi
+    amdsmi.amdsmi_init()
+    h = amdsmi.amdsmi_get_processor_handles()[0]
+    cap = amdsmi.amdsmi_get_power_cap_info(h)["power_cap"] / 1e6
+except Exception as e:
+    open(out, "w").write("error %s: %s\n" % (type(e).__name__, e))
+    sys.exit(0)
+with open(out, "w", buffering=1) as f:
+    f.write("cap %r\n" % cap)
+    while True:
+        try:
+            m = amdsmi.amdsmi_get_gpu_metrics_info(h)
+            clk = [c for c in (m.get("current_gfxclks") or []) if isinstance(c, (int, float)) and c < 10000]
+            pw = m.get("current_socket_power")
+            if isinstance(pw, (int, float)) and clk:
+                f.write("%.6f %r %s\n" % (time.time(), float(pw), " ".join(str(c) for c in clk)))
+        except Exception as e:
+            f.write("error %s: %s\n" % (type(e).__name__, e))
+        time.sleep(period)
+"""
+
+
 class BoardMonitor:
-    """Socket power and per-XCD shader clocks, read by a host thread through
-    amdsmi (read-only metrics) every `period_s` while `active` is set; the
-    summary is None where amdsmi is unavailable."""
+    """Socket power and per-XCD shader clocks, sampled every `period_s` by a
+    child process (started before this process touches the GPU, so the
+    sampling takes no time of the measured process) and kept for the time
+    windows passed to `window`; the summary is None where amdsmi is
+    unavailable."""
 
     def __init__(self, period_s=0.02):
-        import threading
-        self.active, self.samples, self.stop, self.err = False, [], False, None
-        try:
-            import amdsmi
-            amdsmi.amdsmi_init()
-            self.amdsmi = amdsmi
-            self.h = amdsmi.amdsmi_get_processor_handles()[0]
-            self.cap_w = amdsmi.amdsmi_get_power_cap_info(self.h)["power_cap"] / 1e6
-        except Exception as e:   # no amdsmi, no device access
-            self.err = f"{type(e).__name__}: {e}"
-            return
-        self.period = period_s
-        self.th = threading.Thread(target=self._run, daemon=True)
-        self.th.start()
+        import subprocess
+        import tempfile
+        self.period, self.windows = period_s, []
+        fd, self.path = tempfile.mkstemp(prefix="board_", suffix=".txt")
+        os.close(fd)
+        self.proc = subprocess.Popen([sys.executable, "-c", _SAMPLER, self.path, str(period_s)],
+                                     stdin=subprocess.DEVNULL, stdout=subprocess.DEVNULL,
+                                     stderr=subprocess.DEVNULL)
+        import atexit
+        atexit.register(self._stop)   # every exit path ends the sampler
 
-    def _run(self):
-        while not self.stop:
-            if self.active:
-                try:
-                    m = self.amdsmi.amdsmi_get_gpu_metrics_info(self.h)
-                    clk = [c for c in (m.get("current_gfxclks") or []) if isinstance(c, (int, float)) and c < 10000]
-                    pw = m.get("current_socket_power")
-                    if isinstance(pw, (int, float)) and clk:
-                        self.samples.append((float(pw), clk))
-                except Exception as e:
-                    self.err = f"{type(e).__name__}: {e}"
-            time.sleep(self.period)
+    def _stop(self):
+        if self.proc.poll() is None:
+            self.proc.terminate()
+            try:
+                self.proc.wait(timeout=10)
+            except Exception:
+                self.proc.kill()
+                self.proc.wait()
+
+    def window(self, t0, t1):
+        self.windows.append((t0, t1))
 
     def summary(self):
-        self.stop = True
-        if self.err and not self.samples:
-            return {"error": self.err}
-        if not self.samples:
-            return None
-        pw = np.array([s[0] for s in self.samples])
-        n = min(len(s[1]) for s in self.samples)
-        clk = np.array([s[1][:n] for s in self.samples], dtype=np.float64)
+        self._stop()
+        try:
+            lines = open(self.path).read().splitlines()
+        finally:
+            os.unlink(self.path)
+        cap, samples, err = None, [], None
+        for ln in lines:
+            f = ln.split()
+            if not f:
+                continue
+            if f[0] == "cap":
+                cap = float(f[1])
+            elif f[0] == "error":
+                err = ln
+            else:
+                t = float(f[0])
+                if any(a <= t <= b for a, b in self.windows):
+                    samples.append((float(f[1]), [float(c) for c in f[2:]]))
+        if not samples:
+            return {"error": err} if err else None
+        pw = np.array([x[0] for x in samples])
+        n = min(len(x[1]) for x in samples)
+        clk = np.array([x[1][:n] for x in samples], dtype=np.float64)
         return {"socket_power_w_mean": round(float(pw.mean()), 1), "socket_power_w_max": round(float(pw.max()), 1),
-                "power_cap_w": round(self.cap_w, 1), "gfxclk_mhz_mean": round(float(clk.mean()), 1),
+                "power_cap_w": round(cap, 1) if cap else None, "gfxclk_mhz_mean": round(float(clk.mean()), 1),
                 "gfxclk_mhz_per_xcd": [round(float(c), 1) for c in clk.mean(axis=0)],
-                "samples": len(self.samples),
-                "source": f"amdsmi current_socket_power / current_gfxclks every {self.period * 1e3:.0f} ms "
-                          "inside the timed steps (GPU busy and idle parts alike)"}
+                "samples": len(samples),
+                "source": f"amdsmi current_socket_power / current_gfxclks every {self.period * 1e3:.0f} ms from a "
+                          "child process, samples inside the timed steps (GPU busy and idle parts alike)"}
 
 
 def measured_traffic(kernel, workload):
@@ -385,6 +425,7 @@ def main():
         print(f"bench.py measures one GPU: the engine has no multi-GPU path (asked for --gpus {args.gpus})",
               file=sys.stderr)
         sys.exit(2)
+    board = BoardMonitor()   # before anything touches the GPU
 
     # torch (device buffers of the calibration copy and the shard-kernel
     # timings) brings its own HIP runtime; initialising it before libmz is
@@ -437,18 +478,18 @@ def main():
 
     ttft, toks, logit_err = [], [], []
     stats = None
-    board = BoardMonitor()
     for step in range(args.warmup + args.steps):
         timed = step >= args.warmup
         if step == args.warmup:
             mz.mz_set_option(e, "kernel_timing", 1)
         mz.mz_evict(e, plan.kv_state, plan.w_state)
-        board.active = timed
+        w0 = time.time()
         t0 = time.perf_counter()
         mz.mz_restore_and_prefill(e, prompt)
         tok, logits = mz.mz_first_token(e, m.vocab)
         dt = time.perf_counter() - t0
-        board.active = False
+        if timed:
+            board.window(w0, time.time())
         if timed:
             ttft.append(dt)
         toks.append(tok)
