@@ -706,9 +706,34 @@ void launch_rows(const _Float16* X, const int32_t* a_rows, int r0, int m, int n,
 // MFMA work, the same weight traffic and dequantization).
 constexpr double kTile64Cost = 0.35;
 
+// Rows [r0, r0 + m) of the product split over K (partials in ws, then the
+// reduce with the epilogue): for a remainder of few rows whose tiles alone
+// would leave most of the CUs idle while each runs the whole K range.
+template <int EPI>
+void launch_rows_split(const _Float16* X, const int32_t* a_rows, int r0, int m, int n, int k, const uint8_t* W,
+                       void* y, hipStream_t s, const GemmRope& ea, void* ws, int ns) {
+  const _Float16* x = a_rows ? X : X + (size_t)r0 * k;
+  const int32_t* ar = a_rows ? a_rows + r0 : nullptr;
+  GemmRope e = ea;
+  if (e.pos) e.pos += r0;
+  if (e.kv_off) e.kv_off += r0;
+  void* yy = y;
+  if (EPI == kEpiSwiGLU)
+    yy = reinterpret_cast<_Float16*>(y) + (size_t)r0 * (n / 2);
+  else if (EPI == kEpiRopeQ)
+    yy = reinterpret_cast<_Float16*>(y) + (size_t)r0 * ea.n_valid;
+  else if (EPI == kEpiStore || EPI == kEpiAdd)
+    yy = reinterpret_cast<float*>(y) + (size_t)r0 * n;
+  if (EPI == kEpiRopeQ || EPI == kEpiRopeKV)
+    launch_gemm_q4_splitk_rope(x, m, n, k, W, EPI, e, yy, ns, ws, s, ar);
+  else
+    launch_gemm_q4_splitk(x, m, n, k, W, EPI, yy, ns, ws, s, ar);
+}
+
 template <int EPI>
 void launch_epi(const _Float16* X, const int32_t* a_rows, int m, int n, int k, const uint8_t* W, void* y,
-                hipStream_t s, const GemmRope& ea = GemmRope{}, int* wq = nullptr) {
+                hipStream_t s, const GemmRope& ea = GemmRope{}, int* wq = nullptr, void* ws = nullptr,
+                int64_t ws_bytes = 0) {
   // 256-row tiles unless they leave most of the 256 CUs idle
   if (gemm_row_tile(m, n) == 64) {
     launch_bm<EPI, 64>(X, a_rows, m, n, k, W, y, s, 1, 0, ea, wq);
@@ -726,7 +751,13 @@ void launch_epi(const _Float16* X, const int32_t* a_rows, int m, int n, int k, c
     const double two = rounds(nt * full) + kTile64Cost * rounds(nt * ((rem + 63) / 64));
     if (two < one) {
       launch_rows<EPI, 256>(X, a_rows, 0, full * 256, n, k, W, y, s, ea, wq);
-      launch_rows<EPI, 64>(X, a_rows, full * 256, rem, n, k, W, y, s, ea, wq);
+      // the remainder split over K when a workspace is at hand and its
+      // tiles alone would not fill the chip
+      const int ns = ws ? gemm_auto_splits(rem, n, k, ws_bytes) : 1;
+      if (ns > 1)
+        launch_rows_split<EPI>(X, a_rows, full * 256, rem, n, k, W, y, s, ea, ws, ns);
+      else
+        launch_rows<EPI, 64>(X, a_rows, full * 256, rem, n, k, W, y, s, ea, wq);
       return;
     }
   }
@@ -807,13 +838,13 @@ void launch_gemm_q4_splitk(const void* x, int m, int n, int k, const void* w, in
 }
 
 void launch_gemm_q4(const void* x, int m, int n, int k, const void* w, int epilogue, void* y,
-                    hipStream_t s, const int32_t* a_rows, int* work_queues) {
+                    hipStream_t s, const int32_t* a_rows, int* work_queues, void* ws, int64_t ws_bytes) {
   const _Float16* X = reinterpret_cast<const _Float16*>(x);
   const uint8_t* W = reinterpret_cast<const uint8_t*>(w);
   switch (epilogue) {
-    case kEpiStore: launch_epi<kEpiStore>(X, a_rows, m, n, k, W, y, s, GemmRope{}, work_queues); break;
-    case kEpiAdd: launch_epi<kEpiAdd>(X, a_rows, m, n, k, W, y, s, GemmRope{}, work_queues); break;
-    default: launch_epi<kEpiSwiGLU>(X, a_rows, m, n, k, W, y, s, GemmRope{}, work_queues); break;
+    case kEpiStore: launch_epi<kEpiStore>(X, a_rows, m, n, k, W, y, s, GemmRope{}, work_queues, ws, ws_bytes); break;
+    case kEpiAdd: launch_epi<kEpiAdd>(X, a_rows, m, n, k, W, y, s, GemmRope{}, work_queues, ws, ws_bytes); break;
+    default: launch_epi<kEpiSwiGLU>(X, a_rows, m, n, k, W, y, s, GemmRope{}, work_queues, ws, ws_bytes); break;
   }
 }
 
@@ -823,13 +854,14 @@ bool gemm_rope_fusable(int head_dim, int chunk_tokens) {
 }
 
 void launch_gemm_q4_rope(const void* x, int m, int n, int k, const void* w, int epilogue, const GemmRope& ea,
-                         void* y, hipStream_t s, const int32_t* a_rows, int* work_queues) {
+                         void* y, hipStream_t s, const int32_t* a_rows, int* work_queues, void* ws,
+                         int64_t ws_bytes) {
   const _Float16* X = reinterpret_cast<const _Float16*>(x);
   const uint8_t* W = reinterpret_cast<const uint8_t*>(w);
   if (epilogue == kEpiRopeQ)
-    launch_epi<kEpiRopeQ>(X, a_rows, m, n, k, W, y, s, ea, work_queues);
+    launch_epi<kEpiRopeQ>(X, a_rows, m, n, k, W, y, s, ea, work_queues, ws, ws_bytes);
   else
-    launch_epi<kEpiRopeKV>(X, a_rows, m, n, k, W, y, s, ea, work_queues);
+    launch_epi<kEpiRopeKV>(X, a_rows, m, n, k, W, y, s, ea, work_queues, ws, ws_bytes);
 }
 
 }  // namespace mzk

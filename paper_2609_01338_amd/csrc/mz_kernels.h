@@ -44,15 +44,20 @@ struct GemmRope {
 // more of them; the results are the same bits.  (launch_gemm_q4_rope takes
 // the argument but always runs one workgroup per tile.)
 constexpr int kGemmQueueInts = 16;
+// With ws (ws_bytes of device scratch, not in use by launches in flight), a
+// ragged remainder of rows whose tiles alone would leave most CUs idle runs
+// split over K (as launch_gemm_q4_splitk) instead of as 64-row tiles.
 void launch_gemm_q4(const void* x, int m, int n, int k, const void* w, int epilogue, void* y,
-                    hipStream_t s, const int32_t* a_rows = nullptr, int* work_queues = nullptr);
+                    hipStream_t s, const int32_t* a_rows = nullptr, int* work_queues = nullptr,
+                    void* ws = nullptr, int64_t ws_bytes = 0);
 
 // Y = X . W^T with a rotary-embedding epilogue (kEpiRopeQ / kEpiRopeKV, see
 // GemmRope); n_valid <= n.  Only for gemm_rope_fusable(hd, C): head
 // dimension 32, 64 or 128, C a power of two.
 bool gemm_rope_fusable(int head_dim, int chunk_tokens);
 void launch_gemm_q4_rope(const void* x, int m, int n, int k, const void* w, int epilogue, const GemmRope& ea,
-                         void* y, hipStream_t s, const int32_t* a_rows = nullptr, int* work_queues = nullptr);
+                         void* y, hipStream_t s, const int32_t* a_rows = nullptr, int* work_queues = nullptr,
+                         void* ws = nullptr, int64_t ws_bytes = 0);
 
 // Split-K form for few rows: n_split ranges of whole 64-wide K steps
 // (ceil((k / 64) / n_split) steps each) write fp32 partials into ws

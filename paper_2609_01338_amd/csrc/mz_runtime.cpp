@@ -515,7 +515,8 @@ struct mz_ctx {
     if (ns > 1)
       mzk::launch_gemm_q4_splitk(X, m, n, k, W, epi, Y, ns, split_ws, s, rows, hn, cfg.rms_eps);
     else
-      mzk::launch_gemm_q4(X, m, n, k, W, epi, Y, s, rows, gemm_queue ? gemm_wq : nullptr);
+      mzk::launch_gemm_q4(X, m, n, k, W, epi, Y, s, rows, gemm_queue ? gemm_wq : nullptr,
+                          gemm_split ? split_ws : nullptr, split_ws_bytes);
   }
   // The projection with rotary embedding fused into its epilogue (or into
   // the reduce of its K splits), when the shape allows it (false: the caller
@@ -527,7 +528,8 @@ struct mz_ctx {
     if (ns > 1)
       mzk::launch_gemm_q4_splitk_rope(X, m, n, k, W, epi, ea, Y, ns, split_ws, s, rows, hn, cfg.rms_eps);
     else
-      mzk::launch_gemm_q4_rope(X, m, n, k, W, epi, ea, Y, s, rows);
+      mzk::launch_gemm_q4_rope(X, m, n, k, W, epi, ea, Y, s, rows, nullptr, gemm_split ? split_ws : nullptr,
+                               split_ws_bytes);
     return true;
   }
   // A one-row product that runs as the split-K GEMV, which can normalize its
