@@ -168,10 +168,36 @@ __device__ __forceinline__ void rope_epilogue(const f32x4 (&acc)[BM / 64][8], co
             yr[col + HALF] = (_Float16)y.y;
           }
         }
-        if constexpr (EPI == kEpiRopeKV) {
-          // values: V^T[c][pos % C] of the row's slot
+      }
+    if constexpr (EPI == kEpiRopeKV) {
+      // values: V^T[c][pos % C] of each row's slot.  A lane's 4 rows that
+      // are 4 consecutive positions from a multiple of 4 in one slot (the
+      // common case: recomputed chunks and prompts are runs of positions)
+      // leave as one 8-byte store per column; any other row as 2-byte ones.
+      const int i = i0;
+      const int row0 = mt * BM + wm * (BM / 4) + i * 16 + row_in;
+      bool vec = row0 + 3 < M && (pos[i][0] & 3) == 0 && off[0][0] >= 0;
+#pragma unroll
+      for (int r = 1; r < 4; ++r)
+        vec = vec && pos[i][r] == pos[i][0] + r && off[0][r] == off[0][0] + (int64_t)r * ea.n_valid;
+      if (vec) {
+        const int pc = pos[i][0] & (ea.C - 1);
+        uint8_t* vt = ea.slab + off[0][0] - (int64_t)pc * ea.n_valid + (int64_t)ea.C * ea.n_valid + pc * 2;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int col = col0 + j * 16;
+          if (col >= rot_end && col < ea.n_valid) {
+            typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+            *reinterpret_cast<f16x4*>(vt + (int64_t)(col - rot_end) * ea.C * 2) =
+                f16x4{(_Float16)acc[i][j][0], (_Float16)acc[i][j][1], (_Float16)acc[i][j][2], (_Float16)acc[i][j][3]};
+          }
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          if (row0 + r >= M || off[0][r] < 0) continue;
           const int pc = pos[i][r] & (ea.C - 1);
-          uint8_t* vt = ea.slab + off[ii][r] - (int64_t)pc * ea.n_valid + (int64_t)ea.C * ea.n_valid + pc * 2;
+          uint8_t* vt = ea.slab + off[0][r] - (int64_t)pc * ea.n_valid + (int64_t)ea.C * ea.n_valid + pc * 2;
 #pragma unroll
           for (int j = 0; j < 8; ++j) {
             const int col = col0 + j * 16;
@@ -180,6 +206,7 @@ __device__ __forceinline__ void rope_epilogue(const f32x4 (&acc)[BM / 64][8], co
           }
         }
       }
+    }
   }
 }
 
