@@ -94,8 +94,9 @@ class Weights:
 
     LAYER_TENSORS = ("wq", "wk", "wv", "wo", "wg", "wu", "wd")
 
-    def __init__(self, hp: Hyper, blob: np.ndarray):
+    def __init__(self, hp: Hyper, blob: np.ndarray, threads: int = 1):
         self.hp = hp
+        self.threads = threads
         self.blob = np.asarray(blob, dtype=np.uint8).reshape(-1)
         d, dq, dkv, ff, V = hp.d_model, hp.dq, hp.dkv, hp.d_ffn, hp.vocab
         shapes = {"wq": (dq, d), "wk": (dkv, d), "wv": (dkv, d), "wo": (d, dq),
@@ -125,8 +126,23 @@ class Weights:
         return self.blob[off0: off1 + r * q4_0_row_bytes(c)].tobytes()
 
     def tensor(self, name: str, layer: int = -1) -> np.ndarray:
+        """Decode a whole tensor (rows split over `threads` threads: each row
+        decodes on its own)."""
         off, r, c = self.index[(name, layer)]
-        return q4_0_decode(self.raw(name, layer), r, c)
+        raw = self.raw(name, layer).reshape(r, q4_0_row_bytes(c))
+        if self.threads <= 1 or r < 2 * self.threads:
+            return q4_0_decode(raw, r, c)
+        out = np.empty((r, c), dtype=np.float64)
+        step = (r + self.threads - 1) // self.threads
+
+        def part(r0: int):
+            r1 = min(r, r0 + step)
+            out[r0:r1] = q4_0_decode(raw[r0:r1], r1 - r0, c)
+
+        from concurrent.futures import ThreadPoolExecutor
+        with ThreadPoolExecutor(self.threads) as ex:
+            list(ex.map(part, range(0, r, step)))
+        return out
 
     def layer(self, l: int) -> Dict[str, np.ndarray]:
         if l not in self._cache:
@@ -167,30 +183,55 @@ def silu(z: np.ndarray) -> np.ndarray:
 
 
 def causal_gqa_attention(q: np.ndarray, qpos: np.ndarray, k: np.ndarray, v: np.ndarray,
-                         block: int = 64) -> np.ndarray:
+                         block: int = 64, threads: int = 1) -> np.ndarray:
     """o[i, h] = sum_{j <= qpos[i]} softmax_j(q[i,h] . k[j,g(h)] / sqrt(hd)) v[j,g(h)].
 
     q [n, nq, hd] at absolute positions qpos [n]; k, v [S, nkv, hd] hold keys for
     positions 0..S-1; g(h) = h // (nq / nkv).  The softmax subtracts the row max.
-    Queries are taken a few at a time only to bound memory.
+
+    The query heads of one KV head share its keys, so they are taken together
+    as the rows of one product with that head's keys (no copy of K/V per query
+    head).  Queries are taken `block` at a time only to bound memory; with
+    threads > 1 the independent (query block, KV head) pieces run on that many
+    threads with a single-threaded BLAS each: the same steps, bit for bit what
+    the serial loop gives under a single-threaded BLAS (a multi-threaded BLAS
+    may add the products of one piece in another order, an fp64 rounding).
     """
     n, nq, hd = q.shape
     nkv = k.shape[1]
     group = nq // nkv
-    kh = np.repeat(k, group, axis=1)      # [S, nq, hd]: key head of each query head
-    vh = np.repeat(v, group, axis=1)
-    out = np.empty_like(q)
+    qpos = np.asarray(qpos, dtype=np.int64)
     scale = 1.0 / math.sqrt(hd)
-    for b0 in range(0, n, block):
-        qb, pb = q[b0:b0 + block], np.asarray(qpos[b0:b0 + block])
+    kg = [np.ascontiguousarray(k[:, g]) for g in range(nkv)]       # [S, hd] per KV head
+    vg = [np.ascontiguousarray(v[:, g]) for g in range(nkv)]
+    out = np.empty((n, nq, hd), dtype=np.float64)
+
+    def piece(b0: int, g: int):
+        pb = qpos[b0:b0 + block]
+        nb = pb.size
         last = int(pb.max()) + 1
-        s = np.einsum("nhd,jhd->nhj", qb, kh[:last]) * scale            # [nb, nq, last]
-        mask = np.arange(last)[None, :] > pb[:, None]                    # key after query
-        s = np.where(mask[:, None, :], -np.inf, s)
-        s = s - s.max(axis=-1, keepdims=True)
-        p = np.exp(s)
-        p = p / p.sum(axis=-1, keepdims=True)
-        out[b0:b0 + block] = np.einsum("nhj,jhd->nhd", p, vh[:last])
+        heads = slice(g * group, (g + 1) * group)
+        rows = q[b0:b0 + nb, heads].reshape(nb * group, hd)          # (query, head) rows
+        s = (rows @ kg[g][:last].T).reshape(nb, group, last)
+        s *= scale
+        lo = int(pb.min()) + 1                                      # keys below lo are seen by every query
+        if lo < last:
+            after = np.arange(lo, last)[None, :] > pb[:, None]       # key after its query
+            s[:, :, lo:last][np.broadcast_to(after[:, None, :], (nb, group, last - lo))] = -np.inf
+        s -= s.max(axis=-1, keepdims=True)
+        np.exp(s, out=s)
+        s /= s.sum(axis=-1, keepdims=True)
+        out[b0:b0 + nb, heads] = (s.reshape(nb * group, last) @ vg[g][:last]).reshape(nb, group, hd)
+
+    work = [(b0, g) for b0 in range(0, n, block) for g in range(nkv)]
+    if threads <= 1 or len(work) == 1:
+        for b0, g in work:
+            piece(b0, g)
+    else:
+        from concurrent.futures import ThreadPoolExecutor
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(1), ThreadPoolExecutor(threads) as ex:
+            list(ex.map(lambda bg: piece(*bg), work))
     return out
 
 
@@ -204,28 +245,34 @@ def f16(x: np.ndarray) -> np.ndarray:
 
 
 def layer_forward(hp: Hyper, w: Dict[str, np.ndarray], h: np.ndarray, pos: np.ndarray,
-                  kv_write, kv_read) -> np.ndarray:
+                  kv_write, kv_read, threads: int = 1, mlp_rows: int = 8192) -> np.ndarray:
     """One decoder layer over the rows h [n, d] at positions pos.
 
     kv_write(k_f16 [n, dkv], v_f16 [n, dkv]) stores the rows' keys/values
     wherever the caller decides; kv_read(last) returns (K, V) float64 [last, dkv]
-    for positions 0..last-1 as stored.
+    for positions 0..last-1 as stored.  The feed-forward block acts on each row
+    alone; it runs mlp_rows rows at a time only to bound memory.
     """
     n = h.shape[0]
     x = rmsnorm(h, hp.rms_eps)
     q = (x @ w["wq"].T).reshape(n, hp.n_q_heads, hp.head_dim)
     k = (x @ w["wk"].T).reshape(n, hp.n_kv_heads, hp.head_dim)
     v = (x @ w["wv"].T).reshape(n, hp.n_kv_heads, hp.head_dim)
+    del x
     q = rope(q, pos, hp.rope_theta)
     k = rope(k, pos, hp.rope_theta)
     kv_write(f16(k.reshape(n, hp.dkv)), f16(v.reshape(n, hp.dkv)))
+    del k, v
     last = int(np.max(pos)) + 1
     K, V = kv_read(last)
     o = causal_gqa_attention(q, pos, K.reshape(last, hp.n_kv_heads, hp.head_dim),
-                             V.reshape(last, hp.n_kv_heads, hp.head_dim))
+                             V.reshape(last, hp.n_kv_heads, hp.head_dim), threads=threads)
+    del q, K, V
     h = h + o.reshape(n, hp.dq) @ w["wo"].T
-    y = rmsnorm(h, hp.rms_eps)
-    h = h + (silu(y @ w["wg"].T) * (y @ w["wu"].T)) @ w["wd"].T
+    del o
+    for r0 in range(0, n, mlp_rows):
+        y = rmsnorm(h[r0:r0 + mlp_rows], hp.rms_eps)
+        h[r0:r0 + mlp_rows] += (silu(y @ w["wg"].T) * (y @ w["wu"].T)) @ w["wd"].T
     return h
 
 
@@ -241,7 +288,7 @@ def output_logits(hp: Hyper, wts: Weights, h_last: np.ndarray, block: int = 1638
 
 # ----------------------------------------------------------------------------- clean prefill
 
-def clean_prefill(hp: Hyper, wts: Weights, tokens: np.ndarray):
+def clean_prefill(hp: Hyper, wts: Weights, tokens: np.ndarray, threads: int = 1, progress=None):
     """Never-evicted prefill of all tokens: per-layer fp16 K, V [S, dkv] and the logits."""
     tokens = np.asarray(tokens, dtype=np.int64)
     S = tokens.size
@@ -258,9 +305,11 @@ def clean_prefill(hp: Hyper, wts: Weights, tokens: np.ndarray):
         def read(last, K=K, V=V):
             return K[:last].astype(np.float64), V[:last].astype(np.float64)
 
-        h = layer_forward(hp, wts.layer(l), h, pos, write, read)
+        h = layer_forward(hp, wts.layer(l), h, pos, write, read, threads=threads)
         Ks.append(K)
         Vs.append(V)
+        if progress:
+            progress(l)
     logits = output_logits(hp, wts, h[-1])
     return Ks, Vs, logits
 
@@ -293,9 +342,10 @@ class OracleContext:
     dropped chunks over R_l / D_l; first_token returns (token, logits).
     """
 
-    def __init__(self, hyper, blob: np.ndarray):
+    def __init__(self, hyper, blob: np.ndarray, threads: int = 1):
         self.hp = Hyper(hyper)
-        self.wts = Weights(self.hp, blob)
+        self.threads = threads
+        self.wts = Weights(self.hp, blob, threads=threads)
         L, C = self.hp.n_layers, self.hp.chunk_tokens
         self.C = C
         self.tokens = np.zeros(0, np.int64)
@@ -328,7 +378,7 @@ class OracleContext:
 
     def prefill_context(self, tokens: np.ndarray):
         tokens = np.asarray(tokens, dtype=np.int64)
-        Ks, Vs, logits = clean_prefill(self.hp, self.wts, tokens)
+        Ks, Vs, logits = clean_prefill(self.hp, self.wts, tokens, threads=self.threads)
         self.tokens = tokens.copy()
         self.chunks = [[] for _ in range(self.hp.n_layers)]
         self.kv_state = np.zeros((self.hp.n_layers, 0), np.uint8)
@@ -410,7 +460,7 @@ class OracleContext:
                 self.w_state[l] = tgt
 
     # -- inference phase
-    def restore_and_prefill(self, prompt: np.ndarray):
+    def restore_and_prefill(self, prompt: np.ndarray, progress=None):
         hp, C = self.hp, self.C
         prompt = np.asarray(prompt, dtype=np.int64)
         N, P = self.n_ctx, prompt.size
@@ -461,9 +511,11 @@ class OracleContext:
                 V = np.concatenate([layer_chunks[c][1] for c in range(nch)])[:last]
                 return K.astype(np.float64), V.astype(np.float64)
 
-            h = layer_forward(hp, self.wts.layer(l), h, pos, write, read)
+            h = layer_forward(hp, self.wts.layer(l), h, pos, write, read, threads=self.threads)
             if l + 1 < hp.n_layers:
                 h = h[np.isin(pos, R[l + 1])]
+            if progress:
+                progress(l)
         self.h_last = h[-1].copy()           # R_l always ends with S-1
         self.tokens = all_tokens
         self.kv_state = np.zeros((hp.n_layers, (S + C - 1) // C), np.uint8)

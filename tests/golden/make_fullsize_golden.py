@@ -1,0 +1,144 @@
+"""Writes tests/golden/fullsize_<key>.npz: the CPU oracle's own evict -> restore
+-> first token on a workload at its full shape (all layers, full context and
+prompt, its own eviction plan).  Calls only oracle/ and the seeded input
+generator; nothing here comes from the HIP engine.
+
+For a workload with context ctx [N], prompt [P] and plan (kv_state, w_state):
+ 1. the never-evicted prefill of ctx + prompt (oracle clean_prefill) gives the
+    cached K/V of ctx and the never-evicted first-token logits;
+ 2. that K/V is the cached context; the plan is applied (swap / drop per unit,
+    backward-out order), then restore_and_prefill(prompt) recomputes every
+    dropped chunk over R_l / D_l and first_token gives the token and logits;
+ 3. the two restore invariants are checked at full size (recomputed K/V equals
+    the clean prefill's, logits equal the never-evicted ones) and recorded.
+
+Stored (npz, no pickled objects):
+  token, logits (float32 [V]) of the restore; margin (top-1 minus top-2 logit,
+  fp64) and top2 (the two indices); for one position per recomputed (layer,
+  chunk) -- every chunk holding a row of D_l -- its layer, chunk, position and
+  stored K and V rows (float16 [dkv], the oracle's stored halves); nR, nD per
+  layer; the invariant residues; and SHA-256 digests of the blob, the tokens
+  and the plan, so that a test can check it runs on the same inputs.
+
+    python tests/golden/make_fullsize_golden.py [--threads T] [keys...]
+"""
+
+import argparse
+import hashlib
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+import oracle as O  # noqa: E402
+from paper_2609_01338_amd import workloads as W  # noqa: E402
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def sha(*arrays) -> str:
+    h = hashlib.sha256()
+    for a in arrays:
+        h.update(np.ascontiguousarray(a).tobytes())
+    return h.hexdigest()
+
+
+def input_digests(w):
+    """Digests of what a run of workload w consumes (used by the GPU test too)."""
+    blob = W.make_blob(w)
+    ctx, prompt = W.make_tokens(w)
+    plan = W.make_plan(w)
+    return {"blob_sha256": sha(blob), "tokens_sha256": sha(ctx, prompt),
+            "plan_sha256": sha(plan.kv_state, plan.w_state)}, blob, ctx, prompt, plan
+
+
+def sample_rows(D, C, n_ctx):
+    """One position per (layer, chunk) that holds a row of D_l."""
+    out = []
+    for l, d in enumerate(D):
+        chunks = d // C
+        for c in np.unique(chunks):
+            rows = d[chunks == c]
+            out.append((l, int(c), int(rows[(l * 131 + int(c) * 71) % rows.size])))
+    return out
+
+
+def run(key, threads, log):
+    w = W.WORKLOADS[key]
+    m = w.model
+    C = m.chunk_tokens
+    t0 = time.time()
+    digests, blob, ctx, prompt, plan = input_digests(w)
+    hp = O.Hyper(m)
+    wts = O.Weights(hp, blob, threads=threads)
+    toks = np.concatenate([ctx, prompt]).astype(np.int64)
+    N = ctx.size
+
+    Kc, Vc, clean_logits = O.clean_prefill(hp, wts, toks, threads=threads,
+                                           progress=lambda l: log(f"{key} clean layer {l}"))
+    t_clean = time.time() - t0
+    ox = O.OracleContext(m, blob, threads=threads)
+    ox.set_context(ctx)
+    for l in range(m.n_layers):
+        for c in range(w.n_chunks):
+            p0, p1 = c * C, min(N, (c + 1) * C)
+            k = np.zeros((C, m.dkv), np.float16)
+            v = np.zeros((C, m.dkv), np.float16)
+            k[:p1 - p0], v[:p1 - p0] = Kc[l][p0:p1], Vc[l][p0:p1]
+            ox.import_kv(l, c, k, v)
+    ox.evict(plan.kv_state, plan.w_state)
+    t1 = time.time()
+    stats = ox.restore_and_prefill(prompt, progress=lambda l: log(f"{key} restore layer {l}"))
+    tok, logits = ox.first_token()
+    t_restore = time.time() - t1
+
+    R, D = O.restore_rows(plan.kv_state, N, prompt.size, C)
+    picks = sample_rows(D, C, N)
+    kv_diff = 0.0
+    ks, vs = [], []
+    for l, c, p in picks:
+        K, V = ox.read_kv(l, c)
+        ks.append(K[p - c * C])
+        vs.append(V[p - c * C])
+        kv_diff = max(kv_diff, float(np.abs(K[p - c * C].astype(np.float64) - Kc[l][p].astype(np.float64)).max()),
+                      float(np.abs(V[p - c * C].astype(np.float64) - Vc[l][p].astype(np.float64)).max()))
+    top = np.argsort(-logits, kind="stable")[:2]
+    out = dict(
+        token=np.int64(tok), logits=logits.astype(np.float32),
+        margin=np.float64(logits[top[0]] - logits[top[1]]), top2=top.astype(np.int64),
+        clean_token=np.int64(O.argmax_first(clean_logits)),
+        logits_vs_clean=np.float64(np.abs(logits - clean_logits).max()),
+        kv_vs_clean=np.float64(kv_diff),
+        kv_layer=np.array([a for a, _, _ in picks], np.int32),
+        kv_chunk=np.array([b for _, b, _ in picks], np.int32),
+        kv_pos=np.array([p for _, _, p in picks], np.int32),
+        k=np.array(ks, np.float16), v=np.array(vs, np.float16),
+        nR=np.array(stats["nR"], np.int32), nD=np.array(stats["nD"], np.int32),
+        seconds_clean=np.float64(t_clean), seconds_restore=np.float64(t_restore),
+        **{k: np.array(v) for k, v in digests.items()})
+    path = os.path.join(HERE, f"fullsize_{key}.npz")
+    np.savez_compressed(path, **out)
+    log(f"{key}: token {tok} (clean {out['clean_token']}), margin {out['margin']:.4e}, "
+        f"logits vs clean {out['logits_vs_clean']:.3e}, kv vs clean {kv_diff:.3e}, {len(picks)} K/V rows, "
+        f"clean {t_clean:.0f} s, restore {t_restore:.0f} s -> {path}")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--threads", type=int, default=len(os.sched_getaffinity(0)))
+    ap.add_argument("keys", nargs="*", default=["1b", "3b", "1p5b", "8b"])
+    a = ap.parse_args()
+
+    def log(msg):
+        print(time.strftime("%H:%M:%S"), msg, flush=True)
+
+    for key in a.keys:
+        run(key, a.threads, log)
+
+
+if __name__ == "__main__":
+    main()

@@ -272,6 +272,76 @@ def test_kv_head_permutation_invariance():
             assert np.array_equal(Ka[l][:, g * hd:(g + 1) * hd], Kb[l][:, ng * hd:(ng + 1) * hd])
 
 
+def test_layer_forward_closed_form():
+    """One decoder layer (Sec. 2.1, in the Llama-style reading) on a shape small
+    enough to work out by hand: d = 4, one query and one KV head of width 2,
+    d_ffn = 1, eps = 0, two rows at positions 0 and 1.  Every weight is 0 or 1,
+    which Q4_0 represents exactly (scale 1, codes 8 and 9).
+
+      Wq picks (x1, x2), Wk picks (x2, x1), Wv picks (x3, x4); Wo adds o to
+      (h1, h2); W_gate picks y1, W_up picks y3, W_down adds to h4.
+
+    With h0 = (1, 1, 1, 1) and h1 = (1, -1, 1, -1) both rows have RMS 1, so
+    x = h.  At position 1 the single rotary pair turns by 1 radian
+    (theta^0 = 1), so with c = cos 1, s = sin 1:
+      q1 = (c + s, s - c), k1 = (-c - s, c - s), and q0 = k0 = v0 = (1, 1),
+      v1 = (1, -1) (values are not rotated).
+    Keys are stored in half precision and read back, so k1 enters the scores
+    as half(k1).  Query 0 sees only key 0: o0 = v0.  Query 1 scores
+      z0 = q1 . k0 / sqrt 2,  z1 = q1 . half(k1) / sqrt 2,
+    a = softmax(z0, z1), o1 = a0 v0 + a1 v1.  Then h' = h + (o, 0, 0),
+    y = h' / rms(h'), and h'' = h' + (0, 0, 0, silu(y1) * y3).
+
+    A gate/up swap, a rotation of V, a missing rotation of K, the wrong score
+    scale, the second norm taken before the attention residual, or a dropped
+    residual each change these numbers."""
+    hp = O.Hyper(dict(n_layers=1, d_model=4, n_q_heads=1, n_kv_heads=1, head_dim=2, d_ffn=1,
+                      vocab=2, rope_theta=1e4, rms_eps=0.0, chunk_tokens=8))
+    w = {"wq": np.array([[1, 0, 0, 0], [0, 1, 0, 0]], float),
+         "wk": np.array([[0, 1, 0, 0], [1, 0, 0, 0]], float),
+         "wv": np.array([[0, 0, 1, 0], [0, 0, 0, 1]], float),
+         "wo": np.array([[1, 0], [0, 1], [0, 0], [0, 0]], float),
+         "wg": np.array([[1, 0, 0, 0]], float),
+         "wu": np.array([[0, 0, 1, 0]], float),
+         "wd": np.array([[0], [0], [0], [1]], float)}
+    for m in w.values():                                   # Q4_0-exact weights
+        assert np.array_equal(O.q4_0_decode(W.encode_q4_0(m.astype(np.float32)).reshape(-1), *m.shape), m)
+    h = np.array([[1.0, 1.0, 1.0, 1.0], [1.0, -1.0, 1.0, -1.0]])
+    store = {}
+
+    def write(k, v):
+        store["k"], store["v"] = k.copy(), v.copy()
+
+    def read(last):
+        return store["k"][:last].astype(np.float64), store["v"][:last].astype(np.float64)
+
+    out = O.layer_forward(hp, w, h, np.array([0, 1]), write, read)
+
+    c, s = math.cos(1.0), math.sin(1.0)
+    k1h = [float(np.float16(-c - s)), float(np.float16(c - s))]
+    assert store["k"].tolist() == [[1.0, 1.0], k1h]
+    assert store["v"].tolist() == [[1.0, 1.0], [1.0, -1.0]]
+    q1 = (c + s, s - c)
+    z0 = (q1[0] * 1.0 + q1[1] * 1.0) / math.sqrt(2.0)
+    z1 = (q1[0] * k1h[0] + q1[1] * k1h[1]) / math.sqrt(2.0)
+    e0, e1 = math.exp(z0 - max(z0, z1)), math.exp(z1 - max(z0, z1))
+    a0, a1 = e0 / (e0 + e1), e1 / (e0 + e1)
+    o = [(1.0, 1.0), (a0 + a1, a0 - a1)]
+
+    def silu(z):
+        return z / (1.0 + math.exp(-z))
+
+    expect = []
+    for r in range(2):
+        hr = [h[r, 0] + o[r][0], h[r, 1] + o[r][1], h[r, 2], h[r, 3]]
+        rms = math.sqrt(sum(t * t for t in hr) / 4.0)
+        y1, y3 = hr[0] / rms, hr[2] / rms
+        expect.append([hr[0], hr[1], hr[2], hr[3] + silu(y1) * y3])
+    assert np.allclose(out, expect, rtol=0, atol=1e-14)
+    # the hand numbers at a glance: row 0 is (2, 2, 1, 1 + silu(2/sqrt 2.5)/sqrt 2.5)
+    assert abs(out[0, 3] - (1.0 + silu(2 / math.sqrt(2.5)) / math.sqrt(2.5))) < 1e-14
+
+
 # ----------------------------------------------------------------------------- rows R_l / D_l
 
 def _brute_rows(state, N, P, C):
@@ -534,6 +604,37 @@ def test_kv_codec_error_bound_and_no_accumulation():
         ulp = np.spacing(np.abs(cur).astype(np.float16)).astype(np.float64)
         err = np.abs(cur.astype(np.float64) - x.astype(np.float64))
         assert np.all(err <= 0.5 * d + 0.5 * ulp + 1e-12), cycle
+
+
+def test_kv_codec_idempotent():
+    """Repeated compression and decompression does not accumulate error (Sec.
+    6).  On zero-centred groups of KV-like values (many scales), a value that
+    has been through the codec once comes back from a second cycle as the same
+    codes, the same (m, d) and the same halves, bit for bit.  A group far off
+    zero relative to its range can move once more: the half rounding of its
+    decoded maximum can shift the range by one ulp and so d by one half ulp;
+    from the second cycle on it is a fixed point."""
+    from oracle import kv_codec as Q
+    rng = np.random.default_rng(5)
+    n_groups = 4096
+    scale = np.repeat(rng.uniform(1e-3, 40.0, n_groups), 64)
+    x = (rng.standard_normal(64 * n_groups) * scale).astype(np.float16)
+    x[:64] = 1.5                                            # constant group
+    x[64:128] = np.where(rng.random(64) < 0.5, -2.0, 7.0)   # two-valued group
+    b1 = Q.compress(x)
+    y1 = Q.decompress(b1, x.size)
+    b2 = Q.compress(y1)
+    assert np.array_equal(b2, b1)
+    assert Q.decompress(b2, x.size).tobytes() == y1.tobytes()
+    # off-centre groups: a fixed point after the second cycle
+    offset = np.repeat(rng.uniform(-60.0, 60.0, n_groups), 64)
+    x = (rng.standard_normal(64 * n_groups) * scale + offset).astype(np.float16)
+    y1 = Q.decompress(Q.compress(x), x.size)
+    b2 = Q.compress(y1)
+    y2 = Q.decompress(b2, x.size)
+    assert np.array_equal(Q.compress(y2), b2)
+    moved = (y1.reshape(-1, 64) != y2.reshape(-1, 64)).any(axis=1)
+    assert moved.sum() <= n_groups // 1000
 
 
 def test_kv_codec_chunk_order_round_trip():
