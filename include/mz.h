@@ -257,6 +257,12 @@ typedef enum {
   MZ_STAGE_EXHAUSTED = 3       /* nothing resident is left to evict */
 } mz_evict_stage;
 
+/* How the threshold T and the KV_AND_W pairing are formed (see mz_plan_evict_size). */
+typedef enum {
+  MZ_SIZE_RULE_PAPER = 0,      /* T = N_W^total * floor(t_W / t_d), floor(t_W / t_d) chunks per weight layer */
+  MZ_SIZE_RULE_TOTAL = 1       /* T and the pairing from the path totals of the plan's exact costs */
+} mz_size_rule;
+
 typedef struct {
   int64_t bytes;               /* device bytes to release: KV slots and weight units */
   int32_t n_prompt;            /* expected prompt length of the coming restore (0 if unknown) */
@@ -264,6 +270,7 @@ typedef struct {
   double link_bytes_per_s;     /* host link rate */
   double recompute_flops_per_s;/* GPU recompute rate */
   int32_t kv_codec;            /* 1: full swapped chunks are priced at their compressed size */
+  int32_t rule;                /* mz_size_rule (0, the paper's, in a zeroed request) */
 } mz_evict_size_request;
 
 /* Plan the next increment of size-driven eviction from the current unit
@@ -274,17 +281,32 @@ typedef struct {
  * chunks: a chunk costs the growth of the restore's exact FLOP count when it
  * is dropped, / recompute rate; this depends on the rest of the plan).
  * Totals: link = every non-resident weight unit and swapped chunk, recompute
- * = FLOPs(plan) - FLOPs(nothing dropped).  Threshold T = the largest n such
- * that dropping the n front-most chunks (the last n of the backward-out
- * order, nothing else dropped) costs no more recompute time than reloading
- * all n_w_total weight layers over the link.  Units are taken one at a time,
- * rearmost first, until `bytes` are released:
+ * = FLOPs(plan) - FLOPs(nothing dropped).  N_KV and N_W count the resident
+ * chunks and evictable weight layers.  Threshold and pairing (req->rule):
+ *   MZ_SIZE_RULE_PAPER  the paper's (Sec. 4.3): t_W = one weight unit's link
+ *                       time, t_d = the recompute time of the front-most chunk
+ *                       (chunk 0 of layer 0, restored last in backward-out
+ *                       order) dropped alone -- its rows' layer-0 K/V
+ *                       projection; k = floor(t_W / t_d) and T = n_w_total * k;
+ *                       in KV_AND_W each weight layer is followed by k dropped
+ *                       chunks (the stage's progress is read from the unit
+ *                       counts: chunks taken = min(T, all chunks) - N_KV,
+ *                       weights taken = n_w_total - N_W; the next unit is a
+ *                       weight layer iff chunks taken >= k * weights taken);
+ *   MZ_SIZE_RULE_TOTAL  T = the largest n such that dropping the n front-most
+ *                       chunks (the last n of the backward-out order, nothing
+ *                       else dropped) costs no more recompute time than
+ *                       reloading all n_w_total weight layers; in KV_AND_W the
+ *                       next chunk is dropped if the recompute total with it
+ *                       does not pass the link total, else the next weight
+ *                       layer is evicted.
+ * Units are taken one at a time, rearmost first, until `bytes` are released:
  *   N_KV > T          KV_ONLY: the next chunk is dropped iff the recompute
  *                     total with it stays below the link total with it
  *                     swapped, else swapped;
- *   N_KV > 0, N_W > 0 KV_AND_W: the next chunk is dropped if the recompute
- *                     total with it does not pass the link total, else the
- *                     next weight layer is evicted;
+ *   N_KV > 0, N_W > 0 KV_AND_W: weight layers and dropped chunks, paired by
+ *                     the rule above (paper rule: also with N_W = 0 while
+ *                     the weight layers taken cover chunks not yet taken);
  *   N_KV > 0, N_W = 0 the KV_ONLY rule (no weight layer left to pair with);
  *   N_W > 0           W_ONLY: the next weight layer;
  *   otherwise         EXHAUSTED: stop short of `bytes`.
@@ -297,7 +319,7 @@ typedef struct {
  * entries) the stage that took each, *n_evicted their count.  info (NULL or
  * 8 doubles): released bytes, T, stage after the call, link total (s),
  * recompute total (s), N_KV, N_W, whether `bytes` was reached (1/0).
- * Errors: EINVAL (sizes, states, non-positive rates). */
+ * Errors: EINVAL (sizes, states, non-positive rates, unknown rule). */
 mz_status mz_plan_evict_size(const mz_model_cfg *cfg, int32_t n_ctx, const mz_evict_size_request *req,
                              uint8_t *kv_state, uint8_t *w_state, int32_t *order, int32_t *stage,
                              int32_t *n_evicted, double *info);

@@ -34,6 +34,7 @@ the workloads and agrees with the library decision for decision.
 
 from __future__ import annotations
 
+import math
 from fractions import Fraction
 from typing import List, Tuple
 
@@ -157,26 +158,52 @@ def plan_evict(L: int, d: int, dq: int, dkv: int, ff: int, chunk: int, n_ctx: in
 #
 # Paths: the link (weight layers, swapped chunks) plays the storage path of
 # the paper, the one weights are tied to; recompute (dropped chunks) plays
-# the in-memory decompression path, which takes KV chunks only.  A chunk's
-# recompute time is not a constant here, so every time below is a path
-# total: link = sum of link times of non-resident units, recompute = time of
-# the plan's extra restore work.  Stages, from the counts of resident units:
+# the in-memory decompression path, which takes KV chunks only.  Stages, from
+# the counts N_KV / N_W of resident evictable units (Alg. 1):
 #   N_KV > T              KV_ONLY   chunk to the path that stays behind
-#   N_KV > 0 and N_W > 0  KV_AND_W  chunk dropped if recompute stays within
-#                                   the link total, else a weight layer
+#   N_KV > 0 and N_W > 0  KV_AND_W  weight layers, each followed by the KV
+#                                   chunks its reload covers, all dropped
+#                                   (paper rule: also while the last weight
+#                                   layer taken still covers chunks)
 #   N_KV > 0, N_W = 0               the KV_ONLY rule (no weight left)
 #   N_W > 0               W_ONLY    a weight layer
 #   else                  EXHAUSTED (the paper's CompKV has no counterpart:
 #                                    nothing compressed stays on the device)
-# T = the largest n for which dropping the n front-most chunks costs no more
-# recompute than reloading all N_W^total weight layers; with a constant
-# per-chunk time t_d this is floor(N_W^total * t_W / t_d).
+#
+# Two rules for T and the KV_AND_W pairing:
+#   "paper" (default)  the paper's: with per-unit times t_d (one KV chunk on
+#                      the recompute path) and t_W (one weight layer over the
+#                      link), k = floor(t_W / t_d) chunks are dropped per
+#                      weight layer and T = N_W^total * k.  A chunk's
+#                      recompute time is not a constant on this engine; t_d
+#                      is the per-unit time of the front-most chunk (chunk 0
+#                      of layer 0, the unit restored last in backward-out
+#                      order) dropped alone: its rows' layer-0 K/V projection.
+#   "total"            every time a path total over the plan: T = the largest
+#                      n for which dropping the n front-most chunks costs no
+#                      more recompute than reloading all N_W^total weight
+#                      layers; in KV_AND_W a chunk is dropped while the
+#                      recompute total with it stays within the link total,
+#                      else the next weight layer goes.  With a constant t_d
+#                      this T is floor(N_W^total * t_W / t_d), which carries
+#                      the fractions of one layer's share into the next.
+# In KV_ONLY (both rules) the chunk goes to recompute iff the recompute total
+# with it stays below the link total with it swapped (the split in inverse
+# proportion to the two per-unit times, with the plan's exact costs).
 
 KV_ONLY, KV_AND_W, W_ONLY, EXHAUSTED = 0, 1, 2, 3
 
 
-def size_threshold(kv_seq, rec_time, n_w_total, t_w):
-    """T: front-most chunks (the tail of kv_seq) that the weight reload covers."""
+def paper_threshold(n_w_total, t_w, t_d):
+    """(T, k): k = floor(t_W / t_d) chunks per weight layer, T = N_W^total * k
+    (Sec. 4.3)."""
+    k = math.floor(Fraction(t_w) / Fraction(t_d)) if t_d > 0 else 0
+    return n_w_total * k, k
+
+
+def total_threshold(kv_seq, rec_time, n_w_total, t_w):
+    """T of the "total" rule: front-most chunks (the tail of kv_seq) whose
+    recompute fits the reload of all evictable weight layers."""
     T = 0
     budget = n_w_total * t_w
     for n in range(1, len(kv_seq) + 1):
@@ -187,14 +214,15 @@ def size_threshold(kv_seq, rec_time, n_w_total, t_w):
 
 
 def hybrid_swap_evict(kv_seq, w_seq, kv_state, w_state, T, request, kv_release, w_release, kv_link, w_link,
-                      rec_time):
+                      rec_time, k=None):
     """One evict(size) call.
 
     kv_seq / w_seq: every evictable chunk / weight id in eviction order;
     kv_state / w_state: dicts id -> RES / SWAP / DROP, updated in place;
     kv_link(id), w_link: link time of a unit; rec_time(set of dropped chunk
-    ids): recompute time of that plan's extra work.  Returns (evicted ids with
-    their stage, released bytes)."""
+    ids): recompute time of that plan's extra work.  k: chunks per weight
+    layer in KV_AND_W (the paper's rule); None for the "total" rule.  Returns
+    (evicted ids with their stage, released bytes)."""
     dropped = {u for u, s in kv_state.items() if s == DROP}
     link = sum((kv_link(u) for u, s in kv_state.items() if s == SWAP), Fraction(0))
     link += sum((w_link for s in w_state.values() if s != RES), Fraction(0))
@@ -203,11 +231,16 @@ def hybrid_swap_evict(kv_seq, w_seq, kv_state, w_state, T, request, kv_release, 
     def counts():
         return (sum(1 for u in kv_seq if kv_state[u] == RES), sum(1 for u in w_seq if w_state[u] == RES))
 
+    def owed(n_kv, n_w):
+        # paper rule: the weight layers taken in KV_AND_W still cover chunks
+        # not yet taken (the stage began at N_KV = min(T, all chunks))
+        return k is not None and min(T, len(kv_seq)) - n_kv < k * (len(w_seq) - n_w)
+
     def stage():
         n_kv, n_w = counts()
         if n_kv > T:
             return KV_ONLY
-        if n_kv > 0 and n_w > 0:
+        if n_kv > 0 and (n_w > 0 or owed(n_kv, n_w)):
             return KV_AND_W
         if n_kv > 0:
             return KV_ONLY
@@ -228,9 +261,15 @@ def hybrid_swap_evict(kv_seq, w_seq, kv_state, w_state, T, request, kv_release, 
         if st == W_ONLY:
             evict_weight(st)
             continue
+        if st == KV_AND_W and k is not None:
+            # a weight layer, then the k chunks its reload covers
+            n_kv, n_w = counts()
+            if n_w > 0 and not owed(n_kv, n_w):
+                evict_weight(st)
+                continue
         u = next(u for u in kv_seq if kv_state[u] == RES)
         rec_with = rec_time(dropped | {u})
-        if st == KV_AND_W and rec_with > link:
+        if st == KV_AND_W and k is None and rec_with > link:
             evict_weight(st)
             continue
         if st == KV_AND_W or rec_with < link + kv_link(u):
@@ -246,7 +285,8 @@ def hybrid_swap_evict(kv_seq, w_seq, kv_state, w_state, T, request, kv_release, 
 
 def plan_evict_size(L: int, d: int, dq: int, dkv: int, ff: int, chunk: int, n_ctx: int, n_prompt: int,
                     kv_state: np.ndarray, w_state: np.ndarray, request: int, n_w_total: int, link_rate: float,
-                    recompute_rate: float, slot_bytes: int, unit_bytes: int, codec: bool = False):
+                    recompute_rate: float, slot_bytes: int, unit_bytes: int, codec: bool = False,
+                    rule: str = "paper"):
     """The policy on this engine's restore: chunk (l, c) and weight layer l,
     link times from bytes, recompute time from the restore's FLOP count.
     Returns (kv_state, w_state, unit ids in order with stages, released, T)."""
@@ -267,11 +307,16 @@ def plan_evict_size(L: int, d: int, dq: int, dkv: int, ff: int, chunk: int, n_ct
     kv_link = lambda u: Fraction(slot_bytes // 2 + slot_bytes // 32
                                  if codec and (u[1] + 1) * chunk <= n_ctx else slot_bytes, bw)
     w_link = Fraction(unit_bytes, bw)
-    T = size_threshold(kv_seq, rec_time, n_w_total, w_link)
+    if rule == "paper":
+        T, k = paper_threshold(n_w_total, w_link, rec_time({(0, 0)}))
+    elif rule == "total":
+        T, k = total_threshold(kv_seq, rec_time, n_w_total, w_link), None
+    else:
+        raise ValueError(rule)
     kvs = {(l, c): int(kv_state[l, c]) for l in range(L) for c in range(nc)}
     ws = {l: int(w_state[l]) for l in range(L)}
     taken, released = hybrid_swap_evict(kv_seq, w_seq, kvs, ws, T, request, slot_bytes, unit_bytes, kv_link,
-                                        w_link, rec_time)
+                                        w_link, rec_time, k)
     out_kv = np.array([[kvs[(l, c)] for c in range(nc)] for l in range(L)], np.uint8)
     out_w = np.array([ws[l] for l in range(L)], np.uint8)
     ids = [u[0] * nc + u[1] if kind == "kv" else L * nc + u for (kind, u), _ in taken]

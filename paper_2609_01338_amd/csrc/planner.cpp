@@ -260,6 +260,8 @@ mz_status mz_plan_evict_size(const mz_model_cfg* cfg, int32_t n_ctx, const mz_ev
     if (req->n_w_total < 0 || req->n_w_total > c.n_layers) throw PlanError{MZ_EINVAL, "n_w_total out of range"};
     if (!(req->link_bytes_per_s >= 1.0 && req->recompute_flops_per_s >= 1.0))
       throw PlanError{MZ_EINVAL, "size-driven eviction needs positive rates"};
+    if (req->rule != MZ_SIZE_RULE_PAPER && req->rule != MZ_SIZE_RULE_TOTAL)
+      throw PlanError{MZ_EINVAL, "unknown size rule"};
     Work w(c, n_ctx, req->n_prompt);
     const int L = w.L, nc = w.nc, total = L * nc;
     for (int u = 0; u < total; ++u)
@@ -281,20 +283,33 @@ mz_status mz_plan_evict_size(const mz_model_cfg* cfg, int32_t n_ctx, const mz_ev
     for (int l = L - 1; l >= 0; --l)
       for (int k = nc - 1; k >= 0; --k) seq.push_back({l, k});
 
-    // threshold T: the front-most chunks whose recompute fits the reload of
-    // all evictable weight layers
-    const i128 budget = (i128)req->n_w_total * unit * RF;
-    auto tail_fits = [&](int n) {
+    // threshold T and the KV_AND_W pairing
+    const bool paper = req->rule == MZ_SIZE_RULE_PAPER;
+    int64_t T = 0, k_pair = 0;
+    if (paper) {
+      // k = floor(t_W / t_d): t_W = unit / BW, t_d = (front-most chunk's FLOPs) / RF
       Work t(c, n_ctx, req->n_prompt);
-      for (int i = total - n; i < total; ++i) t.drop(seq[i].first, seq[i].second);
-      return (i128)(t.flops() - F0) * BW <= budget;
-    };
-    int lo = 0, hi = total;   // the cost grows with n
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) / 2;
-      if (tail_fits(mid)) lo = mid; else hi = mid - 1;
+      t.drop(0, 0);
+      const i128 den = (i128)(t.flops() - F0) * BW;
+      const i128 kk = den > 0 ? (i128)unit * RF / den : 0;
+      k_pair = kk > (i128)INT32_MAX ? (int64_t)INT32_MAX : (int64_t)kk;
+      T = (int64_t)req->n_w_total * k_pair;
+    } else {
+      // the front-most chunks whose recompute fits the reload of all
+      // evictable weight layers
+      const i128 budget = (i128)req->n_w_total * unit * RF;
+      auto tail_fits = [&](int n) {
+        Work t(c, n_ctx, req->n_prompt);
+        for (int i = total - n; i < total; ++i) t.drop(seq[i].first, seq[i].second);
+        return (i128)(t.flops() - F0) * BW <= budget;
+      };
+      int lo = 0, hi = total;   // the cost grows with n
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) / 2;
+        if (tail_fits(mid)) lo = mid; else hi = mid - 1;
+      }
+      T = lo;
     }
-    const int T = lo;
 
     // current state
     int64_t link = 0;
@@ -321,9 +336,14 @@ mz_status mz_plan_evict_size(const mz_model_cfg* cfg, int32_t n_ctx, const mz_ev
       while (w_state[w_cur] != MZ_RES) --w_cur;
       return w_cur;
     };
+    // paper rule: the weight layers taken in KV_AND_W still cover chunks not
+    // yet taken (the stage began at N_KV = min(T, all chunks))
+    auto owed = [&]() {
+      return paper && std::min<int64_t>(T, total) - n_kv < k_pair * (int64_t)(req->n_w_total - n_w);
+    };
     auto stage_now = [&]() {
       if (n_kv > T) return (int)MZ_STAGE_KV_ONLY;
-      if (n_kv > 0 && n_w > 0) return (int)MZ_STAGE_KV_AND_W;
+      if (n_kv > 0 && (n_w > 0 || owed())) return (int)MZ_STAGE_KV_AND_W;
       if (n_kv > 0) return (int)MZ_STAGE_KV_ONLY;
       if (n_w > 0) return (int)MZ_STAGE_W_ONLY;
       return (int)MZ_STAGE_EXHAUSTED;
@@ -341,6 +361,14 @@ mz_status mz_plan_evict_size(const mz_model_cfg* cfg, int32_t n_ctx, const mz_ev
         --n_w;
         released += unit;
         unit_id = total + l;
+      } else if (st == MZ_STAGE_KV_AND_W && paper && n_w > 0 && !owed()) {
+        // the paper's pairing: a weight layer, then the k chunks its reload covers
+        const int l = next_w();
+        w_state[l] = MZ_DROP;
+        link += unit;
+        --n_w;
+        released += unit;
+        unit_id = total + l;
       } else {
         const auto lk = next_kv();
         const int l = lk.first, k = lk.second, old = w.md[k];
@@ -350,6 +378,8 @@ mz_status mz_plan_evict_size(const mz_model_cfg* cfg, int32_t n_ctx, const mz_ev
         bool drop, take_weight = false;
         if (st == MZ_STAGE_KV_ONLY) {
           drop = rec_with < (i128)(link + chunk_link_bytes(k)) * RF;
+        } else if (paper) {
+          drop = true;
         } else {
           drop = rec_with <= (i128)link * RF;
           take_weight = !drop;

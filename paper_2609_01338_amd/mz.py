@@ -53,9 +53,10 @@ class mz_evict_request(ctypes.Structure):
 class mz_evict_size_request(ctypes.Structure):
     _fields_ = [("bytes", ctypes.c_int64), ("n_prompt", ctypes.c_int32), ("n_w_total", ctypes.c_int32),
                 ("link_bytes_per_s", ctypes.c_double), ("recompute_flops_per_s", ctypes.c_double),
-                ("kv_codec", ctypes.c_int32)]
+                ("kv_codec", ctypes.c_int32), ("rule", ctypes.c_int32)]
 
 
+SIZE_RULES = {"paper": 0, "total": 1}
 STAGES = ("kv-only", "kv-and-w", "w-only", "exhausted")
 _INFO_KEYS = ("released", "T", "stage", "link_s", "recompute_s", "n_kv", "n_w", "reached")
 
@@ -202,11 +203,11 @@ def mz_evict(ctx, kv_state: np.ndarray, w_state: Optional[np.ndarray] = None,
 
 
 def mz_evict_size(ctx, nbytes: int, link_bytes_per_s: float, recompute_flops_per_s: float,
-                  n_w_total: int, n_prompt: int = 0) -> dict:
+                  n_w_total: int, n_prompt: int = 0, rule: str = "paper") -> dict:
     """Release at least nbytes of device memory by the hybrid-swap policy;
     returns {released, T, stage, link_s, recompute_s, n_kv, n_w, reached}."""
     req = mz_evict_size_request(int(nbytes), int(n_prompt), int(n_w_total), float(link_bytes_per_s),
-                                float(recompute_flops_per_s), 0)
+                                float(recompute_flops_per_s), 0, SIZE_RULES[rule])
     info = np.zeros(8, np.float64)
     _check(lib().mz_evict_size(ctx, ctypes.byref(req), info.ctypes.data), ctx)
     return _size_info(info)
@@ -269,7 +270,7 @@ def mz_plan_evict(cfg: mz_model_cfg, n_ctx: int, n_prompt: int, n_kv_evict: int,
 
 def mz_plan_evict_size(cfg: mz_model_cfg, n_ctx: int, kv_state: np.ndarray, w_state: np.ndarray, nbytes: int,
                        link_bytes_per_s: float, recompute_flops_per_s: float, n_w_total: int,
-                       n_prompt: int = 0, kv_codec: bool = False):
+                       n_prompt: int = 0, kv_codec: bool = False, rule: str = "paper"):
     """Next increment of size-driven eviction from the given states:
     (kv_state, w_state updated copies, evicted unit ids in order, their
     stages, info dict)."""
@@ -281,7 +282,7 @@ def mz_plan_evict_size(cfg: mz_model_cfg, n_ctx: int, kv_state: np.ndarray, w_st
     n = ctypes.c_int32()
     info = np.zeros(8, np.float64)
     req = mz_evict_size_request(int(nbytes), int(n_prompt), int(n_w_total), float(link_bytes_per_s),
-                                float(recompute_flops_per_s), int(kv_codec))
+                                float(recompute_flops_per_s), int(kv_codec), SIZE_RULES[rule])
     _check(lib().mz_plan_evict_size(ctypes.byref(cfg), n_ctx, ctypes.byref(req), kv.ctypes.data, ws.ctypes.data,
                                     order.ctypes.data, stage.ctypes.data, ctypes.byref(n), info.ctypes.data),
            None)
