@@ -391,6 +391,27 @@ mz_status mz_q4_gemm_split(const void *x_f16, int32_t m, int32_t n_pad, int32_t 
 /* Workspace bytes of mz_q4_gemm_split (-1 for invalid arguments). */
 int64_t mz_q4_gemm_split_workspace_bytes(int32_t m, int32_t n_pad, int32_t n_split);
 
+/* Size of the fixed device array that holds the partials of
+ * mz_q4_gemm_split_noalloc: 32 MiB on each GPU the library runs it on. */
+#define MZ_NOALLOC_SCRATCH_BYTES (32 * 1024 * 1024)
+
+/* mz_q4_gemm_split for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, hosts that forbid allocation.  The
+ * same kernels and the same result bits as mz_q4_gemm_split with n_split, but
+ * the fp32 partials go to a fixed device array of MZ_NOALLOC_SCRATCH_BYTES
+ * that the library holds on each GPU it has run this call on, until the
+ * process ends; the call allocates nothing.  The array's address on a device
+ * is looked up on the first call there, with that device current.  stream
+ * (NULL = the default stream) must belong to the current device.  Every call
+ * on one GPU shares that GPU's array: calls that overlap on one GPU race
+ * (serialize them, e.g. on one stream).  Errors: EINVAL as mz_q4_gemm_split,
+ * and when n_split * m * n_pad * 4 bytes exceed MZ_NOALLOC_SCRATCH_BYTES or
+ * the stream is on another device (checked before any GPU work); EHIP when no
+ * device is usable or the array's address cannot be found. */
+mz_status mz_q4_gemm_split_noalloc(const void *x_f16, int32_t m, int32_t n_pad, int32_t k,
+                                   const void *w_packed, int32_t epilogue, void *y, int32_t n_split,
+                                   void *stream);
+
 /* The split count the restore uses for this shape with workspace_bytes of
  * workspace: about two workgroups per compute unit, at least 4 K steps per
  * split, at most 32 splits; 1 when the tile grid already fills the GPU. */

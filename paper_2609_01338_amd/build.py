@@ -12,7 +12,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libmz.so")
-SOURCES = ["gemm_q4.hip", "attention.hip", "elementwise.hip", "probe.hip", "codec.hip", "mz_runtime.cpp", "planner.cpp"]
+SOURCES = ["gemm_q4.hip", "attention.hip", "elementwise.hip", "probe.hip", "codec.hip", "noalloc.hip", "mz_runtime.cpp",
+           "planner.cpp"]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # Packed FP32 instructions are kept out of the generated code.

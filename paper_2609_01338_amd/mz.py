@@ -114,6 +114,7 @@ def lib() -> ctypes.CDLL:
         "mz_kv_decompress": ([vp, i64, vp, vp], i32),
         "mz_q4_gemm_split": ([vp, i32, i32, i32, vp, i32, vp, i32, vp, i64, vp], i32),
         "mz_q4_gemm_split_workspace_bytes": ([i32, i32, i32], i64),
+        "mz_q4_gemm_split_noalloc": ([vp, i32, i32, i32, vp, i32, vp, i32, vp], i32),
         "mz_q4_gemm_auto_splits": ([i32, i32, i32, i64], i32),
         "mz_attention_split": ([vp, vp, i32, i32, vp, vp, i32, i32, i32, i32, i32, i32, vp, i64, vp, vp], i32),
         "mz_attention_split_workspace_bytes": ([i32, i32, i32, i32], i64),
@@ -356,6 +357,14 @@ def mz_q4_gemm_split(x_ptr: int, m: int, n_pad: int, k: int, w_ptr: int, epilogu
                      n_split: int, ws_ptr: int, ws_bytes: int, stream: Optional[int] = None) -> None:
     _check(lib().mz_q4_gemm_split(x_ptr, m, n_pad, k, w_ptr, epilogue, y_ptr, n_split, ws_ptr, ws_bytes, stream),
            None)
+
+
+NOALLOC_SCRATCH_BYTES = 32 * 1024 * 1024
+
+
+def mz_q4_gemm_split_noalloc(x_ptr: int, m: int, n_pad: int, k: int, w_ptr: int, epilogue: int, y_ptr: int,
+                             n_split: int, stream: Optional[int] = None) -> None:
+    _check(lib().mz_q4_gemm_split_noalloc(x_ptr, m, n_pad, k, w_ptr, epilogue, y_ptr, n_split, stream), None)
 
 
 def mz_q4_gemm_split_workspace_bytes(m: int, n_pad: int, n_split: int) -> int:
