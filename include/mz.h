@@ -373,6 +373,45 @@ mz_status mz_q4_gemm_queued(const void *x_f16, int32_t m, int32_t n_pad, int32_t
                             const void *w_packed, int32_t epilogue, void *y, int32_t *work_queues,
                             void *stream);
 
+/* Optional parts of a projection launch (mz_q4_gemm_ex), as the restore
+ * issues it; a zeroed struct means none of them. */
+typedef struct {
+  const int32_t *a_rows;     /* device int32 [m]: output row r is computed from X row a_rows[r]
+                                (NULL: from X row r) */
+  int32_t *work_queues;      /* device, 16 int32 zero on entry and left zero, as in mz_q4_gemm_queued
+                                (NULL: one workgroup per tile); epilogues 0-2 only */
+  void *workspace;           /* device scratch, not shared with launches in flight: the rows after the
+                                last whole 256-row tile run split over K in it (as mz_q4_gemm_split)
+                                when their tiles alone would leave most compute units idle (NULL:
+                                they run as 64-row tiles) */
+  int64_t workspace_bytes;
+  /* rotary epilogues (Sec. 2.1 prefill, rotate-half pairs i, i + head_dim/2 of every head) */
+  const int32_t *pos;        /* device int32 [m]: position of output row r */
+  const void *rope_cs;       /* device float2 [max(pos) + 1][head_dim / 2]: (cos, sin) of
+                                pos * rope_theta^(-2i / head_dim) */
+  const int64_t *kv_off;     /* epilogue 5, device int64 [m]: byte offset in slab of row r's key row
+                                in its chunk slot, or -1: the row writes nothing */
+  void *slab;                /* epilogue 5, device: chunk slots laid out as in mz_attention */
+  int32_t head_dim;          /* 32, 64 or 128 */
+  int32_t n_valid;           /* epilogue 4: query columns (y row stride); 5: 2 * key columns */
+  int32_t chunk_tokens;      /* epilogue 5: tokens per slot, a power of two */
+} mz_q4_gemm_args;
+
+/* mz_q4_gemm with the optional parts of mz_q4_gemm_args (args NULL: none),
+ * the launch the restore makes for each projection of the prefill that
+ * recomputes dropped chunks (paper Sec. 2.1 and 4.2).  Epilogues 0-2 as in
+ * mz_q4_gemm; 4: y f16 [m][n_valid] = the rotated queries; 5: columns
+ * [0, n_valid/2) are keys, rotated and stored as f16 at slab + kv_off[r],
+ * columns [n_valid/2, n_valid) values, stored as f16 into the same slot's
+ * V^T half at its position's column (y is not used).  Results equal
+ * mz_q4_gemm's bit for bit where no row runs split over K, and to the order
+ * of the fp32 sums where one does.  The caller keeps pos, kv_off and a_rows
+ * inside their tables and buffers.  Errors: EINVAL for the shapes of
+ * mz_q4_gemm, a bad epilogue, missing pointers an epilogue needs, n_valid
+ * outside 1..n_pad, head_dim not 32/64/128, chunk_tokens not a power of two. */
+mz_status mz_q4_gemm_ex(const void *x_f16, int32_t m, int32_t n_pad, int32_t k, const void *w_packed,
+                        int32_t epilogue, const mz_q4_gemm_args *args, void *y, void *stream);
+
 /* Split-K form of mz_q4_gemm for few rows (the short requests of the
  * paper's evaluation, Sec. 6, and every decode step): a grid of 256-column
  * tiles alone leaves most of the GPU idle there.  The k / 64 steps are cut

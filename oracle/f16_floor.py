@@ -1,4 +1,4 @@
-"""Rounding floor of half-precision GEMM operands over the depth of the model.
+"""Rounding floor of reduced-precision GEMM operands over the depth of the model.
 
 TEST INFRASTRUCTURE ONLY (like the rest of oracle/): it sets a tolerance, it is
 never called by the product path, and it shares no code with it.
@@ -11,20 +11,27 @@ output), with exact accumulation -- cannot stay closer to that reference than
 the rounding itself allows, and after many layers the rounding of one layer
 has moved every later layer's input.  This module runs the oracle's layer
 (paper Sec. 2.1: the prefill that produces each layer's keys and values) over
-a token prefix twice, once in fp64 and once with those half-precision operand
-roundings, and reports how far apart the stored (half) keys and values end up
-at each layer.  Keys and values are stored as half in both runs, as the
-KV cache is.
+a token prefix twice, once in fp64 and once with operand roundings, and
+reports how far apart the stored (half) keys and values end up at each layer.
+Keys and values are stored as half in both runs, as the KV cache is.
 
-Parity unpinned beyond its special case: with every rounding switched off it
-reproduces the fp64 oracle's keys and values bit for bit (pinned in
-tests/test_oracle_pins.py); the size of the floor is a measurement, not a
+Which operands are rounded, and to what, is a Rounding: weights (the
+dequantized matrices), activations (every other product input), and the
+attention probabilities that multiply V, each "exact", "half" or "bf16"
+(round to nearest even).  The half-operand floor is weights and activations
+in half, probabilities exact.
+
+Parity unpinned beyond its special cases: with every rounding switched off it
+reproduces the fp64 oracle's keys and values bit for bit, and with weights
+and activations in half it equals the half-operand floor (both pinned in
+tests/test_oracle_pins.py); the size of a floor is a measurement, not a
 closed form.
 """
 
 from __future__ import annotations
 
-from typing import Callable, List, Tuple
+import math
+from typing import Callable, List, NamedTuple, Tuple
 
 import numpy as np
 
@@ -35,16 +42,61 @@ def _half(a: np.ndarray) -> np.ndarray:
     return np.asarray(a, dtype=np.float64).astype(np.float16).astype(np.float64)
 
 
+def _bf16(a: np.ndarray) -> np.ndarray:
+    """Round to the nearest bfloat16 (8 significant bits), ties to even, via
+    the top 16 bits of the float32 that holds the value after rounding."""
+    x = np.asarray(a, dtype=np.float64).astype(np.float32)
+    b = x.view(np.uint32).astype(np.uint64)
+    b = (b + 0x7FFF + ((b >> 16) & 1)) & 0xFFFF0000
+    return b.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
 def _ident(a: np.ndarray) -> np.ndarray:
     return a
 
 
-def prefix_kv(hp: Hyper, wts: Weights, tokens: np.ndarray, half_operands: bool,
+ROUND = {"exact": _ident, "half": _half, "bf16": _bf16}
+
+
+class Rounding(NamedTuple):
+    weights: str = "exact"
+    acts: str = "exact"
+    probs: str = "exact"
+
+
+HALF_OPERANDS = Rounding("half", "half", "exact")
+EXACT = Rounding()
+
+
+def _attention_rounded_probs(q, pos, K, V, rp):
+    """causal_gqa_attention with the softmax probabilities rounded by rp
+    before they multiply V (queries one at a time; for short prefixes)."""
+    n, nq, hd = q.shape
+    nkv = K.shape[1]
+    group = nq // nkv
+    out = np.empty_like(q)
+    for i in range(n):
+        last = int(pos[i]) + 1
+        for h in range(nq):
+            g = h // group
+            s = K[:last, g] @ q[i, h] / math.sqrt(hd)
+            p = np.exp(s - s.max())
+            p = rp(p / p.sum())
+            out[i, h] = p @ V[:last, g]
+    return out
+
+
+def prefix_kv(hp: Hyper, wts: Weights, tokens: np.ndarray, rounding,
               progress: Callable[[int], None] = None) -> Tuple[List[np.ndarray], List[np.ndarray], np.ndarray]:
     """Keys and values (float64 of the stored half values, [L][n, dkv]) of a
-    prefill over `tokens`, and the final hidden state of the last row.  With
-    half_operands, every matrix-product operand is rounded to half first."""
-    r = _half if half_operands else _ident
+    prefill over `tokens`, and the final hidden state of the last row, with
+    the operands rounded as `rounding` says (True: the half-operand floor's
+    rounding; False: none)."""
+    if rounding is True:
+        rounding = HALF_OPERANDS
+    elif rounding is False:
+        rounding = EXACT
+    rw, ra, rp = ROUND[rounding.weights], ROUND[rounding.acts], ROUND[rounding.probs]
     tokens = np.asarray(tokens, dtype=np.int64)
     n = tokens.size
     pos = np.arange(n)
@@ -52,8 +104,8 @@ def prefix_kv(hp: Hyper, wts: Weights, tokens: np.ndarray, half_operands: bool,
     Ks, Vs = [], []
     for l in range(hp.n_layers):
         w = wts.layer(l)
-        wq, wk, wv, wo, wg, wu, wd = (r(w[k]) for k in ("wq", "wk", "wv", "wo", "wg", "wu", "wd"))
-        x = r(rmsnorm(h, hp.rms_eps))
+        wq, wk, wv, wo, wg, wu, wd = (rw(w[k]) for k in ("wq", "wk", "wv", "wo", "wg", "wu", "wd"))
+        x = ra(rmsnorm(h, hp.rms_eps))
         q = rope((x @ wq.T).reshape(n, hp.n_q_heads, hp.head_dim), pos, hp.rope_theta)
         k = rope((x @ wk.T).reshape(n, hp.n_kv_heads, hp.head_dim), pos, hp.rope_theta)
         v = (x @ wv.T).reshape(n, hp.n_kv_heads, hp.head_dim)
@@ -61,14 +113,24 @@ def prefix_kv(hp: Hyper, wts: Weights, tokens: np.ndarray, half_operands: bool,
         V = _half(v.reshape(n, hp.dkv))
         Ks.append(K)
         Vs.append(V)
-        o = causal_gqa_attention(r(q), pos, K.reshape(n, hp.n_kv_heads, hp.head_dim),
-                                 V.reshape(n, hp.n_kv_heads, hp.head_dim))
-        h = h + r(o.reshape(n, hp.dq)) @ wo.T
-        y = r(rmsnorm(h, hp.rms_eps))
-        h = h + r(silu(y @ wg.T) * (y @ wu.T)) @ wd.T
+        Kh = K.reshape(n, hp.n_kv_heads, hp.head_dim)
+        Vh = V.reshape(n, hp.n_kv_heads, hp.head_dim)
+        if rounding.probs == "exact":
+            o = causal_gqa_attention(ra(q), pos, Kh, Vh)
+        else:
+            o = _attention_rounded_probs(ra(q), pos, Kh, Vh, rp)
+        h = h + ra(o.reshape(n, hp.dq)) @ wo.T
+        y = ra(rmsnorm(h, hp.rms_eps))
+        h = h + ra(silu(y @ wg.T) * (y @ wu.T)) @ wd.T
         if progress:
             progress(l)
     return Ks, Vs, h[-1]
+
+
+def kv_distance(A: Tuple[List[np.ndarray], List[np.ndarray]], B) -> np.ndarray:
+    """Per layer: max |K, V of A - K, V of B|."""
+    return np.array([max(np.abs(a - b).max(), np.abs(c - d).max())
+                     for a, b, c, d in zip(A[0], B[0], A[1], B[1])])
 
 
 def f16_operand_floor(hp: Hyper, wts: Weights, tokens: np.ndarray,
@@ -76,4 +138,4 @@ def f16_operand_floor(hp: Hyper, wts: Weights, tokens: np.ndarray,
     """Per layer: max |K, V (half operands) - K, V (fp64)| over the prefix."""
     K0, V0, _ = prefix_kv(hp, wts, tokens, False, progress and (lambda l: progress("fp64", l)))
     K1, V1, _ = prefix_kv(hp, wts, tokens, True, progress and (lambda l: progress("half", l)))
-    return np.array([max(np.abs(a - b).max(), np.abs(c - d).max()) for a, b, c, d in zip(K1, K0, V1, V0)])
+    return kv_distance((K1, V1), (K0, V0))

@@ -1746,6 +1746,45 @@ mz_status mz_q4_gemm_queued(const void* x_f16, int32_t m, int32_t n_pad, int32_t
   return gemm_entry(x_f16, m, n_pad, k, w_packed, epilogue, y, work_queues, stream);
 }
 
+mz_status mz_q4_gemm_ex(const void* x_f16, int32_t m, int32_t n_pad, int32_t k, const void* w_packed,
+                        int32_t epilogue, const mz_q4_gemm_args* args, void* y, void* stream) {
+  return guarded(nullptr, [&] {
+    const mz_q4_gemm_args a = args ? *args : mz_q4_gemm_args{};
+    if (!x_f16 || !w_packed) fail(MZ_EINVAL, "NULL pointer");
+    if (m < 1 || n_pad < 1 || k < 1) fail(MZ_EINVAL, "sizes must be positive");
+    if (n_pad % mzk::kGemmTileN) fail(MZ_EINVAL, "n_pad must be a multiple of %d", mzk::kGemmTileN);
+    if (k % mzk::kGemmTileK) fail(MZ_EINVAL, "k must be a multiple of %d", mzk::kGemmTileK);
+    if (a.workspace_bytes < 0 || (a.workspace_bytes > 0 && !a.workspace)) fail(MZ_EINVAL, "bad workspace");
+    hipStream_t s = (hipStream_t)stream;
+    if (epilogue >= 0 && epilogue <= 2) {
+      if (!y) fail(MZ_EINVAL, "NULL y");
+      mzk::launch_gemm_q4(x_f16, m, n_pad, k, w_packed, epilogue, y, s, a.a_rows, a.work_queues, a.workspace,
+                          a.workspace_bytes);
+    } else if (epilogue == mzk::kEpiRopeQ || epilogue == mzk::kEpiRopeKV) {
+      if (!a.pos || !a.rope_cs) fail(MZ_EINVAL, "the rotary epilogues need pos and rope_cs");
+      if (epilogue == mzk::kEpiRopeQ && !y) fail(MZ_EINVAL, "NULL y");
+      if (epilogue == mzk::kEpiRopeKV && (!a.kv_off || !a.slab)) fail(MZ_EINVAL, "epilogue 5 needs kv_off and slab");
+      if (!mzk::gemm_rope_fusable(a.head_dim, epilogue == mzk::kEpiRopeKV ? a.chunk_tokens : 1))
+        fail(MZ_EINVAL, "head_dim must be 32, 64 or 128 and chunk_tokens a power of two");
+      if (a.n_valid < 1 || a.n_valid > n_pad || a.n_valid % (epilogue == mzk::kEpiRopeKV ? 2 * a.head_dim : a.head_dim))
+        fail(MZ_EINVAL, "n_valid must be whole heads within n_pad");
+      mzk::GemmRope ea;
+      ea.pos = a.pos;
+      ea.kv_off = a.kv_off;
+      ea.rope_cs = reinterpret_cast<const float2*>(a.rope_cs);
+      ea.slab = reinterpret_cast<uint8_t*>(a.slab);
+      ea.hd = a.head_dim;
+      ea.n_valid = a.n_valid;
+      ea.C = epilogue == mzk::kEpiRopeKV ? a.chunk_tokens : 1;
+      mzk::launch_gemm_q4_rope(x_f16, m, n_pad, k, w_packed, epilogue, ea, y, s, a.a_rows, nullptr, a.workspace,
+                               a.workspace_bytes);
+    } else {
+      fail(MZ_EINVAL, "bad epilogue");
+    }
+    HIPCHK(hipGetLastError());
+  });
+}
+
 int64_t mz_q4_gemm_split_workspace_bytes(int32_t m, int32_t n_pad, int32_t n_split) {
   if (m < 1 || n_pad < 1 || n_split < 1) return -1;
   return mzk::gemm_splitk_ws_bytes(m, n_pad, n_split);

@@ -56,6 +56,13 @@ class mz_evict_size_request(ctypes.Structure):
                 ("kv_codec", ctypes.c_int32), ("rule", ctypes.c_int32)]
 
 
+class mz_q4_gemm_args(ctypes.Structure):
+    _fields_ = [("a_rows", ctypes.c_void_p), ("work_queues", ctypes.c_void_p), ("workspace", ctypes.c_void_p),
+                ("workspace_bytes", ctypes.c_int64), ("pos", ctypes.c_void_p), ("rope_cs", ctypes.c_void_p),
+                ("kv_off", ctypes.c_void_p), ("slab", ctypes.c_void_p), ("head_dim", ctypes.c_int32),
+                ("n_valid", ctypes.c_int32), ("chunk_tokens", ctypes.c_int32)]
+
+
 SIZE_RULES = {"paper": 0, "total": 1}
 STAGES = ("kv-only", "kv-and-w", "w-only", "exhausted")
 _INFO_KEYS = ("released", "T", "stage", "link_s", "recompute_s", "n_kv", "n_w", "reached")
@@ -107,6 +114,7 @@ def lib() -> ctypes.CDLL:
         "mz_attention": ([vp, vp, i32, vp, vp, i32, i32, i32, i32, i32, vp, vp], i32),
         "mz_attention_queued": ([vp, vp, i32, vp, vp, i32, i32, i32, i32, i32, vp, vp, vp], i32),
         "mz_q4_gemm_queued": ([vp, i32, i32, i32, vp, i32, vp, vp, vp], i32),
+        "mz_q4_gemm_ex": ([vp, i32, i32, i32, vp, i32, ctypes.POINTER(mz_q4_gemm_args), vp, vp], i32),
         "mz_rmsnorm": ([vp, i32, i32, ctypes.c_float, vp, vp], i32),
         "mz_probe_ceilings": ([i32, ctypes.c_char_p, sz], i32),
         "mz_plan_evict": ([ctypes.POINTER(mz_model_cfg), ctypes.POINTER(mz_evict_request), vp, vp, vp], i32),
@@ -337,6 +345,16 @@ def mz_q4_gemm(x_ptr: int, m: int, n_pad: int, k: int, w_ptr: int, epilogue: int
 def mz_q4_gemm_queued(x_ptr: int, m: int, n_pad: int, k: int, w_ptr: int, epilogue: int, y_ptr: int,
                       queues_ptr: int, stream: Optional[int] = None) -> None:
     _check(lib().mz_q4_gemm_queued(x_ptr, m, n_pad, k, w_ptr, epilogue, y_ptr, queues_ptr, stream), None)
+
+
+def mz_q4_gemm_ex(x_ptr: int, m: int, n_pad: int, k: int, w_ptr: int, epilogue: int, y_ptr: Optional[int],
+                  stream: Optional[int] = None, a_rows: int = 0, work_queues: int = 0, workspace: int = 0,
+                  workspace_bytes: int = 0, pos: int = 0, rope_cs: int = 0, kv_off: int = 0, slab: int = 0,
+                  head_dim: int = 0, n_valid: int = 0, chunk_tokens: int = 0) -> None:
+    """Device pointers as integers (0: absent)."""
+    a = mz_q4_gemm_args(a_rows or None, work_queues or None, workspace or None, workspace_bytes, pos or None,
+                        rope_cs or None, kv_off or None, slab or None, head_dim, n_valid, chunk_tokens)
+    _check(lib().mz_q4_gemm_ex(x_ptr, m, n_pad, k, w_ptr, epilogue, ctypes.byref(a), y_ptr or None, stream), None)
 
 
 def mz_attention(q_ptr: int, qpos_ptr: int, m: int, slab_ptr: int, table_ptr: int, n_table: int,

@@ -151,17 +151,154 @@ def _layer_gemms(key):
             (M, m.d_ffn, m.d_model, 2), (M, m.d_model, ffp, 1)]
 
 
+def _tile_rows(M, tile, seed):
+    """One row in every `tile`-row tile (at a seeded offset inside it), the
+    first and last rows, and both sides of the last whole 256-row tile."""
+    rng = np.random.default_rng(seed)
+    starts = np.arange(0, M, tile)
+    rows = np.minimum(starts + rng.integers(0, tile, starts.size), M - 1)
+    edge = [r for r in (M // 256 * 256 - 1, M // 256 * 256) if 0 <= r < M]
+    return np.unique(np.concatenate([rows, [0, M - 1], edge])).astype(np.int64)
+
+
 @pytest.mark.parametrize("key", ["tiny", "1b", "3b", "1p5b", "8b"])
 def test_gemm_full_layer_shapes(key):
     """Every projection of the workload at its full row count (the launch the
-    benchmark times), checked on sampled rows including the ragged tail and
-    both sides of the row where whole 256-row tiles end (a ragged remainder
-    may run as 64-row tiles in a second launch)."""
+    benchmark times), checked on one row in every 64-row tile (so in every
+    256- and 64-row tile of either launch form) including the ragged tail and
+    both sides of the row where whole 256-row tiles end."""
     for i, (M, N, K, epi) in enumerate(_layer_gemms(key)):
-        rng = np.random.default_rng(i)
-        edge = [r for r in (M // 256 * 256 - 1, M // 256 * 256) if 0 <= r < M]
-        rows = np.unique(np.concatenate([rng.choice(M, min(M, 24), replace=False), [0, M - 1], edge]))
-        _gemm_case(M, N, K, epi, seed=100 + i, sample_rows=rows, n_split="queued")
+        _gemm_case(M, N, K, epi, seed=100 + i, sample_rows=_tile_rows(M, 64, i), n_split="queued")
+
+
+def _rope_table(max_pos, hd, theta):
+    """(cos, sin) of p * theta^(-2i/hd) in fp64, stored as fp32 pairs [max_pos][hd/2]."""
+    i = np.arange(hd // 2, dtype=np.float64)
+    ang = np.arange(max_pos, dtype=np.float64)[:, None] * theta ** (-2.0 * i / hd)[None, :]
+    return np.stack([np.cos(ang), np.sin(ang)], axis=-1).astype(np.float32)
+
+
+@pytest.mark.parametrize("key", ["1b", "3b", "1p5b", "8b"])
+def test_gemm_restore_launches(key):
+    """The projections as the restore launches them (mz_q4_gemm_ex), at the
+    workload's full row count: with the runtime's 64 MiB workspace, so the
+    rows after the last whole 256-row tile run split over K where their tiles
+    alone would leave the chip idle; through a row list (a ragged subset of the
+    activation rows, as the restore passes R_l / D_l); with the work queues;
+    and with the rotary epilogues (queries to f16; keys and values into chunk
+    slots).  Against the exact product (and the oracle's rotary embedding) on
+    one row in every 64-row tile and both sides of the last whole 256-row
+    tile; rows in whole 256-row tiles bit-equal to mz_q4_gemm's."""
+    torch = torch_cuda()
+    w = W.WORKLOADS[key]
+    m = w.model
+    S = w.n_ctx + w.n_prompt
+    d, hd, C = m.d_model, m.head_dim, m.chunk_tokens
+    rng = np.random.default_rng(17)
+    gen = torch.Generator(device="cuda").manual_seed(17)
+    X = torch.randn(S, d, device="cuda", generator=gen).to(torch.float16)
+    Xh = X.float().cpu().numpy().astype(np.float64)
+    ws_bytes = 64 << 20
+    ws = torch.full((ws_bytes // 4,), float("nan"), device="cuda")
+    queues = torch.zeros(16, device="cuda", dtype=torch.int32)
+    cs = torch.from_numpy(_rope_table(S, hd, m.rope_theta)).cuda()
+    # a ragged row list: every row of a random half of the chunks, then the prompt
+    keep = rng.random(w.n_chunks) < 0.5
+    sub = np.array([p for p in range(S) if p >= w.n_ctx or keep[p // C]], np.int32)
+    d_sub = torch.from_numpy(sub).cuda()
+    for rows_name, M, arow, pos_np in (("all", S, None, np.arange(S, dtype=np.int32)), ("list", sub.size, sub, sub)):
+        d_pos = torch.from_numpy(np.ascontiguousarray(pos_np)).cuda()
+        xr = Xh if arow is None else Xh[arow]
+        ar_ptr = 0 if arow is None else d_sub.data_ptr()
+        check = _tile_rows(M, 64, M)
+        full = M // 256 * 256
+        # queries, rotated
+        raw = W.encode_q4_0((rng.standard_normal((m.dq, d)) * 0.02).astype(np.float32))
+        Wm = O.q4_0_decode(raw.reshape(-1), m.dq, d)
+        n_pad = (m.dq + 255) // 256 * 256
+        wdev = torch.from_numpy(mz.mz_q4_gemm_pack(raw, m.dq, d)).cuda()
+        yq = torch.full((M, m.dq), float("nan"), device="cuda", dtype=torch.float16)
+        report("restore launch", workload=key, rows=rows_name, M=M, proj="q-rope")
+        mz.mz_q4_gemm_ex(X.data_ptr(), M, n_pad, d, wdev.data_ptr(), 4, yq.data_ptr(), stream(), a_rows=ar_ptr,
+                         workspace=ws.data_ptr(), workspace_bytes=ws_bytes, pos=d_pos.data_ptr(),
+                         rope_cs=cs.data_ptr(), head_dim=hd, n_valid=m.dq)
+        torch.cuda.synchronize()
+        xs = xr[check]
+        prod = xs @ Wm.T
+        b = REL * (np.abs(xs) @ np.abs(Wm).T) + 1e-6
+        ref = O.rope(prod.reshape(-1, m.n_q_heads, hd), pos_np[check], m.rope_theta).reshape(-1, m.dq)
+        bh = b.reshape(-1, m.n_q_heads, hd)
+        bound = (bh + np.concatenate([bh[..., hd // 2:], bh[..., :hd // 2]], -1)).reshape(-1, m.dq)
+        bound = bound + F16_REL * np.abs(ref) + 2.0 ** -22 * np.abs(prod).max()
+        got = yq.float().cpu().numpy()[check].astype(np.float64)
+        err = np.abs(got - ref)
+        report("  err", max=float(err.max()), worst_ratio=float((err / bound).max()))
+        assert np.all(err <= bound)
+        # keys and values into chunk slots
+        rk = W.encode_q4_0((rng.standard_normal((m.dkv, d)) * 0.02).astype(np.float32))
+        rv = W.encode_q4_0((rng.standard_normal((m.dkv, d)) * 0.02).astype(np.float32))
+        Wk, Wv = O.q4_0_decode(rk.reshape(-1), m.dkv, d), O.q4_0_decode(rv.reshape(-1), m.dkv, d)
+        n_kv = 2 * m.dkv
+        wdev = torch.from_numpy(mz.mz_q4_gemm_pack(np.concatenate([rk, rv]), n_kv, d)).cuda()
+        n_slots = (S + C - 1) // C + 1
+        slot_bytes = C * m.dkv * 4
+        perm = rng.permutation(n_slots)[: (S + C - 1) // C]
+        kv_off = (perm[pos_np // C].astype(np.int64) * slot_bytes + (pos_np % C).astype(np.int64) * m.dkv * 2)
+        slab = torch.full((n_slots * slot_bytes // 2,), float("nan"), device="cuda", dtype=torch.float16)
+        d_off = torch.from_numpy(kv_off).cuda()
+        report("restore launch", workload=key, rows=rows_name, M=M, proj="kv-rope-slots")
+        mz.mz_q4_gemm_ex(X.data_ptr(), M, (n_kv + 255) // 256 * 256, d, wdev.data_ptr(), 5, 0, stream(),
+                         a_rows=ar_ptr, workspace=ws.data_ptr(), workspace_bytes=ws_bytes, pos=d_pos.data_ptr(),
+                         rope_cs=cs.data_ptr(), kv_off=d_off.data_ptr(), slab=slab.data_ptr(), head_dim=hd,
+                         n_valid=n_kv, chunk_tokens=C)
+        torch.cuda.synchronize()
+        sl = slab.view(torch.uint8).cpu().numpy()
+        pk, pv = xs @ Wk.T, xs @ Wv.T
+        bk = REL * (np.abs(xs) @ np.abs(Wk).T) + 1e-6
+        bv = REL * (np.abs(xs) @ np.abs(Wv).T) + 1e-6
+        kref = O.rope(pk.reshape(-1, m.n_kv_heads, hd), pos_np[check], m.rope_theta).reshape(-1, m.dkv)
+        bkh = bk.reshape(-1, m.n_kv_heads, hd)
+        kb = (bkh + np.concatenate([bkh[..., hd // 2:], bkh[..., :hd // 2]], -1)).reshape(-1, m.dkv)
+        kb = kb + F16_REL * np.abs(kref) + 2.0 ** -22 * np.abs(pk).max()
+        vb = bv + F16_REL * np.abs(pv)
+        for j, r in enumerate(check):
+            off = int(kv_off[r])
+            kg = sl[off:off + m.dkv * 2].view(np.float16).astype(np.float64)
+            base = off - int(pos_np[r] % C) * m.dkv * 2 + C * m.dkv * 2
+            vt = sl[base:base + m.dkv * C * 2].view(np.float16).reshape(m.dkv, C)[:, pos_np[r] % C]
+            assert np.all(np.abs(kg - kref[j]) <= kb[j]), (key, rows_name, int(r), "K")
+            assert np.all(np.abs(vt.astype(np.float64) - pv[j]) <= vb[j]), (key, rows_name, int(r), "V")
+        # plain epilogues (store, residual add, SwiGLU) with queues and workspace,
+        # against mz_q4_gemm bit for bit on whole 256-row tiles
+        for i, (N, K, epi) in enumerate([(m.d_model, m.dq, 1), (m.d_ffn, m.d_model, 2)]):
+            if K != d:
+                continue           # the activation rows are [S][d]
+            if epi == 2:
+                g_ = W.encode_q4_0((rng.standard_normal((N, K)) * 0.02).astype(np.float32))
+                u_ = W.encode_q4_0((rng.standard_normal((N, K)) * 0.02).astype(np.float32))
+                wdev = torch.from_numpy(mz.mz_q4_gemm_pack(g_, N, K, w_up=u_)).cuda()
+                n_pad = 2 * ((N + 127) // 128 * 128)
+                y1 = torch.zeros(M, n_pad // 2, device="cuda", dtype=torch.float16)
+            else:
+                raw = W.encode_q4_0((rng.standard_normal((N, K)) * 0.02).astype(np.float32))
+                wdev = torch.from_numpy(mz.mz_q4_gemm_pack(raw, N, K)).cuda()
+                n_pad = (N + 255) // 256 * 256
+                y1 = torch.randn(M, n_pad, device="cuda", generator=gen)
+            y0 = y1.clone()
+            xg = X if arow is None else X[d_sub.long()].contiguous()
+            report("restore launch", workload=key, rows=rows_name, M=M, proj=f"epi{epi}")
+            mz.mz_q4_gemm_ex(X.data_ptr(), M, n_pad, K, wdev.data_ptr(), epi, y1.data_ptr(), stream(), a_rows=ar_ptr,
+                             work_queues=queues.data_ptr(), workspace=ws.data_ptr(), workspace_bytes=ws_bytes)
+            y2 = y0.clone()
+            mz.mz_q4_gemm(xg.data_ptr(), M, n_pad, K, wdev.data_ptr(), epi, y2.data_ptr(), stream())
+            torch.cuda.synchronize()
+            assert int(queues.abs().sum()) == 0
+            assert torch.equal(y1[:full].view(torch.uint8), y2[:full].view(torch.uint8)), (key, rows_name, epi)
+            a1 = y1[full:].float().cpu().numpy().astype(np.float64)
+            a2 = y2[full:].float().cpu().numpy().astype(np.float64)
+            if a1.size:
+                scale = np.abs(a2).max() + 1e-3
+                assert np.abs(a1 - a2).max() <= 4 * F16_REL * scale, (key, rows_name, epi)
 
 
 @pytest.mark.parametrize("M,N,K,epi", [
@@ -273,16 +410,30 @@ def test_attention_small(nq, nkv, hd, C, S):
 
 @pytest.mark.parametrize("key", ["1b", "3b", "1p5b", "8b"])
 def test_attention_full_context(key):
-    """All S query rows of the workload, sampled check, through the work
-    queues (the restore's launch) and bit-equal to the one-tile-per-workgroup
-    form."""
+    """All S query rows of the workload through the work queues (the
+    restore's launch), bit-equal to the one-tile-per-workgroup form, and one
+    query row (every head, so every KV head) in every 32-row query tile
+    checked against the exact definition."""
     w = W.WORKLOADS[key]
     m = w.model
     S = w.n_ctx + w.n_prompt
-    rng = np.random.default_rng(7)
-    sample = np.unique(np.concatenate([rng.choice(S, 12, replace=False), [0, S - 1]]))
     _attn_case(m.n_q_heads, m.n_kv_heads, m.head_dim, m.chunk_tokens, S, np.arange(S), seed=5,
-               sample=sample, n_split="queued")
+               sample=_tile_rows(S, 32, 5), n_split="queued")
+
+
+def test_attention_full_context_gappy_1p5b():
+    """The 1.5B shape (12 query / 2 KV heads, head dim 128) at its full
+    16384-token context with gappy query rows: the rows of a seeded 30 % of
+    the chunks (a recompute's R_l), through the work queues; one query in
+    every 32-row tile checked."""
+    w = W.WORKLOADS["1p5b"]
+    m = w.model
+    S = w.n_ctx
+    rng = np.random.default_rng(31)
+    keep = rng.random(w.n_chunks) < 0.3
+    qpos = np.array([p for p in range(S) if keep[p // m.chunk_tokens] or p == S - 1], np.int32)
+    _attn_case(m.n_q_heads, m.n_kv_heads, m.head_dim, m.chunk_tokens, S, qpos, seed=6,
+               sample=_tile_rows(qpos.size, 32, 6), n_split="queued")
 
 
 @pytest.mark.parametrize("nq,nkv,hd,C,S", [

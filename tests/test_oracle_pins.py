@@ -560,6 +560,27 @@ def test_f16_floor_reduces_to_fp64_oracle():
     assert fl.max() <= 8 * 2.0 ** -11 * max(1.0, kmax)
 
 
+def test_bf16_rounding_and_rounded_probability_attention():
+    """The floor's bf16 rounding is round-to-nearest-even to 8 significant
+    bits: hand values at the ties, and torch's own float32 -> bfloat16
+    conversion on random values.  Its attention with rounded probabilities
+    reduces to the oracle's attention when nothing is rounded."""
+    from oracle.f16_floor import _attention_rounded_probs, _bf16
+    t = [1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8, 1.0 + 2.0 ** -8 + 2.0 ** -20, -(2.0 + 2.0 ** -7), 0.0]
+    assert _bf16(np.array(t)).tolist() == [1.0, 1.0 + 2.0 ** -6, 1.0 + 2.0 ** -7, -2.0, 0.0]
+    import torch
+    x = np.random.default_rng(3).standard_normal(10000) * 10.0 ** np.random.default_rng(4).uniform(-6, 6, 10000)
+    ref = torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(_bf16(x.astype(np.float32)), ref)
+    rng = np.random.default_rng(6)
+    q = rng.standard_normal((7, 4, 8))
+    k = rng.standard_normal((12, 2, 8))
+    v = rng.standard_normal((12, 2, 8))
+    pos = np.array([0, 1, 3, 5, 8, 10, 11])
+    assert np.allclose(_attention_rounded_probs(q, pos, k, v, lambda a: a),
+                       O.causal_gqa_attention(q, pos, k, v), rtol=0, atol=1e-13)
+
+
 # ----------------------------------------------------------------------------- KV codec
 
 def test_kv_codec_exact_grid_group():
