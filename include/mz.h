@@ -85,23 +85,34 @@ mz_status mz_load_model(const mz_model_cfg *cfg, const void *q4_blob, size_t nby
                         int32_t device, mz_ctx **out);
 
 /* Replace the cached context by tokens[0..n) (host) and build its KV cache
- * with a full prefill on the GPU (every chunk resident afterwards). */
+ * with a full prefill on the GPU: every layer computes the key and value
+ * vectors of every token, kept as the KV cache (paper Sec. 2.1), here in the
+ * per-layer chunk slots (Sec. 4.2); every chunk is resident afterwards.
+ * EINVAL for n < 0, n > max_ctx, a NULL tokens with n > 0, or a token id
+ * outside the vocabulary. */
 mz_status mz_prefill_context(mz_ctx *ctx, const int32_t *tokens, int32_t n);
 
 /* Replace the cached context by tokens[0..n) (host) without computing KV:
  * every chunk is allocated, zero-filled and resident; fill it with
- * mz_import_kv.  Used to start from KV produced elsewhere. */
+ * mz_import_kv.  Used to start from KV produced elsewhere -- the cached
+ * context of a context-aware request (paper Sec. 2.2) whose KV cache was
+ * built before.  Errors as mz_prefill_context. */
 mz_status mz_set_context(mz_ctx *ctx, const int32_t *tokens, int32_t n);
 
-/* Write chunk `chunk` of layer `layer` from host arrays k, v, each
+/* Write chunk `chunk` of layer `layer` -- one KV unit of the fine-grained
+ * memory management, a fixed run of tokens of one layer's K and V (paper
+ * Sec. 4.2, chunk size in Sec. 4.3) -- from host arrays k, v, each
  * [chunk_tokens][n_kv_heads * head_dim] IEEE half, hidden index innermost
- * (the exchange layout; the device slot keeps V transposed).  ESTATE if the
- * chunk is not resident. */
+ * (the exchange layout; the device slot keeps V transposed).  Rows past the
+ * context's last token are written too.  EINVAL for a layer or chunk out of
+ * range, ESTATE if the chunk is not resident. */
 mz_status mz_import_kv(mz_ctx *ctx, int32_t layer, int32_t chunk, const void *k_f16,
                        const void *v_f16);
 
-/* Read a resident chunk into host arrays laid out as in mz_import_kv.
- * ESTATE if the chunk is not resident. */
+/* Read a resident KV chunk (paper Sec. 4.2) into host arrays k, v laid out
+ * as in mz_import_kv (caller-owned, chunk_tokens * n_kv_heads * head_dim
+ * halves each).  EINVAL for a layer or chunk out of range, ESTATE if the
+ * chunk is not resident. */
 mz_status mz_read_kv(mz_ctx *ctx, int32_t layer, int32_t chunk, void *k_f16, void *v_f16);
 
 /* Keep only the first n tokens of the cached context (0 <= n <= current):
@@ -123,10 +134,12 @@ mz_status mz_evict(mz_ctx *ctx, const mz_evict_plan *plan);
  * total exceeds max_ctx or a token is out of range. */
 mz_status mz_restore_and_prefill(mz_ctx *ctx, const int32_t *prompt, int32_t n_prompt);
 
-/* Greedy first token after mz_restore_and_prefill / mz_prefill_context:
- * RMSNorm of the last position's final hidden state, output head, argmax
- * (lowest index on ties).  Synchronizes.  logits_out (host, [vocab] float) may
- * be NULL.  ESTATE if nothing was prefilled since the last first token. */
+/* Greedy first token after mz_restore_and_prefill / mz_prefill_context --
+ * the token that ends the prefill stage, whose latency is the TTFT (paper
+ * Sec. 2.1): RMSNorm of the last position's final hidden state, output head,
+ * argmax (lowest index on ties).  Synchronizes.  logits_out (host, [vocab]
+ * float) may be NULL.  EINVAL for a NULL token_out, ESTATE if nothing was
+ * prefilled since the last first token. */
 mz_status mz_first_token(mz_ctx *ctx, int32_t *token_out, float *logits_out);
 
 /* Greedy generation past the first token: append `token` to the context,
@@ -167,7 +180,10 @@ mz_status mz_generate(mz_ctx *ctx, int32_t token, int32_t n, int32_t *tokens_out
  * eviction, default).  Test hooks: "debug_poison" (1: fill every
  * slot and weight unit allocated by a restore with NaN before it is
  * restored or recomputed), "debug_swap_delay_us" (delay the swap stream by a
- * bounded busy wait before its copies).  EINVAL for an unknown key. */
+ * bounded busy wait before its copies), "debug_kv_slot_limit" (at most this
+ * many KV chunk slots in use, so a restore that needs more fails with
+ * MZ_ENOMEM and leaves the context as it was; negative: the whole pool, the
+ * default).  EINVAL for an unknown key. */
 mz_status mz_set_option(mz_ctx *ctx, const char *key, int64_t value);
 
 /* JSON summary of the last restore (row counts, bytes moved, per-kernel

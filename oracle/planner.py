@@ -15,7 +15,8 @@ drags its rows through every layer up to the one that dropped it.
                  forward-out    layer ascending, chunk ascending
                  token-aligned  chunk descending, then layer descending
                  random-out     backward-out shuffled by Fisher-Yates, the
-                                indices drawn from splitmix64(seed)
+                                indices drawn from splitmix64(seed) (Steele,
+                                Lea and Flood, OOPSLA 2014)
   weights      n_w units, always swapped: the last layers (the first ones for
                forward-out)
   placement    balanced: a chunk is dropped when the restore's schedule

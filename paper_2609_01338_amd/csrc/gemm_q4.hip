@@ -77,7 +77,10 @@ __device__ __forceinline__ uint32_t and_or(uint32_t x, uint32_t mask, uint32_t m
 }
 
 // The 8 codes of one pre-ordered dword (pair m at bits 4m and 16 + 4m) ->
-// 4 f16x2 of d * (q - 8), pair m in component m.
+// 4 f16x2 of d * (q - 8), pair m in component m.  The integer-to-half step
+// is the published exponent-bias conversion of 4-bit integers (Kim et al.,
+// arXiv:2211.10017): OR-ing a code into the mantissa of a half whose ulp is 1
+// (or 1/16 for the high nibble) and subtracting the bias gives it exactly.
 __device__ __forceinline__ uint4 dequant_dword(uint32_t w, f16x2 d2) {
   const uint32_t mag_lo = 0x64006400u;   // 1024: code bits 0-3 add q
   const uint32_t mag_hi = 0x54005400u;   // 64: code bits 4-7 add q (ulp 1/16)

@@ -277,6 +277,7 @@ Rows compute_rows(const uint8_t* kv_state, int L, int nc, int N, int P, int C) {
 
 struct SlotPool {
   int n = 0;
+  int limit = -1;   // test hook: at most this many slots in use (-1: the whole pool)
   std::set<int> free;
   void init(int count) {
     n = count;
@@ -284,14 +285,14 @@ struct SlotPool {
     for (int i = 0; i < count; ++i) free.insert(i);
   }
   int alloc_one() {
-    if (free.empty()) return -1;
+    if (free.empty() || (limit >= 0 && used() >= limit)) return -1;
     int s = *free.begin();
     free.erase(free.begin());
     return s;
   }
   // first-fit contiguous run of k slots; -1 if none
   int alloc_run(int k) {
-    if (k <= 0) return -1;
+    if (k <= 0 || (limit >= 0 && used() + k > limit)) return -1;
     int start = -1, len = 0, prev = -2;
     for (int s : free) {
       if (s == prev + 1) {
@@ -1321,6 +1322,7 @@ mz_status mz_set_option(mz_ctx* x, const char* key, int64_t value) {
     if (k == "overlap") x->overlap = value != 0;
     else if (k == "debug_swap_delay_us") x->debug_swap_delay_us = value < 0 ? 0 : value;
     else if (k == "debug_poison") x->debug_poison = value != 0;
+    else if (k == "debug_kv_slot_limit") x->kv_pool.limit = value < 0 ? -1 : (int)std::min<int64_t>(value, INT32_MAX);
     else if (k == "swap_trim") x->swap_trim = value != 0;
     else if (k == "attn_split") x->attn_split = value != 0;
     else if (k == "attn_queue") x->attn_queue = value != 0;

@@ -46,7 +46,8 @@ struct PlanError {
   const char* msg;
 };
 
-// splitmix64: the random-out order's generator (published constants).
+// splitmix64 (Steele, Lea and Flood, OOPSLA 2014, with the published
+// constants): the random-out order's generator.
 uint64_t splitmix64(uint64_t& x) {
   uint64_t z = (x += 0x9E3779B97F4A7C15ull);
   z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
