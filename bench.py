@@ -148,17 +148,41 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def cpu_baseline(w, blob, plan_nR, sample_rows=64):
-    """The oracle as it stands, on a bounded sample: one layer's weight decode
-    plus `sample_rows` evenly spaced positions through that layer (attention
-    over a synthetic KV cache of the full context), extrapolated to the whole
-    restore: L decodes and sum_l nR(l) row-layers."""
-    import oracle as O
+def host_info():
+    """Host the oracle runs on: cores this process may use, CPU model, BLAS."""
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas, threads = "unknown", None
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        for i in threadpool_info():
+            if i.get("user_api") == "blas":
+                blas = f"{i.get('internal_api')} {i.get('version')}"
+                threads = int(i.get("num_threads", 1))
+                break
     except Exception:
-        threads = len(os.sched_getaffinity(0))
+        pass
+    cores = len(os.sched_getaffinity(0))
+    return {"cores_available": cores, "cpu_model": model, "blas": blas,
+            "blas_threads": threads if threads else cores}
+
+
+def cpu_baseline(w, blob, plan_nR, sample_rows=64):
+    """The oracle as it stands, on a bounded sample of the workload's restore:
+    one layer's weight decode plus `sample_rows` evenly spaced positions
+    through that layer (attention over a synthetic KV cache of the full
+    context), extrapolated to the whole restore (L decodes and sum_l nR(l)
+    row-layers): an estimate, labelled as one.  The oracle's full restore is
+    timed by --cpu-full."""
+    import oracle as O
+    info = host_info()
     m = w.model
     hp = O.Hyper(m)
     wts = O.Weights(hp, blob)
@@ -176,12 +200,41 @@ def cpu_baseline(w, blob, plan_nR, sample_rows=64):
                     lambda last: (K[:last].astype(np.float64), V[:last].astype(np.float64)))
     t_rows = time.perf_counter() - t1
     total = m.n_layers * t_decode + t_rows * float(np.sum(plan_nR)) / sample_rows
-    return {"value": round(plan_nR[0] / total, 3), "unit": "tokens/s", "cores": int(threads),
-            "kind": "oracle",
+    return {"value": round(plan_nR[0] / total, 3), "unit": "tokens/s", "cores": info["blas_threads"],
+            "kind": "oracle", "estimate": True, **info,
             "sample": (f"layer-0 weight decode ({t_decode:.2f} s) + {sample_rows} evenly spaced positions "
                        f"through layer 0 with attention over all {S} keys ({t_rows:.2f} s), extrapolated "
                        f"to {m.n_layers} layers and sum nR = {int(np.sum(plan_nR))} row-layers "
-                       f"(est. {total:.1f} s per restore)")}
+                       f"(est. {total:.1f} s per restore); fp64 numpy, BLAS on {info['blas_threads']} threads")}
+
+
+def cpu_full_restore(W, key):
+    """The oracle's complete evict -> restore -> first token on workload
+    `key` (its own plan, context and prompt), timed on this host: the
+    never-evicted prefill that builds the cached KV (untimed when nothing is
+    kept), then the eviction and the timed restore and first token."""
+    import oracle as O
+    w = W.WORKLOADS[key]
+    m = w.model
+    blob = W.make_blob(w)
+    ctx, prompt = W.make_tokens(w)
+    plan = W.make_plan(w)
+    threads = host_info()["blas_threads"]
+    ox = O.OracleContext(m, blob, threads=threads)
+    t0 = time.perf_counter()
+    if (plan.kv_state == W.DROP).all():
+        ox.set_context(ctx)           # every chunk is recomputed: no cached KV is read
+    else:
+        ox.prefill_context(ctx)
+    t_pre = time.perf_counter() - t0
+    ox.evict(plan.kv_state, plan.w_state)
+    t1 = time.perf_counter()
+    st = ox.restore_and_prefill(prompt)
+    tok, _ = ox.first_token()
+    t_restore = time.perf_counter() - t1
+    return {"workload": key, "ttft_s": round(t_restore, 3), "tokens_per_s": round(st["nR"][0] / t_restore, 3),
+            "nR0": int(st["nR"][0]), "sum_nR": int(sum(st["nR"])), "token": int(tok),
+            "context_build_s": round(t_pre, 3)}
 
 
 def tp_shard_kernels(w, tp):
@@ -418,6 +471,9 @@ def main():
     ap.add_argument("--recompute-tflops", type=float, default=400.0,
                     help="recompute rate the balanced placement assumes (partial-layer recompute of a "
                          "balanced plan runs at about 400 TFLOP/s on MI355X: few rows per GEMM)")
+    ap.add_argument("--cpu-full", default=None,
+                    help="comma list of workloads: instead of the GPU steps, time the oracle's full evict -> "
+                         "restore -> first token on this host (one JSON line)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one plain 1 GiB device copy first (reference for profiler byte counters)")
     args = ap.parse_args()
@@ -425,6 +481,14 @@ def main():
         print(f"bench.py measures one GPU: the engine has no multi-GPU path (asked for --gpus {args.gpus})",
               file=sys.stderr)
         sys.exit(2)
+    if args.cpu_full:
+        from paper_2609_01338_amd import workloads as W
+        runs = []
+        for key in args.cpu_full.split(","):
+            runs.append(cpu_full_restore(W, key))
+            log(f"[bench] oracle full restore: {runs[-1]}")
+        print(json.dumps({"cpu_full_restore": runs, "kind": "oracle", **host_info()}), flush=True)
+        return
     board = BoardMonitor()   # before anything touches the GPU
 
     # torch (device buffers of the calibration copy and the shard-kernel
