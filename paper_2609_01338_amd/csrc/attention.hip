@@ -592,51 +592,240 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
   }
 }
 
-// Merge of the key splits: one wave per (query row, head).  With m_s, l_s
-// and the normalised partial o_s of split s, and M = max m_s over the splits
-// that hold keys of the query: O = sum_s 2^(m_s - M) l_s o_s / sum_s
-// 2^(m_s - M) l_s.  Split 0 always holds key 0, so the denominator is
-// positive.  Splits past the one holding the query's own position were not
-// written for it and are not read.  Lane s reads split s's (m, l) (at most
-// 64 splits); M and the denominator are wave reductions, and the output sum
-// walks the splits with independent loads, each weight broadcast from its
-// lane.
+// Split-key attention of few query columns (decode steps and short prompts):
+// a column is one (query row, query head) pair of a KV head's group, at most
+// 16 of them (m rows x G heads), so the score and output products run on
+// v_mfma_f32_16x16x32_f16 with the columns as the 16-wide side instead of
+// padding each query row to 32 MFMA rows.  Workgroup (split, KV head): the
+// split's key tiles (KT = 64 keys) in 32-key blocks; its 4 waves take blocks
+// round-robin, each with its own online softmax, and combine through LDS into
+// the split partial of the split kernel (f16 output normalised by its own
+// sum, and (max, sum) in log2 units), so the same merge follows.
+//
+// Per 32-key block: S^T[keys][cols] = K Q^T as 2 (16-key) x HD/32 MFMAs with
+// K fragments loaded straight from the slot rows; the accumulator holds keys
+// 4 (l/16) + r (and 16 + 4 (l/16) + r for the second half) of column l%16,
+// which is directly the B operand of O^T[dims][cols] += V^T P^T once the
+// 32 keys are taken in that order (k slots 0-3: the first half's keys, 4-7:
+// the second's); the V^T fragments are loaded in the same key order (two
+// 8-byte reads of a dimension row).  Keys past the last query position hold
+// whatever the slot holds: their scores are masked and their V values zeroed.
+constexpr int kFewCols = 16, kFewWaves = 4, kFewBlock = 32;
+
 template <int HD>
-__global__ __launch_bounds__(256) void attn_merge_kernel(const _Float16* __restrict__ Opart,
-                                                         const float2* __restrict__ MLpart,
-                                                         const int32_t* __restrict__ qpos, int M, int nq,
-                                                         int n_split, int tps, _Float16* __restrict__ O) {
-  constexpr int DPL = HD / 64;   // dimensions per lane (1 or 2)
-  const int wv = (int)((blockIdx.x * blockDim.x + threadIdx.x) >> 6);
-  const int lane = threadIdx.x & 63;
-  if (wv >= M * nq) return;      // whole waves leave together
-  const int qi = wv / nq, h = wv % nq;
-  const int nv = min(n_split, (qpos[qi] / KT) / tps + 1);
-  const size_t stride = (size_t)M * nq;          // between splits, in (row, head) entries
-  const size_t e0 = (size_t)qi * nq + h;
-  float2 ml = make_float2(-INFINITY, 0.f);
-  if (lane < nv) ml = MLpart[lane * stride + e0];
-  if (!(ml.y > 0.f)) ml.x = -INFINITY;            // no key of this split: weight 0
-  float mx = ml.x;
+__global__ __launch_bounds__(64 * kFewWaves) void attn_few_kernel(
+    const _Float16* __restrict__ Q, const int32_t* __restrict__ qpos, int M, const uint8_t* __restrict__ slab,
+    const int32_t* __restrict__ table, int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group,
+    float scale_log2, int tps, _Float16* __restrict__ Opart, float2* __restrict__ MLpart) {
+  constexpr int KS = HD / 32;          // 32-wide dimension steps of a score product
+  constexpr int DB = HD / 16;          // 16-dimension blocks of the output
+  __shared__ float s_o[kFewWaves][DB][4][64];   // per wave: O^T fragments, lane-major
+  __shared__ float s_ml[kFewWaves][2][kFewCols];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int split = blockIdx.x, kvh = blockIdx.y;
+  const int col = lane & 15, lg = lane >> 4;
+  const int ncol = M * group;
+  const bool cvalid = col < ncol;
+  const int qr = cvalid ? col / group : 0, qh = kvh * group + (cvalid ? col % group : 0);
+  const int p = cvalid ? qpos[qr] : -1;             // keys 0..p are seen by this column
+  const int kmax = qpos[M - 1];
+  const int dkv = nkv * HD;
+  const int64_t krow_bytes = (int64_t)dkv * 2;
+  // Q^T fragments: column col, dimensions 32 ks + 8 lg .. +8
+  typedef _Float16 f16x8v __attribute__((ext_vector_type(8)));
+  typedef float f32x4v __attribute__((ext_vector_type(4)));
+  f16x8v bq[KS];
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
-  const float wgt = ml.x == -INFINITY ? 0.f : exp2f(ml.x - mx) * ml.y;
-  float den = wgt;
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) den += __shfl_xor(den, o);
-  float acc[DPL] = {};
-  const _Float16* src = Opart + e0 * HD + lane * DPL;
-#pragma unroll 8
-  for (int j = 0; j < nv; ++j) {
-    const float wj = __shfl(wgt, j);
-    const _Float16* p = src + (size_t)j * stride * HD;
-#pragma unroll
-    for (int e = 0; e < DPL; ++e) acc[e] = __builtin_fmaf(wj, (float)p[e], acc[e]);
+  for (int ks = 0; ks < KS; ++ks) {
+    bq[ks] = f16x8v{};
+    if (cvalid) bq[ks] = *reinterpret_cast<const f16x8v*>(Q + ((size_t)qr * nq + qh) * HD + ks * 32 + lg * 8);
   }
-  const float inv = 1.0f / den;
-  _Float16* dst = O + (size_t)qi * nq * HD + h * HD + lane * DPL;
+  f32x4v o[DB];
 #pragma unroll
-  for (int e = 0; e < DPL; ++e) dst[e] = (_Float16)(acc[e] * inv);
+  for (int d = 0; d < DB; ++d) o[d] = f32x4v{0.f, 0.f, 0.f, 0.f};
+  float m_c = -INFINITY, l_c = 0.f;
+  const int nb_all = (kmax / KT + 1) * (KT / kFewBlock);      // blocks up to kmax's tile
+  const int b_begin = split * tps * (KT / kFewBlock);
+  const int b_end = min(b_begin + tps * (KT / kFewBlock), nb_all);
+  for (int b = b_begin + w; b < b_end; b += kFewWaves) {
+    const int j0 = b * kFewBlock;
+    if (j0 > kmax) break;
+    const uint8_t* slot = slab + (int64_t)(uint32_t)table[j0 >> cshift] * slot_bytes;
+    const int jc = j0 & (C - 1);
+    f16x8v ka[2][KS];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        ka[h][ks] = *reinterpret_cast<const f16x8v*>(slot + (int64_t)(jc + h * 16 + col) * krow_bytes +
+                                                      (kvh * HD + ks * 32 + lg * 8) * 2);
+    // V^T fragments: dimension row 16 d + col, keys jc + 4 lg .. +4 and jc + 16 + 4 lg .. +4
+    uint2 va[DB][2];
+    const uint8_t* vt = slot + (int64_t)C * dkv * 2 + ((int64_t)(kvh * HD + col) * C + jc + 4 * lg) * 2;
+#pragma unroll
+    for (int d = 0; d < DB; ++d)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) va[d][h] = *reinterpret_cast<const uint2*>(vt + (int64_t)d * 16 * C * 2 + h * 32);
+    f32x4v sc[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      sc[h] = f32x4v{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) sc[h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ka[h][ks], bq[ks], sc[h], 0, 0, 0);
+    }
+    // scale, causal mask (key j0 + 16 h + 4 lg + r against the column's position)
+    float bm = -INFINITY;
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int j = j0 + h * 16 + 4 * lg + r;
+        const float v = j <= p ? sc[h][r] * scale_log2 : -INFINITY;
+        sc[h][r] = v;
+        bm = fmaxf(bm, v);
+      }
+    bm = fmaxf(bm, __shfl_xor(bm, 16));
+    bm = fmaxf(bm, __shfl_xor(bm, 32));
+    const float m_new = fmaxf(m_c, bm);
+    const float base = m_new == -INFINITY ? 0.f : m_new;   // a column that has seen no key yet
+    const float alpha = exp2f(m_c - base);
+    m_c = m_new;
+    l_c *= alpha;
+#pragma unroll
+    for (int d = 0; d < DB; ++d) o[d] *= alpha;
+    f16x8v pb;
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const _Float16 e = (_Float16)exp2f(sc[h][r] - base);
+        pb[h * 4 + r] = e;
+        l_c += (float)e;
+      }
+    // values of keys past the last query position are not data: zero them
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int nvk = kmax - (j0 + h * 16 + 4 * lg) + 1;   // keys of this 4-key run that exist
+      if (nvk < 4) {
+#pragma unroll
+        for (int d = 0; d < DB; ++d) {
+          uint2 v = va[d][h];
+          if (nvk <= 0) v = make_uint2(0u, 0u);
+          else if (nvk == 1) v = make_uint2(v.x & 0xFFFFu, 0u);
+          else if (nvk == 2) v = make_uint2(v.x, 0u);
+          else v = make_uint2(v.x, v.y & 0xFFFFu);
+          va[d][h] = v;
+        }
+      }
+    }
+#pragma unroll
+    for (int d = 0; d < DB; ++d) {
+      const uint4 a4 = make_uint4(va[d][0].x, va[d][0].y, va[d][1].x, va[d][1].y);
+      o[d] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8v, a4), pb, o[d], 0, 0, 0);
+    }
+  }
+  // the column's sum over its four lane groups; then the waves combine
+  l_c += __shfl_xor(l_c, 16);
+  l_c += __shfl_xor(l_c, 32);
+  if (lg == 0) {
+    s_ml[w][0][col] = m_c;
+    s_ml[w][1][col] = l_c;
+  }
+#pragma unroll
+  for (int d = 0; d < DB; ++d)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) s_o[w][d][r][lane] = o[d][r];
+  __syncthreads();
+  // thread t: column t % 16, output dimensions (t / 16) * DPT .. + DPT
+  static_assert(HD % (4 * kFewWaves) == 0, "output dimensions per thread");
+  const int t = threadIdx.x;
+  const int c = t & 15;
+  if (c >= ncol) return;
+  float mx = -INFINITY;
+#pragma unroll
+  for (int v = 0; v < kFewWaves; ++v) mx = fmaxf(mx, s_ml[v][0][c]);
+  float wsum[kFewWaves], den = 0.f;
+#pragma unroll
+  for (int v = 0; v < kFewWaves; ++v) {
+    const float mv = s_ml[v][0][c];
+    wsum[v] = (mv == -INFINITY) ? 0.f : exp2f(mv - mx);
+    den += wsum[v] * s_ml[v][1][c];
+  }
+  const int r_ = c / group, h_ = kvh * group + c % group;
+  const size_t e0 = (size_t)split * M * nq + (size_t)r_ * nq + h_;
+  if (t < 16) MLpart[e0] = make_float2(den > 0.f ? mx : -INFINITY, den);
+  const float inv = den > 0.f ? 1.0f / den : 0.f;
+  constexpr int DPT = HD / (4 * kFewWaves);    // output dimensions per thread (64 * waves / 16 threads per column)
+  const int dbase = (t >> 4) * DPT;
+#pragma unroll
+  for (int e = 0; e < DPT; ++e) {
+    const int dim = dbase + e;                 // dimension = 16 d + 4 lg' + r of a fragment lane
+    const int d = dim >> 4, lg2 = (dim >> 2) & 3, r = dim & 3;
+    float acc = 0.f;
+#pragma unroll
+    for (int v = 0; v < kFewWaves; ++v) acc += wsum[v] * s_o[v][d][r][lg2 * 16 + c];
+    Opart[e0 * HD + dim] = (_Float16)(acc * inv);
+  }
+}
+
+// Merge of the key splits, one workgroup per (query row, head).  With m_s,
+// l_s and the normalised partial o_s of split s, and M = max m_s over the
+// splits that hold keys of the query: O = sum_s 2^(m_s - M) l_s o_s / sum_s
+// 2^(m_s - M) l_s.  Split 0 always holds key 0, so the denominator is
+// positive; splits past the one holding the query's own position were not
+// written for it and are not read.  64 lanes of output dimensions x 4 groups
+// of splits (split g + 4k in group g, at most 64 splits), the group maxima,
+// denominators and sums combined through LDS.
+template <int HD>
+__global__ __launch_bounds__(256) void attn_merge_wide_kernel(const _Float16* __restrict__ Opart,
+                                                              const float2* __restrict__ MLpart,
+                                                              const int32_t* __restrict__ qpos, int M, int nq,
+                                                              int n_split, int tps, _Float16* __restrict__ O) {
+  constexpr int DPL = HD / 64;
+  __shared__ float s_m[4], s_d[4];
+  __shared__ float s_acc[4][64 * DPL];
+  const int e = blockIdx.x;                       // (row, head)
+  const int qi = e / nq;
+  const int t = threadIdx.x, dl = t & 63, sg = t >> 6;
+  const int nv = min(n_split, (qpos[qi] / KT) / tps + 1);
+  const size_t stride = (size_t)M * nq;
+  float2 ml[16];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    const int sp = sg + 4 * k;
+    ml[k] = sp < nv ? MLpart[sp * stride + e] : make_float2(-INFINITY, 0.f);
+    if (!(ml[k].y > 0.f)) ml[k].x = -INFINITY;
+    mx = fmaxf(mx, ml[k].x);
+  }
+  if (dl == 0) s_m[sg] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(s_m[0], s_m[1]), fmaxf(s_m[2], s_m[3]));
+  float den = 0.f, acc[DPL] = {};
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    const int sp = sg + 4 * k;
+    if (sp >= nv) break;
+    const float wgt = ml[k].x == -INFINITY ? 0.f : exp2f(ml[k].x - mx) * ml[k].y;
+    den += wgt;
+    const _Float16* p = Opart + ((size_t)sp * stride + e) * HD + dl * DPL;
+#pragma unroll
+    for (int q = 0; q < DPL; ++q) acc[q] = __builtin_fmaf(wgt, (float)p[q], acc[q]);
+  }
+  if (dl == 0) s_d[sg] = den;
+#pragma unroll
+  for (int q = 0; q < DPL; ++q) s_acc[sg][dl * DPL + q] = acc[q];
+  __syncthreads();
+  if (sg == 0) {
+    const float dsum = s_d[0] + s_d[1] + s_d[2] + s_d[3];
+    const float inv = 1.0f / dsum;
+#pragma unroll
+    for (int q = 0; q < DPL; ++q) {
+      const int i = dl * DPL + q;
+      const float a = s_acc[0][i] + s_acc[1][i] + s_acc[2][i] + s_acc[3][i];
+      O[(size_t)e * HD + i] = (_Float16)(a * inv);
+    }
+  }
 }
 
 struct SplitArgs {
@@ -782,16 +971,31 @@ void launch_attention_split(const void* q, const int32_t* qpos, int m, int max_p
   sa.opart = reinterpret_cast<_Float16*>(ws);
   const int64_t o = (int64_t)sa.n_split * m * n_q * head_dim * 2;
   sa.ml = reinterpret_cast<float2*>(reinterpret_cast<uint8_t*>(ws) + ((o + 255) / 256) * 256);
-  launch_any(q, qpos, m, slab, table, chunk_tokens, slot_bytes, n_q, n_kv, head_dim, out, sa, true, nullptr, s);
-  const int waves = m * n_q;
-  const dim3 grid((unsigned)((waves + 3) / 4));
+  const int group = n_q / n_kv;
+  if (m * group <= kFewCols && chunk_tokens >= kFewBlock) {
+    // few query columns: one workgroup per (split, KV head) on 16-wide products
+    int cshift = 0;
+    while ((1 << cshift) < chunk_tokens) ++cshift;
+    const float scale_log2 = 1.4426950408889634f / __builtin_sqrtf((float)head_dim);
+    const dim3 grid((unsigned)sa.n_split, (unsigned)n_kv);
+    const _Float16* Q = reinterpret_cast<const _Float16*>(q);
+    const uint8_t* S = reinterpret_cast<const uint8_t*>(slab);
+    if (head_dim == 128)
+      hipLaunchKernelGGL(attn_few_kernel<128>, grid, dim3(64 * kFewWaves), 0, s, Q, qpos, m, S, table, chunk_tokens,
+                         cshift, slot_bytes, n_q, n_kv, group, scale_log2, sa.tps, sa.opart, sa.ml);
+    else
+      hipLaunchKernelGGL(attn_few_kernel<64>, grid, dim3(64 * kFewWaves), 0, s, Q, qpos, m, S, table, chunk_tokens,
+                         cshift, slot_bytes, n_q, n_kv, group, scale_log2, sa.tps, sa.opart, sa.ml);
+  } else {
+    launch_any(q, qpos, m, slab, table, chunk_tokens, slot_bytes, n_q, n_kv, head_dim, out, sa, true, nullptr, s);
+  }
   _Float16* O = reinterpret_cast<_Float16*>(out);
   if (head_dim == 128)
-    hipLaunchKernelGGL(attn_merge_kernel<128>, grid, dim3(256), 0, s, sa.opart, sa.ml, qpos, m, n_q, sa.n_split,
-                       sa.tps, O);
+    hipLaunchKernelGGL(attn_merge_wide_kernel<128>, dim3(m * n_q), dim3(256), 0, s, sa.opart, sa.ml, qpos, m, n_q,
+                       sa.n_split, sa.tps, O);
   else
-    hipLaunchKernelGGL(attn_merge_kernel<64>, grid, dim3(256), 0, s, sa.opart, sa.ml, qpos, m, n_q, sa.n_split,
-                       sa.tps, O);
+    hipLaunchKernelGGL(attn_merge_wide_kernel<64>, dim3(m * n_q), dim3(256), 0, s, sa.opart, sa.ml, qpos, m, n_q,
+                       sa.n_split, sa.tps, O);
 }
 
 }  // namespace mzk

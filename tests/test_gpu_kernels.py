@@ -465,16 +465,21 @@ def test_attention_split(nq, nkv, hd, C, S):
             _attn_case(nq, nkv, hd, C, S, qp, seed=20 + i, n_split=n_split)
 
 
-@pytest.mark.parametrize("m", [1, 129])
+@pytest.mark.parametrize("m", [1, 4, 129])
 def test_attention_split_8b_context(m):
     """The 8B layer at its full context (32768 cached + 128 prompt tokens):
     the last m rows, as the restore runs them when nothing before the prompt
-    is recomputed, with the restore's split choice; every row checked."""
+    is recomputed, with the restore's split choice; every row checked.  One
+    and four rows take the few-column kernel (4 and 16 (row, head) columns
+    of a KV head), 129 rows the tiled one."""
     w = W.WORKLOADS["8b"]
     mdl = w.model
     S = w.n_ctx + w.n_prompt
     _attn_case(mdl.n_q_heads, mdl.n_kv_heads, mdl.head_dim, mdl.chunk_tokens, S, np.arange(S - m, S), seed=9,
                n_split="auto")
+    if m == 4:   # four rows far apart (different splits hold their last keys)
+        _attn_case(mdl.n_q_heads, mdl.n_kv_heads, mdl.head_dim, mdl.chunk_tokens, S,
+                   np.array([5, 300, 17000, S - 1]), seed=10, n_split="auto")
 
 
 def test_attention_split_validation():
