@@ -175,7 +175,11 @@ mz_status mz_generate(mz_ctx *ctx, int32_t token, int32_t n, int32_t *tokens_out
  * (1: a layer step of a single row whose projections all run split over K
  * forms that row's RMSNorm inside them, the same f16 values the RMSNorm
  * pass writes, and leaves that pass out, default; 0: always a separate
- * pass), "swap_trim" (1: free the pinned swap segments after each restore,
+ * pass), "gemv_fused" (1: a single-row product that runs split over K
+ * adds its splits and applies its epilogue inside the same kernel, by the
+ * last workgroup of each 256-column tile; 0: a separate reduce kernel,
+ * default; experimental: not to be enabled, a test run with it hung and the
+ * cause is not known), "swap_trim" (1: free the pinned swap segments after each restore,
  * as the paper's growing swap stack does; 0: keep them for the next
  * eviction, default).  Test hooks: "debug_poison" (1: fill every
  * slot and weight unit allocated by a restore with NaN before it is

@@ -494,14 +494,83 @@ __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict_
 // gemm_splitk_reduce.  NORM: the row is RMSNorm's input, fp32 H [.][K]; each
 // workgroup first takes its scale r through the norm kernel's own routine
 // and stages (f16)(h * r), the values the norm kernel would have written.
+// The split-K reduce of one 256-column tile of a single-row product, run by
+// the last workgroup of the tile to finish (tickets: one counter per column
+// tile, zero on entry; the last workgroup sets it back to zero).  Every
+// workgroup writes its partials and fences them before taking its ticket; the
+// last one reads the splits of its tile past the L1 and adds them in split
+// order, then applies the epilogue: the same sums and the same epilogue
+// arithmetic as gemm_splitk_reduce and gemm_splitk_reduce_rope, so the same
+// bits, without their launch.
+template <int EPI>
+__device__ __forceinline__ void gemv_tile_reduce(const float* part, int N, int nt, int* tickets, void* Y,
+                                                 const GemmRope& ea) {
+  __shared__ int s_last;
+  __shared__ float s_sum[BN];
+  const int r = threadIdx.x;
+  const int ns = gridDim.y;
+  __threadfence();                         // this workgroup's partials, device-wide, before its ticket
+  __syncthreads();
+  if (r == 0) s_last = __hip_atomic_fetch_add(&tickets[nt], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) == ns - 1;
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+  const int col = nt * BN + r;
+  float a = __hip_atomic_load(part + col, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  for (int sp = 1; sp < ns; ++sp)
+    a += __hip_atomic_load(part + (size_t)sp * N + col, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (r == 0) __hip_atomic_store(&tickets[nt], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if constexpr (EPI == kEpiStore) {
+    reinterpret_cast<float*>(Y)[col] = a;
+  } else if constexpr (EPI == kEpiAdd) {
+    float* y = reinterpret_cast<float*>(Y) + col;
+    *y = a + *y;
+  } else {
+    s_sum[r] = a;
+    __syncthreads();
+    if constexpr (EPI == kEpiSwiGLU) {
+      // output column o takes gate column 32 (o / 16) + o % 16 and the up column 16 after it
+      if (r < BN / 2) {
+        const int cg = 32 * (r / 16) + r % 16;
+        const float g = s_sum[cg], u = s_sum[cg + 16];
+        reinterpret_cast<_Float16*>(Y)[(size_t)nt * (BN / 2) + r] = (_Float16)(silu(g) * u);
+      }
+    } else {
+      const int half = ea.hd >> 1;
+      const int rot = EPI == kEpiRopeQ ? ea.n_valid : ea.n_valid >> 1;   // rotated columns
+      const int64_t off = EPI == kEpiRopeKV ? ea.kv_off[0] : 0;
+      if (off < 0) return;
+      const int p = ea.pos[0];
+      if (col < rot) {
+        // the first column of each rotated pair (c, c + hd/2) of a head
+        if ((col % ea.hd) < half) {
+          const int i = col % ea.hd;
+          const float x1 = s_sum[r], x2 = s_sum[r + half];
+          const float2 cv = ea.rope_cs[(size_t)p * half + i];
+          _Float16* yr = EPI == kEpiRopeQ ? reinterpret_cast<_Float16*>(Y) : reinterpret_cast<_Float16*>(ea.slab + off);
+          const float2 y = rope_rotate(x1, x2, cv.x, cv.y);
+          yr[col] = (_Float16)y.x;
+          yr[col + half] = (_Float16)y.y;
+        }
+      } else if (EPI == kEpiRopeKV && col < ea.n_valid) {
+        const int v = col - rot;
+        const int pc = p & (ea.C - 1);
+        uint8_t* vt = ea.slab + off - (int64_t)pc * ea.n_valid + (int64_t)ea.C * ea.n_valid + pc * 2;
+        *reinterpret_cast<_Float16*>(vt + (int64_t)v * ea.C * 2) = (_Float16)s_sum[r];
+      }
+    }
+  }
+}
+
 constexpr int kGemvAhead = 8;     // K tiles whose codes are in flight per thread
 
-template <bool NORM>
+template <bool NORM, int EPI>
 __global__ __launch_bounds__(256) void gemv_q4_kernel(const _Float16* __restrict__ X,
                                                       const float* __restrict__ H, float eps,
                                                       const int32_t* __restrict__ a_rows, int K,
                                                       const uint8_t* __restrict__ Wp, int N,
-                                                      float* __restrict__ part, int k_steps) {
+                                                      float* __restrict__ part, int k_steps, int* __restrict__ tickets,
+                                                      void* __restrict__ Y, GemmRope ea) {
   __shared__ f16x2 xs[kGemvAhead * 32];   // 256 pairs: one per thread and batch
   const int nk = K / BK;
   const int split = blockIdx.y;
@@ -567,6 +636,7 @@ __global__ __launch_bounds__(256) void gemv_q4_kernel(const _Float16* __restrict
     }
   }
   part[(size_t)split * N + (size_t)nt * BN + r] = acc;
+  if constexpr (EPI != kEpiPartial) gemv_tile_reduce<EPI>(part, N, nt, tickets, Y, ea);
 }
 
 // Sum of the K splits in split order, then the epilogue; 4 columns per
@@ -827,22 +897,47 @@ int launch_partials(const void* x, int m, int n, int k, const void* w, int n_spl
   const int ks = gemm_k_steps(k, n_split);
   const int ns = (k / BK + ks - 1) / ks;
   if (h_norm)
-    hipLaunchKernelGGL(gemv_q4_kernel<true>, dim3(n / BN, ns), dim3(256), 0, s, X, h_norm, eps, a_rows, k, W, n,
-                       reinterpret_cast<float*>(ws), ks);
+    hipLaunchKernelGGL((gemv_q4_kernel<true, kEpiPartial>), dim3(n / BN, ns), dim3(256), 0, s, X, h_norm, eps, a_rows,
+                       k, W, n, reinterpret_cast<float*>(ws), ks, nullptr, nullptr, GemmRope{});
   else if (m == 1)
-    hipLaunchKernelGGL(gemv_q4_kernel<false>, dim3(n / BN, ns), dim3(256), 0, s, X, nullptr, 0.f, a_rows, k, W,
-                       n, reinterpret_cast<float*>(ws), ks);
+    hipLaunchKernelGGL((gemv_q4_kernel<false, kEpiPartial>), dim3(n / BN, ns), dim3(256), 0, s, X, nullptr, 0.f,
+                       a_rows, k, W, n, reinterpret_cast<float*>(ws), ks, nullptr, nullptr, GemmRope{});
   else if (gemm_row_tile(m, n) == 64)
     launch_bm<kEpiPartial, 64>(X, a_rows, m, n, k, W, ws, s, ns, ks);
   else
     launch_bm<kEpiPartial, 256>(X, a_rows, m, n, k, W, ws, s, ns, ks);
   return ns;
 }
+// A single-row split-K product whose reduce and epilogue run inside it, by
+// the last workgroup of each column tile (gemv_tile_reduce).
+template <int EPI>
+void launch_gemv_fused(const _Float16* X, int n, int k, const uint8_t* W, int n_split, void* ws, hipStream_t s,
+                       const int32_t* a_rows, const float* h_norm, float eps, int* tickets, void* y,
+                       const GemmRope& ea) {
+  const int ks = gemm_k_steps(k, n_split);
+  const int ns = (k / BK + ks - 1) / ks;
+  float* part = reinterpret_cast<float*>(ws);
+  if (h_norm)
+    hipLaunchKernelGGL((gemv_q4_kernel<true, EPI>), dim3(n / BN, ns), dim3(256), 0, s, X, h_norm, eps, a_rows, k, W,
+                       n, part, ks, tickets, y, ea);
+  else
+    hipLaunchKernelGGL((gemv_q4_kernel<false, EPI>), dim3(n / BN, ns), dim3(256), 0, s, X, nullptr, 0.f, a_rows, k,
+                       W, n, part, ks, tickets, y, ea);
+}
 }  // namespace
 
 void launch_gemm_q4_splitk_rope(const void* x, int m, int n, int k, const void* w, int epilogue, const GemmRope& ea,
                                 void* y, int n_split, void* ws, hipStream_t s, const int32_t* a_rows,
-                                const float* h_norm, float eps) {
+                                const float* h_norm, float eps, int* tickets) {
+  if (tickets && m == 1) {
+    const _Float16* X = reinterpret_cast<const _Float16*>(x);
+    const uint8_t* W = reinterpret_cast<const uint8_t*>(w);
+    if (epilogue == kEpiRopeQ)
+      launch_gemv_fused<kEpiRopeQ>(X, n, k, W, n_split, ws, s, a_rows, h_norm, eps, tickets, y, ea);
+    else
+      launch_gemv_fused<kEpiRopeKV>(X, n, k, W, n_split, ws, s, a_rows, h_norm, eps, tickets, y, ea);
+    return;
+  }
   const int ns = launch_partials(x, m, n, k, w, n_split, ws, s, a_rows, h_norm, eps);
   const int rot = epilogue == kEpiRopeQ ? ea.n_valid : ea.n_valid / 2;
   const int64_t per_row = rot / 2 + (epilogue == kEpiRopeKV ? ea.n_valid / 2 : 0);
@@ -855,7 +950,18 @@ void launch_gemm_q4_splitk_rope(const void* x, int m, int n, int k, const void* 
 }
 
 void launch_gemm_q4_splitk(const void* x, int m, int n, int k, const void* w, int epilogue, void* y, int n_split,
-                           void* ws, hipStream_t s, const int32_t* a_rows, const float* h_norm, float eps) {
+                           void* ws, hipStream_t s, const int32_t* a_rows, const float* h_norm, float eps,
+                           int* tickets) {
+  if (tickets && m == 1) {
+    const _Float16* X = reinterpret_cast<const _Float16*>(x);
+    const uint8_t* W = reinterpret_cast<const uint8_t*>(w);
+    switch (epilogue) {
+      case kEpiStore: launch_gemv_fused<kEpiStore>(X, n, k, W, n_split, ws, s, a_rows, h_norm, eps, tickets, y, GemmRope{}); break;
+      case kEpiAdd: launch_gemv_fused<kEpiAdd>(X, n, k, W, n_split, ws, s, a_rows, h_norm, eps, tickets, y, GemmRope{}); break;
+      default: launch_gemv_fused<kEpiSwiGLU>(X, n, k, W, n_split, ws, s, a_rows, h_norm, eps, tickets, y, GemmRope{}); break;
+    }
+    return;
+  }
   const int ns = launch_partials(x, m, n, k, w, n_split, ws, s, a_rows, h_norm, eps);
   const int64_t outs = (int64_t)m * (epilogue == kEpiSwiGLU ? n / 2 : n) / 4;
   const dim3 grid((unsigned)((outs + 255) / 256));

@@ -65,16 +65,20 @@ void launch_gemm_q4_rope(const void* x, int m, int n, int k, const void* w, int 
 // split order and applies the epilogue.  h_norm (m == 1 only): x is not read;
 // the row is RMSNorm(h_norm row, eps) formed inside the product, the same
 // f16 values launch_rmsnorm writes.
+// tickets (m == 1 only; device, one int32 per 256-column tile, zero on entry
+// and left zero; not shared with launches in flight): the reduce and the
+// epilogue run inside the product, by the last workgroup of each column
+// tile, with the same bits; no second kernel.
 void launch_gemm_q4_splitk(const void* x, int m, int n, int k, const void* w, int epilogue, void* y, int n_split,
                            void* ws, hipStream_t s, const int32_t* a_rows = nullptr,
-                           const float* h_norm = nullptr, float eps = 0.f);
+                           const float* h_norm = nullptr, float eps = 0.f, int* tickets = nullptr);
 int64_t gemm_splitk_ws_bytes(int m, int n, int n_split);
 // Split-K form with a rotary-embedding epilogue (kEpiRopeQ / kEpiRopeKV): the
 // splits are added in order, then rotated and written as the unsplit
 // epilogues do.
 void launch_gemm_q4_splitk_rope(const void* x, int m, int n, int k, const void* w, int epilogue, const GemmRope& ea,
                                 void* y, int n_split, void* ws, hipStream_t s, const int32_t* a_rows = nullptr,
-                                const float* h_norm = nullptr, float eps = 0.f);
+                                const float* h_norm = nullptr, float eps = 0.f, int* tickets = nullptr);
 // Splits that fill the chip for this shape within ws_cap bytes (1: no split).
 int gemm_auto_splits(int m, int n, int k, int64_t ws_cap);
 

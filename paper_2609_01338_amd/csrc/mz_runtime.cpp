@@ -42,6 +42,9 @@
 namespace {
 
 constexpr const char* kVersion = "mz-mi355x 0.1";
+// Column tiles of 256 that a single-row projection may have for its reduce to
+// run inside it (wider products keep the separate reduce).
+constexpr int kGemvTicketInts = 256;
 
 thread_local std::string g_load_error;
 
@@ -502,11 +505,18 @@ struct mz_ctx {
   int32_t* attn_wq = nullptr;
   bool attn_queue = true;            // option attn_queue
   int32_t* gemm_wq = nullptr;        // the same for the unsplit projections
+  int32_t* gemv_tickets = nullptr;   // per 256-column tile: the single-row split-K products' in-kernel reduce
+  bool gemv_fused = false;           // option gemv_fused (off: a run with it hung, cause not found)
   bool gemm_queue = true;            // option gemm_queue
   bool gemm_split = true;            // option gemm_split
   bool fuse_rope = true;             // option fuse_rope: RoPE (and the KV slot writes) in the GEMM epilogue
   bool fuse_norm = true;             // option fuse_norm: a single row's RMSNorm inside its split-K GEMVs
 
+  // Tile counters for a single-row split-K product of n columns whose reduce
+  // runs inside it (null: the separate reduce kernel).
+  int32_t* tickets_for(int n) const {
+    return gemv_fused && n / mzk::kGemmTileN <= kGemvTicketInts ? gemv_tickets : nullptr;
+  }
   // Y = X W^T on the compute stream, split over K when the tile grid alone
   // would leave most of the GPU idle.  hn: X is RMSNorm(hn) formed inside the
   // product (only where norm_in_gemv(m, n, k)).
@@ -514,7 +524,7 @@ struct mz_ctx {
             const int32_t* rows = nullptr, const float* hn = nullptr) {
     const int ns = gemm_split ? mzk::gemm_auto_splits(m, n, k, split_ws_bytes) : 1;
     if (ns > 1)
-      mzk::launch_gemm_q4_splitk(X, m, n, k, W, epi, Y, ns, split_ws, s, rows, hn, cfg.rms_eps);
+      mzk::launch_gemm_q4_splitk(X, m, n, k, W, epi, Y, ns, split_ws, s, rows, hn, cfg.rms_eps, tickets_for(n));
     else
       mzk::launch_gemm_q4(X, m, n, k, W, epi, Y, s, rows, gemm_queue ? gemm_wq : nullptr,
                           gemm_split ? split_ws : nullptr, split_ws_bytes);
@@ -527,7 +537,8 @@ struct mz_ctx {
     if (!fuse_rope || !mzk::gemm_rope_fusable(ea.hd, ea.C)) return false;
     const int ns = gemm_split ? mzk::gemm_auto_splits(m, n, k, split_ws_bytes) : 1;
     if (ns > 1)
-      mzk::launch_gemm_q4_splitk_rope(X, m, n, k, W, epi, ea, Y, ns, split_ws, s, rows, hn, cfg.rms_eps);
+      mzk::launch_gemm_q4_splitk_rope(X, m, n, k, W, epi, ea, Y, ns, split_ws, s, rows, hn, cfg.rms_eps,
+                                      tickets_for(n));
     else
       mzk::launch_gemm_q4_rope(X, m, n, k, W, epi, ea, Y, s, rows, nullptr, gemm_split ? split_ws : nullptr,
                                split_ws_bytes);
@@ -1268,6 +1279,8 @@ mz_status mz_load_model(const mz_model_cfg* cfg, const void* blob, size_t nbytes
     HIPCHK(hipMemset(c.attn_wq, 0, mzk::kAttnQueueInts * sizeof(int32_t)));
     c.gemm_wq = (int32_t*)dmalloc(mzk::kGemmQueueInts * sizeof(int32_t));
     HIPCHK(hipMemset(c.gemm_wq, 0, mzk::kGemmQueueInts * sizeof(int32_t)));
+    c.gemv_tickets = (int32_t*)dmalloc(kGemvTicketInts * sizeof(int32_t));
+    HIPCHK(hipMemset(c.gemv_tickets, 0, kGemvTicketInts * sizeof(int32_t)));
     HIPCHK(hipEventCreateWithFlags(&c.ev_meta, hipEventDisableTiming));
     void* stage = nullptr;
     if (hipHostMalloc(&stage, c.stage_bytes, hipHostMallocDefault) != hipSuccess || !stage)
@@ -1292,7 +1305,7 @@ void mz_free(mz_ctx* x) {
   (void)hipSetDevice(x->device);
   if (x->s_compute) (void)hipStreamSynchronize(x->s_compute);
   if (x->s_swap) (void)hipStreamSynchronize(x->s_swap);
-  void* dptrs[] = {x->codec_stage, x->d_codec_slots, x->split_ws, x->attn_wq, x->gemm_wq, x->w_slab, x->emb_nib, x->emb_sc, x->lm_nib, x->lm_sc,
+  void* dptrs[] = {x->codec_stage, x->d_codec_slots, x->split_ws, x->attn_wq, x->gemm_wq, x->gemv_tickets, x->w_slab, x->emb_nib, x->emb_sc, x->lm_nib, x->lm_sc,
                    x->rope_cs, x->kv_slab,
                    x->h[0], x->h[1], x->xb, x->qf, x->kvf, x->q16, x->act, x->logits, x->part_val,
                    x->part_idx, x->d_token, x->d_tables, x->d_pos, x->d_kvoff, x->d_dix, x->d_posq,
@@ -1328,6 +1341,7 @@ mz_status mz_set_option(mz_ctx* x, const char* key, int64_t value) {
     else if (k == "attn_queue") x->attn_queue = value != 0;
     else if (k == "gemm_queue") x->gemm_queue = value != 0;
     else if (k == "gemm_split") x->gemm_split = value != 0;
+    else if (k == "gemv_fused") x->gemv_fused = value != 0;
     else if (k == "fuse_norm") x->fuse_norm = value != 0;
     else if (k == "fuse_rope") x->fuse_rope = value != 0;
     else if (k == "kv_codec") {

@@ -412,12 +412,21 @@ def test_scaled_8b_evict_size():
 
 
 @pytest.mark.parametrize("key", ["8b", "tiny"])
-def test_decode_norm_in_gemv_same_bits(key):
+@pytest.mark.parametrize("option", [
+    "fuse_norm",
+    pytest.param("gemv_fused", marks=pytest.mark.skip(
+        reason="the in-kernel split-K reduce (option gemv_fused) is switched off: a run of this test with it hung "
+               "(killed for silence) and the cause has not been found; it stays off the GPU until it is")),
+])
+def test_decode_norm_in_gemv_same_bits(key, option):
     """Decode steps with each single row's RMSNorm formed inside its split-K
-    GEMVs (fuse_norm 1) against the separate RMSNorm pass (fuse_norm 0):
-    the same tokens, and K/V rows and logits equal bit for bit, since both
-    take the norm scale through one routine (the oracle comparison of decode
-    is test_scaled_8b_generate / test_tiny_generate_after_restore)."""
+    GEMVs (fuse_norm 1) against the separate RMSNorm pass (fuse_norm 0), and
+    with the split-K reduce and epilogue run inside the GEMV by the last
+    workgroup of each column tile (gemv_fused 1) against the separate reduce
+    kernel (gemv_fused 0): the same tokens, and K/V rows and logits equal bit
+    for bit, since both forms add the same partials in the same order through
+    the same routines (the oracle comparison of decode is
+    test_scaled_8b_generate / test_tiny_generate_after_restore)."""
     torch_cuda()
     w = W.WORKLOADS[key]
     if key == "8b":
@@ -430,7 +439,7 @@ def test_decode_norm_in_gemv_same_bits(key):
     for fuse in (1, 0):
         eng = mz.Engine(m, blob_for(w), max_ctx=S + n + 9)
         try:
-            mz.mz_set_option(eng.ctx, "fuse_norm", fuse)
+            mz.mz_set_option(eng.ctx, option, fuse)
             mz.mz_prefill_context(eng.ctx, np.concatenate([ctx, prm]))
             tok, _ = mz.mz_first_token(eng.ctx, m.vocab)
             toks = mz.mz_generate(eng.ctx, tok, n)
@@ -442,7 +451,7 @@ def test_decode_norm_in_gemv_same_bits(key):
         finally:
             eng.close()
     (t1, g1, kv1), (t0, g0, kv0) = outs
-    report("case", name=f"{key}-fuse-norm-bits", tokens=list(map(int, t1)))
+    report("case", name=f"{key}-{option}-bits", tokens=list(map(int, t1)))
     assert (t1 == t0).all(), key
     assert g1.tobytes() == g0.tobytes(), key
     for (k1, v1), (k0, v0) in zip(kv1, kv0):
