@@ -414,15 +414,17 @@ def run_ablation(mz, W, eng, w, prompt, clean_logits, recompute_tflops, link_gbp
     _, _, e1 = mz.mz_plan_evict(cfg, w.n_ctx, w.n_prompt, 0, 1, "backward-out", "all-swap")
     total = m.n_layers * nc * slot + m.n_layers * int(e1["swap_bytes"])
     mz.mz_set_option(e, "kv_codec", 1)
-    for frac in ((0.25, 0.5, 0.75, 1.0) if "size" in parts else ()):
+    cases = [(r, f) for r in ("paper", "total") for f in (0.25, 0.5, 0.75, 1.0)] if "size" in parts else []
+    for rule, frac in cases:
         want = int(total * frac)
         kv0 = np.zeros((m.n_layers, nc), np.uint8)
         ws0 = np.zeros(m.n_layers, np.uint8)
         kv, ws, _, stg, info = mz.mz_plan_evict_size(cfg, w.n_ctx, kv0, ws0, want, link_gbps * 1e9,
-                                                     recompute_tflops * 1e12, m.n_layers, w.n_prompt, True)
+                                                     recompute_tflops * 1e12, m.n_layers, w.n_prompt, True, rule)
         ts, err = [], 0.0
         for step in range(steps + 1):
-            got = mz.mz_evict_size(e, want, link_gbps * 1e9, recompute_tflops * 1e12, m.n_layers, w.n_prompt)
+            got = mz.mz_evict_size(e, want, link_gbps * 1e9, recompute_tflops * 1e12, m.n_layers, w.n_prompt,
+                                   rule)
             assert got["released"] == info["released"]
             t0 = time.perf_counter()
             mz.mz_restore_and_prefill(e, prompt)
@@ -438,13 +440,13 @@ def run_ablation(mz, W, eng, w, prompt, clean_logits, recompute_tflops, link_gbp
                                        link_gbps * 1e9, recompute_tflops * 1e12, kv_codec=True)
         tb, _ = ttft_of(kvb, wsb)
         counts = np.bincount(stg, minlength=4)
-        size_rows.append({"fraction": frac, "released_bytes": info["released"], "T": info["T"],
+        size_rows.append({"rule": rule, "fraction": frac, "released_bytes": info["released"], "T": info["T"],
                           "stage_units": {"kv_only": int(counts[0]), "kv_and_w": int(counts[1]),
                                           "w_only": int(counts[2])},
                           "swap_chunks": int((kv == W.SWAP).sum()), "drop_chunks": int((kv == W.DROP).sum()),
                           "weight_layers": n_w_s, "ttft_ms": round(t, 2), "max_logit_err_vs_clean": err,
                           "balanced_plan_same_units_ttft_ms": round(tb, 2)})
-        log(f"[ablation] evict_size {frac:4.2f} of {total / 1e9:.2f} GB: T {info['T']} stages {counts[:3].tolist()} "
+        log(f"[ablation] evict_size ({rule}) {frac:4.2f} of {total / 1e9:.2f} GB: T {info['T']} stages {counts[:3].tolist()} "
             f"swap/drop {size_rows[-1]['swap_chunks']}/{size_rows[-1]['drop_chunks']} weights {n_w_s} "
             f"TTFT {t:8.2f} ms (balanced plan, same units: {tb:8.2f} ms) max|logit - clean| {err:.3e}")
     mz.mz_set_option(e, "kv_codec", 0)

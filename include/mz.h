@@ -175,11 +175,7 @@ mz_status mz_generate(mz_ctx *ctx, int32_t token, int32_t n, int32_t *tokens_out
  * (1: a layer step of a single row whose projections all run split over K
  * forms that row's RMSNorm inside them, the same f16 values the RMSNorm
  * pass writes, and leaves that pass out, default; 0: always a separate
- * pass), "gemv_fused" (1: a single-row product that runs split over K
- * adds its splits and applies its epilogue inside the same kernel, by the
- * last workgroup of each 256-column tile; 0: a separate reduce kernel,
- * default; experimental: not to be enabled, a test run with it hung and the
- * cause is not known), "swap_trim" (1: free the pinned swap segments after each restore,
+ * pass), "swap_trim" (1: free the pinned swap segments after each restore,
  * as the paper's growing swap stack does; 0: keep them for the next
  * eviction, default).  Test hooks: "debug_poison" (1: fill every
  * slot and weight unit allocated by a restore with NaN before it is
@@ -431,6 +427,22 @@ typedef struct {
  * outside 1..n_pad, head_dim not 32/64/128, chunk_tokens not a power of two. */
 mz_status mz_q4_gemm_ex(const void *x_f16, int32_t m, int32_t n_pad, int32_t k, const void *w_packed,
                         int32_t epilogue, const mz_q4_gemm_args *args, void *y, void *stream);
+
+/* One activation row times the packed matrix in a single launch, with any
+ * epilogue of mz_q4_gemm_ex: the projections of a decode step and of a
+ * restore layer that carries one row (the prefill of Sec. 2.1 and 4.2 at
+ * m = 1).  Each workgroup owns a few output columns over the whole K range
+ * and applies the epilogue itself, so no workspace and no second kernel are
+ * needed.  The row is X row args->a_rows[0] (row 0 without a_rows); with
+ * h_norm (device fp32 [.][k]) x_f16 is not read and the row is the RMSNorm
+ * of h_norm's row with eps, formed as mz_rmsnorm forms it (the same f16
+ * values).  args as in mz_q4_gemm_ex for one output row (pos[0], kv_off[0]);
+ * work_queues and workspace must be NULL.  Results equal mz_q4_gemm's up to
+ * the order of the fp32 sums.  Errors: EINVAL for n_pad not a positive
+ * multiple of 256, k not a multiple of 64 or above 16384, the epilogue and
+ * pointer errors of mz_q4_gemm_ex, a negative eps, or a workspace. */
+mz_status mz_q4_gemv(const void *x_f16, int32_t k, const void *w_packed, int32_t n_pad, int32_t epilogue,
+                     const mz_q4_gemm_args *args, const float *h_norm, float eps, void *y, void *stream);
 
 /* Split-K form of mz_q4_gemm for few rows (the short requests of the
  * paper's evaluation, Sec. 6, and every decode step): a grid of 256-column

@@ -494,83 +494,14 @@ __global__ __launch_bounds__(NT) void gemm_q4_kernel(const _Float16* __restrict_
 // gemm_splitk_reduce.  NORM: the row is RMSNorm's input, fp32 H [.][K]; each
 // workgroup first takes its scale r through the norm kernel's own routine
 // and stages (f16)(h * r), the values the norm kernel would have written.
-// The split-K reduce of one 256-column tile of a single-row product, run by
-// the last workgroup of the tile to finish (tickets: one counter per column
-// tile, zero on entry; the last workgroup sets it back to zero).  Every
-// workgroup writes its partials and fences them before taking its ticket; the
-// last one reads the splits of its tile past the L1 and adds them in split
-// order, then applies the epilogue: the same sums and the same epilogue
-// arithmetic as gemm_splitk_reduce and gemm_splitk_reduce_rope, so the same
-// bits, without their launch.
-template <int EPI>
-__device__ __forceinline__ void gemv_tile_reduce(const float* part, int N, int nt, int* tickets, void* Y,
-                                                 const GemmRope& ea) {
-  __shared__ int s_last;
-  __shared__ float s_sum[BN];
-  const int r = threadIdx.x;
-  const int ns = gridDim.y;
-  __threadfence();                         // this workgroup's partials, device-wide, before its ticket
-  __syncthreads();
-  if (r == 0) s_last = __hip_atomic_fetch_add(&tickets[nt], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) == ns - 1;
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-  const int col = nt * BN + r;
-  float a = __hip_atomic_load(part + col, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  for (int sp = 1; sp < ns; ++sp)
-    a += __hip_atomic_load(part + (size_t)sp * N + col, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  if (r == 0) __hip_atomic_store(&tickets[nt], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  if constexpr (EPI == kEpiStore) {
-    reinterpret_cast<float*>(Y)[col] = a;
-  } else if constexpr (EPI == kEpiAdd) {
-    float* y = reinterpret_cast<float*>(Y) + col;
-    *y = a + *y;
-  } else {
-    s_sum[r] = a;
-    __syncthreads();
-    if constexpr (EPI == kEpiSwiGLU) {
-      // output column o takes gate column 32 (o / 16) + o % 16 and the up column 16 after it
-      if (r < BN / 2) {
-        const int cg = 32 * (r / 16) + r % 16;
-        const float g = s_sum[cg], u = s_sum[cg + 16];
-        reinterpret_cast<_Float16*>(Y)[(size_t)nt * (BN / 2) + r] = (_Float16)(silu(g) * u);
-      }
-    } else {
-      const int half = ea.hd >> 1;
-      const int rot = EPI == kEpiRopeQ ? ea.n_valid : ea.n_valid >> 1;   // rotated columns
-      const int64_t off = EPI == kEpiRopeKV ? ea.kv_off[0] : 0;
-      if (off < 0) return;
-      const int p = ea.pos[0];
-      if (col < rot) {
-        // the first column of each rotated pair (c, c + hd/2) of a head
-        if ((col % ea.hd) < half) {
-          const int i = col % ea.hd;
-          const float x1 = s_sum[r], x2 = s_sum[r + half];
-          const float2 cv = ea.rope_cs[(size_t)p * half + i];
-          _Float16* yr = EPI == kEpiRopeQ ? reinterpret_cast<_Float16*>(Y) : reinterpret_cast<_Float16*>(ea.slab + off);
-          const float2 y = rope_rotate(x1, x2, cv.x, cv.y);
-          yr[col] = (_Float16)y.x;
-          yr[col + half] = (_Float16)y.y;
-        }
-      } else if (EPI == kEpiRopeKV && col < ea.n_valid) {
-        const int v = col - rot;
-        const int pc = p & (ea.C - 1);
-        uint8_t* vt = ea.slab + off - (int64_t)pc * ea.n_valid + (int64_t)ea.C * ea.n_valid + pc * 2;
-        *reinterpret_cast<_Float16*>(vt + (int64_t)v * ea.C * 2) = (_Float16)s_sum[r];
-      }
-    }
-  }
-}
-
 constexpr int kGemvAhead = 8;     // K tiles whose codes are in flight per thread
 
-template <bool NORM, int EPI>
+template <bool NORM>
 __global__ __launch_bounds__(256) void gemv_q4_kernel(const _Float16* __restrict__ X,
                                                       const float* __restrict__ H, float eps,
                                                       const int32_t* __restrict__ a_rows, int K,
                                                       const uint8_t* __restrict__ Wp, int N,
-                                                      float* __restrict__ part, int k_steps, int* __restrict__ tickets,
-                                                      void* __restrict__ Y, GemmRope ea) {
+                                                      float* __restrict__ part, int k_steps) {
   __shared__ f16x2 xs[kGemvAhead * 32];   // 256 pairs: one per thread and batch
   const int nk = K / BK;
   const int split = blockIdx.y;
@@ -636,7 +567,6 @@ __global__ __launch_bounds__(256) void gemv_q4_kernel(const _Float16* __restrict
     }
   }
   part[(size_t)split * N + (size_t)nt * BN + r] = acc;
-  if constexpr (EPI != kEpiPartial) gemv_tile_reduce<EPI>(part, N, nt, tickets, Y, ea);
 }
 
 // Sum of the K splits in split order, then the epilogue; 4 columns per
@@ -721,6 +651,234 @@ __global__ __launch_bounds__(256) void gemm_splitk_reduce_rope(const float* __re
     uint8_t* vt = ea.slab + off - (int64_t)pc * ea.n_valid + (int64_t)ea.C * ea.n_valid + pc * 2;
     *reinterpret_cast<_Float16*>(vt + (int64_t)v * ea.C * 2) = (_Float16)a;
   }
+}
+
+// One activation row in one launch, with its epilogue (a decode step; a
+// restore layer that carries a single row).  Workgroup g owns CPW output
+// columns over the whole K range: no partials leave the workgroup and no
+// second kernel runs.  Lane items are (column, Q4_0 block): 2 CPW lanes
+// cover one 64-wide K tile of the CPW columns, and the 256 threads form
+// S = 128 / CPW streams that take K tiles s, s + S, s + 2S, ...  A lane reads
+// its block's 16 code bytes and 2-byte scale (the 2 CPW lanes of a K tile
+// read 32 CPW contiguous code bytes: a column's two blocks are 32 contiguous
+// bytes of the tile), decodes each code pair exactly as the GEMM does (one
+// rounding of d * (q - 8) to f16) and accumulates the products with the f16
+// activations in fp32 (v_dot2), K tiles in increasing order.  The activation
+// row is staged once in LDS.  The 2 S partial sums of a column are then added
+// in a fixed order (stream by stream, block 0 then block 1), so results are
+// deterministic; they equal the split-K form's up to the order of the fp32
+// sums.  NORM: the row is RMSNorm's input, fp32 H [.][K]; the workgroup first
+// takes its scale through the norm kernel's own routine and stages
+// (f16)(h * r), the values the norm kernel would have written.
+//
+// Column maps: kEpiSwiGLU takes CPW = 32 consecutive columns, the 16 gate and
+// the 16 up columns of output columns 16 g .. 16 g + 15.  The rotary
+// epilogues take, for workgroups of rotated columns, P = CPW / 2 pairs
+// (i, i + hd / 2) of one head, so each pair is rotated where it is summed;
+// the value columns of kEpiRopeKV follow as consecutive runs.
+template <int EPI, int CPW>
+__device__ __forceinline__ int gemv1_col(int g, int j, const GemmRope& ea) {
+  if constexpr (EPI == kEpiRopeQ || EPI == kEpiRopeKV) {
+    constexpr int P = CPW / 2;
+    const int half = ea.hd >> 1;
+    const int rot = EPI == kEpiRopeQ ? ea.n_valid : ea.n_valid >> 1;
+    const int g_rot = rot / CPW;
+    if (g < g_rot) {
+      const int per_head = half / P;
+      const int i = (g % per_head) * P + (j % P);
+      return (g / per_head) * ea.hd + i + (j >= P ? half : 0);
+    }
+    return rot + (g - g_rot) * CPW + j;
+  } else {
+    return g * CPW + j;
+  }
+}
+
+constexpr int kGemv1Batch = 8;    // K tiles whose codes are in flight per lane
+
+// Codes and scales of K tiles sid + S (i0 + u), u < kGemv1Batch, of one
+// lane.  Every load is issued, without a branch around it (a guarded load
+// made the compiler wait for each one): positions past the stream's last
+// tile reload that tile (a stream with none reloads a tile in range), and
+// gemv1_dot skips them.
+template <int S>
+__device__ __forceinline__ void gemv1_load(const uint8_t* codes, const uint8_t* scales, int sid, int i0, int n_i,
+                                           int nk, uint4 (&c)[kGemv1Batch], uint32_t (&sc)[kGemv1Batch]) {
+#pragma unroll
+  for (int u = 0; u < kGemv1Batch; ++u) {
+    const int kt = min(max(sid + S * min(i0 + u, n_i - 1), 0), nk - 1);
+    const size_t off = (size_t)kt * kGemmTileBytes;
+    c[u] = *reinterpret_cast<const uint4*>(codes + off);
+    sc[u] = *reinterpret_cast<const uint16_t*>(scales + off);
+  }
+}
+
+// acc += the products of one lane's batch with the staged activations.
+template <int S>
+__device__ __forceinline__ float gemv1_dot(const _Float16* xb, int sid, int i0, int n_i,
+                                           const uint4 (&c)[kGemv1Batch], const uint32_t (&sc)[kGemv1Batch],
+                                           float acc) {
+#pragma unroll
+  for (int u = 0; u < kGemv1Batch; ++u) {
+    if (i0 + u < n_i) {
+      const int kt = sid + S * (i0 + u);
+      const _Float16 d = __builtin_bit_cast(_Float16, (uint16_t)sc[u]);
+      const f16x2 d2 = {d, d};
+      const f16x2* xp = reinterpret_cast<const f16x2*>(xb + kt * BK);
+      const uint32_t w[4] = {c[u].x, c[u].y, c[u].z, c[u].w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint4 o = dequant_dword(w[q], d2);
+        acc = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, o.x), xp[4 * q + 0], acc, false);
+        acc = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, o.y), xp[4 * q + 1], acc, false);
+        acc = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, o.z), xp[4 * q + 2], acc, false);
+        acc = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, o.w), xp[4 * q + 3], acc, false);
+      }
+    }
+  }
+  return acc;
+}
+
+// LDS of the single-row products: the staged row is dynamic (K halves).
+struct Gemv1Lds {
+  float red[256];     // the lanes' partial sums
+  float sum[32];      // the columns' sums
+  float norm[4];      // block sum of the RMSNorm scale
+};
+
+// Workgroup g of one single-row product (see gemv1_kernel).
+template <bool NORM, int EPI, int CPW>
+__device__ __forceinline__ void gemv1_body(int g, const _Float16* __restrict__ X, const float* __restrict__ H,
+                                           float eps, const int32_t* __restrict__ a_rows, int K,
+                                           const uint8_t* __restrict__ Wp, void* __restrict__ Y,
+                                           const GemmRope& ea, _Float16* xs, Gemv1Lds& lds) {
+  constexpr int LK = 2 * CPW, S = 256 / LK;
+  float* s_red = lds.red;
+  float* s_sum = lds.sum;
+  const int t = threadIdx.x;
+  const int nk = K / BK;
+  const int item = t % LK, sid = t / LK;
+  const int j = item >> 1, blk = item & 1;
+  const int col = gemv1_col<EPI, CPW>(g, j, ea);
+  const uint8_t* wc = Wp + (size_t)(col / BN) * nk * kGemmTileBytes;
+  const uint8_t* codes = wc + (col % BN) * 32 + blk * 16;
+  const uint8_t* scales = wc + NIB_BYTES + (col % BN) * 4 + blk * 2;
+  const int n_i = sid < nk ? (nk - sid + S - 1) / S : 0;   // K tiles of this stream
+  // the first batch of weights is in flight while the row is staged
+  uint4 ca[kGemv1Batch], cb[kGemv1Batch];
+  uint32_t sa[kGemv1Batch], sb[kGemv1Batch];
+  gemv1_load<S>(codes, scales, sid, 0, n_i, nk, ca, sa);
+  const size_t row = a_rows ? a_rows[0] : 0;
+  if constexpr (NORM) {
+    float4 v[kRowNormRegs];
+    const float* hrow = H + row * K;
+    const float rn = row_inv_rms(hrow, K, eps, v, lds.norm);
+    const int n4 = K / 4;
+#pragma unroll
+    for (int k = 0; k < kRowNormRegs; ++k) {
+      const int i = t + k * 256;
+      if (i < n4) {
+        const f16x2 a = {norm_to_f16(v[k].x, rn), norm_to_f16(v[k].y, rn)};
+        const f16x2 b = {norm_to_f16(v[k].z, rn), norm_to_f16(v[k].w, rn)};
+        *reinterpret_cast<uint2*>(xs + 4 * i) =
+            make_uint2(__builtin_bit_cast(uint32_t, a), __builtin_bit_cast(uint32_t, b));
+      }
+    }
+    for (int i = t + kRowNormRegs * 256; i < n4; i += 256) {
+      const float4 h = reinterpret_cast<const float4*>(hrow)[i];
+      const f16x2 a = {norm_to_f16(h.x, rn), norm_to_f16(h.y, rn)};
+      const f16x2 b = {norm_to_f16(h.z, rn), norm_to_f16(h.w, rn)};
+      *reinterpret_cast<uint2*>(xs + 4 * i) =
+          make_uint2(__builtin_bit_cast(uint32_t, a), __builtin_bit_cast(uint32_t, b));
+    }
+  } else {
+    const uint4* xr = reinterpret_cast<const uint4*>(X + row * K);
+    for (int i = t; i < K / 8; i += 256) reinterpret_cast<uint4*>(xs)[i] = xr[i];
+  }
+  __syncthreads();   // xs staged
+  const _Float16* xb = xs + blk * 32;
+  float acc = 0.f;
+  // two batches in flight: the next one loads while this one is summed
+  for (int i0 = 0; i0 < n_i; i0 += 2 * kGemv1Batch) {
+    if (i0 + kGemv1Batch < n_i) gemv1_load<S>(codes, scales, sid, i0 + kGemv1Batch, n_i, nk, cb, sb);
+    acc = gemv1_dot<S>(xb, sid, i0, n_i, ca, sa, acc);
+    if (i0 + 2 * kGemv1Batch < n_i) gemv1_load<S>(codes, scales, sid, i0 + 2 * kGemv1Batch, n_i, nk, ca, sa);
+    if (i0 + kGemv1Batch < n_i) acc = gemv1_dot<S>(xb, sid, i0 + kGemv1Batch, n_i, cb, sb, acc);
+  }
+  s_red[t] = acc;
+  __syncthreads();
+  if (t < CPW) {
+    float a = 0.f;
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+      a += s_red[s * LK + 2 * t];
+      a += s_red[s * LK + 2 * t + 1];
+    }
+    s_sum[t] = a;
+  }
+  __syncthreads();
+  if constexpr (EPI == kEpiStore || EPI == kEpiAdd) {
+    if (t < CPW) {
+      float* y = reinterpret_cast<float*>(Y) + gemv1_col<EPI, CPW>(g, t, ea);
+      *y = EPI == kEpiAdd ? s_sum[t] + *y : s_sum[t];
+    }
+  } else if constexpr (EPI == kEpiSwiGLU) {
+    static_assert(CPW == 32, "SwiGLU takes the 16 gate and 16 up columns of 16 outputs");
+    if (t < 16) reinterpret_cast<_Float16*>(Y)[(size_t)g * 16 + t] = (_Float16)(silu(s_sum[t]) * s_sum[t + 16]);
+  } else {
+    constexpr int P = CPW / 2;
+    const int half = ea.hd >> 1;
+    const int rot = EPI == kEpiRopeQ ? ea.n_valid : ea.n_valid >> 1;
+    const int64_t off = EPI == kEpiRopeKV ? ea.kv_off[0] : 0;
+    if (off < 0) return;                       // the row writes no KV
+    const int p = ea.pos[0];
+    if (g < rot / CPW) {
+      if (t < P) {
+        const int c = gemv1_col<EPI, CPW>(g, t, ea);
+        const float2 cv = ea.rope_cs[(size_t)p * half + c % ea.hd];
+        _Float16* yr = EPI == kEpiRopeQ ? reinterpret_cast<_Float16*>(Y) : reinterpret_cast<_Float16*>(ea.slab + off);
+        const float2 y = rope_rotate(s_sum[t], s_sum[t + P], cv.x, cv.y);
+        yr[c] = (_Float16)y.x;
+        yr[c + half] = (_Float16)y.y;
+      }
+    } else if (EPI == kEpiRopeKV && t < CPW) {
+      const int v = gemv1_col<EPI, CPW>(g, t, ea) - rot;
+      const int pc = p & (ea.C - 1);
+      uint8_t* vt = ea.slab + off - (int64_t)pc * ea.n_valid + (int64_t)ea.C * ea.n_valid + pc * 2;
+      *reinterpret_cast<_Float16*>(vt + (int64_t)v * ea.C * 2) = (_Float16)s_sum[t];
+    }
+  }
+}
+
+template <bool NORM, int EPI, int CPW>
+__global__ __launch_bounds__(256) void gemv1_kernel(const _Float16* __restrict__ X,
+                                                    const float* __restrict__ H, float eps,
+                                                    const int32_t* __restrict__ a_rows, int K,
+                                                    const uint8_t* __restrict__ Wp, void* __restrict__ Y,
+                                                    GemmRope ea) {
+  extern __shared__ __align__(16) _Float16 xs[];   // the K activations of the row
+  __shared__ Gemv1Lds lds;
+  gemv1_body<NORM, EPI, CPW>(blockIdx.x, X, H, eps, a_rows, K, Wp, Y, ea, xs, lds);
+}
+
+// The query and the key/value projections of one row in one launch (a decode
+// step): workgroups [0, g_q) are the rotary query product, the rest the
+// key/value product into the chunk slot, both from the same activations.
+constexpr int kGemv1QkvCols = 8;
+template <bool NORM>
+__global__ __launch_bounds__(256) void gemv1_qkv_kernel(int g_q, const _Float16* __restrict__ X,
+                                                        const float* __restrict__ H, float eps, int K,
+                                                        const int32_t* __restrict__ rows_q,
+                                                        const uint8_t* __restrict__ Wq, void* __restrict__ Yq,
+                                                        GemmRope eq, const int32_t* __restrict__ rows_kv,
+                                                        const uint8_t* __restrict__ Wkv, GemmRope ekv) {
+  extern __shared__ __align__(16) _Float16 xs[];
+  __shared__ Gemv1Lds lds;
+  if ((int)blockIdx.x < g_q)
+    gemv1_body<NORM, kEpiRopeQ, kGemv1QkvCols>(blockIdx.x, X, H, eps, rows_q, K, Wq, Yq, eq, xs, lds);
+  else
+    gemv1_body<NORM, kEpiRopeKV, kGemv1QkvCols>(blockIdx.x - g_q, X, H, eps, rows_kv, K, Wkv, nullptr, ekv, xs,
+                                                lds);
 }
 
 template <int BM>
@@ -897,47 +1055,81 @@ int launch_partials(const void* x, int m, int n, int k, const void* w, int n_spl
   const int ks = gemm_k_steps(k, n_split);
   const int ns = (k / BK + ks - 1) / ks;
   if (h_norm)
-    hipLaunchKernelGGL((gemv_q4_kernel<true, kEpiPartial>), dim3(n / BN, ns), dim3(256), 0, s, X, h_norm, eps, a_rows,
-                       k, W, n, reinterpret_cast<float*>(ws), ks, nullptr, nullptr, GemmRope{});
+    hipLaunchKernelGGL(gemv_q4_kernel<true>, dim3(n / BN, ns), dim3(256), 0, s, X, h_norm, eps, a_rows, k, W, n,
+                       reinterpret_cast<float*>(ws), ks);
   else if (m == 1)
-    hipLaunchKernelGGL((gemv_q4_kernel<false, kEpiPartial>), dim3(n / BN, ns), dim3(256), 0, s, X, nullptr, 0.f,
-                       a_rows, k, W, n, reinterpret_cast<float*>(ws), ks, nullptr, nullptr, GemmRope{});
+    hipLaunchKernelGGL(gemv_q4_kernel<false>, dim3(n / BN, ns), dim3(256), 0, s, X, nullptr, 0.f, a_rows, k, W,
+                       n, reinterpret_cast<float*>(ws), ks);
   else if (gemm_row_tile(m, n) == 64)
     launch_bm<kEpiPartial, 64>(X, a_rows, m, n, k, W, ws, s, ns, ks);
   else
     launch_bm<kEpiPartial, 256>(X, a_rows, m, n, k, W, ws, s, ns, ks);
   return ns;
 }
-// A single-row split-K product whose reduce and epilogue run inside it, by
-// the last workgroup of each column tile (gemv_tile_reduce).
+}  // namespace
+
+namespace {
+template <bool NORM, int EPI, int CPW>
+void launch_gemv1_t(const _Float16* X, int n, int k, const uint8_t* W, const GemmRope& ea, void* y, hipStream_t s,
+                    const int32_t* a_rows, const float* h, float eps) {
+  const int cols = (EPI == kEpiRopeQ || EPI == kEpiRopeKV) ? ea.n_valid : n;
+  hipLaunchKernelGGL((gemv1_kernel<NORM, EPI, CPW>), dim3(cols / CPW), dim3(256), (size_t)k * sizeof(_Float16), s,
+                     X, h, eps, a_rows, k, W, y, ea);
+}
+
+// Columns per workgroup: 32 for SwiGLU (gate and up of 16 outputs), else 16
+// when that still gives at least 512 workgroups (two per CU), else 8.
 template <int EPI>
-void launch_gemv_fused(const _Float16* X, int n, int k, const uint8_t* W, int n_split, void* ws, hipStream_t s,
-                       const int32_t* a_rows, const float* h_norm, float eps, int* tickets, void* y,
-                       const GemmRope& ea) {
-  const int ks = gemm_k_steps(k, n_split);
-  const int ns = (k / BK + ks - 1) / ks;
-  float* part = reinterpret_cast<float*>(ws);
-  if (h_norm)
-    hipLaunchKernelGGL((gemv_q4_kernel<true, EPI>), dim3(n / BN, ns), dim3(256), 0, s, X, h_norm, eps, a_rows, k, W,
-                       n, part, ks, tickets, y, ea);
-  else
-    hipLaunchKernelGGL((gemv_q4_kernel<false, EPI>), dim3(n / BN, ns), dim3(256), 0, s, X, nullptr, 0.f, a_rows, k,
-                       W, n, part, ks, tickets, y, ea);
+void launch_gemv1_e(const _Float16* X, int n, int k, const uint8_t* W, const GemmRope& ea, void* y, hipStream_t s,
+                    const int32_t* a_rows, const float* h, float eps) {
+  const int cols = (EPI == kEpiRopeQ || EPI == kEpiRopeKV) ? ea.n_valid : n;
+  if constexpr (EPI == kEpiSwiGLU) {
+    if (h) launch_gemv1_t<true, EPI, 32>(X, n, k, W, ea, y, s, a_rows, h, eps);
+    else launch_gemv1_t<false, EPI, 32>(X, n, k, W, ea, y, s, a_rows, h, eps);
+  } else if (cols / 16 >= 512) {
+    if (h) launch_gemv1_t<true, EPI, 16>(X, n, k, W, ea, y, s, a_rows, h, eps);
+    else launch_gemv1_t<false, EPI, 16>(X, n, k, W, ea, y, s, a_rows, h, eps);
+  } else {
+    if (h) launch_gemv1_t<true, EPI, 8>(X, n, k, W, ea, y, s, a_rows, h, eps);
+    else launch_gemv1_t<false, EPI, 8>(X, n, k, W, ea, y, s, a_rows, h, eps);
+  }
 }
 }  // namespace
 
+void launch_gemv1_qkv(const void* x, int k, const void* wq, void* yq, const GemmRope& eq, const int32_t* rows_q,
+                      const void* wkv, const GemmRope& ekv, const int32_t* rows_kv, hipStream_t s,
+                      const float* h_norm, float eps) {
+  const _Float16* X = reinterpret_cast<const _Float16*>(x);
+  const int g_q = eq.n_valid / kGemv1QkvCols, g_kv = ekv.n_valid / kGemv1QkvCols;
+  const size_t lds = (size_t)k * sizeof(_Float16);
+  const uint8_t* Wq = reinterpret_cast<const uint8_t*>(wq);
+  const uint8_t* Wkv = reinterpret_cast<const uint8_t*>(wkv);
+  if (h_norm)
+    hipLaunchKernelGGL(gemv1_qkv_kernel<true>, dim3(g_q + g_kv), dim3(256), lds, s, g_q, X, h_norm, eps, k, rows_q,
+                       Wq, yq, eq, rows_kv, Wkv, ekv);
+  else
+    hipLaunchKernelGGL(gemv1_qkv_kernel<false>, dim3(g_q + g_kv), dim3(256), lds, s, g_q, X, h_norm, eps, k, rows_q,
+                       Wq, yq, eq, rows_kv, Wkv, ekv);
+}
+
+bool gemv1_ok(int n, int k) { return n > 0 && k > 0 && n % BN == 0 && k % BK == 0 && k <= kGemv1MaxK; }
+
+void launch_gemv1(const void* x, int n, int k, const void* w, int epilogue, const GemmRope& ea, void* y,
+                  hipStream_t s, const int32_t* a_rows, const float* h_norm, float eps) {
+  const _Float16* X = reinterpret_cast<const _Float16*>(x);
+  const uint8_t* W = reinterpret_cast<const uint8_t*>(w);
+  switch (epilogue) {
+    case kEpiStore: launch_gemv1_e<kEpiStore>(X, n, k, W, ea, y, s, a_rows, h_norm, eps); break;
+    case kEpiAdd: launch_gemv1_e<kEpiAdd>(X, n, k, W, ea, y, s, a_rows, h_norm, eps); break;
+    case kEpiSwiGLU: launch_gemv1_e<kEpiSwiGLU>(X, n, k, W, ea, y, s, a_rows, h_norm, eps); break;
+    case kEpiRopeQ: launch_gemv1_e<kEpiRopeQ>(X, n, k, W, ea, y, s, a_rows, h_norm, eps); break;
+    default: launch_gemv1_e<kEpiRopeKV>(X, n, k, W, ea, y, s, a_rows, h_norm, eps); break;
+  }
+}
+
 void launch_gemm_q4_splitk_rope(const void* x, int m, int n, int k, const void* w, int epilogue, const GemmRope& ea,
                                 void* y, int n_split, void* ws, hipStream_t s, const int32_t* a_rows,
-                                const float* h_norm, float eps, int* tickets) {
-  if (tickets && m == 1) {
-    const _Float16* X = reinterpret_cast<const _Float16*>(x);
-    const uint8_t* W = reinterpret_cast<const uint8_t*>(w);
-    if (epilogue == kEpiRopeQ)
-      launch_gemv_fused<kEpiRopeQ>(X, n, k, W, n_split, ws, s, a_rows, h_norm, eps, tickets, y, ea);
-    else
-      launch_gemv_fused<kEpiRopeKV>(X, n, k, W, n_split, ws, s, a_rows, h_norm, eps, tickets, y, ea);
-    return;
-  }
+                                const float* h_norm, float eps) {
   const int ns = launch_partials(x, m, n, k, w, n_split, ws, s, a_rows, h_norm, eps);
   const int rot = epilogue == kEpiRopeQ ? ea.n_valid : ea.n_valid / 2;
   const int64_t per_row = rot / 2 + (epilogue == kEpiRopeKV ? ea.n_valid / 2 : 0);
@@ -950,18 +1142,7 @@ void launch_gemm_q4_splitk_rope(const void* x, int m, int n, int k, const void* 
 }
 
 void launch_gemm_q4_splitk(const void* x, int m, int n, int k, const void* w, int epilogue, void* y, int n_split,
-                           void* ws, hipStream_t s, const int32_t* a_rows, const float* h_norm, float eps,
-                           int* tickets) {
-  if (tickets && m == 1) {
-    const _Float16* X = reinterpret_cast<const _Float16*>(x);
-    const uint8_t* W = reinterpret_cast<const uint8_t*>(w);
-    switch (epilogue) {
-      case kEpiStore: launch_gemv_fused<kEpiStore>(X, n, k, W, n_split, ws, s, a_rows, h_norm, eps, tickets, y, GemmRope{}); break;
-      case kEpiAdd: launch_gemv_fused<kEpiAdd>(X, n, k, W, n_split, ws, s, a_rows, h_norm, eps, tickets, y, GemmRope{}); break;
-      default: launch_gemv_fused<kEpiSwiGLU>(X, n, k, W, n_split, ws, s, a_rows, h_norm, eps, tickets, y, GemmRope{}); break;
-    }
-    return;
-  }
+                           void* ws, hipStream_t s, const int32_t* a_rows, const float* h_norm, float eps) {
   const int ns = launch_partials(x, m, n, k, w, n_split, ws, s, a_rows, h_norm, eps);
   const int64_t outs = (int64_t)m * (epilogue == kEpiSwiGLU ? n / 2 : n) / 4;
   const dim3 grid((unsigned)((outs + 255) / 256));

@@ -65,20 +65,34 @@ void launch_gemm_q4_rope(const void* x, int m, int n, int k, const void* w, int 
 // split order and applies the epilogue.  h_norm (m == 1 only): x is not read;
 // the row is RMSNorm(h_norm row, eps) formed inside the product, the same
 // f16 values launch_rmsnorm writes.
-// tickets (m == 1 only; device, one int32 per 256-column tile, zero on entry
-// and left zero; not shared with launches in flight): the reduce and the
-// epilogue run inside the product, by the last workgroup of each column
-// tile, with the same bits; no second kernel.
 void launch_gemm_q4_splitk(const void* x, int m, int n, int k, const void* w, int epilogue, void* y, int n_split,
                            void* ws, hipStream_t s, const int32_t* a_rows = nullptr,
-                           const float* h_norm = nullptr, float eps = 0.f, int* tickets = nullptr);
+                           const float* h_norm = nullptr, float eps = 0.f);
 int64_t gemm_splitk_ws_bytes(int m, int n, int n_split);
 // Split-K form with a rotary-embedding epilogue (kEpiRopeQ / kEpiRopeKV): the
 // splits are added in order, then rotated and written as the unsplit
 // epilogues do.
 void launch_gemm_q4_splitk_rope(const void* x, int m, int n, int k, const void* w, int epilogue, const GemmRope& ea,
                                 void* y, int n_split, void* ws, hipStream_t s, const int32_t* a_rows = nullptr,
-                                const float* h_norm = nullptr, float eps = 0.f, int* tickets = nullptr);
+                                const float* h_norm = nullptr, float eps = 0.f);
+// One activation row in one launch (m = 1, no workspace): workgroups own a
+// few output columns over the whole K range and apply the epilogue
+// themselves (any of kEpiStore .. kEpiRopeKV, with ea as for
+// launch_gemm_q4_rope).  Results equal launch_gemm_q4's up to the order of
+// the fp32 sums.  h_norm as in launch_gemm_q4_splitk.  Only where
+// gemv1_ok(n, k): n % 256 == 0, k % 64 == 0, k <= kGemv1MaxK (the row is
+// staged in LDS).
+constexpr int kGemv1MaxK = 16384;
+bool gemv1_ok(int n, int k);
+void launch_gemv1(const void* x, int n, int k, const void* w, int epilogue, const GemmRope& ea, void* y,
+                  hipStream_t s, const int32_t* a_rows = nullptr, const float* h_norm = nullptr, float eps = 0.f);
+// The rotary query product (kEpiRopeQ into yq, eq) and the key/value product
+// into the chunk slot (kEpiRopeKV, ekv) of one row in one launch, both of k
+// inputs from x (or RMSNorm(h_norm)); the same results as the two
+// launch_gemv1 calls.  Only where gemv1_ok holds for both.
+void launch_gemv1_qkv(const void* x, int k, const void* wq, void* yq, const GemmRope& eq, const int32_t* rows_q,
+                      const void* wkv, const GemmRope& ekv, const int32_t* rows_kv, hipStream_t s,
+                      const float* h_norm = nullptr, float eps = 0.f);
 // Splits that fill the chip for this shape within ws_cap bytes (1: no split).
 int gemm_auto_splits(int m, int n, int k, int64_t ws_cap);
 

@@ -42,9 +42,6 @@
 namespace {
 
 constexpr const char* kVersion = "mz-mi355x 0.1";
-// Column tiles of 256 that a single-row projection may have for its reduce to
-// run inside it (wider products keep the separate reduce).
-constexpr int kGemvTicketInts = 256;
 
 thread_local std::string g_load_error;
 
@@ -388,18 +385,21 @@ struct HostArena {
 
 enum KernelKind {
   kKEmbed, kKRmsnorm, kKGemmKV, kKRopeKV, kKGemmQ, kKRopeQ, kKGather, kKAttention, kKGemmO,
-  kKGemmGateUp, kKGemmDown, kKLmHead, kKAttentionSplit, kKCount
+  kKGemmGateUp, kKGemmDown, kKLmHead, kKAttentionSplit, kKGemmQKV1, kKCount
 };
 const char* kKindName[kKCount] = {"embed_q4", "rmsnorm", "gemm_q4_kv", "rope_kv", "gemm_q4_q",
                                   "rope_q", "gather_rows", "attention", "gemm_q4_o",
-                                  "gemm_q4_gateup", "gemm_q4_down", "lm_head_argmax", "attention_split"};
+                                  "gemm_q4_gateup", "gemm_q4_down", "lm_head_argmax", "attention_split",
+                                  "gemm_q4_qkv_one_row"};
 // HIP kernel symbol each kind launches (to line up with profiler summaries;
 // the Q and K/V projections name their unsplit RoPE-epilogue form)
 const char* kKindKernel[kKCount] = {"embed_kernel", "rmsnorm_kernel", "gemm_q4_kernel<5>",
                                     "rope_kv_kernel", "gemm_q4_kernel<4>", "rope_kv_kernel",
                                     "gather_rows_kernel", "attn_kernel", "gemm_q4_kernel<1>",
                                     "gemm_q4_kernel<2>", "gemm_q4_kernel<1>",
-                                    "lm_head_kernel+argmax_kernel", "attn_kernel<split>+attn_merge_kernel"};
+                                    "lm_head_kernel+argmax_kernel",
+                                    "attn_kernel<split>|attn_few_kernel+attn_merge_wide_kernel",
+                                    "gemv1_qkv_kernel"};
 
 struct KindStats {
   int64_t launches = 0;
@@ -505,26 +505,25 @@ struct mz_ctx {
   int32_t* attn_wq = nullptr;
   bool attn_queue = true;            // option attn_queue
   int32_t* gemm_wq = nullptr;        // the same for the unsplit projections
-  int32_t* gemv_tickets = nullptr;   // per 256-column tile: the single-row split-K products' in-kernel reduce
-  bool gemv_fused = false;           // option gemv_fused (off: a run with it hung, cause not found)
   bool gemm_queue = true;            // option gemm_queue
   bool gemm_split = true;            // option gemm_split
+  bool gemv_direct = true;           // option gemv_direct
+  bool gemv_qkv = true;              // option gemv_qkv
   bool fuse_rope = true;             // option fuse_rope: RoPE (and the KV slot writes) in the GEMM epilogue
   bool fuse_norm = true;             // option fuse_norm: a single row's RMSNorm inside its split-K GEMVs
 
-  // Tile counters for a single-row split-K product of n columns whose reduce
-  // runs inside it (null: the separate reduce kernel).
-  int32_t* tickets_for(int n) const {
-    return gemv_fused && n / mzk::kGemmTileN <= kGemvTicketInts ? gemv_tickets : nullptr;
-  }
   // Y = X W^T on the compute stream, split over K when the tile grid alone
   // would leave most of the GPU idle.  hn: X is RMSNorm(hn) formed inside the
   // product (only where norm_in_gemv(m, n, k)).
   void gemm(const void* X, int m, int n, int k, const uint8_t* W, int epi, void* Y, hipStream_t s,
             const int32_t* rows = nullptr, const float* hn = nullptr) {
+    if (gemv_one(m, n, k)) {
+      mzk::launch_gemv1(X, n, k, W, epi, mzk::GemmRope{}, Y, s, rows, hn, cfg.rms_eps);
+      return;
+    }
     const int ns = gemm_split ? mzk::gemm_auto_splits(m, n, k, split_ws_bytes) : 1;
     if (ns > 1)
-      mzk::launch_gemm_q4_splitk(X, m, n, k, W, epi, Y, ns, split_ws, s, rows, hn, cfg.rms_eps, tickets_for(n));
+      mzk::launch_gemm_q4_splitk(X, m, n, k, W, epi, Y, ns, split_ws, s, rows, hn, cfg.rms_eps);
     else
       mzk::launch_gemm_q4(X, m, n, k, W, epi, Y, s, rows, gemm_queue ? gemm_wq : nullptr,
                           gemm_split ? split_ws : nullptr, split_ws_bytes);
@@ -535,10 +534,13 @@ struct mz_ctx {
   bool gemm_rope(const void* X, int m, int n, int k, const uint8_t* W, int epi, const mzk::GemmRope& ea, void* Y,
                  hipStream_t s, const int32_t* rows, const float* hn = nullptr) {
     if (!fuse_rope || !mzk::gemm_rope_fusable(ea.hd, ea.C)) return false;
+    if (gemv_one(m, n, k)) {
+      mzk::launch_gemv1(X, n, k, W, epi, ea, Y, s, rows, hn, cfg.rms_eps);
+      return true;
+    }
     const int ns = gemm_split ? mzk::gemm_auto_splits(m, n, k, split_ws_bytes) : 1;
     if (ns > 1)
-      mzk::launch_gemm_q4_splitk_rope(X, m, n, k, W, epi, ea, Y, ns, split_ws, s, rows, hn, cfg.rms_eps,
-                                      tickets_for(n));
+      mzk::launch_gemm_q4_splitk_rope(X, m, n, k, W, epi, ea, Y, ns, split_ws, s, rows, hn, cfg.rms_eps);
     else
       mzk::launch_gemm_q4_rope(X, m, n, k, W, epi, ea, Y, s, rows, nullptr, gemm_split ? split_ws : nullptr,
                                split_ws_bytes);
@@ -547,8 +549,11 @@ struct mz_ctx {
   // A one-row product that runs as the split-K GEMV, which can normalize its
   // own input row (a decode step: the RMSNorm launch is then left out)
   bool norm_in_gemv(int m, int n, int k) const {
-    return fuse_norm && gemm_split && m == 1 && mzk::gemm_auto_splits(m, n, k, split_ws_bytes) > 1;
+    return fuse_norm && m == 1 &&
+           (gemv_one(m, n, k) || (gemm_split && mzk::gemm_auto_splits(m, n, k, split_ws_bytes) > 1));
   }
+  // A single row runs as the one-launch GEMV (option gemv_direct)
+  bool gemv_one(int m, int n, int k) const { return gemv_direct && m == 1 && mzk::gemv1_ok(n, k); }
   int32_t* d_codec_slots = nullptr;  // per restore: destination slot of each compressed chunk
   hipEvent_t ev_meta = nullptr;      // restore metadata uploaded (the swap stream reads some)
   bool timing = false;
@@ -998,8 +1003,34 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
     const bool early_wait = kv_copy[l] && P > 0 && N % C != 0 &&
                             x->kv_state[(size_t)l * MC + (nc_old - 1)] == MZ_SWAP;
     if (early_wait) HIPCHK(hipStreamWaitEvent(cs, x->ev_kv[l], 0));
+    const int32_t* qix = x->d_qix + qofs[l];
+    const int32_t* posq = x->d_posq + qofs[l];
+    // a single row's query and key/value products in one launch
+    const bool qkv1 = x->gemv_qkv && nd == 1 && nq == 1 && x->fuse_rope && mzk::gemm_rope_fusable(x->hd, C) &&
+                      x->gemv_one(1, x->kv_pad, d) && x->gemv_one(1, x->dq_pad, d);
+    if (qkv1) {
+      mzk::GemmRope ekv, eq;
+      ekv.pos = x->d_pos + dofs[l];
+      ekv.kv_off = x->d_kvoff + dofs[l];
+      ekv.rope_cs = x->rope_cs;
+      ekv.slab = x->kv_slab;
+      ekv.hd = x->hd;
+      ekv.n_valid = 2 * x->dkv;
+      ekv.C = C;
+      eq.pos = posq;
+      eq.rope_cs = x->rope_cs;
+      eq.hd = x->hd;
+      eq.n_valid = x->dq;
+      eq.C = C;
+      x->timed(kKGemmQKV1, 2.0 * d * (2 * x->dkv + x->dq), (2.0 * x->dkv + x->dq) * d * bpe_w +
+                                                              d * 4.0 + (2 * x->dkv + x->dq) * 2.0,
+               cs, [&] {
+                 mzk::launch_gemv1_qkv(x->xb, d, unit + x->off_q, x->q16, eq, qix, unit + x->off_kv, ekv,
+                                       x->d_dix + dofs[l], cs, hn1, x->cfg.rms_eps);
+               });
+    }
     // keys and values of the rows written at this layer (D_l)
-    if (nd > 0) {
+    if (nd > 0 && !qkv1) {
       const int32_t* dix = x->d_dix + dofs[l];
       mzk::GemmRope ea;
       ea.pos = x->d_pos + dofs[l];
@@ -1026,9 +1057,7 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
     if (kv_copy[l] && !early_wait) HIPCHK(hipStreamWaitEvent(cs, x->ev_kv[l], 0));
     // queries, attention and MLP of the rows carried on (R_{l+1}; the last
     // position after the last layer)
-    const int32_t* qix = x->d_qix + qofs[l];
-    const int32_t* posq = x->d_posq + qofs[l];
-    {
+    if (!qkv1) {
       mzk::GemmRope ea;
       ea.pos = posq;
       ea.rope_cs = x->rope_cs;
@@ -1279,8 +1308,6 @@ mz_status mz_load_model(const mz_model_cfg* cfg, const void* blob, size_t nbytes
     HIPCHK(hipMemset(c.attn_wq, 0, mzk::kAttnQueueInts * sizeof(int32_t)));
     c.gemm_wq = (int32_t*)dmalloc(mzk::kGemmQueueInts * sizeof(int32_t));
     HIPCHK(hipMemset(c.gemm_wq, 0, mzk::kGemmQueueInts * sizeof(int32_t)));
-    c.gemv_tickets = (int32_t*)dmalloc(kGemvTicketInts * sizeof(int32_t));
-    HIPCHK(hipMemset(c.gemv_tickets, 0, kGemvTicketInts * sizeof(int32_t)));
     HIPCHK(hipEventCreateWithFlags(&c.ev_meta, hipEventDisableTiming));
     void* stage = nullptr;
     if (hipHostMalloc(&stage, c.stage_bytes, hipHostMallocDefault) != hipSuccess || !stage)
@@ -1305,7 +1332,7 @@ void mz_free(mz_ctx* x) {
   (void)hipSetDevice(x->device);
   if (x->s_compute) (void)hipStreamSynchronize(x->s_compute);
   if (x->s_swap) (void)hipStreamSynchronize(x->s_swap);
-  void* dptrs[] = {x->codec_stage, x->d_codec_slots, x->split_ws, x->attn_wq, x->gemm_wq, x->gemv_tickets, x->w_slab, x->emb_nib, x->emb_sc, x->lm_nib, x->lm_sc,
+  void* dptrs[] = {x->codec_stage, x->d_codec_slots, x->split_ws, x->attn_wq, x->gemm_wq, x->w_slab, x->emb_nib, x->emb_sc, x->lm_nib, x->lm_sc,
                    x->rope_cs, x->kv_slab,
                    x->h[0], x->h[1], x->xb, x->qf, x->kvf, x->q16, x->act, x->logits, x->part_val,
                    x->part_idx, x->d_token, x->d_tables, x->d_pos, x->d_kvoff, x->d_dix, x->d_posq,
@@ -1341,7 +1368,8 @@ mz_status mz_set_option(mz_ctx* x, const char* key, int64_t value) {
     else if (k == "attn_queue") x->attn_queue = value != 0;
     else if (k == "gemm_queue") x->gemm_queue = value != 0;
     else if (k == "gemm_split") x->gemm_split = value != 0;
-    else if (k == "gemv_fused") x->gemv_fused = value != 0;
+    else if (k == "gemv_direct") x->gemv_direct = value != 0;
+    else if (k == "gemv_qkv") x->gemv_qkv = value != 0;
     else if (k == "fuse_norm") x->fuse_norm = value != 0;
     else if (k == "fuse_rope") x->fuse_rope = value != 0;
     else if (k == "kv_codec") {
@@ -1797,6 +1825,42 @@ mz_status mz_q4_gemm_ex(const void* x_f16, int32_t m, int32_t n_pad, int32_t k, 
     } else {
       fail(MZ_EINVAL, "bad epilogue");
     }
+    HIPCHK(hipGetLastError());
+  });
+}
+
+mz_status mz_q4_gemv(const void* x_f16, int32_t k, const void* w_packed, int32_t n_pad, int32_t epilogue,
+                     const mz_q4_gemm_args* args, const float* h_norm, float eps, void* y, void* stream) {
+  return guarded(nullptr, [&] {
+    const mz_q4_gemm_args a = args ? *args : mz_q4_gemm_args{};
+    if ((!x_f16 && !h_norm) || !w_packed) fail(MZ_EINVAL, "NULL pointer");
+    if (!mzk::gemv1_ok(n_pad, k))
+      fail(MZ_EINVAL, "n_pad must be a positive multiple of %d and k of %d, k at most %d", mzk::kGemmTileN,
+           mzk::kGemmTileK, mzk::kGemv1MaxK);
+    if (h_norm && !(eps >= 0.f)) fail(MZ_EINVAL, "eps must be >= 0");
+    if (a.work_queues || a.workspace) fail(MZ_EINVAL, "the single-row product takes no work queues or workspace");
+    mzk::GemmRope ea;
+    if (epilogue >= 0 && epilogue <= 2) {
+      if (!y) fail(MZ_EINVAL, "NULL y");
+    } else if (epilogue == mzk::kEpiRopeQ || epilogue == mzk::kEpiRopeKV) {
+      if (!a.pos || !a.rope_cs) fail(MZ_EINVAL, "the rotary epilogues need pos and rope_cs");
+      if (epilogue == mzk::kEpiRopeQ && !y) fail(MZ_EINVAL, "NULL y");
+      if (epilogue == mzk::kEpiRopeKV && (!a.kv_off || !a.slab)) fail(MZ_EINVAL, "epilogue 5 needs kv_off and slab");
+      if (!mzk::gemm_rope_fusable(a.head_dim, epilogue == mzk::kEpiRopeKV ? a.chunk_tokens : 1))
+        fail(MZ_EINVAL, "head_dim must be 32, 64 or 128 and chunk_tokens a power of two");
+      if (a.n_valid < 1 || a.n_valid > n_pad || a.n_valid % (epilogue == mzk::kEpiRopeKV ? 2 * a.head_dim : a.head_dim))
+        fail(MZ_EINVAL, "n_valid must be whole heads within n_pad");
+      ea.pos = a.pos;
+      ea.kv_off = a.kv_off;
+      ea.rope_cs = reinterpret_cast<const float2*>(a.rope_cs);
+      ea.slab = reinterpret_cast<uint8_t*>(a.slab);
+      ea.hd = a.head_dim;
+      ea.n_valid = a.n_valid;
+      ea.C = epilogue == mzk::kEpiRopeKV ? a.chunk_tokens : 1;
+    } else {
+      fail(MZ_EINVAL, "bad epilogue");
+    }
+    mzk::launch_gemv1(x_f16, n_pad, k, w_packed, epilogue, ea, y, (hipStream_t)stream, a.a_rows, h_norm, eps);
     HIPCHK(hipGetLastError());
   });
 }

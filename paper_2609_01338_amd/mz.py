@@ -115,6 +115,7 @@ def lib() -> ctypes.CDLL:
         "mz_attention_queued": ([vp, vp, i32, vp, vp, i32, i32, i32, i32, i32, vp, vp, vp], i32),
         "mz_q4_gemm_queued": ([vp, i32, i32, i32, vp, i32, vp, vp, vp], i32),
         "mz_q4_gemm_ex": ([vp, i32, i32, i32, vp, i32, ctypes.POINTER(mz_q4_gemm_args), vp, vp], i32),
+        "mz_q4_gemv": ([vp, i32, vp, i32, i32, ctypes.POINTER(mz_q4_gemm_args), vp, ctypes.c_float, vp, vp], i32),
         "mz_rmsnorm": ([vp, i32, i32, ctypes.c_float, vp, vp], i32),
         "mz_probe_ceilings": ([i32, ctypes.c_char_p, sz], i32),
         "mz_plan_evict": ([ctypes.POINTER(mz_model_cfg), ctypes.POINTER(mz_evict_request), vp, vp, vp], i32),
@@ -355,6 +356,17 @@ def mz_q4_gemm_ex(x_ptr: int, m: int, n_pad: int, k: int, w_ptr: int, epilogue: 
     a = mz_q4_gemm_args(a_rows or None, work_queues or None, workspace or None, workspace_bytes, pos or None,
                         rope_cs or None, kv_off or None, slab or None, head_dim, n_valid, chunk_tokens)
     _check(lib().mz_q4_gemm_ex(x_ptr, m, n_pad, k, w_ptr, epilogue, ctypes.byref(a), y_ptr or None, stream), None)
+
+
+def mz_q4_gemv(x_ptr: Optional[int], k: int, w_ptr: int, n_pad: int, epilogue: int, y_ptr: Optional[int],
+               stream: Optional[int] = None, a_rows: int = 0, h_norm: int = 0, eps: float = 0.0, pos: int = 0,
+               rope_cs: int = 0, kv_off: int = 0, slab: int = 0, head_dim: int = 0, n_valid: int = 0,
+               chunk_tokens: int = 0) -> None:
+    """Device pointers as integers (0: absent)."""
+    a = mz_q4_gemm_args(a_rows or None, None, None, 0, pos or None, rope_cs or None, kv_off or None, slab or None,
+                        head_dim, n_valid, chunk_tokens)
+    _check(lib().mz_q4_gemv(x_ptr or None, k, w_ptr, n_pad, epilogue, ctypes.byref(a), h_norm or None, eps,
+                            y_ptr or None, stream), None)
 
 
 def mz_attention(q_ptr: int, qpos_ptr: int, m: int, slab_ptr: int, table_ptr: int, n_table: int,

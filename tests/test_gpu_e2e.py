@@ -411,22 +411,16 @@ def test_scaled_8b_evict_size():
     _size_flow(w, [half // 2, half - half // 2, 10 ** 13], 56e9, 1e13, 2, prm, "8b-size", codec=True)
 
 
+@pytest.mark.parametrize("option", ["fuse_norm", "gemv_qkv"])
 @pytest.mark.parametrize("key", ["8b", "tiny"])
-@pytest.mark.parametrize("option", [
-    "fuse_norm",
-    pytest.param("gemv_fused", marks=pytest.mark.skip(
-        reason="the in-kernel split-K reduce (option gemv_fused) is switched off: a run of this test with it hung "
-               "(killed for silence) and the cause has not been found; it stays off the GPU until it is")),
-])
-def test_decode_norm_in_gemv_same_bits(key, option):
-    """Decode steps with each single row's RMSNorm formed inside its split-K
-    GEMVs (fuse_norm 1) against the separate RMSNorm pass (fuse_norm 0), and
-    with the split-K reduce and epilogue run inside the GEMV by the last
-    workgroup of each column tile (gemv_fused 1) against the separate reduce
-    kernel (gemv_fused 0): the same tokens, and K/V rows and logits equal bit
-    for bit, since both forms add the same partials in the same order through
-    the same routines (the oracle comparison of decode is
-    test_scaled_8b_generate / test_tiny_generate_after_restore)."""
+def test_decode_fused_paths_same_bits(key, option):
+    """Decode steps with a fused path on (1) and off (0): the same tokens,
+    and K/V rows and logits equal bit for bit.  fuse_norm: each single row's
+    RMSNorm formed inside its single-row products against the separate
+    RMSNorm pass (both take the norm scale through one routine).  gemv_qkv:
+    the query and key/value products of the row in one launch against two
+    (the same per-workgroup code).  The oracle comparison of decode is
+    test_scaled_8b_generate / test_tiny_generate_after_restore."""
     torch_cuda()
     w = W.WORKLOADS[key]
     if key == "8b":
@@ -462,9 +456,10 @@ def test_decode_norm_in_gemv_same_bits(key, option):
 def test_rope_fused_same_bits(gemm_split):
     """The rotary embedding in the projection epilogues and split-K reduces
     (fuse_rope 1) against the projection followed by the separate RoPE pass
-    (fuse_rope 0): a clean prefill (many rows) and decode steps (one row; split
-    over K unless gemm_split is 0) give the same tokens, K/V and logits bit
-    for bit, since every path rotates through one routine."""
+    (fuse_rope 0): a clean prefill (many rows, its ragged remainder split over
+    K unless gemm_split is 0) and decode steps (one row: the single-row
+    product) give the same tokens, K/V and logits bit for bit, since every
+    path rotates through one routine."""
     torch_cuda()
     w = W.WORKLOADS["8b"].scaled(n_layers=2, n_ctx=512, n_prompt=16)
     m = w.model

@@ -301,6 +301,159 @@ def test_gemm_restore_launches(key):
                 assert np.abs(a1 - a2).max() <= 4 * F16_REL * scale, (key, rows_name, epi)
 
 
+def _single_row_shapes(key):
+    m = W.WORKLOADS[key].model
+    ffp = (m.d_ffn + 127) // 128 * 128      # the SwiGLU output width, as the down projection reads it
+    return [("q-rope", m.dq, m.d_model, 4), ("kv-rope-slots", 2 * m.dkv, m.d_model, 5),
+            ("q-store", m.dq, m.d_model, 0), ("o-add", m.d_model, m.dq, 1),
+            ("gateup-swiglu", m.d_ffn, m.d_model, 2), ("down-add", m.d_model, ffp, 1)]
+
+
+@pytest.mark.parametrize("key", ["tiny", "1b", "3b", "1p5b", "8b"])
+def test_gemv_single_row(key):
+    """mz_q4_gemv, the one-launch single-row product (decode steps), for every
+    projection of the workload at its full shape, with each epilogue the
+    runtime gives it: against the exact product of the decoded weights (and
+    the oracle's rotary embedding) on every output column, for a row picked
+    from a matrix through a_rows; the RMSNorm-forming variant against the
+    same product of mz_rmsnorm's output, bit for bit."""
+    torch = torch_cuda()
+    w = W.WORKLOADS[key]
+    m = w.model
+    hd, C = m.head_dim, m.chunk_tokens
+    rng = np.random.default_rng(23)
+    gen = torch.Generator(device="cuda").manual_seed(23)
+    n_rows = 5
+    row = 3
+    d_row = torch.tensor([row], device="cuda", dtype=torch.int32)
+    p = int(w.n_ctx + w.n_prompt - 1)                 # the position of a decode row
+    cs = torch.from_numpy(_rope_table(p + 1, hd, m.rope_theta)).cuda()
+    d_pos = torch.tensor([p], device="cuda", dtype=torch.int32)
+    for name, N, K, epi in _single_row_shapes(key):
+        report("gemv", workload=key, proj=name, N=N, K=K, epi=epi)
+        X = torch.randn(n_rows, K, device="cuda", generator=gen).to(torch.float16)
+        xs = X[row].float().cpu().numpy().astype(np.float64)[None, :]
+        if epi == 2:
+            g_ = W.encode_q4_0((rng.standard_normal((N, K)) * 0.02).astype(np.float32))
+            u_ = W.encode_q4_0((rng.standard_normal((N, K)) * 0.02).astype(np.float32))
+            wdev = torch.from_numpy(mz.mz_q4_gemm_pack(g_, N, K, w_up=u_)).cuda()
+            n_pad = 2 * ((N + 127) // 128 * 128)
+            G, U = O.q4_0_decode(g_.reshape(-1), N, K), O.q4_0_decode(u_.reshape(-1), N, K)
+        elif epi == 5:
+            half_n = N // 2
+            rk = W.encode_q4_0((rng.standard_normal((half_n, K)) * 0.02).astype(np.float32))
+            rv = W.encode_q4_0((rng.standard_normal((half_n, K)) * 0.02).astype(np.float32))
+            wdev = torch.from_numpy(mz.mz_q4_gemm_pack(np.concatenate([rk, rv]), N, K)).cuda()
+            n_pad = (N + 255) // 256 * 256
+            Wk, Wv = O.q4_0_decode(rk.reshape(-1), half_n, K), O.q4_0_decode(rv.reshape(-1), half_n, K)
+        else:
+            raw = W.encode_q4_0((rng.standard_normal((N, K)) * 0.02).astype(np.float32))
+            wdev = torch.from_numpy(mz.mz_q4_gemm_pack(raw, N, K)).cuda()
+            n_pad = (N + 255) // 256 * 256
+            Wm = O.q4_0_decode(raw.reshape(-1), N, K)
+
+        def run(x_ptr, h_ptr, out):
+            kw = dict(a_rows=d_row.data_ptr(), h_norm=h_ptr, eps=float(m.rms_eps))
+            if epi == 4:
+                kw.update(pos=d_pos.data_ptr(), rope_cs=cs.data_ptr(), head_dim=hd, n_valid=N)
+            if epi == 5:
+                kw.update(pos=d_pos.data_ptr(), rope_cs=cs.data_ptr(), kv_off=d_off.data_ptr(),
+                          slab=out.data_ptr(), head_dim=hd, n_valid=N, chunk_tokens=C)
+            mz.mz_q4_gemv(x_ptr, K, wdev.data_ptr(), n_pad, epi, 0 if epi == 5 else out.data_ptr(), stream(),
+                          **kw)
+
+        if epi == 5:
+            slot_bytes = C * (N // 2) * 4
+            slot, pc = 2, p % C
+            out = torch.full((4 * slot_bytes // 2,), float("nan"), device="cuda", dtype=torch.float16)
+            d_off = torch.tensor([slot * slot_bytes + pc * (N // 2) * 2], device="cuda", dtype=torch.int64)
+        elif epi == 4:
+            out = torch.full((1, N), float("nan"), device="cuda", dtype=torch.float16)
+        elif epi == 2:
+            out = torch.full((1, n_pad // 2), float("nan"), device="cuda", dtype=torch.float16)
+        elif epi == 1:
+            out = torch.randn(1, n_pad, device="cuda", generator=gen)
+        else:
+            out = torch.full((1, n_pad), float("nan"), device="cuda")
+        out0 = out.clone()
+        run(X.data_ptr(), 0, out)
+        torch.cuda.synchronize()
+        if epi == 4:
+            prod = xs @ Wm.T
+            b = REL * (np.abs(xs) @ np.abs(Wm).T) + 1e-6
+            ref = O.rope(prod.reshape(1, m.n_q_heads, hd), np.array([p]), m.rope_theta).reshape(1, N)
+            bh = b.reshape(1, m.n_q_heads, hd)
+            bound = (bh + np.concatenate([bh[..., hd // 2:], bh[..., :hd // 2]], -1)).reshape(1, N)
+            bound = bound + F16_REL * np.abs(ref) + 2.0 ** -22 * np.abs(prod).max()
+            got = out.float().cpu().numpy().astype(np.float64)
+        elif epi == 5:
+            dkv = N // 2
+            pk, pv = xs @ Wk.T, xs @ Wv.T
+            bk = REL * (np.abs(xs) @ np.abs(Wk).T) + 1e-6
+            bv = REL * (np.abs(xs) @ np.abs(Wv).T) + 1e-6
+            kref = O.rope(pk.reshape(1, m.n_kv_heads, hd), np.array([p]), m.rope_theta).reshape(1, dkv)
+            bkh = bk.reshape(1, m.n_kv_heads, hd)
+            kb = (bkh + np.concatenate([bkh[..., hd // 2:], bkh[..., :hd // 2]], -1)).reshape(1, dkv)
+            kb = kb + F16_REL * np.abs(kref) + 2.0 ** -22 * np.abs(pk).max()
+            sl = out.view(torch.uint8).cpu().numpy()
+            off = slot * slot_bytes + pc * dkv * 2
+            kg = sl[off:off + dkv * 2].view(np.float16).astype(np.float64)[None, :]
+            base = slot * slot_bytes + C * dkv * 2
+            vt = sl[base:base + dkv * C * 2].view(np.float16).reshape(dkv, C)[:, pc].astype(np.float64)[None, :]
+            got = np.concatenate([kg, vt], 1)
+            ref = np.concatenate([kref, pv], 1)
+            bound = np.concatenate([kb, bv + F16_REL * np.abs(pv)], 1)
+            # nothing else of the slab was written
+            touched = np.zeros(sl.size // 2, bool)
+            touched[off // 2: off // 2 + dkv] = True
+            touched[base // 2 + np.arange(dkv) * C + pc] = True
+            assert np.all(np.isnan(out.float().cpu().numpy()[~touched]))
+        elif epi == 2:
+            gr, ur = xs @ G.T, xs @ U.T
+            bg = REL * (np.abs(xs) @ np.abs(G).T) + 1e-6
+            bu = REL * (np.abs(xs) @ np.abs(U).T) + 1e-6
+            ref = O.silu(gr) * ur
+            bound = 1.1 * bg * (np.abs(ur) + bu) + np.abs(O.silu(gr)) * bu + REL * np.abs(ref) + 1e-6
+            ys = out.float().cpu().numpy().astype(np.float64)
+            got = ys[:, :N]
+            assert np.all(ys[:, N:] == 0)          # padded gate/up columns give silu(0) * 0
+        else:
+            ref = xs @ Wm.T + (out0.cpu().numpy().astype(np.float64)[:, :N] if epi == 1 else 0.0)
+            bound = REL * (np.abs(xs) @ np.abs(Wm).T) + 1e-5 * (1 + np.abs(ref))
+            got = out.cpu().numpy().astype(np.float64)[:, :N]
+        err = np.abs(got - ref)
+        report("  err", max=float(err.max()), worst_ratio=float((err / bound).max()))
+        assert np.all(err <= bound), (key, name)
+        # the RMSNorm-forming variant: the same bits as the product of mz_rmsnorm's rows
+        if K == m.d_model:
+            H = torch.randn(n_rows, K, device="cuda", generator=gen) * 3.0
+            Xn = torch.empty(n_rows, K, device="cuda", dtype=torch.float16)
+            mz.mz_rmsnorm(H.data_ptr(), n_rows, K, float(m.rms_eps), Xn.data_ptr(), stream())
+            o1, o2 = out0.clone(), out0.clone()
+            if epi == 5:
+                o1.fill_(float("nan"))
+                o2.fill_(float("nan"))
+            run(Xn.data_ptr(), 0, o1)
+            run(0, H.data_ptr(), o2)
+            torch.cuda.synchronize()
+            assert torch.equal(o1.view(torch.uint8), o2.view(torch.uint8)), (key, name, "norm in gemv")
+
+
+def test_gemv_validation():
+    torch = torch_cuda()
+    x = torch.zeros(1, 256, device="cuda", dtype=torch.float16)
+    w = torch.zeros(mz.mz_q4_gemm_packed_bytes(256, 256), device="cuda", dtype=torch.uint8)
+    y = torch.zeros(1, 256, device="cuda")
+    bad = [dict(k=256, n_pad=100, epi=0), dict(k=100, n_pad=256, epi=0), dict(k=16448, n_pad=256, epi=0),
+           dict(k=256, n_pad=256, epi=3), dict(k=256, n_pad=256, epi=4)]
+    for b in bad:
+        with pytest.raises(mz.MzError):
+            mz.mz_q4_gemv(x.data_ptr(), b["k"], w.data_ptr(), b["n_pad"], b["epi"], y.data_ptr(), stream())
+    with pytest.raises(mz.MzError):
+        mz.mz_q4_gemv(x.data_ptr(), 256, w.data_ptr(), 256, 0, y.data_ptr(), stream(), h_norm=y.data_ptr(),
+                      eps=-1.0)
+
+
 @pytest.mark.parametrize("M,N,K,epi", [
     (20000, 14336, 128, 0), (16640, 16384, 64, 1), (20000, 7168, 128, 2), (33000, 8192, 64, 1),
     (1000, 2048, 512, 0), (9000, 4096, 512, 1), (300, 512, 128, 1)])
