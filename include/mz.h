@@ -437,7 +437,10 @@ mz_status mz_q4_gemm_ex(const void *x_f16, int32_t m, int32_t n_pad, int32_t k, 
  * h_norm (device fp32 [.][k]) x_f16 is not read and the row is the RMSNorm
  * of h_norm's row with eps, formed as mz_rmsnorm forms it (the same f16
  * values).  args as in mz_q4_gemm_ex for one output row (pos[0], kv_off[0]);
- * work_queues and workspace must be NULL.  Results equal mz_q4_gemm's up to
+ * work_queues and workspace must be NULL.  The products of the 4-bit codes
+ * with the f16 activations are exact and each block's scale is applied to
+ * its fp32 sum, so no weight is rounded to f16 (mz_q4_gemm rounds
+ * d * (q - 8) to f16): results agree with mz_q4_gemm's to that rounding and
  * the order of the fp32 sums.  Errors: EINVAL for n_pad not a positive
  * multiple of 256, k not a multiple of 64 or above 16384, the epilogue and
  * pointer errors of mz_q4_gemm_ex, a negative eps, or a workspace. */

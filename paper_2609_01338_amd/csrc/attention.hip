@@ -773,7 +773,8 @@ __global__ __launch_bounds__(64 * kFewWaves) void attn_few_kernel(
 // splits that hold keys of the query: O = sum_s 2^(m_s - M) l_s o_s / sum_s
 // 2^(m_s - M) l_s.  Split 0 always holds key 0, so the denominator is
 // positive; splits past the one holding the query's own position were not
-// written for it and are not read.  64 lanes of output dimensions x 4 groups
+// written for it: they are loaded with the others (the workspace holds every
+// split) but not used.  64 lanes of output dimensions x 4 groups
 // of splits (split g + 4k in group g, at most 64 splits), the group maxima,
 // denominators and sums combined through LDS.
 template <int HD>
@@ -787,15 +788,26 @@ __global__ __launch_bounds__(256) void attn_merge_wide_kernel(const _Float16* __
   const int e = blockIdx.x;                       // (row, head)
   const int qi = e / nq;
   const int t = threadIdx.x, dl = t & 63, sg = t >> 6;
-  const int nv = min(n_split, (qpos[qi] / KT) / tps + 1);
   const size_t stride = (size_t)M * nq;
+  // every load goes out at once, from split indices clamped into the
+  // workspace (a branch around each load made the compiler wait for each);
+  // entries past the row's splits are masked below, never used
+  const int qp = qpos[qi];
   float2 ml[16];
+  _Float16 pv[16][DPL];
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    const int sp = min(sg + 4 * k, n_split - 1);
+    ml[k] = MLpart[sp * stride + e];
+    const _Float16* p = Opart + ((size_t)sp * stride + e) * HD + dl * DPL;
+#pragma unroll
+    for (int q = 0; q < DPL; ++q) pv[k][q] = p[q];
+  }
+  const int nv = min(n_split, (qp / KT) / tps + 1);
   float mx = -INFINITY;
 #pragma unroll
   for (int k = 0; k < 16; ++k) {
-    const int sp = sg + 4 * k;
-    ml[k] = sp < nv ? MLpart[sp * stride + e] : make_float2(-INFINITY, 0.f);
-    if (!(ml[k].y > 0.f)) ml[k].x = -INFINITY;
+    if (!(sg + 4 * k < nv && ml[k].y > 0.f)) ml[k].x = -INFINITY;
     mx = fmaxf(mx, ml[k].x);
   }
   if (dl == 0) s_m[sg] = mx;
@@ -804,13 +816,11 @@ __global__ __launch_bounds__(256) void attn_merge_wide_kernel(const _Float16* __
   float den = 0.f, acc[DPL] = {};
 #pragma unroll
   for (int k = 0; k < 16; ++k) {
-    const int sp = sg + 4 * k;
-    if (sp >= nv) break;
-    const float wgt = ml[k].x == -INFINITY ? 0.f : exp2f(ml[k].x - mx) * ml[k].y;
+    if (ml[k].x == -INFINITY) continue;       // past the row's splits, or a range it sees nothing of
+    const float wgt = exp2f(ml[k].x - mx) * ml[k].y;
     den += wgt;
-    const _Float16* p = Opart + ((size_t)sp * stride + e) * HD + dl * DPL;
 #pragma unroll
-    for (int q = 0; q < DPL; ++q) acc[q] = __builtin_fmaf(wgt, (float)p[q], acc[q]);
+    for (int q = 0; q < DPL; ++q) acc[q] = __builtin_fmaf(wgt, (float)pv[k][q], acc[q]);
   }
   if (dl == 0) s_d[sg] = den;
 #pragma unroll

@@ -661,10 +661,10 @@ __global__ __launch_bounds__(256) void gemm_splitk_reduce_rope(const float* __re
 // S = 128 / CPW streams that take K tiles s, s + S, s + 2S, ...  A lane reads
 // its block's 16 code bytes and 2-byte scale (the 2 CPW lanes of a K tile
 // read 32 CPW contiguous code bytes: a column's two blocks are 32 contiguous
-// bytes of the tile), decodes each code pair exactly as the GEMM does (one
-// rounding of d * (q - 8) to f16) and accumulates the products with the f16
-// activations in fp32 (v_dot2), K tiles in increasing order.  The activation
-// row is staged once in LDS.  The 2 S partial sums of a column are then added
+// bytes of the tile) and adds the block's exact code-activation products,
+// then d times the block's sum, in fp32 (gemv1_dot), K tiles in increasing
+// order.  The activation row is staged once in LDS with the sum of each of
+// its 32-element blocks.  The 2 S partial sums of a column are then added
 // in a fixed order (stream by stream, block 0 then block 1), so results are
 // deterministic; they equal the split-K form's up to the order of the fp32
 // sums.  NORM: the row is RMSNorm's input, fp32 H [.][K]; the workgroup first
@@ -713,31 +713,51 @@ __device__ __forceinline__ void gemv1_load(const uint8_t* codes, const uint8_t* 
   }
 }
 
-// acc += the products of one lane's batch with the staged activations.
+// acc += the products of one lane's batch with the staged activations.  A
+// block's codes are not decoded to weights: one v_and_or_b32 per code pair
+// makes the pair an exact f16 integer, 1024 + q for a pair at bits 0-3 and
+// 64 + q for a pair at bits 4-7 (the exponent-bias conversion of the GEMM's
+// dequant without its subtract and multiply), and v_dot2 adds their exact
+// products with the activations into s.  With X_lo and X_hi the sums of the
+// block's activations at the two kinds of pair,
+// sum_k (q_k - 8) x_k = s - (1032 X_lo + 72 X_hi), and the block's term is
+// d times that, in fp32 (xc holds 1032 X_lo + 72 X_hi of every block, formed
+// once per row).  9 vector operations per 8 codes instead of 17, and no
+// rounding of d (q - 8) to f16.
 template <int S>
-__device__ __forceinline__ float gemv1_dot(const _Float16* xb, int sid, int i0, int n_i,
+__device__ __forceinline__ float gemv1_dot(const _Float16* xb, const float* xc, int blk, int sid, int i0, int n_i,
                                            const uint4 (&c)[kGemv1Batch], const uint32_t (&sc)[kGemv1Batch],
                                            float acc) {
+  const uint32_t mag_lo = 0x64006400u, mag_hi = 0x54005400u;
 #pragma unroll
   for (int u = 0; u < kGemv1Batch; ++u) {
     if (i0 + u < n_i) {
       const int kt = sid + S * (i0 + u);
-      const _Float16 d = __builtin_bit_cast(_Float16, (uint16_t)sc[u]);
-      const f16x2 d2 = {d, d};
+      const float d = (float)__builtin_bit_cast(_Float16, (uint16_t)sc[u]);
       const f16x2* xp = reinterpret_cast<const f16x2*>(xb + kt * BK);
       const uint32_t w[4] = {c[u].x, c[u].y, c[u].z, c[u].w};
+      float sum = 0.f;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const uint4 o = dequant_dword(w[q], d2);
-        acc = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, o.x), xp[4 * q + 0], acc, false);
-        acc = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, o.y), xp[4 * q + 1], acc, false);
-        acc = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, o.z), xp[4 * q + 2], acc, false);
-        acc = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, o.w), xp[4 * q + 3], acc, false);
+        const uint32_t w8 = w[q] >> 8;
+        sum = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, and_or(w[q], 0x000F000Fu, mag_lo)), xp[4 * q + 0],
+                                     sum, false);
+        sum = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, and_or(w[q], 0x00F000F0u, mag_hi)), xp[4 * q + 1],
+                                     sum, false);
+        sum = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, and_or(w8, 0x000F000Fu, mag_lo)), xp[4 * q + 2],
+                                     sum, false);
+        sum = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, and_or(w8, 0x00F000F0u, mag_hi)), xp[4 * q + 3],
+                                     sum, false);
       }
+      acc = __builtin_fmaf(d, sum - xc[2 * kt + blk], acc);
     }
   }
   return acc;
 }
+
+// Dynamic LDS of a single-row product: the staged row (K halves), then the
+// correction term of each 32-element block (K / 32 floats).
+constexpr size_t gemv1_lds_bytes(int k) { return (size_t)k * sizeof(_Float16) + (size_t)(k / 32) * sizeof(float); }
 
 // LDS of the single-row products: the staged row is dynamic (K halves).
 struct Gemv1Lds {
@@ -768,6 +788,21 @@ __device__ __forceinline__ void gemv1_body(int g, const _Float16* __restrict__ X
   uint4 ca[kGemv1Batch], cb[kGemv1Batch];
   uint32_t sa[kGemv1Batch], sb[kGemv1Batch];
   gemv1_load<S>(codes, scales, sid, 0, n_i, nk, ca, sa);
+  // the epilogue's operands are fetched now too, each thread from an index
+  // in range (threads past the epilogue's ones fetch a duplicate), so no
+  // dependent load waits at the end: the residual a column adds to, and the
+  // row's position, slot offset and (cos, sin) of its pair
+  [[maybe_unused]] float y_old = 0.f;
+  [[maybe_unused]] float2 cs_e = {};
+  [[maybe_unused]] int p_e = 0;
+  [[maybe_unused]] int64_t off_e = 0;
+  if constexpr (EPI == kEpiAdd) y_old = reinterpret_cast<const float*>(Y)[gemv1_col<EPI, CPW>(g, t % CPW, ea)];
+  if constexpr (EPI == kEpiRopeQ || EPI == kEpiRopeKV) {
+    const int half = ea.hd >> 1;
+    p_e = ea.pos[0];
+    if constexpr (EPI == kEpiRopeKV) off_e = ea.kv_off[0];
+    cs_e = ea.rope_cs[(size_t)p_e * half + gemv1_col<EPI, CPW>(g, t % (CPW / 2), ea) % half];
+  }
   const size_t row = a_rows ? a_rows[0] : 0;
   if constexpr (NORM) {
     float4 v[kRowNormRegs];
@@ -796,14 +831,32 @@ __device__ __forceinline__ void gemv1_body(int g, const _Float16* __restrict__ X
     for (int i = t; i < K / 8; i += 256) reinterpret_cast<uint4*>(xs)[i] = xr[i];
   }
   __syncthreads();   // xs staged
+  // 1032 X_lo + 72 X_hi of every 32-element block of the row (gemv1_dot):
+  // pair j of a block (elements 2j, 2j + 1) is of the bits-0-3 kind for even
+  // j, of the bits-4-7 kind for odd j
+  float* xc = reinterpret_cast<float*>(xs + K);
+  for (int b = t; b < K / 32; b += 256) {
+    const f16x2* xp = reinterpret_cast<const f16x2*>(xs + 32 * b);
+    float x_lo = 0.f, x_hi = 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; i += 2) {
+      const f16x2 a = xp[i], h = xp[i + 1];
+      x_lo += (float)a.x;
+      x_lo += (float)a.y;
+      x_hi += (float)h.x;
+      x_hi += (float)h.y;
+    }
+    xc[b] = __builtin_fmaf(1032.f, x_lo, 72.f * x_hi);
+  }
+  __syncthreads();
   const _Float16* xb = xs + blk * 32;
   float acc = 0.f;
   // two batches in flight: the next one loads while this one is summed
   for (int i0 = 0; i0 < n_i; i0 += 2 * kGemv1Batch) {
     if (i0 + kGemv1Batch < n_i) gemv1_load<S>(codes, scales, sid, i0 + kGemv1Batch, n_i, nk, cb, sb);
-    acc = gemv1_dot<S>(xb, sid, i0, n_i, ca, sa, acc);
+    acc = gemv1_dot<S>(xb, xc, blk, sid, i0, n_i, ca, sa, acc);
     if (i0 + 2 * kGemv1Batch < n_i) gemv1_load<S>(codes, scales, sid, i0 + 2 * kGemv1Batch, n_i, nk, ca, sa);
-    if (i0 + kGemv1Batch < n_i) acc = gemv1_dot<S>(xb, sid, i0 + kGemv1Batch, n_i, cb, sb, acc);
+    if (i0 + kGemv1Batch < n_i) acc = gemv1_dot<S>(xb, xc, blk, sid, i0 + kGemv1Batch, n_i, cb, sb, acc);
   }
   s_red[t] = acc;
   __syncthreads();
@@ -820,7 +873,7 @@ __device__ __forceinline__ void gemv1_body(int g, const _Float16* __restrict__ X
   if constexpr (EPI == kEpiStore || EPI == kEpiAdd) {
     if (t < CPW) {
       float* y = reinterpret_cast<float*>(Y) + gemv1_col<EPI, CPW>(g, t, ea);
-      *y = EPI == kEpiAdd ? s_sum[t] + *y : s_sum[t];
+      *y = EPI == kEpiAdd ? s_sum[t] + y_old : s_sum[t];
     }
   } else if constexpr (EPI == kEpiSwiGLU) {
     static_assert(CPW == 32, "SwiGLU takes the 16 gate and 16 up columns of 16 outputs");
@@ -829,15 +882,14 @@ __device__ __forceinline__ void gemv1_body(int g, const _Float16* __restrict__ X
     constexpr int P = CPW / 2;
     const int half = ea.hd >> 1;
     const int rot = EPI == kEpiRopeQ ? ea.n_valid : ea.n_valid >> 1;
-    const int64_t off = EPI == kEpiRopeKV ? ea.kv_off[0] : 0;
+    const int64_t off = off_e;
     if (off < 0) return;                       // the row writes no KV
-    const int p = ea.pos[0];
+    const int p = p_e;
     if (g < rot / CPW) {
       if (t < P) {
         const int c = gemv1_col<EPI, CPW>(g, t, ea);
-        const float2 cv = ea.rope_cs[(size_t)p * half + c % ea.hd];
         _Float16* yr = EPI == kEpiRopeQ ? reinterpret_cast<_Float16*>(Y) : reinterpret_cast<_Float16*>(ea.slab + off);
-        const float2 y = rope_rotate(s_sum[t], s_sum[t + P], cv.x, cv.y);
+        const float2 y = rope_rotate(s_sum[t], s_sum[t + P], cs_e.x, cs_e.y);
         yr[c] = (_Float16)y.x;
         yr[c + half] = (_Float16)y.y;
       }
@@ -1073,7 +1125,7 @@ template <bool NORM, int EPI, int CPW>
 void launch_gemv1_t(const _Float16* X, int n, int k, const uint8_t* W, const GemmRope& ea, void* y, hipStream_t s,
                     const int32_t* a_rows, const float* h, float eps) {
   const int cols = (EPI == kEpiRopeQ || EPI == kEpiRopeKV) ? ea.n_valid : n;
-  hipLaunchKernelGGL((gemv1_kernel<NORM, EPI, CPW>), dim3(cols / CPW), dim3(256), (size_t)k * sizeof(_Float16), s,
+  hipLaunchKernelGGL((gemv1_kernel<NORM, EPI, CPW>), dim3(cols / CPW), dim3(256), gemv1_lds_bytes(k), s,
                      X, h, eps, a_rows, k, W, y, ea);
 }
 
@@ -1101,7 +1153,7 @@ void launch_gemv1_qkv(const void* x, int k, const void* wq, void* yq, const Gemm
                       const float* h_norm, float eps) {
   const _Float16* X = reinterpret_cast<const _Float16*>(x);
   const int g_q = eq.n_valid / kGemv1QkvCols, g_kv = ekv.n_valid / kGemv1QkvCols;
-  const size_t lds = (size_t)k * sizeof(_Float16);
+  const size_t lds = gemv1_lds_bytes(k);
   const uint8_t* Wq = reinterpret_cast<const uint8_t*>(wq);
   const uint8_t* Wkv = reinterpret_cast<const uint8_t*>(wkv);
   if (h_norm)

@@ -78,8 +78,8 @@ void launch_gemm_q4_splitk_rope(const void* x, int m, int n, int k, const void* 
 // One activation row in one launch (m = 1, no workspace): workgroups own a
 // few output columns over the whole K range and apply the epilogue
 // themselves (any of kEpiStore .. kEpiRopeKV, with ea as for
-// launch_gemm_q4_rope).  Results equal launch_gemm_q4's up to the order of
-// the fp32 sums.  h_norm as in launch_gemm_q4_splitk.  Only where
+// launch_gemm_q4_rope).  The code-activation products are exact and each
+// block's scale multiplies its fp32 sum (no f16 rounding of d (q - 8)).  h_norm as in launch_gemm_q4_splitk.  Only where
 // gemv1_ok(n, k): n % 256 == 0, k % 64 == 0, k <= kGemv1MaxK (the row is
 // staged in LDS).
 constexpr int kGemv1MaxK = 16384;
