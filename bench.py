@@ -32,8 +32,8 @@ METRIC = "KV-recompute prefill tokens/s + TTFT ms from evicted state, 1 MI355X"
 # valid only for the kernel source they were taken on and the 8B workload.
 MEASURED_TRAFFIC = {"kernel": "attn_kernel", "workload": "8b",
                     "source": "paper_2609_01338_amd/csrc/attention.hip",
-                    "sha256": "d951c04492062eb71d0da0615efbd2a5f443306b753f2f8a87f7618257b5be2d",
-                    "bytes_per_launch": 1.660e9}
+                    "sha256": "a178aa091067b7c4e349dfb1aee0e46d6a4c96b3b6c835809ec403801e060bbf",
+                    "bytes_per_launch": 1.663e9}
 PEAK_MFMA_TFLOPS = 2500.0      # MI355X dense bf16 / fp16 MFMA
 PEAK_HBM_GBPS = 8000.0
 
@@ -464,6 +464,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-overlap", action="store_true")
     ap.add_argument("--no-shard", action="store_true", help="skip the per-GPU shard kernel timings")
+    ap.add_argument("--decode-only", type=int, default=0, metavar="N",
+                    help="after the clean prefill, one restore by the plan, then N timed greedy decode steps "
+                         "(no timed restores, CPU baseline or shard timings); prints one JSON line")
     ap.add_argument("--no-decode", action="store_true",
                     help="skip the decode steps after the timed restores (profiler runs of the restore alone)")
     ap.add_argument("--ablation", action="store_true",
@@ -522,7 +525,7 @@ def main():
     plan = W.make_plan(w)
 
     t = time.perf_counter()
-    eng = mz.Engine(m, blob, max_ctx=S + 64)   # room for the decode steps after the restore
+    eng = mz.Engine(m, blob, max_ctx=S + 64 + args.decode_only)   # room for the decode steps after the restore
     e = eng.ctx
     log(f"[bench] model loaded in {time.perf_counter() - t:.1f} s")
     if args.no_overlap:
@@ -534,6 +537,23 @@ def main():
     clean_tok, clean_logits = mz.mz_first_token(e, m.vocab)
     mz.mz_truncate_context(e, w.n_ctx)
     log(f"[bench] clean prefill of {S} tokens in {time.perf_counter() - t:.2f} s, token {clean_tok}")
+
+    if args.decode_only:
+        mz.mz_evict(e, plan.kv_state, plan.w_state)
+        mz.mz_restore_and_prefill(e, prompt)
+        tok = mz.mz_first_token(e)
+        toks = mz.mz_generate(e, tok, 4)                      # warm
+        w0 = time.time()
+        t = time.perf_counter()
+        mz.mz_generate(e, int(toks[-1]), args.decode_only)
+        dt = time.perf_counter() - t
+        board.window(w0, time.time())
+        eng.close()
+        res = {"tokens": args.decode_only, "ms_per_token": round(dt * 1e3 / args.decode_only, 3),
+               "tokens_per_s": round(args.decode_only / dt, 1), "context": S + 5}
+        log(f"[bench] decode after restore: {res['ms_per_token']} ms/token over {args.decode_only} tokens")
+        print(json.dumps({"decode_after_restore": res, "workload": w.key, "board": board.summary()}), flush=True)
+        return
 
     if args.ablation:
         res = run_ablation(mz, W, eng, w, prompt, clean_logits, args.recompute_tflops,
