@@ -646,26 +646,31 @@ __global__ __launch_bounds__(64 * kFewWaves) void attn_few_kernel(
   float m_c = -INFINITY, l_c = 0.f;
   const int nb_all = (kmax / KT + 1) * (KT / kFewBlock);      // blocks up to kmax's tile
   const int b_begin = split * tps * (KT / kFewBlock);
-  const int b_end = min(b_begin + tps * (KT / kFewBlock), nb_all);
-  for (int b = b_begin + w; b < b_end; b += kFewWaves) {
-    const int j0 = b * kFewBlock;
-    if (j0 > kmax) break;
-    const uint8_t* slot = slab + (int64_t)(uint32_t)table[j0 >> cshift] * slot_bytes;
-    const int jc = j0 & (C - 1);
-    f16x8v ka[2][KS];
+  // blocks b_begin + w, + kFewWaves, ... that hold a key <= kmax
+  const int b_stop = min(min(b_begin + tps * (KT / kFewBlock), nb_all), kmax / kFewBlock + 1);
+  const int n_w = b_begin + w < b_stop ? (b_stop - (b_begin + w) + kFewWaves - 1) / kFewWaves : 0;
+  // block k of this wave, clamped to its last one (repeated loads of a valid block stand in for the
+  // blocks past the end, so no branch wraps a load)
+  auto blk = [&](int k) { return b_begin + w + kFewWaves * min(k, n_w - 1); };
+  // K fragments of keys jc + 16 h + col (dimensions 32 ks + 8 lg .. +8) and V^T fragments of dimension
+  // rows 16 d + col (keys jc + 4 lg .. +4 and jc + 16 + 4 lg .. +4) of block bb, in slot `sl`
+  auto load = [&](int bb, int32_t sl, f16x8v (&ka)[2][KS], uint2 (&va)[DB][2]) {
+    const uint8_t* slot = slab + (int64_t)(uint32_t)sl * slot_bytes;
+    const int jc = (bb * kFewBlock) & (C - 1);
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
         ka[h][ks] = *reinterpret_cast<const f16x8v*>(slot + (int64_t)(jc + h * 16 + col) * krow_bytes +
                                                       (kvh * HD + ks * 32 + lg * 8) * 2);
-    // V^T fragments: dimension row 16 d + col, keys jc + 4 lg .. +4 and jc + 16 + 4 lg .. +4
-    uint2 va[DB][2];
     const uint8_t* vt = slot + (int64_t)C * dkv * 2 + ((int64_t)(kvh * HD + col) * C + jc + 4 * lg) * 2;
 #pragma unroll
     for (int d = 0; d < DB; ++d)
 #pragma unroll
       for (int h = 0; h < 2; ++h) va[d][h] = *reinterpret_cast<const uint2*>(vt + (int64_t)d * 16 * C * 2 + h * 32);
+  };
+  auto compute = [&](int bb, f16x8v (&ka)[2][KS], uint2 (&va)[DB][2]) {
+    const int j0 = bb * kFewBlock;
     f32x4v sc[2];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
@@ -722,6 +727,18 @@ __global__ __launch_bounds__(64 * kFewWaves) void attn_few_kernel(
     for (int d = 0; d < DB; ++d) {
       const uint4 a4 = make_uint4(va[d][0].x, va[d][0].y, va[d][1].x, va[d][1].y);
       o[d] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8v, a4), pb, o[d], 0, 0, 0);
+    }
+  };
+  if (n_w > 0) {
+    // the next block's chunk-table entry is fetched while this block is summed, so each block waits on
+    // one memory round trip (its keys and values), not two
+    f16x8v ka[2][KS];
+    uint2 va[DB][2];
+    int32_t t_cur = table[(blk(0) * kFewBlock) >> cshift];
+    for (int k = 0; k < n_w; ++k) {
+      load(blk(k), t_cur, ka, va);
+      t_cur = table[(blk(k + 1) * kFewBlock) >> cshift];
+      compute(blk(k), ka, va);
     }
   }
   // the column's sum over its four lane groups; then the waves combine
