@@ -80,7 +80,8 @@ typedef struct {
  * bytes: element j in the low nibble of byte j, element j+16 in the high).
  * The blob is repacked into device layouts and a host copy of the layer
  * weights is retained for dropped-weight reloads.  EINVAL on a shape or size
- * mismatch, ENOMEM / EHIP on allocation failure. */
+ * mismatch or more than 8192 chunks per layer (max_ctx / chunk_tokens),
+ * ENOMEM / EHIP on allocation failure. */
 mz_status mz_load_model(const mz_model_cfg *cfg, const void *q4_blob, size_t nbytes,
                         int32_t device, mz_ctx **out);
 
@@ -491,13 +492,15 @@ mz_status mz_q4_gemm_split_noalloc(const void *x_f16, int32_t m, int32_t n_pad, 
  * split, at most 32 splits; 1 when the tile grid already fills the GPU. */
 int32_t mz_q4_gemm_auto_splits(int32_t m, int32_t n_pad, int32_t k, int64_t workspace_bytes);
 
-/* Causal GQA attention of q (f16 [m][n_q_heads][head_dim], rotated) at
- * positions qpos (int32 [m], ascending) over the KV chunks of one layer:
- * chunk c of the layer lives in slot table[c] of slab.  A slot holds K
+/* Causal GQA attention (paper Sec. 2.1; read through the chunk table as in
+ * Sec. 4.2) of q (f16 [m][n_q_heads][head_dim], rotated) at positions qpos
+ * (int32 [m], ascending) over the KV chunks of one layer: chunk c of the
+ * layer lives in slot table[c] of slab.  A slot holds K
  * token-major ([chunk_tokens][n_kv_heads * head_dim] f16) followed by V
  * dimension-major ([n_kv_heads * head_dim][chunk_tokens] f16); chunk_tokens is
  * a power of two and a multiple of 8.  Keys 0..qpos[i] are read; table must
- * cover chunk (qpos[m-1] / chunk_tokens).  out: f16 [m][n_q_heads * head_dim]. */
+ * cover chunk (qpos[m-1] / chunk_tokens) and has n_table entries, at most
+ * 8192.  out: f16 [m][n_q_heads * head_dim]. */
 mz_status mz_attention(const void *q_f16, const int32_t *qpos, int32_t m, const void *slab,
                        const int32_t *table, int32_t n_table, int32_t chunk_tokens,
                        int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, void *out_f16,
@@ -568,11 +571,17 @@ mz_status mz_kv_decompress(const void *in, int64_t n_halves, void *dst_f16, void
  * restore path; for stating measured rates against them): f16 MFMA
  * throughput with operand bits that keep changing as real data does, a plain
  * 1 GiB device copy (bytes read + written), and 1 GiB pinned host -> device
- * and device -> host copies.  Writes JSON
- * {"mfma_f16_tflops", "hbm_copy_gbps", "h2d_pinned_gbps", "d2h_pinned_gbps"}
+ * and device -> host copies.  Two more MFMA figures price an exact-integer
+ * weight operand: "mfma_f16_codes_tflops" with one operand holding exact
+ * 4-bit codes q - 8, and "mfma_f16_block_scaled_tflops" with, in addition,
+ * each 32-deep product summed into a zero accumulator and scaled into the
+ * running sum by four fp32 FMAs (a Q4_0 block scale applied after the
+ * product).  Writes JSON
+ * {"mfma_f16_tflops", "mfma_f16_codes_tflops", "mfma_f16_block_scaled_tflops",
+ *  "hbm_copy_gbps", "h2d_pinned_gbps", "d2h_pinned_gbps"}
  * into json_out (cap bytes, NUL-terminated).  Allocates and frees about
- * 2 GiB of device memory and 1 GiB of pinned host memory; takes about a
- * second.  Errors: MZ_EINVAL (buffer), MZ_ENOMEM / MZ_EHIP (device). */
+ * 2 GiB of device memory and 1 GiB of pinned host memory; takes about
+ * two seconds.  Errors: MZ_EINVAL (buffer), MZ_ENOMEM / MZ_EHIP (device). */
 mz_status mz_probe_ceilings(int32_t device, char *json_out, size_t cap);
 
 #ifdef __cplusplus

@@ -34,6 +34,8 @@
 // row 8 * (r / 4) + 4 * (l / 32) + r % 4, column l % 32.  Both operands of a
 // product only need to agree on which logical k sits in (lane group, slot).
 #include <algorithm>
+#include <map>
+#include <mutex>
 
 #include "mz_kernels.h"
 
@@ -82,6 +84,7 @@ constexpr int v_tile_halves() { return HD * KT; }
 template <int HD, int NW, bool DIRECT, bool SPLIT>
 __device__ __forceinline__ void attn_tile(const _Float16* __restrict__ Q, const int32_t* __restrict__ qpos, int M,
                                           const uint8_t* __restrict__ slab, const int32_t* __restrict__ table,
+                                          int n_table,
                                           int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group,
                                           int qw, float scale_log2, _Float16* __restrict__ O, int tps,
                                           _Float16* __restrict__ Opart, float2* __restrict__ MLpart, int tile,
@@ -218,7 +221,11 @@ __device__ __forceinline__ void attn_tile(const _Float16* __restrict__ Q, const 
   }
   typedef __attribute__((address_space(3))) void lds_void;
   auto lds_addr = [&](const _Float16* p_) { return (uint32_t)(uintptr_t)(lds_void*)p_; };
-  auto dload = [&](const uint8_t* gbase, uint32_t lds0, const uint32_t* ofs, int nq_, int per) {
+  auto dload = [&](const uint8_t* gbase_, uint32_t lds0, const uint32_t* ofs, int nq_, int per) {
+    // the base address is uniform: kept in scalar registers for the asm
+    const uint64_t ga = (uint64_t)(uintptr_t)gbase_;
+    const uint8_t* gbase = (const uint8_t*)(uintptr_t)(((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(ga >> 32)) << 32) |
+                                                       (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)ga));
 #pragma unroll
     for (int i = 0; i < per; ++i) {
       const int q = i * NW + wu;
@@ -238,6 +245,22 @@ __device__ __forceinline__ void attn_tile(const _Float16* __restrict__ Q, const 
     const uint8_t* g = vbase + (uint64_t)(uint32_t)table[j0 >> cshift] * slot_bytes + (uint32_t)((j0 & cmask) * 2);
     dload(g, __builtin_amdgcn_readfirstlane(lds_addr(Vt)), vofs, VQ, VQ_PER);
   };
+  // The same with the tile's slot at hand.  Inside the key loop the slots
+  // come from a copy of the item's stretch of the chunk table in LDS (ltab,
+  // chunks c_lo ..): a scalar-memory read there is waited for with
+  // lgkmcnt(0), two round trips per key tile before its loads can go out.
+  auto dload_k_at = [&](int t, int slot, const _Float16* Ks) {
+    const int j0 = t * KT;
+    const uint8_t* g = kbase + (uint64_t)(uint32_t)slot * slot_bytes + (uint32_t)((j0 & cmask) * krow_bytes);
+    dload(g, __builtin_amdgcn_readfirstlane(lds_addr(Ks)), kofs, KQ, KQ_PER);
+  };
+  auto dload_v_at = [&](int t, int slot, const _Float16* Vt) {
+    const int j0 = t * KT;
+    const uint8_t* g = vbase + (uint64_t)(uint32_t)slot * slot_bytes + (uint32_t)((j0 & cmask) * 2);
+    dload(g, __builtin_amdgcn_readfirstlane(lds_addr(Vt)), vofs, VQ, VQ_PER);
+  };
+  int* ltab = reinterpret_cast<int*>(lds + 2 * (k_tile_halves<HD>() + v_tile_halves<HD>()) + 8);
+  const int c_lo = (kt0 * KT) >> cshift;
   // After the wave's own loads of V^T tile t have landed: zero the keys past
   // kmax in the pieces this lane fetched (P is 0 there, but the slot rows past
   // the last written position may hold anything).
@@ -355,12 +378,21 @@ __device__ __forceinline__ void attn_tile(const _Float16* __restrict__ Q, const 
   // loads of K tile kt+2 and V tile kt+1 are in flight across the iteration
   // and land in the buffers freed in iteration kt-1; one barrier per
   // iteration.
+  int ts1 = 0, ts2 = 0;   // slots of key tiles kt+1 and kt+2 at the start of step kt
   if constexpr (DIRECT) {
+    {
+      // (a table shorter than the item's keys breaks the call's contract; the
+      // copy still stays inside its LDS region)
+      const int c_n = min((((kt_end - 1) * KT) >> cshift) - c_lo + 1, n_table - c_lo);
+      for (int c = tid; c < c_n; c += NTH) ltab[c] = table[c_lo + c];
+    }
     dload_k(kt0, Kbuf(kt0));
     dload_v(kt0, Vbuf(kt0));
     if (kt0 + 1 < kt_end) dload_k(kt0 + 1, Kbuf(kt0 + 1));
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     if (kt0 + 1 == kt_end) vfix(kt0, Vbuf(kt0));
+    ts1 = table[(min(kt0 + 1, kt_end - 1) * KT) >> cshift];
+    ts2 = table[(min(kt0 + 2, kt_end - 1) * KT) >> cshift];
   } else {
     gload_k(kt0);
     gload_v(kt0);
@@ -383,9 +415,11 @@ __device__ __forceinline__ void attn_tile(const _Float16* __restrict__ Q, const 
   }
 
   auto step = [&](int kt, f32x16* sc, f32x16* sn) {
+    int tnext = 0;   // slot of key tile kt+3, read from ltab now, used a step later
     if constexpr (DIRECT) {
-      if (kt + 2 < kt_end) dload_k(kt + 2, Kbuf(kt));
-      if (kt + 1 < kt_end) dload_v(kt + 1, Vbuf(kt + 1));
+      if (kt + 2 < kt_end) dload_k_at(kt + 2, ts2, Kbuf(kt));
+      if (kt + 1 < kt_end) dload_v_at(kt + 1, ts1, Vbuf(kt + 1));
+      tnext = ltab[((min(kt + 3, kt_end - 1) * KT) >> cshift) - c_lo];
     } else {
       if (kt + 2 < kt_end) gload_k(kt + 2);
       if (kt + 1 < kt_end) gload_v(kt + 1);
@@ -449,6 +483,8 @@ __device__ __forceinline__ void attn_tile(const _Float16* __restrict__ Q, const 
     if (more) update_max(mx);
     if constexpr (DIRECT) {
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      ts1 = ts2;
+      ts2 = __builtin_amdgcn_readfirstlane(tnext);
       if (kt + 2 == kt_end) vfix(kt + 1, Vbuf(kt + 1));
     } else {
       if (kt + 2 < kt_end) lstore_k(Kbuf(kt));
@@ -522,7 +558,7 @@ template <int HD, int NW, bool DIRECT, bool SPLIT>
 __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restrict__ Q,
                                                        const int32_t* __restrict__ qpos, int M,
                                                        const uint8_t* __restrict__ slab,
-                                                       const int32_t* __restrict__ table, int C,
+                                                       const int32_t* __restrict__ table, int n_table, int C,
                                                        int cshift, int64_t slot_bytes, int nq, int nkv,
                                                        int group, int qw, int n_qtiles,
                                                        float scale_log2, _Float16* __restrict__ O, int tps,
@@ -542,7 +578,7 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
       tile_rank = (j / nkv) * 8 + xcd;
     }
     if (tile_rank >= n_qtiles) return;
-    attn_tile<HD, NW, DIRECT, SPLIT>(Q, qpos, M, slab, table, C, cshift, slot_bytes, nq, nkv, group, qw,
+    attn_tile<HD, NW, DIRECT, SPLIT>(Q, qpos, M, slab, table, n_table, C, cshift, slot_bytes, nq, nkv, group, qw,
                                      scale_log2, O, tps, Opart, MLpart, n_qtiles - 1 - tile_rank, kvh);
     return;
   }
@@ -580,7 +616,7 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
       }
       if (tile_rank >= n_qtiles) break;
     }
-    attn_tile<HD, NW, DIRECT, SPLIT>(Q, qpos, M, slab, table, C, cshift, slot_bytes, nq, nkv, group, qw,
+    attn_tile<HD, NW, DIRECT, SPLIT>(Q, qpos, M, slab, table, n_table, C, cshift, slot_bytes, nq, nkv, group, qw,
                                      scale_log2, O, tps, Opart, MLpart, n_qtiles - 1 - tile_rank, kvh);
   }
   if (persistent && threadIdx.x == 0) {
@@ -861,32 +897,44 @@ struct SplitArgs {
   float2* ml = nullptr;
 };
 
-// Workgroups of one kernel instance that the whole GPU holds at once.
+// Workgroups of one kernel instance that the whole GPU holds at once with
+// lds_bytes of dynamic LDS each (cached per instance and size).
 template <int HD, int NW, bool DIRECT, bool SPLIT>
 int resident_wgs(size_t lds_bytes) {
-  static const int n = [&] {
-    int dev = 0, cus = 0, per = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
-      cus = 256;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
-            &per, reinterpret_cast<const void*>(&attn_kernel<HD, NW, DIRECT, SPLIT>), 64 * NW, lds_bytes) !=
-            hipSuccess || per <= 0)
-      per = 1;
-    return cus * per;
-  }();
-  return n;
+  static std::mutex mu;
+  static std::map<size_t, int> cache;
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = cache.find(lds_bytes);
+  if (it != cache.end()) return it->second;
+  int dev = 0, cus = 0, per = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    cus = 256;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+          &per, reinterpret_cast<const void*>(&attn_kernel<HD, NW, DIRECT, SPLIT>), 64 * NW, lds_bytes) !=
+          hipSuccess || per <= 0)
+    per = 1;
+  cache[lds_bytes] = cus * per;
+  return cus * per;
+}
+
+// Dynamic LDS of a launch: the K/V tiles, double buffered, the item of the
+// persistent form and, with direct loads, the copy of the chunk table.
+template <int HD, bool DIRECT>
+constexpr size_t attn_lds_bytes(int n_table) {
+  return 2 * (k_tile_halves<HD>() + v_tile_halves<HD>()) * sizeof(_Float16) + 16 +
+         (DIRECT ? 4 * (size_t)((n_table + 3) & ~3) : 0);
 }
 
 template <int HD, int NW, bool DIRECT, bool SPLIT>
 void launch_nwd(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S, const int32_t* table,
-               int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group, int qw, float scale_log2,
-               _Float16* O, const SplitArgs& sa, int* wq, hipStream_t s) {
-  // the K/V tiles, double buffered, and the item of the persistent form
-  const size_t lds_bytes = 2 * (k_tile_halves<HD>() + v_tile_halves<HD>()) * sizeof(_Float16) + 16;
-  static const bool attr = [&] {
+               int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group, int qw, int n_table,
+               float scale_log2, _Float16* O, const SplitArgs& sa, int* wq, hipStream_t s) {
+  const size_t lds_bytes = attn_lds_bytes<HD, DIRECT>(n_table);
+  static const bool attr = [] {
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<HD, NW, DIRECT, SPLIT>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
+                              hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)attn_lds_bytes<HD, DIRECT>(kAttnTableMax));
     return true;
   }();
   (void)attr;
@@ -902,35 +950,35 @@ void launch_nwd(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S,
     blocks = (8 % nkv == 0) ? 8 * ((n_qtiles + 8 / nkv - 1) / (8 / nkv)) : 8 * ((n_qtiles + 7) / 8) * nkv;
   }
   hipLaunchKernelGGL((attn_kernel<HD, NW, DIRECT, SPLIT>), dim3(blocks, SPLIT ? sa.n_split : 1), dim3(64 * NW),
-                     lds_bytes, s, Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, n_qtiles,
+                     lds_bytes, s, Q, qpos, m, S, table, n_table, C, cshift, slot_bytes, nq, nkv, group, qw, n_qtiles,
                      scale_log2, O, sa.tps, sa.opart, sa.ml, wq);
 }
 
 template <int HD, int NW, bool SPLIT>
 void launch_nw(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S, const int32_t* table,
-               int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group, int qw, float scale_log2,
-               _Float16* O, const SplitArgs& sa, int* wq, hipStream_t s) {
+               int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group, int qw, int n_table,
+               float scale_log2, _Float16* O, const SplitArgs& sa, int* wq, hipStream_t s) {
   if (C >= KT)
-    launch_nwd<HD, NW, true, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2,
-                                    O, sa, wq, s);
+    launch_nwd<HD, NW, true, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, n_table,
+                                    scale_log2, O, sa, wq, s);
   else
-    launch_nwd<HD, NW, false, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2,
-                                     O, sa, wq, s);
+    launch_nwd<HD, NW, false, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, n_table,
+                                     scale_log2, O, sa, wq, s);
 }
 
 template <int HD, bool SPLIT>
 void launch_hd(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S, const int32_t* table,
-               int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group, int qw, float scale_log2,
-               _Float16* O, const SplitArgs& sa, int* wq, hipStream_t s) {
+               int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group, int qw, int n_table,
+               float scale_log2, _Float16* O, const SplitArgs& sa, int* wq, hipStream_t s) {
   switch (group * qw) {
-    case 5: launch_nw<HD, 5, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, sa, wq, s); break;
-    case 6: launch_nw<HD, 6, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, sa, wq, s); break;
-    case 7: launch_nw<HD, 7, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, sa, wq, s); break;
-    default: launch_nw<HD, 8, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, scale_log2, O, sa, wq, s); break;
+    case 5: launch_nw<HD, 5, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, n_table, scale_log2, O, sa, wq, s); break;
+    case 6: launch_nw<HD, 6, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, n_table, scale_log2, O, sa, wq, s); break;
+    case 7: launch_nw<HD, 7, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, n_table, scale_log2, O, sa, wq, s); break;
+    default: launch_nw<HD, 8, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, n_table, scale_log2, O, sa, wq, s); break;
   }
 }
 
-void launch_any(const void* q, const int32_t* qpos, int m, const void* slab, const int32_t* table,
+void launch_any(const void* q, const int32_t* qpos, int m, const void* slab, const int32_t* table, int n_table,
                 int chunk_tokens, int64_t slot_bytes, int n_q, int n_kv, int head_dim, void* out,
                 const SplitArgs& sa, bool split, int* wq, hipStream_t s) {
   const int group = n_q / n_kv;          // 1..8
@@ -944,20 +992,20 @@ void launch_any(const void* q, const int32_t* qpos, int m, const void* slab, con
   int cshift = 0;
   while ((1 << cshift) < chunk_tokens) ++cshift;   // chunk_tokens is a power of two
   if (head_dim == 128) {
-    if (split) launch_hd<128, true>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, scale_log2, O, sa, nullptr, s);
-    else launch_hd<128, false>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, scale_log2, O, sa, wq, s);
+    if (split) launch_hd<128, true>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, n_table, scale_log2, O, sa, nullptr, s);
+    else launch_hd<128, false>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, n_table, scale_log2, O, sa, wq, s);
   } else {
-    if (split) launch_hd<64, true>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, scale_log2, O, sa, nullptr, s);
-    else launch_hd<64, false>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, scale_log2, O, sa, wq, s);
+    if (split) launch_hd<64, true>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, n_table, scale_log2, O, sa, nullptr, s);
+    else launch_hd<64, false>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, n_table, scale_log2, O, sa, wq, s);
   }
 }
 
 }  // namespace
 
 void launch_attention(const void* q, const int32_t* qpos, int m, const void* slab,
-                      const int32_t* table, int chunk_tokens, int64_t slot_bytes, int n_q,
+                      const int32_t* table, int n_table, int chunk_tokens, int64_t slot_bytes, int n_q,
                       int n_kv, int head_dim, void* out, hipStream_t s, int* work_queues) {
-  launch_any(q, qpos, m, slab, table, chunk_tokens, slot_bytes, n_q, n_kv, head_dim, out, SplitArgs(), false,
+  launch_any(q, qpos, m, slab, table, n_table, chunk_tokens, slot_bytes, n_q, n_kv, head_dim, out, SplitArgs(), false,
              work_queues, s);
 }
 
@@ -989,7 +1037,7 @@ int attention_auto_splits(int m, int max_pos, int n_q, int n_kv, int head_dim, i
 }
 
 void launch_attention_split(const void* q, const int32_t* qpos, int m, int max_pos, const void* slab,
-                            const int32_t* table, int chunk_tokens, int64_t slot_bytes, int n_q, int n_kv,
+                            const int32_t* table, int n_table, int chunk_tokens, int64_t slot_bytes, int n_q, int n_kv,
                             int head_dim, int n_split, void* ws, void* out, hipStream_t s) {
   SplitArgs sa;
   sa.tps = attention_split_tiles(max_pos, n_split);
@@ -1014,7 +1062,7 @@ void launch_attention_split(const void* q, const int32_t* qpos, int m, int max_p
       hipLaunchKernelGGL(attn_few_kernel<64>, grid, dim3(64 * kFewWaves), 0, s, Q, qpos, m, S, table, chunk_tokens,
                          cshift, slot_bytes, n_q, n_kv, group, scale_log2, sa.tps, sa.opart, sa.ml);
   } else {
-    launch_any(q, qpos, m, slab, table, chunk_tokens, slot_bytes, n_q, n_kv, head_dim, out, sa, true, nullptr, s);
+    launch_any(q, qpos, m, slab, table, n_table, chunk_tokens, slot_bytes, n_q, n_kv, head_dim, out, sa, true, nullptr, s);
   }
   _Float16* O = reinterpret_cast<_Float16*>(out);
   if (head_dim == 128)

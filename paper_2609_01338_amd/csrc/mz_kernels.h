@@ -96,14 +96,16 @@ void launch_gemv1_qkv(const void* x, int k, const void* wq, void* yq, const Gemm
 // Splits that fill the chip for this shape within ws_cap bytes (1: no split).
 int gemm_auto_splits(int m, int n, int k, int64_t ws_cap);
 
-// Causal GQA attention over chunked KV (see mz.h, mz_attention).  With
+// Causal GQA attention over chunked KV (see mz.h, mz_attention).  table has
+// n_table entries (at most kAttnTableMax).  With
 // work_queues (device, kAttnQueueInts int32, zero on entry and left zero on
 // return; not shared by launches in flight together) and n_kv dividing 8,
 // persistent workgroups take the query tiles from per-KV-head queues, so
 // XCDs that run faster take more of them; otherwise one workgroup per tile.
 constexpr int kAttnQueueInts = 16;
+constexpr int kAttnTableMax = 8192;
 void launch_attention(const void* q, const int32_t* qpos, int m, const void* slab,
-                      const int32_t* table, int chunk_tokens, int64_t slot_bytes, int n_q,
+                      const int32_t* table, int n_table, int chunk_tokens, int64_t slot_bytes, int n_q,
                       int n_kv, int head_dim, void* out, hipStream_t s, int* work_queues = nullptr);
 
 // Split-key attention for few query rows: n_split key ranges of whole 64-key
@@ -112,8 +114,8 @@ void launch_attention(const void* q, const int32_t* qpos, int m, const void* sla
 // max_pos >= qpos[m - 1]; ws holds attention_split_ws_bytes(m, n_q,
 // head_dim, n_split) bytes.
 void launch_attention_split(const void* q, const int32_t* qpos, int m, int max_pos, const void* slab,
-                            const int32_t* table, int chunk_tokens, int64_t slot_bytes, int n_q, int n_kv,
-                            int head_dim, int n_split, void* ws, void* out, hipStream_t s);
+                            const int32_t* table, int n_table, int chunk_tokens, int64_t slot_bytes, int n_q,
+                            int n_kv, int head_dim, int n_split, void* ws, void* out, hipStream_t s);
 int64_t attention_split_ws_bytes(int m, int n_q, int head_dim, int n_split);
 // Splits that fill the chip for this shape within ws_cap bytes (1: no split).
 int attention_auto_splits(int m, int max_pos, int n_q, int n_kv, int head_dim, int64_t ws_cap);
@@ -158,9 +160,11 @@ void launch_fill(void* p, int64_t n_words, uint32_t value, hipStream_t s);
 void launch_spin(int64_t us, hipStream_t s);
 
 // Ceiling probes: blocks x 512 threads of f16 MFMAs with changing operands
-// (out: blocks*512 floats), and a plain copy of `bytes` (multiple of 16).
+// (out: blocks*512 floats; mode 0 random halves, 1 the B operand as exact
+// 4-bit codes, 2 codes with each 32-deep product scaled into the sum by
+// fp32 FMAs), and a plain copy of `bytes` (multiple of 16).
 double mfma_probe_flops_per_launch(int blocks, int iters);
-void launch_mfma_probe(float* out, int blocks, int iters, hipStream_t s);
+void launch_mfma_probe(float* out, int blocks, int iters, int mode, hipStream_t s);
 void launch_copy_probe(const void* src, void* dst, int64_t bytes, hipStream_t s);
 
 // 8-bit group-wise KV codec (groups of 64 halves; compressed run = n code

@@ -672,6 +672,8 @@ void validate_cfg(const mz_model_cfg* c) {
   if (c->d_ffn < 1 || c->vocab < 1) fail(MZ_EINVAL, "d_ffn and vocab must be positive");
   if (c->chunk_tokens < 8 || (c->chunk_tokens & (c->chunk_tokens - 1)) || c->max_ctx < 1)
     fail(MZ_EINVAL, "chunk_tokens must be a power of two >= 8 and max_ctx positive");
+  if ((c->max_ctx + c->chunk_tokens - 1) / c->chunk_tokens > mzk::kAttnTableMax)
+    fail(MZ_EINVAL, "max_ctx / chunk_tokens exceeds %d chunks per layer", mzk::kAttnTableMax);
   if (!(c->rope_theta > 0) || !(c->rms_eps >= 0)) fail(MZ_EINVAL, "rope_theta must be > 0 and rms_eps >= 0");
 }
 
@@ -1094,10 +1096,10 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
         x->attn_split ? mzk::attention_auto_splits(nq, max_pos, x->nq, x->nkv, x->hd, x->split_ws_bytes) : 1;
     x->timed(n_split > 1 ? kKAttentionSplit : kKAttention, att_flops, (double)nq * x->dq * 4.0, cs, [&] {
       if (n_split > 1)
-        mzk::launch_attention_split(x->q16, posq, nq, max_pos, x->kv_slab, x->d_tables + (size_t)l * MC, C,
+        mzk::launch_attention_split(x->q16, posq, nq, max_pos, x->kv_slab, x->d_tables + (size_t)l * MC, MC, C,
                                     x->slot_bytes, x->nq, x->nkv, x->hd, n_split, x->split_ws, x->xb, cs);
       else
-        mzk::launch_attention(x->q16, posq, nq, x->kv_slab, x->d_tables + (size_t)l * MC, C, x->slot_bytes,
+        mzk::launch_attention(x->q16, posq, nq, x->kv_slab, x->d_tables + (size_t)l * MC, MC, C, x->slot_bytes,
                               x->nq, x->nkv, x->hd, x->xb, cs, x->attn_queue ? x->attn_wq : nullptr);
     });
     x->timed(kKGemmO, 2.0 * nq * x->dq * d, (double)d * x->dq * bpe_w + nq * (x->dq * 2.0 + d * 8.0), cs,
@@ -1899,11 +1901,12 @@ static mz_status attention_entry(const void* q, const int32_t* qpos, int32_t m, 
   return guarded(nullptr, [&] {
     if (!q || !qpos || !slab || !table || !out) fail(MZ_EINVAL, "NULL pointer");
     if (m < 1 || n_table < 1) fail(MZ_EINVAL, "sizes must be positive");
+    if (n_table > mzk::kAttnTableMax) fail(MZ_EINVAL, "n_table above %d", mzk::kAttnTableMax);
     if (chunk_tokens < 8 || (chunk_tokens & (chunk_tokens - 1))) fail(MZ_EINVAL, "chunk_tokens must be a power of two >= 8");
     if (head_dim != 64 && head_dim != 128) fail(MZ_EINVAL, "head_dim must be 64 or 128");
     if (n_kv < 1 || n_q % n_kv || n_q / n_kv > 8) fail(MZ_EINVAL, "bad head counts");
     const int64_t slot_bytes = (int64_t)chunk_tokens * n_kv * head_dim * 2 * 2;
-    mzk::launch_attention(q, qpos, m, slab, table, chunk_tokens, slot_bytes, n_q, n_kv, head_dim, out,
+    mzk::launch_attention(q, qpos, m, slab, table, n_table, chunk_tokens, slot_bytes, n_q, n_kv, head_dim, out,
                           (hipStream_t)stream, queues);
     HIPCHK(hipGetLastError());
   });
@@ -1942,6 +1945,7 @@ mz_status mz_attention_split(const void* q, const int32_t* qpos, int32_t m, int3
   return guarded(nullptr, [&] {
     if (!q || !qpos || !slab || !table || !out || !workspace) fail(MZ_EINVAL, "NULL pointer");
     if (m < 1 || n_table < 1 || max_pos < 0) fail(MZ_EINVAL, "sizes must be positive");
+    if (n_table > mzk::kAttnTableMax) fail(MZ_EINVAL, "n_table above %d", mzk::kAttnTableMax);
     if (chunk_tokens < 8 || (chunk_tokens & (chunk_tokens - 1))) fail(MZ_EINVAL, "chunk_tokens must be a power of two >= 8");
     if (head_dim != 64 && head_dim != 128) fail(MZ_EINVAL, "head_dim must be 64 or 128");
     if (n_kv < 1 || n_q % n_kv || n_q / n_kv > 8) fail(MZ_EINVAL, "bad head counts");
@@ -1950,7 +1954,7 @@ mz_status mz_attention_split(const void* q, const int32_t* qpos, int32_t m, int3
     if (workspace_bytes < mzk::attention_split_ws_bytes(m, n_q, head_dim, n_split))
       fail(MZ_EINVAL, "workspace too small for %d splits", n_split);
     const int64_t slot_bytes = (int64_t)chunk_tokens * n_kv * head_dim * 2 * 2;
-    mzk::launch_attention_split(q, qpos, m, max_pos, slab, table, chunk_tokens, slot_bytes, n_q, n_kv, head_dim,
+    mzk::launch_attention_split(q, qpos, m, max_pos, slab, table, n_table, chunk_tokens, slot_bytes, n_q, n_kv, head_dim,
                                 n_split, workspace, out, (hipStream_t)stream);
     HIPCHK(hipGetLastError());
   });
@@ -2021,8 +2025,11 @@ mz_status mz_probe_ceilings(int32_t device, char* json_out, size_t cap) {
       };
       const int blocks = 2048, iters = 16000;   // ~45 ms per run: long enough for the clock to settle
       HIPCHK(hipMalloc((void**)&out, (size_t)blocks * 512 * sizeof(float)));
-      const double mfma_ms = best_ms(3, [&] { mzk::launch_mfma_probe(out, blocks, iters, s); });
-      const double tflops = mzk::mfma_probe_flops_per_launch(blocks, iters) / (mfma_ms * 1e-3) / 1e12;
+      double tf[3];
+      for (int mode = 0; mode < 3; ++mode) {
+        const double ms = best_ms(3, [&] { mzk::launch_mfma_probe(out, blocks, iters, mode, s); });
+        tf[mode] = mzk::mfma_probe_flops_per_launch(blocks, iters) / (ms * 1e-3) / 1e12;
+      }
       const size_t bytes = (size_t)1 << 30;
       HIPCHK(hipMalloc(&a, bytes));
       HIPCHK(hipMalloc(&b, bytes));
@@ -2035,9 +2042,10 @@ mz_status mz_probe_ceilings(int32_t device, char* json_out, size_t cap) {
       HIPCHK(hipStreamSynchronize(s));
       char buf[512];
       snprintf(buf, sizeof buf,
-               "{\"mfma_f16_tflops\": %.1f, \"hbm_copy_gbps\": %.1f, \"h2d_pinned_gbps\": %.2f, "
+               "{\"mfma_f16_tflops\": %.1f, \"mfma_f16_codes_tflops\": %.1f, "
+               "\"mfma_f16_block_scaled_tflops\": %.1f, \"hbm_copy_gbps\": %.1f, \"h2d_pinned_gbps\": %.2f, "
                "\"d2h_pinned_gbps\": %.2f}",
-               tflops, 2.0 * bytes / (copy_ms * 1e-3) / 1e9, bytes / (h2d_ms * 1e-3) / 1e9,
+               tf[0], tf[1], tf[2], 2.0 * bytes / (copy_ms * 1e-3) / 1e9, bytes / (h2d_ms * 1e-3) / 1e9,
                bytes / (d2h_ms * 1e-3) / 1e9);
       if (strlen(buf) + 1 > cap) fail(MZ_EINVAL, "json_out buffer too small");
       memcpy(json_out, buf, strlen(buf) + 1);

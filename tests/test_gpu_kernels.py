@@ -672,6 +672,10 @@ def test_kernel_entry_validation():
     assert e.value.status == mz.MZ_EINVAL
     with pytest.raises(mz.MzError):
         mz.mz_attention(1, 1, 4, 1, 1, 1, 16, 6, 4, 64, 1)   # 6 q heads over 4 kv heads
+    with pytest.raises(mz.MzError):
+        mz.mz_attention(1, 1, 4, 1, 1, 8193, 16, 8, 2, 64, 1)   # a chunk table above 8192 entries
+    with pytest.raises(mz.MzError):
+        mz.mz_attention_split(1, 1, 4, 10, 1, 1, 8193, 16, 8, 2, 64, 2, 1, 1 << 30, 1)
 
 
 @pytest.mark.parametrize("n,scale_kind", [(64, "normal"), (4096, "normal"), (64 * 1237, "mixed"),
