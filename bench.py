@@ -32,8 +32,8 @@ METRIC = "KV-recompute prefill tokens/s + TTFT ms from evicted state, 1 MI355X"
 # valid only for the kernel source they were taken on and the 8B workload.
 MEASURED_TRAFFIC = {"kernel": "attn_kernel", "workload": "8b",
                     "source": "paper_2609_01338_amd/csrc/attention.hip",
-                    "sha256": "a178aa091067b7c4e349dfb1aee0e46d6a4c96b3b6c835809ec403801e060bbf",
-                    "bytes_per_launch": 1.663e9}
+                    "sha256": "b85b555e8eaac305f1058310613f10d0d46284bb4ec6a863cc700d4e6eeb916c",
+                    "bytes_per_launch": 1.667e9}
 PEAK_MFMA_TFLOPS = 2500.0      # MI355X dense bf16 / fp16 MFMA
 PEAK_HBM_GBPS = 8000.0
 
