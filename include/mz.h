@@ -546,9 +546,10 @@ int64_t mz_attention_split_workspace_bytes(int32_t m, int32_t n_q_heads, int32_t
                                            int32_t n_split);
 
 /* The split count the restore uses for m query rows up to max_pos with
- * workspace_bytes of workspace: enough workgroups for two per compute unit,
- * at least 4 key tiles per split, at most 64 splits; 1 when the unsplit
- * kernel already fills the GPU. */
+ * workspace_bytes of workspace: enough workgroups for two per compute unit
+ * (one where the m rows make at most 16 (row, query head) columns per KV
+ * head, the few-column kernel), at least 4 key tiles per split, at most 64
+ * splits; 1 when the unsplit kernel already fills the GPU. */
 int32_t mz_attention_auto_splits(int32_t m, int32_t max_pos, int32_t n_q_heads, int32_t n_kv_heads,
                                  int32_t head_dim, int64_t workspace_bytes);
 

@@ -1025,11 +1025,15 @@ int attention_auto_splits(int m, int max_pos, int n_q, int n_kv, int head_dim, i
   const int n_qtiles = (m + 32 * qw - 1) / (32 * qw);
   const int wgs = n_qtiles * n_kv;
   const int n_kt = max_pos / KT + 1;
-  // two workgroups per CU (their LDS fits twice) over 256 CUs, at least 4
-  // key tiles per split, and partials that fit the workspace
+  // two workgroups per CU (their LDS fits twice) over 256 CUs -- one for
+  // the few-column kernel, which streams a split's keys fastest alone (8B
+  // decode step, 32900 keys: 30.5 us at 31 splits against 32.0 at 58, 36.7
+  // at 47 and 36.1 at 24) -- at least 4 key tiles per split, and partials
+  // that fit the workspace
   constexpr int kTarget = 512, kMinTiles = 4, kMaxSplits = 64;
+  const int target = m * group <= kFewCols ? kTarget / 2 : kTarget;
   if (wgs >= kTarget / 2 || n_kt < 2 * kMinTiles) return 1;
-  int ns = std::min({(kTarget + wgs - 1) / wgs, n_kt / kMinTiles, kMaxSplits});
+  int ns = std::min({(target + wgs - 1) / wgs, n_kt / kMinTiles, kMaxSplits});
   while (ns > 1 && attention_split_ws_bytes(m, n_q, head_dim, ns) > ws_cap) --ns;
   if (ns <= 1) return 1;
   const int tps = (n_kt + ns - 1) / ns;
