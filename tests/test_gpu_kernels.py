@@ -472,7 +472,7 @@ def test_gemm_queued(M, N, K, epi):
     _gemm_case(M, N, K, epi, seed=M + 7, sample_rows=rows, n_split="queued")
 
 
-def _attn_case(nq, nkv, hd, C, S, qpos, seed, sample=None, n_split=None):
+def _attn_case(nq, nkv, hd, C, S, qpos, seed, sample=None, n_split=None, n_table=None):
     """n_split: None for mz_attention, "queued" for mz_attention_queued (run
     twice on the same queues, which must come back zero, and equal to
     mz_attention bit for bit), else mz_attention_split with that many key
@@ -496,6 +496,10 @@ def _attn_case(nq, nkv, hd, C, S, qpos, seed, sample=None, n_split=None):
         kpart[table[c], :n] = K[c * C:c * C + n]
         vpart[table[c], :, :n] = V[c * C:c * C + n].T
     slab = np.concatenate([kpart.reshape(n_slots, -1), vpart.reshape(n_slots, -1)], axis=1)
+    if n_table is not None:
+        # a longer table than the keys need (entries past them name slot 0)
+        table = np.concatenate([table, np.zeros(n_table - nch, np.int32)])
+        nch = n_table
     qpos = np.asarray(qpos, np.int32)
     M = qpos.size
     q = (rng.standard_normal((M, nq, hd)) * 1.0).astype(np.float16)
@@ -601,6 +605,14 @@ def test_attention_queued(nq, nkv, hd, C, S):
     _attn_case(nq, nkv, hd, C, S, np.arange(S), seed=11, n_split="queued")
     _attn_case(nq, nkv, hd, C, S, gappy, seed=12, n_split="queued")
     _attn_case(nq, nkv, hd, C, S, [S - 1], seed=13, n_split="queued")
+
+
+def test_attention_max_table():
+    """A chunk table of 8192 entries, the most the attention entry points
+    take (its stretch for each work item is copied into LDS): the plain, the
+    work-queue and the split forms against the exact definition."""
+    for n_split in (None, "queued", 4):
+        _attn_case(32, 8, 128, 64, 700, np.arange(700), seed=41, n_split=n_split, n_table=8192)
 
 
 @pytest.mark.parametrize("nq,nkv,hd,C,S", [
