@@ -177,7 +177,8 @@ constexpr int LM_GROUP = 4;    // rows whose codes are in flight together per wa
 // codes q in 0..15, x . d (q - 8) over a block = d (sum x q - 8 sum x), the
 // block's sum of x being precomputed; nibbles become floats with the
 // byte-to-float conversions.  A wave takes its 64 rows LM_GROUP at a time,
-// issuing the loads of the group before any arithmetic.
+// with two groups in flight: the loads of the next group are issued before
+// the current one is summed.
 // byte K of v as a float (one v_cvt_f32_ubyteK)
 template <int K>
 __device__ __forceinline__ float ubyte_f32(uint32_t v) { return (float)((v >> (8 * K)) & 0xFFu); }
@@ -224,23 +225,22 @@ __global__ __launch_bounds__(256) void lm_head_kernel(const float* __restrict__ 
   float best = -INFINITY;
   int32_t best_i = 0x7fffffff;
   const int v0 = blockIdx.x * LM_ROWS + w * (LM_ROWS / 4);
-  for (int g = 0; g < LM_ROWS / 4; g += LM_GROUP) {
-    uint4 q[LM_GROUP][NBL];
-    uint16_t sc[LM_GROUP][NBL];
+  // codes and scales of rows g .. g + LM_GROUP - 1 of this wave, from indices
+  // clamped into range (blocks past the row's end read its last block and
+  // meet x = 0; rows past the vocabulary read its last row and are not kept)
+  auto load_group = [&](int g, uint4 (&q)[LM_GROUP][NBL], uint16_t (&sc)[LM_GROUP][NBL]) {
 #pragma unroll
     for (int k = 0; k < LM_GROUP; ++k) {
       const int v = min(v0 + g + k, vocab - 1);
 #pragma unroll
       for (int j = 0; j < NBL; ++j) {
-        const int b = lane + 64 * j;
-        q[k][j] = make_uint4(0, 0, 0, 0);
-        sc[k][j] = 0;
-        if (b < nb) {
-          q[k][j] = *reinterpret_cast<const uint4*>(nib + (int64_t)v * (d / 2) + b * 16);
-          sc[k][j] = scale[(int64_t)v * nb + b];
-        }
+        const int b = min(lane + 64 * j, nb - 1);
+        q[k][j] = *reinterpret_cast<const uint4*>(nib + (int64_t)v * (d / 2) + b * 16);
+        sc[k][j] = scale[(int64_t)v * nb + b];
       }
     }
+  };
+  auto dot_group = [&](int g, const uint4 (&q)[LM_GROUP][NBL], const uint16_t (&sc)[LM_GROUP][NBL]) {
 #pragma unroll
     for (int k = 0; k < LM_GROUP; ++k) {
       float acc = 0.f;
@@ -274,6 +274,17 @@ __global__ __launch_bounds__(256) void lm_head_kernel(const float* __restrict__ 
         if (lane == 0) logits[v] = acc;
       }
     }
+  };
+  // two groups in flight: the next group's codes load while this one is summed
+  static_assert((LM_ROWS / 4) % (2 * LM_GROUP) == 0, "whole group pairs per wave");
+  uint4 qa[LM_GROUP][NBL], qb[LM_GROUP][NBL];
+  uint16_t sa[LM_GROUP][NBL], sb[LM_GROUP][NBL];
+  load_group(0, qa, sa);
+  for (int g = 0; g < LM_ROWS / 4; g += 2 * LM_GROUP) {
+    load_group(g + LM_GROUP, qb, sb);
+    dot_group(g, qa, sa);
+    if (g + 2 * LM_GROUP < LM_ROWS / 4) load_group(g + 2 * LM_GROUP, qa, sa);
+    dot_group(g + LM_GROUP, qb, sb);
   }
   if (lane == 0) {
     bval[w] = best;

@@ -465,7 +465,10 @@ struct mz_ctx {
   int32_t* part_idx = nullptr;
   int32_t* d_token = nullptr;
 
-  // restore metadata (device + pinned staging)
+  // restore metadata: a pinned staging block and its device mirror of the
+  // same size, uploaded by one copy per restore; the pointers below are set
+  // per restore to their stretches of the mirror
+  uint8_t* d_meta = nullptr;
   int32_t* d_tables = nullptr;
   // per layer: rows whose K/V are written (positions, slot offsets, indices
   // into the layer's input rows) and rows carried on (positions, indices)
@@ -554,7 +557,7 @@ struct mz_ctx {
   }
   // A single row runs as the one-launch GEMV (option gemv_direct)
   bool gemv_one(int m, int n, int k) const { return gemv_direct && m == 1 && mzk::gemv1_ok(n, k); }
-  int32_t* d_codec_slots = nullptr;  // per restore: destination slot of each compressed chunk
+  int32_t* d_codec_slots = nullptr;  // per restore: destination slot of each compressed chunk (in d_meta)
   hipEvent_t ev_meta = nullptr;      // restore metadata uploaded (the swap stream reads some)
   bool timing = false;
   std::vector<hipEvent_t> ev_pool;
@@ -902,19 +905,21 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
     s_tok[i] = p < N ? x->tokens[p] : prompt[p - N];
   }
   hipStream_t cs = x->s_compute, ss = x->s_swap;
-  HIPCHK(hipMemcpyAsync(x->d_tables, s_tab, b_tab, hipMemcpyHostToDevice, cs));
-  if (b_pos) {
-    HIPCHK(hipMemcpyAsync(x->d_pos, s_pos, b_pos, hipMemcpyHostToDevice, cs));
-    HIPCHK(hipMemcpyAsync(x->d_kvoff, s_off, b_off, hipMemcpyHostToDevice, cs));
-    HIPCHK(hipMemcpyAsync(x->d_dix, s_dix, b_dix, hipMemcpyHostToDevice, cs));
-  }
-  HIPCHK(hipMemcpyAsync(x->d_posq, s_posq, b_posq, hipMemcpyHostToDevice, cs));
-  HIPCHK(hipMemcpyAsync(x->d_qix, s_qix, b_qix, hipMemcpyHostToDevice, cs));
-  HIPCHK(hipMemcpyAsync(x->d_tok, s_tok, b_tok, hipMemcpyHostToDevice, cs));
-  if (b_cs) {
-    HIPCHK(hipMemcpyAsync(x->d_codec_slots, s_cs, b_cs, hipMemcpyHostToDevice, cs));
-    HIPCHK(hipEventRecord(x->ev_meta, cs));
-  }
+  // one upload of the whole staged stretch: each copy call costs tens of
+  // microseconds of host time, which a one-token step waits on in full
+  auto dev = [&](const void* hp) { return x->d_meta + ((const uint8_t*)hp - sp); };
+  x->d_tables = (int32_t*)dev(s_tab);
+  x->d_pos = (int32_t*)dev(s_pos);
+  x->d_kvoff = (int64_t*)dev(s_off);
+  x->d_dix = (int32_t*)dev(s_dix);
+  x->d_posq = (int32_t*)dev(s_posq);
+  x->d_qix = (int32_t*)dev(s_qix);
+  x->d_tok = (int32_t*)dev(s_tok);
+  x->d_codec_slots = (int32_t*)dev(s_cs);
+  const size_t b_meta = (size_t)((const uint8_t*)s_cs - sp) + b_cs;
+  if (b_meta > x->stage_bytes) fail(MZ_EINVAL, "internal: restore metadata overruns the staging buffer");
+  HIPCHK(hipMemcpyAsync(x->d_meta, sp, b_meta, hipMemcpyHostToDevice, cs));
+  if (b_cs) HIPCHK(hipEventRecord(x->ev_meta, cs));
 
   if (x->debug_poison) {
     // fresh slots hold fp16 NaN until restored or recomputed: a missed row or
@@ -1293,14 +1298,10 @@ mz_status mz_load_model(const mz_model_cfg* cfg, const void* blob, size_t nbytes
 
     // restore metadata
     const int64_t tot = (int64_t)c.L * M;
-    c.d_tables = (int32_t*)dmalloc((size_t)c.L * c.max_chunks * 4);
-    c.d_pos = (int32_t*)dmalloc((size_t)tot * 4);
-    c.d_kvoff = (int64_t*)dmalloc((size_t)tot * 8);
-    c.d_dix = (int32_t*)dmalloc((size_t)tot * 4);
-    c.d_posq = (int32_t*)dmalloc((size_t)tot * 4);
-    c.d_qix = (int32_t*)dmalloc((size_t)tot * 4);
-    c.d_tok = (int32_t*)dmalloc((size_t)M * 4);
+    // tables and compressed-chunk slots (4 + 4 bytes per layer and chunk),
+    // five per-row arrays (24 bytes per layer and row), tokens, alignment
     c.stage_bytes = (size_t)c.L * c.max_chunks * 8 + (size_t)tot * 24 + (size_t)M * 4 + 9 * 256;
+    c.d_meta = (uint8_t*)dmalloc(c.stage_bytes);
     c.comp_bytes = mzk::kv_compressed_bytes(c.slot_bytes / 2);
     c.split_ws_bytes = std::min<int64_t>(
         int64_t(64) << 20, std::max(mzk::attention_split_ws_bytes(std::min<int64_t>(M, 4096), c.nq, c.hd, 64),
@@ -1334,11 +1335,10 @@ void mz_free(mz_ctx* x) {
   (void)hipSetDevice(x->device);
   if (x->s_compute) (void)hipStreamSynchronize(x->s_compute);
   if (x->s_swap) (void)hipStreamSynchronize(x->s_swap);
-  void* dptrs[] = {x->codec_stage, x->d_codec_slots, x->split_ws, x->attn_wq, x->gemm_wq, x->w_slab, x->emb_nib, x->emb_sc, x->lm_nib, x->lm_sc,
+  void* dptrs[] = {x->codec_stage, x->d_meta, x->split_ws, x->attn_wq, x->gemm_wq, x->w_slab, x->emb_nib, x->emb_sc, x->lm_nib, x->lm_sc,
                    x->rope_cs, x->kv_slab,
                    x->h[0], x->h[1], x->xb, x->qf, x->kvf, x->q16, x->act, x->logits, x->part_val,
-                   x->part_idx, x->d_token, x->d_tables, x->d_pos, x->d_kvoff, x->d_dix, x->d_posq,
-                   x->d_qix, x->d_tok};
+                   x->part_idx, x->d_token};
   for (void* p : dptrs)
     if (p) (void)hipFree(p);
   if (x->w_image) (void)hipHostFree(x->w_image);
@@ -1377,7 +1377,6 @@ mz_status mz_set_option(mz_ctx* x, const char* key, int64_t value) {
     else if (k == "kv_codec") {
       if (value && !x->codec_stage) {
         HIPCHK(hipMalloc((void**)&x->codec_stage, (size_t)x->max_chunks * (size_t)x->comp_bytes));
-        HIPCHK(hipMalloc((void**)&x->d_codec_slots, (size_t)x->L * x->max_chunks * sizeof(int32_t)));
       }
       x->kv_codec = value != 0;
     }
