@@ -305,6 +305,8 @@ __device__ __forceinline__ void attn_tile(const _Float16* __restrict__ Q, const 
   // causal mask of tile kt (keys past the lane's query position -> -inf).
   // Score slot (kk, r) of lane group `half` holds key
   // kt*KT + 8*half + kk*32 + 16*(r/8) + 4*((r/4)%2) + r%4 (the pi order).
+  // (a bit select per score, -inf where the sign of th - c says c > th: no
+  // per-score compare masks in scalar registers)
   auto mask_tile = [&](f32x16* sc, int kt) {
     const int th = p - kt * KT - 8 * half;
 #pragma unroll
@@ -312,7 +314,9 @@ __device__ __forceinline__ void attn_tile(const _Float16* __restrict__ Q, const 
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int c = kk * 32 + 16 * (r >> 3) + 4 * ((r >> 2) & 1) + (r & 3);
-        if (c > th) sc[kk][r] = -INFINITY;
+        const uint32_t m = (uint32_t)((th - c) >> 31);
+        const float v = sc[kk][r];   // (a bit cast of a vector element itself reads element 0)
+        sc[kk][r] = __builtin_bit_cast(float, (__builtin_bit_cast(uint32_t, v) & ~m) | (0xFF800000u & m));
       }
   };
   auto tile_max = [&](const f32x16* sc) {
@@ -352,6 +356,7 @@ __device__ __forceinline__ void attn_tile(const _Float16* __restrict__ Q, const 
     dst[2 * (r2 & 3)] = (_Float16)e0;
     dst[2 * (r2 & 3) + 1] = (_Float16)e1;
     l_i = __builtin_amdgcn_fdot2(f16x2{dst[2 * (r2 & 3)], dst[2 * (r2 & 3) + 1]}, ones, l_i, false);
+    asm volatile("" : "+v"(l_i));   // the row sum is added here, beside its exponentials
   };
   constexpr int TN = HD / 32;          // output accumulators (32 dimensions each)
   constexpr int NQK = 2 * (HD / 16);   // score MFMAs per tile (8 or 16)

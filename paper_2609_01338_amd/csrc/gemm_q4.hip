@@ -370,6 +370,30 @@ __device__ __forceinline__ void gemm_tile(const _Float16* __restrict__ X, const 
       rope_epilogue<EPI, BM, 1>(acc, ea, Y, M, mt, nt, wm, wn, col_in, row_in);
     return;
   }
+  if constexpr (EPI == kEpiAdd) {
+    // the residuals of a lane's 4 rows x 8 columns are all read before any
+    // is written back (from rows clamped into range): one memory round trip
+    // per 16-row group instead of one per row
+#pragma unroll
+    for (int i = 0; i < MI; ++i) {
+      const int row0 = mt * BM + wm * (BM / 4) + i * 16 + row_in;
+      float y_old[4][8];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float* y = reinterpret_cast<const float*>(Y) + (size_t)min(row0 + r, M - 1) * N;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) y_old[r][j] = y[nt * BN + wn * 128 + j * 16 + col_in];
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        if (row0 + r >= M) continue;
+        float* y = reinterpret_cast<float*>(Y) + (size_t)(row0 + r) * N;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) y[nt * BN + wn * 128 + j * 16 + col_in] = y_old[r][j] + acc[i][j][r];
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < MI; ++i) {
 #pragma unroll
