@@ -371,25 +371,37 @@ __device__ __forceinline__ void gemm_tile(const _Float16* __restrict__ X, const 
     return;
   }
   if constexpr (EPI == kEpiAdd) {
-    // the residuals of a lane's 4 rows x 8 columns are all read before any
-    // is written back (from rows clamped into range): one memory round trip
-    // per 16-row group instead of one per row
-#pragma unroll
-    for (int i = 0; i < MI; ++i) {
+    // the residuals of a lane's 4 rows x 8 columns of one 16-row group are
+    // read together (from rows clamped into range), and the next group's are
+    // requested before this group is written back
+    auto load_group = [&](int i, float (&yo)[4][8]) {
       const int row0 = mt * BM + wm * (BM / 4) + i * 16 + row_in;
-      float y_old[4][8];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const float* y = reinterpret_cast<const float*>(Y) + (size_t)min(row0 + r, M - 1) * N;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) y_old[r][j] = y[nt * BN + wn * 128 + j * 16 + col_in];
+        for (int j = 0; j < 8; ++j) yo[r][j] = y[nt * BN + wn * 128 + j * 16 + col_in];
       }
+    };
+    auto store_group = [&](int i, const float (&yo)[4][8]) {
+      const int row0 = mt * BM + wm * (BM / 4) + i * 16 + row_in;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         if (row0 + r >= M) continue;
         float* y = reinterpret_cast<float*>(Y) + (size_t)(row0 + r) * N;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) y[nt * BN + wn * 128 + j * 16 + col_in] = y_old[r][j] + acc[i][j][r];
+        for (int j = 0; j < 8; ++j) y[nt * BN + wn * 128 + j * 16 + col_in] = yo[r][j] + acc[i][j][r];
+      }
+    };
+    float ya[4][8], yb[4][8];
+    load_group(0, ya);
+#pragma unroll
+    for (int i = 0; i < MI; i += 2) {
+      if (i + 1 < MI) load_group(i + 1, yb);
+      store_group(i, ya);
+      if (i + 1 < MI) {
+        if (i + 2 < MI) load_group(i + 2, ya);
+        store_group(i + 1, yb);
       }
     }
     return;
