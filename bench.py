@@ -32,8 +32,8 @@ METRIC = "KV-recompute prefill tokens/s + TTFT ms from evicted state, 1 MI355X"
 # valid only for the kernel source they were taken on and the 8B workload.
 MEASURED_TRAFFIC = {"kernel": "attn_kernel", "workload": "8b",
                     "source": "paper_2609_01338_amd/csrc/attention.hip",
-                    "sha256": "b85b555e8eaac305f1058310613f10d0d46284bb4ec6a863cc700d4e6eeb916c",
-                    "bytes_per_launch": 1.667e9}
+                    "sha256": "87004af1d4db739bc9f78d377b38fddb685b5d3d973c1b468e54257ecba67e42",
+                    "bytes_per_launch": 1.658e9}
 PEAK_MFMA_TFLOPS = 2500.0      # MI355X dense bf16 / fp16 MFMA
 PEAK_HBM_GBPS = 8000.0
 
