@@ -149,9 +149,12 @@ mz_status mz_first_token(mz_ctx *ctx, int32_t *token_out, float *logits_out);
  * tokens_out[0]; then append that and continue, n tokens in all (host,
  * caller-owned tokens_out [n]).  The last generated token is not appended,
  * as with mz_first_token.  Any evicted units are restored by the first step
- * (it is a restore with a one-token prompt).  Errors: EINVAL (n < 0, NULL
- * tokens_out, token out of range, or a context that would pass max_ctx),
- * and those of mz_restore_and_prefill. */
+ * (it is a restore with a one-token prompt).  The steps after the first are
+ * issued back to back: each step's token stays on the device for the next
+ * step's embedding, and tokens_out is written when all have run.  Errors:
+ * EINVAL (n < 0, NULL tokens_out, token out of range, or a context that
+ * would pass max_ctx), and those of mz_restore_and_prefill; tokens_out then
+ * holds the tokens of the steps that ran. */
 mz_status mz_generate(mz_ctx *ctx, int32_t token, int32_t n, int32_t *tokens_out);
 
 /* Engine options: "overlap" (1: swap-in overlapped with compute, default;

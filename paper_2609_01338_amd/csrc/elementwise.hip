@@ -135,12 +135,14 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(const float* __restrict__ 
 }
 
 // One block per row: thread b dequantizes block b of the row.
+// last_tok (device, or null): the last row's token, read from device memory
+// instead of tok (a decode step whose token the previous step chose).
 __global__ __launch_bounds__(256) void embed_kernel(const uint8_t* __restrict__ nib,
                                                     const uint16_t* __restrict__ scale,
                                                     const int32_t* __restrict__ tok, int d,
-                                                    float* __restrict__ h) {
+                                                    float* __restrict__ h, const int32_t* __restrict__ last_tok) {
   const int row = blockIdx.x;
-  const int64_t t = tok[row];
+  const int64_t t = (last_tok && row == (int)gridDim.x - 1) ? *last_tok : tok[row];
   const int nb = d / 32;
   float* out = h + (size_t)row * d;
   for (int b = threadIdx.x; b < nb; b += blockDim.x) {
@@ -306,7 +308,7 @@ __global__ __launch_bounds__(256) void lm_head_kernel(const float* __restrict__ 
 
 __global__ __launch_bounds__(256) void argmax_kernel(const float* __restrict__ val,
                                                      const int32_t* __restrict__ idx, int n,
-                                                     int32_t* __restrict__ token) {
+                                                     int32_t* __restrict__ token, int32_t* __restrict__ token2) {
   __shared__ float sv[256];
   __shared__ int32_t si[256];
   float bv = -INFINITY;
@@ -330,7 +332,10 @@ __global__ __launch_bounds__(256) void argmax_kernel(const float* __restrict__ v
     }
     __syncthreads();
   }
-  if (threadIdx.x == 0) *token = si[0];
+  if (threadIdx.x == 0) {
+    *token = si[0];
+    if (token2) *token2 = si[0];
+  }
 }
 
 __global__ void fill_kernel(uint32_t* __restrict__ p, int64_t n, uint32_t value) {
@@ -365,8 +370,8 @@ void launch_rope_kv(const float* qkv, int qkv_stride, int m, const int32_t* pos,
 }
 
 void launch_embed(const uint8_t* e_nib, const uint16_t* e_scale, const int32_t* tok, int m, int d,
-                  float* h, hipStream_t s) {
-  hipLaunchKernelGGL(embed_kernel, dim3(m), dim3(256), 0, s, e_nib, e_scale, tok, d, h);
+                  float* h, hipStream_t s, const int32_t* last_tok) {
+  hipLaunchKernelGGL(embed_kernel, dim3(m), dim3(256), 0, s, e_nib, e_scale, tok, d, h, last_tok);
 }
 
 void launch_gather_rows(const float* src, const int32_t* idx, int m, int d, float* dst,
@@ -376,7 +381,7 @@ void launch_gather_rows(const float* src, const int32_t* idx, int m, int d, floa
 
 void launch_lm_head(const float* h_last, int d, float eps, const uint8_t* w_nib,
                     const uint16_t* w_scale, int vocab, float* logits, float* part_val,
-                    int32_t* part_idx, int32_t* token, hipStream_t s) {
+                    int32_t* part_idx, int32_t* token, hipStream_t s, int32_t* token2) {
   const int nblk = (vocab + LM_ROWS - 1) / LM_ROWS;
   const int nbl = (d / 32 + 63) / 64;   // 32-element blocks per lane (d <= 8192)
   switch (nbl) {
@@ -389,7 +394,7 @@ void launch_lm_head(const float* h_last, int d, float eps, const uint8_t* w_nib,
     default: hipLaunchKernelGGL(lm_head_kernel<4>, dim3(nblk), dim3(256), 0, s, h_last, d, eps, w_nib, w_scale,
                                 vocab, logits, part_val, part_idx); break;
   }
-  hipLaunchKernelGGL(argmax_kernel, dim3(1), dim3(256), 0, s, part_val, part_idx, nblk, token);
+  hipLaunchKernelGGL(argmax_kernel, dim3(1), dim3(256), 0, s, part_val, part_idx, nblk, token, token2);
 }
 
 void launch_fill(void* p, int64_t n_words, uint32_t value, hipStream_t s) {

@@ -134,20 +134,20 @@ void launch_rope_kv(const float* qkv, int qkv_stride, int m, const int32_t* pos,
                     void* q_out, void* slab, hipStream_t s);
 
 // h float [m][d] = dequant(E[tok[i]]) with E split into nibbles [V][d/2] and
-// fp16 scales [V][d/32].
+// fp16 scales [V][d/32]; with last_tok (device) row m - 1 takes *last_tok.
 void launch_embed(const uint8_t* e_nib, const uint16_t* e_scale, const int32_t* tok, int m, int d,
-                  float* h, hipStream_t s);
+                  float* h, hipStream_t s, const int32_t* last_tok = nullptr);
 
 // dst[i] = src[idx[i]] for rows of d floats.
 void launch_gather_rows(const float* src, const int32_t* idx, int m, int d, float* dst,
                         hipStream_t s);
 
 // logits float [V] = RMSNorm(h_last) . W_lm^T (split layout as the embedding),
-// then token = argmax (lowest index on ties).  part_val/part_idx hold
-// ceil(V / 64) partials.
+// then token = argmax (lowest index on ties), also stored to token2 when
+// given.  part_val/part_idx hold ceil(V / 256) partials (256 rows a block).
 void launch_lm_head(const float* h_last, int d, float eps, const uint8_t* w_nib,
                     const uint16_t* w_scale, int vocab, float* logits, float* part_val,
-                    int32_t* part_idx, int32_t* token, hipStream_t s);
+                    int32_t* part_idx, int32_t* token, hipStream_t s, int32_t* token2 = nullptr);
 
 // Fill n 32-bit words with zero (graph-capturable, unlike memset nodes).
 void launch_zero(void* p, int64_t n_words, hipStream_t s);

@@ -464,6 +464,7 @@ struct mz_ctx {
   float* part_val = nullptr;
   int32_t* part_idx = nullptr;
   int32_t* d_token = nullptr;
+  int32_t* d_gen = nullptr;          // [max_ctx] tokens chosen by the steps of mz_generate
 
   // restore metadata: a pinned staging block and its device mirror of the
   // same size, uploaded by one copy per restore; the pointers below are set
@@ -559,6 +560,7 @@ struct mz_ctx {
   bool gemv_one(int m, int n, int k) const { return gemv_direct && m == 1 && mzk::gemv1_ok(n, k); }
   int32_t* d_codec_slots = nullptr;  // per restore: destination slot of each compressed chunk (in d_meta)
   hipEvent_t ev_meta = nullptr;      // restore metadata uploaded (the swap stream reads some)
+  bool meta_recorded = false;        // ev_meta stands for an upload from the staging block
   bool timing = false;
   std::vector<hipEvent_t> ev_pool;
   size_t ev_used = 0;
@@ -709,7 +711,11 @@ struct CopyJob {
 };
 
 // Shared by mz_restore_and_prefill and mz_prefill_context.
-void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt) {
+// dev_tok (device, or null): the last prompt token is read from there by the
+// embedding instead of from prompt (a decode step whose token the previous
+// step left on the device; prompt then holds a placeholder).
+void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt,
+                              const int32_t* dev_tok = nullptr) {
   const auto t_entry = std::chrono::steady_clock::now();
   auto ms_since = [&](std::chrono::steady_clock::time_point t) {
     return std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t).count();
@@ -855,6 +861,10 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
                b_tok = (size_t)rows.nR[0] * 4, b_cs = (size_t)cofs[L] * 4;
   const size_t need = b_tab + b_pos + b_off + b_dix + b_posq + b_qix + b_tok + b_cs + 8 * 256;
   if (need > x->stage_bytes) fail(MZ_EINVAL, "restore metadata exceeds the staging buffer");
+  // the staging block is rewritten only after the previous restore's upload
+  // out of it has been done (a restore issued before the last one's first
+  // token may find it still in flight)
+  if (x->meta_recorded) HIPCHK(hipEventSynchronize(x->ev_meta));
   uint8_t* sp = x->h_stage;
   int32_t* s_tab = (int32_t*)sp;
   int32_t* s_pos = (int32_t*)(sp + round_up(b_tab, 256));
@@ -919,7 +929,8 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
   const size_t b_meta = (size_t)((const uint8_t*)s_cs - sp) + b_cs;
   if (b_meta > x->stage_bytes) fail(MZ_EINVAL, "internal: restore metadata overruns the staging buffer");
   HIPCHK(hipMemcpyAsync(x->d_meta, sp, b_meta, hipMemcpyHostToDevice, cs));
-  if (b_cs) HIPCHK(hipEventRecord(x->ev_meta, cs));
+  HIPCHK(hipEventRecord(x->ev_meta, cs));
+  x->meta_recorded = true;
 
   if (x->debug_poison) {
     // fresh slots hold fp16 NaN until restored or recomputed: a missed row or
@@ -989,7 +1000,7 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
   const int d = x->d;
   const double bpe_w = 0.5625;   // Q4_0 bytes per weight
   x->timed(kKEmbed, 0, (double)rows.nR[0] * (d * bpe_w + d * 4.0), cs, [&] {
-    mzk::launch_embed(x->emb_nib, x->emb_sc, x->d_tok, rows.nR[0], d, x->h[0], cs);
+    mzk::launch_embed(x->emb_nib, x->emb_sc, x->d_tok, rows.nR[0], d, x->h[0], cs, dev_tok);
   });
   int cur = 0;
   double algo = 2.0 * d * x->V;
@@ -1295,6 +1306,7 @@ mz_status mz_load_model(const mz_model_cfg* cfg, const void* blob, size_t nbytes
     c.part_val = (float*)dmalloc((size_t)nblk * 4);
     c.part_idx = (int32_t*)dmalloc((size_t)nblk * 4);
     c.d_token = (int32_t*)dmalloc(4);
+    c.d_gen = (int32_t*)dmalloc((size_t)c.max_ctx * 4);
 
     // restore metadata
     const int64_t tot = (int64_t)c.L * M;
@@ -1338,7 +1350,7 @@ void mz_free(mz_ctx* x) {
   void* dptrs[] = {x->codec_stage, x->d_meta, x->split_ws, x->attn_wq, x->gemm_wq, x->w_slab, x->emb_nib, x->emb_sc, x->lm_nib, x->lm_sc,
                    x->rope_cs, x->kv_slab,
                    x->h[0], x->h[1], x->xb, x->qf, x->kvf, x->q16, x->act, x->logits, x->part_val,
-                   x->part_idx, x->d_token};
+                   x->part_idx, x->d_token, x->d_gen};
   for (void* p : dptrs)
     if (p) (void)hipFree(p);
   if (x->w_image) (void)hipHostFree(x->w_image);
@@ -1666,14 +1678,52 @@ mz_status mz_first_token(mz_ctx* x, int32_t* token_out, float* logits_out) {
 mz_status mz_generate(mz_ctx* x, int32_t token, int32_t n, int32_t* tokens_out) {
   if (!x) return MZ_EINVAL;
   if (n < 0 || (n > 0 && !tokens_out)) return guarded(x, [&] { fail(MZ_EINVAL, "bad n or tokens_out"); });
-  for (int32_t i = 0; i < n; ++i) {
-    const int32_t t = i == 0 ? token : tokens_out[i - 1];
-    mz_status st = mz_restore_and_prefill(x, &t, 1);
-    if (st != MZ_OK) return st;
-    st = mz_first_token(x, &tokens_out[i], nullptr);
-    if (st != MZ_OK) return st;
-  }
-  return MZ_OK;
+  if (n == 0) return MZ_OK;
+  // the first step as a restore and first token of its own (it may bring
+  // back evicted units and time their copies)
+  mz_status st = mz_restore_and_prefill(x, &token, 1);
+  if (st != MZ_OK) return st;
+  st = mz_first_token(x, &tokens_out[0], nullptr);
+  if (st != MZ_OK || n == 1) return st;
+  // the others back to back: each step's token stays on the device, where
+  // the argmax leaves it (d_gen[i]) and the next step's embedding reads it;
+  // the host plans the next step while the GPU runs this one and learns
+  // the tokens at the end (the context records placeholders until then)
+  return guarded(x, [&] {
+    const size_t base = x->tokens.size();   // position at which step 1 prefills tokens_out[0]
+    if ((int64_t)n > (int64_t)x->max_ctx) fail(MZ_EINVAL, "n exceeds max_ctx");
+    hipStream_t cs = x->s_compute;
+    int done = 1;   // steps 0 .. done - 1 are enqueued (and their tokens final after settle)
+    auto settle = [&]() {
+      HIPCHK(hipStreamSynchronize(cs));
+      if (done > 1)
+        HIPCHK(hipMemcpy(&tokens_out[1], x->d_gen + 1, (size_t)(done - 1) * 4, hipMemcpyDeviceToHost));
+      // step i >= 2 prefilled tokens_out[i - 1] at position base + i - 1
+      for (int i = 2; i < done; ++i) x->tokens[base + i - 1] = tokens_out[i - 1];
+    };
+    try {
+      for (int i = 1; i < n; ++i) {
+        const int32_t placeholder = 0;
+        if (i == 1)
+          restore_and_prefill_impl(x, &tokens_out[0], 1);
+        else
+          restore_and_prefill_impl(x, &placeholder, 1, x->d_gen + (i - 1));
+        x->timed(kKLmHead, 2.0 * x->d * x->V, (double)x->V * x->d * 0.5625 + x->V * 4.0, cs, [&] {
+          mzk::launch_lm_head(x->h_last, x->d, x->cfg.rms_eps, x->lm_nib, x->lm_sc, x->V, x->logits,
+                              x->part_val, x->part_idx, x->d_token, cs, x->d_gen + i);
+        });
+        x->have_last = false;
+        done = i + 1;
+      }
+    } catch (...) {
+      try {
+        settle();
+      } catch (...) {
+      }
+      throw;
+    }
+    settle();
+  });
 }
 
 mz_status mz_stats(mz_ctx* x, char* out, size_t cap) {

@@ -457,6 +457,54 @@ def test_decode_fused_paths_same_bits(key, option):
         assert k1.tobytes() == k0.tobytes() and v1.tobytes() == v0.tobytes(), key
 
 
+@pytest.mark.parametrize("key", ["tiny", "8b"])
+def test_generate_matches_step_by_step(key):
+    """mz_generate issues its steps after the first back to back, each
+    step's token read by the next step's embedding from device memory; a
+    loop of one-token restores and first tokens waits for every token on
+    the host.  Same tokens, and the context they leave behind is the same:
+    the next restore's logits and the generated positions' K/V rows equal
+    bit for bit (the placeholders recorded during the run are replaced by
+    the tokens)."""
+    torch_cuda()
+    w = W.WORKLOADS[key]
+    if key == "8b":
+        w = w.scaled(n_layers=2, n_ctx=512, n_prompt=16)
+    m = w.model
+    C, dkv = m.chunk_tokens, m.dkv
+    ctx, prm = W.make_tokens(w)
+    S, n = ctx.size + len(prm), 7
+    outs = []
+    for piped in (1, 0):
+        eng = mz.Engine(m, blob_for(w), max_ctx=S + n + 9)
+        try:
+            mz.mz_prefill_context(eng.ctx, np.concatenate([ctx, prm]))
+            tok, _ = mz.mz_first_token(eng.ctx, m.vocab)
+            if piped:
+                toks = mz.mz_generate(eng.ctx, tok, n)
+            else:
+                toks, t = [], tok
+                for _ in range(n):
+                    mz.mz_restore_and_prefill(eng.ctx, np.array([t], np.int32))
+                    t = mz.mz_first_token(eng.ctx)
+                    toks.append(t)
+                toks = np.array(toks, np.int32)
+            # the context now ends with tokens toks[:-1]: evict nothing, prefill the last one
+            mz.mz_restore_and_prefill(eng.ctx, toks[-1:].astype(np.int32))
+            _, logits = mz.mz_first_token(eng.ctx, m.vocab)
+            kv = [mz.mz_read_kv(eng.ctx, l, c, C, dkv) for l in range(m.n_layers)
+                  for c in range(S // C, (S + n) // C + 1)]
+            outs.append((np.asarray(toks), logits, kv))
+        finally:
+            eng.close()
+    (t1, g1, kv1), (t0, g0, kv0) = outs
+    report("case", name=f"{key}-generate-piped", tokens=list(map(int, t1)))
+    assert (t1 == t0).all(), (t1, t0)
+    assert g1.tobytes() == g0.tobytes(), key
+    for (k1, v1), (k0, v0) in zip(kv1, kv0):
+        assert k1.tobytes() == k0.tobytes() and v1.tobytes() == v0.tobytes(), key
+
+
 @pytest.mark.parametrize("gemm_split", [1, 0])
 def test_rope_fused_same_bits(gemm_split):
     """The rotary embedding in the projection epilogues and split-K reduces
