@@ -505,6 +505,43 @@ def test_generate_matches_step_by_step(key):
         assert k1.tobytes() == k0.tobytes() and v1.tobytes() == v0.tobytes(), key
 
 
+def test_generate_past_max_ctx_keeps_tokens():
+    """mz_generate that runs out of context fails with EINVAL after the
+    steps that fit, and the context it leaves holds their real tokens (not
+    the placeholders recorded while their tokens were still on the device):
+    dropping every chunk and restoring recomputes all positions from the
+    recorded tokens, and gives the same logits, bit for bit, as after the
+    same steps taken one restore and first token at a time."""
+    torch_cuda()
+    m = TINY.model
+    ctx, _ = W.make_tokens(TINY)
+    S, fit = ctx.size, 6
+    outs = []
+    for piped in (1, 0):
+        eng = mz.Engine(m, blob_for(TINY), max_ctx=S + fit)
+        try:
+            e = eng.ctx
+            mz.mz_prefill_context(e, ctx)
+            tok = mz.mz_first_token(e)
+            if piped:
+                with pytest.raises(mz.MzError) as ei:
+                    mz.mz_generate(e, tok, fit + 4)
+                assert ei.value.status == mz.MZ_EINVAL
+            else:
+                t = tok
+                for _ in range(fit):
+                    mz.mz_restore_and_prefill(e, np.array([t], np.int32))
+                    t = mz.mz_first_token(e)
+            n_ch = (S + fit + m.chunk_tokens - 1) // m.chunk_tokens
+            mz.mz_evict(e, np.full((m.n_layers, n_ch), O.DROP, np.uint8))
+            mz.mz_restore_and_prefill(e, np.zeros(0, np.int32))
+            _, logits = mz.mz_first_token(e, m.vocab)
+            outs.append(logits)
+        finally:
+            eng.close()
+    assert outs[0].tobytes() == outs[1].tobytes()
+
+
 @pytest.mark.parametrize("gemm_split", [1, 0])
 def test_rope_fused_same_bits(gemm_split):
     """The rotary embedding in the projection epilogues and split-K reduces
