@@ -418,6 +418,9 @@ __device__ __forceinline__ void attn_tile(const _Float16* __restrict__ Q, const 
   if constexpr (SPLIT) {
     if (m_i == -INFINITY) m_i = 0.f;
   }
+  // every wave has read key tile kt0 before the first step's loads may reuse
+  // its buffer
+  __syncthreads();
 
   auto step = [&](int kt, f32x16* sc, f32x16* sn) {
     int tnext = 0;   // slot of key tile kt+3, read from ltab now, used a step later
