@@ -32,8 +32,8 @@ METRIC = "KV-recompute prefill tokens/s + TTFT ms from evicted state, 1 MI355X"
 # valid only for the kernel source they were taken on and the 8B workload.
 MEASURED_TRAFFIC = {"kernel": "attn_kernel", "workload": "8b",
                     "source": "paper_2609_01338_amd/csrc/attention.hip",
-                    "sha256": "87004af1d4db739bc9f78d377b38fddb685b5d3d973c1b468e54257ecba67e42",
-                    "bytes_per_launch": 1.658e9}
+                    "sha256": "914f2b770006ff42f74588729e8ee333a51d4c2bb5c06126eafac519b67bdd88",
+                    "bytes_per_launch": 1.654e9}
 PEAK_MFMA_TFLOPS = 2500.0      # MI355X dense bf16 / fp16 MFMA
 PEAK_HBM_GBPS = 8000.0
 
