@@ -10,8 +10,10 @@
 // A chunk slot stores K token-major ([C][dkv]) and V dimension-major
 // ([dkv][C], "hidden-dimension-first"), so both tiles load as plain 16-byte
 // rows.  A workgroup serves one KV head and a tile of query rows for all of
-// that head's G query heads; each wave owns 32 queries of one query head.  Per
-// 64-key tile K and V^T are staged in LDS once for the whole group, double
+// that head's G query heads when G divides 8 (8 waves: G heads x 8/G groups of
+// 32 rows), else for one of them (8 waves of 32 rows); each wave owns 32
+// queries of one query head.  Per 64-key tile K and V^T are staged in LDS
+// once for the whole workgroup, double
 // buffered: the next tile's global loads are in flight while the current one
 // is multiplied.  Scores are computed transposed, S^T = K Q^T,
 // with v_mfma_f32_32x32x16_f16 so that each lane holds 32 scores of a single
@@ -86,9 +88,9 @@ __device__ __forceinline__ void attn_tile(const _Float16* __restrict__ Q, const 
                                           const uint8_t* __restrict__ slab, const int32_t* __restrict__ table,
                                           int n_table,
                                           int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group,
-                                          int qw, float scale_log2, _Float16* __restrict__ O, int tps,
+                                          int qw, int gpw, float scale_log2, _Float16* __restrict__ O, int tps,
                                           _Float16* __restrict__ Opart, float2* __restrict__ MLpart, int tile,
-                                          int kvh) {
+                                          int kvh, int hsub0) {
   constexpr int NTH = 64 * NW;
   constexpr int KC = HD / 8;                        // 16-byte columns of a K row
   constexpr int K_SEGS = KT * KC;                   // 16-byte pieces of a K tile
@@ -116,9 +118,9 @@ __device__ __forceinline__ void attn_tile(const _Float16* __restrict__ Q, const 
   const int kt_end = SPLIT ? min(kt0 + tps, n_kt) : n_kt;
   if (kt0 >= kt_end) return;   // no query of this tile reaches the split
 
-  const int h = kvh * group + (w % group);
-  const bool wave_active = w < group * qw;
-  const int qi = row0 + (w / group) * 32 + col;
+  const int h = kvh * group + hsub0 + (w % gpw);
+  const bool wave_active = w < gpw * qw;
+  const int qi = row0 + (w / gpw) * 32 + col;
   const bool qvalid = wave_active && qi < M;
   const int qc = min(qi, M - 1);
   const int p = qpos[qc];
@@ -533,21 +535,24 @@ __device__ __forceinline__ void attn_tile(const _Float16* __restrict__ Q, const 
 constexpr int kWqDone = 15;
 static_assert(kWqDone < kAttnQueueInts, "done counter inside the queue block");
 
-// Next item of a persistent workgroup (thread 0): a tile of its home KV head
-// while that queue lasts, then the lightest tiles left in the other queues
-// (home + 1, home + 2, ...); -1 when every queue is exhausted.
-__device__ __forceinline__ int attn_pop(int* wq, int home, int nkv, int n_qtiles) {
+// Next item of a persistent workgroup (thread 0): an item (query tile, or
+// query tile and head) of its home KV head while that queue lasts, then the
+// lightest items left in the other queues (home + 1, home + 2, ...); -1 when
+// every queue is exhausted.
+__device__ __forceinline__ int attn_pop(int* wq, int home, int nkv, int n_items) {
   for (int k = 0; k < nkv; ++k) {
     int qk = home + k;
     if (qk >= nkv) qk -= nkv;
-    if (__hip_atomic_load(&wq[qk], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= n_qtiles) continue;
+    if (__hip_atomic_load(&wq[qk], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= n_items) continue;
     const int i = atomicAdd(&wq[qk], 1);
-    if (i < n_qtiles) return qk * n_qtiles + i;
+    if (i < n_items) return qk * n_items + i;
   }
   return -1;
 }
 
-// Scheduling of the work items (tile, kvh) over the workgroups.
+// Scheduling of the work items (tile, kvh) over the workgroups (with one
+// query head per workgroup an item is (tile, head of kvh's group), the heads
+// of a tile in a row).
 //
 // Static form (wq == nullptr, and every split launch): workgroup b takes one
 // item.  Workgroups are dealt to the 8 XCDs round-robin (x = b % 8).  When nkv
@@ -568,7 +573,7 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
                                                        const uint8_t* __restrict__ slab,
                                                        const int32_t* __restrict__ table, int n_table, int C,
                                                        int cshift, int64_t slot_bytes, int nq, int nkv,
-                                                       int group, int qw, int n_qtiles,
+                                                       int group, int qw, int gpw, int n_items,
                                                        float scale_log2, _Float16* __restrict__ O, int tps,
                                                        _Float16* __restrict__ Opart,
                                                        float2* __restrict__ MLpart, int* __restrict__ wq) {
@@ -585,9 +590,11 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
       kvh = j % nkv;
       tile_rank = (j / nkv) * 8 + xcd;
     }
-    if (tile_rank >= n_qtiles) return;
+    if (tile_rank >= n_items) return;
+    const int hpi = group / gpw, n_qtiles = n_items / hpi;
     attn_tile<HD, NW, DIRECT, SPLIT>(Q, qpos, M, slab, table, n_table, C, cshift, slot_bytes, nq, nkv, group, qw,
-                                     scale_log2, O, tps, Opart, MLpart, n_qtiles - 1 - tile_rank, kvh);
+                                     gpw, scale_log2, O, tps, Opart, MLpart, n_qtiles - 1 - tile_rank / hpi, kvh,
+                                     (tile_rank % hpi) * gpw);
     return;
   }
   const bool persistent = wq != nullptr;
@@ -604,13 +611,13 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
   for (int round = 0;; ++round) {
     int kvh, tile_rank;
     if (persistent) {
-      if (threadIdx.x == 0) s_item = attn_pop(wq, home, nkv, n_qtiles);
+      if (threadIdx.x == 0) s_item = attn_pop(wq, home, nkv, n_items);
       __syncthreads();
       const int item = __builtin_amdgcn_readfirstlane(s_item);   // uniform: item addressing stays scalar
       __syncthreads();   // every thread has the item before thread 0 pops again
       if (item < 0) break;
-      kvh = item / n_qtiles;
-      tile_rank = item - kvh * n_qtiles;
+      kvh = item / n_items;
+      tile_rank = item - kvh * n_items;
     } else {
       if (round > 0) break;
       const int b = blockIdx.x;
@@ -622,10 +629,12 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const _Float16* __restric
         kvh = j % nkv;
         tile_rank = (j / nkv) * 8 + xcd;
       }
-      if (tile_rank >= n_qtiles) break;
+      if (tile_rank >= n_items) break;
     }
+    const int hpi = group / gpw, n_qtiles = n_items / hpi;
     attn_tile<HD, NW, DIRECT, SPLIT>(Q, qpos, M, slab, table, n_table, C, cshift, slot_bytes, nq, nkv, group, qw,
-                                     scale_log2, O, tps, Opart, MLpart, n_qtiles - 1 - tile_rank, kvh);
+                                     gpw, scale_log2, O, tps, Opart, MLpart, n_qtiles - 1 - tile_rank / hpi, kvh,
+                                     (tile_rank % hpi) * gpw);
   }
   if (persistent && threadIdx.x == 0) {
     // no pop of this launch follows: the last workgroup zeroes the queues
@@ -899,6 +908,26 @@ __global__ __launch_bounds__(256) void attn_merge_wide_kernel(const _Float16* __
   }
 }
 
+// The waves of a workgroup: gpw query heads of one KV head's group times qw
+// 32-row query groups, 8 waves in all: gpw is the largest divisor of the
+// group size G that divides 8 (G itself when it does), and a work item is a
+// (query tile, gpw of the G heads) pair.  (G waves of one row group each, for
+// G = 3, 5, 6, 7, would leave SIMDs with 1 or 2 waves.)
+inline void attn_wave_map(int group, int& gpw, int& qw) {
+  if (group >= 8) {
+    gpw = group;
+    qw = 1;
+    return;
+  }
+  gpw = 1;
+  for (int g = group; g > 1; --g)
+    if (group % g == 0 && 8 % g == 0) {
+      gpw = g;
+      break;
+    }
+  qw = 8 / gpw;
+}
+
 struct SplitArgs {
   int tps = 0, n_split = 1;
   _Float16* opart = nullptr;
@@ -936,7 +965,7 @@ constexpr size_t attn_lds_bytes(int n_table) {
 
 template <int HD, int NW, bool DIRECT, bool SPLIT>
 void launch_nwd(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S, const int32_t* table,
-               int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group, int qw, int n_table,
+               int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group, int qw, int gpw, int n_table,
                float scale_log2, _Float16* O, const SplitArgs& sa, int* wq, hipStream_t s) {
   const size_t lds_bytes = attn_lds_bytes<HD, DIRECT>(n_table);
   static const bool attr = [] {
@@ -947,42 +976,43 @@ void launch_nwd(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S,
   }();
   (void)attr;
   const int bq = 32 * qw;
-  const int n_qtiles = (m + bq - 1) / bq;
+  // items per KV head: query tiles times the head subsets of its group
+  const int n_items = (m + bq - 1) / bq * (group / gpw);
   int blocks;
   if (DIRECT && !SPLIT && wq && 8 % nkv == 0) {
     // persistent: one workgroup per resident slot, at most one per item
-    blocks = (int)std::min<int64_t>((int64_t)n_qtiles * nkv, resident_wgs<HD, NW, DIRECT, SPLIT>(lds_bytes));
+    blocks = (int)std::min<int64_t>((int64_t)n_items * nkv, resident_wgs<HD, NW, DIRECT, SPLIT>(lds_bytes));
   } else {
     wq = nullptr;
     // a multiple of 8, so a split's workgroups keep the XCD mapping of blockIdx.x
-    blocks = (8 % nkv == 0) ? 8 * ((n_qtiles + 8 / nkv - 1) / (8 / nkv)) : 8 * ((n_qtiles + 7) / 8) * nkv;
+    blocks = (8 % nkv == 0) ? 8 * ((n_items + 8 / nkv - 1) / (8 / nkv)) : 8 * ((n_items + 7) / 8) * nkv;
   }
   hipLaunchKernelGGL((attn_kernel<HD, NW, DIRECT, SPLIT>), dim3(blocks, SPLIT ? sa.n_split : 1), dim3(64 * NW),
-                     lds_bytes, s, Q, qpos, m, S, table, n_table, C, cshift, slot_bytes, nq, nkv, group, qw, n_qtiles,
-                     scale_log2, O, sa.tps, sa.opart, sa.ml, wq);
+                     lds_bytes, s, Q, qpos, m, S, table, n_table, C, cshift, slot_bytes, nq, nkv, group, qw, gpw,
+                     n_items, scale_log2, O, sa.tps, sa.opart, sa.ml, wq);
 }
 
 template <int HD, int NW, bool SPLIT>
 void launch_nw(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S, const int32_t* table,
-               int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group, int qw, int n_table,
+               int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group, int qw, int gpw, int n_table,
                float scale_log2, _Float16* O, const SplitArgs& sa, int* wq, hipStream_t s) {
   if (C >= KT)
-    launch_nwd<HD, NW, true, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, n_table,
+    launch_nwd<HD, NW, true, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, gpw, n_table,
                                     scale_log2, O, sa, wq, s);
   else
-    launch_nwd<HD, NW, false, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, n_table,
+    launch_nwd<HD, NW, false, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, gpw, n_table,
                                      scale_log2, O, sa, wq, s);
 }
 
 template <int HD, bool SPLIT>
 void launch_hd(const _Float16* Q, const int32_t* qpos, int m, const uint8_t* S, const int32_t* table,
-               int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group, int qw, int n_table,
+               int C, int cshift, int64_t slot_bytes, int nq, int nkv, int group, int qw, int gpw, int n_table,
                float scale_log2, _Float16* O, const SplitArgs& sa, int* wq, hipStream_t s) {
-  switch (group * qw) {
-    case 5: launch_nw<HD, 5, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, n_table, scale_log2, O, sa, wq, s); break;
-    case 6: launch_nw<HD, 6, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, n_table, scale_log2, O, sa, wq, s); break;
-    case 7: launch_nw<HD, 7, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, n_table, scale_log2, O, sa, wq, s); break;
-    default: launch_nw<HD, 8, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, n_table, scale_log2, O, sa, wq, s); break;
+  switch (gpw * qw) {
+    case 5: launch_nw<HD, 5, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, gpw, n_table, scale_log2, O, sa, wq, s); break;
+    case 6: launch_nw<HD, 6, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, gpw, n_table, scale_log2, O, sa, wq, s); break;
+    case 7: launch_nw<HD, 7, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, gpw, n_table, scale_log2, O, sa, wq, s); break;
+    default: launch_nw<HD, 8, SPLIT>(Q, qpos, m, S, table, C, cshift, slot_bytes, nq, nkv, group, qw, gpw, n_table, scale_log2, O, sa, wq, s); break;
   }
 }
 
@@ -990,9 +1020,8 @@ void launch_any(const void* q, const int32_t* qpos, int m, const void* slab, con
                 int chunk_tokens, int64_t slot_bytes, int n_q, int n_kv, int head_dim, void* out,
                 const SplitArgs& sa, bool split, int* wq, hipStream_t s) {
   const int group = n_q / n_kv;          // 1..8
-  // 32-query row groups per workgroup: 5..8 waves, so one staged K/V tile
-  // serves as many queries as the registers allow
-  const int qw = group >= 8 ? 1 : 8 / group;
+  int gpw, qw;
+  attn_wave_map(group, gpw, qw);
   const float scale_log2 = 1.4426950408889634f / __builtin_sqrtf((float)head_dim);
   const _Float16* Q = reinterpret_cast<const _Float16*>(q);
   const uint8_t* S = reinterpret_cast<const uint8_t*>(slab);
@@ -1000,11 +1029,11 @@ void launch_any(const void* q, const int32_t* qpos, int m, const void* slab, con
   int cshift = 0;
   while ((1 << cshift) < chunk_tokens) ++cshift;   // chunk_tokens is a power of two
   if (head_dim == 128) {
-    if (split) launch_hd<128, true>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, n_table, scale_log2, O, sa, nullptr, s);
-    else launch_hd<128, false>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, n_table, scale_log2, O, sa, wq, s);
+    if (split) launch_hd<128, true>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, gpw, n_table, scale_log2, O, sa, nullptr, s);
+    else launch_hd<128, false>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, gpw, n_table, scale_log2, O, sa, wq, s);
   } else {
-    if (split) launch_hd<64, true>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, n_table, scale_log2, O, sa, nullptr, s);
-    else launch_hd<64, false>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, n_table, scale_log2, O, sa, wq, s);
+    if (split) launch_hd<64, true>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, gpw, n_table, scale_log2, O, sa, nullptr, s);
+    else launch_hd<64, false>(Q, qpos, m, S, table, chunk_tokens, cshift, slot_bytes, n_q, n_kv, group, qw, gpw, n_table, scale_log2, O, sa, wq, s);
   }
 }
 
@@ -1029,9 +1058,12 @@ int attention_split_tiles(int max_pos, int n_split) {
 
 int attention_auto_splits(int m, int max_pos, int n_q, int n_kv, int head_dim, int64_t ws_cap) {
   const int group = n_q / n_kv;
-  const int qw = group >= 8 ? 1 : 8 / group;
+  int gpw, qw;
+  attn_wave_map(group, gpw, qw);
   const int n_qtiles = (m + 32 * qw - 1) / (32 * qw);
-  const int wgs = n_qtiles * n_kv;
+  // workgroups per key split: one per KV head in the few-column kernel, one
+  // per item and KV head in the tiled one
+  const int wgs = m * group <= kFewCols ? n_kv : n_qtiles * (group / gpw) * n_kv;
   const int n_kt = max_pos / KT + 1;
   // two workgroups per CU (their LDS fits twice) over 256 CUs -- one for
   // the few-column kernel, which streams a split's keys fastest alone (8B

@@ -170,3 +170,17 @@ def test_load_model_without_gpu_fails_cleanly():
     with pytest.raises(mz.MzError) as e:
         mz.mz_load_model(mz.make_cfg(w.model, 256), blob[:-1], 0)
     assert e.value.status == mz.MZ_EINVAL
+
+
+def test_attention_auto_splits_decode_rows():
+    """Split counts are host logic: for a decode row (the few-column kernel,
+    one workgroup per key split and KV head) the count depends on the KV
+    heads and the key range only, not on how many query heads share a KV
+    head (which changes the tiled kernel's waves per workgroup); the 8B
+    decode step over 32900 keys takes about one workgroup per CU."""
+    counts = {g: mz.mz_attention_auto_splits(1, 16399, 2 * g, 2, 128, 64 << 20) for g in (1, 2, 3, 4, 6, 7)}
+    assert len(set(counts.values())) == 1, counts
+    assert 24 <= mz.mz_attention_auto_splits(1, 32899, 32, 8, 128, 64 << 20) <= 32
+    assert mz.mz_attention_auto_splits(1, 32899, 24, 8, 128, 64 << 20) == \
+        mz.mz_attention_auto_splits(1, 32899, 32, 8, 128, 64 << 20)
+    assert mz.mz_attention_auto_splits(40000, 40000, 24, 8, 128, 64 << 20) == 1   # the chip is full already
