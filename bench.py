@@ -32,8 +32,8 @@ METRIC = "KV-recompute prefill tokens/s + TTFT ms from evicted state, 1 MI355X"
 # valid only for the kernel source they were taken on and the 8B workload.
 MEASURED_TRAFFIC = {"kernel": "attn_kernel", "workload": "8b",
                     "source": "paper_2609_01338_amd/csrc/attention.hip",
-                    "sha256": "914f2b770006ff42f74588729e8ee333a51d4c2bb5c06126eafac519b67bdd88",
-                    "bytes_per_launch": 1.654e9}
+                    "sha256": "e379ff2aaacd1b9dd9310f20c3a615f36248714731ee685123cbb4cc4c9eb928",
+                    "bytes_per_launch": 1.662e9}
 PEAK_MFMA_TFLOPS = 2500.0      # MI355X dense bf16 / fp16 MFMA
 PEAK_HBM_GBPS = 8000.0
 
