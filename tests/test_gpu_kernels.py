@@ -554,8 +554,11 @@ def _attn_case(nq, nkv, hd, C, S, qpos, seed, sample=None, n_split=None, n_table
 @pytest.mark.parametrize("nq,nkv,hd,C,S", [
     (4, 2, 64, 16, 128), (4, 2, 64, 16, 117), (32, 8, 64, 256, 600), (24, 8, 128, 256, 700),
     (12, 2, 128, 256, 530), (32, 8, 128, 256, 400), (8, 8, 128, 64, 200), (6, 1, 64, 32, 90),
-    (4, 4, 128, 8, 77)])
+    (4, 4, 128, 8, 77), (10, 2, 64, 64, 450), (14, 2, 128, 128, 600), (16, 2, 64, 32, 333)])
 def test_attention_small(nq, nkv, hd, C, S):
+    """Query-head groups of 1-8 (so every wave map: G heads x 8/G row groups,
+    2 heads x 4 for G = 6, one head x 8 for G = 3, 5, 7), dense, gappy, first
+    and last query rows, against the exact definition."""
     rng = np.random.default_rng(S)
     dense = np.arange(S)
     gappy = np.sort(rng.choice(S, max(1, S // 3), replace=False))
