@@ -403,7 +403,9 @@ typedef struct {
   void *workspace;           /* device scratch, not shared with launches in flight: the rows after the
                                 last whole 256-row tile run split over K in it (as mz_q4_gemm_split)
                                 when their tiles alone would leave most compute units idle (NULL:
-                                they run as 64-row tiles) */
+                                they run as 64-row tiles); and a product with too few 256-row tiles
+                                for the GPU but a long K range runs in it as 256-row tiles split over
+                                K (mz_q4_gemm_long_k_splits; NULL: as 64-row tiles over all of K) */
   int64_t workspace_bytes;
   /* rotary epilogues (Sec. 2.1 prefill, rotate-half pairs i, i + head_dim/2 of every head) */
   const int32_t *pos;        /* device int32 [m]: position of output row r */
@@ -494,6 +496,14 @@ mz_status mz_q4_gemm_split_noalloc(const void *x_f16, int32_t m, int32_t n_pad, 
  * workspace: about two workgroups per compute unit, at least 4 K steps per
  * split, at most 32 splits; 1 when the tile grid already fills the GPU. */
 int32_t mz_q4_gemm_auto_splits(int32_t m, int32_t n_pad, int32_t k, int64_t workspace_bytes);
+
+/* The K splits mz_q4_gemm_ex takes with workspace_bytes of workspace when
+ * the product's 256-row tiles alone are too few for the GPU while its 64-row
+ * tiles fill it: 256-row tiles split into about one round of the compute
+ * units, when every split keeps at least 16 K steps of 64 and the fp32
+ * partials (splits x m x n_pad x 4 bytes) fit the workspace; 1 otherwise
+ * (64-row tiles over the whole K range).  Host only, no GPU work. */
+int32_t mz_q4_gemm_long_k_splits(int32_t m, int32_t n_pad, int32_t k, int64_t workspace_bytes);
 
 /* Causal GQA attention (paper Sec. 2.1; read through the chunk table as in
  * Sec. 4.2) of q (f16 [m][n_q_heads][head_dim], rotated) at positions qpos

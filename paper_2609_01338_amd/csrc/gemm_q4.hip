@@ -1057,7 +1057,7 @@ constexpr double kTile64Cost = 0.35;
 // would leave most of the CUs idle while each runs the whole K range.
 template <int EPI>
 void launch_rows_split(const _Float16* X, const int32_t* a_rows, int r0, int m, int n, int k, const uint8_t* W,
-                       void* y, hipStream_t s, const GemmRope& ea, void* ws, int ns) {
+                       void* y, hipStream_t s, const GemmRope& ea, void* ws, int ns, int row_tile = 0) {
   const _Float16* x = a_rows ? X : X + (size_t)r0 * k;
   const int32_t* ar = a_rows ? a_rows + r0 : nullptr;
   GemmRope e = ea;
@@ -1071,18 +1071,23 @@ void launch_rows_split(const _Float16* X, const int32_t* a_rows, int r0, int m, 
   else if (EPI == kEpiStore || EPI == kEpiAdd)
     yy = reinterpret_cast<float*>(y) + (size_t)r0 * n;
   if (EPI == kEpiRopeQ || EPI == kEpiRopeKV)
-    launch_gemm_q4_splitk_rope(x, m, n, k, W, EPI, e, yy, ns, ws, s, ar);
+    launch_gemm_q4_splitk_rope(x, m, n, k, W, EPI, e, yy, ns, ws, s, ar, nullptr, 0.f, row_tile);
   else
-    launch_gemm_q4_splitk(x, m, n, k, W, EPI, yy, ns, ws, s, ar);
+    launch_gemm_q4_splitk(x, m, n, k, W, EPI, yy, ns, ws, s, ar, nullptr, 0.f, row_tile);
 }
 
 template <int EPI>
 void launch_epi(const _Float16* X, const int32_t* a_rows, int m, int n, int k, const uint8_t* W, void* y,
                 hipStream_t s, const GemmRope& ea = GemmRope{}, int* wq = nullptr, void* ws = nullptr,
                 int64_t ws_bytes = 0) {
-  // 256-row tiles unless they leave most of the 256 CUs idle
+  // 256-row tiles unless they leave most of the 256 CUs idle; then 256-row
+  // tiles split over K where the K range is long, else 64-row tiles
   if (gemm_row_tile(m, n) == 64) {
-    launch_bm<EPI, 64>(X, a_rows, m, n, k, W, y, s, 1, 0, ea, wq);
+    const int ns = ws ? gemm_long_k_splits(m, n, k, ws_bytes) : 1;
+    if (ns > 1)
+      launch_rows_split<EPI>(X, a_rows, 0, m, n, k, W, y, s, ea, ws, ns, 256);
+    else
+      launch_bm<EPI, 64>(X, a_rows, m, n, k, W, y, s, 1, 0, ea, wq);
     return;
   }
   // A ragged last row of 256-row tiles can make a final round of workgroups
@@ -1133,11 +1138,27 @@ int gemm_auto_splits(int m, int n, int k, int64_t ws_cap) {
   return (nk + ks - 1) / ks;   // no empty trailing split
 }
 
+int gemm_long_k_splits(int m, int n, int k, int64_t ws_cap) {
+  // The 64-row tiles fill the chip, but each dequantizes its weight tiles over
+  // the whole K range for 64 rows.  256-row tiles split over K into one round
+  // of the chip do a quarter of that dequantization per MFMA, which pays for
+  // the fp32 partials and their reduce when each split keeps at least 16 K
+  // steps (2048 x 2048 x 8192: 4 splits of 32 steps).
+  constexpr int kMinSteps = 16;
+  const int cus = device_cus();
+  const int tiles = (n / BN) * ((m + 255) / 256), nk = k / BK;
+  if (tiles >= cus || (n / BN) * ((m + 63) / 64) < cus) return 1;
+  const int ns = (cus + tiles - 1) / tiles;
+  if (ns < 2 || nk / ns < kMinSteps || gemm_splitk_ws_bytes(m, n, ns) > ws_cap) return 1;
+  const int ks = gemm_k_steps(k, ns);
+  return (nk + ks - 1) / ks;
+}
+
 namespace {
 // The fp32 partials [split][m][n] of a split-K product; returns the number of
 // splits written.
 int launch_partials(const void* x, int m, int n, int k, const void* w, int n_split, void* ws, hipStream_t s,
-                    const int32_t* a_rows, const float* h_norm, float eps) {
+                    const int32_t* a_rows, const float* h_norm, float eps, int row_tile) {
   const _Float16* X = reinterpret_cast<const _Float16*>(x);
   const uint8_t* W = reinterpret_cast<const uint8_t*>(w);
   const int ks = gemm_k_steps(k, n_split);
@@ -1148,7 +1169,7 @@ int launch_partials(const void* x, int m, int n, int k, const void* w, int n_spl
   else if (m == 1)
     hipLaunchKernelGGL(gemv_q4_kernel<false>, dim3(n / BN, ns), dim3(256), 0, s, X, nullptr, 0.f, a_rows, k, W,
                        n, reinterpret_cast<float*>(ws), ks);
-  else if (gemm_row_tile(m, n) == 64)
+  else if ((row_tile ? row_tile : gemm_row_tile(m, n)) == 64)
     launch_bm<kEpiPartial, 64>(X, a_rows, m, n, k, W, ws, s, ns, ks);
   else
     launch_bm<kEpiPartial, 256>(X, a_rows, m, n, k, W, ws, s, ns, ks);
@@ -1217,8 +1238,8 @@ void launch_gemv1(const void* x, int n, int k, const void* w, int epilogue, cons
 
 void launch_gemm_q4_splitk_rope(const void* x, int m, int n, int k, const void* w, int epilogue, const GemmRope& ea,
                                 void* y, int n_split, void* ws, hipStream_t s, const int32_t* a_rows,
-                                const float* h_norm, float eps) {
-  const int ns = launch_partials(x, m, n, k, w, n_split, ws, s, a_rows, h_norm, eps);
+                                const float* h_norm, float eps, int row_tile) {
+  const int ns = launch_partials(x, m, n, k, w, n_split, ws, s, a_rows, h_norm, eps, row_tile);
   const int rot = epilogue == kEpiRopeQ ? ea.n_valid : ea.n_valid / 2;
   const int64_t per_row = rot / 2 + (epilogue == kEpiRopeKV ? ea.n_valid / 2 : 0);
   const dim3 grid((unsigned)(((int64_t)m * per_row + 255) / 256));
@@ -1230,8 +1251,9 @@ void launch_gemm_q4_splitk_rope(const void* x, int m, int n, int k, const void* 
 }
 
 void launch_gemm_q4_splitk(const void* x, int m, int n, int k, const void* w, int epilogue, void* y, int n_split,
-                           void* ws, hipStream_t s, const int32_t* a_rows, const float* h_norm, float eps) {
-  const int ns = launch_partials(x, m, n, k, w, n_split, ws, s, a_rows, h_norm, eps);
+                           void* ws, hipStream_t s, const int32_t* a_rows, const float* h_norm, float eps,
+                           int row_tile) {
+  const int ns = launch_partials(x, m, n, k, w, n_split, ws, s, a_rows, h_norm, eps, row_tile);
   const int64_t outs = (int64_t)m * (epilogue == kEpiSwiGLU ? n / 2 : n) / 4;
   const dim3 grid((unsigned)((outs + 255) / 256));
   const float* part = reinterpret_cast<const float*>(ws);

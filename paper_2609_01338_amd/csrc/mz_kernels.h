@@ -46,7 +46,10 @@ struct GemmRope {
 constexpr int kGemmQueueInts = 16;
 // With ws (ws_bytes of device scratch, not in use by launches in flight), a
 // ragged remainder of rows whose tiles alone would leave most CUs idle runs
-// split over K (as launch_gemm_q4_splitk) instead of as 64-row tiles.
+// split over K (as launch_gemm_q4_splitk) instead of as 64-row tiles, and a
+// product whose 256-row tiles are too few for the chip but whose K range is
+// long runs as 256-row tiles split over K (gemm_long_k_splits) instead of as
+// 64-row tiles over the whole K range.
 void launch_gemm_q4(const void* x, int m, int n, int k, const void* w, int epilogue, void* y,
                     hipStream_t s, const int32_t* a_rows = nullptr, int* work_queues = nullptr,
                     void* ws = nullptr, int64_t ws_bytes = 0);
@@ -64,17 +67,18 @@ void launch_gemm_q4_rope(const void* x, int m, int n, int k, const void* w, int 
 // (gemm_splitk_ws_bytes(m, n, n_split) bytes), then one kernel adds them in
 // split order and applies the epilogue.  h_norm (m == 1 only): x is not read;
 // the row is RMSNorm(h_norm row, eps) formed inside the product, the same
-// f16 values launch_rmsnorm writes.
+// f16 values launch_rmsnorm writes.  row_tile: 64 or 256 rows per partial
+// tile (0: the size launch_gemm_q4 takes for m rows).
 void launch_gemm_q4_splitk(const void* x, int m, int n, int k, const void* w, int epilogue, void* y, int n_split,
                            void* ws, hipStream_t s, const int32_t* a_rows = nullptr,
-                           const float* h_norm = nullptr, float eps = 0.f);
+                           const float* h_norm = nullptr, float eps = 0.f, int row_tile = 0);
 int64_t gemm_splitk_ws_bytes(int m, int n, int n_split);
 // Split-K form with a rotary-embedding epilogue (kEpiRopeQ / kEpiRopeKV): the
 // splits are added in order, then rotated and written as the unsplit
 // epilogues do.
 void launch_gemm_q4_splitk_rope(const void* x, int m, int n, int k, const void* w, int epilogue, const GemmRope& ea,
                                 void* y, int n_split, void* ws, hipStream_t s, const int32_t* a_rows = nullptr,
-                                const float* h_norm = nullptr, float eps = 0.f);
+                                const float* h_norm = nullptr, float eps = 0.f, int row_tile = 0);
 // One activation row in one launch (m = 1, no workspace): workgroups own a
 // few output columns over the whole K range and apply the epilogue
 // themselves (any of kEpiStore .. kEpiRopeKV, with ea as for
@@ -95,6 +99,10 @@ void launch_gemv1_qkv(const void* x, int k, const void* wq, void* yq, const Gemm
                       const float* h_norm = nullptr, float eps = 0.f);
 // Splits that fill the chip for this shape within ws_cap bytes (1: no split).
 int gemm_auto_splits(int m, int n, int k, int64_t ws_cap);
+// K splits of 256-row tiles for launch_gemm_q4 with a workspace of ws_cap
+// bytes where its 256-row tiles alone are too few for the chip, the 64-row
+// tiles fill it and every split keeps at least 16 K steps; 1 otherwise.
+int gemm_long_k_splits(int m, int n, int k, int64_t ws_cap);
 
 // Causal GQA attention over chunked KV (see mz.h, mz_attention).  table has
 // n_table entries (at most kAttnTableMax).  With

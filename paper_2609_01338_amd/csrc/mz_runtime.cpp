@@ -1926,6 +1926,11 @@ int32_t mz_q4_gemm_auto_splits(int32_t m, int32_t n_pad, int32_t k, int64_t work
   return mzk::gemm_auto_splits(m, n_pad, k, workspace_bytes);
 }
 
+int32_t mz_q4_gemm_long_k_splits(int32_t m, int32_t n_pad, int32_t k, int64_t workspace_bytes) {
+  if (m < 1 || n_pad < mzk::kGemmTileN || k < mzk::kGemmTileK) return 1;
+  return mzk::gemm_long_k_splits(m, n_pad, k, workspace_bytes);
+}
+
 mz_status mz_q4_gemm_split(const void* x_f16, int32_t m, int32_t n_pad, int32_t k, const void* w_packed,
                            int32_t epilogue, void* y, int32_t n_split, void* workspace, int64_t workspace_bytes,
                            void* stream) {

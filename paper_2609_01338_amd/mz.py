@@ -125,6 +125,7 @@ def lib() -> ctypes.CDLL:
         "mz_q4_gemm_split_workspace_bytes": ([i32, i32, i32], i64),
         "mz_q4_gemm_split_noalloc": ([vp, i32, i32, i32, vp, i32, vp, i32, vp], i32),
         "mz_q4_gemm_auto_splits": ([i32, i32, i32, i64], i32),
+        "mz_q4_gemm_long_k_splits": ([i32, i32, i32, i64], i32),
         "mz_attention_split": ([vp, vp, i32, i32, vp, vp, i32, i32, i32, i32, i32, i32, vp, i64, vp, vp], i32),
         "mz_attention_split_workspace_bytes": ([i32, i32, i32, i32], i64),
         "mz_attention_auto_splits": ([i32, i32, i32, i32, i32, i64], i32),
@@ -403,6 +404,10 @@ def mz_q4_gemm_split_workspace_bytes(m: int, n_pad: int, n_split: int) -> int:
 
 def mz_q4_gemm_auto_splits(m: int, n_pad: int, k: int, ws_bytes: int) -> int:
     return int(lib().mz_q4_gemm_auto_splits(m, n_pad, k, ws_bytes))
+
+
+def mz_q4_gemm_long_k_splits(m: int, n_pad: int, k: int, ws_bytes: int) -> int:
+    return int(lib().mz_q4_gemm_long_k_splits(m, n_pad, k, ws_bytes))
 
 
 def mz_attention_split(q_ptr: int, qpos_ptr: int, m: int, max_pos: int, slab_ptr: int, table_ptr: int,

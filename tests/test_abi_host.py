@@ -184,3 +184,22 @@ def test_attention_auto_splits_decode_rows():
     assert mz.mz_attention_auto_splits(1, 32899, 24, 8, 128, 64 << 20) == \
         mz.mz_attention_auto_splits(1, 32899, 32, 8, 128, 64 << 20)
     assert mz.mz_attention_auto_splits(40000, 40000, 24, 8, 128, 64 << 20) == 1   # the chip is full already
+
+
+def test_gemm_long_k_splits():
+    """256-row tiles split over K only where they alone are too few for the
+    chip, the 64-row tiles fill it, every split keeps 16 K steps and the
+    partials fit the workspace: the 1B down projection (2048 rows, 2048
+    outputs, K 8192) with the restore's 64 MiB takes 4 splits of 32 steps;
+    its output projection (K 2048, 8 steps a split) and the 8B full-row
+    products stay whole, few rows are left to the split-K rule for few
+    rows."""
+    ws = 64 << 20
+    assert mz.mz_q4_gemm_long_k_splits(2048, 2048, 8192, ws) == 4
+    assert mz.mz_q4_gemm_long_k_splits(2048, 2048, 8192, ws - 1) == 1      # partials would not fit
+    assert mz.mz_q4_gemm_long_k_splits(2048, 2048, 4096, ws) == 4
+    assert mz.mz_q4_gemm_long_k_splits(2048, 2048, 2048, ws) == 1
+    assert mz.mz_q4_gemm_long_k_splits(32896, 4096, 14336, ws) == 1
+    assert mz.mz_q4_gemm_long_k_splits(1024, 2048, 8192, ws) == 1          # 128 64-row tiles
+    assert mz.mz_q4_gemm_long_k_splits(1536, 4096, 14336, 80 << 20) == 3
+    assert mz.mz_q4_gemm_long_k_splits(1536, 4096, 14336, ws) == 1

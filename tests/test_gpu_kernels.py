@@ -28,8 +28,10 @@ pytestmark = pytest.mark.gpu
 def _gemm_case(M, N, K, epi, seed, sample_rows=None, n_split=None):
     """n_split: None for mz_q4_gemm, "queued" for mz_q4_gemm_queued (run
     twice from the same initial output on the same queues, which must come
-    back zero, and equal to mz_q4_gemm bit for bit), else mz_q4_gemm_split with
-    that many K splits ("auto": the restore's choice)."""
+    back zero, and equal to mz_q4_gemm bit for bit), "long-k" for
+    mz_q4_gemm_ex with the restore's 64 MiB workspace on a shape it splits
+    over K as 256-row tiles, else mz_q4_gemm_split with that many K splits
+    ("auto": the restore's choice)."""
     torch = torch_cuda()
     rng = np.random.default_rng(seed)
     report("gemm", M=M, N=N, K=K, epi=epi, seed=seed, n_split=n_split)
@@ -67,6 +69,14 @@ def _gemm_case(M, N, K, epi, seed, sample_rows=None, n_split=None):
             torch.cuda.synchronize()
             assert int(queues.abs().sum()) == 0, "work queues not left at zero"
             assert torch.equal(y.view(torch.uint8), plain.view(torch.uint8)), "queued != mz_q4_gemm"
+    elif n_split == "long-k":
+        wsb = 64 << 20
+        ns = mz.mz_q4_gemm_long_k_splits(M, n_pad, K, wsb)
+        report("  long-K splits", n_split=ns)
+        assert ns > 1, "shape outside the long-K split rule"
+        ws = torch.full((wsb // 4,), float("nan"), device="cuda")      # stale partials must not leak in
+        mz.mz_q4_gemm_ex(x.data_ptr(), M, n_pad, K, w.data_ptr(), epi, y.data_ptr(), stream(),
+                         workspace=ws.data_ptr(), workspace_bytes=wsb)
     else:
         if n_split == "auto":
             n_split = mz.mz_q4_gemm_auto_splits(M, n_pad, K, 64 << 20)
@@ -117,6 +127,17 @@ def test_gemm_split(M, N, K, epi):
         if ns != "auto" and ns > nk:
             continue
         _gemm_case(M, N, K, epi, seed=M + N + K, n_split=ns)
+
+
+@pytest.mark.parametrize("M,N,K,epi", [(2048, 2048, 8192, 1), (2000, 2048, 8192, 0), (2048, 2048, 4096, 0),
+                                       (2048, 1024, 8192, 2)])
+def test_gemm_long_k_split(M, N, K, epi):
+    """Products with too few 256-row tiles for the chip but a long K range,
+    as the restore launches them (with its workspace): 256-row tiles split
+    over K.  The 1B down projection (4 splits of 32 K steps), a ragged last
+    row tile, 16 steps per split, and the SwiGLU epilogue, against the exact
+    product on one row in every 64-row tile."""
+    _gemm_case(M, N, K, epi, seed=M + N + K + 5, sample_rows=_tile_rows(M, 64, M + K), n_split="long-k")
 
 
 @pytest.mark.parametrize("M", [1, 129])
