@@ -494,7 +494,8 @@ mz_status mz_q4_gemm_split_noalloc(const void *x_f16, int32_t m, int32_t n_pad, 
 
 /* The split count the restore uses for this shape with workspace_bytes of
  * workspace: about two workgroups per compute unit, at least 4 K steps per
- * split, at most 32 splits; 1 when the tile grid already fills the GPU. */
+ * split, at most 32 splits; 1 when the tile grid already fills the GPU, or
+ * when m >= 1024 and the tiles cover half of its compute units. */
 int32_t mz_q4_gemm_auto_splits(int32_t m, int32_t n_pad, int32_t k, int64_t workspace_bytes);
 
 /* The K splits mz_q4_gemm_ex takes with workspace_bytes of workspace when

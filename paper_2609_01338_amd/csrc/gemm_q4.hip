@@ -1128,9 +1128,13 @@ int gemm_auto_splits(int m, int n, int k, int64_t ws_cap) {
   const int bm = gemm_row_tile(m, n);
   const int tiles = (n / BN) * ((m + bm - 1) / bm);
   const int nk = k / BK;
-  // about two workgroups per CU, at least 4 K steps per split
-  constexpr int kTarget = 512, kMinSteps = 4, kMaxSplits = 32;
-  if (tiles >= kTarget / 2 || nk < 2 * kMinSteps) return 1;
+  // about two workgroups per CU, at least 4 K steps per split.  From 1024
+  // rows on, tiles that cover half the CUs run whole: there the partials and
+  // their reduce cost more than the idle CUs save (K/V of 2048 rows, 1024
+  // outputs, K 2048: 29.3 us whole against 31.1 in 4 splits; of 4979 rows,
+  // 512 outputs, K 1536: 23.1 against 33.6)
+  constexpr int kTarget = 512, kMinSteps = 4, kMaxSplits = 32, kWholeRows = 1024;
+  if (tiles >= kTarget / 2 || nk < 2 * kMinSteps || (m >= kWholeRows && tiles >= kTarget / 4)) return 1;
   int ns = std::min({(kTarget + tiles - 1) / tiles, nk / kMinSteps, kMaxSplits});
   while (ns > 1 && gemm_splitk_ws_bytes(m, n, ns) > ws_cap) --ns;
   if (ns <= 1) return 1;

@@ -203,3 +203,16 @@ def test_gemm_long_k_splits():
     assert mz.mz_q4_gemm_long_k_splits(1024, 2048, 8192, ws) == 1          # 128 64-row tiles
     assert mz.mz_q4_gemm_long_k_splits(1536, 4096, 14336, 80 << 20) == 3
     assert mz.mz_q4_gemm_long_k_splits(1536, 4096, 14336, ws) == 1
+
+
+def test_gemm_auto_splits_medium_rows():
+    """Few rows split over K; from 1024 rows on, 64-row tiles that cover half
+    the chip run whole (the 1B and 1.5B K/V projections); the rows after the
+    last whole 256-row tile of a long product keep their split."""
+    ws = 64 << 20
+    assert mz.mz_q4_gemm_auto_splits(2048, 1024, 2048, ws) == 1
+    assert mz.mz_q4_gemm_auto_splits(4979, 512, 1536, ws) == 1
+    assert mz.mz_q4_gemm_auto_splits(1023, 2048, 2048, ws) > 1          # 128 tiles, fewer rows
+    assert mz.mz_q4_gemm_auto_splits(1024, 2048, 2048, ws) == 1
+    assert mz.mz_q4_gemm_auto_splits(128, 28672, 4096, ws) == 3
+    assert mz.mz_q4_gemm_auto_splits(129, 4096, 4096, ws) > 1
