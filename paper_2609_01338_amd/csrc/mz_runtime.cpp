@@ -556,6 +556,26 @@ struct mz_ctx {
     return fuse_norm && m == 1 &&
            (gemv_one(m, n, k) || (gemm_split && mzk::gemm_auto_splits(m, n, k, split_ws_bytes) > 1));
   }
+  // An unsplit attention launch takes the work queues (option attn_queue)
+  // from 4 (query tile, KV head) items per CU on; a workgroup covers 256
+  // (query row, query head) pairs.  The queues even out XCDs that run at
+  // different clocks, which takes several rounds of items; with fewer, one
+  // workgroup per item is as fast or faster, with the same results.
+  // Same-box A/B, persistent against one item per workgroup, causal rows:
+  // 2048 rows, 32/8 heads of 64 (256 items): 55.2 against 41.4 us; 8256
+  // rows, 24/8 heads of 128 (792): 449 against 446; 8320 rows, 32/8 heads of
+  // 128 (1040): 548 against 558; 32896 rows (4112): 7890 against 8200.
+  bool attn_queue_pays(int m) const {
+    static const int cus = [] {
+      int dev = 0, n = 0;
+      if (hipGetDevice(&dev) != hipSuccess ||
+          hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+        n = 256;
+      return n;
+    }();
+    constexpr int64_t kMinItemsPerCu = 4, kPairsPerItem = 256;
+    return attn_queue && (int64_t)m * nq >= kMinItemsPerCu * kPairsPerItem * cus;
+  }
   // A single row runs as the one-launch GEMV (option gemv_direct)
   bool gemv_one(int m, int n, int k) const { return gemv_direct && m == 1 && mzk::gemv1_ok(n, k); }
   int32_t* d_codec_slots = nullptr;  // per restore: destination slot of each compressed chunk (in d_meta)
@@ -1116,7 +1136,7 @@ void restore_and_prefill_impl(mz_ctx* x, const int32_t* prompt, int32_t n_prompt
                                     x->slot_bytes, x->nq, x->nkv, x->hd, n_split, x->split_ws, x->xb, cs);
       else
         mzk::launch_attention(x->q16, posq, nq, x->kv_slab, x->d_tables + (size_t)l * MC, MC, C, x->slot_bytes,
-                              x->nq, x->nkv, x->hd, x->xb, cs, x->attn_queue ? x->attn_wq : nullptr);
+                              x->nq, x->nkv, x->hd, x->xb, cs, x->attn_queue_pays(nq) ? x->attn_wq : nullptr);
     });
     x->timed(kKGemmO, 2.0 * nq * x->dq * d, (double)d * x->dq * bpe_w + nq * (x->dq * 2.0 + d * 8.0), cs,
              [&] { x->gemm(x->xb, nq, x->d_pad, x->dq, unit + x->off_o, mzk::kEpiAdd, h, cs); });
