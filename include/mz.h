@@ -167,7 +167,8 @@ mz_status mz_generate(mz_ctx *ctx, int32_t token, int32_t n, int32_t *tokens_out
  * enabling it the first time allocates a device staging ring of one layer's
  * chunks), "attn_split" (1: attention of few query rows against a long
  * context runs split over the keys, as mz_attention_split, default; 0: always
- * one pass), "attn_queue" (1: the attention of many rows runs as
+ * one pass), "attn_queue" (1: the attention of many rows, at least
+ * 4 * 256 (query row, query head) pairs per compute unit, runs as
  * mz_attention_queued with queues owned by the context, default; 0: as
  * mz_attention), "gemm_queue" (1: the unsplit projections with a store,
  * residual-add or SwiGLU epilogue run as mz_q4_gemm_queued, default; 0: one
