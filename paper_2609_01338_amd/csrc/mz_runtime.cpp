@@ -561,7 +561,7 @@ struct mz_ctx {
   // (query row, query head) pairs.  The queues even out XCDs that run at
   // different clocks, which takes several rounds of items; with fewer, one
   // workgroup per item is as fast or faster, with the same results.
-  // Same-box A/B, persistent against one item per workgroup, causal rows:
+  // Measured on one MI355X, persistent against one item per workgroup, causal rows:
   // 2048 rows, 32/8 heads of 64 (256 items): 55.2 against 41.4 us; 8256
   // rows, 24/8 heads of 128 (792): 449 against 446; 8320 rows, 32/8 heads of
   // 128 (1040): 548 against 558; 32896 rows (4112): 7890 against 8200.
